@@ -1,0 +1,196 @@
+/*
+ * sr.h -- C ABI of libsr, the MI355X (gfx950) hot path of Sparse-Reslim:
+ * random (or top-k) token selection, gather, the n2 middle transformer blocks
+ * run on the routed tokens only (forward and backward), and the residual-delta
+ * scatter back into the full token sequence, plus the dense keep=100% mode.
+ *
+ * The operations follow the paper's statement of the method:
+ *   selection            Sec. 3.2 "Random token selection"; Alg. 1 stage 2; App. A.4
+ *   gather / scatter     Sec. 3.2 "Residual delta formulation", Eq. (scatter)
+ *   middle stack         Eq. (sparse_forward); block of Sec. 3.3
+ *   dense mode           Sec. 3.4 "Architecture-agnostic design" (r = 1)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensor arguments are DEVICE pointers owned by the caller, contiguous,
+ *    row-major, 16-byte aligned.  The library allocates no device memory:
+ *    saved activations and scratch space are caller buffers sized by
+ *    sr_workspace_bytes / sr_select_scratch_bytes.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls enqueue work
+ *    on it and return without waiting.
+ *  - Arguments are validated on the host before anything is enqueued; on error
+ *    nothing is launched, a non-zero sr_status is returned and sr_last_error()
+ *    (thread-local) describes it.  SR_EHIP reports a failed launch.
+ *  - Storage dtype (sr_config.dtype): SR_F32 or SR_BF16.  Activations, weights,
+ *    biases, LayerNorm parameters and the conditioning vector are stored in it;
+ *    all accumulation is fp32; weight gradients and dcond are always fp32.
+ *  - Shapes: B samples, L tokens per sample, D channels, H heads (D % H == 0),
+ *    F MLP width, n_blocks middle blocks; S = K (routed) or L (dense) tokens per
+ *    sample inside the stack.
+ *  - Support: D % 64 == 0 and F % 64 == 0; any head dim (hd = 64 runs the MFMA
+ *    attention, other sizes a generic kernel); 1 <= K <= L; B*L*D*elt < 2^31 bytes
+ *    per tensor.  Anything else returns SR_EUNSUPPORTED.
+ */
+#ifndef SR_H
+#define SR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifndef SR_API
+#define SR_API __attribute__((visibility("default")))
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SR_OK = 0,
+  SR_EINVAL = 1,        /* null pointer, negative size, bad enum value        */
+  SR_ESHAPE = 2,        /* inconsistent shapes (K > L, D % H != 0, ...)        */
+  SR_EDTYPE = 3,        /* unknown storage dtype                              */
+  SR_EALIGN = 4,        /* a tensor pointer is not 16-byte aligned            */
+  SR_EWORKSPACE = 5,    /* saved / scratch buffer smaller than required       */
+  SR_EUNSUPPORTED = 6,  /* valid but not supported by this build              */
+  SR_EHIP = 7           /* a HIP launch failed; sr_last_error() has the text  */
+} sr_status;
+
+typedef enum { SR_F32 = 0, SR_BF16 = 1 } sr_dtype;
+
+/* Block kinds.
+ * SR_BLOCK_PRELN: h1 = h + Attn(LN1(h)); h' = h1 + MLP(LN2(h1))  (Sec. 3.3).
+ * SR_BLOCK_ADALN: (shift1,scale1,gate1,shift2,scale2,gate2) = c W_ada^T + b_ada per
+ *   sample; h1 = h + gate1*Attn(LN0(h)*(1+scale1)+shift1);
+ *   h' = h1 + gate2*MLP(LN0(h1)*(1+scale2)+shift2), LN0 = LayerNorm without affine
+ *   (FiLM scale/shift and a gate from a global conditioning vector, as in the
+ *   paper's EDM block, Sec. 2 "Generative forecasting"). */
+typedef enum { SR_BLOCK_PRELN = 0, SR_BLOCK_ADALN = 1 } sr_block_kind;
+
+/* Selectors.
+ * SR_SEL_RANDOM: per sample, the K tokens with the smallest SplitMix64 keys
+ *   key_i = mix(s_b + (i+1)*gamma), s_b = mix(s_step + (b+1)*gamma),
+ *   s_step = mix(seed + (step+1)*gamma): a uniformly random K-subset
+ *   (randperm(L)[:K]), ascending (Sec. 3.2; App. A.4).  A fresh `step` gives a
+ *   fresh draw (Sec. 3.4 "Training and inference").
+ * SR_SEL_TOPK_DIFFNORM: the K tokens with the largest
+ *   score_i = sum_d (x_t[i,d] - x_prev[i,d])^2 (fp32, fixed evaluation order:
+ *   16-byte chunks dealt round-robin to 64 partial sums, each summed in order,
+ *   then combined by an xor butterfly 32,16,8,4,2,1; no fused multiply-add),
+ *   ties to the lower index, ascending (deterministic routing ablation,
+ *   App. "regularization decomposition"). */
+typedef enum { SR_SEL_RANDOM = 0, SR_SEL_TOPK_DIFFNORM = 1 } sr_select_kind;
+
+typedef struct {
+  int32_t B, L, D, H, F, n_blocks;
+  int32_t dtype;       /* sr_dtype */
+  int32_t kind;        /* sr_block_kind */
+  float ln_eps;        /* LayerNorm epsilon (the paper leaves it unstated; 1e-6 here) */
+  int32_t idx_shared;  /* 1: idx is [1,K], one index set for every sample (the
+                          App. A.4 listing); 0: idx is [B,K], one set per sample */
+} sr_config;
+
+/* Parameters of one block, nn.Linear layout [out, in], storage dtype, device
+ * pointers.  QKV rows are ordered q, k, v; head j owns rows j*hd .. j*hd+hd-1 of
+ * each.  PRELN blocks read ln*, w_qkv..b_fc2 (w_ada/b_ada may be NULL); ADALN
+ * blocks read w_qkv..b_fc2 and w_ada [6D,D] / b_ada [6D] (ln* may be NULL). */
+typedef struct {
+  const void *ln1_w, *ln1_b, *w_qkv, *b_qkv, *w_o, *b_o;
+  const void *ln2_w, *ln2_b, *w_fc1, *b_fc1, *w_fc2, *b_fc2;
+  const void *w_ada, *b_ada;
+} sr_block_params;
+
+/* Gradients of one block, fp32 device buffers shaped like the parameters.
+ * They are OVERWRITTEN (not accumulated).  A NULL member skips that gradient;
+ * members for parameters the block kind does not use are written with zeros. */
+typedef struct {
+  float *ln1_w, *ln1_b, *w_qkv, *b_qkv, *w_o, *b_o;
+  float *ln2_w, *ln2_b, *w_fc1, *b_fc1, *w_fc2, *b_fc2;
+  float *w_ada, *b_ada;
+} sr_block_grads;
+
+/* Text of the last error on this thread ("" if none).  The pointer stays valid
+ * until the next failing call on the same thread. */
+SR_API const char* sr_last_error(void);
+
+/* Library version string. */
+SR_API const char* sr_version(void);
+
+/* Bytes of the `saved` (activations kept from forward for backward) and
+ * `scratch` buffers needed by the block calls at S tokens per sample. */
+SR_API sr_status sr_workspace_bytes(const sr_config* cfg, int32_t S, size_t* saved_bytes,
+                             size_t* scratch_bytes);
+
+/* Bytes of scratch sr_select_indices needs for `select_kind` (0 for random). */
+SR_API sr_status sr_select_scratch_bytes(const sr_config* cfg, int32_t select_kind,
+                                  size_t* scratch_bytes);
+
+/* Token selection (Sec. 3.2; Alg. 1 stage 2; App. A.4).
+ *   K: tokens kept per sample, K = floor(r*L) computed by the caller (1 <= K <= L).
+ *   select_kind: sr_select_kind.  seed, step: the random draw (RANDOM only).
+ *   x_t, x_prev: [B,L,D] storage dtype (TOPK only; NULL for RANDOM).
+ *   idx: [B,K] int32 out (or [1,K] with idx_shared, drawn for sample 0),
+ *        strictly increasing per row.
+ *   scratch: sr_select_scratch_bytes bytes (may be NULL when that is 0). */
+SR_API sr_status sr_select_indices(const sr_config* cfg, int32_t K, int32_t select_kind,
+                            uint64_t seed, uint64_t step, const void* x_t,
+                            const void* x_prev, int32_t* idx, void* scratch,
+                            size_t scratch_bytes, void* stream);
+
+/* Gather (Sec. 3.2, h0 = Gather(x, I)): h0[b,k,:] = x[b, idx[b,k], :], a bit copy.
+ *   x: [B,L,D] storage dtype; idx: [B,K] (or [1,K]); h0: [B,K,D] out.
+ *   idx entries must lie in [0,L) (sr_select_indices guarantees it). */
+SR_API sr_status sr_gather(const sr_config* cfg, int32_t K, const void* x, const int32_t* idx,
+                    void* h0, void* stream);
+
+/* Residual-delta scatter (Eq. scatter), IN PLACE on x:
+ *   x[b,i,:] <- rnd( f32(x[b,i,:]) + (f32(h[b,k,:]) - f32(h0[b,k,:])) ), i = idx[b,k],
+ * fp32 subtract then add, one round-to-nearest-even to the storage dtype; rows not
+ * in idx are not touched (they keep x0 bit for bit).  h0 == NULL re-reads x[idx]
+ * (equal to h0 by definition).  idx rows must be duplicate-free.
+ * The backward of the routed step uses the same call:
+ *   gather(g) -> blocks_bwd -> scatter_delta(g, dh_in, NULL, idx). */
+SR_API sr_status sr_scatter_delta(const sr_config* cfg, int32_t K, void* x, const void* h,
+                           const void* h0, const int32_t* idx, void* stream);
+
+/* The n_blocks middle blocks on S tokens per sample (Eq. sparse_forward).
+ *   params: host array of n_blocks sr_block_params.
+ *   cond: [B,D] storage dtype (ADALN) or NULL.
+ *   h_in: [B,S,D] in; h_out: [B,S,D] out (may not alias h_in).
+ *   saved: activations for sr_sparse_blocks_bwd; must outlive it.
+ * Inside the stack the residual stream is fp32; h_out is rounded once. */
+SR_API sr_status sr_sparse_blocks_fwd(const sr_config* cfg, int32_t S,
+                               const sr_block_params* params, const void* cond,
+                               const void* h_in, void* h_out, void* saved,
+                               size_t saved_bytes, void* scratch, size_t scratch_bytes,
+                               void* stream);
+
+/* Vector-Jacobian product of sr_sparse_blocks_fwd (same cfg, S, params, cond, saved).
+ *   dh_out: [B,S,D] storage dtype in;  dh_in: [B,S,D] out (may alias dh_out).
+ *   grads: host array of n_blocks sr_block_grads (fp32, overwritten).
+ *   dcond: [B,D] fp32 out (ADALN; summed over blocks) or NULL. */
+SR_API sr_status sr_sparse_blocks_bwd(const sr_config* cfg, int32_t S,
+                               const sr_block_params* params, const void* cond,
+                               const void* saved, size_t saved_bytes, const void* dh_out,
+                               void* dh_in, const sr_block_grads* grads, float* dcond,
+                               void* scratch, size_t scratch_bytes, void* stream);
+
+/* Dense keep=100% mode (Sec. 3.4, r = 1): the same blocks on all L tokens. */
+SR_API sr_status sr_dense_blocks_fwd(const sr_config* cfg, const sr_block_params* params,
+                              const void* cond, const void* x_in, void* x_out, void* saved,
+                              size_t saved_bytes, void* scratch, size_t scratch_bytes,
+                              void* stream);
+SR_API sr_status sr_dense_blocks_bwd(const sr_config* cfg, const sr_block_params* params,
+                              const void* cond, const void* saved, size_t saved_bytes,
+                              const void* dx_out, void* dx_in, const sr_block_grads* grads,
+                              float* dcond, void* scratch, size_t scratch_bytes, void* stream);
+
+/* Debug check of an index set: *ok_dev (device int32) is set to 1 if every row of
+ * idx is strictly increasing and inside [0,L), else 0. */
+SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx,
+                              int32_t* ok_dev, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SR_H */

@@ -1,0 +1,178 @@
+"""ctypes binding of libsr (include/sr.h): the same names, argument marshalling only.
+
+Tensor arguments are torch tensors on the GPU (their ``data_ptr()`` is passed) or
+raw integer device addresses; ``stream=None`` uses torch's current stream.  A
+non-OK status raises ``SrError`` carrying ``sr_last_error()``.  If libsr.so has
+not been built, ``lib()`` raises ``SrLibraryMissing``: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsr.so")
+
+SR_OK, SR_EINVAL, SR_ESHAPE, SR_EDTYPE, SR_EALIGN, SR_EWORKSPACE, SR_EUNSUPPORTED, SR_EHIP = range(8)
+SR_F32, SR_BF16 = 0, 1
+SR_BLOCK_PRELN, SR_BLOCK_ADALN = 0, 1
+SR_SEL_RANDOM, SR_SEL_TOPK_DIFFNORM = 0, 1
+
+PARAM_FIELDS = ("ln1_w", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o", "ln2_w", "ln2_b",
+                "w_fc1", "b_fc1", "w_fc2", "b_fc2", "w_ada", "b_ada")
+
+EXPORTS = ("sr_last_error", "sr_version", "sr_workspace_bytes", "sr_select_scratch_bytes",
+           "sr_select_indices", "sr_gather", "sr_scatter_delta", "sr_sparse_blocks_fwd",
+           "sr_sparse_blocks_bwd", "sr_dense_blocks_fwd", "sr_dense_blocks_bwd", "sr_validate_indices")
+
+
+class SrLibraryMissing(RuntimeError):
+    pass
+
+
+class SrError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"libsr status {status}: {msg}")
+        self.status = status
+
+
+class SrConfig(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("L", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("H", ctypes.c_int32), ("F", ctypes.c_int32), ("n_blocks", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("kind", ctypes.c_int32), ("ln_eps", ctypes.c_float),
+                ("idx_shared", ctypes.c_int32)]
+
+
+class SrBlockParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_FIELDS]
+
+
+class SrBlockGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in PARAM_FIELDS]
+
+
+_lib = None
+
+
+def lib(path: str = LIB_PATH):
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise SrLibraryMissing(f"{path} is not built; run `python -m paper_2607_02829_amd.build`")
+    L = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    I32, U64, SZ = ctypes.c_int32, ctypes.c_uint64, ctypes.c_size_t
+    CP = ctypes.POINTER(SrConfig)
+    sig = {
+        "sr_last_error": ([], ctypes.c_char_p),
+        "sr_version": ([], ctypes.c_char_p),
+        "sr_workspace_bytes": ([CP, I32, ctypes.POINTER(SZ), ctypes.POINTER(SZ)], I32),
+        "sr_select_scratch_bytes": ([CP, I32, ctypes.POINTER(SZ)], I32),
+        "sr_select_indices": ([CP, I32, I32, U64, U64, P, P, P, P, SZ, P], I32),
+        "sr_gather": ([CP, I32, P, P, P, P], I32),
+        "sr_scatter_delta": ([CP, I32, P, P, P, P, P], I32),
+        "sr_sparse_blocks_fwd": ([CP, I32, P, P, P, P, P, SZ, P, SZ, P], I32),
+        "sr_sparse_blocks_bwd": ([CP, I32, P, P, P, SZ, P, P, P, P, P, SZ, P], I32),
+        "sr_dense_blocks_fwd": ([CP, P, P, P, P, P, SZ, P, SZ, P], I32),
+        "sr_dense_blocks_bwd": ([CP, P, P, P, SZ, P, P, P, P, P, SZ, P], I32),
+        "sr_validate_indices": ([CP, I32, P, P, P], I32),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def _p(t):
+    """torch tensor -> data_ptr; (address, nbytes) -> address; int -> int; None -> NULL."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if isinstance(t, tuple):
+        return t[0]
+    return t.data_ptr()
+
+
+def _nbytes(t):
+    """Size in bytes of a buffer argument (0 for NULL or a bare address)."""
+    if t is None or isinstance(t, int):
+        return 0
+    if isinstance(t, tuple):
+        return t[1]
+    return t.numel() * t.element_size()
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(status: int):
+    if status != SR_OK:
+        raise SrError(status, lib().sr_last_error().decode())
+
+
+def sr_version() -> str:
+    return lib().sr_version().decode()
+
+
+def sr_last_error() -> str:
+    return lib().sr_last_error().decode()
+
+
+def sr_workspace_bytes(cfg: SrConfig, S: int) -> tuple[int, int]:
+    a, b = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().sr_workspace_bytes(ctypes.byref(cfg), S, ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
+
+
+def sr_select_scratch_bytes(cfg: SrConfig, select_kind: int) -> int:
+    a = ctypes.c_size_t()
+    _check(lib().sr_select_scratch_bytes(ctypes.byref(cfg), select_kind, ctypes.byref(a)))
+    return a.value
+
+
+def sr_select_indices(cfg, K, select_kind, seed, step, x_t, x_prev, idx, scratch=None, stream=None):
+    _check(lib().sr_select_indices(ctypes.byref(cfg), K, select_kind, seed, step, _p(x_t), _p(x_prev),
+                                   _p(idx), _p(scratch), _nbytes(scratch), _stream(stream)))
+
+
+def sr_gather(cfg, K, x, idx, h0, stream=None):
+    _check(lib().sr_gather(ctypes.byref(cfg), K, _p(x), _p(idx), _p(h0), _stream(stream)))
+
+
+def sr_scatter_delta(cfg, K, x, h, h0, idx, stream=None):
+    _check(lib().sr_scatter_delta(ctypes.byref(cfg), K, _p(x), _p(h), _p(h0), _p(idx), _stream(stream)))
+
+
+def sr_sparse_blocks_fwd(cfg, S, params, cond, h_in, h_out, saved, scratch=None, stream=None):
+    _check(lib().sr_sparse_blocks_fwd(ctypes.byref(cfg), S, params, _p(cond), _p(h_in), _p(h_out),
+                                      _p(saved), _nbytes(saved), _p(scratch), _nbytes(scratch),
+                                      _stream(stream)))
+
+
+def sr_sparse_blocks_bwd(cfg, S, params, cond, saved, dh_out, dh_in, grads, dcond, scratch, stream=None):
+    _check(lib().sr_sparse_blocks_bwd(ctypes.byref(cfg), S, params, _p(cond), _p(saved), _nbytes(saved),
+                                      _p(dh_out), _p(dh_in), grads, _p(dcond), _p(scratch),
+                                      _nbytes(scratch), _stream(stream)))
+
+
+def sr_dense_blocks_fwd(cfg, params, cond, x_in, x_out, saved, scratch=None, stream=None):
+    _check(lib().sr_dense_blocks_fwd(ctypes.byref(cfg), params, _p(cond), _p(x_in), _p(x_out), _p(saved),
+                                     _nbytes(saved), _p(scratch), _nbytes(scratch), _stream(stream)))
+
+
+def sr_dense_blocks_bwd(cfg, params, cond, saved, dx_out, dx_in, grads, dcond, scratch, stream=None):
+    _check(lib().sr_dense_blocks_bwd(ctypes.byref(cfg), params, _p(cond), _p(saved), _nbytes(saved),
+                                     _p(dx_out), _p(dx_in), grads, _p(dcond), _p(scratch), _nbytes(scratch),
+                                     _stream(stream)))
+
+
+def sr_validate_indices(cfg, K, idx, ok_dev, stream=None):
+    _check(lib().sr_validate_indices(ctypes.byref(cfg), K, _p(idx), _p(ok_dev), _stream(stream)))

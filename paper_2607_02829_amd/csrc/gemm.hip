@@ -1,0 +1,290 @@
+// GEMMs of the block (QKV, output projection, MLP; forward, dX and dW).
+//
+//   C[m, n] = sum_k A(m, k) * B(n, k)
+//
+// A(m,k) is either "k-major" (A[m*lda + k]) or "m-major" (A[k*lda + m]); B(n,k)
+// likewise.  Forward X W^T is k-major x k-major; dX = dY W is k-major x n-major;
+// dW = dY^T X is m-major x n-major (the reduction runs over tokens).
+//
+// gemm_mfma: bf16 operands, fp32 accumulation on gfx950 matrix cores
+// (v_mfma_f32_32x32x16_bf16).  Workgroup tile 128 x 128 x 64, four waves in a
+// 2 x 2 arrangement, each wave 64 x 64 = 2 x 2 MFMA tiles.  Operand tiles are
+// staged in LDS in k-contiguous rows (padded by 16 bytes against bank conflicts);
+// m-major operands are transposed in registers (4 x 8 blocks) on the way in.
+// The next k-tile is prefetched into registers while the current one is consumed.
+// Global loads go through buffer resources, so rows past the end of an operand
+// read as zero: ragged token counts need no predicates in the main loop.
+//
+// gemm_simple: any element type, generic strides, fp32 FMA; used by the fp32
+// storage mode and for the tiny adaLN modulation products.
+//
+// Epilogues (per element, fp32 value v = accumulator):
+//   EPI_BIAS_ACT  out_act = Ta(v + bias)                           (QKV)
+//   EPI_RESID     t = v + bias; [adaLN: a_save = Ta(t); t *= gate_b]
+//                 out_f32 = resid + t; [out_st = T(out_f32)]       (O-proj, FC2)
+//   EPI_GELU      z = v + bias; out_act = Ta(z); out_act2 = Ta(GELU(z))   (FC1)
+//   EPI_DGELU     out_act = Ta(v * GELU'(z_in))                     (FC2 dX)
+//   EPI_ACT       out_act = Ta(v)                                   (O-proj dX)
+//   EPI_F32       out_f32[split] = v                                (dX for LN, dW partials)
+//   EPI_F32_ACC   out_f32 += v                                      (dcond over blocks)
+//   EPI_BIAS_F32  out_f32 = v + bias                                (adaLN modulation vectors)
+#include "common.h"
+#include "sr_internal.h"
+
+namespace sr {
+
+SR_DEV float gelu_f(float z) { return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f)); }
+SR_DEV float gelu_grad_f(float z) {
+  return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) + z * 0.39894228040143268f * __expf(-0.5f * z * z);
+}
+
+template <int EPI, typename T, typename Ta>
+SR_DEV void epilogue(const EpiArgs& e, int m, int n, float v) {
+  const size_t o = (size_t)m * e.ldo + n;
+  if constexpr (EPI == EPI_BIAS_ACT) {
+    ((Ta*)e.out_act)[o] = from_f32<Ta>(v + to_f32<T>(((const T*)e.bias)[n]));
+  } else if constexpr (EPI == EPI_RESID) {
+    float t = v + to_f32<T>(((const T*)e.bias)[n]);
+    if (e.gate) {
+      ((Ta*)e.a_save)[o] = from_f32<Ta>(t);
+      t *= e.gate[(size_t)(m / e.S) * e.gate_stride + n];
+    }
+    const float r = e.resid[o] + t;
+    if (e.out_f32) e.out_f32[o] = r;
+    if (e.out_st) ((T*)e.out_st)[o] = from_f32<T>(r);
+  } else if constexpr (EPI == EPI_GELU) {
+    const float z = v + to_f32<T>(((const T*)e.bias)[n]);
+    ((Ta*)e.out_act)[o] = from_f32<Ta>(z);
+    ((Ta*)e.out_act2)[o] = from_f32<Ta>(gelu_f(z));
+  } else if constexpr (EPI == EPI_DGELU) {
+    const float z = to_f32<Ta>(((const Ta*)e.z_in)[o]);
+    ((Ta*)e.out_act)[o] = from_f32<Ta>(v * gelu_grad_f(z));
+  } else if constexpr (EPI == EPI_ACT) {
+    ((Ta*)e.out_act)[o] = from_f32<Ta>(v);
+  } else if constexpr (EPI == EPI_F32) {
+    e.out_f32[(size_t)blockIdx.z * e.split_stride + o] = v;
+  } else if constexpr (EPI == EPI_F32_ACC) {
+    e.out_f32[o] += v;
+  } else if constexpr (EPI == EPI_BIAS_F32) {
+    e.out_f32[o] = v + to_f32<T>(((const T*)e.bias)[n]);
+  }
+}
+
+// ============================================================================ MFMA kernel
+
+constexpr int GM = 128, GN = 128, GK = 64;
+constexpr int LDSP = GK + 8;   // padded LDS row (bf16 elements)
+
+// Register staging of one 128 x 64 operand tile.
+struct TileRegs {
+  i32x4 v[4];
+};
+
+// k-major operand: rows r0.., k columns k0..k0+63 of X[r*ld + k].
+SR_DEV void load_kmajor(TileRegs& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    const int row = c >> 3, kc = c & 7;
+    const uint32_t off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + kc * 8)) * 2u;
+    t.v[i] = buf_load16(rs, off);
+  }
+}
+SR_DEV void store_kmajor(const TileRegs& t, bf16_t* lds) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    const int row = c >> 3, kc = c & 7;
+    *reinterpret_cast<i32x4*>(lds + row * LDSP + kc * 8) = t.v[i];
+  }
+}
+
+// r-major operand: X[k*ld + r]; thread covers 4 consecutive k x 8 consecutive r.
+SR_DEV void load_rmajor(TileRegs& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
+  const int rc = threadIdx.x & 15, kg = threadIdx.x >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t off = ((uint32_t)(k0 + kg * 4 + i) * (uint32_t)ld + (uint32_t)(r0 + rc * 8)) * 2u;
+    t.v[i] = buf_load16(rs, off);
+  }
+}
+SR_DEV void store_rmajor(const TileRegs& t, bf16_t* lds) {
+  const int rc = threadIdx.x & 15, kg = threadIdx.x >> 4;
+  const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&t.v[0]);
+  const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&t.v[1]);
+  const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&t.v[2]);
+  const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&t.v[3]);
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    i32x2 w;
+    w[0] = (int)((uint32_t)e0[r] | ((uint32_t)e1[r] << 16));
+    w[1] = (int)((uint32_t)e2[r] | ((uint32_t)e3[r] << 16));
+    *reinterpret_cast<i32x2*>(lds + (rc * 8 + r) * LDSP + kg * 4) = w;
+  }
+}
+
+template <bool AK, bool BK, int EPI, typename T, typename Ta>
+__global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bm,
+                                                          int M, int N, int Kd, int lda, int ldb, uint32_t a_bytes,
+                                                          uint32_t b_bytes, int k_per_split, EpiArgs ep) {
+  __shared__ __attribute__((aligned(16))) bf16_t As[GM * LDSP];
+  __shared__ __attribute__((aligned(16))) bf16_t Bs[GN * LDSP];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int wm = wid >> 1, wn = wid & 1;
+  const int m0 = blockIdx.y * GM, n0 = blockIdx.x * GN;
+  const int kbeg = blockIdx.z * k_per_split;
+  const int kend = min(Kd, kbeg + k_per_split);
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bm, b_bytes);
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  TileRegs ta, tb;
+  auto gload = [&](int k0) {
+    if constexpr (AK) load_kmajor(ta, ra, m0, k0, lda); else load_rmajor(ta, ra, m0, k0, lda);
+    if constexpr (BK) load_kmajor(tb, rb, n0, k0, ldb); else load_rmajor(tb, rb, n0, k0, ldb);
+  };
+  auto lstore = [&]() {
+    if constexpr (AK) store_kmajor(ta, As); else store_rmajor(ta, As);
+    if constexpr (BK) store_kmajor(tb, Bs); else store_rmajor(tb, Bs);
+  };
+
+  if (kbeg < kend) gload(kbeg);
+  for (int k0 = kbeg; k0 < kend; k0 += GK) {
+    __syncthreads();
+    lstore();
+    __syncthreads();
+    if (k0 + GK < kend) gload(k0 + GK);
+#pragma unroll
+    for (int ks = 0; ks < GK / 16; ++ks) {
+      bf16x8 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        a[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 64 + i * 32 + (lane & 31)) * LDSP + ks * 16 + (lane >> 5) * 8);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        b[j] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + j * 32 + (lane & 31)) * LDSP + ks * 16 + (lane >> 5) * 8);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+
+  // accumulator layout: register r of a 32x32 tile holds row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int n = n0 + wn * 64 + j * 32 + (lane & 31);
+        if (m < M && n < N) epilogue<EPI, T, Ta>(ep, m, n, acc[i][j][r]);
+      }
+}
+
+// ============================================================================ generic kernel
+
+template <typename TA, typename TB, int EPI, typename T, typename Ta>
+__global__ __launch_bounds__(256) void gemm_simple_kernel(const TA* __restrict__ A, const TB* __restrict__ Bm, int M,
+                                                          int N, int Kd, long long a_sm, long long a_sk,
+                                                          long long b_sn, long long b_sk, EpiArgs ep) {
+  __shared__ float As[16][65];
+  __shared__ float Bs[16][65];
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < Kd; k0 += 16) {
+    for (int t = threadIdx.x; t < 64 * 16; t += 256) {
+      const int kk = t >> 6, r = t & 63;
+      const int m = m0 + r, n = n0 + r, k = k0 + kk;
+      As[kk][r] = (m < M && k < Kd) ? to_f32<TA>(A[m * a_sm + k * a_sk]) : 0.f;
+      Bs[kk][r] = (n < N && k < Kd) ? to_f32<TB>(Bm[n * b_sn + k * b_sk]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+      if (m < M && n < N) epilogue<EPI, T, Ta>(ep, m, n, acc[i][j]);
+    }
+}
+
+// ============================================================================ dispatch
+
+template <int EPI, typename T, typename Ta>
+static hipError_t run_mfma(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
+  dim3 grid((g.N + GN - 1) / GN, (g.M + GM - 1) / GM, g.splits);
+  const int kps = g.splits > 1 ? g.k_per_split : g.K;
+#define SR_GEMM_L(AK, BK)                                                                                     \
+  hipLaunchKernelGGL((gemm_mfma_kernel<AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st, (const bf16_t*)g.A,       \
+                     (const bf16_t*)g.B, g.M, g.N, g.K, (int)g.lda, (int)g.ldb, (uint32_t)g.a_bytes,          \
+                     (uint32_t)g.b_bytes, kps, ep)
+  if (g.a_kmajor && g.b_kmajor) SR_GEMM_L(true, true);
+  else if (g.a_kmajor && !g.b_kmajor) SR_GEMM_L(true, false);
+  else if (!g.a_kmajor && !g.b_kmajor) SR_GEMM_L(false, false);
+  else SR_GEMM_L(false, true);
+#undef SR_GEMM_L
+  return hipGetLastError();
+}
+
+template <int EPI, typename T, typename Ta, typename TA, typename TB>
+static hipError_t run_simple(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
+  dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, 1);
+  const long long a_sm = g.a_kmajor ? g.lda : 1, a_sk = g.a_kmajor ? 1 : g.lda;
+  const long long b_sn = g.b_kmajor ? g.ldb : 1, b_sk = g.b_kmajor ? 1 : g.ldb;
+  hipLaunchKernelGGL((gemm_simple_kernel<TA, TB, EPI, T, Ta>), grid, dim3(256), 0, st, (const TA*)g.A,
+                     (const TB*)g.B, g.M, g.N, g.K, a_sm, a_sk, b_sn, b_sk, ep);
+  return hipGetLastError();
+}
+
+template <int EPI>
+static hipError_t dispatch(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
+  if (g.use_mfma) return run_mfma<EPI, bf16_t, bf16_t>(g, ep, st);
+  // simple path: element types of A and B, T/Ta = storage / activation type
+  if (g.dtype == kBF16) {
+    if (g.a_type == kBF16 && g.b_type == kBF16) return run_simple<EPI, bf16_t, bf16_t, bf16_t, bf16_t>(g, ep, st);
+    if (g.a_type == kF32 && g.b_type == kBF16) return run_simple<EPI, bf16_t, bf16_t, float, bf16_t>(g, ep, st);
+    if (g.a_type == kBF16 && g.b_type == kF32) return run_simple<EPI, bf16_t, bf16_t, bf16_t, float>(g, ep, st);
+    return run_simple<EPI, bf16_t, bf16_t, float, float>(g, ep, st);
+  }
+  return run_simple<EPI, float, float, float, float>(g, ep, st);
+}
+
+hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_t st) {
+  switch (epi) {
+    case EPI_BIAS_ACT: return dispatch<EPI_BIAS_ACT>(g, ep, st);
+    case EPI_RESID: return dispatch<EPI_RESID>(g, ep, st);
+    case EPI_GELU: return dispatch<EPI_GELU>(g, ep, st);
+    case EPI_DGELU: return dispatch<EPI_DGELU>(g, ep, st);
+    case EPI_ACT: return dispatch<EPI_ACT>(g, ep, st);
+    case EPI_F32: return dispatch<EPI_F32>(g, ep, st);
+    case EPI_F32_ACC: return dispatch<EPI_F32_ACC>(g, ep, st);
+    case EPI_BIAS_F32: return dispatch<EPI_BIAS_F32>(g, ep, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace sr

@@ -1,0 +1,84 @@
+// Gather and residual-delta scatter (Sec. 3.2 "Residual delta formulation",
+// Eq. scatter).  Both are HBM-bound row copies: one wave per routed row, 16-byte
+// vector accesses, rows of D * sizeof(T) bytes (a multiple of 16 bytes).
+#include "common.h"
+#include "sr_internal.h"
+
+namespace sr {
+
+constexpr int kRowsPerBlock = 4;   // one wave per row, 4 waves per workgroup
+
+// h0[b,k,:] = x[b, idx[b,k], :]
+__global__ __launch_bounds__(256) void gather_kernel(const i32x4* __restrict__ x,
+                                                     const int32_t* __restrict__ idx,
+                                                     i32x4* __restrict__ h0, int B, int L, int K,
+                                                     int chunks, int shared) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= B * K) return;
+  const int b = r / K, k = r - b * K;
+  const int i = idx[(shared ? 0 : b) * K + k];
+  const i32x4* src = x + ((size_t)b * L + i) * chunks;
+  i32x4* dst = h0 + (size_t)r * chunks;
+  for (int c = lane; c < chunks; c += 64) dst[c] = src[c];
+}
+
+// x[b,i,:] = rnd(f32(x[b,i,:]) + (f32(h[b,k,:]) - f32(h0[b,k,:]))), i = idx[b,k]
+template <typename T>
+__global__ __launch_bounds__(256) void scatter_delta_kernel(i32x4* __restrict__ x,
+                                                            const i32x4* __restrict__ h,
+                                                            const i32x4* __restrict__ h0,
+                                                            const int32_t* __restrict__ idx, int B,
+                                                            int L, int K, int chunks, int shared) {
+#pragma clang fp contract(off)
+  constexpr int V = 16 / sizeof(T);
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= B * K) return;
+  const int b = r / K, k = r - b * K;
+  const int i = idx[(shared ? 0 : b) * K + k];
+  i32x4* xr = x + ((size_t)b * L + i) * chunks;
+  const i32x4* hr = h + (size_t)r * chunks;
+  const i32x4* h0r = h0 ? h0 + (size_t)r * chunks : xr;
+  for (int c = lane; c < chunks; c += 64) {
+    i32x4 vx = xr[c];
+    i32x4 vh = __builtin_nontemporal_load(&hr[c]);
+    i32x4 v0 = h0 ? __builtin_nontemporal_load(&h0r[c]) : vx;
+    const T* ex = reinterpret_cast<const T*>(&vx);
+    const T* eh = reinterpret_cast<const T*>(&vh);
+    const T* e0 = reinterpret_cast<const T*>(&v0);
+    i32x4 out;
+    T* eo = reinterpret_cast<T*>(&out);
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      float d = __fsub_rn(to_f32<T>(eh[e]), to_f32<T>(e0[e]));
+      eo[e] = from_f32<T>(__fadd_rn(to_f32<T>(ex[e]), d));
+    }
+    xr[c] = out;
+  }
+}
+
+hipError_t launch_gather(int elt, int B, int L, int K, int D, const void* x, const int32_t* idx, void* h0,
+                         int shared, hipStream_t st) {
+  const int chunks = D * elt / 16;
+  dim3 g((B * K + kRowsPerBlock - 1) / kRowsPerBlock);
+  hipLaunchKernelGGL(gather_kernel, g, dim3(256), 0, st, (const i32x4*)x, idx, (i32x4*)h0, B, L, K, chunks,
+                     shared);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_delta(int dtype, int B, int L, int K, int D, void* x, const void* h, const void* h0,
+                                const int32_t* idx, int shared, hipStream_t st) {
+  const int elt = dtype == kBF16 ? 2 : 4;
+  const int chunks = D * elt / 16;
+  dim3 g((B * K + kRowsPerBlock - 1) / kRowsPerBlock);
+  if (dtype == kBF16)
+    hipLaunchKernelGGL(scatter_delta_kernel<bf16_t>, g, dim3(256), 0, st, (i32x4*)x, (const i32x4*)h,
+                       (const i32x4*)h0, idx, B, L, K, chunks, shared);
+  else
+    hipLaunchKernelGGL(scatter_delta_kernel<float>, g, dim3(256), 0, st, (i32x4*)x, (const i32x4*)h,
+                       (const i32x4*)h0, idx, B, L, K, chunks, shared);
+  return hipGetLastError();
+}
+
+}  // namespace sr

@@ -1,0 +1,303 @@
+// Row-wise and column-wise kernels of the block: LayerNorm forward/backward (with
+// the optional adaLN modulation), deterministic column reductions (bias and
+// modulation gradients), dtype conversion, and the attention row-sum
+// delta_i = sum_d dO[i,d] * O[i,d].
+//
+// LayerNorm (block of Sec. 3.3): y = (x - mean) * rstd * gamma + beta, biased
+// variance over D, two-pass mean/variance in fp32 registers, one wave per row.
+// With adaLN the affine step is replaced by y = xhat * (1 + scale_b) + shift_b.
+#include "common.h"
+#include "sr_internal.h"
+
+namespace sr {
+
+constexpr int kMaxPerLane = 32;   // D <= 2048
+
+// x: fp32 [M, D]; mod (adaLN): fp32 [B, 6D] with shift at mod_off, scale at mod_off + D.
+template <typename T, typename Ta>
+__global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x, const T* __restrict__ gamma,
+                                                     const T* __restrict__ beta, const float* __restrict__ mod,
+                                                     int mod_off, int M, int S, int D, float eps,
+                                                     Ta* __restrict__ y, float* __restrict__ mean_out,
+                                                     float* __restrict__ rstd_out) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const int n = D / 64;
+  const float* xr = x + (size_t)row * D;
+  float v[kMaxPerLane];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxPerLane; ++j)
+    if (j < n) { v[j] = xr[lane + 64 * j]; s += v[j]; }
+  const float mean = wave_sum(s) / (float)D;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxPerLane; ++j)
+    if (j < n) { float d = v[j] - mean; q += d * d; }
+  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+  Ta* yr = y + (size_t)row * D;
+  const int b = row / S;
+  const float* shift = mod ? mod + (size_t)b * 6 * D + mod_off : nullptr;
+  const float* scale = mod ? shift + D : nullptr;
+#pragma unroll
+  for (int j = 0; j < kMaxPerLane; ++j)
+    if (j < n) {
+      const int c = lane + 64 * j;
+      float xh = (v[j] - mean) * rstd;
+      float o = mod ? xh * (1.0f + scale[c]) + shift[c]
+                    : xh * to_f32<T>(gamma[c]) + to_f32<T>(beta[c]);
+      yr[c] = from_f32<Ta>(o);
+    }
+  if (lane == 0) { mean_out[row] = mean; rstd_out[row] = rstd; }
+}
+
+// Backward.  du: fp32 [M, D] gradient of the LayerNorm output (after modulation);
+// dres: fp32 [M, D] residual gradient added to the result (may alias dx).
+// dx = dres + (dxhat - mean(dxhat) - xhat * mean(dxhat * xhat)) * rstd with
+// dxhat = du * gamma (or du * (1 + scale_b)).  Per chunk of rows (never straddling
+// a sample) it writes partial column sums of du * xhat and du to part[(b*nchunk + c) * 2D].
+constexpr int kLnBwdRows = 16;
+
+template <typename T, typename Ta>
+__global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ du, const float* __restrict__ x,
+                                                     const float* __restrict__ mean, const float* __restrict__ rstd,
+                                                     const T* __restrict__ gamma, const float* __restrict__ mod,
+                                                     int mod_off, const float* dres, int S, int D, float* dx,
+                                                     Ta* __restrict__ dx_act, float* __restrict__ part) {
+  __shared__ float red[4][2][kMaxPerLane * 64 / 4];   // four waves' partials, 512 columns per pass
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int b = blockIdx.y, chunk = blockIdx.x, nchunk = gridDim.x;
+  const int r0 = chunk * kLnBwdRows;
+  const int n = D / 64;
+  const float* scale = mod ? mod + (size_t)b * 6 * D + mod_off + D : nullptr;
+  float pg[kMaxPerLane], pb[kMaxPerLane];
+#pragma unroll
+  for (int j = 0; j < kMaxPerLane; ++j) { pg[j] = 0.f; pb[j] = 0.f; }
+  for (int rr = wid; rr < kLnBwdRows; rr += 4) {
+    const int s = r0 + rr;
+    if (s >= S) break;
+    const size_t row = (size_t)b * S + s;
+    const float mu = mean[row], rs = rstd[row];
+    const float* dur = du + row * D;
+    const float* xr = x + row * D;
+    float xh[kMaxPerLane], dxh[kMaxPerLane];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < kMaxPerLane; ++j)
+      if (j < n) {
+        const int c = lane + 64 * j;
+        float g = dur[c];
+        xh[j] = (xr[c] - mu) * rs;
+        float w = mod ? 1.0f + scale[c] : to_f32<T>(gamma[c]);
+        dxh[j] = g * w;
+        s1 += dxh[j];
+        s2 += dxh[j] * xh[j];
+        pg[j] += g * xh[j];
+        pb[j] += g;
+      }
+    const float m1 = wave_sum(s1) / (float)D, m2 = wave_sum(s2) / (float)D;
+#pragma unroll
+    for (int j = 0; j < kMaxPerLane; ++j)
+      if (j < n) {
+        const int c = lane + 64 * j;
+        float o = (dxh[j] - m1 - xh[j] * m2) * rs + dres[row * D + c];
+        dx[row * D + c] = o;
+        if (dx_act) dx_act[row * D + c] = from_f32<Ta>(o);
+      }
+  }
+  // combine the four waves' partials through LDS, D/4 columns per pass
+  float* out = part + ((size_t)b * nchunk + chunk) * 2 * D;
+  const int cols_per_pass = 64 * kMaxPerLane / 4;   // 512
+  for (int c0 = 0; c0 < D; c0 += cols_per_pass) {
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kMaxPerLane; ++j) {
+      const int c = lane + 64 * j;
+      if (j < n && c >= c0 && c < c0 + cols_per_pass) {
+        red[wid][0][c - c0] = pg[j];
+        red[wid][1][c - c0] = pb[j];
+      }
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < cols_per_pass && c0 + t < D; t += 256) {
+      float a = red[0][0][t] + red[1][0][t] + red[2][0][t] + red[3][0][t];
+      float bb = red[0][1][t] + red[1][1][t] + red[2][1][t] + red[3][1][t];
+      out[c0 + t] = a;
+      out[D + c0 + t] = bb;
+    }
+  }
+}
+
+// out[g*out_stride + c] = sum_k part[(g*nchunk + k)*stride + c] for c < width; with
+// sum_groups the groups are summed as well (out[c]).  Fixed order: deterministic.
+__global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restrict__ part, int groups, int nchunk,
+                                                           int width, long long stride, int sum_groups,
+                                                           float* __restrict__ out0, int out_stride) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int g = blockIdx.y;
+  if (c >= width) return;
+  if (sum_groups) {
+    if (g > 0) return;
+    float acc = 0.f;
+    for (int gg = 0; gg < groups; ++gg)
+      for (int k = 0; k < nchunk; ++k) acc += part[((size_t)gg * nchunk + k) * stride + c];
+    out0[c] = acc;
+  } else {
+    float acc = 0.f;
+    for (int k = 0; k < nchunk; ++k) acc += part[((size_t)g * nchunk + k) * stride + c];
+    out0[(size_t)g * out_stride + c] = acc;
+  }
+}
+
+// Per-sample column sums of X (or X * Y), in chunks of kColRows rows:
+// part[(b * nchunk + chunk) * N + c].  Optional per-sample column weights w[b*wstride + c].
+constexpr int kColRows = 64;
+template <typename TX, typename TY>
+__global__ __launch_bounds__(256) void colsum_kernel(const TX* __restrict__ X, const TY* __restrict__ Y,
+                                                     const float* __restrict__ w, int wstride, int S, int N,
+                                                     float* __restrict__ part) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  const int chunk = blockIdx.y, b = blockIdx.z, nchunk = gridDim.y;
+  if (c >= N) return;
+  const int s0 = chunk * kColRows, s1 = min(S, s0 + kColRows);
+  float acc = 0.f;
+  for (int s = s0; s < s1; ++s) {
+    const size_t o = ((size_t)b * S + s) * N + c;
+    float v = to_f32<TX>(X[o]);
+    if (Y) v *= to_f32<TY>(Y[o]);
+    acc += v;
+  }
+  if (w) acc *= w[(size_t)b * wstride + c];
+  part[((size_t)b * nchunk + chunk) * N + c] = acc;
+}
+
+// y = T(x) elementwise (storage -> fp32, fp32 -> storage, fp32 -> activation), with an
+// optional per-sample column weight (adaLN gates): y[b,s,c] = x * w[b*wstride + c].
+template <typename TI, typename TO>
+__global__ __launch_bounds__(256) void convert_kernel(const TI* __restrict__ x, TO* __restrict__ y, size_t n,
+                                                      const float* __restrict__ w, int wstride, int S, int D,
+                                                      float* __restrict__ y32) {
+  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t stride = (size_t)gridDim.x * 256;
+  for (; i < n; i += stride) {
+    float v = to_f32<TI>(x[i]);
+    if (w) {
+      const size_t row = i / D;
+      const int c = (int)(i - row * D);
+      v *= w[(row / S) * wstride + c];
+    }
+    y[i] = from_f32<TO>(v);
+    if (y32) y32[i] = v;
+  }
+}
+
+// delta[b,h,s] = sum_d dO[b,s,h*hd+d] * O[b,s,h*hd+d]
+template <typename Ta>
+__global__ __launch_bounds__(256) void attn_delta_kernel(const Ta* __restrict__ dO, const Ta* __restrict__ O,
+                                                         int B, int S, int H, int hd, float* __restrict__ delta) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= B * S * H) return;
+  const int h = t % H;
+  const int row = t / H;
+  const int b = row / S, s = row - b * S;
+  const size_t o = (size_t)row * H * hd + (size_t)h * hd;
+  float acc = 0.f;
+  for (int d = 0; d < hd; ++d) acc += to_f32<Ta>(dO[o + d]) * to_f32<Ta>(O[o + d]);
+  delta[((size_t)b * H + h) * S + s] = acc;
+}
+
+// Fill with a constant (a kernel rather than a memset node, so captured graphs replay it safely).
+__global__ __launch_bounds__(256) void fill_kernel(float* __restrict__ p, size_t n, float v) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) p[i] = v;
+}
+
+// ------------------------------------------------------------------------------ launchers
+
+static inline dim3 grid1d(size_t n, int per) { return dim3((unsigned)((n + per - 1) / per)); }
+
+hipError_t launch_ln_fwd(int dtype, const float* x, const void* gamma, const void* beta, const float* mod,
+                         int mod_off, int M, int S, int D, float eps, void* y, float* mean, float* rstd,
+                         hipStream_t st) {
+  if (dtype == kBF16)
+    hipLaunchKernelGGL((ln_fwd_kernel<bf16_t, bf16_t>), grid1d(M, 4), dim3(256), 0, st, x, (const bf16_t*)gamma,
+                       (const bf16_t*)beta, mod, mod_off, M, S, D, eps, (bf16_t*)y, mean, rstd);
+  else
+    hipLaunchKernelGGL((ln_fwd_kernel<float, float>), grid1d(M, 4), dim3(256), 0, st, x, (const float*)gamma,
+                       (const float*)beta, mod, mod_off, M, S, D, eps, (float*)y, mean, rstd);
+  return hipGetLastError();
+}
+
+int ln_bwd_chunks(int S) { return (S + kLnBwdRows - 1) / kLnBwdRows; }
+
+hipError_t launch_ln_bwd(int dtype, const float* du, const float* x, const float* mean, const float* rstd,
+                         const void* gamma, const float* mod, int mod_off, const float* dres, int B, int S, int D,
+                         float* dx, void* dx_act, float* part, hipStream_t st) {
+  dim3 g(ln_bwd_chunks(S), B);
+  if (dtype == kBF16)
+    hipLaunchKernelGGL((ln_bwd_kernel<bf16_t, bf16_t>), g, dim3(256), 0, st, du, x, mean, rstd,
+                       (const bf16_t*)gamma, mod, mod_off, dres, S, D, dx, (bf16_t*)dx_act, part);
+  else
+    hipLaunchKernelGGL((ln_bwd_kernel<float, float>), g, dim3(256), 0, st, du, x, mean, rstd,
+                       (const float*)gamma, mod, mod_off, dres, S, D, dx, (float*)dx_act, part);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_parts(const float* part, int groups, int nchunk, int width, long long stride, int sum_groups,
+                               float* out, int out_stride, hipStream_t st) {
+  dim3 g((width + 255) / 256, sum_groups ? 1 : groups);
+  hipLaunchKernelGGL(reduce_parts_kernel, g, dim3(256), 0, st, part, groups, nchunk, width, stride, sum_groups, out,
+                     out_stride);
+  return hipGetLastError();
+}
+
+int colsum_chunks(int S) { return (S + kColRows - 1) / kColRows; }
+
+// X type: 0 = fp32, 1 = bf16; Y likewise (Y may be null).
+hipError_t launch_colsum(int xt, const void* X, int yt, const void* Y, const float* w, int wstride, int B, int S,
+                         int N, float* part, hipStream_t st) {
+  dim3 g((N + 255) / 256, colsum_chunks(S), B);
+#define SR_COLSUM(TX, TY) \
+  hipLaunchKernelGGL((colsum_kernel<TX, TY>), g, dim3(256), 0, st, (const TX*)X, (const TY*)Y, w, wstride, S, N, part)
+  if (xt == kBF16) {
+    if (yt == kBF16) SR_COLSUM(bf16_t, bf16_t); else SR_COLSUM(bf16_t, float);
+  } else {
+    if (yt == kBF16) SR_COLSUM(float, bf16_t); else SR_COLSUM(float, float);
+  }
+#undef SR_COLSUM
+  return hipGetLastError();
+}
+
+hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, const float* w, int wstride, int S,
+                          int D, float* y32, hipStream_t st) {
+  dim3 g((unsigned)std::min<size_t>((n + 255) / 256, 65536));
+#define SR_CONV(TI, TO) \
+  hipLaunchKernelGGL((convert_kernel<TI, TO>), g, dim3(256), 0, st, (const TI*)x, (TO*)y, n, w, wstride, S, D, y32)
+  if (ti == kBF16) {
+    if (to == kBF16) SR_CONV(bf16_t, bf16_t); else SR_CONV(bf16_t, float);
+  } else {
+    if (to == kBF16) SR_CONV(float, bf16_t); else SR_CONV(float, float);
+  }
+#undef SR_CONV
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st) {
+  dim3 g((unsigned)std::min<size_t>((n + 255) / 256, 65536));
+  hipLaunchKernelGGL(fill_kernel, g, dim3(256), 0, st, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_delta(int dtype, const void* dO, const void* O, int B, int S, int H, int hd, float* delta,
+                             hipStream_t st) {
+  const size_t n = (size_t)B * S * H;
+  if (dtype == kBF16)
+    hipLaunchKernelGGL(attn_delta_kernel<bf16_t>, grid1d(n, 256), dim3(256), 0, st, (const bf16_t*)dO,
+                       (const bf16_t*)O, B, S, H, hd, delta);
+  else
+    hipLaunchKernelGGL(attn_delta_kernel<float>, grid1d(n, 256), dim3(256), 0, st, (const float*)dO,
+                       (const float*)O, B, S, H, hd, delta);
+  return hipGetLastError();
+}
+
+}  // namespace sr

@@ -1,0 +1,88 @@
+// Internal interfaces of libsr: kernel launchers and the GEMM descriptor.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace sr {
+
+enum { kF32 = 0, kBF16 = 1 };
+
+enum {
+  EPI_BIAS_ACT = 0,
+  EPI_RESID = 1,
+  EPI_GELU = 2,
+  EPI_DGELU = 3,
+  EPI_ACT = 4,
+  EPI_F32 = 5,
+  EPI_F32_ACC = 6,
+  EPI_BIAS_F32 = 7,
+};
+
+struct EpiArgs {
+  void* out_act = nullptr;     // activation-type output
+  void* out_act2 = nullptr;    // second activation output (GELU value)
+  float* out_f32 = nullptr;    // fp32 output
+  void* out_st = nullptr;      // storage-type output
+  const void* bias = nullptr;  // storage type, [N]
+  const float* resid = nullptr;
+  const float* gate = nullptr;  // per-sample column gate (adaLN), gate[b * gate_stride + n]
+  int gate_stride = 0;
+  void* a_save = nullptr;       // branch output saved before gating (adaLN)
+  const void* z_in = nullptr;   // pre-activation for GELU'
+  long long ldo = 0;            // row stride of the outputs
+  int S = 1;                    // rows per sample (gate indexing)
+  long long split_stride = 0;   // element stride between split-K partial outputs
+};
+
+struct GemmDesc {
+  const void* A = nullptr;
+  const void* B = nullptr;
+  int M = 0, N = 0, K = 0;
+  long long lda = 0, ldb = 0;
+  size_t a_bytes = 0, b_bytes = 0;  // exact sizes of the operands (bounds of the buffer loads)
+  bool a_kmajor = true, b_kmajor = true;
+  int splits = 1, k_per_split = 0;
+  bool use_mfma = false;
+  int dtype = kBF16;          // storage type (bias / residual output)
+  int a_type = kBF16, b_type = kBF16;
+};
+
+hipError_t launch_select_random(int rows, int L, int K, uint64_t seed, uint64_t step, int32_t* idx, hipStream_t st);
+hipError_t launch_select_topk(int dtype, int rows, int L, int D, int K, const void* xt, const void* xp, float* score,
+                              int32_t* idx, hipStream_t st);
+hipError_t launch_validate(const int32_t* idx, int rows, int K, int L, int32_t* ok, hipStream_t st);
+
+hipError_t launch_gather(int elt, int B, int L, int K, int D, const void* x, const int32_t* idx, void* h0, int shared,
+                         hipStream_t st);
+hipError_t launch_scatter_delta(int dtype, int B, int L, int K, int D, void* x, const void* h, const void* h0,
+                                const int32_t* idx, int shared, hipStream_t st);
+
+hipError_t launch_ln_fwd(int dtype, const float* x, const void* gamma, const void* beta, const float* mod, int mod_off,
+                         int M, int S, int D, float eps, void* y, float* mean, float* rstd, hipStream_t st);
+int ln_bwd_chunks(int S);
+hipError_t launch_ln_bwd(int dtype, const float* du, const float* x, const float* mean, const float* rstd,
+                         const void* gamma, const float* mod, int mod_off, const float* dres, int B, int S, int D,
+                         float* dx, void* dx_act, float* part, hipStream_t st);
+hipError_t launch_reduce_parts(const float* part, int groups, int nchunk, int width, long long stride, int sum_groups,
+                               float* out, int out_stride, hipStream_t st);
+int colsum_chunks(int S);
+hipError_t launch_colsum(int xt, const void* X, int yt, const void* Y, const float* w, int wstride, int B, int S,
+                         int N, float* part, hipStream_t st);
+hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, const float* w, int wstride, int S, int D,
+                          float* y32, hipStream_t st);
+hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st);
+hipError_t launch_attn_delta(int dtype, const void* dO, const void* O, int B, int S, int H, int hd, float* delta,
+                             hipStream_t st);
+
+hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_t st);
+
+bool attn_uses_mfma(int dtype, int hd);
+hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int B, int S, int H, int D,
+                           hipStream_t st);
+hipError_t launch_attn_bwd(int dtype, const void* qkv, const void* dO, const float* lse, const float* delta,
+                           void* dqkv, int B, int S, int H, int D, hipStream_t st);
+
+}  // namespace sr

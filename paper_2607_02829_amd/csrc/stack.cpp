@@ -1,0 +1,336 @@
+// Launch sequences of the middle-block stack (Eq. sparse_forward; block of
+// Sec. 3.3) and of its vector-Jacobian product.
+//
+// Forward, per block (pre-LN; adaLN replaces the LN affine by the per-sample
+// modulation and gates the two residual branches):
+//   u1 = LN1(h)                      rowops  ln_fwd
+//   qkv = u1 W_qkv^T + b_qkv         gemm    EPI_BIAS_ACT
+//   O, lse = attention(qkv)          attention fwd
+//   h1 = h + O W_o^T + b_o           gemm    EPI_RESID
+//   u2 = LN2(h1)                     rowops  ln_fwd
+//   z, g = GELU(u2 W1^T + b1)        gemm    EPI_GELU
+//   h' = h1 + g W2^T + b2            gemm    EPI_RESID (fp32 residual stream; last block
+//                                                      rounds to the storage type once)
+// Backward runs the same steps in reverse (dW by split-K GEMMs over tokens with a
+// deterministic partial-sum reduction; bias / LN / modulation gradients by
+// chunked column sums).
+#include "stack.h"
+
+#include <cmath>
+
+namespace sr {
+
+namespace {
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(char* b) : base(b) {}
+  template <typename P>
+  P* take(size_t bytes) {
+    off = (off + 255) & ~(size_t)255;
+    P* p = base ? reinterpret_cast<P*>(base + off) : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+#define SR_TRY(x)                           \
+  do {                                      \
+    hipError_t _e = (x);                    \
+    if (_e != hipSuccess) return _e;        \
+  } while (0)
+
+GemmDesc desc(const Dims& d, const void* A, bool ak, long long lda, size_t abytes, const void* B, bool bk,
+              long long ldb, size_t bbytes, int M, int N, int K) {
+  GemmDesc g;
+  g.A = A; g.B = B; g.M = M; g.N = N; g.K = K;
+  g.lda = lda; g.ldb = ldb; g.a_bytes = abytes; g.b_bytes = bbytes;
+  g.a_kmajor = ak; g.b_kmajor = bk;
+  g.use_mfma = d.dtype == kBF16;
+  g.dtype = d.dtype;
+  g.a_type = d.dtype; g.b_type = d.dtype;
+  return g;
+}
+
+}  // namespace
+
+size_t layout_saved(const Dims& d, char* base, BlockSaved* out) {
+  Carver c(base);
+  const size_t M = d.M, D = d.D, F = d.F, e = d.elt;
+  for (int i = 0; i < d.nb; ++i) {
+    BlockSaved s{};
+    s.hin = c.take<float>(M * D * 4);
+    s.mean1 = c.take<float>(M * 4);
+    s.rstd1 = c.take<float>(M * 4);
+    s.u1 = c.take<void>(M * D * e);
+    s.qkv = c.take<void>(M * 3 * D * e);
+    s.O = c.take<void>(M * D * e);
+    s.lse = c.take<float>((size_t)d.B * d.H * d.S * 4);
+    s.h1 = c.take<float>(M * D * 4);
+    s.mean2 = c.take<float>(M * 4);
+    s.rstd2 = c.take<float>(M * 4);
+    s.u2 = c.take<void>(M * D * e);
+    s.z = c.take<void>(M * F * e);
+    s.gz = c.take<void>(M * F * e);
+    if (d.kind == SR_BLOCK_ADALN) {
+      s.mod = c.take<float>((size_t)d.B * 6 * D * 4);
+      s.a_out = c.take<void>(M * D * e);
+      s.m_out = c.take<void>(M * D * e);
+    }
+    if (out) out[i] = s;
+  }
+  return c.off;
+}
+
+int dw_splits(const Dims& d, int N, int K) {
+  if (d.dtype != kBF16) return 1;
+  const int tiles = ((N + 127) / 128) * ((K + 127) / 128);
+  int s = (512 + tiles - 1) / tiles;
+  s = std::min(s, std::max(1, d.M / 512));
+  return std::max(1, std::min(s, 16));
+}
+
+size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
+  Carver c(base);
+  const size_t M = d.M, D = d.D, F = d.F, e = d.elt;
+  Scratch s{};
+  s.g_res = c.take<float>(M * D * 4);
+  s.g_res2 = c.take<float>(M * D * 4);
+  s.du = c.take<float>(M * D * 4);
+  s.delta = c.take<float>((size_t)d.B * d.H * d.S * 4);
+  size_t wp = 0;
+  const int shapes[4][2] = {{3 * d.D, d.D}, {d.D, d.D}, {d.F, d.D}, {d.D, d.F}};
+  for (auto& sh : shapes) {
+    const int sp = dw_splits(d, sh[0], sh[1]);
+    if (sp > 1) wp = std::max(wp, (size_t)sp * sh[0] * sh[1]);
+  }
+  s.wpart = c.take<float>(std::max<size_t>(wp, 1) * 4);
+  const size_t wmax = std::max<size_t>(std::max<size_t>(3 * D, F), 6 * D);
+  s.part = c.take<float>((size_t)d.B * colsum_chunks(d.S) * wmax * 4);
+  s.lnpart = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
+  s.dmod = c.take<float>((size_t)d.B * 6 * D * 4);
+  s.g_act = c.take<void>(M * D * e);
+  s.dz = c.take<void>(M * F * e);
+  s.dO = c.take<void>(M * D * e);
+  s.dqkv = c.take<void>(M * 3 * D * e);
+  if (out) *out = s;
+  return c.off;
+}
+
+// ============================================================================ forward
+
+hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, const void* h_in, void* h_out,
+                     char* saved, hipStream_t st) {
+  BlockSaved* sv = new BlockSaved[d.nb];
+  layout_saved(d, saved, sv);
+  const int M = d.M, D = d.D, F = d.F, S = d.S;
+  const size_t e = d.elt;
+  const bool ada = d.kind == SR_BLOCK_ADALN;
+  hipError_t err = hipSuccess;
+  auto run = [&]() -> hipError_t {
+    SR_TRY(launch_convert(d.dtype, h_in, kF32, sv[0].hin, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
+    for (int i = 0; i < d.nb; ++i) {
+      const BlockSaved& s = sv[i];
+      const sr_block_params& w = p[i];
+      if (ada) {
+        GemmDesc g = desc(d, cond, true, D, (size_t)d.B * D * e, w.w_ada, true, D, (size_t)6 * D * D * e, d.B,
+                          6 * D, D);
+        g.use_mfma = false;
+        EpiArgs ep; ep.out_f32 = s.mod; ep.bias = w.b_ada; ep.ldo = 6 * D;
+        SR_TRY(launch_gemm(g, EPI_BIAS_F32, ep, st));
+      }
+      SR_TRY(launch_ln_fwd(d.dtype, s.hin, w.ln1_w, w.ln1_b, ada ? s.mod : nullptr, 0, M, S, D, d.eps, s.u1,
+                           s.mean1, s.rstd1, st));
+      {
+        GemmDesc g = desc(d, s.u1, true, D, (size_t)M * D * e, w.w_qkv, true, D, (size_t)3 * D * D * e, M, 3 * D, D);
+        EpiArgs ep; ep.out_act = s.qkv; ep.bias = w.b_qkv; ep.ldo = 3 * D;
+        SR_TRY(launch_gemm(g, EPI_BIAS_ACT, ep, st));
+      }
+      SR_TRY(launch_attn_fwd(d.dtype, s.qkv, s.O, s.lse, d.B, S, d.H, D, st));
+      {
+        GemmDesc g = desc(d, s.O, true, D, (size_t)M * D * e, w.w_o, true, D, (size_t)D * D * e, M, D, D);
+        EpiArgs ep; ep.bias = w.b_o; ep.resid = s.hin; ep.out_f32 = s.h1; ep.ldo = D; ep.S = S;
+        if (ada) { ep.gate = s.mod + 2 * D; ep.gate_stride = 6 * D; ep.a_save = s.a_out; }
+        SR_TRY(launch_gemm(g, EPI_RESID, ep, st));
+      }
+      SR_TRY(launch_ln_fwd(d.dtype, s.h1, w.ln2_w, w.ln2_b, ada ? s.mod : nullptr, 3 * D, M, S, D, d.eps, s.u2,
+                           s.mean2, s.rstd2, st));
+      {
+        GemmDesc g = desc(d, s.u2, true, D, (size_t)M * D * e, w.w_fc1, true, D, (size_t)F * D * e, M, F, D);
+        EpiArgs ep; ep.bias = w.b_fc1; ep.out_act = s.z; ep.out_act2 = s.gz; ep.ldo = F;
+        SR_TRY(launch_gemm(g, EPI_GELU, ep, st));
+      }
+      {
+        GemmDesc g = desc(d, s.gz, true, F, (size_t)M * F * e, w.w_fc2, true, F, (size_t)D * F * e, M, D, F);
+        EpiArgs ep; ep.bias = w.b_fc2; ep.resid = s.h1; ep.ldo = D; ep.S = S;
+        if (i + 1 < d.nb) ep.out_f32 = sv[i + 1].hin; else ep.out_st = h_out;
+        if (ada) { ep.gate = s.mod + 5 * D; ep.gate_stride = 6 * D; ep.a_save = s.m_out; }
+        SR_TRY(launch_gemm(g, EPI_RESID, ep, st));
+      }
+    }
+    return hipSuccess;
+  };
+  err = run();
+  delete[] sv;
+  return err;
+}
+
+// ============================================================================ backward
+
+namespace {
+
+// dW[N x K] = sum_m dY[m, n] X[m, k], both operands token-major ([M, N] and [M, K]).
+hipError_t weight_grad(const Dims& d, const void* dY, int N, const void* X, int K, float* out, const Scratch& sc,
+                       hipStream_t st) {
+  if (!out) return hipSuccess;
+  const size_t e = d.elt;
+  GemmDesc g = desc(d, dY, false, N, (size_t)d.M * N * e, X, false, K, (size_t)d.M * K * e, N, K, d.M);
+  const int sp = dw_splits(d, N, K);
+  EpiArgs ep; ep.ldo = K;
+  if (sp > 1) {
+    g.splits = sp;
+    g.k_per_split = ((d.M + sp - 1) / sp + 63) / 64 * 64;
+    g.splits = (d.M + g.k_per_split - 1) / g.k_per_split;
+    ep.out_f32 = sc.wpart;
+    ep.split_stride = (long long)N * K;
+    SR_TRY(launch_gemm(g, EPI_F32, ep, st));
+    return launch_reduce_parts(sc.wpart, 1, g.splits, N * K, (long long)N * K, 0, out, 0, st);
+  }
+  ep.out_f32 = out;
+  return launch_gemm(g, EPI_F32, ep, st);
+}
+
+// out[c] = sum over all tokens of X (optionally * per-sample weight w[b*wstride + c]).
+hipError_t bias_grad(const Dims& d, int xt, const void* X, const float* w, int wstride, int N, float* out,
+                     const Scratch& sc, hipStream_t st) {
+  if (!out) return hipSuccess;
+  SR_TRY(launch_colsum(xt, X, kF32, nullptr, w, wstride, d.B, d.S, N, sc.part, st));
+  return launch_reduce_parts(sc.part, d.B, colsum_chunks(d.S), N, N, 1, out, 0, st);
+}
+
+// dmod[b, off + c] = sum_s X[b,s,c] * Y[b,s,c]
+hipError_t gate_grad(const Dims& d, const float* X, const void* Y, float* dmod, int off, const Scratch& sc,
+                     hipStream_t st) {
+  SR_TRY(launch_colsum(kF32, X, d.dtype, Y, nullptr, 0, d.B, d.S, d.D, sc.part, st));
+  return launch_reduce_parts(sc.part, d.B, colsum_chunks(d.S), d.D, d.D, 0, dmod + off, 6 * d.D, st);
+}
+
+hipError_t zero_f32(float* p, size_t n, hipStream_t st) {
+  return p ? launch_fill_f32(p, n, 0.0f, st) : hipSuccess;
+}
+
+}  // namespace
+
+hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, const char* saved,
+                     const void* dh_out, void* dh_in, const sr_block_grads* gr, float* dcond, char* scratch,
+                     hipStream_t st) {
+  BlockSaved* sv = new BlockSaved[d.nb];
+  layout_saved(d, const_cast<char*>(saved), sv);
+  Scratch sc;
+  layout_scratch(d, scratch, &sc);
+  const int M = d.M, D = d.D, F = d.F, S = d.S;
+  const size_t e = d.elt;
+  const bool ada = d.kind == SR_BLOCK_ADALN;
+  const int nln = ln_bwd_chunks(S);
+
+  auto run = [&]() -> hipError_t {
+    // g_res = fp32(dh_out); the activation copy is made per block below
+    SR_TRY(launch_convert(d.dtype, dh_out, kF32, sc.g_res, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
+    for (int i = d.nb - 1; i >= 0; --i) {
+      const BlockSaved& s = sv[i];
+      const sr_block_params& w = p[i];
+      const sr_block_grads& g = gr[i];
+      // activation copy of the MLP-branch gradient (gated for adaLN)
+      SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, sc.g_act, (size_t)M * D, ada ? s.mod + 5 * D : nullptr, 6 * D,
+                            S, D, nullptr, st));
+      if (ada) SR_TRY(gate_grad(d, sc.g_res, s.m_out, sc.dmod, 5 * D, sc, st));
+      // FC2
+      SR_TRY(weight_grad(d, sc.g_act, D, s.gz, F, g.w_fc2, sc, st));
+      SR_TRY(bias_grad(d, kF32, sc.g_res, ada ? s.mod + 5 * D : nullptr, 6 * D, D, g.b_fc2, sc, st));
+      {
+        GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
+        EpiArgs ep; ep.z_in = s.z; ep.out_act = sc.dz; ep.ldo = F;
+        SR_TRY(launch_gemm(gd, EPI_DGELU, ep, st));
+      }
+      // FC1
+      SR_TRY(weight_grad(d, sc.dz, F, s.u2, D, g.w_fc1, sc, st));
+      SR_TRY(bias_grad(d, d.dtype, sc.dz, nullptr, 0, F, g.b_fc1, sc, st));
+      {
+        GemmDesc gd = desc(d, sc.dz, true, F, (size_t)M * F * e, w.w_fc1, false, D, (size_t)F * D * e, M, D, F);
+        EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
+        SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
+      }
+      // LN2 (residual: g_res2 = g_res + LN2^T du)
+      SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
+                           d.B, S, D, sc.g_res2, ada ? nullptr : sc.g_act, sc.lnpart, st));
+      if (ada) {
+        SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 0, sc.dmod + 4 * D, 6 * D, st));   // dscale2
+        SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 0, sc.dmod + 3 * D, 6 * D, st));  // dshift2
+        SR_TRY(gate_grad(d, sc.g_res2, s.a_out, sc.dmod, 2 * D, sc, st));
+        SR_TRY(launch_convert(kF32, sc.g_res2, d.dtype, sc.g_act, (size_t)M * D, s.mod + 2 * D, 6 * D, S, D, nullptr,
+                              st));
+      } else {
+        if (g.ln2_w) SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 1, g.ln2_w, 0, st));
+        if (g.ln2_b) SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 1, g.ln2_b, 0, st));
+      }
+      // output projection
+      SR_TRY(weight_grad(d, sc.g_act, D, s.O, D, g.w_o, sc, st));
+      SR_TRY(bias_grad(d, kF32, sc.g_res2, ada ? s.mod + 2 * D : nullptr, 6 * D, D, g.b_o, sc, st));
+      {
+        GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_o, false, D, (size_t)D * D * e, M, D, D);
+        EpiArgs ep; ep.out_act = sc.dO; ep.ldo = D;
+        SR_TRY(launch_gemm(gd, EPI_ACT, ep, st));
+      }
+      // attention
+      SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, d.B, S, d.H, D / d.H, sc.delta, st));
+      SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, d.B, S, d.H, D, st));
+      // QKV
+      SR_TRY(weight_grad(d, sc.dqkv, 3 * D, s.u1, D, g.w_qkv, sc, st));
+      SR_TRY(bias_grad(d, d.dtype, sc.dqkv, nullptr, 0, 3 * D, g.b_qkv, sc, st));
+      {
+        GemmDesc gd = desc(d, sc.dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,
+                           M, D, 3 * D);
+        EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
+        SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
+      }
+      // LN1 (residual: g_res = g_res2 + LN1^T du)
+      SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2, d.B,
+                           S, D, sc.g_res, nullptr, sc.lnpart, st));
+      if (ada) {
+        SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 0, sc.dmod + D, 6 * D, st));   // dscale1
+        SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 0, sc.dmod, 6 * D, st));   // dshift1
+        // dW_ada = dmod^T c ; db_ada = sum_b dmod ; dcond (+)= dmod W_ada
+        if (g.w_ada) {
+          GemmDesc gd = desc(d, sc.dmod, false, 6 * D, (size_t)d.B * 6 * D * 4, cond, false, D, (size_t)d.B * D * e,
+                             6 * D, D, d.B);
+          gd.use_mfma = false; gd.a_type = kF32;
+          EpiArgs ep; ep.out_f32 = g.w_ada; ep.ldo = D;
+          SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
+        }
+        if (g.b_ada) SR_TRY(launch_reduce_parts(sc.dmod, d.B, 1, 6 * D, 6 * D, 1, g.b_ada, 0, st));
+        if (dcond) {
+          GemmDesc gd = desc(d, sc.dmod, true, 6 * D, (size_t)d.B * 6 * D * 4, w.w_ada, false, D,
+                             (size_t)6 * D * D * e, d.B, D, 6 * D);
+          gd.use_mfma = false; gd.a_type = kF32;
+          EpiArgs ep; ep.out_f32 = dcond; ep.ldo = D;
+          SR_TRY(launch_gemm(gd, i == d.nb - 1 ? EPI_F32 : EPI_F32_ACC, ep, st));
+        }
+        // parameters the adaLN block does not use get zero gradients
+        SR_TRY(zero_f32(g.ln1_w, D, st)); SR_TRY(zero_f32(g.ln1_b, D, st));
+        SR_TRY(zero_f32(g.ln2_w, D, st)); SR_TRY(zero_f32(g.ln2_b, D, st));
+      } else {
+        if (g.ln1_w) SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 1, g.ln1_w, 0, st));
+        if (g.ln1_b) SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 1, g.ln1_b, 0, st));
+        SR_TRY(zero_f32(g.w_ada, (size_t)6 * D * D, st));
+        SR_TRY(zero_f32(g.b_ada, (size_t)6 * D, st));
+      }
+    }
+    return launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st);
+  };
+  hipError_t err = run();
+  delete[] sv;
+  return err;
+}
+
+}  // namespace sr

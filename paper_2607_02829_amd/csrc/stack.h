@@ -1,0 +1,41 @@
+// Host-side orchestration of the middle-block stack: workspace layout and the
+// per-block launch sequences (forward and backward).
+#pragma once
+#include <string>
+
+#include "../../include/sr.h"
+#include "sr_internal.h"
+
+namespace sr {
+
+struct Dims {
+  int B, L, D, H, F, nb, S, M;
+  int dtype, kind;
+  float eps;
+  size_t elt;   // bytes per storage / activation element
+};
+
+struct BlockSaved {
+  float *hin, *mean1, *rstd1, *lse, *h1, *mean2, *rstd2, *mod;
+  void *u1, *qkv, *O, *u2, *z, *gz, *a_out, *m_out;
+};
+
+struct Scratch {
+  float *g_res, *g_res2, *du, *delta, *wpart, *part, *lnpart, *dmod;
+  void *g_act, *dz, *dO, *dqkv;
+};
+
+// Carve `base` (may be null: sizes only).  Returns the bytes used.
+size_t layout_saved(const Dims& d, char* base, BlockSaved* out /* [nb] or null */);
+size_t layout_scratch(const Dims& d, char* base, Scratch* out /* or null */);
+
+// Split-K factor of the weight-gradient GEMM producing an N x K result.
+int dw_splits(const Dims& d, int N, int K);
+
+hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, const void* h_in, void* h_out,
+                     char* saved, hipStream_t st);
+hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, const char* saved,
+                     const void* dh_out, void* dh_in, const sr_block_grads* g, float* dcond, char* scratch,
+                     hipStream_t st);
+
+}  // namespace sr

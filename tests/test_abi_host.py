@@ -1,0 +1,99 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol the header
+declares, sizes workspaces, and rejects bad arguments before launching anything."""
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2607_02829_amd import abi
+
+pytestmark = pytest.mark.cpu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sr.h")
+
+
+def _lib_or_skip():
+    try:
+        return abi.lib()
+    except abi.SrLibraryMissing as e:
+        pytest.skip(str(e))
+
+
+def test_header_symbols_exported():
+    _lib_or_skip()
+    declared = set(re.findall(r"SR_API\s+[\w\s\*]+?\b(sr_\w+)\s*\(", open(HEADER).read()))
+    assert declared == set(abi.EXPORTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", abi.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (sr_\w+)", out))
+    assert declared <= exported, declared - exported
+
+
+def _cfg(**kw):
+    base = dict(B=2, L=100, D=256, H=4, F=1024, n_blocks=2, dtype=abi.SR_BF16, kind=abi.SR_BLOCK_PRELN,
+                ln_eps=1e-6, idx_shared=0)
+    base.update(kw)
+    return abi.SrConfig(**base)
+
+
+def test_workspace_sizes_scale_with_tokens():
+    _lib_or_skip()
+    s1, c1 = abi.sr_workspace_bytes(_cfg(), 25)
+    s2, c2 = abi.sr_workspace_bytes(_cfg(), 100)
+    assert 0 < s1 < s2 and 0 < c1 < c2
+    # saved activations: per token per block at least D*(4+4+2*6) + F*2*2 bytes
+    assert s2 >= 2 * 2 * 100 * (256 * 20 + 1024 * 4)
+    s3, _ = abi.sr_workspace_bytes(_cfg(n_blocks=4), 100)
+    assert s3 > 1.9 * s2
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(D=250), abi.SR_ESHAPE),          # D % H != 0  (250 % 4)
+    (dict(D=192, H=4, F=768), abi.SR_EUNSUPPORTED),   # head dim 48
+    (dict(dtype=7), abi.SR_EDTYPE),
+    (dict(kind=3), abi.SR_EINVAL),
+    (dict(B=0), abi.SR_EINVAL),
+    (dict(D=96, H=3), abi.SR_EUNSUPPORTED),  # D % 64
+])
+def test_bad_config_rejected(kw, status):
+    _lib_or_skip()
+    with pytest.raises(abi.SrError) as ei:
+        abi.sr_workspace_bytes(_cfg(**kw), 10)
+    assert ei.value.status == status
+    assert abi.sr_last_error()
+
+
+def test_bad_call_arguments_rejected_before_launch():
+    _lib_or_skip()
+    cfg = _cfg()
+    fake = 1 << 40          # aligned, never dereferenced: validation fails first
+    with pytest.raises(abi.SrError) as ei:
+        abi.sr_gather(cfg, 101, fake, fake, fake, stream=0)       # K > L
+    assert ei.value.status == abi.SR_ESHAPE
+    with pytest.raises(abi.SrError) as ei:
+        abi.sr_gather(cfg, 10, fake + 2, fake, fake, stream=0)    # misaligned x
+    assert ei.value.status == abi.SR_EALIGN
+    with pytest.raises(abi.SrError) as ei:
+        abi.sr_scatter_delta(cfg, 10, None, fake, None, fake, stream=0)
+    assert ei.value.status == abi.SR_EINVAL
+    with pytest.raises(abi.SrError) as ei:
+        abi.sr_select_indices(cfg, 0, abi.SR_SEL_RANDOM, 1, 0, None, None, fake, stream=0)
+    assert ei.value.status == abi.SR_ESHAPE
+    with pytest.raises(abi.SrError) as ei:
+        abi.sr_select_indices(cfg, 10, abi.SR_SEL_TOPK_DIFFNORM, 1, 0, fake, fake, fake, fake, stream=0)
+    assert ei.value.status == abi.SR_EWORKSPACE or ei.value.status == abi.SR_EINVAL
+    # blocks: workspace too small
+    params = (abi.SrBlockParams * 2)()
+    for i in range(2):
+        for n in abi.PARAM_FIELDS:
+            setattr(params[i], n, fake)
+    lib = abi.lib()
+    import ctypes
+    st = lib.sr_sparse_blocks_fwd(ctypes.byref(cfg), 25, params, None, fake, fake + 4096, fake, 16, None, 0, None)
+    assert st == abi.SR_EWORKSPACE
+    st = lib.sr_sparse_blocks_fwd(ctypes.byref(cfg), 25, params, None, fake, fake, fake, 1 << 40, None, 0, None)
+    assert st == abi.SR_EINVAL        # h_out aliases h_in
+    ada = _cfg(kind=abi.SR_BLOCK_ADALN)
+    st = lib.sr_sparse_blocks_fwd(ctypes.byref(ada), 25, params, None, fake, fake + 4096, fake, 1 << 40, None, 0, None)
+    assert st == abi.SR_EINVAL        # adaLN without cond

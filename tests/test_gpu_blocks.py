@@ -1,0 +1,76 @@
+"""GPU parity of the middle-block stack (forward and backward) against the fp64
+oracle, at small shapes (several tiles plus ragged tails) and at the 5.625 deg
+workload; dense mode equals the stack run on all tokens."""
+import numpy as np
+import pytest
+
+from gpu_helpers import compare, gpu_blocks, host_inputs, oracle_blocks, tol_for
+from paper_2607_02829_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(w, S, n_blocks, backward=True, randomise_affine=True):
+    h, params, cond, dh = host_inputs(w, n_blocks, randomise_affine=randomise_affine, S=S)
+    gpu = gpu_blocks(w, S, h, params, cond, dh if backward else None)
+    ref = oracle_blocks(w, h, params, cond, dh if backward else None)
+    errs = compare(gpu, ref, w.dtype, w.kind)
+    tol = tol_for(w.dtype)
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    print(f"{w.name} S={S} max rel err {max(errs.values()):.3e} ({max(errs, key=errs.get)})")
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("S", [50, 130])
+def test_preln_bf16_small(S):
+    _check(inputs.small(name="preln_bf16", Hg=10, Wg=20), S, 2)
+
+
+@pytest.mark.parametrize("S", [61])
+def test_adaln_bf16_small(S):
+    _check(inputs.small(name="adaln_bf16", kind="adaln"), S, 2)
+
+
+def test_preln_bf16_hd32_generic_attention():
+    _check(inputs.small(name="hd32", H=8), 70, 1)
+
+
+def test_preln_bf16_hd128_generic_attention():
+    _check(inputs.small(name="hd128", H=2), 45, 1)
+
+
+def test_preln_f32_small_fwd_bwd():
+    _check(inputs.small(name="preln_f32", dtype="f32", D=128, H=2, F=256), 37, 2)
+
+
+def test_adaln_f32_small_fwd_bwd():
+    _check(inputs.small(name="adaln_f32", dtype="f32", D=128, H=4, F=512, kind="adaln"), 29, 2)
+
+
+def test_tiny_workload_f32_forward():
+    # 8 x 16 grid, D=128, 4 heads, 2 blocks, fp32, forward only, 32 routed tokens
+    w = inputs.WORKLOADS["tiny"]
+    _check(w, w.K, w.n_blocks, backward=False, randomise_affine=False)
+
+
+def test_b5625_workload_full_stack():
+    # 5.625 deg workload: B=8, K=128 routed tokens, D=1024, 16 heads, 8 blocks, bf16, fwd+bwd
+    w = inputs.WORKLOADS["b5625"]
+    _check(w, w.K, w.n_blocks, randomise_affine=False)
+
+
+def test_dense_mode_equals_stack_on_all_tokens():
+    w = inputs.small(name="dense", Hg=6, Wg=15)
+    h, params, cond, dh = host_inputs(w, 2, S=w.L)
+    a = gpu_blocks(w, w.L, h, params, cond, dh, dense=True)
+    b = gpu_blocks(w, w.L, h, params, cond, dh, dense=False)
+    assert np.array_equal(a["h_out"], b["h_out"])
+    assert np.array_equal(a["dh_in"], b["dh_in"])
+
+
+def test_zero_branches_identity():
+    w = inputs.small(name="zero", Hg=5, Wg=13)
+    h, _, _, _ = host_inputs(w, 2, S=w.L)
+    params = inputs.params_to_storage(inputs.block_params(w, 2, zero=("w_o", "b_o", "w_fc2", "b_fc2")), w.dtype)
+    out = gpu_blocks(w, w.L, h, params, None)
+    assert np.array_equal(out["h_out"], h)

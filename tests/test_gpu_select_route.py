@@ -1,0 +1,114 @@
+"""GPU parity: selection, gather, residual-delta scatter and the index validator,
+bit-exact against the oracle."""
+import numpy as np
+import pytest
+
+from oracle import routing as orouting
+from oracle import select as osel
+from paper_2607_02829_amd import abi, device, inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _cfg(B, L, D=64, dtype="bf16", shared=0):
+    return abi.SrConfig(B=B, L=L, D=D, H=max(1, D // 64), F=64, n_blocks=1, dtype=abi.SR_BF16 if dtype == "bf16" else abi.SR_F32,
+                        kind=0, ln_eps=1e-6, idx_shared=shared)
+
+
+@pytest.mark.parametrize("B,L,K", [
+    (1, 128, 32), (8, 512, 128), (2, 8192, 2048), (1, 16200, 4050),   # the workloads' shapes
+    (3, 5, 1), (2, 9, 9), (1, 1, 1), (1, 1025, 1000), (1, 20000, 3), (4, 3000, 2999),
+])
+def test_select_random_bitexact(B, L, K):
+    import torch
+    cfg = _cfg(B, L)
+    for step in (0, 1, 12345):
+        idx = torch.full((B, K), -1, dtype=torch.int32, device="cuda")
+        abi.sr_select_indices(cfg, K, abi.SR_SEL_RANDOM, 42, step, None, None, idx)
+        got = idx.cpu().numpy()
+        want = osel.select_random(B, L, K, 42, step)
+        assert np.array_equal(got, want), (B, L, K, step)
+
+
+def test_select_random_shared_row():
+    import torch
+    cfg = _cfg(3, 700, shared=1)
+    idx = torch.full((1, 100), -1, dtype=torch.int32, device="cuda")
+    abi.sr_select_indices(cfg, 100, abi.SR_SEL_RANDOM, 5, 2, None, None, idx)
+    assert np.array_equal(idx.cpu().numpy(), osel.select_random(1, 700, 100, 5, 2))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,L,D,K", [(2, 8192, 1024, 2048), (3, 333, 128, 70), (1, 64, 512, 64)])
+def test_select_topk_bitexact(dtype, B, L, D, K):
+    import torch
+    w = inputs.small(B=B, Hg=1, Wg=L, D=D, dtype=dtype, ell=4.0, seed=11)
+    xt = inputs.to_storage(inputs.token_field(w, 0), dtype)
+    xp = inputs.to_storage(inputs.token_field(w, 1), dtype)
+    cfg = _cfg(B, L, D, dtype)
+    scratch = torch.empty(abi.sr_select_scratch_bytes(cfg, abi.SR_SEL_TOPK_DIFFNORM), dtype=torch.uint8, device="cuda")
+    idx = torch.full((B, K), -1, dtype=torch.int32, device="cuda")
+    abi.sr_select_indices(cfg, K, abi.SR_SEL_TOPK_DIFFNORM, 0, 0, device.to_device(xt), device.to_device(xp), idx,
+                          scratch)
+    assert np.array_equal(idx.cpu().numpy(), osel.select_topk(xt, xp, K))
+    # the scores themselves (scratch holds them) are bit-identical to the oracle's
+    got_scores = scratch.view(torch.float32)[:B * L].cpu().numpy().reshape(B, L)
+    assert np.array_equal(got_scores.view(np.uint32), osel.topk_score(xt, xp).view(np.uint32))
+
+
+def test_select_topk_ties_lower_index():
+    import torch
+    B, L, D, K = 2, 300, 64, 40
+    xt = np.zeros((B, L, D), np.float32)
+    xt[:, ::3, 0] = 1.0            # 100 equal scores per sample
+    xt[1, 7, 0] = 3.0
+    xt_s, xp_s = inputs.to_storage(xt, "bf16"), inputs.to_storage(np.zeros_like(xt), "bf16")
+    cfg = _cfg(B, L, D)
+    scratch = torch.empty(B * L * 4, dtype=torch.uint8, device="cuda")
+    idx = torch.empty((B, K), dtype=torch.int32, device="cuda")
+    abi.sr_select_indices(cfg, K, abi.SR_SEL_TOPK_DIFFNORM, 0, 0, device.to_device(xt_s), device.to_device(xp_s),
+                          idx, scratch)
+    want = osel.select_topk(xt_s, xp_s, K)
+    assert np.array_equal(idx.cpu().numpy(), want)
+    assert want[0].tolist() == list(range(0, 3 * K, 3))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,L,D,K,shared", [(1, 16200, 1024, 4050, 0), (2, 8192, 1024, 2048, 0), (8, 512, 1024, 128, 0),
+                                            (3, 77, 64, 13, 0), (3, 77, 128, 13, 1)])
+def test_gather_scatter_bitexact(dtype, B, L, D, K, shared):
+    import torch
+    w = inputs.small(B=B, Hg=1, Wg=L, D=D, dtype=dtype, ell=3.0, seed=3)
+    x = inputs.to_storage(inputs.token_field(w, 0), dtype)
+    h = inputs.to_storage(inputs.token_field(w, 1)[:, :K], dtype)
+    rows = 1 if shared else B
+    idx = osel.select_random(rows, L, K, 9, 1)
+    cfg = _cfg(B, L, D, dtype, shared)
+    xd, idd = device.to_device(x), device.to_device(idx)
+    h0 = torch.empty((B, K, D), dtype=xd.dtype, device="cuda")
+    abi.sr_gather(cfg, K, xd, idd, h0)
+    want_h0 = orouting.gather(x, idx, bool(shared))
+    assert np.array_equal(device.to_host(h0), want_h0)
+    hd = device.to_device(h)
+    # explicit h0
+    x1 = xd.clone()
+    abi.sr_scatter_delta(cfg, K, x1, hd, h0, idd)
+    want = orouting.scatter_delta(x, h, want_h0, idx, bool(shared))
+    assert np.array_equal(device.to_host(x1).view(np.uint8), want.view(np.uint8))
+    # h0 = NULL (re-read from x): the backward's form
+    x2 = xd.clone()
+    abi.sr_scatter_delta(cfg, K, x2, hd, None, idd)
+    want2 = orouting.scatter_delta(x, h, None, idx, bool(shared))
+    assert np.array_equal(device.to_host(x2).view(np.uint8), want2.view(np.uint8))
+
+
+def test_validate_indices():
+    import torch
+    cfg = _cfg(2, 50)
+    ok = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    good = torch.tensor([[1, 5, 49], [0, 2, 3]], dtype=torch.int32, device="cuda")
+    abi.sr_validate_indices(cfg, 3, good, ok)
+    assert ok.item() == 1
+    for bad in ([[1, 5, 50], [0, 2, 3]], [[1, 1, 4], [0, 2, 3]], [[1, 5, 9], [3, 2, 4]], [[-1, 5, 9], [0, 2, 3]]):
+        abi.sr_validate_indices(cfg, 3, torch.tensor(bad, dtype=torch.int32, device="cuda"), ok)
+        assert ok.item() == 0, bad
