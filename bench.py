@@ -1,0 +1,270 @@
+#!/usr/bin/env python3
+"""Benchmark of the routed middle-block stack on one MI355X.
+
+One step is one pass of the whole hot path over one batch:
+    select -> gather -> blocks fwd -> residual-delta scatter
+           -> gather(g) -> blocks bwd -> scatter(g)
+(Alg. 1 stage 2 and its backward), on the 0.25 deg workload by default:
+B=1, 90 x 180 token grid (L=16200), keep 25% (K=4050), D=1024, 16 heads, MLP 4096,
+12 middle blocks, bf16 storage with fp32 accumulation, synthetic smooth token
+fields and N(0, 0.02) weights, all resident in HBM before timing starts.
+
+Prints ONE JSON line: routed tokens/s (B*K per step time), ms/step, the
+dense keep=100% step time and speedup, peak memory of both modes, the roofline
+of the dominant kernel (HIP-event timing inside the timed region), and the CPU
+oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_FLOPS = 2.5e15      # MI355X dense bf16 MFMA
+PEAK_HBM_BYTES = 8.0e12       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class Step:
+    """Device buffers and the launch sequence of one routed (or dense) step."""
+
+    def __init__(self, w, dense: bool, seed: int = 42):
+        import torch
+        from paper_2607_02829_amd import abi, device, inputs
+        self.abi, self.w, self.dense = abi, w, dense
+        self.cfg = device.config_for(w)
+        self.K = w.L if dense else w.K
+        self.S = self.K
+        self.seed = seed
+        x = inputs.to_storage(inputs.token_field(w, 0), w.dtype)
+        self.x = device.to_device(x)
+        self.g = device.to_device(inputs.to_storage(inputs.upstream_grad(w), w.dtype))
+        self.params = device.DeviceParams(inputs.params_to_storage(inputs.block_params(w), w.dtype), w.kind)
+        self.cond = device.to_device(inputs.to_storage(inputs.cond_vector(w), w.dtype)) if w.kind == "adaln" else None
+        self.dcond = torch.empty((w.B, w.D), dtype=torch.float32, device="cuda") if w.kind == "adaln" else None
+        self.grads = device.DeviceGrads(w, w.n_blocks)
+        self.saved, self.scratch = device.workspace(self.cfg, self.S)
+        self.sel = abi.SR_SEL_TOPK_DIFFNORM if w.select == "topk" else abi.SR_SEL_RANDOM
+        if self.sel == abi.SR_SEL_TOPK_DIFFNORM:
+            self.x_prev = device.to_device(inputs.to_storage(inputs.token_field(w, 1), w.dtype))
+            self.sel_scratch = torch.empty(abi.sr_select_scratch_bytes(self.cfg, self.sel), dtype=torch.uint8,
+                                           device="cuda")
+        else:
+            self.x_prev = self.sel_scratch = None
+        if not dense:
+            self.idx = torch.empty((w.B, self.K), dtype=torch.int32, device="cuda")
+            self.h0 = torch.empty((w.B, self.K, w.D), dtype=self.x.dtype, device="cuda")
+            self.h = torch.empty_like(self.h0)
+            self.gh = torch.empty_like(self.h0)
+            self.dh = torch.empty_like(self.h0)
+        else:
+            self.x_out = torch.empty_like(self.x)
+            self.dx = torch.empty_like(self.x)
+
+    def run(self, step: int):
+        a, c, K, S = self.abi, self.cfg, self.K, self.S
+        p, g = self.params.array, self.grads.array
+        if self.dense:
+            a.sr_dense_blocks_fwd(c, p, self.cond, self.x, self.x_out, self.saved, self.scratch)
+            a.sr_dense_blocks_bwd(c, p, self.cond, self.saved, self.g, self.dx, g, self.dcond, self.scratch)
+            return
+        x_t = self.x if self.sel == a.SR_SEL_TOPK_DIFFNORM else None
+        a.sr_select_indices(c, K, self.sel, self.seed, step, x_t, self.x_prev, self.idx, self.sel_scratch)
+        a.sr_gather(c, K, self.x, self.idx, self.h0)
+        a.sr_sparse_blocks_fwd(c, S, p, self.cond, self.h0, self.h, self.saved, self.scratch)
+        a.sr_scatter_delta(c, K, self.x, self.h, self.h0, self.idx)
+        a.sr_gather(c, K, self.g, self.idx, self.gh)
+        a.sr_sparse_blocks_bwd(c, S, p, self.cond, self.saved, self.gh, self.dh, g, self.dcond, self.scratch)
+        a.sr_scatter_delta(c, K, self.g, self.dh, None, self.idx)
+
+
+def time_steps(st: Step, steps: int, warmup: int, start: int = 0, profile_filter: str | None = None):
+    import torch
+    for i in range(warmup):
+        st.run(start + i)
+    torch.cuda.synchronize()
+    prof = None
+    if profile_filter is not None:
+        st.abi.sr_profile_start(profile_filter)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for i in range(steps):
+        st.run(start + warmup + i)
+    ev1.record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if profile_filter is not None:
+        prof = st.abi.sr_profile_stop()
+    return (t1 - t0) * 1e3 / steps, ev0.elapsed_time(ev1) / steps, prof
+
+
+def kernel_breakdown(st: Step, step_index: int):
+    """One profiled step with every launch group bracketed by events."""
+    import torch
+    torch.cuda.synchronize()
+    st.abi.sr_profile_start("")
+    st.run(step_index)
+    torch.cuda.synchronize()
+    return st.abi.sr_profile_stop()
+
+
+def cpu_baseline(w) -> dict:
+    """Time the oracle on a bounded sample: one block forward+backward on the K routed
+    tokens of one sample plus the routing (selection, gather, scatter) of one step;
+    the step time is estimated as n_blocks x block + routing."""
+    import numpy as np
+    from oracle import block as oblk
+    from oracle import routing as orouting
+    from oracle import select as osel
+    from oracle import stack as ostack
+    from oracle.numerics import storage_to_f64
+    from paper_2607_02829_amd import inputs
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        cores = os.cpu_count() or 1
+    K = w.K
+    x = inputs.to_storage(inputs.token_field(w), w.dtype)[:1]
+    p = ostack.params_f64(inputs.params_to_storage(inputs.block_params(w, 1), w.dtype))[0]
+    t0 = time.perf_counter()
+    idx = osel.select_random(1, w.L, K, 42, 0)
+    h0 = orouting.gather(x, idx)
+    t1 = time.perf_counter()
+    out, cache = oblk.block_fwd(storage_to_f64(h0), p, w.H, 1e-6, w.kind)
+    t2 = time.perf_counter()
+    oblk.block_bwd(np.ones_like(out), p, cache)
+    t3 = time.perf_counter()
+    orouting.scatter_delta(x, h0, h0, idx)
+    t4 = time.perf_counter()
+    routing_s = (t1 - t0) + (t4 - t3)
+    step_s = w.B * (w.n_blocks * (t3 - t1) + 2 * routing_s)
+    return {"value": w.B * K / step_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": (f"fp64 oracle: 1 block fwd+bwd on {K} routed tokens of 1 sample ({t3 - t1:.1f} s) plus "
+                       f"select/gather/scatter ({routing_s:.2f} s); step = B x (n_blocks x block + 2 x routing) "
+                       f"= {step_s:.1f} s (extrapolated)")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="d025", help="tiny | b5625 | c1406 | d025 | edm")
+    ap.add_argument("--dense-steps", type=int, default=3, help="timed steps of the dense keep=100%% mode (0: skip)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="print the per-kernel breakdown to stderr")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the routed stack is built and timed on a single MI355X; "
+              "multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_02829_amd import abi, inputs
+
+    abi.lib()
+    torch.cuda.set_device(0)
+    w = inputs.WORKLOADS[args.workload]
+    log(f"workload {w.name}: B={w.B} L={w.L} K={w.K} D={w.D} H={w.H} F={w.F} blocks={w.n_blocks} {w.dtype}")
+
+    # ---------------------------------------------------------------- routed (sparse) mode
+    torch.cuda.reset_peak_memory_stats()
+    base_mem = torch.cuda.memory_allocated()
+    sp = Step(w, dense=False)
+    sp.run(0)
+    torch.cuda.synchronize()
+    sparse_peak = torch.cuda.max_memory_allocated() - base_mem
+    breakdown = kernel_breakdown(sp, 1)
+    dom = max(breakdown, key=lambda k: breakdown[k]["ms"])
+    if args.breakdown:
+        tot = sum(v["ms"] for v in breakdown.values())
+        for k, v in sorted(breakdown.items(), key=lambda kv: -kv[1]["ms"]):
+            log(f"  {k:16s} {v['launches']:5.0f} launches {v['ms']:9.3f} ms ({100 * v['ms'] / tot:5.1f}%)")
+    log(f"dominant kernel group: {dom}")
+    # timed region: K steps; HIP events bracket only the dominant kernel's launches
+    ms_step, ms_gpu, prof = time_steps(sp, args.steps, args.warmup, start=2, profile_filter=dom)
+    finite = bool(torch.isfinite(sp.x.float()).all().item() and torch.isfinite(sp.g.float()).all().item())
+    del sp
+    torch.cuda.empty_cache()
+
+    d = prof[dom]
+    per_launch_ms = d["ms"] / d["launches"]
+    per_launch_flops = d["flops"] / d["launches"]
+    per_launch_bytes = d["bytes"] / d["launches"]
+    if per_launch_flops > 0:
+        achieved, peak, unit, bound = per_launch_flops / (per_launch_ms * 1e-3), PEAK_BF16_FLOPS, "TFLOP/s", "mfma"
+        achieved_u, peak_u = achieved / 1e12, peak / 1e12
+    else:
+        achieved, peak, unit, bound = per_launch_bytes / (per_launch_ms * 1e-3), PEAK_HBM_BYTES, "GB/s", "hbm"
+        achieved_u, peak_u = achieved / 1e9, peak / 1e9
+
+    # whole-stack MFMA fraction: algorithmic block FLOPs per step over step time
+    M = w.B * w.K
+    blk_flops = 3 * w.n_blocks * (2 * M * (3 * w.D * w.D + w.D * w.D + 2 * w.D * w.F) + 4 * w.B * w.K * w.K * w.D)
+
+    # ---------------------------------------------------------------- dense keep=100% mode
+    dense = None
+    if args.dense_steps > 0:
+        torch.cuda.reset_peak_memory_stats()
+        base_mem = torch.cuda.memory_allocated()
+        dn = Step(w, dense=True)
+        dn.run(0)
+        torch.cuda.synchronize()
+        dense_peak = torch.cuda.max_memory_allocated() - base_mem
+        dms, _, _ = time_steps(dn, args.dense_steps, 1, start=1)
+        dense = {"ms_per_step": round(dms, 3), "peak_bytes": int(dense_peak)}
+        del dn
+        torch.cuda.empty_cache()
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w)
+
+    routed_tok_s = w.B * w.K / (ms_step * 1e-3)
+    out = {
+        "metric": "routed tokens/s fwd+bwd, ms/step at 0.25°-shape; speedup vs dense keep=100%",
+        "value": round(routed_tok_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded smooth Gaussian random token fields, N(0,0.02) weights)",
+        "config": {"workload": f"{w.name}: {w.Hg}x{w.Wg} token grid (L={w.L}), keep 25% (K={w.K}), B={w.B}, "
+                               f"D={w.D}, H={w.H}, F={w.F}, {w.n_blocks} {w.kind} blocks, {w.select} selection",
+                   "B": w.B, "L": w.L, "K": w.K, "D": w.D, "H": w.H, "F": w.F, "n_blocks": w.n_blocks,
+                   "parallelism": "none (1 GPU)"},
+        "gpu_ms_per_step_events": round(ms_gpu, 4),
+        "full_grid_tokens_per_s": round(w.B * w.L / (ms_step * 1e-3), 1),
+        "stack_mfma_frac": round(blk_flops / (ms_step * 1e-3) / PEAK_BF16_FLOPS, 4),
+        "dense": dense,
+        "speedup_vs_dense": round(dense["ms_per_step"] / ms_step, 3) if dense else None,
+        "peak_bytes": {"sparse": int(sparse_peak), "dense": dense["peak_bytes"] if dense else None,
+                       "ratio": round(dense["peak_bytes"] / sparse_peak, 3) if dense else None},
+        "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved_u, 2), "peak": peak_u, "unit": unit,
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "launches_timed": int(d["launches"]), "avg_launch_us": round(per_launch_ms * 1e3, 2)},
+        "cpu_baseline": cpu,
+        "outputs_finite": finite,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -190,6 +190,18 @@ SR_API sr_status sr_dense_blocks_bwd(const sr_config* cfg, const sr_block_params
 SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx,
                               int32_t* ok_dev, void* stream);
 
+/* Launch timing for measurement (not needed by the method).  After
+ * sr_profile_start, every library launch group whose name contains `name_filter`
+ * ("" or NULL = all) is bracketed by HIP events on its own stream.
+ * sr_profile_stop waits for those events, stops recording and writes one line per
+ * name: "<name> <launches> <total_ms> <algorithmic_flops> <algorithmic_bytes>\n"
+ * into `out` (NUL-terminated, truncated to out_bytes); *needed receives the full
+ * size.  Names: select_random, select_topk, gather, scatter_delta, ln_fwd, ln_bwd,
+ * gemm_<op> (qkv, o, fc1, fc2, dx_fc2, dx_fc1, dx_o, dx_qkv, dw_<op>), attn_fwd,
+ * attn_bwd, colsum, convert, mod. */
+SR_API sr_status sr_profile_start(const char* name_filter);
+SR_API sr_status sr_profile_stop(char* out, size_t out_bytes, size_t* needed);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,7 +23,8 @@ PARAM_FIELDS = ("ln1_w", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o", "ln2_w", "ln2_
 
 EXPORTS = ("sr_last_error", "sr_version", "sr_workspace_bytes", "sr_select_scratch_bytes",
            "sr_select_indices", "sr_gather", "sr_scatter_delta", "sr_sparse_blocks_fwd",
-           "sr_sparse_blocks_bwd", "sr_dense_blocks_fwd", "sr_dense_blocks_bwd", "sr_validate_indices")
+           "sr_sparse_blocks_bwd", "sr_dense_blocks_fwd", "sr_dense_blocks_bwd", "sr_validate_indices",
+           "sr_profile_start", "sr_profile_stop")
 
 
 class SrLibraryMissing(RuntimeError):
@@ -77,6 +78,8 @@ def lib(path: str = LIB_PATH):
         "sr_dense_blocks_fwd": ([CP, P, P, P, P, P, SZ, P, SZ, P], I32),
         "sr_dense_blocks_bwd": ([CP, P, P, P, SZ, P, P, P, P, P, SZ, P], I32),
         "sr_validate_indices": ([CP, I32, P, P, P], I32),
+        "sr_profile_start": ([ctypes.c_char_p], I32),
+        "sr_profile_stop": ([ctypes.c_char_p, SZ, ctypes.POINTER(SZ)], I32),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -176,3 +179,23 @@ def sr_dense_blocks_bwd(cfg, params, cond, saved, dx_out, dx_in, grads, dcond, s
 
 def sr_validate_indices(cfg, K, idx, ok_dev, stream=None):
     _check(lib().sr_validate_indices(ctypes.byref(cfg), K, _p(idx), _p(ok_dev), _stream(stream)))
+
+
+def sr_profile_start(name_filter: str = "") -> None:
+    _check(lib().sr_profile_start(name_filter.encode()))
+
+
+def sr_profile_stop() -> dict[str, dict[str, float]]:
+    """Stop recording; returns {name: {launches, ms, flops, bytes}} (totals)."""
+    buf = ctypes.create_string_buffer(1 << 20)
+    need = ctypes.c_size_t()
+    _check(lib().sr_profile_stop(buf, len(buf), ctypes.byref(need)))
+    return _parse_profile(buf.value.decode())
+
+
+def _parse_profile(text: str) -> dict[str, dict[str, float]]:
+    out = {}
+    for line in text.strip().splitlines():
+        name, n, ms, fl, by = line.split()
+        out[name] = {"launches": float(n), "ms": float(ms), "flops": float(fl), "bytes": float(by)}
+    return out

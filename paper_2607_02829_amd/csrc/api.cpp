@@ -6,6 +6,7 @@
 #include <string>
 
 #include "../../include/sr.h"
+#include "profile.h"
 #include "stack.h"
 
 namespace {
@@ -144,6 +145,7 @@ sr_status sr_select_indices(const sr_config* cfg, int32_t K, int32_t select_kind
   const int rows = cfg->idx_shared ? 1 : cfg->B;
   hipStream_t st = (hipStream_t)stream;
   if (select_kind == SR_SEL_RANDOM) {
+    sr::ProfScope ps("select_random", 0, (double)rows * K * 4, st);
     return hip_status(sr::launch_select_random(rows, cfg->L, K, seed, step, idx, st), "select_random");
   }
   SR_CHECK(select_kind == SR_SEL_TOPK_DIFFNORM, SR_EINVAL, "unknown selector %d", select_kind);
@@ -153,6 +155,7 @@ sr_status sr_select_indices(const sr_config* cfg, int32_t K, int32_t select_kind
   SR_CHECK(scratch_bytes >= (size_t)cfg->B * cfg->L * 4, SR_EWORKSPACE, "top-k scratch needs %zu bytes",
            (size_t)cfg->B * cfg->L * 4);
   const int dt = cfg->dtype == SR_BF16 ? sr::kBF16 : sr::kF32;
+  sr::ProfScope ps("select_topk", 0, (double)rows * cfg->L * cfg->D * 2 * elt_of(cfg->dtype), st);
   return hip_status(sr::launch_select_topk(dt, rows, cfg->L, cfg->D, K, x_t, x_prev, (float*)scratch, idx, st),
                     "select_topk");
 }
@@ -164,6 +167,7 @@ sr_status sr_gather(const sr_config* cfg, int32_t K, const void* x, const int32_
   SR_PTR(x, "x");
   SR_PTR(idx, "idx");
   SR_PTR(h0, "h0");
+  sr::ProfScope ps("gather", 0, 2.0 * cfg->B * K * cfg->D * elt_of(cfg->dtype) + 4.0 * cfg->B * K, (hipStream_t)stream);
   return hip_status(sr::launch_gather((int)elt_of(cfg->dtype), cfg->B, cfg->L, K, cfg->D, x, idx, h0,
                                       cfg->idx_shared, (hipStream_t)stream),
                     "gather");
@@ -179,6 +183,8 @@ sr_status sr_scatter_delta(const sr_config* cfg, int32_t K, void* x, const void*
   SR_PTR(idx, "idx");
   if (h0) SR_CHECK(aligned16(h0), SR_EALIGN, "h0 is not 16-byte aligned");
   const int dt = cfg->dtype == SR_BF16 ? sr::kBF16 : sr::kF32;
+  sr::ProfScope ps("scatter_delta", 0, (h0 ? 4.0 : 3.0) * cfg->B * K * cfg->D * elt_of(cfg->dtype) + 4.0 * cfg->B * K,
+                   (hipStream_t)stream);
   return hip_status(sr::launch_scatter_delta(dt, cfg->B, cfg->L, K, cfg->D, x, h, h0, idx, cfg->idx_shared,
                                              (hipStream_t)stream),
                     "scatter_delta");

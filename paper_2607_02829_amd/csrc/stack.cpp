@@ -18,6 +18,8 @@
 
 #include <cmath>
 
+#include "profile.h"
+
 namespace sr {
 
 namespace {
@@ -40,6 +42,12 @@ struct Carver {
     hipError_t _e = (x);                    \
     if (_e != hipSuccess) return _e;        \
   } while (0)
+
+// Algorithmic work of a launch group, for the optional event timing.
+double gemm_flops(int M, int N, int K) { return 2.0 * M * N * K; }
+double gemm_bytes(const Dims& d, int M, int N, int K, int out_elt) {
+  return ((double)M * K + (double)N * K) * d.elt + (double)M * N * out_elt;
+}
 
 GemmDesc desc(const Dims& d, const void* A, bool ak, long long lda, size_t abytes, const void* B, bool bk,
               long long ldb, size_t bbytes, int M, int N, int K) {
@@ -129,7 +137,10 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
   const bool ada = d.kind == SR_BLOCK_ADALN;
   hipError_t err = hipSuccess;
   auto run = [&]() -> hipError_t {
-    SR_TRY(launch_convert(d.dtype, h_in, kF32, sv[0].hin, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
+    {
+      ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
+      SR_TRY(launch_convert(d.dtype, h_in, kF32, sv[0].hin, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
+    }
     for (int i = 0; i < d.nb; ++i) {
       const BlockSaved& s = sv[i];
       const sr_block_params& w = p[i];
@@ -138,27 +149,40 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
                           6 * D, D);
         g.use_mfma = false;
         EpiArgs ep; ep.out_f32 = s.mod; ep.bias = w.b_ada; ep.ldo = 6 * D;
+        ProfScope ps("mod", gemm_flops(d.B, 6 * D, D), gemm_bytes(d, d.B, 6 * D, D, 4), st);
         SR_TRY(launch_gemm(g, EPI_BIAS_F32, ep, st));
       }
-      SR_TRY(launch_ln_fwd(d.dtype, s.hin, w.ln1_w, w.ln1_b, ada ? s.mod : nullptr, 0, M, S, D, d.eps, s.u1,
-                           s.mean1, s.rstd1, st));
+      {
+        ProfScope ps("ln_fwd", 0, (double)M * D * (4 + e), st);
+        SR_TRY(launch_ln_fwd(d.dtype, s.hin, w.ln1_w, w.ln1_b, ada ? s.mod : nullptr, 0, M, S, D, d.eps, s.u1,
+                             s.mean1, s.rstd1, st));
+      }
       {
         GemmDesc g = desc(d, s.u1, true, D, (size_t)M * D * e, w.w_qkv, true, D, (size_t)3 * D * D * e, M, 3 * D, D);
         EpiArgs ep; ep.out_act = s.qkv; ep.bias = w.b_qkv; ep.ldo = 3 * D;
+        ProfScope ps("gemm_qkv", gemm_flops(M, 3 * D, D), gemm_bytes(d, M, 3 * D, D, (int)e), st);
         SR_TRY(launch_gemm(g, EPI_BIAS_ACT, ep, st));
       }
-      SR_TRY(launch_attn_fwd(d.dtype, s.qkv, s.O, s.lse, d.B, S, d.H, D, st));
+      {
+        ProfScope ps("attn_fwd", 4.0 * d.B * (double)S * S * D, (double)M * D * e * 4, st);
+        SR_TRY(launch_attn_fwd(d.dtype, s.qkv, s.O, s.lse, d.B, S, d.H, D, st));
+      }
       {
         GemmDesc g = desc(d, s.O, true, D, (size_t)M * D * e, w.w_o, true, D, (size_t)D * D * e, M, D, D);
         EpiArgs ep; ep.bias = w.b_o; ep.resid = s.hin; ep.out_f32 = s.h1; ep.ldo = D; ep.S = S;
         if (ada) { ep.gate = s.mod + 2 * D; ep.gate_stride = 6 * D; ep.a_save = s.a_out; }
+        ProfScope ps("gemm_o", gemm_flops(M, D, D), gemm_bytes(d, M, D, D, 8), st);
         SR_TRY(launch_gemm(g, EPI_RESID, ep, st));
       }
-      SR_TRY(launch_ln_fwd(d.dtype, s.h1, w.ln2_w, w.ln2_b, ada ? s.mod : nullptr, 3 * D, M, S, D, d.eps, s.u2,
-                           s.mean2, s.rstd2, st));
+      {
+        ProfScope ps("ln_fwd", 0, (double)M * D * (4 + e), st);
+        SR_TRY(launch_ln_fwd(d.dtype, s.h1, w.ln2_w, w.ln2_b, ada ? s.mod : nullptr, 3 * D, M, S, D, d.eps, s.u2,
+                             s.mean2, s.rstd2, st));
+      }
       {
         GemmDesc g = desc(d, s.u2, true, D, (size_t)M * D * e, w.w_fc1, true, D, (size_t)F * D * e, M, F, D);
         EpiArgs ep; ep.bias = w.b_fc1; ep.out_act = s.z; ep.out_act2 = s.gz; ep.ldo = F;
+        ProfScope ps("gemm_fc1", gemm_flops(M, F, D), gemm_bytes(d, M, F, D, 2 * (int)e), st);
         SR_TRY(launch_gemm(g, EPI_GELU, ep, st));
       }
       {
@@ -166,6 +190,7 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
         EpiArgs ep; ep.bias = w.b_fc2; ep.resid = s.h1; ep.ldo = D; ep.S = S;
         if (i + 1 < d.nb) ep.out_f32 = sv[i + 1].hin; else ep.out_st = h_out;
         if (ada) { ep.gate = s.mod + 5 * D; ep.gate_stride = 6 * D; ep.a_save = s.m_out; }
+        ProfScope ps("gemm_fc2", gemm_flops(M, D, F), gemm_bytes(d, M, D, F, 8), st);
         SR_TRY(launch_gemm(g, EPI_RESID, ep, st));
       }
     }
@@ -181,9 +206,10 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
 namespace {
 
 // dW[N x K] = sum_m dY[m, n] X[m, k], both operands token-major ([M, N] and [M, K]).
-hipError_t weight_grad(const Dims& d, const void* dY, int N, const void* X, int K, float* out, const Scratch& sc,
-                       hipStream_t st) {
+hipError_t weight_grad(const char* name, const Dims& d, const void* dY, int N, const void* X, int K, float* out,
+                       const Scratch& sc, hipStream_t st) {
   if (!out) return hipSuccess;
+  ProfScope ps(name, gemm_flops(N, K, d.M), gemm_bytes(d, N, K, d.M, 4), st);
   const size_t e = d.elt;
   GemmDesc g = desc(d, dY, false, N, (size_t)d.M * N * e, X, false, K, (size_t)d.M * K * e, N, K, d.M);
   const int sp = dw_splits(d, N, K);
@@ -205,6 +231,7 @@ hipError_t weight_grad(const Dims& d, const void* dY, int N, const void* X, int 
 hipError_t bias_grad(const Dims& d, int xt, const void* X, const float* w, int wstride, int N, float* out,
                      const Scratch& sc, hipStream_t st) {
   if (!out) return hipSuccess;
+  ProfScope ps("colsum", 0, (double)d.M * N * (xt == kBF16 ? 2 : 4), st);
   SR_TRY(launch_colsum(xt, X, kF32, nullptr, w, wstride, d.B, d.S, N, sc.part, st));
   return launch_reduce_parts(sc.part, d.B, colsum_chunks(d.S), N, N, 1, out, 0, st);
 }
@@ -212,6 +239,7 @@ hipError_t bias_grad(const Dims& d, int xt, const void* X, const float* w, int w
 // dmod[b, off + c] = sum_s X[b,s,c] * Y[b,s,c]
 hipError_t gate_grad(const Dims& d, const float* X, const void* Y, float* dmod, int off, const Scratch& sc,
                      hipStream_t st) {
+  ProfScope ps("colsum", 0, (double)d.M * d.D * (4 + d.elt), st);
   SR_TRY(launch_colsum(kF32, X, d.dtype, Y, nullptr, 0, d.B, d.S, d.D, sc.part, st));
   return launch_reduce_parts(sc.part, d.B, colsum_chunks(d.S), d.D, d.D, 0, dmod + off, 6 * d.D, st);
 }
@@ -236,34 +264,45 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
 
   auto run = [&]() -> hipError_t {
     // g_res = fp32(dh_out); the activation copy is made per block below
-    SR_TRY(launch_convert(d.dtype, dh_out, kF32, sc.g_res, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
+    {
+      ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
+      SR_TRY(launch_convert(d.dtype, dh_out, kF32, sc.g_res, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
+    }
     for (int i = d.nb - 1; i >= 0; --i) {
       const BlockSaved& s = sv[i];
       const sr_block_params& w = p[i];
       const sr_block_grads& g = gr[i];
       // activation copy of the MLP-branch gradient (gated for adaLN)
-      SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, sc.g_act, (size_t)M * D, ada ? s.mod + 5 * D : nullptr, 6 * D,
-                            S, D, nullptr, st));
+      {
+        ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
+        SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, sc.g_act, (size_t)M * D, ada ? s.mod + 5 * D : nullptr, 6 * D,
+                              S, D, nullptr, st));
+      }
       if (ada) SR_TRY(gate_grad(d, sc.g_res, s.m_out, sc.dmod, 5 * D, sc, st));
       // FC2
-      SR_TRY(weight_grad(d, sc.g_act, D, s.gz, F, g.w_fc2, sc, st));
+      SR_TRY(weight_grad("gemm_dw_fc2", d, sc.g_act, D, s.gz, F, g.w_fc2, sc, st));
       SR_TRY(bias_grad(d, kF32, sc.g_res, ada ? s.mod + 5 * D : nullptr, 6 * D, D, g.b_fc2, sc, st));
       {
         GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
         EpiArgs ep; ep.z_in = s.z; ep.out_act = sc.dz; ep.ldo = F;
+        ProfScope ps("gemm_dx_fc2", gemm_flops(M, F, D), gemm_bytes(d, M, F, D, 2 * (int)e), st);
         SR_TRY(launch_gemm(gd, EPI_DGELU, ep, st));
       }
       // FC1
-      SR_TRY(weight_grad(d, sc.dz, F, s.u2, D, g.w_fc1, sc, st));
+      SR_TRY(weight_grad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, g.w_fc1, sc, st));
       SR_TRY(bias_grad(d, d.dtype, sc.dz, nullptr, 0, F, g.b_fc1, sc, st));
       {
         GemmDesc gd = desc(d, sc.dz, true, F, (size_t)M * F * e, w.w_fc1, false, D, (size_t)F * D * e, M, D, F);
         EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
+        ProfScope ps("gemm_dx_fc1", gemm_flops(M, D, F), gemm_bytes(d, M, D, F, 4), st);
         SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
       }
       // LN2 (residual: g_res2 = g_res + LN2^T du)
-      SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
-                           d.B, S, D, sc.g_res2, ada ? nullptr : sc.g_act, sc.lnpart, st));
+      {
+        ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
+        SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
+                             d.B, S, D, sc.g_res2, ada ? nullptr : sc.g_act, sc.lnpart, st));
+      }
       if (ada) {
         SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 0, sc.dmod + 4 * D, 6 * D, st));   // dscale2
         SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 0, sc.dmod + 3 * D, 6 * D, st));  // dshift2
@@ -275,28 +314,36 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         if (g.ln2_b) SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 1, g.ln2_b, 0, st));
       }
       // output projection
-      SR_TRY(weight_grad(d, sc.g_act, D, s.O, D, g.w_o, sc, st));
+      SR_TRY(weight_grad("gemm_dw_o", d, sc.g_act, D, s.O, D, g.w_o, sc, st));
       SR_TRY(bias_grad(d, kF32, sc.g_res2, ada ? s.mod + 2 * D : nullptr, 6 * D, D, g.b_o, sc, st));
       {
         GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_o, false, D, (size_t)D * D * e, M, D, D);
         EpiArgs ep; ep.out_act = sc.dO; ep.ldo = D;
+        ProfScope ps("gemm_dx_o", gemm_flops(M, D, D), gemm_bytes(d, M, D, D, (int)e), st);
         SR_TRY(launch_gemm(gd, EPI_ACT, ep, st));
       }
       // attention
-      SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, d.B, S, d.H, D / d.H, sc.delta, st));
-      SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, d.B, S, d.H, D, st));
+      {
+        ProfScope ps("attn_bwd", 8.0 * d.B * (double)S * S * D, (double)M * D * e * 8, st);
+        SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, d.B, S, d.H, D / d.H, sc.delta, st));
+        SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, d.B, S, d.H, D, st));
+      }
       // QKV
-      SR_TRY(weight_grad(d, sc.dqkv, 3 * D, s.u1, D, g.w_qkv, sc, st));
+      SR_TRY(weight_grad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u1, D, g.w_qkv, sc, st));
       SR_TRY(bias_grad(d, d.dtype, sc.dqkv, nullptr, 0, 3 * D, g.b_qkv, sc, st));
       {
         GemmDesc gd = desc(d, sc.dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,
                            M, D, 3 * D);
         EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
+        ProfScope ps("gemm_dx_qkv", gemm_flops(M, D, 3 * D), gemm_bytes(d, M, D, 3 * D, 4), st);
         SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
       }
       // LN1 (residual: g_res = g_res2 + LN1^T du)
-      SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2, d.B,
-                           S, D, sc.g_res, nullptr, sc.lnpart, st));
+      {
+        ProfScope ps("ln_bwd", 0, (double)M * D * 16, st);
+        SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2,
+                             d.B, S, D, sc.g_res, nullptr, sc.lnpart, st));
+      }
       if (ada) {
         SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 0, sc.dmod + D, 6 * D, st));   // dscale1
         SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 0, sc.dmod, 6 * D, st));   // dshift1
@@ -326,6 +373,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(zero_f32(g.b_ada, (size_t)6 * D, st));
       }
     }
+    ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
     return launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st);
   };
   hipError_t err = run();
