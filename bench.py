@@ -51,7 +51,7 @@ class Step:
         self.params = device.DeviceParams(inputs.params_to_storage(inputs.block_params(w), w.dtype), w.kind)
         self.cond = device.to_device(inputs.to_storage(inputs.cond_vector(w), w.dtype)) if w.kind == "adaln" else None
         self.dcond = torch.empty((w.B, w.D), dtype=torch.float32, device="cuda") if w.kind == "adaln" else None
-        self.grads = device.DeviceGrads(w, w.n_blocks)
+        self.grads = device.DeviceGrads(w, w.n_blocks, skip_unused=True)
         self.saved, self.scratch = device.workspace(self.cfg, self.S)
         self.sel = abi.SR_SEL_TOPK_DIFFNORM if w.select == "topk" else abi.SR_SEL_RANDOM
         if self.sel == abi.SR_SEL_TOPK_DIFFNORM:

@@ -22,6 +22,7 @@
 // Generic kernels (any storage type, hd in {32, 64, 128}): one thread per row,
 // online softmax over keys, fp32 throughout.
 #include "common.h"
+#include "profile.h"
 #include "sr_internal.h"
 
 namespace sr {
@@ -507,12 +508,21 @@ hipError_t launch_attn_bwd(int dtype, const void* qkv, const void* dO, const flo
   if (attn_uses_mfma(dtype, hd)) {
     dim3 g((S + QW - 1) / QW, H, B);
     const float sl2 = attn_sl2(hd), sc = 1.0f / sqrtf((float)hd);
-    hipLaunchKernelGGL(attn_bwd_dkv_mfma, g, dim3(256), 0, st, (const bf16_t*)qkv, (const bf16_t*)dO, lse, delta,
-                       (bf16_t*)dqkv, S, H, D, sl2, sc);
-    hipLaunchKernelGGL(attn_bwd_dq_mfma, g, dim3(256), 0, st, (const bf16_t*)qkv, (const bf16_t*)dO, lse, delta,
-                       (bf16_t*)dqkv, S, H, D, sl2, sc);
+    const double units = 2.0 * B * (double)S * S * D;   // one S x S x hd product over all heads
+    {
+      // algorithmic: dP, dV, dK (the recomputed scores are not counted)
+      ProfScope ps("attn_bwd_dkv", 3 * units, (double)B * S * D * 2 * 6, st);
+      hipLaunchKernelGGL(attn_bwd_dkv_mfma, g, dim3(256), 0, st, (const bf16_t*)qkv, (const bf16_t*)dO, lse, delta,
+                         (bf16_t*)dqkv, S, H, D, sl2, sc);
+    }
+    {
+      ProfScope ps("attn_bwd_dq", units, (double)B * S * D * 2 * 5, st);
+      hipLaunchKernelGGL(attn_bwd_dq_mfma, g, dim3(256), 0, st, (const bf16_t*)qkv, (const bf16_t*)dO, lse, delta,
+                         (bf16_t*)dqkv, S, H, D, sl2, sc);
+    }
     return hipGetLastError();
   }
+  ProfScope ps("attn_bwd_generic", 8.0 * B * (double)S * S * D, 0, st);
   if (dtype == kBF16)
     return bwd_simple((const bf16_t*)qkv, (const bf16_t*)dO, lse, delta, (bf16_t*)dqkv, B, S, H, D, hd, st);
   return bwd_simple((const float*)qkv, (const float*)dO, lse, delta, (float*)dqkv, B, S, H, D, hd, st);

@@ -28,6 +28,9 @@
 //   EPI_F32       out_f32[split] = v                                (dX for LN, dW partials)
 //   EPI_F32_ACC   out_f32 += v                                      (dcond over blocks)
 //   EPI_BIAS_F32  out_f32 = v + bias                                (adaLN modulation vectors)
+//   EPI_DW        dW = v, db = row sums of A (weight and bias gradients); split-K partials
+//                 are combined by the last workgroup of each tile, in split order, so the
+//                 result does not depend on which workgroup finishes last.
 #include "common.h"
 #include "sr_internal.h"
 
@@ -73,7 +76,15 @@ SR_DEV void epilogue(const EpiArgs& e, int m, int n, float v) {
 // ============================================================================ MFMA kernel
 
 constexpr int GM = 128, GN = 128, GK = 64;
-constexpr int LDSP = GK + 8;   // padded LDS row (bf16 elements)
+constexpr int STAGE = (GM + GN) * GK;   // bf16 elements of one LDS stage (A tile then B tile)
+constexpr int EPI_LD = GN + 8;          // fp32 row stride of the epilogue staging tile
+constexpr int SMEM_BYTES = GM * EPI_LD * 4 > 2 * STAGE * 2 ? GM * EPI_LD * 4 : 2 * STAGE * 2;
+
+// Operand tiles sit in LDS as rows of 64 bf16 (eight 16-byte chunks), unpadded; chunk c
+// of row r is stored at chunk position c ^ ((r ^ (r >> 3)) & 7).  With it, the 16-byte
+// fragment reads of eight consecutive rows, the k-major tile stores (eight chunks of a
+// row) and the transposed 8-byte stores (eight rows 8 apart) all hit distinct banks.
+SR_DEV int lds_off(int row, int chunk) { return row * GK + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 3); }
 
 // Register staging of one 128 x 64 operand tile.
 struct TileRegs {
@@ -94,12 +105,12 @@ SR_DEV void store_kmajor(const TileRegs& t, bf16_t* lds) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int c = threadIdx.x + 256 * i;
-    const int row = c >> 3, kc = c & 7;
-    *reinterpret_cast<i32x4*>(lds + row * LDSP + kc * 8) = t.v[i];
+    *reinterpret_cast<i32x4*>(lds + lds_off(c >> 3, c & 7)) = t.v[i];
   }
 }
 
-// r-major operand: X[k*ld + r]; thread covers 4 consecutive k x 8 consecutive r.
+// r-major operand: X[k*ld + r]; a thread covers 4 consecutive k x 8 consecutive r and
+// transposes them in registers into eight 4-element k runs.
 SR_DEV void load_rmajor(TileRegs& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
   const int rc = threadIdx.x & 15, kg = threadIdx.x >> 4;
 #pragma unroll
@@ -119,7 +130,77 @@ SR_DEV void store_rmajor(const TileRegs& t, bf16_t* lds) {
     i32x2 w;
     w[0] = (int)((uint32_t)e0[r] | ((uint32_t)e1[r] << 16));
     w[1] = (int)((uint32_t)e2[r] | ((uint32_t)e3[r] << 16));
-    *reinterpret_cast<i32x2*>(lds + (rc * 8 + r) * LDSP + kg * 4) = w;
+    *reinterpret_cast<i32x2*>(lds + lds_off(rc * 8 + r, kg >> 1) + (kg & 1) * 4) = w;
+  }
+}
+
+// Vectorised epilogue on four consecutive columns n..n+3 of row m (inputs already loaded).
+struct EpiIn {
+  f32x4 resid;
+  i32x2 z;     // four activation-type values (bf16) of the GELU pre-activation
+  f32x4 zf;    // the same for fp32 activations (unused in the MFMA path)
+};
+
+template <int EPI>
+SR_DEV void epi_load(const EpiArgs& e, int m, int n, EpiIn& in) {
+  const size_t o = (size_t)m * e.ldo + n;
+  if constexpr (EPI == EPI_RESID) in.resid = *reinterpret_cast<const f32x4*>(e.resid + o);
+  if constexpr (EPI == EPI_DGELU) in.z = *reinterpret_cast<const i32x2*>((const bf16_t*)e.z_in + o);
+  if constexpr (EPI == EPI_F32_ACC) in.resid = *reinterpret_cast<const f32x4*>(e.out_f32 + o);
+}
+
+SR_DEV i32x2 pack4(f32x4 v) {
+  i32x2 w;
+  w[0] = (int)f2bf2(v[0], v[1]);
+  w[1] = (int)f2bf2(v[2], v[3]);
+  return w;
+}
+
+template <int EPI>
+SR_DEV void epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in) {
+  const size_t o = (size_t)m * e.ldo + n;
+  f32x4 b = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (EPI == EPI_BIAS_ACT || EPI == EPI_RESID || EPI == EPI_GELU || EPI == EPI_BIAS_F32) {
+    const i32x2 bw = *reinterpret_cast<const i32x2*>((const bf16_t*)e.bias + n);
+    const bf16_t* be = reinterpret_cast<const bf16_t*>(&bw);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) b[q] = bf2f(be[q]);
+  }
+  if constexpr (EPI == EPI_BIAS_ACT) {
+    *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(v + b);
+  } else if constexpr (EPI == EPI_RESID) {
+    f32x4 t = v + b;
+    if (e.gate) {
+      *reinterpret_cast<i32x2*>((bf16_t*)e.a_save + o) = pack4(t);
+      t *= *reinterpret_cast<const f32x4*>(e.gate + (size_t)(m / e.S) * e.gate_stride + n);
+    }
+    const f32x4 r = in.resid + t;
+    if (e.out_f32) *reinterpret_cast<f32x4*>(e.out_f32 + o) = r;
+    if (e.out_st) *reinterpret_cast<i32x2*>((bf16_t*)e.out_st + o) = pack4(r);
+  } else if constexpr (EPI == EPI_GELU) {
+    const f32x4 z = v + b;
+    f32x4 gz;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) gz[q] = gelu_f(z[q]);
+    *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(z);
+    *reinterpret_cast<i32x2*>((bf16_t*)e.out_act2 + o) = pack4(gz);
+  } else if constexpr (EPI == EPI_DGELU) {
+    const bf16_t* ze = reinterpret_cast<const bf16_t*>(&in.z);
+    f32x4 d;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) d[q] = v[q] * gelu_grad_f(bf2f(ze[q]));
+    *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(d);
+  } else if constexpr (EPI == EPI_ACT) {
+    *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(v);
+  } else if constexpr (EPI == EPI_F32) {
+    *reinterpret_cast<f32x4*>(e.out_f32 + (size_t)blockIdx.z * e.split_stride + o) = v;
+  } else if constexpr (EPI == EPI_F32_ACC) {
+    *reinterpret_cast<f32x4*>(e.out_f32 + o) = in.resid + v;
+  } else if constexpr (EPI == EPI_BIAS_F32) {
+    *reinterpret_cast<f32x4*>(e.out_f32 + o) = v + b;
+  } else if constexpr (EPI == EPI_DW) {
+    float* out = gridDim.z == 1 ? e.out_f32 : e.part + (size_t)blockIdx.z * e.split_stride;
+    *reinterpret_cast<f32x4*>(out + o) = v;
   }
 }
 
@@ -127,8 +208,10 @@ template <bool AK, bool BK, int EPI, typename T, typename Ta>
 __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bm,
                                                           int M, int N, int Kd, int lda, int ldb, uint32_t a_bytes,
                                                           uint32_t b_bytes, int k_per_split, EpiArgs ep) {
-  __shared__ __attribute__((aligned(16))) bf16_t As[GM * LDSP];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[GN * LDSP];
+  // two operand stages (the next k-tile is written into one while the other is consumed);
+  // the same memory stages the fp32 result tile for the epilogue
+  __shared__ __attribute__((aligned(16))) char smem_raw[SMEM_BYTES];
+  bf16_t* smem = reinterpret_cast<bf16_t*>(smem_raw);
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int wm = wid >> 1, wn = wid & 1;
   const int m0 = blockIdx.y * GM, n0 = blockIdx.x * GN;
@@ -150,44 +233,127 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const bf16_t* __restr
     if constexpr (AK) load_kmajor(ta, ra, m0, k0, lda); else load_rmajor(ta, ra, m0, k0, lda);
     if constexpr (BK) load_kmajor(tb, rb, n0, k0, ldb); else load_rmajor(tb, rb, n0, k0, ldb);
   };
-  auto lstore = [&]() {
-    if constexpr (AK) store_kmajor(ta, As); else store_rmajor(ta, As);
-    if constexpr (BK) store_kmajor(tb, Bs); else store_rmajor(tb, Bs);
+  auto lstore = [&](int s) {
+    bf16_t* st = smem + s * STAGE;
+    if constexpr (AK) store_kmajor(ta, st); else store_rmajor(ta, st);
+    if constexpr (BK) store_kmajor(tb, st + GM * GK); else store_rmajor(tb, st + GM * GK);
   };
 
-  if (kbeg < kend) gload(kbeg);
-  for (int k0 = kbeg; k0 < kend; k0 += GK) {
-    __syncthreads();
-    lstore();
-    __syncthreads();
-    if (k0 + GK < kend) gload(k0 + GK);
+  // EPI_DW: the first column of tiles also sums its A rows (bias gradient)
+  const bool do_db = EPI == EPI_DW && ep.db_out != nullptr && blockIdx.x == 0;
+  float dbacc = 0.f;
+
+  // fragment rows of this lane: A rows wm*64 + i*32 + lane%32, B rows wn*64 + j*32 + lane%32
+  const int h = lane >> 5;
+  if (kbeg < kend) {
+    gload(kbeg);
+    lstore(0);
+  }
+  __syncthreads();
+  int it = 0;
+  for (int k0 = kbeg; k0 < kend; k0 += GK, ++it) {
+    const int cur = it & 1;
+    const bool more = k0 + GK < kend;
+    if (more) gload(k0 + GK);   // in flight while this tile is consumed
+    const bf16_t* As = smem + cur * STAGE;
+    const bf16_t* Bs = As + GM * GK;
+    if (do_db) {
+      const int row = threadIdx.x >> 1;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        i32x4 v = *reinterpret_cast<const i32x4*>(As + lds_off(row, (threadIdx.x & 1) * 4 + q));
+        const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dbacc += bf2f(e[j]);
+      }
+    }
 #pragma unroll
     for (int ks = 0; ks < GK / 16; ++ks) {
       bf16x8 a[2], b[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 64 + i * 32 + (lane & 31)) * LDSP + ks * 16 + (lane >> 5) * 8);
+        a[i] = *reinterpret_cast<const bf16x8*>(As + lds_off(wm * 64 + i * 32 + (lane & 31), 2 * ks + h));
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        b[j] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + j * 32 + (lane & 31)) * LDSP + ks * 16 + (lane >> 5) * 8);
+        b[j] = *reinterpret_cast<const bf16x8*>(Bs + lds_off(wn * 64 + j * 32 + (lane & 31), 2 * ks + h));
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
+    if (more) lstore(cur ^ 1);
+    __syncthreads();
   }
 
-  // accumulator layout: register r of a 32x32 tile holds row 8*(r/4) + 4*(lane/32) + r%4, column lane%32
+  if constexpr (EPI == EPI_DW) {
+    dbacc += __shfl_xor(dbacc, 1, 64);
+    const int dbrow = m0 + (threadIdx.x >> 1);
+    if (do_db && (threadIdx.x & 1) == 0 && dbrow < M) {
+      if (gridDim.z == 1) ep.db_out[dbrow] = dbacc;
+      else ep.dbpart[(size_t)blockIdx.z * M + dbrow] = dbacc;
+    }
+  }
+
+  // stage the fp32 tile: register r of a 32x32 MFMA tile holds row 8*(r/4) + 4*(lane/32) + r%4,
+  // column lane%32
+  float* stage = reinterpret_cast<float*>(smem_raw);
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        const int n = n0 + wn * 64 + j * 32 + (lane & 31);
-        if (m < M && n < N) epilogue<EPI, T, Ta>(ep, m, n, acc[i][j][r]);
+        const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        const int col = wn * 64 + j * 32 + (lane & 31);
+        stage[row * EPI_LD + col] = acc[i][j][r];
       }
+  __syncthreads();
+  // 128 rows x 32 four-column chunks, 16 per thread in two batches (inputs first, then outputs)
+#pragma unroll
+  for (int bch = 0; bch < 2; ++bch) {
+    EpiIn in[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int c = threadIdx.x + 256 * (bch * 8 + q);
+      const int m = m0 + (c >> 5), n = n0 + (c & 31) * 4;
+      if (m < M && n < N) epi_load<EPI>(ep, m, n, in[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int c = threadIdx.x + 256 * (bch * 8 + q);
+      const int row = c >> 5, c4 = (c & 31) * 4;
+      const int m = m0 + row, n = n0 + c4;
+      if (m < M && n < N) epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stage + row * EPI_LD + c4), in[q]);
+    }
+  }
+}
+
+// Sum of split-K partial planes, in split order: out[i] = sum_z part[z * n + i] (float4 lanes),
+// and likewise for the bias-gradient partials.
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, int splits, size_t n4,
+                                                            float* __restrict__ out, const float* __restrict__ dbpart,
+                                                            int nb, float* __restrict__ dbout) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n4) {
+    const f32x4* p = reinterpret_cast<const f32x4*>(part);
+    f32x4 s = p[i];
+    for (int z = 1; z < splits; ++z) s += p[(size_t)z * n4 + i];
+    reinterpret_cast<f32x4*>(out)[i] = s;
+  } else if (dbout && i - n4 < (size_t)nb) {
+    const size_t c = i - n4;
+    float s = dbpart[c];
+    for (int z = 1; z < splits; ++z) s += dbpart[(size_t)z * nb + c];
+    dbout[c] = s;
+  }
+}
+
+hipError_t launch_reduce_splits(const float* part, int splits, size_t n, float* out, const float* dbpart, int nb,
+                                float* dbout, hipStream_t st) {
+  const size_t n4 = n / 4;
+  const size_t total = n4 + (dbout ? nb : 0);
+  hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, part, splits, n4,
+                     out, dbpart, nb, dbout);
+  return hipGetLastError();
 }
 
 // ============================================================================ generic kernel
@@ -201,6 +367,8 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(const TA* __restrict__
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
   float acc[4][4] = {};
+  const bool do_db = EPI == EPI_DW && ep.db_out != nullptr && blockIdx.x == 0;
+  float dbacc = 0.f;
   for (int k0 = 0; k0 < Kd; k0 += 16) {
     for (int t = threadIdx.x; t < 64 * 16; t += 256) {
       const int kk = t >> 6, r = t & 63;
@@ -209,6 +377,8 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(const TA* __restrict__
       Bs[kk][r] = (n < N && k < Kd) ? to_f32<TB>(Bm[n * b_sn + k * b_sk]) : 0.f;
     }
     __syncthreads();
+    if (do_db && threadIdx.x < 64)
+      for (int kk = 0; kk < 16; ++kk) dbacc += As[kk][threadIdx.x];
 #pragma unroll
     for (int kk = 0; kk < 16; ++kk) {
       float a[4], b[4];
@@ -223,12 +393,16 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(const TA* __restrict__
     }
     __syncthreads();
   }
+  if (do_db && threadIdx.x < 64 && m0 + (int)threadIdx.x < M) ep.db_out[m0 + threadIdx.x] = dbacc;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
-      if (m < M && n < N) epilogue<EPI, T, Ta>(ep, m, n, acc[i][j]);
+      if (m < M && n < N) {
+        if constexpr (EPI == EPI_DW) ep.out_f32[(size_t)m * ep.ldo + n] = acc[i][j];
+        else epilogue<EPI, T, Ta>(ep, m, n, acc[i][j]);
+      }
     }
 }
 
@@ -283,6 +457,7 @@ hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_
     case EPI_F32: return dispatch<EPI_F32>(g, ep, st);
     case EPI_F32_ACC: return dispatch<EPI_F32_ACC>(g, ep, st);
     case EPI_BIAS_F32: return dispatch<EPI_BIAS_F32>(g, ep, st);
+    case EPI_DW: return dispatch<EPI_DW>(g, ep, st);
   }
   return hipErrorInvalidValue;
 }

@@ -129,27 +129,6 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ d
   }
 }
 
-// out[g*out_stride + c] = sum_k part[(g*nchunk + k)*stride + c] for c < width; with
-// sum_groups the groups are summed as well (out[c]).  Fixed order: deterministic.
-__global__ __launch_bounds__(256) void reduce_parts_kernel(const float* __restrict__ part, int groups, int nchunk,
-                                                           int width, long long stride, int sum_groups,
-                                                           float* __restrict__ out0, int out_stride) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  const int g = blockIdx.y;
-  if (c >= width) return;
-  if (sum_groups) {
-    if (g > 0) return;
-    float acc = 0.f;
-    for (int gg = 0; gg < groups; ++gg)
-      for (int k = 0; k < nchunk; ++k) acc += part[((size_t)gg * nchunk + k) * stride + c];
-    out0[c] = acc;
-  } else {
-    float acc = 0.f;
-    for (int k = 0; k < nchunk; ++k) acc += part[((size_t)g * nchunk + k) * stride + c];
-    out0[(size_t)g * out_stride + c] = acc;
-  }
-}
-
 // Per-sample column sums of X (or X * Y), in chunks of kColRows rows:
 // part[(b * nchunk + chunk) * N + c].  Optional per-sample column weights w[b*wstride + c].
 constexpr int kColRows = 64;
@@ -207,6 +186,37 @@ __global__ __launch_bounds__(256) void attn_delta_kernel(const Ta* __restrict__ 
   delta[((size_t)b * H + h) * S + s] = acc;
 }
 
+// Column sums of row partials, in a fixed order (deterministic):
+//   v[g][c] = sum_{r < R} part[(g*R + r) * width + c]      (sum_groups: one group of G*R rows)
+// columns c < half go to out_lo[g*out_stride + c], the rest to out_hi[g*out_stride + c - half].
+// A block covers 64 columns with 16 row phases, combined through LDS.
+__global__ __launch_bounds__(1024) void reduce_cols_kernel(const float* __restrict__ part, int R, int G, int sum_groups,
+                                                           int width, int half, float* __restrict__ out_lo,
+                                                           float* __restrict__ out_hi, int out_stride) {
+  __shared__ float red[16][65];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + tx;
+  const int g = blockIdx.y;
+  const int nrows = sum_groups ? R * G : R;
+  const size_t row0 = sum_groups ? 0 : (size_t)g * R;
+  float acc = 0.f;
+  if (c < width)
+    for (int rr = ty; rr < nrows; rr += 16) acc += part[(row0 + rr) * width + c];
+  red[ty][tx] = acc;
+  __syncthreads();
+  for (int s = 8; s >= 1; s >>= 1) {
+    if (ty < s) red[ty][tx] += red[ty + s][tx];
+    __syncthreads();
+  }
+  if (ty == 0 && c < width) {
+    if (c < half) {
+      if (out_lo) out_lo[(size_t)g * out_stride + c] = red[0][tx];
+    } else if (out_hi) {
+      out_hi[(size_t)g * out_stride + c - half] = red[0][tx];
+    }
+  }
+}
+
 // Fill with a constant (a kernel rather than a memset node, so captured graphs replay it safely).
 __global__ __launch_bounds__(256) void fill_kernel(float* __restrict__ p, size_t n, float v) {
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) p[i] = v;
@@ -243,14 +253,6 @@ hipError_t launch_ln_bwd(int dtype, const float* du, const float* x, const float
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_parts(const float* part, int groups, int nchunk, int width, long long stride, int sum_groups,
-                               float* out, int out_stride, hipStream_t st) {
-  dim3 g((width + 255) / 256, sum_groups ? 1 : groups);
-  hipLaunchKernelGGL(reduce_parts_kernel, g, dim3(256), 0, st, part, groups, nchunk, width, stride, sum_groups, out,
-                     out_stride);
-  return hipGetLastError();
-}
-
 int colsum_chunks(int S) { return (S + kColRows - 1) / kColRows; }
 
 // X type: 0 = fp32, 1 = bf16; Y likewise (Y may be null).
@@ -279,6 +281,14 @@ hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, cons
     if (to == kBF16) SR_CONV(float, bf16_t); else SR_CONV(float, float);
   }
 #undef SR_CONV
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_cols(const float* part, int R, int G, int sum_groups, int width, int half, float* out_lo,
+                              float* out_hi, int out_stride, hipStream_t st) {
+  dim3 g((width + 63) / 64, sum_groups ? 1 : G);
+  hipLaunchKernelGGL(reduce_cols_kernel, g, dim3(1024), 0, st, part, R, G, sum_groups, width, half, out_lo, out_hi,
+                     out_stride);
   return hipGetLastError();
 }
 

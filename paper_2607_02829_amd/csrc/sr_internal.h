@@ -19,6 +19,7 @@ enum {
   EPI_F32 = 5,
   EPI_F32_ACC = 6,
   EPI_BIAS_F32 = 7,
+  EPI_DW = 8,
 };
 
 struct EpiArgs {
@@ -35,6 +36,12 @@ struct EpiArgs {
   long long ldo = 0;            // row stride of the outputs
   int S = 1;                    // rows per sample (gate indexing)
   long long split_stride = 0;   // element stride between split-K partial outputs
+  // EPI_DW (weight gradient, reduction over tokens): out_f32 receives dW and db_out (optional)
+  // the row sums of A (the bias gradient); with split-K each split writes its plane of
+  // part / dbpart instead and launch_reduce_splits adds them in split order.
+  float* db_out = nullptr;
+  float* part = nullptr;
+  float* dbpart = nullptr;
 };
 
 struct GemmDesc {
@@ -66,18 +73,20 @@ int ln_bwd_chunks(int S);
 hipError_t launch_ln_bwd(int dtype, const float* du, const float* x, const float* mean, const float* rstd,
                          const void* gamma, const float* mod, int mod_off, const float* dres, int B, int S, int D,
                          float* dx, void* dx_act, float* part, hipStream_t st);
-hipError_t launch_reduce_parts(const float* part, int groups, int nchunk, int width, long long stride, int sum_groups,
-                               float* out, int out_stride, hipStream_t st);
 int colsum_chunks(int S);
 hipError_t launch_colsum(int xt, const void* X, int yt, const void* Y, const float* w, int wstride, int B, int S,
                          int N, float* part, hipStream_t st);
 hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, const float* w, int wstride, int S, int D,
                           float* y32, hipStream_t st);
+hipError_t launch_reduce_cols(const float* part, int R, int G, int sum_groups, int width, int half, float* out_lo,
+                              float* out_hi, int out_stride, hipStream_t st);
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st);
 hipError_t launch_attn_delta(int dtype, const void* dO, const void* O, int B, int S, int H, int hd, float* delta,
                              hipStream_t st);
 
 hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_t st);
+hipError_t launch_reduce_splits(const float* part, int splits, size_t n, float* out, const float* dbpart, int nb,
+                                float* dbout, hipStream_t st);
 
 bool attn_uses_mfma(int dtype, int hd);
 hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int B, int S, int H, int D,

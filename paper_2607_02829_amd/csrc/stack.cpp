@@ -113,7 +113,10 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
     const int sp = dw_splits(d, sh[0], sh[1]);
     if (sp > 1) wp = std::max(wp, (size_t)sp * sh[0] * sh[1]);
   }
-  s.wpart = c.take<float>(std::max<size_t>(wp, 1) * 4);
+  size_t wmax_out = 0;
+  for (auto& sh : shapes) wmax_out = std::max(wmax_out, (size_t)sh[0] * sh[1]);
+  s.wpart = c.take<float>((wp + wmax_out) * 4);   // split partials, then room for an unwanted dW
+  s.dbpart = c.take<float>((size_t)16 * std::max<size_t>(3 * D, F) * 4);
   const size_t wmax = std::max<size_t>(std::max<size_t>(3 * D, F), 6 * D);
   s.part = c.take<float>((size_t)d.B * colsum_chunks(d.S) * wmax * 4);
   s.lnpart = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
@@ -205,43 +208,45 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
 
 namespace {
 
-// dW[N x K] = sum_m dY[m, n] X[m, k], both operands token-major ([M, N] and [M, K]).
+// dW[N x K] = sum_m dY[m, n] X[m, k] and db[n] = sum_m dY[m, n], both operands token-major
+// ([M, N] and [M, K]).  Split-K over tokens when the output has few tiles: each split
+// writes a partial plane and one reduction adds them in split order (deterministic).
 hipError_t weight_grad(const char* name, const Dims& d, const void* dY, int N, const void* X, int K, float* out,
-                       const Scratch& sc, hipStream_t st) {
-  if (!out) return hipSuccess;
-  ProfScope ps(name, gemm_flops(N, K, d.M), gemm_bytes(d, N, K, d.M, 4), st);
+                       float* db, const Scratch& sc, hipStream_t st) {
+  if (!out && !db) return hipSuccess;
   const size_t e = d.elt;
   GemmDesc g = desc(d, dY, false, N, (size_t)d.M * N * e, X, false, K, (size_t)d.M * K * e, N, K, d.M);
+  EpiArgs ep;
+  ep.ldo = K;
+  float* dw = out ? out : sc.wpart;   // the kernel always produces dW; park an unwanted one in scratch
+  ep.out_f32 = dw;
+  ep.db_out = db;
   const int sp = dw_splits(d, N, K);
-  EpiArgs ep; ep.ldo = K;
   if (sp > 1) {
-    g.splits = sp;
     g.k_per_split = ((d.M + sp - 1) / sp + 63) / 64 * 64;
     g.splits = (d.M + g.k_per_split - 1) / g.k_per_split;
-    ep.out_f32 = sc.wpart;
+    if (!out) dw = sc.wpart + (size_t)g.splits * N * K;   // beyond the partials
+    ep.part = sc.wpart;
+    ep.dbpart = sc.dbpart;
     ep.split_stride = (long long)N * K;
-    SR_TRY(launch_gemm(g, EPI_F32, ep, st));
-    return launch_reduce_parts(sc.wpart, 1, g.splits, N * K, (long long)N * K, 0, out, 0, st);
   }
-  ep.out_f32 = out;
-  return launch_gemm(g, EPI_F32, ep, st);
+  {
+    ProfScope ps(name, gemm_flops(N, K, d.M), gemm_bytes(d, N, K, d.M, 4), st);
+    SR_TRY(launch_gemm(g, EPI_DW, ep, st));
+  }
+  if (g.splits > 1) {
+    ProfScope ps("reduce", 0, (double)(g.splits + 1) * N * K * 4, st);
+    SR_TRY(launch_reduce_splits(sc.wpart, g.splits, (size_t)N * K, dw, sc.dbpart, N, db, st));
+  }
+  return hipSuccess;
 }
 
-// out[c] = sum over all tokens of X (optionally * per-sample weight w[b*wstride + c]).
-hipError_t bias_grad(const Dims& d, int xt, const void* X, const float* w, int wstride, int N, float* out,
-                     const Scratch& sc, hipStream_t st) {
-  if (!out) return hipSuccess;
-  ProfScope ps("colsum", 0, (double)d.M * N * (xt == kBF16 ? 2 : 4), st);
-  SR_TRY(launch_colsum(xt, X, kF32, nullptr, w, wstride, d.B, d.S, N, sc.part, st));
-  return launch_reduce_parts(sc.part, d.B, colsum_chunks(d.S), N, N, 1, out, 0, st);
-}
-
-// dmod[b, off + c] = sum_s X[b,s,c] * Y[b,s,c]
+// dmod[b, off + c] = sum_s X[b,s,c] * Y[b,s,c]  (adaLN gate gradients)
 hipError_t gate_grad(const Dims& d, const float* X, const void* Y, float* dmod, int off, const Scratch& sc,
                      hipStream_t st) {
   ProfScope ps("colsum", 0, (double)d.M * d.D * (4 + d.elt), st);
   SR_TRY(launch_colsum(kF32, X, d.dtype, Y, nullptr, 0, d.B, d.S, d.D, sc.part, st));
-  return launch_reduce_parts(sc.part, d.B, colsum_chunks(d.S), d.D, d.D, 0, dmod + off, 6 * d.D, st);
+  return launch_reduce_cols(sc.part, colsum_chunks(d.S), d.B, 0, d.D, d.D, dmod + off, nullptr, 6 * d.D, st);
 }
 
 hipError_t zero_f32(float* p, size_t n, hipStream_t st) {
@@ -263,74 +268,74 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
   const int nln = ln_bwd_chunks(S);
 
   auto run = [&]() -> hipError_t {
-    // g_res = fp32(dh_out); the activation copy is made per block below
+    // g_res = fp32(dh_out) and, for pre-LN, its activation copy
     {
-      ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
-      SR_TRY(launch_convert(d.dtype, dh_out, kF32, sc.g_res, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
+      ProfScope ps("convert", 0, (double)M * D * (2 * e + 4), st);
+      SR_TRY(launch_convert(d.dtype, dh_out, d.dtype, sc.g_act, (size_t)M * D, nullptr, 0, S, D, sc.g_res, st));
     }
     for (int i = d.nb - 1; i >= 0; --i) {
       const BlockSaved& s = sv[i];
       const sr_block_params& w = p[i];
       const sr_block_grads& g = gr[i];
-      // activation copy of the MLP-branch gradient (gated for adaLN)
-      {
+      if (ada) {
+        // MLP-branch gradient dm = dh' * gate2 (activation copy) and dgate2 = sum_s dh' * m_out
         ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
-        SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, sc.g_act, (size_t)M * D, ada ? s.mod + 5 * D : nullptr, 6 * D,
-                              S, D, nullptr, st));
+        SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, sc.g_act, (size_t)M * D, s.mod + 5 * D, 6 * D, S, D, nullptr,
+                              st));
+        SR_TRY(gate_grad(d, sc.g_res, s.m_out, sc.dmod, 5 * D, sc, st));
       }
-      if (ada) SR_TRY(gate_grad(d, sc.g_res, s.m_out, sc.dmod, 5 * D, sc, st));
-      // FC2
-      SR_TRY(weight_grad("gemm_dw_fc2", d, sc.g_act, D, s.gz, F, g.w_fc2, sc, st));
-      SR_TRY(bias_grad(d, kF32, sc.g_res, ada ? s.mod + 5 * D : nullptr, 6 * D, D, g.b_fc2, sc, st));
+      // FC2: dW2, db2; dz = (dm W2) * GELU'(z)
+      SR_TRY(weight_grad("gemm_dw_fc2", d, sc.g_act, D, s.gz, F, g.w_fc2, g.b_fc2, sc, st));
       {
         GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
         EpiArgs ep; ep.z_in = s.z; ep.out_act = sc.dz; ep.ldo = F;
         ProfScope ps("gemm_dx_fc2", gemm_flops(M, F, D), gemm_bytes(d, M, F, D, 2 * (int)e), st);
         SR_TRY(launch_gemm(gd, EPI_DGELU, ep, st));
       }
-      // FC1
-      SR_TRY(weight_grad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, g.w_fc1, sc, st));
-      SR_TRY(bias_grad(d, d.dtype, sc.dz, nullptr, 0, F, g.b_fc1, sc, st));
+      // FC1: dW1, db1; du = dz W1
+      SR_TRY(weight_grad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, g.w_fc1, g.b_fc1, sc, st));
       {
         GemmDesc gd = desc(d, sc.dz, true, F, (size_t)M * F * e, w.w_fc1, false, D, (size_t)F * D * e, M, D, F);
         EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
         ProfScope ps("gemm_dx_fc1", gemm_flops(M, D, F), gemm_bytes(d, M, D, F, 4), st);
         SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
       }
-      // LN2 (residual: g_res2 = g_res + LN2^T du)
+      // LN2 backward: g_res2 = g_res + LN2^T du (pre-LN also writes the activation copy)
       {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
                              d.B, S, D, sc.g_res2, ada ? nullptr : sc.g_act, sc.lnpart, st));
       }
+      {
+        ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
+        if (ada)   // dscale2 -> dmod[4D..5D), dshift2 -> dmod[3D..4D)
+          SR_TRY(launch_reduce_cols(sc.lnpart, nln, d.B, 0, 2 * D, D, sc.dmod + 4 * D, sc.dmod + 3 * D, 6 * D, st));
+        else if (g.ln2_w || g.ln2_b)
+          SR_TRY(launch_reduce_cols(sc.lnpart, nln, d.B, 1, 2 * D, D, g.ln2_w, g.ln2_b, 0, st));
+      }
       if (ada) {
-        SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 0, sc.dmod + 4 * D, 6 * D, st));   // dscale2
-        SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 0, sc.dmod + 3 * D, 6 * D, st));  // dshift2
+        // attention-branch gradient da = dh1 * gate1 and dgate1 = sum_s dh1 * a_out
         SR_TRY(gate_grad(d, sc.g_res2, s.a_out, sc.dmod, 2 * D, sc, st));
+        ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
         SR_TRY(launch_convert(kF32, sc.g_res2, d.dtype, sc.g_act, (size_t)M * D, s.mod + 2 * D, 6 * D, S, D, nullptr,
                               st));
-      } else {
-        if (g.ln2_w) SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 1, g.ln2_w, 0, st));
-        if (g.ln2_b) SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 1, g.ln2_b, 0, st));
       }
-      // output projection
-      SR_TRY(weight_grad("gemm_dw_o", d, sc.g_act, D, s.O, D, g.w_o, sc, st));
-      SR_TRY(bias_grad(d, kF32, sc.g_res2, ada ? s.mod + 2 * D : nullptr, 6 * D, D, g.b_o, sc, st));
+      // output projection: dWo, dbo; dO = da Wo
+      SR_TRY(weight_grad("gemm_dw_o", d, sc.g_act, D, s.O, D, g.w_o, g.b_o, sc, st));
       {
         GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_o, false, D, (size_t)D * D * e, M, D, D);
         EpiArgs ep; ep.out_act = sc.dO; ep.ldo = D;
         ProfScope ps("gemm_dx_o", gemm_flops(M, D, D), gemm_bytes(d, M, D, D, (int)e), st);
         SR_TRY(launch_gemm(gd, EPI_ACT, ep, st));
       }
-      // attention
+      // attention backward
       {
-        ProfScope ps("attn_bwd", 8.0 * d.B * (double)S * S * D, (double)M * D * e * 8, st);
+        ProfScope ps("attn_bwd_delta", 0, (double)M * D * e * 2, st);
         SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, d.B, S, d.H, D / d.H, sc.delta, st));
-        SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, d.B, S, d.H, D, st));
       }
-      // QKV
-      SR_TRY(weight_grad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u1, D, g.w_qkv, sc, st));
-      SR_TRY(bias_grad(d, d.dtype, sc.dqkv, nullptr, 0, 3 * D, g.b_qkv, sc, st));
+      SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, d.B, S, d.H, D, st));
+      // QKV: dWqkv, dbqkv; du = dqkv Wqkv
+      SR_TRY(weight_grad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u1, D, g.w_qkv, g.b_qkv, sc, st));
       {
         GemmDesc gd = desc(d, sc.dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,
                            M, D, 3 * D);
@@ -338,16 +343,22 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         ProfScope ps("gemm_dx_qkv", gemm_flops(M, D, 3 * D), gemm_bytes(d, M, D, 3 * D, 4), st);
         SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
       }
-      // LN1 (residual: g_res = g_res2 + LN1^T du)
+      // LN1 backward: g_res = g_res2 + LN1^T du (pre-LN: plus the activation copy for the next block)
       {
-        ProfScope ps("ln_bwd", 0, (double)M * D * 16, st);
+        ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2,
-                             d.B, S, D, sc.g_res, nullptr, sc.lnpart, st));
+                             d.B, S, D, sc.g_res, ada ? nullptr : sc.g_act, sc.lnpart, st));
+      }
+      {
+        ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
+        if (ada)   // dscale1 -> dmod[D..2D), dshift1 -> dmod[0..D)
+          SR_TRY(launch_reduce_cols(sc.lnpart, nln, d.B, 0, 2 * D, D, sc.dmod + D, sc.dmod, 6 * D, st));
+        else if (g.ln1_w || g.ln1_b)
+          SR_TRY(launch_reduce_cols(sc.lnpart, nln, d.B, 1, 2 * D, D, g.ln1_w, g.ln1_b, 0, st));
       }
       if (ada) {
-        SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 0, sc.dmod + D, 6 * D, st));   // dscale1
-        SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 0, sc.dmod, 6 * D, st));   // dshift1
         // dW_ada = dmod^T c ; db_ada = sum_b dmod ; dcond (+)= dmod W_ada
+        ProfScope ps("mod", 0, 0, st);
         if (g.w_ada) {
           GemmDesc gd = desc(d, sc.dmod, false, 6 * D, (size_t)d.B * 6 * D * 4, cond, false, D, (size_t)d.B * D * e,
                              6 * D, D, d.B);
@@ -355,7 +366,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
           EpiArgs ep; ep.out_f32 = g.w_ada; ep.ldo = D;
           SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
         }
-        if (g.b_ada) SR_TRY(launch_reduce_parts(sc.dmod, d.B, 1, 6 * D, 6 * D, 1, g.b_ada, 0, st));
+        if (g.b_ada) SR_TRY(launch_reduce_cols(sc.dmod, d.B, 1, 1, 6 * D, 6 * D, g.b_ada, nullptr, 0, st));
         if (dcond) {
           GemmDesc gd = desc(d, sc.dmod, true, 6 * D, (size_t)d.B * 6 * D * 4, w.w_ada, false, D,
                              (size_t)6 * D * D * e, d.B, D, 6 * D);
@@ -367,8 +378,6 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(zero_f32(g.ln1_w, D, st)); SR_TRY(zero_f32(g.ln1_b, D, st));
         SR_TRY(zero_f32(g.ln2_w, D, st)); SR_TRY(zero_f32(g.ln2_b, D, st));
       } else {
-        if (g.ln1_w) SR_TRY(launch_reduce_parts(sc.lnpart, d.B, nln, D, 2 * D, 1, g.ln1_w, 0, st));
-        if (g.ln1_b) SR_TRY(launch_reduce_parts(sc.lnpart + D, d.B, nln, D, 2 * D, 1, g.ln1_b, 0, st));
         SR_TRY(zero_f32(g.w_ada, (size_t)6 * D * D, st));
         SR_TRY(zero_f32(g.b_ada, (size_t)6 * D, st));
       }

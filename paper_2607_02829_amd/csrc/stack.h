@@ -21,7 +21,7 @@ struct BlockSaved {
 };
 
 struct Scratch {
-  float *g_res, *g_res2, *du, *delta, *wpart, *part, *lnpart, *dmod;
+  float *g_res, *g_res2, *du, *delta, *wpart, *dbpart, *part, *lnpart, *dmod;
   void *g_act, *dz, *dO, *dqkv;
 };
 

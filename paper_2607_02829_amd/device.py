@@ -57,7 +57,9 @@ class DeviceParams:
 class DeviceGrads:
     """fp32 gradient buffers for n blocks plus the host array of sr_block_grads."""
 
-    def __init__(self, w, n_blocks: int, device="cuda"):
+    def __init__(self, w, n_blocks: int, device="cuda", skip_unused: bool = False):
+        """``skip_unused`` passes NULL for the gradients of parameters the block kind does not
+        read (otherwise the library fills them with zeros)."""
         import torch
         D, F = w.D, w.F
         shapes = {"ln1_w": (D,), "ln1_b": (D,), "w_qkv": (3 * D, D), "b_qkv": (3 * D,), "w_o": (D, D),
@@ -68,7 +70,8 @@ class DeviceGrads:
         self.array = (abi.SrBlockGrads * n_blocks)()
         for i, g in enumerate(self.tensors):
             for name in abi.PARAM_FIELDS:
-                setattr(self.array[i], name, g[name].data_ptr())
+                unused = (w.kind == "preln" and name in ("w_ada", "b_ada")) or (w.kind == "adaln" and name.startswith("ln"))
+                setattr(self.array[i], name, None if (skip_unused and unused) else g[name].data_ptr())
 
 
 def workspace(cfg: abi.SrConfig, S: int, device="cuda"):
