@@ -58,36 +58,43 @@ SR_DEV void zero16(f32x16& a) {
   for (int r = 0; r < 16; ++r) a[r] = 0.f;
 }
 
-// Row-major copy of a 64 x 64 tile (rows r0.., columns of one head) into LDS.
-SR_DEV void tile_rows(bf16_t* lds, const bf16_t* src, size_t ld, int r0, int S) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    const int row = c >> 3, kc = c & 7;
-    i32x4 v = {0, 0, 0, 0};
-    if (r0 + row < S) v = *reinterpret_cast<const i32x4*>(src + (size_t)(r0 + row) * ld + kc * 8);
-    *reinterpret_cast<i32x4*>(lds + row * AP + kc * 8) = v;
-  }
-}
+// A 64 x 64 tile of one head (rows r0.., head columns), moved by 256 threads: thread
+// (dg = tid % 16, rg = tid / 16) holds rows 4rg..4rg+3, columns 4dg..4dg+3 in registers, so
+// one global read can be written to LDS row-major, transposed, or both.
+struct Tile4 {
+  i32x2 v[4];
+};
 
-// Transposed copy: lds[d][row] = src[r0 + row][d].  A thread moves a 4 x 4 block.
-SR_DEV void tile_cols(bf16_t* lds, const bf16_t* src, size_t ld, int r0, int S) {
+SR_DEV void t4_load(Tile4& t, const bf16_t* src, size_t ld, int r0, int S) {
   const int dg = threadIdx.x & 15, rg = threadIdx.x >> 4;
-  uint16_t e[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = r0 + rg * 4 + i;
     i32x2 v = {0, 0};
     if (row < S) v = *reinterpret_cast<const i32x2*>(src + (size_t)row * ld + dg * 4);
-    const uint16_t* pv = reinterpret_cast<const uint16_t*>(&v);
-#pragma unroll
-    for (int c = 0; c < 4; ++c) e[i][c] = pv[c];
+    t.v[i] = v;
   }
+}
+
+// lds[row][d]
+SR_DEV void t4_rows(const Tile4& t, bf16_t* lds) {
+  const int dg = threadIdx.x & 15, rg = threadIdx.x >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<i32x2*>(lds + (rg * 4 + i) * AP + dg * 4) = t.v[i];
+}
+
+// lds[d][row]
+SR_DEV void t4_cols(const Tile4& t, bf16_t* lds) {
+  const int dg = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&t.v[0]);
+  const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&t.v[1]);
+  const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&t.v[2]);
+  const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&t.v[3]);
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     i32x2 w;
-    w[0] = (int)((uint32_t)e[0][c] | ((uint32_t)e[1][c] << 16));
-    w[1] = (int)((uint32_t)e[2][c] | ((uint32_t)e[3][c] << 16));
+    w[0] = (int)((uint32_t)e0[c] | ((uint32_t)e1[c] << 16));
+    w[1] = (int)((uint32_t)e2[c] | ((uint32_t)e3[c] << 16));
     *reinterpret_cast<i32x2*>(lds + (dg * 4 + c) * AP + rg * 4) = w;
   }
 }
@@ -117,13 +124,16 @@ SR_DEV void unstage(const bf16_t* stage, bf16_t* dst, size_t ld, int r0, int S) 
   }
 }
 
+// All three MFMA kernels stream 64-row tiles through two LDS stages: while tile t is
+// consumed from one stage, tile t+1 is already in flight from global memory into
+// registers and is written into the other stage afterwards (one barrier per tile).
+
 // ------------------------------------------------------------------------------ forward
 
-__global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ O,
+__global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ O,
                                                      float* __restrict__ lse, int S, int H, int D, float sl2) {
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * KT * AP];
-  bf16_t* Ks = smem;             // [key][d]
-  bf16_t* Vt = smem + KT * AP;   // [d][key]
+  constexpr int ST = 2 * KT * AP;   // one stage: Ks [key][d], Vt [d][key]
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * ST];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
   const size_t ld = 3 * (size_t)D;
@@ -132,20 +142,32 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16_t* __restrict__ 
   const bf16_t* kp = base + D + hh * HD;
   const bf16_t* vp = base + 2 * D + hh * HD;
   const int myq = blockIdx.x * QW + wid * 32 + l32;
+  const int ntiles = (S + KT - 1) / KT;
 
   bf16x8 qf[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) qf[ks] = myq < S ? ld8(qp + (size_t)myq * ld + ks * 16 + 8 * h32) : zero8();
 
+  Tile4 kr, vr;
+  t4_load(kr, kp, ld, 0, S);
+  t4_load(vr, vp, ld, 0, S);
+  t4_rows(kr, smem);
+  t4_cols(vr, smem + KT * AP);
+  __syncthreads();
+
   f32x16 o[2];
   zero16(o[0]); zero16(o[1]);
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;   // running max of the raw scores, partial sum
 
-  for (int k0 = 0; k0 < S; k0 += KT) {
-    __syncthreads();
-    tile_rows(Ks, kp, ld, k0, S);
-    tile_cols(Vt, vp, ld, k0, S);
-    __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = t * KT;
+    const bool more = t + 1 < ntiles;
+    if (more) {
+      t4_load(kr, kp, ld, k0 + KT, S);
+      t4_load(vr, vp, ld, k0 + KT, S);
+    }
+    const bf16_t* Ks = smem + (t & 1) * ST;
+    const bf16_t* Vt = Ks + KT * AP;
     f32x16 s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -153,35 +175,40 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16_t* __restrict__ 
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) s[kb] = mfma(ld8(Ks + (kb * 32 + l32) * AP + ks * 16 + 8 * h32), qf[ks], s[kb]);
     }
+    if (k0 + KT > S) {   // ragged last tile: keys past S do not exist
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3) >= S) s[kb][r] = -INFINITY;
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3);
-        const float t = key < S ? s[kb][r] * sl2 : -INFINITY;
-        s[kb][r] = t;
-        mx = fmaxf(mx, t);
-      }
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = exp2f((m_run - m_new) * sl2);
+    const float nm = -m_new * sl2;
     float psum = 0.f;
     bf16x8 pb[2][2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[kb][r] - m_new);
+        const float p = exp2f(fmaf(s[kb][r], sl2, nm));
         psum += p;
         pb[kb][r >> 3][r & 7] = (__bf16)p;
       }
     l_run = l_run * alpha + psum;
     m_run = m_new;
+    if (__ballot(alpha != 1.0f)) {
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+      for (int db = 0; db < 2; ++db)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+    }
 #pragma unroll
     for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -189,10 +216,15 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16_t* __restrict__ 
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk)
           o[db] = mfma(ld_perm(Vt + (db * 32 + l32) * AP + kb * 32 + kk * 16, h32), pb[kb][kk], o[db]);
+    if (more) {
+      bf16_t* nx = smem + ((t + 1) & 1) * ST;
+      t4_rows(kr, nx);
+      t4_cols(vr, nx + KT * AP);
+    }
+    __syncthreads();
   }
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  if (h32 == 0 && myq < S) lse[((size_t)b * H + hh) * S + myq] = m_run + log2f(l_tot);
-  __syncthreads();
+  if (h32 == 0 && myq < S) lse[((size_t)b * H + hh) * S + myq] = m_run * sl2 + log2f(l_tot);
   stage_t(smem, o, 1.0f / l_tot, wid, lane);
   __syncthreads();
   unstage(smem, O + (size_t)b * S * D + hh * HD, D, blockIdx.x * QW, S);
@@ -200,16 +232,14 @@ __global__ __launch_bounds__(256) void attn_fwd_mfma(const bf16_t* __restrict__ 
 
 // ------------------------------------------------------------------------------ backward dK, dV
 
-__global__ __launch_bounds__(256) void attn_bwd_dkv_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ dO,
+__global__ __launch_bounds__(256, 2) void attn_bwd_dkv_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ dO,
                                                          const float* __restrict__ lse, const float* __restrict__ delta,
                                                          bf16_t* __restrict__ dqkv, int S, int H, int D, float sl2,
                                                          float scale) {
-  __shared__ __attribute__((aligned(16))) bf16_t smem[4 * KT * AP];
-  __shared__ float lse_s[KT], dl_s[KT];
-  bf16_t* Qs = smem;              // [q][d]
-  bf16_t* dOs = smem + KT * AP;   // [q][d]
-  bf16_t* Qt = smem + 2 * KT * AP;   // [d][q]
-  bf16_t* dOt = smem + 3 * KT * AP;  // [d][q]
+  constexpr int STB = 4 * KT * AP;                 // bf16 per stage: Qs, dOs [q][d]; Qt, dOt [d][q]
+  constexpr int STF = 2 * KT;                      // floats per stage: lse, delta of the tile's rows
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * STB];
+  __shared__ float fsm[2 * STF];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
   const size_t ld = 3 * (size_t)D;
@@ -221,6 +251,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_mfma(const bf16_t* __restric
   const float* lse_b = lse + ((size_t)b * H + hh) * S;
   const float* dl_b = delta + ((size_t)b * H + hh) * S;
   const int mykey = blockIdx.x * QW + wid * 32 + l32;
+  const int ntiles = (S + KT - 1) / KT;
 
   bf16x8 kf[4], vf[4];
 #pragma unroll
@@ -231,18 +262,41 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_mfma(const bf16_t* __restric
   f32x16 dv[2], dk[2];
   zero16(dv[0]); zero16(dv[1]); zero16(dk[0]); zero16(dk[1]);
 
-  for (int q0 = 0; q0 < S; q0 += KT) {
-    __syncthreads();
-    tile_rows(Qs, qp, ld, q0, S);
-    tile_rows(dOs, dop, D, q0, S);
-    tile_cols(Qt, qp, ld, q0, S);
-    tile_cols(dOt, dop, D, q0, S);
+  Tile4 qr, dr;
+  float lr = INFINITY, drl = 0.f;   // this thread's row statistic (threads < 64)
+  auto fetch = [&](int q0) {
+    t4_load(qr, qp, ld, q0, S);
+    t4_load(dr, dop, D, q0, S);
     if (threadIdx.x < KT) {
       const int q = q0 + threadIdx.x;
-      lse_s[threadIdx.x] = q < S ? lse_b[q] : INFINITY;
-      dl_s[threadIdx.x] = q < S ? dl_b[q] : 0.f;
+      lr = q < S ? lse_b[q] : INFINITY;   // rows past S: P = 0
+      drl = q < S ? dl_b[q] : 0.f;
     }
-    __syncthreads();
+  };
+  auto put = [&](int s) {
+    bf16_t* st = smem + s * STB;
+    t4_rows(qr, st);
+    t4_rows(dr, st + KT * AP);
+    t4_cols(qr, st + 2 * KT * AP);
+    t4_cols(dr, st + 3 * KT * AP);
+    if (threadIdx.x < KT) {
+      fsm[s * STF + threadIdx.x] = lr;
+      fsm[s * STF + KT + threadIdx.x] = drl;
+    }
+  };
+  fetch(0);
+  put(0);
+  __syncthreads();
+
+  for (int t = 0; t < ntiles; ++t) {
+    const bool more = t + 1 < ntiles;
+    if (more) fetch((t + 1) * KT);
+    const bf16_t* Qs = smem + (t & 1) * STB;
+    const bf16_t* dOs = Qs + KT * AP;
+    const bf16_t* Qt = Qs + 2 * KT * AP;
+    const bf16_t* dOt = Qs + 3 * KT * AP;
+    const float* lse_s = fsm + (t & 1) * STF;
+    const float* dl_s = lse_s + KT;
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       f32x16 s, dp;
@@ -256,7 +310,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_mfma(const bf16_t* __restric
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int ql = qb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3);
-        const float p = exp2f(s[r] * sl2 - lse_s[ql]);
+        const float p = exp2f(fmaf(s[r], sl2, -lse_s[ql]));
         const float ds = p * (dp[r] - dl_s[ql]);
         pb[r >> 3][r & 7] = (__bf16)p;
         sb[r >> 3][r & 7] = (__bf16)ds;
@@ -269,9 +323,10 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_mfma(const bf16_t* __restric
           dk[db] = mfma(ld_perm(Qt + (db * 32 + l32) * AP + qb * 32 + kk * 16, h32), sb[kk], dk[db]);
         }
     }
+    if (more) put((t + 1) & 1);
+    __syncthreads();
   }
   bf16_t* out = dqkv + (size_t)b * S * ld;
-  __syncthreads();
   stage_t(smem, dk, scale, wid, lane);
   __syncthreads();
   unstage(smem, out + D + hh * HD, ld, blockIdx.x * QW, S);
@@ -283,14 +338,12 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_mfma(const bf16_t* __restric
 
 // ------------------------------------------------------------------------------ backward dQ
 
-__global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ dO,
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ dO,
                                                         const float* __restrict__ lse, const float* __restrict__ delta,
                                                         bf16_t* __restrict__ dqkv, int S, int H, int D, float sl2,
                                                         float scale) {
-  __shared__ __attribute__((aligned(16))) bf16_t smem[3 * KT * AP];
-  bf16_t* Ks = smem;                 // [key][d]
-  bf16_t* Vs = smem + KT * AP;       // [key][d]
-  bf16_t* Kt = smem + 2 * KT * AP;   // [d][key]
+  constexpr int ST = 3 * KT * AP;   // one stage: Ks, Vs [key][d]; Kt [d][key]
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * ST];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
   const size_t ld = 3 * (size_t)D;
@@ -300,6 +353,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16_t* __restrict
   const bf16_t* vp = base + 2 * D + hh * HD;
   const bf16_t* dop = dO + (size_t)b * S * D + hh * HD;
   const int myq = blockIdx.x * QW + wid * 32 + l32;
+  const int ntiles = (S + KT - 1) / KT;
 
   bf16x8 qf[4], df[4];
 #pragma unroll
@@ -307,17 +361,30 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16_t* __restrict
     qf[ks] = myq < S ? ld8(qp + (size_t)myq * ld + ks * 16 + 8 * h32) : zero8();
     df[ks] = myq < S ? ld8(dop + (size_t)myq * D + ks * 16 + 8 * h32) : zero8();
   }
-  const float lse_q = myq < S ? lse[((size_t)b * H + hh) * S + myq] : INFINITY;
+  const float nlse = myq < S ? -lse[((size_t)b * H + hh) * S + myq] : -INFINITY;
   const float dl_q = myq < S ? delta[((size_t)b * H + hh) * S + myq] : 0.f;
   f32x16 dq[2];
   zero16(dq[0]); zero16(dq[1]);
 
-  for (int k0 = 0; k0 < S; k0 += KT) {
-    __syncthreads();
-    tile_rows(Ks, kp, ld, k0, S);
-    tile_rows(Vs, vp, ld, k0, S);
-    tile_cols(Kt, kp, ld, k0, S);
-    __syncthreads();
+  Tile4 kr, vr;
+  t4_load(kr, kp, ld, 0, S);
+  t4_load(vr, vp, ld, 0, S);
+  t4_rows(kr, smem);
+  t4_rows(vr, smem + KT * AP);
+  t4_cols(kr, smem + 2 * KT * AP);
+  __syncthreads();
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = t * KT;
+    const bool more = t + 1 < ntiles;
+    if (more) {
+      t4_load(kr, kp, ld, k0 + KT, S);
+      t4_load(vr, vp, ld, k0 + KT, S);
+    }
+    const bf16_t* Ks = smem + (t & 1) * ST;
+    const bf16_t* Vs = Ks + KT * AP;
+    const bf16_t* Kt = Ks + 2 * KT * AP;
+    const bool ragged = k0 + KT > S;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       f32x16 s, dp;
@@ -330,8 +397,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16_t* __restrict
       bf16x8 sb[2];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int key = k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3);
-        const float p = key < S ? exp2f(s[r] * sl2 - lse_q) : 0.f;
+        float p = exp2f(fmaf(s[r], sl2, nlse));
+        if (ragged && k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3) >= S) p = 0.f;
         sb[r >> 3][r & 7] = (__bf16)(p * (dp[r] - dl_q));
       }
 #pragma unroll
@@ -340,8 +407,14 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_mfma(const bf16_t* __restrict
         for (int kk = 0; kk < 2; ++kk)
           dq[db] = mfma(ld_perm(Kt + (db * 32 + l32) * AP + kb * 32 + kk * 16, h32), sb[kk], dq[db]);
     }
+    if (more) {
+      bf16_t* nx = smem + ((t + 1) & 1) * ST;
+      t4_rows(kr, nx);
+      t4_rows(vr, nx + KT * AP);
+      t4_cols(kr, nx + 2 * KT * AP);
+    }
+    __syncthreads();
   }
-  __syncthreads();
   stage_t(smem, dq, scale, wid, lane);
   __syncthreads();
   unstage(smem, dqkv + (size_t)b * S * ld + hh * HD, ld, blockIdx.x * QW, S);

@@ -28,6 +28,7 @@
 //   EPI_F32       out_f32[split] = v                                (dX for LN, dW partials)
 //   EPI_F32_ACC   out_f32 += v                                      (dcond over blocks)
 //   EPI_BIAS_F32  out_f32 = v + bias                                (adaLN modulation vectors)
+//   EPI_DO        out_act = Ta(v); delta = per-head row sums of Ta(v) * O (attention backward)
 //   EPI_DW        dW = v, db = row sums of A (weight and bias gradients); split-K partials
 //                 are combined by the last workgroup of each tile, in split order, so the
 //                 result does not depend on which workgroup finishes last.
@@ -147,6 +148,7 @@ SR_DEV void epi_load(const EpiArgs& e, int m, int n, EpiIn& in) {
   if constexpr (EPI == EPI_RESID) in.resid = *reinterpret_cast<const f32x4*>(e.resid + o);
   if constexpr (EPI == EPI_DGELU) in.z = *reinterpret_cast<const i32x2*>((const bf16_t*)e.z_in + o);
   if constexpr (EPI == EPI_F32_ACC) in.resid = *reinterpret_cast<const f32x4*>(e.out_f32 + o);
+  if constexpr (EPI == EPI_DO) in.z = *reinterpret_cast<const i32x2*>((const bf16_t*)e.o_in + o);
 }
 
 SR_DEV i32x2 pack4(f32x4 v) {
@@ -156,8 +158,9 @@ SR_DEV i32x2 pack4(f32x4 v) {
   return w;
 }
 
+// Returns the EPI_DO partial sum of this chunk (0 otherwise).
 template <int EPI>
-SR_DEV void epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in) {
+SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in) {
   const size_t o = (size_t)m * e.ldo + n;
   f32x4 b = {0.f, 0.f, 0.f, 0.f};
   if constexpr (EPI == EPI_BIAS_ACT || EPI == EPI_RESID || EPI == EPI_GELU || EPI == EPI_BIAS_F32) {
@@ -201,7 +204,17 @@ SR_DEV void epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in) 
   } else if constexpr (EPI == EPI_DW) {
     float* out = gridDim.z == 1 ? e.out_f32 : e.part + (size_t)blockIdx.z * e.split_stride;
     *reinterpret_cast<f32x4*>(out + o) = v;
+  } else if constexpr (EPI == EPI_DO) {
+    const i32x2 w = pack4(v);
+    *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = w;
+    const bf16_t* de = reinterpret_cast<const bf16_t*>(&w);
+    const bf16_t* oe = reinterpret_cast<const bf16_t*>(&in.z);
+    float s = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s += bf2f(de[q]) * bf2f(oe[q]);
+    return s;
   }
+  return 0.f;
 }
 
 template <bool AK, bool BK, int EPI, typename T, typename Ta>
@@ -323,7 +336,15 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const bf16_t* __restr
       const int c = threadIdx.x + 256 * (bch * 8 + q);
       const int row = c >> 5, c4 = (c & 31) * 4;
       const int m = m0 + row, n = n0 + c4;
-      if (m < M && n < N) epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stage + row * EPI_LD + c4), in[q]);
+      float part = 0.f;
+      if (m < M && n < N) part = epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stage + row * EPI_LD + c4), in[q]);
+      if constexpr (EPI == EPI_DO) {
+        // the 16 lanes (tid % 16) of one head's 64 columns: butterfly within the group
+#pragma unroll
+        for (int o = 8; o >= 1; o >>= 1) part += __shfl_xor(part, o, 64);
+        if ((threadIdx.x & 15) == 0 && m < M && n < N)
+          ep.delta[((size_t)(m / ep.S) * ep.H + (n >> 6)) * ep.S + (m % ep.S)] = part;
+      }
     }
   }
 }
@@ -458,6 +479,7 @@ hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_
     case EPI_F32_ACC: return dispatch<EPI_F32_ACC>(g, ep, st);
     case EPI_BIAS_F32: return dispatch<EPI_BIAS_F32>(g, ep, st);
     case EPI_DW: return dispatch<EPI_DW>(g, ep, st);
+    case EPI_DO: return g.use_mfma ? run_mfma<EPI_DO, bf16_t, bf16_t>(g, ep, st) : hipErrorInvalidValue;
   }
   return hipErrorInvalidValue;
 }

@@ -13,41 +13,96 @@ namespace sr {
 
 constexpr int kMaxPerLane = 32;   // D <= 2048
 
+// Lane-to-column map of the row kernels: with V = 4 (D % 256 == 0) lane l owns the 16-byte
+// groups of columns 4l + 256j .. 4l + 256j + 3; with V = 1 it owns columns l + 64j.
+template <int V> SR_DEV int col_of(int lane, int j) { return (lane + 64 * j) * V; }
+
+template <int V> SR_DEV void ldv(const float* p, float* o) {
+  if constexpr (V == 4) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(p);
+    o[0] = v[0]; o[1] = v[1]; o[2] = v[2]; o[3] = v[3];
+  } else {
+    o[0] = p[0];
+  }
+}
+template <int V> SR_DEV void ldv(const bf16_t* p, float* o) {
+  if constexpr (V == 4) {
+    i32x2 w = *reinterpret_cast<const i32x2*>(p);
+    const bf16_t* e = reinterpret_cast<const bf16_t*>(&w);
+    o[0] = bf2f(e[0]); o[1] = bf2f(e[1]); o[2] = bf2f(e[2]); o[3] = bf2f(e[3]);
+  } else {
+    o[0] = bf2f(p[0]);
+  }
+}
+template <int V> SR_DEV void stv(float* p, const float* v) {
+  if constexpr (V == 4) {
+    f32x4 w = {v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<f32x4*>(p) = w;
+  } else {
+    p[0] = v[0];
+  }
+}
+template <int V> SR_DEV void stv(bf16_t* p, const float* v) {
+  if constexpr (V == 4) {
+    i32x2 w;
+    w[0] = (int)f2bf2(v[0], v[1]);
+    w[1] = (int)f2bf2(v[2], v[3]);
+    *reinterpret_cast<i32x2*>(p) = w;
+  } else {
+    p[0] = f2bf(v[0]);
+  }
+}
+
 // x: fp32 [M, D]; mod (adaLN): fp32 [B, 6D] with shift at mod_off, scale at mod_off + D.
-template <typename T, typename Ta>
+template <typename T, typename Ta, int V>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x, const T* __restrict__ gamma,
                                                      const T* __restrict__ beta, const float* __restrict__ mod,
                                                      int mod_off, int M, int S, int D, float eps,
                                                      Ta* __restrict__ y, float* __restrict__ mean_out,
                                                      float* __restrict__ rstd_out) {
+  constexpr int NJ = kMaxPerLane / V;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
-  const int n = D / 64;
+  const int n = D / (64 * V);
   const float* xr = x + (size_t)row * D;
-  float v[kMaxPerLane];
+  float v[NJ][V];
   float s = 0.f;
 #pragma unroll
-  for (int j = 0; j < kMaxPerLane; ++j)
-    if (j < n) { v[j] = xr[lane + 64 * j]; s += v[j]; }
+  for (int j = 0; j < NJ; ++j)
+    if (j < n) {
+      ldv<V>(xr + col_of<V>(lane, j), v[j]);
+#pragma unroll
+      for (int e = 0; e < V; ++e) s += v[j][e];
+    }
   const float mean = wave_sum(s) / (float)D;
   float q = 0.f;
 #pragma unroll
-  for (int j = 0; j < kMaxPerLane; ++j)
-    if (j < n) { float d = v[j] - mean; q += d * d; }
+  for (int j = 0; j < NJ; ++j)
+    if (j < n)
+#pragma unroll
+      for (int e = 0; e < V; ++e) { const float d = v[j][e] - mean; q += d * d; }
   const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
   Ta* yr = y + (size_t)row * D;
   const int b = row / S;
   const float* shift = mod ? mod + (size_t)b * 6 * D + mod_off : nullptr;
-  const float* scale = mod ? shift + D : nullptr;
 #pragma unroll
-  for (int j = 0; j < kMaxPerLane; ++j)
+  for (int j = 0; j < NJ; ++j)
     if (j < n) {
-      const int c = lane + 64 * j;
-      float xh = (v[j] - mean) * rstd;
-      float o = mod ? xh * (1.0f + scale[c]) + shift[c]
-                    : xh * to_f32<T>(gamma[c]) + to_f32<T>(beta[c]);
-      yr[c] = from_f32<Ta>(o);
+      const int c = col_of<V>(lane, j);
+      float w[V], bb[V], o[V];
+      if (mod) {
+        ldv<V>(shift + D + c, w);
+        ldv<V>(shift + c, bb);
+#pragma unroll
+        for (int e = 0; e < V; ++e) w[e] += 1.0f;
+      } else {
+        ldv<V>(gamma + c, w);
+        ldv<V>(beta + c, bb);
+      }
+#pragma unroll
+      for (int e = 0; e < V; ++e) o[e] = (v[j][e] - mean) * rstd * w[e] + bb[e];
+      stv<V>(yr + c, o);
     }
   if (lane == 0) { mean_out[row] = mean; rstd_out[row] = rstd; }
 }
@@ -55,76 +110,107 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
 // Backward.  du: fp32 [M, D] gradient of the LayerNorm output (after modulation);
 // dres: fp32 [M, D] residual gradient added to the result (may alias dx).
 // dx = dres + (dxhat - mean(dxhat) - xhat * mean(dxhat * xhat)) * rstd with
-// dxhat = du * gamma (or du * (1 + scale_b)).  Per chunk of rows (never straddling
-// a sample) it writes partial column sums of du * xhat and du to part[(b*nchunk + c) * 2D].
-constexpr int kLnBwdRows = 16;
+// dxhat = du * gamma (or du * (1 + scale_b)).  A workgroup takes kLnBwdRows rows of one
+// sample (two per wave, loaded together) and writes partial column sums of du * xhat and
+// du to part[(b*nchunk + chunk) * 2D].
+constexpr int kLnBwdRows = 8;
 
-template <typename T, typename Ta>
+template <typename T, typename Ta, int V>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ du, const float* __restrict__ x,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
                                                      const T* __restrict__ gamma, const float* __restrict__ mod,
                                                      int mod_off, const float* dres, int S, int D, float* dx,
                                                      Ta* __restrict__ dx_act, float* __restrict__ part) {
+  constexpr int NJ = kMaxPerLane / V;
+  constexpr int RPW = kLnBwdRows / 4;   // rows per wave
   __shared__ float red[4][2][kMaxPerLane * 64 / 4];   // four waves' partials, 512 columns per pass
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int b = blockIdx.y, chunk = blockIdx.x, nchunk = gridDim.x;
-  const int r0 = chunk * kLnBwdRows;
-  const int n = D / 64;
+  const int n = D / (64 * V);
   const float* scale = mod ? mod + (size_t)b * 6 * D + mod_off + D : nullptr;
-  float pg[kMaxPerLane], pb[kMaxPerLane];
+  float pg[NJ][V], pb[NJ][V], wt[NJ][V];
 #pragma unroll
-  for (int j = 0; j < kMaxPerLane; ++j) { pg[j] = 0.f; pb[j] = 0.f; }
-  for (int rr = wid; rr < kLnBwdRows; rr += 4) {
-    const int s = r0 + rr;
-    if (s >= S) break;
-    const size_t row = (size_t)b * S + s;
-    const float mu = mean[row], rs = rstd[row];
-    const float* dur = du + row * D;
-    const float* xr = x + row * D;
-    float xh[kMaxPerLane], dxh[kMaxPerLane];
-    float s1 = 0.f, s2 = 0.f;
+  for (int j = 0; j < NJ; ++j) {
+    if (j < n) {
+      const int c = col_of<V>(lane, j);
+      if (mod) {
+        ldv<V>(scale + c, wt[j]);
 #pragma unroll
-    for (int j = 0; j < kMaxPerLane; ++j)
-      if (j < n) {
-        const int c = lane + 64 * j;
-        float g = dur[c];
-        xh[j] = (xr[c] - mu) * rs;
-        float w = mod ? 1.0f + scale[c] : to_f32<T>(gamma[c]);
-        dxh[j] = g * w;
-        s1 += dxh[j];
-        s2 += dxh[j] * xh[j];
-        pg[j] += g * xh[j];
-        pb[j] += g;
+        for (int e = 0; e < V; ++e) wt[j][e] += 1.0f;
+      } else {
+        ldv<V>(gamma + c, wt[j]);
       }
-    const float m1 = wave_sum(s1) / (float)D, m2 = wave_sum(s2) / (float)D;
+    }
 #pragma unroll
-    for (int j = 0; j < kMaxPerLane; ++j)
-      if (j < n) {
-        const int c = lane + 64 * j;
-        float o = (dxh[j] - m1 - xh[j] * m2) * rs + dres[row * D + c];
-        dx[row * D + c] = o;
-        if (dx_act) dx_act[row * D + c] = from_f32<Ta>(o);
+    for (int e = 0; e < V; ++e) { pg[j][e] = 0.f; pb[j][e] = 0.f; }
+  }
+  // this wave's rows (loads of both rows are issued before any reduction)
+  float g[RPW][NJ][V], xv[RPW][NJ][V];
+  size_t rows[RPW];
+  bool ok[RPW];
+#pragma unroll
+  for (int rr = 0; rr < RPW; ++rr) {
+    const int s = chunk * kLnBwdRows + wid + 4 * rr;
+    ok[rr] = s < S;
+    rows[rr] = (size_t)b * S + (ok[rr] ? s : 0);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (j < n && ok[rr]) {
+        ldv<V>(du + rows[rr] * D + col_of<V>(lane, j), g[rr][j]);
+        ldv<V>(x + rows[rr] * D + col_of<V>(lane, j), xv[rr][j]);
       }
   }
-  // combine the four waves' partials through LDS, D/4 columns per pass
+#pragma unroll
+  for (int rr = 0; rr < RPW; ++rr) {
+    if (!ok[rr]) continue;
+    const size_t row = rows[rr];
+    const float mu = mean[row], rs = rstd[row];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (j < n)
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          const float xh = (xv[rr][j][e] - mu) * rs;
+          const float dxh = g[rr][j][e] * wt[j][e];
+          s1 += dxh;
+          s2 += dxh * xh;
+          pg[j][e] += g[rr][j][e] * xh;
+          pb[j][e] += g[rr][j][e];
+          xv[rr][j][e] = xh;
+        }
+    const float m1 = wave_sum(s1) / (float)D, m2 = wave_sum(s2) / (float)D;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (j < n) {
+        const int c = col_of<V>(lane, j);
+        float o[V];
+        ldv<V>(dres + row * D + c, o);
+#pragma unroll
+        for (int e = 0; e < V; ++e) o[e] += (g[rr][j][e] * wt[j][e] - m1 - xv[rr][j][e] * m2) * rs;
+        stv<V>(dx + row * D + c, o);
+        if (dx_act) stv<V>(dx_act + row * D + c, o);
+      }
+  }
+  // combine the four waves' partials through LDS, 512 columns per pass
   float* out = part + ((size_t)b * nchunk + chunk) * 2 * D;
-  const int cols_per_pass = 64 * kMaxPerLane / 4;   // 512
+  const int cols_per_pass = 64 * kMaxPerLane / 4;
   for (int c0 = 0; c0 < D; c0 += cols_per_pass) {
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kMaxPerLane; ++j) {
-      const int c = lane + 64 * j;
-      if (j < n && c >= c0 && c < c0 + cols_per_pass) {
-        red[wid][0][c - c0] = pg[j];
-        red[wid][1][c - c0] = pb[j];
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        const int c = col_of<V>(lane, j) + e;
+        if (j < n && c >= c0 && c < c0 + cols_per_pass) {
+          red[wid][0][c - c0] = pg[j][e];
+          red[wid][1][c - c0] = pb[j][e];
+        }
       }
-    }
     __syncthreads();
     for (int t = threadIdx.x; t < cols_per_pass && c0 + t < D; t += 256) {
-      float a = red[0][0][t] + red[1][0][t] + red[2][0][t] + red[3][0][t];
-      float bb = red[0][1][t] + red[1][1][t] + red[2][1][t] + red[3][1][t];
-      out[c0 + t] = a;
-      out[D + c0 + t] = bb;
+      out[c0 + t] = red[0][0][t] + red[1][0][t] + red[2][0][t] + red[3][0][t];
+      out[D + c0 + t] = red[0][1][t] + red[1][1][t] + red[2][1][t] + red[3][1][t];
     }
   }
 }
@@ -229,12 +315,13 @@ static inline dim3 grid1d(size_t n, int per) { return dim3((unsigned)((n + per -
 hipError_t launch_ln_fwd(int dtype, const float* x, const void* gamma, const void* beta, const float* mod,
                          int mod_off, int M, int S, int D, float eps, void* y, float* mean, float* rstd,
                          hipStream_t st) {
-  if (dtype == kBF16)
-    hipLaunchKernelGGL((ln_fwd_kernel<bf16_t, bf16_t>), grid1d(M, 4), dim3(256), 0, st, x, (const bf16_t*)gamma,
-                       (const bf16_t*)beta, mod, mod_off, M, S, D, eps, (bf16_t*)y, mean, rstd);
-  else
-    hipLaunchKernelGGL((ln_fwd_kernel<float, float>), grid1d(M, 4), dim3(256), 0, st, x, (const float*)gamma,
-                       (const float*)beta, mod, mod_off, M, S, D, eps, (float*)y, mean, rstd);
+#define SR_LNF(T, V)                                                                                            \
+  hipLaunchKernelGGL((ln_fwd_kernel<T, T, V>), grid1d(M, 4), dim3(256), 0, st, x, (const T*)gamma, (const T*)beta, \
+                     mod, mod_off, M, S, D, eps, (T*)y, mean, rstd)
+  const bool v4 = D % 256 == 0;
+  if (dtype == kBF16) { if (v4) SR_LNF(bf16_t, 4); else SR_LNF(bf16_t, 1); }
+  else { if (v4) SR_LNF(float, 4); else SR_LNF(float, 1); }
+#undef SR_LNF
   return hipGetLastError();
 }
 
@@ -244,12 +331,13 @@ hipError_t launch_ln_bwd(int dtype, const float* du, const float* x, const float
                          const void* gamma, const float* mod, int mod_off, const float* dres, int B, int S, int D,
                          float* dx, void* dx_act, float* part, hipStream_t st) {
   dim3 g(ln_bwd_chunks(S), B);
-  if (dtype == kBF16)
-    hipLaunchKernelGGL((ln_bwd_kernel<bf16_t, bf16_t>), g, dim3(256), 0, st, du, x, mean, rstd,
-                       (const bf16_t*)gamma, mod, mod_off, dres, S, D, dx, (bf16_t*)dx_act, part);
-  else
-    hipLaunchKernelGGL((ln_bwd_kernel<float, float>), g, dim3(256), 0, st, du, x, mean, rstd,
-                       (const float*)gamma, mod, mod_off, dres, S, D, dx, (float*)dx_act, part);
+#define SR_LNB(T, V)                                                                                       \
+  hipLaunchKernelGGL((ln_bwd_kernel<T, T, V>), g, dim3(256), 0, st, du, x, mean, rstd, (const T*)gamma, mod, \
+                     mod_off, dres, S, D, dx, (T*)dx_act, part)
+  const bool v4 = D % 256 == 0;
+  if (dtype == kBF16) { if (v4) SR_LNB(bf16_t, 4); else SR_LNB(bf16_t, 1); }
+  else { if (v4) SR_LNB(float, 4); else SR_LNB(float, 1); }
+#undef SR_LNB
   return hipGetLastError();
 }
 

@@ -20,6 +20,7 @@ enum {
   EPI_F32_ACC = 6,
   EPI_BIAS_F32 = 7,
   EPI_DW = 8,
+  EPI_DO = 9,   // dO store plus the attention row statistic delta (head dim 64)
 };
 
 struct EpiArgs {
@@ -42,6 +43,11 @@ struct EpiArgs {
   float* db_out = nullptr;
   float* part = nullptr;
   float* dbpart = nullptr;
+  // EPI_DO: out_act = dO; delta[(b*H + h)*S + s] = sum over head h's 64 columns of
+  // bf16(dO) * O, O read from o_in (token-major like dO)
+  const void* o_in = nullptr;
+  float* delta = nullptr;
+  int H = 1;
 };
 
 struct GemmDesc {

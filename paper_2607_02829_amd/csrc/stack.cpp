@@ -94,7 +94,7 @@ size_t layout_saved(const Dims& d, char* base, BlockSaved* out) {
 int dw_splits(const Dims& d, int N, int K) {
   if (d.dtype != kBF16) return 1;
   const int tiles = ((N + 127) / 128) * ((K + 127) / 128);
-  int s = (512 + tiles - 1) / tiles;
+  int s = (256 + tiles - 1) / tiles;
   s = std::min(s, std::max(1, d.M / 512));
   return std::max(1, std::min(s, 16));
 }
@@ -320,16 +320,19 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(launch_convert(kF32, sc.g_res2, d.dtype, sc.g_act, (size_t)M * D, s.mod + 2 * D, 6 * D, S, D, nullptr,
                               st));
       }
-      // output projection: dWo, dbo; dO = da Wo
+      // output projection: dWo, dbo; dO = da Wo (with the attention row statistic
+      // delta = rowsum(dO * O) per head in the same epilogue when the head dim is 64)
       SR_TRY(weight_grad("gemm_dw_o", d, sc.g_act, D, s.O, D, g.w_o, g.b_o, sc, st));
+      const bool fuse_delta = d.dtype == kBF16 && D / d.H == 64;
       {
         GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_o, false, D, (size_t)D * D * e, M, D, D);
         EpiArgs ep; ep.out_act = sc.dO; ep.ldo = D;
+        ep.o_in = s.O; ep.delta = sc.delta; ep.S = S; ep.H = d.H;
         ProfScope ps("gemm_dx_o", gemm_flops(M, D, D), gemm_bytes(d, M, D, D, (int)e), st);
-        SR_TRY(launch_gemm(gd, EPI_ACT, ep, st));
+        SR_TRY(launch_gemm(gd, fuse_delta ? EPI_DO : EPI_ACT, ep, st));
       }
       // attention backward
-      {
+      if (!fuse_delta) {
         ProfScope ps("attn_bwd_delta", 0, (double)M * D * e * 2, st);
         SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, d.B, S, d.H, D / d.H, sc.delta, st));
       }

@@ -21,9 +21,9 @@ def _check(w, S, n_blocks, backward=True, randomise_affine=True):
     assert not bad, bad
 
 
-@pytest.mark.parametrize("S", [50, 130])
+@pytest.mark.parametrize("S", [50, 130, 300])
 def test_preln_bf16_small(S):
-    _check(inputs.small(name="preln_bf16", Hg=10, Wg=20), S, 2)
+    _check(inputs.small(name="preln_bf16", Hg=20, Wg=20), S, 2)
 
 
 @pytest.mark.parametrize("S", [61])
