@@ -76,10 +76,8 @@ SR_DEV void epilogue(const EpiArgs& e, int m, int n, float v) {
 
 // ============================================================================ MFMA kernel
 
-constexpr int GM = 128, GN = 128, GK = 64;
-constexpr int STAGE = (GM + GN) * GK;   // bf16 elements of one LDS stage (A tile then B tile)
-constexpr int EPI_LD = GN + 8;          // fp32 row stride of the epilogue staging tile
-constexpr int SMEM_BYTES = GM * EPI_LD * 4 > 2 * STAGE * 2 ? GM * EPI_LD * 4 : 2 * STAGE * 2;
+constexpr int GN = 128, GK = 64;
+constexpr int EPI_LD = GN + 8;   // fp32 row stride of the epilogue staging tile (128 rows per pass)
 
 // Operand tiles sit in LDS as rows of 64 bf16 (eight 16-byte chunks), unpadded; chunk c
 // of row r is stored at chunk position c ^ ((r ^ (r >> 3)) & 7).  With it, the 16-byte
@@ -87,51 +85,66 @@ constexpr int SMEM_BYTES = GM * EPI_LD * 4 > 2 * STAGE * 2 ? GM * EPI_LD * 4 : 2
 // row) and the transposed 8-byte stores (eight rows 8 apart) all hit distinct banks.
 SR_DEV int lds_off(int row, int chunk) { return row * GK + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 3); }
 
-// Register staging of one 128 x 64 operand tile.
+// Register staging of one R x 64 operand tile (R/32 16-byte vectors per thread).
+template <int R>
 struct TileRegs {
-  i32x4 v[4];
+  i32x4 v[R / 32];
 };
 
 // k-major operand: rows r0.., k columns k0..k0+63 of X[r*ld + k].
-SR_DEV void load_kmajor(TileRegs& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
+template <int R>
+SR_DEV void load_kmajor(TileRegs<R>& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < R / 32; ++i) {
     const int c = threadIdx.x + 256 * i;
     const int row = c >> 3, kc = c & 7;
     const uint32_t off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + kc * 8)) * 2u;
     t.v[i] = buf_load16(rs, off);
   }
 }
-SR_DEV void store_kmajor(const TileRegs& t, bf16_t* lds) {
+template <int R>
+SR_DEV void store_kmajor(const TileRegs<R>& t, bf16_t* lds) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < R / 32; ++i) {
     const int c = threadIdx.x + 256 * i;
     *reinterpret_cast<i32x4*>(lds + lds_off(c >> 3, c & 7)) = t.v[i];
   }
 }
 
-// r-major operand: X[k*ld + r]; a thread covers 4 consecutive k x 8 consecutive r and
-// transposes them in registers into eight 4-element k runs.
-SR_DEV void load_rmajor(TileRegs& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
-  const int rc = threadIdx.x & 15, kg = threadIdx.x >> 4;
+// r-major operand: X[k*ld + r]; a task covers 4 consecutive k x 8 consecutive r and is
+// transposed in registers into eight 4-element k runs (R/128 tasks per thread).
+template <int R>
+SR_DEV void load_rmajor(TileRegs<R>& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
+  constexpr int NRC = R / 8;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t off = ((uint32_t)(k0 + kg * 4 + i) * (uint32_t)ld + (uint32_t)(r0 + rc * 8)) * 2u;
-    t.v[i] = buf_load16(rs, off);
+  for (int p = 0; p < R / 128; ++p) {
+    const int task = threadIdx.x + 256 * p;
+    const int rc = task % NRC, kg = task / NRC;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t off = ((uint32_t)(k0 + kg * 4 + i) * (uint32_t)ld + (uint32_t)(r0 + rc * 8)) * 2u;
+      t.v[p * 4 + i] = buf_load16(rs, off);
+    }
   }
 }
-SR_DEV void store_rmajor(const TileRegs& t, bf16_t* lds) {
-  const int rc = threadIdx.x & 15, kg = threadIdx.x >> 4;
-  const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&t.v[0]);
-  const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&t.v[1]);
-  const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&t.v[2]);
-  const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&t.v[3]);
+template <int R>
+SR_DEV void store_rmajor(const TileRegs<R>& t, bf16_t* lds) {
+  constexpr int NRC = R / 8;
 #pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    i32x2 w;
-    w[0] = (int)((uint32_t)e0[r] | ((uint32_t)e1[r] << 16));
-    w[1] = (int)((uint32_t)e2[r] | ((uint32_t)e3[r] << 16));
-    *reinterpret_cast<i32x2*>(lds + lds_off(rc * 8 + r, kg >> 1) + (kg & 1) * 4) = w;
+  for (int p = 0; p < R / 128; ++p) {
+    const int task = threadIdx.x + 256 * p;
+    const int rc = task % NRC, kg = task / NRC;
+    const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 0]);
+    const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 1]);
+    const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 2]);
+    const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 3]);
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      i32x2 w;
+      w[0] = (int)((uint32_t)e0[r] | ((uint32_t)e1[r] << 16));
+      w[1] = (int)((uint32_t)e2[r] | ((uint32_t)e3[r] << 16));
+      *reinterpret_cast<i32x2*>(lds + lds_off(rc * 8 + r, kg >> 1) + (kg & 1) * 4) = w;
+    }
   }
 }
 
@@ -217,47 +230,69 @@ SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in)
   return 0.f;
 }
 
-template <bool AK, bool BK, int EPI, typename T, typename Ta>
-__global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bm,
-                                                          int M, int N, int Kd, int lda, int ldb, uint32_t a_bytes,
-                                                          uint32_t b_bytes, int k_per_split, EpiArgs ep) {
+// BM x 128 workgroup tile (BM = 128 or 256), four waves in 2 x 2, each (BM/2) x 64, i.e.
+// MI x 2 MFMA tiles of 32 x 32 (MI = BM/64).  BM = 256 halves the LDS bytes read per MFMA
+// of the A operand; BM = 128 keeps two workgroups per CU and more tiles for narrow outputs.
+template <int BM, bool AK, bool BK, int EPI, typename T, typename Ta>
+__global__ __launch_bounds__(256, BM == 128 ? 2 : 1) void gemm_mfma_kernel(
+    const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bm, int M, int N, int Kd, int lda, int ldb,
+    uint32_t a_bytes, uint32_t b_bytes, int k_per_split, EpiArgs ep) {
+  constexpr int MI = BM / 64;
+  constexpr int STAGE = (BM + GN) * GK;   // bf16 elements of one LDS stage (A tile then B tile)
+  constexpr int SMEM = 128 * EPI_LD * 4 > 2 * STAGE * 2 ? 128 * EPI_LD * 4 : 2 * STAGE * 2;
   // two operand stages (the next k-tile is written into one while the other is consumed);
-  // the same memory stages the fp32 result tile for the epilogue
-  __shared__ __attribute__((aligned(16))) char smem_raw[SMEM_BYTES];
+  // the same memory stages the fp32 result, 128 rows at a time, for the epilogue
+  __shared__ __attribute__((aligned(16))) char smem_raw[SMEM];
   bf16_t* smem = reinterpret_cast<bf16_t*>(smem_raw);
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int wm = wid >> 1, wn = wid & 1;
-  const int m0 = blockIdx.y * GM, n0 = blockIdx.x * GN;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * GN;
   const int kbeg = blockIdx.z * k_per_split;
   const int kend = min(Kd, kbeg + k_per_split);
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bm, b_bytes);
 
-  f32x16 acc[2][2];
+  f32x16 acc[MI][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  TileRegs ta, tb;
+  TileRegs<BM> ta;
+  TileRegs<GN> tb;
   auto gload = [&](int k0) {
-    if constexpr (AK) load_kmajor(ta, ra, m0, k0, lda); else load_rmajor(ta, ra, m0, k0, lda);
-    if constexpr (BK) load_kmajor(tb, rb, n0, k0, ldb); else load_rmajor(tb, rb, n0, k0, ldb);
+    if constexpr (AK) load_kmajor<BM>(ta, ra, m0, k0, lda); else load_rmajor<BM>(ta, ra, m0, k0, lda);
+    if constexpr (BK) load_kmajor<GN>(tb, rb, n0, k0, ldb); else load_rmajor<GN>(tb, rb, n0, k0, ldb);
   };
   auto lstore = [&](int s) {
     bf16_t* st = smem + s * STAGE;
-    if constexpr (AK) store_kmajor(ta, st); else store_rmajor(ta, st);
-    if constexpr (BK) store_kmajor(tb, st + GM * GK); else store_rmajor(tb, st + GM * GK);
+    if constexpr (AK) store_kmajor<BM>(ta, st); else store_rmajor<BM>(ta, st);
+    if constexpr (BK) store_kmajor<GN>(tb, st + BM * GK); else store_rmajor<GN>(tb, st + BM * GK);
   };
 
   // EPI_DW: the first column of tiles also sums its A rows (bias gradient)
+  constexpr int TPR = 256 / BM;   // threads per A row for those sums
   const bool do_db = EPI == EPI_DW && ep.db_out != nullptr && blockIdx.x == 0;
   float dbacc = 0.f;
 
-  // fragment rows of this lane: A rows wm*64 + i*32 + lane%32, B rows wn*64 + j*32 + lane%32
   const int h = lane >> 5;
+  // LDS offsets of this lane's fragment rows (the stage and k-step are added per use)
+  int aoff[MI], boff[2], asw[MI], bsw[2];
+#pragma unroll
+  for (int i = 0; i < MI; ++i) {
+    const int row = wm * (BM / 2) + i * 32 + (lane & 31);
+    aoff[i] = row * GK;
+    asw[i] = (row ^ (row >> 3)) & 7;
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int row = wn * 64 + j * 32 + (lane & 31);
+    boff[j] = BM * GK + row * GK;
+    bsw[j] = (row ^ (row >> 3)) & 7;
+  }
+
   if (kbeg < kend) {
     gload(kbeg);
     lstore(0);
@@ -268,82 +303,90 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(const bf16_t* __restr
     const int cur = it & 1;
     const bool more = k0 + GK < kend;
     if (more) gload(k0 + GK);   // in flight while this tile is consumed
-    const bf16_t* As = smem + cur * STAGE;
-    const bf16_t* Bs = As + GM * GK;
+    const bf16_t* St = smem + cur * STAGE;
     if (do_db) {
-      const int row = threadIdx.x >> 1;
+      const int row = threadIdx.x / TPR;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        i32x4 v = *reinterpret_cast<const i32x4*>(As + lds_off(row, (threadIdx.x & 1) * 4 + q));
+      for (int q = 0; q < 8 / TPR; ++q) {
+        i32x4 v = *reinterpret_cast<const i32x4*>(St + lds_off(row, (threadIdx.x % TPR) * (8 / TPR) + q));
         const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
 #pragma unroll
         for (int j = 0; j < 8; ++j) dbacc += bf2f(e[j]);
       }
     }
+    // all fragments of the 64-deep tile are requested before the first MFMA, so the
+    // later k-steps' reads land while the earlier k-steps' MFMAs run
+    bf16x8 a[GK / 16][MI], b[GK / 16][2];
 #pragma unroll
     for (int ks = 0; ks < GK / 16; ++ks) {
-      bf16x8 a[2], b[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(As + lds_off(wm * 64 + i * 32 + (lane & 31), 2 * ks + h));
+      for (int i = 0; i < MI; ++i)
+        a[ks][i] = *reinterpret_cast<const bf16x8*>(St + aoff[i] + (((2 * ks + h) ^ asw[i]) << 3));
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        b[j] = *reinterpret_cast<const bf16x8*>(Bs + lds_off(wn * 64 + j * 32 + (lane & 31), 2 * ks + h));
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        b[ks][j] = *reinterpret_cast<const bf16x8*>(St + boff[j] + (((2 * ks + h) ^ bsw[j]) << 3));
     }
+#pragma unroll
+    for (int ks = 0; ks < GK / 16; ++ks)
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][i], b[ks][j], acc[i][j], 0, 0, 0);
     if (more) lstore(cur ^ 1);
     __syncthreads();
   }
 
   if constexpr (EPI == EPI_DW) {
-    dbacc += __shfl_xor(dbacc, 1, 64);
-    const int dbrow = m0 + (threadIdx.x >> 1);
-    if (do_db && (threadIdx.x & 1) == 0 && dbrow < M) {
+    if constexpr (TPR == 2) dbacc += __shfl_xor(dbacc, 1, 64);
+    const int dbrow = m0 + (int)threadIdx.x / TPR;
+    if (do_db && (threadIdx.x % TPR) == 0 && dbrow < M) {
       if (gridDim.z == 1) ep.db_out[dbrow] = dbacc;
       else ep.dbpart[(size_t)blockIdx.z * M + dbrow] = dbacc;
     }
   }
 
-  // stage the fp32 tile: register r of a 32x32 MFMA tile holds row 8*(r/4) + 4*(lane/32) + r%4,
-  // column lane%32
+  // epilogue, 128 rows per pass: stage the fp32 result (register r of a 32x32 MFMA tile
+  // holds row 8*(r/4) + 4*(lane/32) + r%4, column lane%32), then 4-column chunks per thread
   float* stage = reinterpret_cast<float*>(smem_raw);
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int half = 0; half < BM / 128; ++half) {
+    if (half) __syncthreads();
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        const int col = wn * 64 + j * 32 + (lane & 31);
-        stage[row * EPI_LD + col] = acc[i][j][r];
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * (BM / 2) + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3) - half * 128;
+          const int col = wn * 64 + j * 32 + (lane & 31);
+          if (row >= 0 && row < 128) stage[row * EPI_LD + col] = acc[i][j][r];
+        }
+    __syncthreads();
+#pragma unroll
+    for (int bch = 0; bch < 2; ++bch) {
+      EpiIn in[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int c = threadIdx.x + 256 * (bch * 8 + q);
+        const int m = m0 + half * 128 + (c >> 5), n = n0 + (c & 31) * 4;
+        if (m < M && n < N) epi_load<EPI>(ep, m, n, in[q]);
       }
-  __syncthreads();
-  // 128 rows x 32 four-column chunks, 16 per thread in two batches (inputs first, then outputs)
 #pragma unroll
-  for (int bch = 0; bch < 2; ++bch) {
-    EpiIn in[8];
+      for (int q = 0; q < 8; ++q) {
+        const int c = threadIdx.x + 256 * (bch * 8 + q);
+        const int row = c >> 5, c4 = (c & 31) * 4;
+        const int m = m0 + half * 128 + row, n = n0 + c4;
+        float part = 0.f;
+        if (m < M && n < N)
+          part = epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stage + row * EPI_LD + c4), in[q]);
+        if constexpr (EPI == EPI_DO) {
+          // the 16 lanes (tid % 16) of one head's 64 columns: butterfly within the group
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int c = threadIdx.x + 256 * (bch * 8 + q);
-      const int m = m0 + (c >> 5), n = n0 + (c & 31) * 4;
-      if (m < M && n < N) epi_load<EPI>(ep, m, n, in[q]);
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int c = threadIdx.x + 256 * (bch * 8 + q);
-      const int row = c >> 5, c4 = (c & 31) * 4;
-      const int m = m0 + row, n = n0 + c4;
-      float part = 0.f;
-      if (m < M && n < N) part = epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stage + row * EPI_LD + c4), in[q]);
-      if constexpr (EPI == EPI_DO) {
-        // the 16 lanes (tid % 16) of one head's 64 columns: butterfly within the group
-#pragma unroll
-        for (int o = 8; o >= 1; o >>= 1) part += __shfl_xor(part, o, 64);
-        if ((threadIdx.x & 15) == 0 && m < M && n < N)
-          ep.delta[((size_t)(m / ep.S) * ep.H + (n >> 6)) * ep.S + (m % ep.S)] = part;
+          for (int o = 8; o >= 1; o >>= 1) part += __shfl_xor(part, o, 64);
+          if ((threadIdx.x & 15) == 0 && m < M && n < N)
+            ep.delta[((size_t)(m / ep.S) * ep.H + (n >> 6)) * ep.S + (m % ep.S)] = part;
+        }
       }
     }
   }
@@ -429,13 +472,13 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(const TA* __restrict__
 
 // ============================================================================ dispatch
 
-template <int EPI, typename T, typename Ta>
-static hipError_t run_mfma(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
-  dim3 grid((g.N + GN - 1) / GN, (g.M + GM - 1) / GM, g.splits);
+template <int BM, int EPI, typename T, typename Ta>
+static hipError_t run_mfma_bm(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
+  dim3 grid((g.N + GN - 1) / GN, (g.M + BM - 1) / BM, g.splits);
   const int kps = g.splits > 1 ? g.k_per_split : g.K;
-#define SR_GEMM_L(AK, BK)                                                                                     \
-  hipLaunchKernelGGL((gemm_mfma_kernel<AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st, (const bf16_t*)g.A,       \
-                     (const bf16_t*)g.B, g.M, g.N, g.K, (int)g.lda, (int)g.ldb, (uint32_t)g.a_bytes,          \
+#define SR_GEMM_L(AK, BK)                                                                                         \
+  hipLaunchKernelGGL((gemm_mfma_kernel<BM, AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st, (const bf16_t*)g.A,       \
+                     (const bf16_t*)g.B, g.M, g.N, g.K, (int)g.lda, (int)g.ldb, (uint32_t)g.a_bytes,              \
                      (uint32_t)g.b_bytes, kps, ep)
   if (g.a_kmajor && g.b_kmajor) SR_GEMM_L(true, true);
   else if (g.a_kmajor && !g.b_kmajor) SR_GEMM_L(true, false);
@@ -443,6 +486,11 @@ static hipError_t run_mfma(const GemmDesc& g, const EpiArgs& ep, hipStream_t st)
   else SR_GEMM_L(false, true);
 #undef SR_GEMM_L
   return hipGetLastError();
+}
+
+template <int EPI, typename T, typename Ta>
+static hipError_t run_mfma(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
+  return run_mfma_bm<128, EPI, T, Ta>(g, ep, st);
 }
 
 template <int EPI, typename T, typename Ta, typename TA, typename TB>

@@ -94,7 +94,7 @@ size_t layout_saved(const Dims& d, char* base, BlockSaved* out) {
 int dw_splits(const Dims& d, int N, int K) {
   if (d.dtype != kBF16) return 1;
   const int tiles = ((N + 127) / 128) * ((K + 127) / 128);
-  int s = (256 + tiles - 1) / tiles;
+  int s = (512 + tiles - 1) / tiles;
   s = std::min(s, std::max(1, d.M / 512));
   return std::max(1, std::min(s, 16));
 }
