@@ -74,3 +74,14 @@ def test_zero_branches_identity():
     params = inputs.params_to_storage(inputs.block_params(w, 2, zero=("w_o", "b_o", "w_fc2", "b_fc2")), w.dtype)
     out = gpu_blocks(w, w.L, h, params, None)
     assert np.array_equal(out["h_out"], h)
+
+
+@pytest.mark.parametrize("S", [1, 2, 31, 65])
+def test_degenerate_and_sub_tile_sizes(S):
+    # S = 1 (one routed token: attention returns v), sizes below one MFMA tile and one past a
+    # 64-key tile; D = 64 with a single head is the smallest supported width
+    _check(inputs.small(name="edge", B=2, Hg=4, Wg=20, D=64, H=1, F=256), S, 2)
+
+
+def test_batch_of_one_token_grid_row():
+    _check(inputs.small(name="b1", B=1, Hg=1, Wg=300, D=128, H=2, F=512), 257, 1)

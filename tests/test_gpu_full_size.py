@@ -1,0 +1,88 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration bench.py times:
+the complete 0.25 deg routed stack (12 blocks, K = 4050) forward and backward against the
+fp64 oracle, one block at the 1.40625 deg and diffusion (adaLN) shapes, the dense
+S = 16200 block on sampled query rows, and a whole routed step at the 0.25 deg shape."""
+import numpy as np
+import pytest
+
+from gpu_helpers import compare, gpu_blocks, host_inputs, oracle_blocks, rel_err, tol_for
+from oracle import block as oblk
+from oracle import routing as orouting
+from oracle import select as osel
+from oracle import stack as ostack
+from oracle.numerics import storage_to_f64
+from paper_2607_02829_amd import abi, device, inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _check_full(w, S, n_blocks, randomise_affine=False):
+    h, params, cond, dh = host_inputs(w, n_blocks, randomise_affine=randomise_affine, S=S)
+    print(f"[{w.name}] B={w.B} S={S} blocks={n_blocks}: GPU", flush=True)
+    gpu = gpu_blocks(w, S, h, params, cond, dh)
+    print(f"[{w.name}] oracle", flush=True)
+    ref = oracle_blocks(w, h, params, cond, dh)
+    errs = compare(gpu, ref, w.dtype, w.kind)
+    worst = max(errs, key=errs.get)
+    print(f"[{w.name}] max rel err {errs[worst]:.3e} ({worst})", flush=True)
+    bad = {k: v for k, v in errs.items() if not v <= tol_for(w.dtype)}
+    assert not bad, bad
+
+
+def test_d025_full_stack_fwd_bwd():
+    w = inputs.WORKLOADS["d025"]
+    _check_full(w, w.K, w.n_blocks)
+
+
+def test_c1406_one_block():
+    w = inputs.WORKLOADS["c1406"]
+    _check_full(w, w.K, 1, randomise_affine=True)
+
+
+def test_edm_adaln_one_block():
+    w = inputs.WORKLOADS["edm"]
+    _check_full(w, w.K, 1, randomise_affine=True)
+
+
+def test_d025_dense_block_sampled_rows():
+    # keep = 100 %: one block on all L = 16200 tokens; the oracle evaluates sampled query rows
+    w = inputs.WORKLOADS["d025"]
+    h, params, cond, _ = host_inputs(w, 1, randomise_affine=True, S=w.L)
+    gpu = gpu_blocks(w, w.L, h, params, cond, None, dense=True)
+    rows = np.random.default_rng(5).choice(w.L, size=48, replace=False)
+    rows = np.sort(np.concatenate([rows, [0, w.L - 1]]))
+    p64 = ostack.params_f64(params)
+    ref, _ = oblk.block_fwd(storage_to_f64(h), p64[0], w.H, 1e-6, rows=rows)
+    got = storage_to_f64(gpu["h_out"])[:, rows]
+    err = rel_err(got, ref)
+    print(f"dense S=16200 sampled rows: max rel err {err:.3e}", flush=True)
+    assert err <= 2e-2
+
+
+def test_d025_routed_step():  # noqa: C901
+    # select -> gather -> 12 blocks -> scatter on the full token sequence
+    import torch
+    w = inputs.WORKLOADS["d025"]
+    x = inputs.to_storage(inputs.token_field(w), "bf16")
+    params = inputs.params_to_storage(inputs.block_params(w), "bf16")
+    cfg = device.config_for(w)
+    dp = device.DeviceParams(params, w.kind)
+    xd = device.to_device(x)
+    idx = torch.empty((w.B, w.K), dtype=torch.int32, device="cuda")
+    abi.sr_select_indices(cfg, w.K, abi.SR_SEL_RANDOM, 42, 7, None, None, idx)
+    h0 = torch.empty((w.B, w.K, w.D), dtype=xd.dtype, device="cuda")
+    abi.sr_gather(cfg, w.K, xd, idx, h0)
+    h = torch.empty_like(h0)
+    saved, scratch = device.workspace(cfg, w.K)
+    abi.sr_sparse_blocks_fwd(cfg, w.K, dp.array, None, h0, h, saved, scratch)
+    abi.sr_scatter_delta(cfg, w.K, xd, h, h0, idx)
+    torch.cuda.synchronize()
+    want_idx = osel.select_random(w.B, w.L, w.K, 42, 7)
+    assert np.array_equal(idx.cpu().numpy(), want_idx)
+    got_x = device.to_host(xd)
+    mask = np.ones((w.B, w.L), bool)
+    mask[0, want_idx[0]] = False
+    assert np.array_equal(got_x[mask], x[mask])                      # unselected rows untouched
+    # the scatter applied to the GPU's own h is bit-exact against the oracle's scatter of it
+    want_x = orouting.scatter_delta(x, device.to_host(h), orouting.gather(x, want_idx), want_idx)
+    assert np.array_equal(got_x, want_x)
