@@ -21,6 +21,8 @@
 //
 // Generic kernels (any storage type, hd in {32, 64, 128}): one thread per row,
 // online softmax over keys, fp32 throughout.
+#include <type_traits>
+
 #include "common.h"
 #include "profile.h"
 #include "sr_internal.h"
@@ -53,6 +55,10 @@ SR_DEV bf16x8 ld_perm(const bf16_t* p, int h) {
 
 SR_DEV f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) { return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0); }
 
+// 2^x on the hardware unit directly: the softmax arguments are <= 0 (or -inf), where the
+// unscaled instruction is accurate to ~1 ulp and flushes tiny results to zero.
+SR_DEV float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 SR_DEV void zero16(f32x16& a) {
 #pragma unroll
   for (int r = 0; r < 16; ++r) a[r] = 0.f;
@@ -65,15 +71,15 @@ struct Tile4 {
   i32x2 v[4];
 };
 
-SR_DEV void t4_load(Tile4& t, const bf16_t* src, size_t ld, int r0, int S) {
+// Rows past the sample's S tokens are read without a guard: they belong to the next
+// sample (finite values that the callers neutralise: keys get a -inf score, queries an
+// infinite LSE) or lie past the tensor, where the buffer load returns zero.
+// `base` is the byte offset of (row 0, column 0 of the head) inside the tensor of `rs`.
+SR_DEV void t4_load(Tile4& t, __amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t ld, int r0) {
   const int dg = threadIdx.x & 15, rg = threadIdx.x >> 4;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = r0 + rg * 4 + i;
-    i32x2 v = {0, 0};
-    if (row < S) v = *reinterpret_cast<const i32x2*>(src + (size_t)row * ld + dg * 4);
-    t.v[i] = v;
-  }
+  for (int i = 0; i < 4; ++i)
+    t.v[i] = buf_load8(rs, base + ((uint32_t)(r0 + rg * 4 + i) * ld + (uint32_t)dg * 4u) * 2u);
 }
 
 // lds[row][d]
@@ -139,18 +145,19 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
   const size_t ld = 3 * (size_t)D;
   const bf16_t* base = qkv + (size_t)b * S * ld;
   const bf16_t* qp = base + hh * HD;
-  const bf16_t* kp = base + D + hh * HD;
-  const bf16_t* vp = base + 2 * D + hh * HD;
   const int myq = blockIdx.x * QW + wid * 32 + l32;
   const int ntiles = (S + KT - 1) / KT;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
+  const uint32_t kbase = (uint32_t)(((size_t)b * S * ld + D + hh * HD) * 2);
+  const uint32_t vbase = kbase + (uint32_t)D * 2u;
 
   bf16x8 qf[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) qf[ks] = myq < S ? ld8(qp + (size_t)myq * ld + ks * 16 + 8 * h32) : zero8();
 
   Tile4 kr, vr;
-  t4_load(kr, kp, ld, 0, S);
-  t4_load(vr, vp, ld, 0, S);
+  t4_load(kr, rq, kbase, (uint32_t)ld, 0);
+  t4_load(vr, rq, vbase, (uint32_t)ld, 0);
   t4_rows(kr, smem);
   t4_cols(vr, smem + KT * AP);
   __syncthreads();
@@ -159,70 +166,76 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
   zero16(o[0]); zero16(o[1]);
   float m_run = -INFINITY, l_run = 0.f;   // running max of the raw scores, partial sum
 
-  for (int t = 0; t < ntiles; ++t) {
+  // one key tile: prefetch the next, consume this one from LDS, stage the next
+  auto step = [&](int t, auto ragged) {
     const int k0 = t * KT;
     const bool more = t + 1 < ntiles;
     if (more) {
-      t4_load(kr, kp, ld, k0 + KT, S);
-      t4_load(vr, vp, ld, k0 + KT, S);
+      t4_load(kr, rq, kbase, (uint32_t)ld, k0 + KT);
+      t4_load(vr, rq, vbase, (uint32_t)ld, k0 + KT);
     }
     const bf16_t* Ks = smem + (t & 1) * ST;
     const bf16_t* Vt = Ks + KT * AP;
-    f32x16 s[2];
+    {
+      f32x16 s[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      zero16(s[kb]);
+      for (int kb = 0; kb < 2; ++kb) {
+        zero16(s[kb]);
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) s[kb] = mfma(ld8(Ks + (kb * 32 + l32) * AP + ks * 16 + 8 * h32), qf[ks], s[kb]);
-    }
-    if (k0 + KT > S) {   // ragged last tile: keys past S do not exist
+        for (int ks = 0; ks < 4; ++ks) s[kb] = mfma(ld8(Ks + (kb * 32 + l32) * AP + ks * 16 + 8 * h32), qf[ks], s[kb]);
+      }
+      if constexpr (decltype(ragged)::value) {   // last tile: keys past S do not exist
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3) >= S) s[kb][r] = -INFINITY;
+      }
+      float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3) >= S) s[kb][r] = -INFINITY;
-    }
-    float mx = -INFINITY;
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = ex2((m_run - m_new) * sl2);
+      const float nm = -m_new * sl2;
+      float psum = 0.f;
+      bf16x8 pb[2][2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f((m_run - m_new) * sl2);
-    const float nm = -m_new * sl2;
-    float psum = 0.f;
-    bf16x8 pb[2][2];
+        for (int r = 0; r < 16; ++r) {
+          const float p = ex2(fmaf(s[kb][r], sl2, nm));
+          psum += p;
+          pb[kb][r >> 3][r & 7] = (__bf16)p;
+        }
+      l_run = l_run * alpha + psum;
+      m_run = m_new;
+      if (__ballot(alpha != 1.0f)) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+        for (int db = 0; db < 2; ++db)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(fmaf(s[kb][r], sl2, nm));
-        psum += p;
-        pb[kb][r >> 3][r & 7] = (__bf16)p;
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    if (__ballot(alpha != 1.0f)) {
 #pragma unroll
       for (int db = 0; db < 2; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk)
+            o[db] = mfma(ld_perm(Vt + (db * 32 + l32) * AP + kb * 32 + kk * 16, h32), pb[kb][kk], o[db]);
     }
-#pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-          o[db] = mfma(ld_perm(Vt + (db * 32 + l32) * AP + kb * 32 + kk * 16, h32), pb[kb][kk], o[db]);
     if (more) {
       bf16_t* nx = smem + ((t + 1) & 1) * ST;
       t4_rows(kr, nx);
       t4_cols(vr, nx + KT * AP);
     }
     __syncthreads();
-  }
+  };
+  // full tiles, then the ragged last tile (masking only there)
+  for (int t = 0; t < S / KT; ++t) step(t, std::false_type{});
+  if (S % KT) step(S / KT, std::true_type{});
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   if (h32 == 0 && myq < S) lse[((size_t)b * H + hh) * S + myq] = m_run * sl2 + log2f(l_tot);
   stage_t(smem, o, 1.0f / l_tot, wid, lane);
@@ -264,9 +277,13 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkv_mfma(const bf16_t* __rest
 
   Tile4 qr, dr;
   float lr = INFINITY, drl = 0.f;   // this thread's row statistic (threads < 64)
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
+  const __amdgpu_buffer_rsrc_t rd = make_rsrc(dO, (uint32_t)((size_t)gridDim.z * S * D * 2));
+  const uint32_t qbase = (uint32_t)(((size_t)b * S * ld + hh * HD) * 2);
+  const uint32_t dbase = (uint32_t)(((size_t)b * S * D + hh * HD) * 2);
   auto fetch = [&](int q0) {
-    t4_load(qr, qp, ld, q0, S);
-    t4_load(dr, dop, D, q0, S);
+    t4_load(qr, rq, qbase, (uint32_t)ld, q0);
+    t4_load(dr, rd, dbase, (uint32_t)D, q0);
     if (threadIdx.x < KT) {
       const int q = q0 + threadIdx.x;
       lr = q < S ? lse_b[q] : INFINITY;   // rows past S: P = 0
@@ -310,7 +327,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkv_mfma(const bf16_t* __rest
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int ql = qb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3);
-        const float p = exp2f(fmaf(s[r], sl2, -lse_s[ql]));
+        const float p = ex2(fmaf(s[r], sl2, -lse_s[ql]));
         const float ds = p * (dp[r] - dl_s[ql]);
         pb[r >> 3][r & 7] = (__bf16)p;
         sb[r >> 3][r & 7] = (__bf16)ds;
@@ -366,9 +383,12 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
   f32x16 dq[2];
   zero16(dq[0]); zero16(dq[1]);
 
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
+  const uint32_t kbase = (uint32_t)(((size_t)b * S * ld + D + hh * HD) * 2);
+  const uint32_t vbase = kbase + (uint32_t)D * 2u;
   Tile4 kr, vr;
-  t4_load(kr, kp, ld, 0, S);
-  t4_load(vr, vp, ld, 0, S);
+  t4_load(kr, rq, kbase, (uint32_t)ld, 0);
+  t4_load(vr, rq, vbase, (uint32_t)ld, 0);
   t4_rows(kr, smem);
   t4_rows(vr, smem + KT * AP);
   t4_cols(kr, smem + 2 * KT * AP);
@@ -378,8 +398,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
     const int k0 = t * KT;
     const bool more = t + 1 < ntiles;
     if (more) {
-      t4_load(kr, kp, ld, k0 + KT, S);
-      t4_load(vr, vp, ld, k0 + KT, S);
+      t4_load(kr, rq, kbase, (uint32_t)ld, k0 + KT);
+      t4_load(vr, rq, vbase, (uint32_t)ld, k0 + KT);
     }
     const bf16_t* Ks = smem + (t & 1) * ST;
     const bf16_t* Vs = Ks + KT * AP;
@@ -394,11 +414,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
         s = mfma(ld8(Ks + (kb * 32 + l32) * AP + ks * 16 + 8 * h32), qf[ks], s);
         dp = mfma(ld8(Vs + (kb * 32 + l32) * AP + ks * 16 + 8 * h32), df[ks], dp);
       }
+      if (ragged) {   // last tile: keys past S do not exist
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3) >= S) s[r] = -INFINITY;
+      }
       bf16x8 sb[2];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        float p = exp2f(fmaf(s[r], sl2, nlse));
-        if (ragged && k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3) >= S) p = 0.f;
+        const float p = ex2(fmaf(s[r], sl2, nlse));
         sb[r >> 3][r & 7] = (__bf16)(p * (dp[r] - dl_q));
       }
 #pragma unroll
