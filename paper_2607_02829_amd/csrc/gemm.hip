@@ -88,7 +88,7 @@ SR_DEV int lds_off(int row, int chunk) { return row * GK + ((chunk ^ ((row ^ (ro
 // Register staging of one R x 64 operand tile (R/32 16-byte vectors per thread).
 template <int R>
 struct TileRegs {
-  i32x4 v[R / 32];
+  i32x4 v[R / 32 > 4 ? R / 32 : 4];   // k-major: R/32 vectors; r-major: 4 per task
 };
 
 // k-major operand: rows r0.., k columns k0..k0+63 of X[r*ld + k].
@@ -111,14 +111,34 @@ SR_DEV void store_kmajor(const TileRegs<R>& t, bf16_t* lds) {
   }
 }
 
+// k-major operand straight from global memory into LDS (buffer_load ... lds, 16 bytes per
+// lane): each wave fills whole 1 KB blocks (eight 128-byte rows), lane l landing at byte 16l
+// of its block, so lane l fetches the logical chunk that the swizzle places at physical
+// chunk l % 8 of row l / 8.  No VGPRs and no LDS-store instructions are involved.
+typedef __attribute__((address_space(3))) void lds_ptr_t;
+template <int R>
+SR_DEV void load_kmajor_direct(__amdgpu_buffer_rsrc_t rs, bf16_t* lds, int r0, int k0, int ld) {
+  constexpr int BPW = R / 32;   // 1 KB blocks per wave (four waves)
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    const int blk = wid * BPW + i;
+    const int row = blk * 8 + (lane >> 3);
+    const int chunk = (lane & 7) ^ ((row ^ (row >> 3)) & 7);
+    const uint32_t off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + chunk * 8)) * 2u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t*)(lds + blk * 512), 16, off, 0, 0, 0);
+  }
+}
+
 // r-major operand: X[k*ld + r]; a task covers 4 consecutive k x 8 consecutive r and is
 // transposed in registers into eight 4-element k runs (R/128 tasks per thread).
 template <int R>
 SR_DEV void load_rmajor(TileRegs<R>& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
   constexpr int NRC = R / 8;
 #pragma unroll
-  for (int p = 0; p < R / 128; ++p) {
+  for (int p = 0; p < (R + 127) / 128; ++p) {
     const int task = threadIdx.x + 256 * p;
+    if (R < 128 && task >= 2 * R) break;   // 2R tasks of 4 k x 8 r
     const int rc = task % NRC, kg = task / NRC;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -131,8 +151,9 @@ template <int R>
 SR_DEV void store_rmajor(const TileRegs<R>& t, bf16_t* lds) {
   constexpr int NRC = R / 8;
 #pragma unroll
-  for (int p = 0; p < R / 128; ++p) {
+  for (int p = 0; p < (R + 127) / 128; ++p) {
     const int task = threadIdx.x + 256 * p;
+    if (R < 128 && task >= 2 * R) break;
     const int rc = task % NRC, kg = task / NRC;
     const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 0]);
     const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 1]);
@@ -234,12 +255,14 @@ SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in)
 // MI x 2 MFMA tiles of 32 x 32 (MI = BM/64).  BM = 256 halves the LDS bytes read per MFMA
 // of the A operand; BM = 128 keeps two workgroups per CU and more tiles for narrow outputs.
 template <int BM, bool AK, bool BK, int EPI, typename T, typename Ta>
-__global__ __launch_bounds__(256, BM == 128 ? 2 : 1) void gemm_mfma_kernel(
+__global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bm, int M, int N, int Kd, int lda, int ldb,
     uint32_t a_bytes, uint32_t b_bytes, int k_per_split, EpiArgs ep) {
-  constexpr int MI = BM / 64;
+  constexpr int MI = BM / 64 > 0 ? BM / 64 : 1;
+  static_assert(BM == 64 || BM == 128 || BM == 256, "tile height");
   constexpr int STAGE = (BM + GN) * GK;   // bf16 elements of one LDS stage (A tile then B tile)
-  constexpr int SMEM = 128 * EPI_LD * 4 > 2 * STAGE * 2 ? 128 * EPI_LD * 4 : 2 * STAGE * 2;
+  constexpr int EPI_BYTES = (BM < 128 ? BM : 128) * EPI_LD * 4;
+  constexpr int SMEM = EPI_BYTES > 2 * STAGE * 2 ? EPI_BYTES : 2 * STAGE * 2;
   // two operand stages (the next k-tile is written into one while the other is consumed);
   // the same memory stages the fp32 result, 128 rows at a time, for the epilogue
   __shared__ __attribute__((aligned(16))) char smem_raw[SMEM];
@@ -260,16 +283,18 @@ __global__ __launch_bounds__(256, BM == 128 ? 2 : 1) void gemm_mfma_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // k-major operands go global -> LDS directly; r-major ones through registers (transposed)
   TileRegs<BM> ta;
   TileRegs<GN> tb;
-  auto gload = [&](int k0) {
-    if constexpr (AK) load_kmajor<BM>(ta, ra, m0, k0, lda); else load_rmajor<BM>(ta, ra, m0, k0, lda);
-    if constexpr (BK) load_kmajor<GN>(tb, rb, n0, k0, ldb); else load_rmajor<GN>(tb, rb, n0, k0, ldb);
+  auto gload = [&](int k0, int s) {
+    bf16_t* st = smem + s * STAGE;
+    if constexpr (AK) load_kmajor_direct<BM>(ra, st, m0, k0, lda); else load_rmajor<BM>(ta, ra, m0, k0, lda);
+    if constexpr (BK) load_kmajor_direct<GN>(rb, st + BM * GK, n0, k0, ldb); else load_rmajor<GN>(tb, rb, n0, k0, ldb);
   };
   auto lstore = [&](int s) {
     bf16_t* st = smem + s * STAGE;
-    if constexpr (AK) store_kmajor<BM>(ta, st); else store_rmajor<BM>(ta, st);
-    if constexpr (BK) store_kmajor<GN>(tb, st + BM * GK); else store_rmajor<GN>(tb, st + BM * GK);
+    if constexpr (!AK) store_rmajor<BM>(ta, st);
+    if constexpr (!BK) store_rmajor<GN>(tb, st + BM * GK);
   };
 
   // EPI_DW: the first column of tiles also sums its A rows (bias gradient)
@@ -294,15 +319,16 @@ __global__ __launch_bounds__(256, BM == 128 ? 2 : 1) void gemm_mfma_kernel(
   }
 
   if (kbeg < kend) {
-    gload(kbeg);
+    gload(kbeg, 0);
     lstore(0);
   }
+  __builtin_amdgcn_s_waitcnt(0);   // direct LDS loads are counted by vmcnt
   __syncthreads();
   int it = 0;
   for (int k0 = kbeg; k0 < kend; k0 += GK, ++it) {
     const int cur = it & 1;
     const bool more = k0 + GK < kend;
-    if (more) gload(k0 + GK);   // in flight while this tile is consumed
+    if (more) gload(k0 + GK, cur ^ 1);   // in flight while this tile is consumed
     const bf16_t* St = smem + cur * STAGE;
     if (do_db) {
       const int row = threadIdx.x / TPR;
@@ -334,11 +360,13 @@ __global__ __launch_bounds__(256, BM == 128 ? 2 : 1) void gemm_mfma_kernel(
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][i], b[ks][j], acc[i][j], 0, 0, 0);
     if (more) lstore(cur ^ 1);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
 
   if constexpr (EPI == EPI_DW) {
-    if constexpr (TPR == 2) dbacc += __shfl_xor(dbacc, 1, 64);
+#pragma unroll
+    for (int o = 1; o < TPR; o <<= 1) dbacc += __shfl_xor(dbacc, o, 64);
     const int dbrow = m0 + (int)threadIdx.x / TPR;
     if (do_db && (threadIdx.x % TPR) == 0 && dbrow < M) {
       if (gridDim.z == 1) ep.db_out[dbrow] = dbacc;
@@ -346,11 +374,13 @@ __global__ __launch_bounds__(256, BM == 128 ? 2 : 1) void gemm_mfma_kernel(
     }
   }
 
-  // epilogue, 128 rows per pass: stage the fp32 result (register r of a 32x32 MFMA tile
+  // epilogue, PR rows per pass: stage the fp32 result (register r of a 32x32 MFMA tile
   // holds row 8*(r/4) + 4*(lane/32) + r%4, column lane%32), then 4-column chunks per thread
+  constexpr int PR = BM < 128 ? BM : 128;
+  constexpr int NB = PR / 64;   // batches of 8 chunks per thread in a pass
   float* stage = reinterpret_cast<float*>(smem_raw);
 #pragma unroll
-  for (int half = 0; half < BM / 128; ++half) {
+  for (int half = 0; half < BM / PR; ++half) {
     if (half) __syncthreads();
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -358,25 +388,25 @@ __global__ __launch_bounds__(256, BM == 128 ? 2 : 1) void gemm_mfma_kernel(
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int row = wm * (BM / 2) + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3) - half * 128;
+          const int row = wm * (BM / 2) + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3) - half * PR;
           const int col = wn * 64 + j * 32 + (lane & 31);
-          if (row >= 0 && row < 128) stage[row * EPI_LD + col] = acc[i][j][r];
+          if (row >= 0 && row < PR) stage[row * EPI_LD + col] = acc[i][j][r];
         }
     __syncthreads();
 #pragma unroll
-    for (int bch = 0; bch < 2; ++bch) {
+    for (int bch = 0; bch < NB; ++bch) {
       EpiIn in[8];
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const int c = threadIdx.x + 256 * (bch * 8 + q);
-        const int m = m0 + half * 128 + (c >> 5), n = n0 + (c & 31) * 4;
+        const int m = m0 + half * PR + (c >> 5), n = n0 + (c & 31) * 4;
         if (m < M && n < N) epi_load<EPI>(ep, m, n, in[q]);
       }
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const int c = threadIdx.x + 256 * (bch * 8 + q);
         const int row = c >> 5, c4 = (c & 31) * 4;
-        const int m = m0 + half * 128 + row, n = n0 + c4;
+        const int m = m0 + half * PR + row, n = n0 + c4;
         float part = 0.f;
         if (m < M && n < N)
           part = epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stage + row * EPI_LD + c4), in[q]);
@@ -488,8 +518,15 @@ static hipError_t run_mfma_bm(const GemmDesc& g, const EpiArgs& ep, hipStream_t 
   return hipGetLastError();
 }
 
+// Tile height: 128, or 64 when 128-row tiles would leave fewer than two workgroups per CU.
 template <int EPI, typename T, typename Ta>
 static hipError_t run_mfma(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
+  const long tiles128 = (long)((g.N + GN - 1) / GN) * ((g.M + 127) / 128) * g.splits;
+#ifdef SR_GEMM_FORCE_BM
+  if (SR_GEMM_FORCE_BM == 64) return run_mfma_bm<64, EPI, T, Ta>(g, ep, st);
+  return run_mfma_bm<128, EPI, T, Ta>(g, ep, st);
+#endif
+  if (tiles128 < 512) return run_mfma_bm<64, EPI, T, Ta>(g, ep, st);
   return run_mfma_bm<128, EPI, T, Ta>(g, ep, st);
 }
 
