@@ -28,6 +28,15 @@ if ROOT not in sys.path:
 
 PEAK_BF16_FLOPS = 2.5e15      # MI355X dense bf16 MFMA
 PEAK_HBM_BYTES = 8.0e12       # MI355X HBM3E
+COPY_PROBE_BYTES = 1 << 30    # device-to-device copy of known size (counter calibration)
+PROFILES = os.path.join(ROOT, "profiles")
+
+# kernel group -> (source file whose text the HBM-traffic figure was taken on, kernel symbol)
+KERNEL_SOURCES = {
+    "attn_bwd_dkv": ("paper_2607_02829_amd/csrc/attention.hip", "attn_bwd_dkv_mfma"),
+    "attn_bwd_dq": ("paper_2607_02829_amd/csrc/attention.hip", "attn_bwd_dq_mfma"),
+    "attn_fwd": ("paper_2607_02829_amd/csrc/attention.hip", "attn_fwd_mfma"),
+}
 
 
 def log(*a):
@@ -119,6 +128,99 @@ def kernel_breakdown(st: Step, step_index: int):
     return st.abi.sr_profile_stop()
 
 
+def source_hash(group: str) -> str | None:
+    import hashlib
+    if group not in KERNEL_SOURCES:
+        return None
+    with open(os.path.join(ROOT, KERNEL_SOURCES[group][0]), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_for(group: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, if it was taken on the
+    current source of the kernel (else None)."""
+    path = os.path.join(PROFILES, f"{group}_{workload}_hbm_traffic.md")
+    if not os.path.exists(path) or source_hash(group) is None:
+        return None
+    fields = {}
+    for line in open(path):
+        if line.startswith("- ") and ":" in line:
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    if fields.get("source_sha256") != source_hash(group):
+        return None
+    return float(fields["hbm_bytes_per_launch"])
+
+
+def summarize_pmc(group: str, workload: str, fetch_csv: str, write_csv: str, command: str) -> str:
+    """Turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; KiB per dispatch) into the
+    per-launch HBM traffic of `group`, scaled by the counters of the copy probe."""
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        vals = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return vals
+
+    sym = KERNEL_SOURCES[group][1]
+    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+
+    def pick(vals, needle):
+        keys = [k for k in vals if needle in k]
+        if not keys:
+            raise SystemExit(f"no dispatch of {needle} in the counter file")
+        return statistics.mean(vals[keys[0]]), len(vals[keys[0]]), keys[0]
+
+    def copy_entry(vals):
+        # the copy probe is the largest single dispatch among the copy kernels
+        best = None
+        for k, v in vals.items():
+            if "copy" in k.lower() or "Copy" in k:
+                m = max(v)
+                if best is None or m > best[0]:
+                    best = (m, k)
+        if best is None:
+            raise SystemExit("no copy-probe dispatch in the counter file")
+        return best
+
+    f_k, n_k, name = pick(fetch, sym)
+    w_k, _, _ = pick(write, sym)
+    f_c, copy_name = copy_entry(fetch)
+    w_c, _ = copy_entry(write)
+    f_scale = COPY_PROBE_BYTES / (f_c * 1024.0)
+    w_scale = COPY_PROBE_BYTES / (w_c * 1024.0)
+    total = f_k * 1024.0 * f_scale + w_k * 1024.0 * w_scale
+    lines = [
+        f"# HBM traffic of `{sym}` on the {workload} workload",
+        "",
+        "rocprofv3 counter passes (one counter group per run), KiB per dispatch, averaged over",
+        f"{n_k} dispatches of the kernel; scaled by the same counters read on a device-to-device",
+        f"copy of {COPY_PROBE_BYTES} bytes (`{copy_name.split('(')[0]}`).",
+        "",
+        "Commands (repository root on the GPU box, `cd /tmp && export TMPDIR=/tmp` first):",
+        "",
+        "```",
+        command,
+        "```",
+        "",
+        f"- kernel: `{name.split('(')[0]}`",
+        f"- fetch_kib_per_launch: {f_k:.1f}",
+        f"- write_kib_per_launch: {w_k:.1f}",
+        f"- copy_probe_fetch_kib: {f_c:.1f}",
+        f"- copy_probe_write_kib: {w_c:.1f}",
+        f"- fetch_scale: {f_scale:.4f}",
+        f"- write_scale: {w_scale:.4f}",
+        f"- hbm_bytes_per_launch: {total:.0f}",
+        f"- source_sha256: `{source_hash(group)}`",
+        "",
+    ]
+    return "\n".join(lines)
+
+
 def cpu_baseline(w) -> dict:
     """Time the oracle on a bounded sample: one block forward+backward on the K routed
     tokens of one sample plus the routing (selection, gather, scatter) of one step;
@@ -166,7 +268,20 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=3, help="timed steps of the dense keep=100%% mode (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="print the per-kernel breakdown to stderr")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run one device-to-device copy of known size first (counter calibration)")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("GROUP", "FETCH_CSV", "WRITE_CSV", "OUT_MD"),
+                    help="write the HBM-traffic summary of GROUP from two rocprofv3 --pmc CSVs and exit")
+    ap.add_argument("--pmc-command", default="", help="command text recorded in the summary")
     args = ap.parse_args()
+
+    if args.summarize_pmc:
+        group, fcsv, wcsv, out_md = args.summarize_pmc
+        text = summarize_pmc(group, args.workload, fcsv, wcsv, args.pmc_command)
+        with open(out_md, "w") as f:
+            f.write(text)
+        print(text)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the routed stack is built and timed on a single MI355X; "
@@ -179,6 +294,13 @@ def main():
     abi.lib()
     torch.cuda.set_device(0)
     w = inputs.WORKLOADS[args.workload]
+    if args.copy_probe:
+        src = torch.empty(COPY_PROBE_BYTES, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
     log(f"workload {w.name}: B={w.B} L={w.L} K={w.K} D={w.D} H={w.H} F={w.F} blocks={w.n_blocks} {w.dtype}")
 
     # ---------------------------------------------------------------- routed (sparse) mode
@@ -258,7 +380,7 @@ def main():
         "peak_bytes": {"sparse": int(sparse_peak), "dense": dense["peak_bytes"] if dense else None,
                        "ratio": round(dense["peak_bytes"] / sparse_peak, 3) if dense else None},
         "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved_u, 2), "peak": peak_u, "unit": unit,
-                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "frac": round(achieved / peak, 4), "traffic": traffic_for(dom, w.name),
                      "launches_timed": int(d["launches"]), "avg_launch_us": round(per_launch_ms * 1e3, 2)},
         "cpu_baseline": cpu,
         "outputs_finite": finite,
