@@ -27,9 +27,10 @@
  *  - Shapes: B samples, L tokens per sample, D channels, H heads (D % H == 0),
  *    F MLP width, n_blocks middle blocks; S = K (routed) or L (dense) tokens per
  *    sample inside the stack.
- *  - Support: D % 64 == 0 and F % 64 == 0; any head dim (hd = 64 runs the MFMA
- *    attention, other sizes a generic kernel); 1 <= K <= L; B*L*D*elt < 2^31 bytes
- *    per tensor.  Anything else returns SR_EUNSUPPORTED.
+ *  - Support: D % 64 == 0, F % 64 == 0, D <= 2048, head dim D/H in {32, 64, 128}
+ *    (bf16 with head dim 64 runs the MFMA attention kernels, every other case a
+ *    generic fp32-accumulating kernel); 1 <= K <= L; B*L*D*elt < 2^31 bytes per
+ *    tensor.  Anything else returns SR_EUNSUPPORTED.
  */
 #ifndef SR_H
 #define SR_H

@@ -5,19 +5,25 @@
 // 2D + h*hd); O and dO are [B*S, D]; dqkv mirrors qkv.  lse[b,h,s] is the base-2
 // log-sum-exp of the scaled scores, so P = exp2(s * log2(e)/sqrt(hd) - lse).
 //
-// MFMA kernels (hd = 64, bf16, v_mfma_f32_32x32x16_bf16):
-//  * forward: a wave owns 32 queries and computes S^T = K Q^T for 64-key LDS
-//    tiles, so each lane holds one query's scores and the online-softmax state
-//    (running max, partial sum) is per lane; one xor-32 exchange per tile gives
-//    the row max.  O^T += V^T P^T reuses the score registers directly as the B
-//    operand (the k order inside an MFMA is free as long as A and B agree), with
-//    V staged transposed in LDS.  The S x S score matrix is never stored.
-//  * backward dK/dV: a wave owns 32 keys; for 64-query tiles it forms
-//    S = Q K^T and dP = dO V^T (key per lane), P = exp2(S c - lse),
-//    dS = P (dP - delta), then dV^T += dO^T P and dK^T += Q^T dS.
-//  * backward dQ: a wave owns 32 queries; S^T, dP^T per 64-key tile and
-//    dQ^T += K^T dS^T.
+// MFMA kernels (hd = 64, bf16, v_mfma_f32_32x32x16_bf16).  A workgroup of four waves
+// owns 128 rows (32 per wave) of the resident dimension and streams the other one in
+// 64-row tiles of one head:
+//  * forward: a wave owns 32 queries and forms S^T = K Q^T per 32-key unit, so each
+//    lane holds one query's scores and the online-softmax state is per lane; the row
+//    max needs one exchange between the wave's two halves (v_permlane32_swap).
+//    O^T += V^T P^T reuses the score registers as the MFMA B operand (the k order inside
+//    an MFMA is free as long as A and B agree).  The S x S matrix is never stored.
+//  * backward dK/dV: a wave owns 32 keys; per 32-query unit S = Q K^T and dP = dO V^T
+//    (key per lane), P = exp2(S c - lse), dS = P (dP - delta), dV^T += dO^T P and
+//    dK^T += Q^T dS.
+//  * backward dQ: a wave owns 32 queries; per 32-key unit S^T, dP^T and dQ^T += K^T dS^T.
 // Two backward passes (instead of atomics) keep the result deterministic.
+//
+// Tiles go from global memory straight into LDS (buffer_load ... lds), three stages deep
+// (tile t+2 is in flight while tile t is consumed), row-major with an XOR swizzle of the
+// 16-byte chunks; one workgroup barrier per tile.  Operands needed transposed (V^T, Q^T,
+// dO^T, K^T) are read with ds_read_b64_tr_b16, which hands each lane four consecutive rows
+// of one column, so no transposed copy is ever written.
 //
 // Generic kernels (any storage type, hd in {32, 64, 128}): one thread per row,
 // online softmax over keys, fp32 throughout.
@@ -30,9 +36,17 @@
 namespace sr {
 
 constexpr int HD = 64;
-constexpr int AP = HD + 8;   // padded LDS row (bf16)
+constexpr int AP = HD + 8;   // padded row (bf16) of the output staging tile
 constexpr int QW = 128;      // rows (queries or keys) per workgroup, 32 per wave
 constexpr int KT = 64;       // tile of the streamed dimension
+constexpr int TE = KT * HD;  // bf16 elements of one 64 x 64 tile (8 KB)
+constexpr int NSTG = 3;      // LDS stages
+
+template <int V>
+using IC = std::integral_constant<int, V>;
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 SR_DEV bf16x8 zero8() {
   bf16x8 z;
@@ -42,16 +56,6 @@ SR_DEV bf16x8 zero8() {
 }
 
 SR_DEV bf16x8 ld8(const bf16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
-
-// A fragment whose k order matches a score fragment: elements 0..3 from p[4*h],
-// elements 4..7 from p[8 + 4*h].
-SR_DEV bf16x8 ld_perm(const bf16_t* p, int h) {
-  i32x2 lo = *reinterpret_cast<const i32x2*>(p + 4 * h);
-  i32x2 hi = *reinterpret_cast<const i32x2*>(p + 8 + 4 * h);
-  i32x4 v;
-  v[0] = lo[0]; v[1] = lo[1]; v[2] = hi[0]; v[3] = hi[1];
-  return *reinterpret_cast<bf16x8*>(&v);
-}
 
 SR_DEV f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) { return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0); }
 
@@ -64,46 +68,70 @@ SR_DEV void zero16(f32x16& a) {
   for (int r = 0; r < 16; ++r) a[r] = 0.f;
 }
 
-// A 64 x 64 tile of one head (rows r0.., head columns), moved by 256 threads: thread
-// (dg = tid % 16, rg = tid / 16) holds rows 4rg..4rg+3, columns 4dg..4dg+3 in registers, so
-// one global read can be written to LDS row-major, transposed, or both.
-struct Tile4 {
-  i32x2 v[4];
-};
-
-// Rows past the sample's S tokens are read without a guard: they belong to the next
-// sample (finite values that the callers neutralise: keys get a -inf score, queries an
-// infinite LSE) or lie past the tensor, where the buffer load returns zero.
-// `base` is the byte offset of (row 0, column 0 of the head) inside the tensor of `rs`.
-SR_DEV void t4_load(Tile4& t, __amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t ld, int r0) {
-  const int dg = threadIdx.x & 15, rg = threadIdx.x >> 4;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    t.v[i] = buf_load8(rs, base + ((uint32_t)(r0 + rg * 4 + i) * ld + (uint32_t)dg * 4u) * 2u);
+// Value of the lane 32 apart, combined: max / sum over the wave's two halves.
+SR_DEV float xmax32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+SR_DEV float xadd32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// lds[row][d]
-SR_DEV void t4_rows(const Tile4& t, bf16_t* lds) {
-  const int dg = threadIdx.x & 15, rg = threadIdx.x >> 4;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) *reinterpret_cast<i32x2*>(lds + (rg * 4 + i) * AP + dg * 4) = t.v[i];
-}
+// LDS tile: 64 rows of 64 bf16 (eight 16-byte chunks); chunk c of row r sits at chunk
+// position c ^ swz(r).  Among any 16 consecutive rows the even ones use eight different
+// positions and so do the odd ones (conflict-free 16-byte fragment reads), and rows 16
+// apart share a swizzle, so fragment addresses of different 16-row groups differ by
+// constants (instruction offsets rather than extra address registers).
+SR_DEV int swz(int row) { return (row >> 1) & 7; }
+SR_DEV int toff(int row, int chunk) { return row * HD + ((chunk ^ swz(row)) << 3); }
 
-// lds[d][row]
-SR_DEV void t4_cols(const Tile4& t, bf16_t* lds) {
-  const int dg = threadIdx.x & 15, rg = threadIdx.x >> 4;
-  const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&t.v[0]);
-  const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&t.v[1]);
-  const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&t.v[2]);
-  const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&t.v[3]);
+// Rows r0..r0+63 of one head (columns base.. of a row-major tensor with row length ld)
+// into the LDS tile dst: eight 1 KB blocks of eight rows, two per wave; lane l lands at
+// byte 16 l of its block, so it fetches the chunk that the swizzle places there.  Rows past
+// the sample's S tokens are read without a guard: they belong to the next sample (finite
+// values the callers mask) or lie past the tensor, where the buffer load returns zero.
+SR_DEV void tile_load(__amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t ld, int r0, bf16_t* dst) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    i32x2 w;
-    w[0] = (int)((uint32_t)e0[c] | ((uint32_t)e1[c] << 16));
-    w[1] = (int)((uint32_t)e2[c] | ((uint32_t)e3[c] << 16));
-    *reinterpret_cast<i32x2*>(lds + (dg * 4 + c) * AP + rg * 4) = w;
+  for (int i = 0; i < 2; ++i) {
+    const int blk = wid * 2 + i;
+    const int row = blk * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ swz(row);
+    const uint32_t off = base + ((uint32_t)(r0 + row) * ld + (uint32_t)c * 8u) * 2u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t*)(dst + blk * 512), 16, off, 0, 0, 0);
   }
 }
+
+// Fragment of the 32 rows r0.. (MFMA row index = lane % 32), k-step ks of the 64 columns.
+SR_DEV bf16x8 row_frag(const bf16_t* tile, int r0, int ks) {
+  const int lane = threadIdx.x & 63;
+  return ld8(tile + toff(r0 + (lane & 31), 2 * ks + (lane >> 5)));
+}
+
+// Transposed fragment: MFMA row index = tile column c0 + lane % 32, k = tile rows, in the
+// order of a score fragment: elements 0..3 are rows k0 + 4h .. k0 + 4h + 3 and elements
+// 4..7 rows k0 + 8 + 4h .. (h = lane / 32).  ds_read_b64_tr_b16 gives lane i of each
+// 16-lane group column i of the four rows addressed by the group (lane s: row s / 4,
+// columns 4 (s % 4) .. + 3).
+SR_DEV v4s ds_tr(const bf16_t* p) { return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p); }
+SR_DEV bf16x8 tr_frag(const bf16_t* tile, int k0, int c0) {
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, s = lane & 15;
+  const int col = c0 + 16 * (g & 1) + 4 * (s & 3);
+  const int r1 = k0 + 4 * (g >> 1) + (s >> 2), r2 = r1 + 8;
+  const v4s lo = ds_tr(tile + r1 * HD + (((col >> 3) ^ swz(r1)) << 3) + (col & 7));
+  const v4s hi = ds_tr(tile + r2 * HD + (((col >> 3) ^ swz(r2)) << 3) + (col & 7));
+  i32x4 w;
+  w[0] = __builtin_bit_cast(i32x2, lo)[0];
+  w[1] = __builtin_bit_cast(i32x2, lo)[1];
+  w[2] = __builtin_bit_cast(i32x2, hi)[0];
+  w[3] = __builtin_bit_cast(i32x2, hi)[1];
+  return __builtin_bit_cast(bf16x8, w);
+}
+
+// Row index (within a 32-row unit) of score register r of this lane.
+SR_DEV int srow(int r, int h32) { return 8 * (r >> 2) + 4 * h32 + (r & 3); }
 
 // Write a wave's 32 x 64 result (held transposed: acc[db][r] = X[d][row]) to LDS
 // stage[row_local][d], scaled.
@@ -112,10 +140,7 @@ SR_DEV void stage_t(bf16_t* stage, const f32x16 acc[2], float mul, int wid, int 
 #pragma unroll
   for (int db = 0; db < 2; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int d = db * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3);
-      stage[(wid * 32 + l32) * AP + d] = f2bf(acc[db][r] * mul);
-    }
+    for (int r = 0; r < 16; ++r) stage[(wid * 32 + l32) * AP + db * 32 + srow(r, h32)] = f2bf(acc[db][r] * mul);
 }
 
 // Copy the 128 x 64 staged tile to rows r0.. of dst (column block of one head).
@@ -130,23 +155,18 @@ SR_DEV void unstage(const bf16_t* stage, bf16_t* dst, size_t ld, int r0, int S) 
   }
 }
 
-// All three MFMA kernels stream 64-row tiles through two LDS stages: while tile t is
-// consumed from one stage, tile t+1 is already in flight from global memory into
-// registers and is written into the other stage afterwards (one barrier per tile).
-
 // ------------------------------------------------------------------------------ forward
 
 __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ O,
                                                      float* __restrict__ lse, int S, int H, int D, float sl2) {
-  constexpr int ST = 2 * KT * AP;   // one stage: Ks [key][d], Vt [d][key]
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * ST];
+  __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
   const size_t ld = 3 * (size_t)D;
-  const bf16_t* base = qkv + (size_t)b * S * ld;
-  const bf16_t* qp = base + hh * HD;
+  const bf16_t* qp = qkv + (size_t)b * S * ld + hh * HD;
   const int myq = blockIdx.x * QW + wid * 32 + l32;
-  const int ntiles = (S + KT - 1) / KT;
+  const int nt = (S + KT - 1) / KT;
+  const bool ragged = S % KT != 0;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
   const uint32_t kbase = (uint32_t)(((size_t)b * S * ld + D + hh * HD) * 2);
   const uint32_t vbase = kbase + (uint32_t)D * 2u;
@@ -155,88 +175,87 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) qf[ks] = myq < S ? ld8(qp + (size_t)myq * ld + ks * 16 + 8 * h32) : zero8();
 
-  Tile4 kr, vr;
-  t4_load(kr, rq, kbase, (uint32_t)ld, 0);
-  t4_load(vr, rq, vbase, (uint32_t)ld, 0);
-  t4_rows(kr, smem);
-  t4_cols(vr, smem + KT * AP);
-  __syncthreads();
+  auto load = [&](int t, int s) {
+    tile_load(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE);
+    tile_load(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE);
+  };
+  // S^T of key unit u (32 keys) of the tile in stage s: register r holds key srow(r), query l32
+  auto scores = [&](int s, int u, f32x16& sc) {
+    const bf16_t* Ks = smem + s * 2 * TE;
+    zero16(sc);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) sc = mfma(row_frag(Ks, u * 32, ks), qf[ks], sc);
+  };
+  auto mask = [&](f32x16& sc, int k0) {   // keys past S do not exist
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (k0 + srow(r, h32) >= S) sc[r] = -INFINITY;
+  };
 
   f32x16 o[2];
   zero16(o[0]); zero16(o[1]);
-  float m_run = -INFINITY, l_run = 0.f;   // running max of the raw scores, partial sum
-
-  // one key tile: prefetch the next, consume this one from LDS, stage the next
-  auto step = [&](int t, auto ragged) {
-    const int k0 = t * KT;
-    const bool more = t + 1 < ntiles;
-    if (more) {
-      t4_load(kr, rq, kbase, (uint32_t)ld, k0 + KT);
-      t4_load(vr, rq, vbase, (uint32_t)ld, k0 + KT);
+  float m_run = -INFINITY, l_run = 0.f;   // running max of the raw scores, partial sum (this half's keys)
+  // online softmax of one unit, then O^T += V^T P^T
+  auto consume = [&](int s, int u, const f32x16& sc) {
+    float mx = sc[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[r]);
+    mx = xmax32(mx);
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = ex2((m_run - m_new) * sl2);
+    const float nm = -m_new * sl2;
+    bf16x8 pb[2];
+    float psum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = ex2(fmaf(sc[r], sl2, nm));
+      psum += p;
+      pb[r >> 3][r & 7] = (__bf16)p;
     }
-    const bf16_t* Ks = smem + (t & 1) * ST;
-    const bf16_t* Vt = Ks + KT * AP;
-    {
-      f32x16 s[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        zero16(s[kb]);
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) s[kb] = mfma(ld8(Ks + (kb * 32 + l32) * AP + ks * 16 + 8 * h32), qf[ks], s[kb]);
-      }
-      if constexpr (decltype(ragged)::value) {   // last tile: keys past S do not exist
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3) >= S) s[kb][r] = -INFINITY;
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = ex2((m_run - m_new) * sl2);
-      const float nm = -m_new * sl2;
-      float psum = 0.f;
-      bf16x8 pb[2][2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = ex2(fmaf(s[kb][r], sl2, nm));
-          psum += p;
-          pb[kb][r >> 3][r & 7] = (__bf16)p;
-        }
-      l_run = l_run * alpha + psum;
-      m_run = m_new;
-      if (__ballot(alpha != 1.0f)) {
-#pragma unroll
-        for (int db = 0; db < 2; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+    if (__ballot(alpha != 1.0f)) {
 #pragma unroll
       for (int db = 0; db < 2; ++db)
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+    }
+    const bf16_t* Vs = smem + s * 2 * TE + TE;
 #pragma unroll
-          for (int kk = 0; kk < 2; ++kk)
-            o[db] = mfma(ld_perm(Vt + (db * 32 + l32) * AP + kb * 32 + kk * 16, h32), pb[kb][kk], o[db]);
-    }
-    if (more) {
-      bf16_t* nx = smem + ((t + 1) & 1) * ST;
-      t4_rows(kr, nx);
-      t4_cols(vr, nx + KT * AP);
-    }
-    __syncthreads();
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) o[db] = mfma(tr_frag(Vs, u * 32 + kk * 16, db * 32), pb[kk], o[db]);
   };
-  // full tiles, then the ragged last tile (masking only there)
-  for (int t = 0; t < S / KT; ++t) step(t, std::false_type{});
-  if (S % KT) step(S / KT, std::true_type{});
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+
+  load(0, 0);
+  if (nt > 1) load(1, 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  auto tile = [&](int t, auto stg) {
+    constexpr int s0 = decltype(stg)::value, s2 = (s0 + 2) % NSTG;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      f32x16 sc;
+      scores(s0, u, sc);
+      if (ragged && t + 1 == nt && S - t * KT < (u + 1) * 32) mask(sc, t * KT + u * 32);
+      consume(s0, u, sc);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();   // tile t+1 resident; tile t's stage no longer read
+    if (t + 2 < nt) load(t + 2, s2);
+  };
+  int t = 0;
+  for (; t + NSTG <= nt; t += NSTG) {
+    tile(t, IC<0>{});
+    tile(t + 1, IC<1>{});
+    tile(t + 2, IC<2>{});
+  }
+  if (t < nt) tile(t, IC<0>{});
+  if (t + 1 < nt) tile(t + 1, IC<1>{});
+
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();   // every wave is done with the stages before they hold the output
+  const float l_tot = xadd32(l_run);
   if (h32 == 0 && myq < S) lse[((size_t)b * H + hh) * S + myq] = m_run * sl2 + log2f(l_tot);
   stage_t(smem, o, 1.0f / l_tot, wid, lane);
   __syncthreads();
@@ -249,22 +268,17 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkv_mfma(const bf16_t* __rest
                                                          const float* __restrict__ lse, const float* __restrict__ delta,
                                                          bf16_t* __restrict__ dqkv, int S, int H, int D, float sl2,
                                                          float scale) {
-  constexpr int STB = 4 * KT * AP;                 // bf16 per stage: Qs, dOs [q][d]; Qt, dOt [d][q]
-  constexpr int STF = 2 * KT;                      // floats per stage: lse, delta of the tile's rows
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * STB];
-  __shared__ float fsm[2 * STF];
+  __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: Q tile, dO tile
+  __shared__ __attribute__((aligned(16))) float fsm[NSTG * 2 * KT];     // stage: lse, delta of the tile's rows
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
   const size_t ld = 3 * (size_t)D;
   const bf16_t* base = qkv + (size_t)b * S * ld;
-  const bf16_t* qp = base + hh * HD;
   const bf16_t* kp = base + D + hh * HD;
   const bf16_t* vp = base + 2 * D + hh * HD;
-  const bf16_t* dop = dO + (size_t)b * S * D + hh * HD;
-  const float* lse_b = lse + ((size_t)b * H + hh) * S;
-  const float* dl_b = delta + ((size_t)b * H + hh) * S;
   const int mykey = blockIdx.x * QW + wid * 32 + l32;
-  const int ntiles = (S + KT - 1) / KT;
+  const int nt = (S + KT - 1) / KT;
+  const bool ragged = S % KT != 0;
 
   bf16x8 kf[4], vf[4];
 #pragma unroll
@@ -275,74 +289,94 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dkv_mfma(const bf16_t* __rest
   f32x16 dv[2], dk[2];
   zero16(dv[0]); zero16(dv[1]); zero16(dk[0]); zero16(dk[1]);
 
-  Tile4 qr, dr;
-  float lr = INFINITY, drl = 0.f;   // this thread's row statistic (threads < 64)
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
   const __amdgpu_buffer_rsrc_t rd = make_rsrc(dO, (uint32_t)((size_t)gridDim.z * S * D * 2));
+  const __amdgpu_buffer_rsrc_t rl = make_rsrc(lse, (uint32_t)((size_t)gridDim.z * H * S * 4));
+  const __amdgpu_buffer_rsrc_t rdl = make_rsrc(delta, (uint32_t)((size_t)gridDim.z * H * S * 4));
   const uint32_t qbase = (uint32_t)(((size_t)b * S * ld + hh * HD) * 2);
   const uint32_t dbase = (uint32_t)(((size_t)b * S * D + hh * HD) * 2);
-  auto fetch = [&](int q0) {
-    t4_load(qr, rq, qbase, (uint32_t)ld, q0);
-    t4_load(dr, rd, dbase, (uint32_t)D, q0);
-    if (threadIdx.x < KT) {
-      const int q = q0 + threadIdx.x;
-      lr = q < S ? lse_b[q] : INFINITY;   // rows past S: P = 0
-      drl = q < S ? dl_b[q] : 0.f;
-    }
+  const uint32_t lbase = (uint32_t)(((size_t)b * H + hh) * S * 4);
+  auto load = [&](int t, int s) {
+    tile_load(rq, qbase, (uint32_t)ld, t * KT, smem + s * 2 * TE);
+    tile_load(rd, dbase, (uint32_t)D, t * KT, smem + s * 2 * TE + TE);
+    const uint32_t lo = lbase + (uint32_t)(t * KT + lane) * 4u;
+    if (wid == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_ptr_t*)(fsm + s * 2 * KT), 4, lo, 0, 0, 0);
+    if (wid == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(rdl, (lds_ptr_t*)(fsm + s * 2 * KT + KT), 4, lo, 0, 0, 0);
   };
-  auto put = [&](int s) {
-    bf16_t* st = smem + s * STB;
-    t4_rows(qr, st);
-    t4_rows(dr, st + KT * AP);
-    t4_cols(qr, st + 2 * KT * AP);
-    t4_cols(dr, st + 3 * KT * AP);
-    if (threadIdx.x < KT) {
-      fsm[s * STF + threadIdx.x] = lr;
-      fsm[s * STF + KT + threadIdx.x] = drl;
-    }
+  // S = Q K^T and dP = dO V^T of query unit u: register r holds query srow(r), key l32
+  auto s_of = [&](int s, int u, f32x16& sv) {
+    const bf16_t* Qs = smem + s * 2 * TE;
+    zero16(sv);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) sv = mfma(row_frag(Qs, u * 32, ks), kf[ks], sv);
   };
-  fetch(0);
-  put(0);
-  __syncthreads();
+  auto dp_of = [&](int s, int u, f32x16& dpv) {
+    const bf16_t* dOs = smem + s * 2 * TE + TE;
+    zero16(dpv);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) dpv = mfma(row_frag(dOs, u * 32, ks), vf[ks], dpv);
+  };
+  // P, dS of the unit (queries past S contribute nothing), then dV^T += dO^T P, dK^T += Q^T dS
+  auto grad = [&](int s, int u, const f32x16& sv, int q0, auto rag) {
+    f32x16 dpv;
+    dp_of(s, u, dpv);
+    const float* ls = fsm + s * 2 * KT + u * 32;
+    const float* dls = ls + KT;
+    bf16x8 pb[2], sb[2];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int ql = srow(r, h32);
+      float p = ex2(fmaf(sv[r], sl2, -ls[ql]));
+      float ds = p * (dpv[r] - dls[ql]);
+      if constexpr (decltype(rag)::value) {
+        if (q0 + ql >= S) { p = 0.f; ds = 0.f; }
+      }
+      pb[r >> 3][r & 7] = (__bf16)p;
+      sb[r >> 3][r & 7] = (__bf16)ds;
+    }
+    // keep the transposed fragment reads after the arithmetic: hoisted above it they hold
+    // registers through the exp2 chain (measured slower)
+    __builtin_amdgcn_sched_barrier(0);
+    const bf16_t* Qs = smem + s * 2 * TE;
+    const bf16_t* dOs = Qs + TE;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        dv[db] = mfma(tr_frag(dOs, u * 32 + kk * 16, db * 32), pb[kk], dv[db]);
+        dk[db] = mfma(tr_frag(Qs, u * 32 + kk * 16, db * 32), sb[kk], dk[db]);
+      }
+  };
 
-  for (int t = 0; t < ntiles; ++t) {
-    const bool more = t + 1 < ntiles;
-    if (more) fetch((t + 1) * KT);
-    const bf16_t* Qs = smem + (t & 1) * STB;
-    const bf16_t* dOs = Qs + KT * AP;
-    const bf16_t* Qt = Qs + 2 * KT * AP;
-    const bf16_t* dOt = Qs + 3 * KT * AP;
-    const float* lse_s = fsm + (t & 1) * STF;
-    const float* dl_s = lse_s + KT;
+  load(0, 0);
+  if (nt > 1) load(1, 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  auto tile = [&](int t, auto stg) {
+    constexpr int s0 = decltype(stg)::value, s2 = (s0 + 2) % NSTG;
+    const bool rag = ragged && t + 1 == nt;
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      f32x16 s, dp;
-      zero16(s); zero16(dp);
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        s = mfma(ld8(Qs + (qb * 32 + l32) * AP + ks * 16 + 8 * h32), kf[ks], s);
-        dp = mfma(ld8(dOs + (qb * 32 + l32) * AP + ks * 16 + 8 * h32), vf[ks], dp);
-      }
-      bf16x8 pb[2], sb[2];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ql = qb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3);
-        const float p = ex2(fmaf(s[r], sl2, -lse_s[ql]));
-        const float ds = p * (dp[r] - dl_s[ql]);
-        pb[r >> 3][r & 7] = (__bf16)p;
-        sb[r >> 3][r & 7] = (__bf16)ds;
-      }
-#pragma unroll
-      for (int db = 0; db < 2; ++db)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) {
-          dv[db] = mfma(ld_perm(dOt + (db * 32 + l32) * AP + qb * 32 + kk * 16, h32), pb[kk], dv[db]);
-          dk[db] = mfma(ld_perm(Qt + (db * 32 + l32) * AP + qb * 32 + kk * 16, h32), sb[kk], dk[db]);
-        }
+    for (int u = 0; u < 2; ++u) {
+      f32x16 sv;
+      s_of(s0, u, sv);
+      if (rag) grad(s0, u, sv, t * KT + u * 32, std::true_type{});
+      else grad(s0, u, sv, t * KT + u * 32, std::false_type{});
     }
-    if (more) put((t + 1) & 1);
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();   // tile t+1 resident; tile t's stage no longer read
+    if (t + 2 < nt) load(t + 2, s2);
+  };
+  int t = 0;
+  for (; t + NSTG <= nt; t += NSTG) {
+    tile(t, IC<0>{});
+    tile(t + 1, IC<1>{});
+    tile(t + 2, IC<2>{});
   }
+  if (t < nt) tile(t, IC<0>{});
+  if (t + 1 < nt) tile(t + 1, IC<1>{});
+
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
   bf16_t* out = dqkv + (size_t)b * S * ld;
   stage_t(smem, dk, scale, wid, lane);
   __syncthreads();
@@ -359,18 +393,15 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
                                                         const float* __restrict__ lse, const float* __restrict__ delta,
                                                         bf16_t* __restrict__ dqkv, int S, int H, int D, float sl2,
                                                         float scale) {
-  constexpr int ST = 3 * KT * AP;   // one stage: Ks, Vs [key][d]; Kt [d][key]
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * ST];
+  __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
   const size_t ld = 3 * (size_t)D;
-  const bf16_t* base = qkv + (size_t)b * S * ld;
-  const bf16_t* qp = base + hh * HD;
-  const bf16_t* kp = base + D + hh * HD;
-  const bf16_t* vp = base + 2 * D + hh * HD;
+  const bf16_t* qp = qkv + (size_t)b * S * ld + hh * HD;
   const bf16_t* dop = dO + (size_t)b * S * D + hh * HD;
   const int myq = blockIdx.x * QW + wid * 32 + l32;
-  const int ntiles = (S + KT - 1) / KT;
+  const int nt = (S + KT - 1) / KT;
+  const bool ragged = S % KT != 0;
 
   bf16x8 qf[4], df[4];
 #pragma unroll
@@ -386,59 +417,70 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
   const uint32_t kbase = (uint32_t)(((size_t)b * S * ld + D + hh * HD) * 2);
   const uint32_t vbase = kbase + (uint32_t)D * 2u;
-  Tile4 kr, vr;
-  t4_load(kr, rq, kbase, (uint32_t)ld, 0);
-  t4_load(vr, rq, vbase, (uint32_t)ld, 0);
-  t4_rows(kr, smem);
-  t4_rows(vr, smem + KT * AP);
-  t4_cols(kr, smem + 2 * KT * AP);
-  __syncthreads();
+  auto load = [&](int t, int s) {
+    tile_load(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE);
+    tile_load(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE);
+  };
+  // S^T = K Q^T and dP^T = V dO^T of key unit u: register r holds key srow(r), query l32
+  auto sd = [&](int s, int u, f32x16& sv, f32x16& dpv) {
+    const bf16_t* Ks = smem + s * 2 * TE;
+    const bf16_t* Vs = Ks + TE;
+    zero16(sv); zero16(dpv);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      sv = mfma(row_frag(Ks, u * 32, ks), qf[ks], sv);
+      dpv = mfma(row_frag(Vs, u * 32, ks), df[ks], dpv);
+    }
+  };
+  // dS^T of the unit (keys past S do not exist), then dQ^T += K^T dS^T
+  auto grad = [&](int s, int u, const f32x16& sv, const f32x16& dpv, int k0, auto rag) {
+    bf16x8 sb[2];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float p = ex2(fmaf(sv[r], sl2, nlse));
+      float ds = p * (dpv[r] - dl_q);
+      if constexpr (decltype(rag)::value) {
+        if (k0 + srow(r, h32) >= S) ds = 0.f;
+      }
+      sb[r >> 3][r & 7] = (__bf16)ds;
+    }
+    __builtin_amdgcn_sched_barrier(0);   // as in the dK/dV kernel
+    const bf16_t* Ks = smem + s * 2 * TE;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) dq[db] = mfma(tr_frag(Ks, u * 32 + kk * 16, db * 32), sb[kk], dq[db]);
+  };
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int k0 = t * KT;
-    const bool more = t + 1 < ntiles;
-    if (more) {
-      t4_load(kr, rq, kbase, (uint32_t)ld, k0 + KT);
-      t4_load(vr, rq, vbase, (uint32_t)ld, k0 + KT);
+  load(0, 0);
+  if (nt > 1) load(1, 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  auto tile = [&](int t, auto stg) {
+    constexpr int s0 = decltype(stg)::value, s2 = (s0 + 2) % NSTG;
+    const bool rag = ragged && t + 1 == nt;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      f32x16 sv, dpv;
+      sd(s0, u, sv, dpv);
+      if (rag) grad(s0, u, sv, dpv, t * KT + u * 32, std::true_type{});
+      else grad(s0, u, sv, dpv, t * KT + u * 32, std::false_type{});
     }
-    const bf16_t* Ks = smem + (t & 1) * ST;
-    const bf16_t* Vs = Ks + KT * AP;
-    const bf16_t* Kt = Ks + 2 * KT * AP;
-    const bool ragged = k0 + KT > S;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16 s, dp;
-      zero16(s); zero16(dp);
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        s = mfma(ld8(Ks + (kb * 32 + l32) * AP + ks * 16 + 8 * h32), qf[ks], s);
-        dp = mfma(ld8(Vs + (kb * 32 + l32) * AP + ks * 16 + 8 * h32), df[ks], dp);
-      }
-      if (ragged) {   // last tile: keys past S do not exist
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (k0 + kb * 32 + 8 * (r >> 2) + 4 * h32 + (r & 3) >= S) s[r] = -INFINITY;
-      }
-      bf16x8 sb[2];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float p = ex2(fmaf(s[r], sl2, nlse));
-        sb[r >> 3][r & 7] = (__bf16)(p * (dp[r] - dl_q));
-      }
-#pragma unroll
-      for (int db = 0; db < 2; ++db)
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
-          dq[db] = mfma(ld_perm(Kt + (db * 32 + l32) * AP + kb * 32 + kk * 16, h32), sb[kk], dq[db]);
-    }
-    if (more) {
-      bf16_t* nx = smem + ((t + 1) & 1) * ST;
-      t4_rows(kr, nx);
-      t4_rows(vr, nx + KT * AP);
-      t4_cols(kr, nx + 2 * KT * AP);
-    }
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();   // tile t+1 resident; tile t's stage no longer read
+    if (t + 2 < nt) load(t + 2, s2);
+  };
+  int t = 0;
+  for (; t + NSTG <= nt; t += NSTG) {
+    tile(t, IC<0>{});
+    tile(t + 1, IC<1>{});
+    tile(t + 2, IC<2>{});
   }
+  if (t < nt) tile(t, IC<0>{});
+  if (t + 1 < nt) tile(t + 1, IC<1>{});
+
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
   stage_t(smem, dq, scale, wid, lane);
   __syncthreads();
   unstage(smem, dqkv + (size_t)b * S * ld + hh * HD, ld, blockIdx.x * QW, S);

@@ -17,18 +17,17 @@ typedef __attribute__((__vector_size__(2 * sizeof(int)))) int i32x2;
 // ---------------------------------------------------------------- conversions
 SR_DEV float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
 
-// fp32 -> bf16, round to nearest even; NaN stays NaN.
-SR_DEV bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+// fp32 -> bf16 with the hardware conversion (v_cvt_pk_bf16_f32): round to nearest even,
+// denormals kept, NaN stays NaN.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
-// Packed pair conversion (lo in bits 0..15), same rounding.
+// Packed pair (lo in bits 0..15).
 SR_DEV uint32_t f2bf2(float lo, float hi) {
-  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
+SR_DEV bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 template <typename T> SR_DEV float to_f32(T v);
 template <> SR_DEV float to_f32<float>(float v) { return v; }
@@ -62,3 +61,7 @@ SR_DEV i32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 SR_DEV i32x2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
 }
+
+// LDS address space, for the loads that write LDS directly (buffer_load ... lds) and the
+// transposing LDS reads.
+typedef __attribute__((address_space(3))) void lds_ptr_t;

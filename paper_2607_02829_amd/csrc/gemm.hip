@@ -9,9 +9,10 @@
 // gemm_mfma: bf16 operands, fp32 accumulation on gfx950 matrix cores
 // (v_mfma_f32_32x32x16_bf16).  Workgroup tile 128 x 128 x 64, four waves in a
 // 2 x 2 arrangement, each wave 64 x 64 = 2 x 2 MFMA tiles.  Operand tiles are
-// staged in LDS in k-contiguous rows (padded by 16 bytes against bank conflicts);
-// m-major operands are transposed in registers (4 x 8 blocks) on the way in.
-// The next k-tile is prefetched into registers while the current one is consumed.
+// staged in LDS in k-contiguous rows with an XOR swizzle of the 16-byte chunks;
+// k-major operands go global -> LDS directly, m-major ones are transposed in
+// registers (4 x 8 blocks) on the way in.  The next k-tile is in flight while the
+// current one is consumed.
 // Global loads go through buffer resources, so rows past the end of an operand
 // read as zero: ragged token counts need no predicates in the main loop.
 //
@@ -29,17 +30,43 @@
 //   EPI_F32_ACC   out_f32 += v                                      (dcond over blocks)
 //   EPI_BIAS_F32  out_f32 = v + bias                                (adaLN modulation vectors)
 //   EPI_DO        out_act = Ta(v); delta = per-head row sums of Ta(v) * O (attention backward)
-//   EPI_DW        dW = v, db = row sums of A (weight and bias gradients); split-K partials
-//                 are combined by the last workgroup of each tile, in split order, so the
-//                 result does not depend on which workgroup finishes last.
+//   EPI_DW        dW = v, db = row sums of A (weight and bias gradients); with split-K each
+//                 split writes a partial plane and reduce_splits_kernel sums the planes in
+//                 split order, so the result does not depend on scheduling.
 #include "common.h"
 #include "sr_internal.h"
 
 namespace sr {
 
-SR_DEV float gelu_f(float z) { return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f)); }
+// GELU(z) = z Phi(z) and GELU'(z) = Phi(z) + z phi(z) with the standard normal CDF Phi and
+// density phi (exact GELU, not the tanh form).  Phi comes from erfc in the Chebyshev-fitted form
+// of Press et al. (Numerical Recipes, Sec. 6.2): with x = |z|/sqrt(2) and t = 1/(1 + x/2),
+// erfc(x) = t exp(-x^2 + q(t)); here q is a degree-9 least-squares fit of log2(erfc(x) e^{x^2} / t)
+// on t in (0, 1] (coefficients of our own fit, relative error of erfc <= 1.1e-7 for all x >= 0).
+// Branch-free, one reciprocal and one exp2; the tails have relative, not absolute, accuracy.
+SR_DEV float half_erfc_of(float z, float zz) {   // 0.5 erfc(|z|/sqrt(2)), zz = z*z
+  const float t = __builtin_amdgcn_rcpf(fmaf(fabsf(z), 0.35355339059327376f, 1.0f));
+  float q = 0.24651731550693512f;
+  q = fmaf(q, t, -1.1861149072647095f);
+  q = fmaf(q, t, 2.147474527359009f);
+  q = fmaf(q, t, -1.6377531290054321f);
+  q = fmaf(q, t, 0.40232160687446594f);
+  q = fmaf(q, t, -0.2687568664550781f);
+  q = fmaf(q, t, 0.13963006436824799f);
+  q = fmaf(q, t, 0.5397006273269653f);
+  q = fmaf(q, t, 1.4427292346954346f);
+  q = fmaf(q, t, -2.8257482051849365f);   // constant term minus 1: the factor 1/2
+  return t * __builtin_amdgcn_exp2f(fmaf(zz, -0.72134752044448170f, q));
+}
+SR_DEV float norm_cdf(float z, float zz) {
+  const float h = half_erfc_of(z, zz);
+  return z >= 0.f ? 1.0f - h : h;
+}
+SR_DEV float gelu_f(float z) { return z * norm_cdf(z, z * z); }
 SR_DEV float gelu_grad_f(float z) {
-  return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) + z * 0.39894228040143268f * __expf(-0.5f * z * z);
+  const float zz = z * z;
+  // phi(z) = 2^(-z^2 log2(e)/2 - log2(sqrt(2 pi)))
+  return norm_cdf(z, zz) + z * __builtin_amdgcn_exp2f(fmaf(zz, -0.72134752044448170f, -1.3257480647361593f));
 }
 
 template <int EPI, typename T, typename Ta>
@@ -76,8 +103,9 @@ SR_DEV void epilogue(const EpiArgs& e, int m, int n, float v) {
 
 // ============================================================================ MFMA kernel
 
-constexpr int GN = 128, GK = 64;
-constexpr int EPI_LD = GN + 8;   // fp32 row stride of the epilogue staging tile (128 rows per pass)
+constexpr int GK = 64;
+// s_waitcnt immediates (vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
+constexpr int kLgkm0 = 0xC07F;   // LDS / scalar-memory counter at zero, the others untouched
 
 // Operand tiles sit in LDS as rows of 64 bf16 (eight 16-byte chunks), unpadded; chunk c
 // of row r is stored at chunk position c ^ ((r ^ (r >> 3)) & 7).  With it, the 16-byte
@@ -115,7 +143,6 @@ SR_DEV void store_kmajor(const TileRegs<R>& t, bf16_t* lds) {
 // lane): each wave fills whole 1 KB blocks (eight 128-byte rows), lane l landing at byte 16l
 // of its block, so lane l fetches the logical chunk that the swizzle places at physical
 // chunk l % 8 of row l / 8.  No VGPRs and no LDS-store instructions are involved.
-typedef __attribute__((address_space(3))) void lds_ptr_t;
 template <int R>
 SR_DEV void load_kmajor_direct(__amdgpu_buffer_rsrc_t rs, bf16_t* lds, int r0, int k0, int ld) {
   constexpr int BPW = R / 32;   // 1 KB blocks per wave (four waves)
@@ -251,17 +278,24 @@ SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in)
   return 0.f;
 }
 
-// BM x 128 workgroup tile (BM = 128 or 256), four waves in 2 x 2, each (BM/2) x 64, i.e.
-// MI x 2 MFMA tiles of 32 x 32 (MI = BM/64).  BM = 256 halves the LDS bytes read per MFMA
-// of the A operand; BM = 128 keeps two workgroups per CU and more tiles for narrow outputs.
-template <int BM, bool AK, bool BK, int EPI, typename T, typename Ta>
-__global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
+// BM x BN workgroup tile, four waves in 2 x 2, each (BM/2) x (BN/2), i.e. MI x NJ MFMA tiles
+// of 32 x 32 (MI = BM/64, NJ = BN/64).  A wave reads (MI + NJ) KB of fragments from LDS per
+// MI * NJ MFMAs, so the big tiles (one workgroup per CU, accumulators in AGPRs) need half the
+// LDS bandwidth of 128 x 128 per MFMA; 128 x 128 and 64 x 128 keep two workgroups per CU and
+// enough tiles for narrow outputs.
+template <int BM, int BN, bool AK, bool BK, int EPI, typename T, typename Ta>
+__global__ __launch_bounds__(256, BM * BN >= 256 * 128 ? 1 : 2) void gemm_mfma_kernel(
     const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bm, int M, int N, int Kd, int lda, int ldb,
     uint32_t a_bytes, uint32_t b_bytes, int k_per_split, EpiArgs ep) {
   constexpr int MI = BM / 64 > 0 ? BM / 64 : 1;
+  constexpr int NJ = BN / 64;
   static_assert(BM == 64 || BM == 128 || BM == 256, "tile height");
-  constexpr int STAGE = (BM + GN) * GK;   // bf16 elements of one LDS stage (A tile then B tile)
-  constexpr int EPI_BYTES = (BM < 128 ? BM : 128) * EPI_LD * 4;
+  static_assert(BN == 128 || BN == 256, "tile width");
+  constexpr int GN = BN;
+  constexpr int STAGE = (BM + BN) * GK;   // bf16 elements of one LDS stage (A tile then B tile)
+  constexpr int EPI_LD = BN + 8;          // fp32 row stride of the epilogue staging tile
+  constexpr int PR = BN == 256 ? (BM < 64 ? BM : 64) : (BM < 128 ? BM : 128);   // rows per pass
+  constexpr int EPI_BYTES = PR * EPI_LD * 4;
   constexpr int SMEM = EPI_BYTES > 2 * STAGE * 2 ? EPI_BYTES : 2 * STAGE * 2;
   // two operand stages (the next k-tile is written into one while the other is consumed);
   // the same memory stages the fp32 result, 128 rows at a time, for the epilogue
@@ -275,11 +309,11 @@ __global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bm, b_bytes);
 
-  f32x16 acc[MI][2];
+  f32x16 acc[MI][NJ];
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
@@ -304,7 +338,7 @@ __global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
 
   const int h = lane >> 5;
   // LDS offsets of this lane's fragment rows (the stage and k-step are added per use)
-  int aoff[MI], boff[2], asw[MI], bsw[2];
+  int aoff[MI], boff[NJ], asw[MI], bsw[NJ];
 #pragma unroll
   for (int i = 0; i < MI; ++i) {
     const int row = wm * (BM / 2) + i * 32 + (lane & 31);
@@ -312,25 +346,51 @@ __global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
     asw[i] = (row ^ (row >> 3)) & 7;
   }
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int row = wn * 64 + j * 32 + (lane & 31);
+  for (int j = 0; j < NJ; ++j) {
+    const int row = wn * (BN / 2) + j * 32 + (lane & 31);
     boff[j] = BM * GK + row * GK;
     bsw[j] = (row ^ (row >> 3)) & 7;
   }
 
-  if (kbeg < kend) {
+  // Software pipeline (two LDS stages, two fragment buffers).  Per k-tile t, k-steps
+  // 0..KS-2 each read the next step's fragments and then issue this step's MFMAs; the
+  // workgroup barrier sits before the last k-step, after which tile t's stage is free for
+  // tile t+2's loads and tile t+1's first fragments are read while the last step's MFMAs
+  // run.  sched_barrier keeps the compiler from sinking the reads to their first use.
+  constexpr int KS = GK / 16;
+  const int ntile = kbeg < kend ? (kend - kbeg + GK - 1) / GK : 0;
+  bf16x8 fa[2][MI], fb[2][NJ];
+  auto read_frags = [&](int s, int ks, int buf) {
+    const bf16_t* St = smem + s * STAGE;
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+      fa[buf][i] = *reinterpret_cast<const bf16x8*>(St + aoff[i] + (((2 * ks + h) ^ asw[i]) << 3));
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      fb[buf][j] = *reinterpret_cast<const bf16x8*>(St + boff[j] + (((2 * ks + h) ^ bsw[j]) << 3));
+  };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+  };
+
+  if (ntile > 0) {
     gload(kbeg, 0);
     lstore(0);
   }
   __builtin_amdgcn_s_waitcnt(0);   // direct LDS loads are counted by vmcnt
   __syncthreads();
-  int it = 0;
-  for (int k0 = kbeg; k0 < kend; k0 += GK, ++it) {
+  if (ntile > 0) read_frags(0, 0, 0);
+  if (ntile > 1) gload(kbeg + GK, 1);
+  __builtin_amdgcn_s_waitcnt(kLgkm0);
+  for (int it = 0; it < ntile; ++it) {
     const int cur = it & 1;
-    const bool more = k0 + GK < kend;
-    if (more) gload(k0 + GK, cur ^ 1);   // in flight while this tile is consumed
-    const bf16_t* St = smem + cur * STAGE;
+    const bool more = it + 1 < ntile;
     if (do_db) {
+      const bf16_t* St = smem + cur * STAGE;
       const int row = threadIdx.x / TPR;
 #pragma unroll
       for (int q = 0; q < 8 / TPR; ++q) {
@@ -340,28 +400,24 @@ __global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
         for (int j = 0; j < 8; ++j) dbacc += bf2f(e[j]);
       }
     }
-    // all fragments of the 64-deep tile are requested before the first MFMA, so the
-    // later k-steps' reads land while the earlier k-steps' MFMAs run
-    bf16x8 a[GK / 16][MI], b[GK / 16][2];
 #pragma unroll
-    for (int ks = 0; ks < GK / 16; ++ks) {
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-        a[ks][i] = *reinterpret_cast<const bf16x8*>(St + aoff[i] + (((2 * ks + h) ^ asw[i]) << 3));
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        b[ks][j] = *reinterpret_cast<const bf16x8*>(St + boff[j] + (((2 * ks + h) ^ bsw[j]) << 3));
+    for (int ks = 0; ks < KS - 1; ++ks) {
+      read_frags(cur, ks + 1, (ks + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      mfmas(ks & 1);
+      __builtin_amdgcn_sched_barrier(0);
     }
-#pragma unroll
-    for (int ks = 0; ks < GK / 16; ++ks)
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][i], b[ks][j], acc[i][j], 0, 0, 0);
     if (more) lstore(cur ^ 1);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of tile it+1 have landed
+    __syncthreads();                 // ... and every wave's; tile it's stage is no longer read
+    if (it + 2 < ntile) gload(kbeg + (it + 2) * GK, cur);
+    if (more) read_frags(cur ^ 1, 0, KS & 1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas((KS - 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
+    // the next tile's first fragments were requested a whole k-step ago: settle them here
+    // so that the top of the loop does not wait for the reads it issues itself
+    __builtin_amdgcn_s_waitcnt(kLgkm0);
   }
 
   if constexpr (EPI == EPI_DW) {
@@ -376,8 +432,9 @@ __global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
 
   // epilogue, PR rows per pass: stage the fp32 result (register r of a 32x32 MFMA tile
   // holds row 8*(r/4) + 4*(lane/32) + r%4, column lane%32), then 4-column chunks per thread
-  constexpr int PR = BM < 128 ? BM : 128;
-  constexpr int NB = PR / 64;   // batches of 8 chunks per thread in a pass
+  constexpr int CPR = BN / 4;                   // 4-column chunks per row
+  constexpr int NB = PR * CPR / (256 * 8);      // batches of 8 chunks per thread in a pass
+  static_assert(NB >= 1 && NB * 256 * 8 == PR * CPR, "epilogue pass shape");
   float* stage = reinterpret_cast<float*>(smem_raw);
 #pragma unroll
   for (int half = 0; half < BM / PR; ++half) {
@@ -385,11 +442,11 @@ __global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int row = wm * (BM / 2) + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3) - half * PR;
-          const int col = wn * 64 + j * 32 + (lane & 31);
+          const int col = wn * (BN / 2) + j * 32 + (lane & 31);
           if (row >= 0 && row < PR) stage[row * EPI_LD + col] = acc[i][j][r];
         }
     __syncthreads();
@@ -399,13 +456,13 @@ __global__ __launch_bounds__(256, BM == 256 ? 1 : 2) void gemm_mfma_kernel(
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const int c = threadIdx.x + 256 * (bch * 8 + q);
-        const int m = m0 + half * PR + (c >> 5), n = n0 + (c & 31) * 4;
+        const int m = m0 + half * PR + c / CPR, n = n0 + (c % CPR) * 4;
         if (m < M && n < N) epi_load<EPI>(ep, m, n, in[q]);
       }
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const int c = threadIdx.x + 256 * (bch * 8 + q);
-        const int row = c >> 5, c4 = (c & 31) * 4;
+        const int row = c / CPR, c4 = (c % CPR) * 4;
         const int m = m0 + half * PR + row, n = n0 + c4;
         float part = 0.f;
         if (m < M && n < N)
@@ -502,12 +559,12 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(const TA* __restrict__
 
 // ============================================================================ dispatch
 
-template <int BM, int EPI, typename T, typename Ta>
-static hipError_t run_mfma_bm(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
-  dim3 grid((g.N + GN - 1) / GN, (g.M + BM - 1) / BM, g.splits);
+template <int BM, int BN, int EPI, typename T, typename Ta>
+static hipError_t run_mfma_tile(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
+  dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, g.splits);
   const int kps = g.splits > 1 ? g.k_per_split : g.K;
 #define SR_GEMM_L(AK, BK)                                                                                         \
-  hipLaunchKernelGGL((gemm_mfma_kernel<BM, AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st, (const bf16_t*)g.A,       \
+  hipLaunchKernelGGL((gemm_mfma_kernel<BM, BN, AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st, (const bf16_t*)g.A,   \
                      (const bf16_t*)g.B, g.M, g.N, g.K, (int)g.lda, (int)g.ldb, (uint32_t)g.a_bytes,              \
                      (uint32_t)g.b_bytes, kps, ep)
   if (g.a_kmajor && g.b_kmajor) SR_GEMM_L(true, true);
@@ -518,16 +575,23 @@ static hipError_t run_mfma_bm(const GemmDesc& g, const EpiArgs& ep, hipStream_t 
   return hipGetLastError();
 }
 
-// Tile height: 128, or 64 when 128-row tiles would leave fewer than two workgroups per CU.
+// Tile shape: 128 x 128, or 64 x 128 when 128 x 128 tiles would leave fewer than two
+// workgroups per CU.
 template <int EPI, typename T, typename Ta>
 static hipError_t run_mfma(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
-  const long tiles128 = (long)((g.N + GN - 1) / GN) * ((g.M + 127) / 128) * g.splits;
-#ifdef SR_GEMM_FORCE_BM
-  if (SR_GEMM_FORCE_BM == 64) return run_mfma_bm<64, EPI, T, Ta>(g, ep, st);
-  return run_mfma_bm<128, EPI, T, Ta>(g, ep, st);
+  const long tiles128 = (long)((g.N + 127) / 128) * ((g.M + 127) / 128) * g.splits;
+#ifdef SR_GEMM_FORCE_TILE
+  // standalone benchmarks: 0 = 64x128, 1 = 128x128, 2 = 256x128, 3 = 128x256, 4 = 256x256
+  switch (SR_GEMM_FORCE_TILE) {
+    case 0: return run_mfma_tile<64, 128, EPI, T, Ta>(g, ep, st);
+    case 1: return run_mfma_tile<128, 128, EPI, T, Ta>(g, ep, st);
+    case 2: return run_mfma_tile<256, 128, EPI, T, Ta>(g, ep, st);
+    case 3: return run_mfma_tile<128, 256, EPI, T, Ta>(g, ep, st);
+    default: return run_mfma_tile<256, 256, EPI, T, Ta>(g, ep, st);
+  }
 #endif
-  if (tiles128 < 512) return run_mfma_bm<64, EPI, T, Ta>(g, ep, st);
-  return run_mfma_bm<128, EPI, T, Ta>(g, ep, st);
+  if (tiles128 < 512) return run_mfma_tile<64, 128, EPI, T, Ta>(g, ep, st);
+  return run_mfma_tile<128, 128, EPI, T, Ta>(g, ep, st);
 }
 
 template <int EPI, typename T, typename Ta, typename TA, typename TB>
