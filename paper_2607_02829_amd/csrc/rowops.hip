@@ -54,27 +54,42 @@ template <int V> SR_DEV void stv(bf16_t* p, const float* v) {
 }
 
 // x: fp32 [M, D]; mod (adaLN): fp32 [B, 6D] with shift at mod_off, scale at mod_off + D.
-template <typename T, typename Ta, int V>
+// One row per wave.  NJC > 0: every lane holds exactly NJC groups of V columns (D = 64 V NJC,
+// all loads unconditional and issued together); NJC = 0: any D <= 64 V kMaxPerLane.
+template <typename T, typename Ta, int V, int NJC>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x, const T* __restrict__ gamma,
                                                      const T* __restrict__ beta, const float* __restrict__ mod,
                                                      int mod_off, int M, int S, int D, float eps,
                                                      Ta* __restrict__ y, float* __restrict__ mean_out,
                                                      float* __restrict__ rstd_out) {
-  constexpr int NJ = kMaxPerLane / V;
+  constexpr int NJ = NJC > 0 ? NJC : kMaxPerLane / V;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
-  const int n = D / (64 * V);
+  const int n = NJC > 0 ? NJC : D / (64 * V);
   const float* xr = x + (size_t)row * D;
-  float v[NJ][V];
-  float s = 0.f;
+  const int b = row / S;
+  const float* shift = mod ? mod + (size_t)b * 6 * D + mod_off : nullptr;
+  float v[NJ][V], w[NJ][V], bb[NJ][V];
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
     if (j < n) {
-      ldv<V>(xr + col_of<V>(lane, j), v[j]);
+      const int c = col_of<V>(lane, j);
+      ldv<V>(xr + c, v[j]);
+      if (mod) {
+        ldv<V>(shift + D + c, w[j]);
+        ldv<V>(shift + c, bb[j]);
+      } else {
+        ldv<V>(gamma + c, w[j]);
+        ldv<V>(beta + c, bb[j]);
+      }
+    }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    if (j < n)
 #pragma unroll
       for (int e = 0; e < V; ++e) s += v[j][e];
-    }
   const float mean = wave_sum(s) / (float)D;
   float q = 0.f;
 #pragma unroll
@@ -84,25 +99,13 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
       for (int e = 0; e < V; ++e) { const float d = v[j][e] - mean; q += d * d; }
   const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
   Ta* yr = y + (size_t)row * D;
-  const int b = row / S;
-  const float* shift = mod ? mod + (size_t)b * 6 * D + mod_off : nullptr;
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
     if (j < n) {
-      const int c = col_of<V>(lane, j);
-      float w[V], bb[V], o[V];
-      if (mod) {
-        ldv<V>(shift + D + c, w);
-        ldv<V>(shift + c, bb);
+      float o[V];
 #pragma unroll
-        for (int e = 0; e < V; ++e) w[e] += 1.0f;
-      } else {
-        ldv<V>(gamma + c, w);
-        ldv<V>(beta + c, bb);
-      }
-#pragma unroll
-      for (int e = 0; e < V; ++e) o[e] = (v[j][e] - mean) * rstd * w[e] + bb[e];
-      stv<V>(yr + c, o);
+      for (int e = 0; e < V; ++e) o[e] = (v[j][e] - mean) * rstd * (mod ? w[j][e] + 1.0f : w[j][e]) + bb[j][e];
+      stv<V>(yr + col_of<V>(lane, j), o);
     }
   if (lane == 0) { mean_out[row] = mean; rstd_out[row] = rstd; }
 }
@@ -115,18 +118,18 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
 // du to part[(b*nchunk + chunk) * 2D].
 constexpr int kLnBwdRows = 8;
 
-template <typename T, typename Ta, int V>
+template <typename T, typename Ta, int V, int NJC>
 __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ du, const float* __restrict__ x,
                                                      const float* __restrict__ mean, const float* __restrict__ rstd,
                                                      const T* __restrict__ gamma, const float* __restrict__ mod,
                                                      int mod_off, const float* dres, int S, int D, float* dx,
                                                      Ta* __restrict__ dx_act, float* __restrict__ part) {
-  constexpr int NJ = kMaxPerLane / V;
+  constexpr int NJ = NJC > 0 ? NJC : kMaxPerLane / V;
   constexpr int RPW = kLnBwdRows / 4;   // rows per wave
   __shared__ float red[4][2][kMaxPerLane * 64 / 4];   // four waves' partials, 512 columns per pass
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int b = blockIdx.y, chunk = blockIdx.x, nchunk = gridDim.x;
-  const int n = D / (64 * V);
+  const int n = NJC > 0 ? NJC : D / (64 * V);
   const float* scale = mod ? mod + (size_t)b * 6 * D + mod_off + D : nullptr;
   float pg[NJ][V], pb[NJ][V], wt[NJ][V];
 #pragma unroll
@@ -145,7 +148,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ d
     for (int e = 0; e < V; ++e) { pg[j][e] = 0.f; pb[j][e] = 0.f; }
   }
   // this wave's rows (loads of both rows are issued before any reduction)
-  float g[RPW][NJ][V], xv[RPW][NJ][V];
+  float g[RPW][NJ][V], xv[RPW][NJ][V], rv[RPW][NJ][V];
   size_t rows[RPW];
   bool ok[RPW];
 #pragma unroll
@@ -158,6 +161,7 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ d
       if (j < n && ok[rr]) {
         ldv<V>(du + rows[rr] * D + col_of<V>(lane, j), g[rr][j]);
         ldv<V>(x + rows[rr] * D + col_of<V>(lane, j), xv[rr][j]);
+        ldv<V>(dres + rows[rr] * D + col_of<V>(lane, j), rv[rr][j]);
       }
   }
 #pragma unroll
@@ -185,9 +189,8 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ d
       if (j < n) {
         const int c = col_of<V>(lane, j);
         float o[V];
-        ldv<V>(dres + row * D + c, o);
 #pragma unroll
-        for (int e = 0; e < V; ++e) o[e] += (g[rr][j][e] * wt[j][e] - m1 - xv[rr][j][e] * m2) * rs;
+        for (int e = 0; e < V; ++e) o[e] = rv[rr][j][e] + (g[rr][j][e] * wt[j][e] - m1 - xv[rr][j][e] * m2) * rs;
         stv<V>(dx + row * D + c, o);
         if (dx_act) stv<V>(dx_act + row * D + c, o);
       }
@@ -286,8 +289,18 @@ __global__ __launch_bounds__(1024) void reduce_cols_kernel(const float* __restri
   const int nrows = sum_groups ? R * G : R;
   const size_t row0 = sum_groups ? 0 : (size_t)g * R;
   float acc = 0.f;
-  if (c < width)
-    for (int rr = ty; rr < nrows; rr += 16) acc += part[(row0 + rr) * width + c];
+  if (c < width) {
+    // eight loads in flight per thread; the sum order (rr ascending) is fixed
+    int rr = ty;
+    for (; rr + 7 * 16 < nrows; rr += 8 * 16) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = part[(row0 + rr + i * 16) * width + c];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc += v[i];
+    }
+    for (; rr < nrows; rr += 16) acc += part[(row0 + rr) * width + c];
+  }
   red[ty][tx] = acc;
   __syncthreads();
   for (int s = 8; s >= 1; s >>= 1) {
@@ -315,12 +328,19 @@ static inline dim3 grid1d(size_t n, int per) { return dim3((unsigned)((n + per -
 hipError_t launch_ln_fwd(int dtype, const float* x, const void* gamma, const void* beta, const float* mod,
                          int mod_off, int M, int S, int D, float eps, void* y, float* mean, float* rstd,
                          hipStream_t st) {
-#define SR_LNF(T, V)                                                                                            \
-  hipLaunchKernelGGL((ln_fwd_kernel<T, T, V>), grid1d(M, 4), dim3(256), 0, st, x, (const T*)gamma, (const T*)beta, \
-                     mod, mod_off, M, S, D, eps, (T*)y, mean, rstd)
-  const bool v4 = D % 256 == 0;
-  if (dtype == kBF16) { if (v4) SR_LNF(bf16_t, 4); else SR_LNF(bf16_t, 1); }
-  else { if (v4) SR_LNF(float, 4); else SR_LNF(float, 1); }
+#define SR_LNF(T, V, NJC)                                                                                    \
+  hipLaunchKernelGGL((ln_fwd_kernel<T, T, V, NJC>), grid1d(M, 4), dim3(256), 0, st, x, (const T*)gamma,      \
+                     (const T*)beta, mod, mod_off, M, S, D, eps, (T*)y, mean, rstd)
+#define SR_LNF_T(T)                                      \
+  switch (D % 256 == 0 ? D / 256 : 0) {                  \
+    case 1: SR_LNF(T, 4, 1); break;                      \
+    case 2: SR_LNF(T, 4, 2); break;                      \
+    case 4: SR_LNF(T, 4, 4); break;                      \
+    case 8: SR_LNF(T, 4, 8); break;                      \
+    default: if (D % 256 == 0) SR_LNF(T, 4, 0); else SR_LNF(T, 1, 0); \
+  }
+  if (dtype == kBF16) { SR_LNF_T(bf16_t); } else { SR_LNF_T(float); }
+#undef SR_LNF_T
 #undef SR_LNF
   return hipGetLastError();
 }
@@ -331,12 +351,19 @@ hipError_t launch_ln_bwd(int dtype, const float* du, const float* x, const float
                          const void* gamma, const float* mod, int mod_off, const float* dres, int B, int S, int D,
                          float* dx, void* dx_act, float* part, hipStream_t st) {
   dim3 g(ln_bwd_chunks(S), B);
-#define SR_LNB(T, V)                                                                                       \
-  hipLaunchKernelGGL((ln_bwd_kernel<T, T, V>), g, dim3(256), 0, st, du, x, mean, rstd, (const T*)gamma, mod, \
-                     mod_off, dres, S, D, dx, (T*)dx_act, part)
-  const bool v4 = D % 256 == 0;
-  if (dtype == kBF16) { if (v4) SR_LNB(bf16_t, 4); else SR_LNB(bf16_t, 1); }
-  else { if (v4) SR_LNB(float, 4); else SR_LNB(float, 1); }
+#define SR_LNB(T, V, NJC)                                                                                  \
+  hipLaunchKernelGGL((ln_bwd_kernel<T, T, V, NJC>), g, dim3(256), 0, st, du, x, mean, rstd, (const T*)gamma, \
+                     mod, mod_off, dres, S, D, dx, (T*)dx_act, part)
+#define SR_LNB_T(T)                                      \
+  switch (D % 256 == 0 ? D / 256 : 0) {                  \
+    case 1: SR_LNB(T, 4, 1); break;                      \
+    case 2: SR_LNB(T, 4, 2); break;                      \
+    case 4: SR_LNB(T, 4, 4); break;                      \
+    case 8: SR_LNB(T, 4, 8); break;                      \
+    default: if (D % 256 == 0) SR_LNB(T, 4, 0); else SR_LNB(T, 1, 0); \
+  }
+  if (dtype == kBF16) { SR_LNB_T(bf16_t); } else { SR_LNB_T(float); }
+#undef SR_LNB_T
 #undef SR_LNB
   return hipGetLastError();
 }
