@@ -17,7 +17,10 @@
  *    saved activations and scratch space are caller buffers sized by
  *    sr_workspace_bytes / sr_select_scratch_bytes.
  *  - `stream` is a hipStream_t (NULL = the default stream).  Calls enqueue work
- *    on it and return without waiting.
+ *    on it and return without waiting.  The blocks backward also uses one extra
+ *    stream per device (created on the first call, default priority, kept until the
+ *    process ends) for its weight gradients, joined to `stream` through events: all of
+ *    the call's work is complete when later work on `stream` starts.
  *  - Arguments are validated on the host before anything is enqueued; on error
  *    nothing is launched, a non-zero sr_status is returned and sr_last_error()
  *    (thread-local) describes it.  SR_EHIP reports a failed launch.
@@ -193,13 +196,16 @@ SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int3
 
 /* Launch timing for measurement (not needed by the method).  After
  * sr_profile_start, every library launch group whose name contains `name_filter`
- * ("" or NULL = all) is bracketed by HIP events on its own stream.
+ * ("" or NULL = all) is bracketed by HIP events on its own stream.  With no filter the
+ * backward issues its weight-gradient GEMMs on the caller's stream (they normally run on
+ * a second stream of the library, overlapping the rest), so each group is timed alone;
+ * with a filter the overlap stays and the named groups are timed as they run.
  * sr_profile_stop waits for those events, stops recording and writes one line per
  * name: "<name> <launches> <total_ms> <algorithmic_flops> <algorithmic_bytes>\n"
  * into `out` (NUL-terminated, truncated to out_bytes); *needed receives the full
  * size.  Names: select_random, select_topk, gather, scatter_delta, ln_fwd, ln_bwd,
  * gemm_<op> (qkv, o, fc1, fc2, dx_fc2, dx_fc1, dx_o, dx_qkv, dw_<op>), attn_fwd,
- * attn_bwd, colsum, convert, mod. */
+ * attn_bwd_dkv, attn_bwd_dq, attn_bwd_delta, reduce, colsum, convert, mod. */
 SR_API sr_status sr_profile_start(const char* name_filter);
 SR_API sr_status sr_profile_stop(char* out, size_t out_bytes, size_t* needed);
 

@@ -39,6 +39,10 @@ hipEvent_t take_event() {
 }  // namespace
 
 bool profiling() { return g_on; }
+bool profiling_all() {
+  std::lock_guard<std::mutex> lk(g_mu);
+  return g_on && g_filter.empty();
+}
 
 ProfScope::ProfScope(const char* name, double flops, double bytes, hipStream_t st) : st_(st) {
   if (!g_on) return;

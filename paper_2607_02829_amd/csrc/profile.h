@@ -7,6 +7,9 @@
 namespace sr {
 
 bool profiling();
+// Profiling every launch group (no name filter): launches that normally overlap on a
+// second stream are issued on the caller's stream instead, so each group's time is its own.
+bool profiling_all();
 
 class ProfScope {
  public:

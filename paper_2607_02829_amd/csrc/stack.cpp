@@ -13,10 +13,14 @@
 //                                                      rounds to the storage type once)
 // Backward runs the same steps in reverse (dW by split-K GEMMs over tokens with a
 // deterministic partial-sum reduction; bias / LN / modulation gradients by
-// chunked column sums).
+// chunked column sums).  The weight-gradient GEMMs are off the critical path: they run
+// on a second stream of the device, forked from the caller's stream after their inputs
+// are written and joined before those inputs are overwritten (and at the end), so they
+// fill the tails of the dX GEMMs, LayerNorms and attention kernels.
 #include "stack.h"
 
 #include <cmath>
+#include <mutex>
 
 #include "profile.h"
 
@@ -253,6 +257,36 @@ hipError_t zero_f32(float* p, size_t n, hipStream_t st) {
   return p ? launch_fill_f32(p, n, 0.0f, st) : hipSuccess;
 }
 
+// One extra stream per device for the weight-gradient work (default priority; created on
+// first use and kept for the life of the process).
+constexpr int kMaxDevices = 64;
+hipError_t side_stream(hipStream_t* out) {
+  static hipStream_t streams[kMaxDevices] = {};
+  static std::mutex mu;
+  int dev = 0;
+  SR_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!streams[dev]) SR_TRY(hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking));
+  *out = streams[dev];
+  return hipSuccess;
+}
+
+// Events of one backward call: fork (caller stream -> side stream) and the completion of
+// each kind of weight-gradient GEMM (side -> caller).  An event is re-recorded only after
+// the waits on its previous record have been enqueued.
+struct BwdEvents {
+  hipEvent_t fork = nullptr, fc2 = nullptr, fc1 = nullptr, o = nullptr, qkv = nullptr;
+  hipError_t create() {
+    for (hipEvent_t* e : {&fork, &fc2, &fc1, &o, &qkv}) SR_TRY(hipEventCreateWithFlags(e, hipEventDisableTiming));
+    return hipSuccess;
+  }
+  ~BwdEvents() {
+    for (hipEvent_t e : {fork, fc2, fc1, o, qkv})
+      if (e) (void)hipEventDestroy(e);
+  }
+};
+
 }  // namespace
 
 hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, const char* saved,
@@ -267,7 +301,32 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
   const bool ada = d.kind == SR_BLOCK_ADALN;
   const int nln = ln_bwd_chunks(S);
 
+  hipStream_t side = nullptr;
+  BwdEvents ev;
+  bool pending[4] = {false, false, false, false};   // fc2, fc1, o, qkv recorded and not yet waited on
+  hipEvent_t* done[4] = {&ev.fc2, &ev.fc1, &ev.o, &ev.qkv};
+  // side stream: wait for everything issued on st so far, run the weight gradient, signal
+  const bool serial = profiling_all();
+  auto on_side = [&](int kind, auto&& launch) -> hipError_t {
+    if (serial) return launch(st);
+    SR_TRY(hipEventRecord(ev.fork, st));
+    SR_TRY(hipStreamWaitEvent(side, ev.fork, 0));
+    SR_TRY(launch(side));
+    SR_TRY(hipEventRecord(*done[kind], side));
+    pending[kind] = true;
+    return hipSuccess;
+  };
+  // st: wait before overwriting what a weight-gradient GEMM of this kind reads
+  auto join = [&](int kind) -> hipError_t {
+    if (pending[kind]) SR_TRY(hipStreamWaitEvent(st, *done[kind], 0));
+    pending[kind] = false;
+    return hipSuccess;
+  };
+  enum { kFc2 = 0, kFc1 = 1, kO = 2, kQkv = 3 };
+
   auto run = [&]() -> hipError_t {
+    SR_TRY(side_stream(&side));
+    SR_TRY(ev.create());
     // g_res = fp32(dh_out) and, for pre-LN, its activation copy
     {
       ProfScope ps("convert", 0, (double)M * D * (2 * e + 4), st);
@@ -279,13 +338,17 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       const sr_block_grads& g = gr[i];
       if (ada) {
         // MLP-branch gradient dm = dh' * gate2 (activation copy) and dgate2 = sum_s dh' * m_out
+        SR_TRY(join(kO));   // g_act is still read by the previous block's dW_o
         ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
         SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, sc.g_act, (size_t)M * D, s.mod + 5 * D, 6 * D, S, D, nullptr,
                               st));
         SR_TRY(gate_grad(d, sc.g_res, s.m_out, sc.dmod, 5 * D, sc, st));
       }
       // FC2: dW2, db2; dz = (dm W2) * GELU'(z)
-      SR_TRY(weight_grad("gemm_dw_fc2", d, sc.g_act, D, s.gz, F, g.w_fc2, g.b_fc2, sc, st));
+      SR_TRY(on_side(kFc2, [&](hipStream_t ss) {
+        return weight_grad("gemm_dw_fc2", d, sc.g_act, D, s.gz, F, g.w_fc2, g.b_fc2, sc, ss);
+      }));
+      SR_TRY(join(kFc1));   // dz is still read by the previous block's dW_fc1
       {
         GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
         EpiArgs ep; ep.z_in = s.z; ep.out_act = sc.dz; ep.ldo = F;
@@ -293,7 +356,9 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(launch_gemm(gd, EPI_DGELU, ep, st));
       }
       // FC1: dW1, db1; du = dz W1
-      SR_TRY(weight_grad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, g.w_fc1, g.b_fc1, sc, st));
+      SR_TRY(on_side(kFc1, [&](hipStream_t ss) {
+        return weight_grad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, g.w_fc1, g.b_fc1, sc, ss);
+      }));
       {
         GemmDesc gd = desc(d, sc.dz, true, F, (size_t)M * F * e, w.w_fc1, false, D, (size_t)F * D * e, M, D, F);
         EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
@@ -301,6 +366,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
       }
       // LN2 backward: g_res2 = g_res + LN2^T du (pre-LN also writes the activation copy)
+      SR_TRY(join(kFc2));   // g_act is still read by dW_fc2
       {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
@@ -322,7 +388,9 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       }
       // output projection: dWo, dbo; dO = da Wo (with the attention row statistic
       // delta = rowsum(dO * O) per head in the same epilogue when the head dim is 64)
-      SR_TRY(weight_grad("gemm_dw_o", d, sc.g_act, D, s.O, D, g.w_o, g.b_o, sc, st));
+      SR_TRY(on_side(kO, [&](hipStream_t ss) {
+        return weight_grad("gemm_dw_o", d, sc.g_act, D, s.O, D, g.w_o, g.b_o, sc, ss);
+      }));
       const bool fuse_delta = d.dtype == kBF16 && D / d.H == 64;
       {
         GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_o, false, D, (size_t)D * D * e, M, D, D);
@@ -336,9 +404,12 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         ProfScope ps("attn_bwd_delta", 0, (double)M * D * e * 2, st);
         SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, d.B, S, d.H, D / d.H, sc.delta, st));
       }
+      SR_TRY(join(kQkv));   // dqkv is still read by the previous block's dW_qkv
       SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, d.B, S, d.H, D, st));
       // QKV: dWqkv, dbqkv; du = dqkv Wqkv
-      SR_TRY(weight_grad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u1, D, g.w_qkv, g.b_qkv, sc, st));
+      SR_TRY(on_side(kQkv, [&](hipStream_t ss) {
+        return weight_grad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u1, D, g.w_qkv, g.b_qkv, sc, ss);
+      }));
       {
         GemmDesc gd = desc(d, sc.dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,
                            M, D, 3 * D);
@@ -347,6 +418,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
       }
       // LN1 backward: g_res = g_res2 + LN1^T du (pre-LN: plus the activation copy for the next block)
+      if (!ada) SR_TRY(join(kO));   // g_act is still read by dW_o
       {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2,
@@ -385,10 +457,19 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(zero_f32(g.b_ada, (size_t)6 * D, st));
       }
     }
-    ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
-    return launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st);
+    {
+      ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
+      SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
+    }
+    for (int k = 0; k < 4; ++k) SR_TRY(join(k));   // every gradient is complete when st is
+    return hipSuccess;
   };
   hipError_t err = run();
+  if (err != hipSuccess && side) {
+    // leave no weight-gradient work unordered with respect to the caller's stream
+    for (int k = 0; k < 4; ++k)
+      if (pending[k]) (void)hipStreamWaitEvent(st, *done[k], 0);
+  }
   delete[] sv;
   return err;
 }
