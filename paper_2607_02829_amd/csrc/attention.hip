@@ -68,22 +68,15 @@ SR_DEV void zero16(f32x16& a) {
   for (int r = 0; r < 16; ++r) a[r] = 0.f;
 }
 
-// Value of the lane 32 apart, combined: max / sum over the wave's two halves.
-SR_DEV float xmax32(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-SR_DEV float xadd32(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 // LDS tile: 64 rows of 64 bf16 (eight 16-byte chunks); chunk c of row r sits at chunk
 // position c ^ swz(r).  Among any 16 consecutive rows the even ones use eight different
-// positions and so do the odd ones (conflict-free 16-byte fragment reads), and rows 16
-// apart share a swizzle, so fragment addresses of different 16-row groups differ by
-// constants (instruction offsets rather than extra address registers).
-SR_DEV int swz(int row) { return (row >> 1) & 7; }
+// positions and so do the odd ones (conflict-free 16-byte fragment reads); rows r and r+2
+// of each group of four differ in bit 2 of the position, so the four rows x 64 bytes that
+// half a wave's transposed read touches fall in different banks (measured conflict-free
+// for both read kinds, where plain XOR swizzles within 64-byte groups cost one extra pass
+// per transposed read); rows 16 apart share a swizzle, so fragment addresses of different
+// 16-row groups differ by constants (instruction offsets rather than address registers).
+SR_DEV int swz(int row) { return (((row >> 1) & 1) << 2) | ((row >> 2) & 3); }
 SR_DEV int toff(int row, int chunk) { return row * HD + ((chunk ^ swz(row)) << 3); }
 
 // Rows r0..r0+63 of one head (columns base.. of a row-major tensor with row length ld)
@@ -200,10 +193,22 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
     float mx = sc[0];
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[r]);
-    mx = xmax32(mx);
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = ex2((m_run - m_new) * sl2);
-    const float nm = -m_new * sl2;
+    mx = half_pair_max(mx);
+    // lazy rescaling: the reference max m_run moves (and O, l are rescaled) only when a
+    // row's max has grown by more than 8 in exp2 units; otherwise p = 2^((s - m_run) c) <= 256,
+    // and since O and l share the reference the result is the same
+    const float grow = (fmaxf(m_run, mx) - m_run) * sl2;   // +inf on the first unit
+    if (__ballot(grow > 8.0f)) {
+      const float m_ref = grow > 8.0f ? mx : m_run;
+      const float alpha = ex2((m_run - m_ref) * sl2);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      m_run = m_ref;
+    }
+    const float nm = -m_run * sl2;
     bf16x8 pb[2];
     float psum = 0.f;
 #pragma unroll
@@ -212,14 +217,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
       psum += p;
       pb[r >> 3][r & 7] = (__bf16)p;
     }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    if (__ballot(alpha != 1.0f)) {
-#pragma unroll
-      for (int db = 0; db < 2; ++db)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-    }
+    l_run += psum;
     const bf16_t* Vs = smem + s * 2 * TE + TE;
 #pragma unroll
     for (int db = 0; db < 2; ++db)
@@ -255,7 +253,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
 
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();   // every wave is done with the stages before they hold the output
-  const float l_tot = xadd32(l_run);
+  const float l_tot = half_pair_sum(l_run);
   if (h32 == 0 && myq < S) lse[((size_t)b * H + hh) * S + myq] = m_run * sl2 + log2f(l_tot);
   stage_t(smem, o, 1.0f / l_tot, wid, lane);
   __syncthreads();
