@@ -42,11 +42,6 @@ constexpr int KT = 64;       // tile of the streamed dimension
 constexpr int TE = KT * HD;  // bf16 elements of one 64 x 64 tile (8 KB)
 constexpr int NSTG = 3;      // LDS stages
 
-template <int V>
-using IC = std::integral_constant<int, V>;
-
-typedef short v4s __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 SR_DEV bf16x8 zero8() {
   bf16x8 z;
@@ -107,7 +102,6 @@ SR_DEV bf16x8 row_frag(const bf16_t* tile, int r0, int ks) {
 // 4..7 rows k0 + 8 + 4h .. (h = lane / 32).  ds_read_b64_tr_b16 gives lane i of each
 // 16-lane group column i of the four rows addressed by the group (lane s: row s / 4,
 // columns 4 (s % 4) .. + 3).
-SR_DEV v4s ds_tr(const bf16_t* p) { return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p); }
 SR_DEV bf16x8 tr_frag(const bf16_t* tile, int k0, int c0) {
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, s = lane & 15;

@@ -101,3 +101,61 @@ SR_DEV i32x2 buf_load8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
 // LDS address space, for the loads that write LDS directly (buffer_load ... lds) and the
 // transposing LDS reads.
 typedef __attribute__((address_space(3))) void lds_ptr_t;
+
+// Transposing LDS read (ds_read_b64_tr_b16): the 16 lanes of each group address four rows
+// of 16 bf16 (lane s: row s / 4, elements 4 (s % 4) .. + 3) and lane s receives element s of
+// each of the four rows.
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
+SR_DEV v4s ds_tr(const bf16_t* p) { return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p); }
+
+template <int V>
+struct IC {
+  static constexpr int value = V;
+};
+
+// s_waitcnt with vmcnt <= N (buffer loads, including those that write LDS directly) and
+// lgkmcnt = 0 (LDS reads), expcnt untouched.
+template <int N>
+SR_DEV void wait_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | ((N >> 4) << 14));
+}
+
+// ---------------------------------------------------------------- explicit LDS reads
+// Fragment reads written as inline asm: the compiler then does not treat them as LDS
+// accesses that might alias a global->LDS fill still in flight (it would wait for every
+// outstanding fill before each read).  Their completion is not tracked by the compiler
+// either: callers wait with lgkm_wait<N>() and pin the destination registers behind it.
+SR_DEV uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+template <int OFF>
+SR_DEV i32x4 lds_read16(uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  i32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(OFF));
+  return v;
+}
+template <int OFF>
+SR_DEV i32x2 lds_read_tr8(uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  i32x2 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(OFF));
+  return v;
+}
+template <int N>
+SR_DEV void lgkm_wait() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N));
+}
+template <typename V>
+SR_DEV void pin(V& v) {
+  asm volatile("" : "+v"(v));
+}
+
+// Workgroup barrier as inline asm.  The compiler makes every global->LDS fill still in flight
+// complete before a barrier it can see (s_waitcnt vmcnt(0)), which would drain a multi-stage
+// fill pipeline at every tile; callers of this one wait explicitly for exactly the fills (and
+// LDS reads) that must be complete.
+SR_DEV void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }

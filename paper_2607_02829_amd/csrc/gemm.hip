@@ -93,106 +93,11 @@ SR_DEV void epilogue(const EpiArgs& e, int m, int n, float v) {
   } else if constexpr (EPI == EPI_ACT) {
     ((Ta*)e.out_act)[o] = from_f32<Ta>(v);
   } else if constexpr (EPI == EPI_F32) {
-    e.out_f32[(size_t)blockIdx.z * e.split_stride + o] = v;
+    e.out_f32[o] = v;
   } else if constexpr (EPI == EPI_F32_ACC) {
     e.out_f32[o] += v;
   } else if constexpr (EPI == EPI_BIAS_F32) {
     e.out_f32[o] = v + to_f32<T>(((const T*)e.bias)[n]);
-  }
-}
-
-// ============================================================================ MFMA kernel
-
-constexpr int GK = 64;
-// s_waitcnt immediates (vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
-constexpr int kLgkm0 = 0xC07F;   // LDS / scalar-memory counter at zero, the others untouched
-
-// Operand tiles sit in LDS as rows of 64 bf16 (eight 16-byte chunks), unpadded; chunk c
-// of row r is stored at chunk position c ^ ((r ^ (r >> 3)) & 7).  With it, the 16-byte
-// fragment reads of eight consecutive rows, the k-major tile stores (eight chunks of a
-// row) and the transposed 8-byte stores (eight rows 8 apart) all hit distinct banks.
-SR_DEV int lds_off(int row, int chunk) { return row * GK + ((chunk ^ ((row ^ (row >> 3)) & 7)) << 3); }
-
-// Register staging of one R x 64 operand tile (R/32 16-byte vectors per thread).
-template <int R>
-struct TileRegs {
-  i32x4 v[R / 32 > 4 ? R / 32 : 4];   // k-major: R/32 vectors; r-major: 4 per task
-};
-
-// k-major operand: rows r0.., k columns k0..k0+63 of X[r*ld + k].
-template <int R>
-SR_DEV void load_kmajor(TileRegs<R>& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
-#pragma unroll
-  for (int i = 0; i < R / 32; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    const int row = c >> 3, kc = c & 7;
-    const uint32_t off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + kc * 8)) * 2u;
-    t.v[i] = buf_load16(rs, off);
-  }
-}
-template <int R>
-SR_DEV void store_kmajor(const TileRegs<R>& t, bf16_t* lds) {
-#pragma unroll
-  for (int i = 0; i < R / 32; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    *reinterpret_cast<i32x4*>(lds + lds_off(c >> 3, c & 7)) = t.v[i];
-  }
-}
-
-// k-major operand straight from global memory into LDS (buffer_load ... lds, 16 bytes per
-// lane): each wave fills whole 1 KB blocks (eight 128-byte rows), lane l landing at byte 16l
-// of its block, so lane l fetches the logical chunk that the swizzle places at physical
-// chunk l % 8 of row l / 8.  No VGPRs and no LDS-store instructions are involved.
-template <int R>
-SR_DEV void load_kmajor_direct(__amdgpu_buffer_rsrc_t rs, bf16_t* lds, int r0, int k0, int ld) {
-  constexpr int BPW = R / 32;   // 1 KB blocks per wave (four waves)
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-#pragma unroll
-  for (int i = 0; i < BPW; ++i) {
-    const int blk = wid * BPW + i;
-    const int row = blk * 8 + (lane >> 3);
-    const int chunk = (lane & 7) ^ ((row ^ (row >> 3)) & 7);
-    const uint32_t off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + chunk * 8)) * 2u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t*)(lds + blk * 512), 16, off, 0, 0, 0);
-  }
-}
-
-// r-major operand: X[k*ld + r]; a task covers 4 consecutive k x 8 consecutive r and is
-// transposed in registers into eight 4-element k runs (R/128 tasks per thread).
-template <int R>
-SR_DEV void load_rmajor(TileRegs<R>& t, __amdgpu_buffer_rsrc_t rs, int r0, int k0, int ld) {
-  constexpr int NRC = R / 8;
-#pragma unroll
-  for (int p = 0; p < (R + 127) / 128; ++p) {
-    const int task = threadIdx.x + 256 * p;
-    if (R < 128 && task >= 2 * R) break;   // 2R tasks of 4 k x 8 r
-    const int rc = task % NRC, kg = task / NRC;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t off = ((uint32_t)(k0 + kg * 4 + i) * (uint32_t)ld + (uint32_t)(r0 + rc * 8)) * 2u;
-      t.v[p * 4 + i] = buf_load16(rs, off);
-    }
-  }
-}
-template <int R>
-SR_DEV void store_rmajor(const TileRegs<R>& t, bf16_t* lds) {
-  constexpr int NRC = R / 8;
-#pragma unroll
-  for (int p = 0; p < (R + 127) / 128; ++p) {
-    const int task = threadIdx.x + 256 * p;
-    if (R < 128 && task >= 2 * R) break;
-    const int rc = task % NRC, kg = task / NRC;
-    const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 0]);
-    const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 1]);
-    const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 2]);
-    const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&t.v[p * 4 + 3]);
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      i32x2 w;
-      w[0] = (int)((uint32_t)e0[r] | ((uint32_t)e1[r] << 16));
-      w[1] = (int)((uint32_t)e2[r] | ((uint32_t)e3[r] << 16));
-      *reinterpret_cast<i32x2*>(lds + lds_off(rc * 8 + r, kg >> 1) + (kg & 1) * 4) = w;
-    }
   }
 }
 
@@ -257,14 +162,13 @@ SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in)
   } else if constexpr (EPI == EPI_ACT) {
     *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(v);
   } else if constexpr (EPI == EPI_F32) {
-    *reinterpret_cast<f32x4*>(e.out_f32 + (size_t)blockIdx.z * e.split_stride + o) = v;
+    *reinterpret_cast<f32x4*>(e.out_f32 + o) = v;
   } else if constexpr (EPI == EPI_F32_ACC) {
     *reinterpret_cast<f32x4*>(e.out_f32 + o) = in.resid + v;
   } else if constexpr (EPI == EPI_BIAS_F32) {
     *reinterpret_cast<f32x4*>(e.out_f32 + o) = v + b;
   } else if constexpr (EPI == EPI_DW) {
-    float* out = gridDim.z == 1 ? e.out_f32 : e.part + (size_t)blockIdx.z * e.split_stride;
-    *reinterpret_cast<f32x4*>(out + o) = v;
+    *reinterpret_cast<f32x4*>(e.out_f32 + o) = v;   // the split's partial plane when split
   } else if constexpr (EPI == EPI_DO) {
     const i32x2 w = pack4(v);
     *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = w;
@@ -278,34 +182,195 @@ SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in)
   return 0.f;
 }
 
-// BM x BN workgroup tile, four waves in 2 x 2, each (BM/2) x (BN/2), i.e. MI x NJ MFMA tiles
-// of 32 x 32 (MI = BM/64, NJ = BN/64).  A wave reads (MI + NJ) KB of fragments from LDS per
-// MI * NJ MFMAs, so the big tiles (one workgroup per CU, accumulators in AGPRs) need half the
-// LDS bandwidth of 128 x 128 per MFMA; 128 x 128 and 64 x 128 keep two workgroups per CU and
-// enough tiles for narrow outputs.
-template <int BM, int BN, bool AK, bool BK, int EPI, typename T, typename Ta>
-__global__ __launch_bounds__(256, BM * BN >= 256 * 128 ? 1 : 2) void gemm_mfma_kernel(
-    const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bm, int M, int N, int Kd, int lda, int ldb,
-    uint32_t a_bytes, uint32_t b_bytes, int k_per_split, EpiArgs ep) {
-  constexpr int MI = BM / 64 > 0 ? BM / 64 : 1;
-  constexpr int NJ = BN / 64;
+// ============================================================================ MFMA kernel
+
+constexpr int GK = 64;        // k extent of an operand tile
+constexpr int KS = GK / 16;   // MFMA k-steps per tile
+
+// LDS layouts of an operand tile (16-byte chunks of eight bf16 at XOR-swizzled positions):
+//  k-major, R rows x 64 k: row r holds its 64 k values, chunk c at position c ^ kswz(r).  The
+//    fragment reads (16 lanes: one chunk of 16 consecutive rows) hit distinct banks.
+//  r-major, 64 k-rows x R: k-row k holds R consecutive r values, chunk c at c ^ rswz(k).
+//    Fragments come from ds_read_b64_tr_b16; the four k-rows x 32 bytes that half a wave
+//    touches per read sit in four different 64-byte bank groups.
+// Both are filled by whole 1 KB blocks of contiguous LDS, so the fills are conflict-free.
+SR_DEV int kswz(int r) { return (r ^ (r >> 3)) & 7; }
+template <int R>
+SR_DEV int rswz(int k) {
+  return R >= 128 ? (k & 3) << 2 : ((k >> 1) & 1) << 2;
+}
+
+// One operand tile (R rows or r-columns, k0 .. k0+63) straight from global memory into LDS
+// (buffer_load ... lds, 16 bytes per lane, no VGPRs): each wave fills whole 1 KB blocks and
+// lane l lands at byte 16 l of its block, so it fetches the chunk the swizzle places there.
+// Offsets at or past the operand's extent read as zero.
+template <int R, bool KMAJ>
+SR_DEV void fill_tile(__amdgpu_buffer_rsrc_t rs, bf16_t* lds, int r0, int k0, int ld, bool valid) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  constexpr int BPW = R / 32;   // the tile is R/8 blocks, four waves
+#pragma unroll
+  for (int i = 0; i < BPW; ++i) {
+    const int blk = wid * BPW + i;
+    uint32_t off;
+    if constexpr (KMAJ) {
+      const int row = blk * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ kswz(row);
+      off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + c * 8)) * 2u;
+    } else {
+      constexpr int CPR = R / 8, RPB = 64 / CPR;   // chunks per k-row, k-rows per block
+      const int k = blk * RPB + lane / CPR;
+      const int c = (lane % CPR) ^ rswz<R>(k);
+      off = ((uint32_t)(k0 + k) * (uint32_t)ld + (uint32_t)(r0 + c * 8)) * 2u;
+    }
+    // a fill past the last k-tile keeps the count of loads in flight uniform: it reads
+    // beyond every operand's extent (2 GiB at most), which returns zeros without a memory access
+    if (!valid) off = 0x80000000u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t*)(lds + blk * 512), 16, off, 0, 0, 0);
+  }
+}
+
+// Workgroups are handed to the eight XCDs round-robin by linear id.  Renumber them so that each
+// XCD owns a contiguous range of tiles, and walk tiles in groups of GM tile rows (column by
+// column within a group), so the tiles that one XCD runs together share A rows and B columns in
+// its L2.  Split-K index outermost.
+constexpr int GM = 8;
+SR_DEV void tile_coords(int bid, int nwg, int tiles_m, int tiles_n, int& tm, int& tn, int& split) {
+  const int x = bid & 7, q = nwg >> 3, rem = nwg & 7;
+  const int t = x * q + min(x, rem) + (bid >> 3);
+  const int per = tiles_m * tiles_n;
+  split = t / per;
+  const int u = t - split * per;
+  const int grp = u / (GM * tiles_n);
+  const int first = grp * GM;
+  const int gm = min(GM, tiles_m - first);
+  const int v = u - first * tiles_n;
+  tm = first + v % gm;
+  tn = v / gm;
+}
+
+template <int N, typename F>
+SR_DEV void static_for(F&& f) {
+  if constexpr (N > 0) {
+    static_for<N - 1>(f);
+    f(IC<N - 1>{});
+  }
+}
+
+// Explicit LDS reads at a compile-time byte offset (the 16-bit instruction offset field takes
+// what fits, the rest is added to the address).
+template <int OFF>
+SR_DEV i32x4 rd16(uint32_t a) {
+  constexpr int HI = OFF & ~0xFFFF;
+  return lds_read16<OFF - HI>(a + HI);
+}
+template <int OFF>
+SR_DEV i32x2 rdtr(uint32_t a) {
+  constexpr int HI = OFF & ~0xFFFF;
+  return lds_read_tr8<OFF - HI>(a + HI);
+}
+
+// Raw fragment as the explicit reads deliver it: one 16-byte read (k-major) or two 8-byte
+// transposing reads (r-major).  The registers are written asynchronously, so nothing may touch
+// them before lgkm_wait: settle() pins each destination behind the wait and only then joins the
+// halves into the MFMA operand.
+template <bool KMAJ>
+struct RawFrag;
+template <>
+struct RawFrag<true> {
+  i32x4 v;
+  SR_DEV bf16x8 settle() {
+    pin(v);
+    return __builtin_bit_cast(bf16x8, v);
+  }
+};
+template <>
+struct RawFrag<false> {
+  i32x2 lo, hi;
+  SR_DEV bf16x8 settle() {
+    pin(lo);
+    pin(hi);
+    i32x4 w;
+    w[0] = lo[0]; w[1] = lo[1]; w[2] = hi[0]; w[3] = hi[1];
+    return __builtin_bit_cast(bf16x8, w);
+  }
+};
+
+// Per-lane LDS byte addresses of one operand's fragments (stage 0, k-step 0 for r-major).
+//  k-major: rows rb + 32 p + lane % 32 (p = 0, 1; rows 64 apart share the swizzle), one address
+//    per k-step (the swizzle does not add).
+//  r-major: r-columns rb + 32 i + ..., one address per i (k-steps and the second read of a
+//    fragment are constant offsets: the swizzle depends on k % 4 only).
+template <int R, bool KMAJ, int NI>
+struct FragAddr {
+  uint32_t a[KMAJ ? 2 : NI][KMAJ ? KS : 1];
+  SR_DEV void init(uint32_t base, int rb, int lane) {
+    const int h = lane >> 5;
+    if constexpr (KMAJ) {
+#pragma unroll
+      for (int p = 0; p < (NI > 1 ? 2 : 1); ++p) {
+        const int r = rb + 32 * p + (lane & 31);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) a[p][ks] = base + (uint32_t)(r * GK + (((2 * ks + h) ^ kswz(r)) << 3)) * 2u;
+      }
+    } else {
+      const int g = lane >> 4, s = lane & 15;
+      const int k1 = 8 * (g >> 1) + (s >> 2);
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int col = rb + 32 * i + 16 * (g & 1) + 4 * (s & 3);
+        a[i][0] = base + (uint32_t)(k1 * R + (((col >> 3) ^ rswz<R>(k1)) << 3) + (col & 7)) * 2u;
+      }
+    }
+  }
+  // fragment I at k-step KSV, byte offset OFF (stage and operand position): rows (or r-columns)
+  // rb + 32 I + lane % 32, k = 16 KSV + 8 h .. + 7
+  template <int I, int KSV, int OFF>
+  SR_DEV void read(RawFrag<KMAJ>& f) const {
+    if constexpr (KMAJ) {
+      f.v = rd16<OFF + (I >> 1) * 64 * GK * 2>(a[I & 1][KSV]);
+    } else {
+      f.lo = rdtr<OFF + KSV * 16 * R * 2>(a[I][0]);
+      f.hi = rdtr<OFF + KSV * 16 * R * 2 + 4 * R * 2>(a[I][0]);
+    }
+  }
+  static constexpr int kReads = KMAJ ? NI : 2 * NI;   // LDS instructions per k-step
+};
+
+// BM x BN workgroup tile, four waves in 2 x 2, each (BM/2) x (BN/2) = MI x NJ MFMA tiles of
+// 32 x 32 (v_mfma_f32_32x32x16_bf16).  NST operand stages in LDS.  Per k-tile t: k-steps
+// 0..KS-2 read the next step's fragments and issue this step's MFMAs; then the wait for tile
+// t+1's fill and the workgroup barrier, after which tile t's stage takes tile t+NST and tile
+// t+1's first fragments are read while the last k-step's MFMAs run.  Fills are issued NST-1
+// tiles ahead; fragment reads are explicit (see lds_read16), so no read waits for a fill it
+// does not need.  OCC workgroups share a CU: with two, one workgroup's epilogue (GELU math,
+// output stores) overlaps the other's MFMAs.
+template <int BM, int BN, int NST, int OCC, bool AK, bool BK, int EPI, typename T, typename Ta>
+__global__ __launch_bounds__(256, OCC) void gemm_mfma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bm,
+                                                           int M, int N, int Kd, int lda, int ldb, uint32_t a_bytes,
+                                                           uint32_t b_bytes, int k_per_split, int tiles_m, int tiles_n,
+                                                           EpiArgs ep) {
+  constexpr int MI = BM / 64, NJ = BN / 64;
   static_assert(BM == 64 || BM == 128 || BM == 256, "tile height");
   static_assert(BN == 128 || BN == 256, "tile width");
-  constexpr int GN = BN;
-  constexpr int STAGE = (BM + BN) * GK;   // bf16 elements of one LDS stage (A tile then B tile)
-  constexpr int EPI_LD = BN + 8;          // fp32 row stride of the epilogue staging tile
-  constexpr int PR = BN == 256 ? (BM < 64 ? BM : 64) : (BM < 128 ? BM : 128);   // rows per pass
-  constexpr int EPI_BYTES = PR * EPI_LD * 4;
-  constexpr int SMEM = EPI_BYTES > 2 * STAGE * 2 ? EPI_BYTES : 2 * STAGE * 2;
-  // two operand stages (the next k-tile is written into one while the other is consumed);
-  // the same memory stages the fp32 result, 128 rows at a time, for the epilogue
-  __shared__ __attribute__((aligned(16))) char smem_raw[SMEM];
-  bf16_t* smem = reinterpret_cast<bf16_t*>(smem_raw);
+  static_assert(NST >= 2 && NST <= 4, "stages");
+  constexpr int STAGE = (BM + BN) * GK;   // bf16 elements: A tile, then B tile
+  constexpr int SB = STAGE * 2;           // bytes of a stage
+  constexpr int LPT = (BM + BN) / 32;     // fill instructions per thread per tile
+  static_assert((NST - 1) * LPT < 64, "loads in flight exceed the vmcnt range");
+  using FA = FragAddr<BM, AK, MI>;
+  using FB = FragAddr<BN, BK, NJ>;
+  constexpr int RPK = FA::kReads + FB::kReads;   // LDS reads per k-step
+  static_assert(RPK < 16, "reads per k-step exceed the lgkmcnt range");
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[NST * STAGE];
+
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int wm = wid >> 1, wn = wid & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * GN;
-  const int kbeg = blockIdx.z * k_per_split;
+  const int wm = wid >> 1, wn = wid & 1, h = lane >> 5;
+  int tm, tn, split;
+  tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn, split);
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kbeg = split * k_per_split;
   const int kend = min(Kd, kbeg + k_per_split);
+  const int ntile = kbeg < kend ? (kend - kbeg + GK - 1) / GK : 0;
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(Bm, b_bytes);
 
@@ -317,173 +382,187 @@ __global__ __launch_bounds__(256, BM * BN >= 256 * 128 ? 1 : 2) void gemm_mfma_k
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // k-major operands go global -> LDS directly; r-major ones through registers (transposed)
-  TileRegs<BM> ta;
-  TileRegs<GN> tb;
-  auto gload = [&](int k0, int s) {
+  auto fill = [&](int t, int s) {
     bf16_t* st = smem + s * STAGE;
-    if constexpr (AK) load_kmajor_direct<BM>(ra, st, m0, k0, lda); else load_rmajor<BM>(ta, ra, m0, k0, lda);
-    if constexpr (BK) load_kmajor_direct<GN>(rb, st + BM * GK, n0, k0, ldb); else load_rmajor<GN>(tb, rb, n0, k0, ldb);
+    const bool valid = t < ntile;
+    fill_tile<BM, AK>(ra, st, m0, kbeg + t * GK, lda, valid);
+    fill_tile<BN, BK>(rb, st + BM * GK, n0, kbeg + t * GK, ldb, valid);
   };
-  auto lstore = [&](int s) {
-    bf16_t* st = smem + s * STAGE;
-    if constexpr (!AK) store_rmajor<BM>(ta, st);
-    if constexpr (!BK) store_rmajor<GN>(tb, st + BM * GK);
+  const uint32_t sbase = lds_addr(smem);
+  FA fad;
+  FB fbd;
+  fad.init(sbase, wm * (BM / 2), lane);
+  fbd.init(sbase + BM * GK * 2, wn * (BN / 2), lane);
+  RawFrag<AK> fa[2][MI];
+  RawFrag<BK> fb[2][NJ];
+  bf16x8 ua[MI], ub[NJ];   // settled operands of the k-step being multiplied
+  // fragments of k-step KSV of stage S into buffer BUF
+  auto read = [&](auto sidx, auto ksv, auto buf) {
+    constexpr int S = decltype(sidx)::value, KSV = decltype(ksv)::value, BUF = decltype(buf)::value;
+    static_for<MI>([&](auto i) { fad.template read<i.value, KSV, S * SB>(fa[BUF][i.value]); });
+    static_for<NJ>([&](auto j) { fbd.template read<j.value, KSV, S * SB>(fb[BUF][j.value]); });
   };
-
-  // EPI_DW: the first column of tiles also sums its A rows (bias gradient)
-  constexpr int TPR = 256 / BM;   // threads per A row for those sums
-  const bool do_db = EPI == EPI_DW && ep.db_out != nullptr && blockIdx.x == 0;
-  float dbacc = 0.f;
-
-  const int h = lane >> 5;
-  // LDS offsets of this lane's fragment rows (the stage and k-step are added per use)
-  int aoff[MI], boff[NJ], asw[MI], bsw[NJ];
+  // after the wait: pin the buffer's registers and form the MFMA operands
+  auto settle = [&](int buf) {
 #pragma unroll
-  for (int i = 0; i < MI; ++i) {
-    const int row = wm * (BM / 2) + i * 32 + (lane & 31);
-    aoff[i] = row * GK;
-    asw[i] = (row ^ (row >> 3)) & 7;
-  }
+    for (int i = 0; i < MI; ++i) ua[i] = fa[buf][i].settle();
 #pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const int row = wn * (BN / 2) + j * 32 + (lane & 31);
-    boff[j] = BM * GK + row * GK;
-    bsw[j] = (row ^ (row >> 3)) & 7;
-  }
-
-  // Software pipeline (two LDS stages, two fragment buffers).  Per k-tile t, k-steps
-  // 0..KS-2 each read the next step's fragments and then issue this step's MFMAs; the
-  // workgroup barrier sits before the last k-step, after which tile t's stage is free for
-  // tile t+2's loads and tile t+1's first fragments are read while the last step's MFMAs
-  // run.  sched_barrier keeps the compiler from sinking the reads to their first use.
-  constexpr int KS = GK / 16;
-  const int ntile = kbeg < kend ? (kend - kbeg + GK - 1) / GK : 0;
-  bf16x8 fa[2][MI], fb[2][NJ];
-  auto read_frags = [&](int s, int ks, int buf) {
-    const bf16_t* St = smem + s * STAGE;
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
-      fa[buf][i] = *reinterpret_cast<const bf16x8*>(St + aoff[i] + (((2 * ks + h) ^ asw[i]) << 3));
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      fb[buf][j] = *reinterpret_cast<const bf16x8*>(St + boff[j] + (((2 * ks + h) ^ bsw[j]) << 3));
+    for (int j = 0; j < NJ; ++j) ub[j] = fb[buf][j].settle();
   };
-  auto mfmas = [&](int buf) {
+  auto mfmas = [&]() {
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ua[i], ub[j], acc[i][j], 0, 0, 0);
   };
 
-  if (ntile > 0) {
-    gload(kbeg, 0);
-    lstore(0);
-  }
-  __builtin_amdgcn_s_waitcnt(0);   // direct LDS loads are counted by vmcnt
-  __syncthreads();
-  if (ntile > 0) read_frags(0, 0, 0);
-  if (ntile > 1) gload(kbeg + GK, 1);
-  __builtin_amdgcn_s_waitcnt(kLgkm0);
-  for (int it = 0; it < ntile; ++it) {
-    const int cur = it & 1;
-    const bool more = it + 1 < ntile;
-    if (do_db) {
-      const bf16_t* St = smem + cur * STAGE;
-      const int row = threadIdx.x / TPR;
+  // EPI_DW bias gradient: row sums of A (r-major there: k-rows of BM values).  The tile row's
+  // tiles_n workgroups share the work: workgroup tn sums the k-tiles t with t % tiles_n == tn.
+  // Thread: chunk position cp of k-rows kg, kg + KG, ...; eight running sums.
+  constexpr int CPR = BM / 8, KG = 256 / CPR;
+  const bool want_db = EPI == EPI_DW && ep.db_out != nullptr;
+  float dbv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const uint32_t db_addr = sbase + (uint32_t)(((threadIdx.x / CPR) * BM + (threadIdx.x % CPR) * 8) * 2);
+  auto db_sum = [&](auto sidx) {
+    constexpr int S = decltype(sidx)::value;
+    i32x4 w[64 / KG];
+    static_for<64 / KG>([&](auto j) { w[j.value] = rd16<S * SB + j.value * KG * BM * 2>(db_addr); });
+    lgkm_wait<0>();
 #pragma unroll
-      for (int q = 0; q < 8 / TPR; ++q) {
-        i32x4 v = *reinterpret_cast<const i32x4*>(St + lds_off(row, (threadIdx.x % TPR) * (8 / TPR) + q));
-        const bf16_t* e = reinterpret_cast<const bf16_t*>(&v);
+    for (int j = 0; j < 64 / KG; ++j) {
+      pin(w[j]);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) dbacc += bf2f(e[j]);
+      for (int q = 0; q < 4; ++q) {
+        dbv[2 * q] += __uint_as_float((uint32_t)w[j][q] << 16);
+        dbv[2 * q + 1] += __uint_as_float((uint32_t)w[j][q] & 0xFFFF0000u);
       }
     }
-#pragma unroll
-    for (int ks = 0; ks < KS - 1; ++ks) {
-      read_frags(cur, ks + 1, (ks + 1) & 1);
+  };
+
+  // prologue: tiles 0..NST-1 in flight (fills past the last k-tile read zeros), wait for tile 0
+  fill(0, 0);
+  fill(1, 1);
+  if constexpr (NST > 2) fill(2, 2);
+  if constexpr (NST > 3) fill(3, 3);
+  wait_vm_lgkm0<(NST - 1) * LPT>();
+  lds_barrier();
+  read(IC<0>{}, IC<0>{}, IC<0>{});
+
+  auto body = [&](int t, auto sidx) {
+    constexpr int S = decltype(sidx)::value;
+    if (want_db && t % tiles_n == tn) db_sum(sidx);
+    static_for<KS - 1>([&](auto ksv) {
+      constexpr int ks = decltype(ksv)::value;
+      read(sidx, IC<ks + 1>{}, IC<(ks + 1) & 1>{});
+      lgkm_wait<RPK>();   // this k-step's fragments (read one step earlier) have arrived
+      settle(ks & 1);
       __builtin_amdgcn_sched_barrier(0);
-      mfmas(ks & 1);
+      mfmas();
       __builtin_amdgcn_sched_barrier(0);
-    }
-    if (more) lstore(cur ^ 1);
-    __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of tile it+1 have landed
-    __syncthreads();                 // ... and every wave's; tile it's stage is no longer read
-    if (it + 2 < ntile) gload(kbeg + (it + 2) * GK, cur);
-    if (more) read_frags(cur ^ 1, 0, KS & 1);
+    });
+    // tile t+1 resident (its fill is the oldest still in flight: every body issues exactly
+    // one), every wave done reading tile t's stage
+    wait_vm_lgkm0<(NST - 2) * LPT>();
+    lds_barrier();
+    settle((KS - 1) & 1);
+    fill(t + NST, S);
+    read(IC<(S + 1) % NST>{}, IC<0>{}, IC<KS & 1>{});   // unused past the last tile
     __builtin_amdgcn_sched_barrier(0);
-    mfmas((KS - 1) & 1);
+    mfmas();
     __builtin_amdgcn_sched_barrier(0);
-    // the next tile's first fragments were requested a whole k-step ago: settle them here
-    // so that the top of the loop does not wait for the reads it issues itself
-    __builtin_amdgcn_s_waitcnt(kLgkm0);
+  };
+  for (int t = 0; t < ntile; t += NST) {
+    body(t, IC<0>{});
+    if (t + 1 < ntile) body(t + 1, IC<1 % NST>{});
+    if constexpr (NST > 2)
+      if (t + 2 < ntile) body(t + 2, IC<2 % NST>{});
+    if constexpr (NST > 3)
+      if (t + 3 < ntile) body(t + 3, IC<3 % NST>{});
   }
+  // the last body read the next tile's first fragments, which nothing uses: keep their
+  // registers allocated until the reads have landed, or the late writes could clobber
+  // whatever the compiler puts there next
+  lgkm_wait<0>();
+  settle(KS & 1);
+  wait_vm_lgkm0<0>();
+  __syncthreads();   // stages free for the epilogue
 
   if constexpr (EPI == EPI_DW) {
+    if (want_db) {
+      // combine the KG partial sums of each row through LDS, in k-group order
+      float* red = reinterpret_cast<float*>(smem);   // [KG][BM]
+      const int cp = threadIdx.x % CPR, kg = threadIdx.x / CPR;
+      const int lc = cp ^ rswz<BM>(kg);   // logical chunk this thread summed
 #pragma unroll
-    for (int o = 1; o < TPR; o <<= 1) dbacc += __shfl_xor(dbacc, o, 64);
-    const int dbrow = m0 + (int)threadIdx.x / TPR;
-    if (do_db && (threadIdx.x % TPR) == 0 && dbrow < M) {
-      if (gridDim.z == 1) ep.db_out[dbrow] = dbacc;
-      else ep.dbpart[(size_t)blockIdx.z * M + dbrow] = dbacc;
+      for (int e = 0; e < 8; ++e) red[kg * BM + lc * 8 + e] = dbv[e];
+      __syncthreads();
+      if ((int)threadIdx.x < BM) {
+        float sum = 0.f;
+        for (int g = 0; g < KG; ++g) sum += red[g * BM + threadIdx.x];
+        const int row = m0 + threadIdx.x;
+        const int nparts = gridDim.x / (tiles_m * tiles_n) * tiles_n;
+        if (row < M) {
+          if (nparts == 1) ep.db_out[row] = sum;
+          else ep.dbpart[(size_t)(split * tiles_n + tn) * M + row] = sum;
+        }
+      }
+      __syncthreads();
     }
   }
 
-  // epilogue, PR rows per pass: stage the fp32 result (register r of a 32x32 MFMA tile
-  // holds row 8*(r/4) + 4*(lane/32) + r%4, column lane%32), then 4-column chunks per thread
-  constexpr int CPR = BN / 4;                   // 4-column chunks per row
-  constexpr int NB = PR * CPR / (256 * 8);      // batches of 8 chunks per thread in a pass
-  static_assert(NB >= 1 && NB * 256 * 8 == PR * CPR, "epilogue pass shape");
-  float* stage = reinterpret_cast<float*>(smem_raw);
+  // epilogue, 32 rows per pass (one i-block of one wave row): stage the fp32 result (register r
+  // of a 32 x 32 MFMA tile holds row 8 (r/4) + 4 h + r%4, column lane%32), then 4-column chunks
+  if constexpr (EPI == EPI_DW)
+    if (gridDim.x > (unsigned)(tiles_m * tiles_n)) ep.out_f32 = ep.part + (size_t)split * ep.split_stride;
+  constexpr int PR = 32;
+  constexpr int EPI_LD = BN + 8;   // fp32 row stride: the two halves of a wave hit disjoint banks
+  constexpr int CPRo = BN / 4;     // 4-column chunks per row
+  constexpr int NB = PR * CPRo / 256;
+  static_assert(PR * EPI_LD * 4 <= NST * SB, "epilogue staging exceeds the stages");
+  float* stg = reinterpret_cast<float*>(smem);
 #pragma unroll
-  for (int half = 0; half < BM / PR; ++half) {
-    if (half) __syncthreads();
-#pragma unroll
-    for (int i = 0; i < MI; ++i)
+  for (int p = 0; p < BM / PR; ++p) {
+    if (p) __syncthreads();
+    if (wm == p / MI) {
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = wm * (BM / 2) + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3) - half * PR;
-          const int col = wn * (BN / 2) + j * 32 + (lane & 31);
-          if (row >= 0 && row < PR) stage[row * EPI_LD + col] = acc[i][j][r];
-        }
+        for (int r = 0; r < 16; ++r)
+          stg[(8 * (r >> 2) + 4 * h + (r & 3)) * EPI_LD + wn * (BN / 2) + j * 32 + (lane & 31)] = acc[p % MI][j][r];
+    }
     __syncthreads();
+    EpiIn in[NB];
 #pragma unroll
-    for (int bch = 0; bch < NB; ++bch) {
-      EpiIn in[8];
+    for (int q = 0; q < NB; ++q) {
+      const int c = threadIdx.x + 256 * q;
+      const int m = m0 + p * PR + c / CPRo, n = n0 + (c % CPRo) * 4;
+      if (m < M && n < N) epi_load<EPI>(ep, m, n, in[q]);
+    }
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int c = threadIdx.x + 256 * (bch * 8 + q);
-        const int m = m0 + half * PR + c / CPR, n = n0 + (c % CPR) * 4;
-        if (m < M && n < N) epi_load<EPI>(ep, m, n, in[q]);
-      }
+    for (int q = 0; q < NB; ++q) {
+      const int c = threadIdx.x + 256 * q;
+      const int row = c / CPRo, c4 = (c % CPRo) * 4;
+      const int m = m0 + p * PR + row, n = n0 + c4;
+      float part = 0.f;
+      if (m < M && n < N)
+        part = epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stg + row * EPI_LD + c4), in[q]);
+      if constexpr (EPI == EPI_DO) {
+        // the 16 lanes (tid % 16) of one head's 64 columns: butterfly within the group
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int c = threadIdx.x + 256 * (bch * 8 + q);
-        const int row = c / CPR, c4 = (c % CPR) * 4;
-        const int m = m0 + half * PR + row, n = n0 + c4;
-        float part = 0.f;
-        if (m < M && n < N)
-          part = epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stage + row * EPI_LD + c4), in[q]);
-        if constexpr (EPI == EPI_DO) {
-          // the 16 lanes (tid % 16) of one head's 64 columns: butterfly within the group
-#pragma unroll
-          for (int o = 8; o >= 1; o >>= 1) part += __shfl_xor(part, o, 64);
-          if ((threadIdx.x & 15) == 0 && m < M && n < N)
-            ep.delta[((size_t)(m / ep.S) * ep.H + (n >> 6)) * ep.S + (m % ep.S)] = part;
-        }
+        for (int o = 8; o >= 1; o >>= 1) part += __shfl_xor(part, o, 64);
+        if ((threadIdx.x & 15) == 0 && m < M && n < N)
+          ep.delta[((size_t)(m / ep.S) * ep.H + (n >> 6)) * ep.S + (m % ep.S)] = part;
       }
     }
   }
 }
 
 // Sum of split-K partial planes, in split order: out[i] = sum_z part[z * n + i] (float4 lanes),
-// and likewise for the bias-gradient partials.
+// and of the bias-gradient partial rows: dbout[c] = sum_z dbpart[z * nb + c].
 __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, int splits, size_t n4,
                                                             float* __restrict__ out, const float* __restrict__ dbpart,
-                                                            int nb, float* __restrict__ dbout) {
+                                                            int dbparts, int nb, float* __restrict__ dbout) {
   const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (i < n4) {
     const f32x4* p = reinterpret_cast<const f32x4*>(part);
@@ -493,17 +572,18 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
   } else if (dbout && i - n4 < (size_t)nb) {
     const size_t c = i - n4;
     float s = dbpart[c];
-    for (int z = 1; z < splits; ++z) s += dbpart[(size_t)z * nb + c];
+    for (int z = 1; z < dbparts; ++z) s += dbpart[(size_t)z * nb + c];
     dbout[c] = s;
   }
 }
 
-hipError_t launch_reduce_splits(const float* part, int splits, size_t n, float* out, const float* dbpart, int nb,
-                                float* dbout, hipStream_t st) {
-  const size_t n4 = n / 4;
+static hipError_t launch_reduce(const float* part, int splits, size_t n, float* out, const float* dbpart, int dbparts,
+                                int nb, float* dbout, hipStream_t st) {
+  const size_t n4 = splits > 1 ? n / 4 : 0;
   const size_t total = n4 + (dbout ? nb : 0);
+  if (total == 0) return hipSuccess;
   hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, part, splits, n4,
-                     out, dbpart, nb, dbout);
+                     out, dbpart, dbparts, nb, dbout);
   return hipGetLastError();
 }
 
@@ -559,14 +639,17 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(const TA* __restrict__
 
 // ============================================================================ dispatch
 
-template <int BM, int BN, int EPI, typename T, typename Ta>
-static hipError_t run_mfma_tile(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
-  dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM, g.splits);
-  const int kps = g.splits > 1 ? g.k_per_split : g.K;
-#define SR_GEMM_L(AK, BK)                                                                                         \
-  hipLaunchKernelGGL((gemm_mfma_kernel<BM, BN, AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st, (const bf16_t*)g.A,   \
-                     (const bf16_t*)g.B, g.M, g.N, g.K, (int)g.lda, (int)g.ldb, (uint32_t)g.a_bytes,              \
-                     (uint32_t)g.b_bytes, kps, ep)
+// Tile shapes of the MFMA kernel, with the stage count that fits the 160 KB of LDS.
+enum TileShape { T256x256 = 0, T256x128 = 1, T128x256 = 2, T128x128 = 3, T64x128 = 4, T128x128x2 = 5 };
+
+template <int BM, int BN, int NST, int OCC, int EPI, typename T, typename Ta>
+static hipError_t run_mfma_tile(const GemmDesc& g, const EpiArgs& ep, int splits, int kps, hipStream_t st) {
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  const dim3 grid((unsigned)(tiles_m * tiles_n * splits));
+#define SR_GEMM_L(AK, BK)                                                                                        \
+  hipLaunchKernelGGL((gemm_mfma_kernel<BM, BN, NST, OCC, AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st,            \
+                     (const bf16_t*)g.A, (const bf16_t*)g.B, g.M, g.N, g.K, (int)g.lda, (int)g.ldb,               \
+                     (uint32_t)g.a_bytes, (uint32_t)g.b_bytes, kps, tiles_m, tiles_n, ep)
   if (g.a_kmajor && g.b_kmajor) SR_GEMM_L(true, true);
   else if (g.a_kmajor && !g.b_kmajor) SR_GEMM_L(true, false);
   else if (!g.a_kmajor && !g.b_kmajor) SR_GEMM_L(false, false);
@@ -575,23 +658,70 @@ static hipError_t run_mfma_tile(const GemmDesc& g, const EpiArgs& ep, hipStream_
   return hipGetLastError();
 }
 
-// Tile shape: 128 x 128, or 64 x 128 when 128 x 128 tiles would leave fewer than two
-// workgroups per CU.
+template <int EPI, typename T, typename Ta>
+static hipError_t run_shape(int shape, const GemmDesc& g, const EpiArgs& ep, int splits, int kps, hipStream_t st) {
+  switch (shape) {
+    case T256x128: return run_mfma_tile<256, 128, 3, 1, EPI, T, Ta>(g, ep, splits, kps, st);
+    case T128x256: return run_mfma_tile<128, 256, 3, 1, EPI, T, Ta>(g, ep, splits, kps, st);
+    case T128x128: return run_mfma_tile<128, 128, 4, 1, EPI, T, Ta>(g, ep, splits, kps, st);
+    case T128x128x2: return run_mfma_tile<128, 128, 2, 2, EPI, T, Ta>(g, ep, splits, kps, st);
+    default: return run_mfma_tile<64, 128, 4, 1, EPI, T, Ta>(g, ep, splits, kps, st);
+  }
+}
+
+static int shape_bm(int s) { return s == T256x256 || s == T256x128 ? 256 : s == T64x128 ? 64 : 128; }
+static int shape_occ(int s) { return s == T128x128x2 ? 2 : 1; }
+static int shape_bn(int s) { return s == T256x256 || s == T128x256 ? 256 : 128; }
+
+// Tile shape by the number of 128 x 128 output tiles (measured on the block's GEMMs at 4050
+// tokens on MI355X): many tiles -> two 128 x 128 workgroups per CU (one's epilogue overlaps the
+// other's MFMAs); about one per CU -> one workgroup with a four-stage pipeline; fewer -> 64 x 128
+// tiles so that the grid still covers the CUs.  The 256 x 128 shapes measured slower throughout
+// and stay available to the benchmarks only.
+static int pick_shape(int M, int N, int splits) {
+  const long tiles = (long)((M + 127) / 128) * ((N + 127) / 128) * splits;
+  if (tiles >= 384) return T128x128x2;
+  if (tiles >= 192) return T128x128;
+  return T64x128;
+}
+
+#ifdef SR_GEMM_FORCE_SHAPE
+int g_force_shape = -1;   // standalone benchmarks: >= 0 overrides the choice
+#endif
+
 template <int EPI, typename T, typename Ta>
 static hipError_t run_mfma(const GemmDesc& g, const EpiArgs& ep, hipStream_t st) {
-  const long tiles128 = (long)((g.N + 127) / 128) * ((g.M + 127) / 128) * g.splits;
-#ifdef SR_GEMM_FORCE_TILE
-  // standalone benchmarks: 0 = 64x128, 1 = 128x128, 2 = 256x128, 3 = 128x256, 4 = 256x256
-  switch (SR_GEMM_FORCE_TILE) {
-    case 0: return run_mfma_tile<64, 128, EPI, T, Ta>(g, ep, st);
-    case 1: return run_mfma_tile<128, 128, EPI, T, Ta>(g, ep, st);
-    case 2: return run_mfma_tile<256, 128, EPI, T, Ta>(g, ep, st);
-    case 3: return run_mfma_tile<128, 256, EPI, T, Ta>(g, ep, st);
-    default: return run_mfma_tile<256, 256, EPI, T, Ta>(g, ep, st);
-  }
+  const int splits = g.splits > 1 ? g.splits : 1;
+  const int kps = splits > 1 ? g.k_per_split : g.K;
+  int shape = pick_shape(g.M, g.N, splits);
+#ifdef SR_GEMM_FORCE_SHAPE
+  if (g_force_shape >= 0) shape = g_force_shape;
 #endif
-  if (tiles128 < 512) return run_mfma_tile<64, 128, EPI, T, Ta>(g, ep, st);
-  return run_mfma_tile<128, 128, EPI, T, Ta>(g, ep, st);
+  return run_shape<EPI, T, Ta>(shape, g, ep, splits, kps, st);
+}
+
+// Weight gradient (EPI_DW; reduction over tokens, both operands r-major): shape and split-K
+// factor.  Few output tiles are split over tokens so that the grid covers the GPU; each split
+// writes a partial plane that one reduction adds in split order.
+struct DwPlan {
+  int shape, splits, kps, tiles_n;
+};
+static DwPlan dw_plan(int M, int N, int K) {
+  DwPlan p;
+  p.shape = pick_shape(M, N, 1);
+#ifdef SR_GEMM_FORCE_SHAPE
+  if (g_force_shape >= 0) p.shape = g_force_shape;
+#endif
+  const int bm = shape_bm(p.shape), bn = shape_bn(p.shape);
+  const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+  int sp = (int)(256 * shape_occ(p.shape) / tiles);   // one round of workgroups at most
+  sp = std::min(sp, std::max(1, K / 512));
+  sp = std::max(1, std::min(sp, 8));
+  p.kps = ((K + sp - 1) / sp + GK - 1) / GK * GK;
+  p.splits = (K + p.kps - 1) / p.kps;
+  if (p.splits <= 1) { p.splits = 1; p.kps = K; }
+  p.tiles_n = (N + bn - 1) / bn;
+  return p;
 }
 
 template <int EPI, typename T, typename Ta, typename TA, typename TB>
@@ -627,10 +757,38 @@ hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_
     case EPI_F32: return dispatch<EPI_F32>(g, ep, st);
     case EPI_F32_ACC: return dispatch<EPI_F32_ACC>(g, ep, st);
     case EPI_BIAS_F32: return dispatch<EPI_BIAS_F32>(g, ep, st);
-    case EPI_DW: return dispatch<EPI_DW>(g, ep, st);
+    case EPI_DW: return g.use_mfma ? hipErrorInvalidValue : dispatch<EPI_DW>(g, ep, st);   // launch_weight_grad
     case EPI_DO: return g.use_mfma ? run_mfma<EPI_DO, bf16_t, bf16_t>(g, ep, st) : hipErrorInvalidValue;
   }
   return hipErrorInvalidValue;
+}
+
+void weight_grad_scratch(int M, int N, int K, size_t* part_floats, size_t* dbpart_floats) {
+  const DwPlan p = dw_plan(M, N, K);
+  *part_floats = p.splits > 1 ? (size_t)p.splits * M * N : 0;
+  *dbpart_floats = (size_t)p.splits * p.tiles_n * M;
+}
+
+hipError_t launch_weight_grad(const GemmDesc& g, float* dw, float* db, float* part, float* dbpart, hipStream_t st) {
+  EpiArgs ep;
+  ep.ldo = g.N;
+  if (!g.use_mfma) {
+    ep.out_f32 = dw;
+    ep.db_out = db;
+    return dispatch<EPI_DW>(g, ep, st);
+  }
+  const DwPlan p = dw_plan(g.M, g.N, g.K);
+  const int nparts = p.splits * p.tiles_n;
+  ep.out_f32 = dw;
+  ep.part = part;
+  ep.split_stride = (long long)g.M * g.N;
+  ep.db_out = db;
+  ep.dbpart = dbpart;
+  hipError_t e = run_shape<EPI_DW, bf16_t, bf16_t>(p.shape, g, ep, p.splits, p.kps, st);
+  if (e != hipSuccess) return e;
+  if (p.splits > 1 || (db && nparts > 1))
+    return launch_reduce(part, p.splits, (size_t)g.M * g.N, dw, dbpart, nparts, g.M, nparts > 1 ? db : nullptr, st);
+  return hipSuccess;
 }
 
 }  // namespace sr

@@ -38,8 +38,9 @@ struct EpiArgs {
   int S = 1;                    // rows per sample (gate indexing)
   long long split_stride = 0;   // element stride between split-K partial outputs
   // EPI_DW (weight gradient, reduction over tokens): out_f32 receives dW and db_out (optional)
-  // the row sums of A (the bias gradient); with split-K each split writes its plane of
-  // part / dbpart instead and launch_reduce_splits adds them in split order.
+  // the row sums of A (the bias gradient); with split-K each split writes its plane of part,
+  // and the bias-gradient sums are spread over the workgroups of a tile row (dbpart rows), so
+  // launch_weight_grad adds the partial planes and rows in a fixed order.
   float* db_out = nullptr;
   float* part = nullptr;
   float* dbpart = nullptr;
@@ -91,8 +92,10 @@ hipError_t launch_attn_delta(int dtype, const void* dO, const void* O, int B, in
                              hipStream_t st);
 
 hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_t st);
-hipError_t launch_reduce_splits(const float* part, int splits, size_t n, float* out, const float* dbpart, int nb,
-                                float* dbout, hipStream_t st);
+// Weight gradient dW[M x N] = sum_k A(m, k) B(n, k) over tokens k (both operands token-major)
+// and db[m] = sum_k A(m, k) (optional).  part / dbpart: scratch of the sizes below.
+hipError_t launch_weight_grad(const GemmDesc& g, float* dw, float* db, float* part, float* dbpart, hipStream_t st);
+void weight_grad_scratch(int M, int N, int K, size_t* part_floats, size_t* dbpart_floats);
 
 bool attn_uses_mfma(int dtype, int hd);
 hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int B, int S, int H, int D,

@@ -95,14 +95,6 @@ size_t layout_saved(const Dims& d, char* base, BlockSaved* out) {
   return c.off;
 }
 
-int dw_splits(const Dims& d, int N, int K) {
-  if (d.dtype != kBF16) return 1;
-  const int tiles = ((N + 127) / 128) * ((K + 127) / 128);
-  int s = (512 + tiles - 1) / tiles;
-  s = std::min(s, std::max(1, d.M / 512));
-  return std::max(1, std::min(s, 16));
-}
-
 size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   Carver c(base);
   const size_t M = d.M, D = d.D, F = d.F, e = d.elt;
@@ -111,16 +103,17 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   s.g_res2 = c.take<float>(M * D * 4);
   s.du = c.take<float>(M * D * 4);
   s.delta = c.take<float>((size_t)d.B * d.H * d.S * 4);
-  size_t wp = 0;
+  size_t wp = 0, dbp = 0, wmax_out = 0;
   const int shapes[4][2] = {{3 * d.D, d.D}, {d.D, d.D}, {d.F, d.D}, {d.D, d.F}};
   for (auto& sh : shapes) {
-    const int sp = dw_splits(d, sh[0], sh[1]);
-    if (sp > 1) wp = std::max(wp, (size_t)sp * sh[0] * sh[1]);
+    size_t pf = 0, df = 0;
+    if (d.dtype == kBF16) weight_grad_scratch(sh[0], sh[1], d.M, &pf, &df);
+    wp = std::max(wp, pf);
+    dbp = std::max(dbp, df);
+    wmax_out = std::max(wmax_out, (size_t)sh[0] * sh[1]);
   }
-  size_t wmax_out = 0;
-  for (auto& sh : shapes) wmax_out = std::max(wmax_out, (size_t)sh[0] * sh[1]);
   s.wpart = c.take<float>((wp + wmax_out) * 4);   // split partials, then room for an unwanted dW
-  s.dbpart = c.take<float>((size_t)16 * std::max<size_t>(3 * D, F) * 4);
+  s.dbpart = c.take<float>(std::max<size_t>(dbp, 1) * 4);
   const size_t wmax = std::max<size_t>(std::max<size_t>(3 * D, F), 6 * D);
   s.part = c.take<float>((size_t)d.B * colsum_chunks(d.S) * wmax * 4);
   s.lnpart = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
@@ -213,36 +206,17 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
 namespace {
 
 // dW[N x K] = sum_m dY[m, n] X[m, k] and db[n] = sum_m dY[m, n], both operands token-major
-// ([M, N] and [M, K]).  Split-K over tokens when the output has few tiles: each split
-// writes a partial plane and one reduction adds them in split order (deterministic).
+// ([M, N] and [M, K]); the GEMM layer picks the tile shape and any split over tokens.
 hipError_t weight_grad(const char* name, const Dims& d, const void* dY, int N, const void* X, int K, float* out,
                        float* db, const Scratch& sc, hipStream_t st) {
   if (!out && !db) return hipSuccess;
   const size_t e = d.elt;
   GemmDesc g = desc(d, dY, false, N, (size_t)d.M * N * e, X, false, K, (size_t)d.M * K * e, N, K, d.M);
-  EpiArgs ep;
-  ep.ldo = K;
-  float* dw = out ? out : sc.wpart;   // the kernel always produces dW; park an unwanted one in scratch
-  ep.out_f32 = dw;
-  ep.db_out = db;
-  const int sp = dw_splits(d, N, K);
-  if (sp > 1) {
-    g.k_per_split = ((d.M + sp - 1) / sp + 63) / 64 * 64;
-    g.splits = (d.M + g.k_per_split - 1) / g.k_per_split;
-    if (!out) dw = sc.wpart + (size_t)g.splits * N * K;   // beyond the partials
-    ep.part = sc.wpart;
-    ep.dbpart = sc.dbpart;
-    ep.split_stride = (long long)N * K;
-  }
-  {
-    ProfScope ps(name, gemm_flops(N, K, d.M), gemm_bytes(d, N, K, d.M, 4), st);
-    SR_TRY(launch_gemm(g, EPI_DW, ep, st));
-  }
-  if (g.splits > 1) {
-    ProfScope ps("reduce", 0, (double)(g.splits + 1) * N * K * 4, st);
-    SR_TRY(launch_reduce_splits(sc.wpart, g.splits, (size_t)N * K, dw, sc.dbpart, N, db, st));
-  }
-  return hipSuccess;
+  size_t pf = 0, df = 0;
+  if (g.use_mfma) weight_grad_scratch(N, K, d.M, &pf, &df);
+  float* dw = out ? out : sc.wpart + pf;   // the kernel always produces dW; park an unwanted one in scratch
+  ProfScope ps(name, gemm_flops(N, K, d.M), gemm_bytes(d, N, K, d.M, 4), st);
+  return launch_weight_grad(g, dw, db, sc.wpart, sc.dbpart, st);
 }
 
 // dmod[b, off + c] = sum_s X[b,s,c] * Y[b,s,c]  (adaLN gate gradients)

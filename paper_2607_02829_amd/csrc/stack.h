@@ -29,9 +29,6 @@ struct Scratch {
 size_t layout_saved(const Dims& d, char* base, BlockSaved* out /* [nb] or null */);
 size_t layout_scratch(const Dims& d, char* base, Scratch* out /* or null */);
 
-// Split-K factor of the weight-gradient GEMM producing an N x K result.
-int dw_splits(const Dims& d, int N, int K);
-
 hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, const void* h_in, void* h_out,
                      char* saved, hipStream_t st);
 hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, const char* saved,
