@@ -79,17 +79,21 @@ SR_DEV int toff(int row, int chunk) { return row * HD + ((chunk ^ swz(row)) << 3
 // byte 16 l of its block, so it fetches the chunk that the swizzle places there.  Rows past
 // the sample's S tokens are read without a guard: they belong to the next sample (finite
 // values the callers mask) or lie past the tensor, where the buffer load returns zero.
-SR_DEV void tile_load(__amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t ld, int r0, bf16_t* dst) {
+SR_DEV void tile_load(__amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t ld, int r0, bf16_t* dst, bool valid = true) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int blk = wid * 2 + i;
     const int row = blk * 8 + (lane >> 3);
     const int c = (lane & 7) ^ swz(row);
-    const uint32_t off = base + ((uint32_t)(r0 + row) * ld + (uint32_t)c * 8u) * 2u;
+    uint32_t off = base + ((uint32_t)(r0 + row) * ld + (uint32_t)c * 8u) * 2u;
+    // a load past the last tile keeps the number of loads in flight uniform: it reads beyond
+    // every tensor's extent (2 GiB at most), which returns zeros without a memory access
+    if (!valid) off = 0x80000000u;
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t*)(dst + blk * 512), 16, off, 0, 0, 0);
   }
 }
+constexpr int kTileLoads = 2;   // buffer loads per thread of one tile_load
 
 // Fragment of the 32 rows r0.. (MFMA row index = lane % 32), k-step ks of the 64 columns.
 SR_DEV bf16x8 row_frag(const bf16_t* tile, int r0, int ks) {
@@ -116,6 +120,50 @@ SR_DEV bf16x8 tr_frag(const bf16_t* tile, int k0, int c0) {
   w[3] = __builtin_bit_cast(i32x2, hi)[1];
   return __builtin_bit_cast(bf16x8, w);
 }
+
+// Explicit fragment reads (see lds_read16) from one LDS array of NSTG stages, each holding two
+// 64 x 64 tiles (tile p of stage s at byte offset (2 s + p) TB): per-lane base addresses are
+// fixed, and the stage, tile, row-group and k-step offsets are instruction immediates.  The
+// compiler then neither waits for fills in flight into other stages nor keeps per-stage
+// address registers; the kernels wait (lgkm_wait) before using what they read.
+constexpr int TB = TE * 2;    // bytes of one tile
+constexpr int SGB = 2 * TB;   // bytes of one stage
+
+// Row fragment: MFMA row index = tile row R0 + lane % 32 (R0 a multiple of 16, which keeps
+// the swizzle), k-step KSV of the 64 columns.
+struct RowAddr {
+  uint32_t a[4];
+  SR_DEV void init(uint32_t base, int lane) {
+    const int l32 = lane & 31, h = lane >> 5;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) a[ks] = base + (uint32_t)(l32 * HD + (((2 * ks + h) ^ swz(l32)) << 3)) * 2u;
+  }
+  template <int OFF, int R0, int KSV>
+  SR_DEV void read(RawFrag<true>& f) const {
+    f.v = rd16<OFF + R0 * HD * 2>(a[KSV]);
+  }
+};
+
+// Transposed fragment (as tr_frag): MFMA row index = tile column 32 DB + lane % 32, k = tile
+// rows K0 + 4 h .. + 3 (first read) and K0 + 8 + 4 h .. + 3 (second read), K0 a multiple of 16.
+struct TrAddr {
+  uint32_t a[2][2];
+  SR_DEV void init(uint32_t base, int lane) {
+    const int g = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int db = 0; db < 2; ++db) {
+      const int col = 32 * db + 16 * (g & 1) + 4 * (s & 3);
+      const int r1 = 4 * (g >> 1) + (s >> 2), r2 = r1 + 8;
+      a[db][0] = base + (uint32_t)(r1 * HD + (((col >> 3) ^ swz(r1)) << 3) + (col & 7)) * 2u;
+      a[db][1] = base + (uint32_t)(r2 * HD + (((col >> 3) ^ swz(r2)) << 3) + (col & 7)) * 2u;
+    }
+  }
+  template <int OFF, int K0, int DB>
+  SR_DEV void read(RawFrag<false>& f) const {
+    f.lo = rdtr<OFF + K0 * HD * 2>(a[DB][0]);
+    f.hi = rdtr<OFF + K0 * HD * 2>(a[DB][1]);
+  }
+};
 
 // Row index (within a 32-row unit) of score register r of this lane.
 SR_DEV int srow(int r, int h32) { return 8 * (r >> 2) + 4 * h32 + (r & 3); }
@@ -157,21 +205,19 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
   const uint32_t kbase = (uint32_t)(((size_t)b * S * ld + D + hh * HD) * 2);
   const uint32_t vbase = kbase + (uint32_t)D * 2u;
+  RowAddr ra;
+  TrAddr ta;
+  ra.init(lds_addr(smem), lane);
+  ta.init(lds_addr(smem), lane);
 
   bf16x8 qf[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) qf[ks] = myq < S ? ld8(qp + (size_t)myq * ld + ks * 16 + 8 * h32) : zero8();
 
+  constexpr int kLoads = 2 * kTileLoads;   // per thread per tile
   auto load = [&](int t, int s) {
-    tile_load(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE);
-    tile_load(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE);
-  };
-  // S^T of key unit u (32 keys) of the tile in stage s: register r holds key srow(r), query l32
-  auto scores = [&](int s, int u, f32x16& sc) {
-    const bf16_t* Ks = smem + s * 2 * TE;
-    zero16(sc);
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) sc = mfma(row_frag(Ks, u * 32, ks), qf[ks], sc);
+    tile_load(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE, t < nt);
+    tile_load(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE, t < nt);
   };
   auto mask = [&](f32x16& sc, int k0) {   // keys past S do not exist
 #pragma unroll
@@ -182,8 +228,27 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
   f32x16 o[2];
   zero16(o[0]); zero16(o[1]);
   float m_run = -INFINITY, l_run = 0.f;   // running max of the raw scores, partial sum (this half's keys)
-  // online softmax of one unit, then O^T += V^T P^T
-  auto consume = [&](int s, int u, const f32x16& sc) {
+  // K row fragments of key unit U of stage SG
+  auto read_k = [&](auto sg, auto uu, RawFrag<true> (&kr)[4]) {
+    constexpr int SG = decltype(sg)::value, U = decltype(uu)::value;
+    static_for<4>([&](auto ks) { ra.template read<SG * SGB, U * 32, decltype(ks)::value>(kr[ks.value]); });
+  };
+  // S^T = K Q^T of a unit: register r holds key srow(r), query l32
+  auto scores = [&](RawFrag<true> (&kr)[4], f32x16& sc) {
+    zero16(sc);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) sc = mfma(kr[ks].settle(), qf[ks], sc);
+  };
+  // online softmax of unit U, then O^T += V^T P^T (V^T fragments read first, so that their
+  // latency hides behind the arithmetic)
+  auto consume = [&](auto sg, auto uu, const f32x16& sc) {
+    constexpr int SG = decltype(sg)::value, U = decltype(uu)::value;
+    RawFrag<false> vt[2][2];
+    static_for<2>([&](auto db) {
+      static_for<2>([&](auto kk) {
+        ta.template read<SG * SGB + TB, U * 32 + decltype(kk)::value * 16, decltype(db)::value>(vt[db.value][kk.value]);
+      });
+    });
     float mx = sc[0];
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[r]);
@@ -212,29 +277,34 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
       pb[r >> 3][r & 7] = (__bf16)p;
     }
     l_run += psum;
-    const bf16_t* Vs = smem + s * 2 * TE + TE;
+    lgkm_wait<0>();
 #pragma unroll
     for (int db = 0; db < 2; ++db)
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) o[db] = mfma(tr_frag(Vs, u * 32 + kk * 16, db * 32), pb[kk], o[db]);
+      for (int kk = 0; kk < 2; ++kk) o[db] = mfma(vt[db][kk].settle(), pb[kk], o[db]);
   };
 
   load(0, 0);
-  if (nt > 1) load(1, 1);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  load(1, 1);   // past the last tile: zeros (a uniform count of loads in flight)
+  wait_vm_lgkm0<kLoads>();
+  lds_barrier();
   auto tile = [&](int t, auto stg) {
-    constexpr int s0 = decltype(stg)::value, s2 = (s0 + 2) % NSTG;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      f32x16 sc;
-      scores(s0, u, sc);
-      if (ragged && t + 1 == nt && S - t * KT < (u + 1) * 32) mask(sc, t * KT + u * 32);
-      consume(s0, u, sc);
-    }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();   // tile t+1 resident; tile t's stage no longer read
-    if (t + 2 < nt) load(t + 2, s2);
+    constexpr int s0 = decltype(stg)::value;
+    const bool rag = ragged && t + 1 == nt;
+    RawFrag<true> k0r[4], k1r[4];
+    f32x16 sc0, sc1;
+    read_k(stg, IC<0>{}, k0r);
+    lgkm_wait<0>();
+    scores(k0r, sc0);
+    read_k(stg, IC<1>{}, k1r);   // lands while unit 0's softmax runs
+    if (rag && S - t * KT < 32) mask(sc0, t * KT);
+    consume(stg, IC<0>{}, sc0);   // its final wait also covers unit 1's K reads
+    scores(k1r, sc1);
+    if (rag && S - t * KT < 64) mask(sc1, t * KT + 32);
+    consume(stg, IC<1>{}, sc1);
+    wait_vm_lgkm0<kLoads>();   // tile t+1 resident (tile t+2's loads may still fly)
+    lds_barrier();             // every wave done with tile t's stage
+    load(t + 2, (s0 + 2) % NSTG);
   };
   int t = 0;
   for (; t + NSTG <= nt; t += NSTG) {
@@ -409,23 +479,39 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
   const uint32_t kbase = (uint32_t)(((size_t)b * S * ld + D + hh * HD) * 2);
   const uint32_t vbase = kbase + (uint32_t)D * 2u;
+  RowAddr ra;
+  TrAddr ta;
+  ra.init(lds_addr(smem), lane);
+  ta.init(lds_addr(smem), lane);
+  constexpr int kLoads = 2 * kTileLoads;   // per thread per tile
   auto load = [&](int t, int s) {
-    tile_load(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE);
-    tile_load(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE);
+    tile_load(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE, t < nt);
+    tile_load(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE, t < nt);
   };
-  // S^T = K Q^T and dP^T = V dO^T of key unit u: register r holds key srow(r), query l32
-  auto sd = [&](int s, int u, f32x16& sv, f32x16& dpv) {
-    const bf16_t* Ks = smem + s * 2 * TE;
-    const bf16_t* Vs = Ks + TE;
+  // K (tile 0) or V (tile 1) row fragments of key unit U of stage SG
+  auto read_rows = [&](auto sg, auto uu, auto tl, RawFrag<true> (&fr)[4]) {
+    constexpr int SG = decltype(sg)::value, U = decltype(uu)::value, TL = decltype(tl)::value;
+    static_for<4>([&](auto ks) { ra.template read<SG * SGB + TL * TB, U * 32, decltype(ks)::value>(fr[ks.value]); });
+  };
+  // S^T = K Q^T and dP^T = V dO^T of a key unit: register r holds key srow(r), query l32
+  auto sd = [&](RawFrag<true> (&kr)[4], RawFrag<true> (&vr)[4], f32x16& sv, f32x16& dpv) {
     zero16(sv); zero16(dpv);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
-      sv = mfma(row_frag(Ks, u * 32, ks), qf[ks], sv);
-      dpv = mfma(row_frag(Vs, u * 32, ks), df[ks], dpv);
+      sv = mfma(kr[ks].settle(), qf[ks], sv);
+      dpv = mfma(vr[ks].settle(), df[ks], dpv);
     }
   };
-  // dS^T of the unit (keys past S do not exist), then dQ^T += K^T dS^T
-  auto grad = [&](int s, int u, const f32x16& sv, const f32x16& dpv, int k0, auto rag) {
+  // dS^T of unit U (keys past S do not exist), then dQ^T += K^T dS^T (K^T fragments read
+  // first, so that their latency hides behind the arithmetic)
+  auto grad = [&](auto sg, auto uu, const f32x16& sv, const f32x16& dpv, int k0, auto rag) {
+    constexpr int SG = decltype(sg)::value, U = decltype(uu)::value;
+    RawFrag<false> fk[2][2];
+    static_for<2>([&](auto db) {
+      static_for<2>([&](auto kk) {
+        ta.template read<SG * SGB, U * 32 + decltype(kk)::value * 16, decltype(db)::value>(fk[db.value][kk.value]);
+      });
+    });
     bf16x8 sb[2];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -436,31 +522,37 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
       }
       sb[r >> 3][r & 7] = (__bf16)ds;
     }
-    __builtin_amdgcn_sched_barrier(0);   // as in the dK/dV kernel
-    const bf16_t* Ks = smem + s * 2 * TE;
+    lgkm_wait<0>();
 #pragma unroll
     for (int db = 0; db < 2; ++db)
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) dq[db] = mfma(tr_frag(Ks, u * 32 + kk * 16, db * 32), sb[kk], dq[db]);
+      for (int kk = 0; kk < 2; ++kk) dq[db] = mfma(fk[db][kk].settle(), sb[kk], dq[db]);
   };
 
   load(0, 0);
-  if (nt > 1) load(1, 1);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
+  load(1, 1);   // past the last tile: zeros (a uniform count of loads in flight)
+  wait_vm_lgkm0<kLoads>();
+  lds_barrier();
   auto tile = [&](int t, auto stg) {
-    constexpr int s0 = decltype(stg)::value, s2 = (s0 + 2) % NSTG;
+    constexpr int s0 = decltype(stg)::value;
     const bool rag = ragged && t + 1 == nt;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      f32x16 sv, dpv;
-      sd(s0, u, sv, dpv);
-      if (rag) grad(s0, u, sv, dpv, t * KT + u * 32, std::true_type{});
-      else grad(s0, u, sv, dpv, t * KT + u * 32, std::false_type{});
-    }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();   // tile t+1 resident; tile t's stage no longer read
-    if (t + 2 < nt) load(t + 2, s2);
+    RawFrag<true> k0r[4], v0r[4], k1r[4], v1r[4];
+    f32x16 sv0, dp0, sv1, dp1;
+    read_rows(stg, IC<0>{}, IC<0>{}, k0r);
+    read_rows(stg, IC<0>{}, IC<1>{}, v0r);
+    lgkm_wait<0>();
+    sd(k0r, v0r, sv0, dp0);
+    read_rows(stg, IC<1>{}, IC<0>{}, k1r);   // unit 1's K rows land while unit 0's arithmetic runs
+    if (rag) grad(stg, IC<0>{}, sv0, dp0, t * KT, std::true_type{});
+    else grad(stg, IC<0>{}, sv0, dp0, t * KT, std::false_type{});   // its wait covers them
+    read_rows(stg, IC<1>{}, IC<1>{}, v1r);
+    lgkm_wait<0>();
+    sd(k1r, v1r, sv1, dp1);
+    if (rag) grad(stg, IC<1>{}, sv1, dp1, t * KT + 32, std::true_type{});
+    else grad(stg, IC<1>{}, sv1, dp1, t * KT + 32, std::false_type{});
+    wait_vm_lgkm0<kLoads>();   // tile t+1 resident (tile t+2's loads may still fly)
+    lds_barrier();             // every wave done with tile t's stage
+    load(t + 2, (s0 + 2) % NSTG);
   };
   int t = 0;
   for (; t + NSTG <= nt; t += NSTG) {

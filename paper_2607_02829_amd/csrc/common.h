@@ -114,6 +114,14 @@ struct IC {
   static constexpr int value = V;
 };
 
+template <int N, typename F>
+SR_DEV void static_for(F&& f) {
+  if constexpr (N > 0) {
+    static_for<N - 1>(f);
+    f(IC<N - 1>{});
+  }
+}
+
 // s_waitcnt with vmcnt <= N (buffer loads, including those that write LDS directly) and
 // lgkmcnt = 0 (LDS reads), expcnt untouched.
 template <int N>
@@ -144,6 +152,19 @@ SR_DEV i32x2 lds_read_tr8(uint32_t a) {
   asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(OFF));
   return v;
 }
+// Explicit LDS reads at a compile-time byte offset (the 16-bit instruction offset field takes
+// what fits, the rest is added to the address).
+template <int OFF>
+SR_DEV i32x4 rd16(uint32_t a) {
+  constexpr int HI = OFF & ~0xFFFF;
+  return lds_read16<OFF - HI>(a + HI);
+}
+template <int OFF>
+SR_DEV i32x2 rdtr(uint32_t a) {
+  constexpr int HI = OFF & ~0xFFFF;
+  return lds_read_tr8<OFF - HI>(a + HI);
+}
+
 template <int N>
 SR_DEV void lgkm_wait() {
   static_assert(N >= 0 && N < 16, "lgkmcnt range");
@@ -153,6 +174,32 @@ template <typename V>
 SR_DEV void pin(V& v) {
   asm volatile("" : "+v"(v));
 }
+
+// Raw fragment as the explicit reads deliver it: one 16-byte read (k-major) or two 8-byte
+// transposing reads (r-major).  The registers are written asynchronously, so nothing may touch
+// them before lgkm_wait: settle() pins each destination behind the wait and only then joins the
+// halves into the MFMA operand.
+template <bool KMAJ>
+struct RawFrag;
+template <>
+struct RawFrag<true> {
+  i32x4 v;
+  SR_DEV bf16x8 settle() {
+    pin(v);
+    return __builtin_bit_cast(bf16x8, v);
+  }
+};
+template <>
+struct RawFrag<false> {
+  i32x2 lo, hi;
+  SR_DEV bf16x8 settle() {
+    pin(lo);
+    pin(hi);
+    i32x4 w;
+    w[0] = lo[0]; w[1] = lo[1]; w[2] = hi[0]; w[3] = hi[1];
+    return __builtin_bit_cast(bf16x8, w);
+  }
+};
 
 // Workgroup barrier as inline asm.  The compiler makes every global->LDS fill still in flight
 // complete before a barrier it can see (s_waitcnt vmcnt(0)), which would drain a multi-stage

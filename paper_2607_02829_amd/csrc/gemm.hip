@@ -248,52 +248,6 @@ SR_DEV void tile_coords(int bid, int nwg, int tiles_m, int tiles_n, int& tm, int
   tn = v / gm;
 }
 
-template <int N, typename F>
-SR_DEV void static_for(F&& f) {
-  if constexpr (N > 0) {
-    static_for<N - 1>(f);
-    f(IC<N - 1>{});
-  }
-}
-
-// Explicit LDS reads at a compile-time byte offset (the 16-bit instruction offset field takes
-// what fits, the rest is added to the address).
-template <int OFF>
-SR_DEV i32x4 rd16(uint32_t a) {
-  constexpr int HI = OFF & ~0xFFFF;
-  return lds_read16<OFF - HI>(a + HI);
-}
-template <int OFF>
-SR_DEV i32x2 rdtr(uint32_t a) {
-  constexpr int HI = OFF & ~0xFFFF;
-  return lds_read_tr8<OFF - HI>(a + HI);
-}
-
-// Raw fragment as the explicit reads deliver it: one 16-byte read (k-major) or two 8-byte
-// transposing reads (r-major).  The registers are written asynchronously, so nothing may touch
-// them before lgkm_wait: settle() pins each destination behind the wait and only then joins the
-// halves into the MFMA operand.
-template <bool KMAJ>
-struct RawFrag;
-template <>
-struct RawFrag<true> {
-  i32x4 v;
-  SR_DEV bf16x8 settle() {
-    pin(v);
-    return __builtin_bit_cast(bf16x8, v);
-  }
-};
-template <>
-struct RawFrag<false> {
-  i32x2 lo, hi;
-  SR_DEV bf16x8 settle() {
-    pin(lo);
-    pin(hi);
-    i32x4 w;
-    w[0] = lo[0]; w[1] = lo[1]; w[2] = hi[0]; w[3] = hi[1];
-    return __builtin_bit_cast(bf16x8, w);
-  }
-};
 
 // Per-lane LDS byte addresses of one operand's fragments (stage 0, k-step 0 for r-major).
 //  k-major: rows rb + 32 p + lane % 32 (p = 0, 1; rows 64 apart share the swizzle), one address
