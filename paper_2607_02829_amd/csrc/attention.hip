@@ -269,13 +269,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
     }
     const float nm = -m_run * sl2;
     bf16x8 pb[2];
-    float psum = 0.f;
+    float pv[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float p = ex2(fmaf(sc[r], sl2, nm));
-      psum += p;
-      pb[r >> 3][r & 7] = (__bf16)p;
+      pv[r] = ex2(fmaf(sc[r], sl2, nm));
+      pb[r >> 3][r & 7] = (__bf16)pv[r];
     }
+    // pairwise sum: shorter dependency chain than a running sum
+#pragma unroll
+    for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+      for (int r = 0; r < w; ++r) pv[r] += pv[r + w];
+    const float psum = pv[0];
     l_run += psum;
     lgkm_wait<0>();
 #pragma unroll
@@ -291,16 +296,19 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
   auto tile = [&](int t, auto stg) {
     constexpr int s0 = decltype(stg)::value;
     const bool rag = ragged && t + 1 == nt;
+    // both units' score MFMAs first: unit 1's run while unit 0's softmax arithmetic does
     RawFrag<true> k0r[4], k1r[4];
     f32x16 sc0, sc1;
     read_k(stg, IC<0>{}, k0r);
+    read_k(stg, IC<1>{}, k1r);
     lgkm_wait<0>();
     scores(k0r, sc0);
-    read_k(stg, IC<1>{}, k1r);   // lands while unit 0's softmax runs
-    if (rag && S - t * KT < 32) mask(sc0, t * KT);
-    consume(stg, IC<0>{}, sc0);   // its final wait also covers unit 1's K reads
     scores(k1r, sc1);
-    if (rag && S - t * KT < 64) mask(sc1, t * KT + 32);
+    if (rag) {
+      if (S - t * KT < 32) mask(sc0, t * KT);
+      if (S - t * KT < 64) mask(sc1, t * KT + 32);
+    }
+    consume(stg, IC<0>{}, sc0);
     consume(stg, IC<1>{}, sc1);
     wait_vm_lgkm0<kLoads>();   // tile t+1 resident (tile t+2's loads may still fly)
     lds_barrier();             // every wave done with tile t's stage
@@ -536,20 +544,24 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
   auto tile = [&](int t, auto stg) {
     constexpr int s0 = decltype(stg)::value;
     const bool rag = ragged && t + 1 == nt;
+    // both units' S^T / dP^T MFMAs first: unit 1's run while unit 0's arithmetic does
     RawFrag<true> k0r[4], v0r[4], k1r[4], v1r[4];
     f32x16 sv0, dp0, sv1, dp1;
     read_rows(stg, IC<0>{}, IC<0>{}, k0r);
     read_rows(stg, IC<0>{}, IC<1>{}, v0r);
     lgkm_wait<0>();
     sd(k0r, v0r, sv0, dp0);
-    read_rows(stg, IC<1>{}, IC<0>{}, k1r);   // unit 1's K rows land while unit 0's arithmetic runs
-    if (rag) grad(stg, IC<0>{}, sv0, dp0, t * KT, std::true_type{});
-    else grad(stg, IC<0>{}, sv0, dp0, t * KT, std::false_type{});   // its wait covers them
+    read_rows(stg, IC<1>{}, IC<0>{}, k1r);
     read_rows(stg, IC<1>{}, IC<1>{}, v1r);
     lgkm_wait<0>();
     sd(k1r, v1r, sv1, dp1);
-    if (rag) grad(stg, IC<1>{}, sv1, dp1, t * KT + 32, std::true_type{});
-    else grad(stg, IC<1>{}, sv1, dp1, t * KT + 32, std::false_type{});
+    if (rag) {
+      grad(stg, IC<0>{}, sv0, dp0, t * KT, std::true_type{});
+      grad(stg, IC<1>{}, sv1, dp1, t * KT + 32, std::true_type{});
+    } else {
+      grad(stg, IC<0>{}, sv0, dp0, t * KT, std::false_type{});
+      grad(stg, IC<1>{}, sv1, dp1, t * KT + 32, std::false_type{});
+    }
     wait_vm_lgkm0<kLoads>();   // tile t+1 resident (tile t+2's loads may still fly)
     lds_barrier();             // every wave done with tile t's stage
     load(t + 2, (s0 + 2) % NSTG);

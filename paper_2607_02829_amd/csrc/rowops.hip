@@ -114,8 +114,8 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
 // dres: fp32 [M, D] residual gradient added to the result (may alias dx).
 // dx = dres + (dxhat - mean(dxhat) - xhat * mean(dxhat * xhat)) * rstd with
 // dxhat = du * gamma (or du * (1 + scale_b)).  A workgroup takes kLnBwdRows rows of one
-// sample (two per wave, loaded together) and writes partial column sums of du * xhat and
-// du to part[(b*nchunk + chunk) * 2D].
+// sample (two per wave, loads issued together) and writes partial column
+// sums of du * xhat and du to part[(b*nchunk + chunk) * 2D].
 constexpr int kLnBwdRows = 8;
 
 template <typename T, typename Ta, int V, int NJC>
@@ -125,8 +125,13 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ d
                                                      int mod_off, const float* dres, int S, int D, float* dx,
                                                      Ta* __restrict__ dx_act, float* __restrict__ part) {
   constexpr int NJ = NJC > 0 ? NJC : kMaxPerLane / V;
-  constexpr int RPW = kLnBwdRows / 4;   // rows per wave
-  __shared__ float red[4][2][kMaxPerLane * 64 / 4];   // four waves' partials, 512 columns per pass
+  constexpr int RG = 2;                        // rows loaded together
+  constexpr int NG = kLnBwdRows / (4 * RG);    // row groups per wave
+  constexpr int CPP = 64 * kMaxPerLane / 4;    // columns per combining pass (512)
+  // four waves' partials of one pass; column q * V + e of the pass at slot e * (CPP / V + 1) + q, so
+  // that the writes (fixed e, consecutive q) and the reads (consecutive columns) are conflict-free
+  constexpr int SLOT = CPP / V + 1;
+  __shared__ float red[4][2][V * SLOT];
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int b = blockIdx.y, chunk = blockIdx.x, nchunk = gridDim.x;
   const int n = NJC > 0 ? NJC : D / (64 * V);
@@ -147,73 +152,77 @@ __global__ __launch_bounds__(256) void ln_bwd_kernel(const float* __restrict__ d
 #pragma unroll
     for (int e = 0; e < V; ++e) { pg[j][e] = 0.f; pb[j][e] = 0.f; }
   }
-  // this wave's rows (loads of both rows are issued before any reduction)
-  float g[RPW][NJ][V], xv[RPW][NJ][V], rv[RPW][NJ][V];
-  size_t rows[RPW];
-  bool ok[RPW];
+#pragma unroll 1
+  for (int grp = 0; grp < NG; ++grp) {
+    // this wave's rows of the group (loads of both rows issued before any reduction)
+    float g[RG][NJ][V], xv[RG][NJ][V], rv[RG][NJ][V];
+    size_t rows[RG];
+    bool ok[RG];
 #pragma unroll
-  for (int rr = 0; rr < RPW; ++rr) {
-    const int s = chunk * kLnBwdRows + wid + 4 * rr;
-    ok[rr] = s < S;
-    rows[rr] = (size_t)b * S + (ok[rr] ? s : 0);
+    for (int rr = 0; rr < RG; ++rr) {
+      const int s = chunk * kLnBwdRows + wid + 4 * (grp * RG + rr);
+      ok[rr] = s < S;
+      rows[rr] = (size_t)b * S + (ok[rr] ? s : 0);
 #pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      if (j < n && ok[rr]) {
-        ldv<V>(du + rows[rr] * D + col_of<V>(lane, j), g[rr][j]);
-        ldv<V>(x + rows[rr] * D + col_of<V>(lane, j), xv[rr][j]);
-        ldv<V>(dres + rows[rr] * D + col_of<V>(lane, j), rv[rr][j]);
-      }
+      for (int j = 0; j < NJ; ++j)
+        if (j < n && ok[rr]) {
+          ldv<V>(du + rows[rr] * D + col_of<V>(lane, j), g[rr][j]);
+          ldv<V>(x + rows[rr] * D + col_of<V>(lane, j), xv[rr][j]);
+          ldv<V>(dres + rows[rr] * D + col_of<V>(lane, j), rv[rr][j]);
+        }
+    }
+#pragma unroll
+    for (int rr = 0; rr < RG; ++rr) {
+      if (!ok[rr]) continue;
+      const size_t row = rows[rr];
+      const float mu = mean[row], rs = rstd[row];
+      float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        if (j < n)
+#pragma unroll
+          for (int e = 0; e < V; ++e) {
+            const float xh = (xv[rr][j][e] - mu) * rs;
+            const float dxh = g[rr][j][e] * wt[j][e];
+            s1 += dxh;
+            s2 += dxh * xh;
+            pg[j][e] += g[rr][j][e] * xh;
+            pb[j][e] += g[rr][j][e];
+            xv[rr][j][e] = xh;
+          }
+      const float m1 = wave_sum(s1) / (float)D, m2 = wave_sum(s2) / (float)D;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        if (j < n) {
+          const int c = col_of<V>(lane, j);
+          float o[V];
+#pragma unroll
+          for (int e = 0; e < V; ++e) o[e] = rv[rr][j][e] + (g[rr][j][e] * wt[j][e] - m1 - xv[rr][j][e] * m2) * rs;
+          stv<V>(dx + row * D + c, o);
+          if (dx_act) stv<V>(dx_act + row * D + c, o);
+        }
+    }
   }
+  // combine the four waves' partials through LDS, CPP columns per pass
+  float* out = part + ((size_t)b * nchunk + chunk) * 2 * D;
+  for (int c0 = 0; c0 < D; c0 += CPP) {
+    __syncthreads();
 #pragma unroll
-  for (int rr = 0; rr < RPW; ++rr) {
-    if (!ok[rr]) continue;
-    const size_t row = rows[rr];
-    const float mu = mean[row], rs = rstd[row];
-    float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      if (j < n)
+    for (int j = 0; j < NJ; ++j) {
+      const int q = lane + 64 * j - c0 / V;   // column group (of V) within the pass
+      if (j < n && q >= 0 && q < CPP / V) {
 #pragma unroll
         for (int e = 0; e < V; ++e) {
-          const float xh = (xv[rr][j][e] - mu) * rs;
-          const float dxh = g[rr][j][e] * wt[j][e];
-          s1 += dxh;
-          s2 += dxh * xh;
-          pg[j][e] += g[rr][j][e] * xh;
-          pb[j][e] += g[rr][j][e];
-          xv[rr][j][e] = xh;
-        }
-    const float m1 = wave_sum(s1) / (float)D, m2 = wave_sum(s2) / (float)D;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      if (j < n) {
-        const int c = col_of<V>(lane, j);
-        float o[V];
-#pragma unroll
-        for (int e = 0; e < V; ++e) o[e] = rv[rr][j][e] + (g[rr][j][e] * wt[j][e] - m1 - xv[rr][j][e] * m2) * rs;
-        stv<V>(dx + row * D + c, o);
-        if (dx_act) stv<V>(dx_act + row * D + c, o);
-      }
-  }
-  // combine the four waves' partials through LDS, 512 columns per pass
-  float* out = part + ((size_t)b * nchunk + chunk) * 2 * D;
-  const int cols_per_pass = 64 * kMaxPerLane / 4;
-  for (int c0 = 0; c0 < D; c0 += cols_per_pass) {
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-#pragma unroll
-      for (int e = 0; e < V; ++e) {
-        const int c = col_of<V>(lane, j) + e;
-        if (j < n && c >= c0 && c < c0 + cols_per_pass) {
-          red[wid][0][c - c0] = pg[j][e];
-          red[wid][1][c - c0] = pb[j][e];
+          red[wid][0][e * SLOT + q] = pg[j][e];
+          red[wid][1][e * SLOT + q] = pb[j][e];
         }
       }
+    }
     __syncthreads();
-    for (int t = threadIdx.x; t < cols_per_pass && c0 + t < D; t += 256) {
-      out[c0 + t] = red[0][0][t] + red[1][0][t] + red[2][0][t] + red[3][0][t];
-      out[D + c0 + t] = red[0][1][t] + red[1][1][t] + red[2][1][t] + red[3][1][t];
+    for (int t = threadIdx.x; t < CPP && c0 + t < D; t += 256) {
+      const int sl = (t % V) * SLOT + t / V;
+      out[c0 + t] = red[0][0][sl] + red[1][0][sl] + red[2][0][sl] + red[3][0][sl];
+      out[D + c0 + t] = red[0][1][sl] + red[1][1][sl] + red[2][1][sl] + red[3][1][sl];
     }
   }
 }

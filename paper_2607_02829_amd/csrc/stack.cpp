@@ -21,6 +21,7 @@
 
 #include <cmath>
 #include <mutex>
+#include <vector>
 
 #include "profile.h"
 
@@ -118,10 +119,12 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   s.part = c.take<float>((size_t)d.B * colsum_chunks(d.S) * wmax * 4);
   s.lnpart = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
   s.dmod = c.take<float>((size_t)d.B * 6 * D * 4);
-  s.g_act = c.take<void>(M * D * e);
-  s.dz = c.take<void>(M * F * e);
+  // two of each buffer a weight-gradient GEMM reads on the side stream, so the main stream
+  // rarely waits for it before writing the next one
+  for (int k = 0; k < 2; ++k) s.g_act[k] = c.take<void>(M * D * e);
+  for (int k = 0; k < 2; ++k) s.dz[k] = c.take<void>(M * F * e);
   s.dO = c.take<void>(M * D * e);
-  s.dqkv = c.take<void>(M * 3 * D * e);
+  for (int k = 0; k < 2; ++k) s.dqkv[k] = c.take<void>(M * 3 * D * e);
   if (out) *out = s;
   return c.off;
 }
@@ -246,20 +249,51 @@ hipError_t side_stream(hipStream_t* out) {
   return hipSuccess;
 }
 
-// Events of one backward call: fork (caller stream -> side stream) and the completion of
-// each kind of weight-gradient GEMM (side -> caller).  An event is re-recorded only after
-// the waits on its previous record have been enqueued.
+// Events of one backward call: fork (caller stream -> side stream) and, per slot, the
+// completion of the last weight-gradient GEMM that read a double-buffered input (side ->
+// caller).  An event is re-recorded only after the waits on its previous record have been
+// enqueued.  Sets are created once and kept in a per-device pool (creating events per call
+// costs tens of microseconds of host time).
+constexpr int kSlots = 6;   // dW_fc2 (g_act[0]), dW_o (g_act[1]), dW_fc1 (dz[0..1]), dW_qkv (dqkv[0..1])
 struct BwdEvents {
-  hipEvent_t fork = nullptr, fc2 = nullptr, fc1 = nullptr, o = nullptr, qkv = nullptr;
+  hipEvent_t fork = nullptr;
+  hipEvent_t done[kSlots] = {};
+  int dev = -1;
   hipError_t create() {
-    for (hipEvent_t* e : {&fork, &fc2, &fc1, &o, &qkv}) SR_TRY(hipEventCreateWithFlags(e, hipEventDisableTiming));
+    SR_TRY(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
+    for (hipEvent_t& e : done) SR_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     return hipSuccess;
   }
-  ~BwdEvents() {
-    for (hipEvent_t e : {fork, fc2, fc1, o, qkv})
-      if (e) (void)hipEventDestroy(e);
-  }
 };
+std::mutex g_ev_mu;
+std::vector<BwdEvents*> g_ev_pool;
+hipError_t take_events(BwdEvents** out) {
+  int dev = 0;
+  SR_TRY(hipGetDevice(&dev));
+  {
+    std::lock_guard<std::mutex> lock(g_ev_mu);
+    for (size_t i = 0; i < g_ev_pool.size(); ++i)
+      if (g_ev_pool[i]->dev == dev) {
+        *out = g_ev_pool[i];
+        g_ev_pool.erase(g_ev_pool.begin() + (long)i);
+        return hipSuccess;
+      }
+  }
+  BwdEvents* e = new BwdEvents;
+  e->dev = dev;
+  const hipError_t r = e->create();
+  if (r != hipSuccess) {
+    delete e;   // the events created so far are leaked: an event-creation failure is fatal anyway
+    return r;
+  }
+  *out = e;
+  return hipSuccess;
+}
+void give_events(BwdEvents* e) {
+  if (!e) return;
+  std::lock_guard<std::mutex> lock(g_ev_mu);
+  g_ev_pool.push_back(e);
+}
 
 }  // namespace
 
@@ -276,75 +310,80 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
   const int nln = ln_bwd_chunks(S);
 
   hipStream_t side = nullptr;
-  BwdEvents ev;
-  bool pending[4] = {false, false, false, false};   // fc2, fc1, o, qkv recorded and not yet waited on
-  hipEvent_t* done[4] = {&ev.fc2, &ev.fc1, &ev.o, &ev.qkv};
-  // side stream: wait for everything issued on st so far, run the weight gradient, signal
+  BwdEvents* ev = nullptr;
+  bool pending[kSlots] = {};   // recorded and not yet waited on
+  // side stream: wait for everything issued on st so far, run the weight gradient, signal slot
   const bool serial = profiling_all();
-  auto on_side = [&](int kind, auto&& launch) -> hipError_t {
+  auto on_side = [&](int slot, auto&& launch) -> hipError_t {
     if (serial) return launch(st);
-    SR_TRY(hipEventRecord(ev.fork, st));
-    SR_TRY(hipStreamWaitEvent(side, ev.fork, 0));
+    SR_TRY(hipEventRecord(ev->fork, st));
+    SR_TRY(hipStreamWaitEvent(side, ev->fork, 0));
     SR_TRY(launch(side));
-    SR_TRY(hipEventRecord(*done[kind], side));
-    pending[kind] = true;
+    SR_TRY(hipEventRecord(ev->done[slot], side));
+    pending[slot] = true;
     return hipSuccess;
   };
-  // st: wait before overwriting what a weight-gradient GEMM of this kind reads
-  auto join = [&](int kind) -> hipError_t {
-    if (pending[kind]) SR_TRY(hipStreamWaitEvent(st, *done[kind], 0));
-    pending[kind] = false;
+  // st: wait before overwriting the buffer the slot's weight-gradient GEMM reads
+  auto join = [&](int slot) -> hipError_t {
+    if (pending[slot]) SR_TRY(hipStreamWaitEvent(st, ev->done[slot], 0));
+    pending[slot] = false;
     return hipSuccess;
   };
-  enum { kFc2 = 0, kFc1 = 1, kO = 2, kQkv = 3 };
+  // slots: g_act[0] (FC2 stage) and g_act[1] (output-projection stage) are read by dW_fc2 and
+  // dW_o; dz[i % 2] by dW_fc1 and dqkv[i % 2] by dW_qkv of block i
+  enum { kFc2 = 0, kO = 1, kFc1 = 2, kQkv = 4 };
 
   auto run = [&]() -> hipError_t {
     SR_TRY(side_stream(&side));
-    SR_TRY(ev.create());
+    SR_TRY(take_events(&ev));
     // g_res = fp32(dh_out) and, for pre-LN, its activation copy
     {
       ProfScope ps("convert", 0, (double)M * D * (2 * e + 4), st);
-      SR_TRY(launch_convert(d.dtype, dh_out, d.dtype, sc.g_act, (size_t)M * D, nullptr, 0, S, D, sc.g_res, st));
+      SR_TRY(launch_convert(d.dtype, dh_out, d.dtype, sc.g_act[0], (size_t)M * D, nullptr, 0, S, D, sc.g_res, st));
     }
+    void* const g0 = sc.g_act[0];   // gradient copy of the FC2 stage (read by dW_fc2)
+    void* const g1 = sc.g_act[1];   // ... of the output-projection stage (read by dW_o)
     for (int i = d.nb - 1; i >= 0; --i) {
       const BlockSaved& s = sv[i];
       const sr_block_params& w = p[i];
       const sr_block_grads& g = gr[i];
+      const int par = i & 1;
+      void* const dz = sc.dz[par];
+      void* const dqkv = sc.dqkv[par];
       if (ada) {
         // MLP-branch gradient dm = dh' * gate2 (activation copy) and dgate2 = sum_s dh' * m_out
-        SR_TRY(join(kO));   // g_act is still read by the previous block's dW_o
+        SR_TRY(join(kFc2));   // g0 may still be read by the previous block's dW_fc2
         ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
-        SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, sc.g_act, (size_t)M * D, s.mod + 5 * D, 6 * D, S, D, nullptr,
-                              st));
+        SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, g0, (size_t)M * D, s.mod + 5 * D, 6 * D, S, D, nullptr, st));
         SR_TRY(gate_grad(d, sc.g_res, s.m_out, sc.dmod, 5 * D, sc, st));
       }
       // FC2: dW2, db2; dz = (dm W2) * GELU'(z)
       SR_TRY(on_side(kFc2, [&](hipStream_t ss) {
-        return weight_grad("gemm_dw_fc2", d, sc.g_act, D, s.gz, F, g.w_fc2, g.b_fc2, sc, ss);
+        return weight_grad("gemm_dw_fc2", d, g0, D, s.gz, F, g.w_fc2, g.b_fc2, sc, ss);
       }));
-      SR_TRY(join(kFc1));   // dz is still read by the previous block's dW_fc1
+      SR_TRY(join(kFc1 + par));   // dz[par] may still be read by dW_fc1 two blocks back
       {
-        GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
-        EpiArgs ep; ep.z_in = s.z; ep.out_act = sc.dz; ep.ldo = F;
+        GemmDesc gd = desc(d, g0, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
+        EpiArgs ep; ep.z_in = s.z; ep.out_act = dz; ep.ldo = F;
         ProfScope ps("gemm_dx_fc2", gemm_flops(M, F, D), gemm_bytes(d, M, F, D, 2 * (int)e), st);
         SR_TRY(launch_gemm(gd, EPI_DGELU, ep, st));
       }
       // FC1: dW1, db1; du = dz W1
-      SR_TRY(on_side(kFc1, [&](hipStream_t ss) {
-        return weight_grad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, g.w_fc1, g.b_fc1, sc, ss);
+      SR_TRY(on_side(kFc1 + par, [&](hipStream_t ss) {
+        return weight_grad("gemm_dw_fc1", d, dz, F, s.u2, D, g.w_fc1, g.b_fc1, sc, ss);
       }));
       {
-        GemmDesc gd = desc(d, sc.dz, true, F, (size_t)M * F * e, w.w_fc1, false, D, (size_t)F * D * e, M, D, F);
+        GemmDesc gd = desc(d, dz, true, F, (size_t)M * F * e, w.w_fc1, false, D, (size_t)F * D * e, M, D, F);
         EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
         ProfScope ps("gemm_dx_fc1", gemm_flops(M, D, F), gemm_bytes(d, M, D, F, 4), st);
         SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
       }
       // LN2 backward: g_res2 = g_res + LN2^T du (pre-LN also writes the activation copy)
-      SR_TRY(join(kFc2));   // g_act is still read by dW_fc2
+      if (!ada) SR_TRY(join(kO));   // g1 may still be read by the previous block's dW_o
       {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
-                             d.B, S, D, sc.g_res2, ada ? nullptr : sc.g_act, sc.lnpart, st));
+                             d.B, S, D, sc.g_res2, ada ? nullptr : g1, sc.lnpart, st));
       }
       {
         ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
@@ -356,18 +395,18 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       if (ada) {
         // attention-branch gradient da = dh1 * gate1 and dgate1 = sum_s dh1 * a_out
         SR_TRY(gate_grad(d, sc.g_res2, s.a_out, sc.dmod, 2 * D, sc, st));
+        SR_TRY(join(kO));   // g1 may still be read by the previous block's dW_o
         ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
-        SR_TRY(launch_convert(kF32, sc.g_res2, d.dtype, sc.g_act, (size_t)M * D, s.mod + 2 * D, 6 * D, S, D, nullptr,
-                              st));
+        SR_TRY(launch_convert(kF32, sc.g_res2, d.dtype, g1, (size_t)M * D, s.mod + 2 * D, 6 * D, S, D, nullptr, st));
       }
       // output projection: dWo, dbo; dO = da Wo (with the attention row statistic
       // delta = rowsum(dO * O) per head in the same epilogue when the head dim is 64)
       SR_TRY(on_side(kO, [&](hipStream_t ss) {
-        return weight_grad("gemm_dw_o", d, sc.g_act, D, s.O, D, g.w_o, g.b_o, sc, ss);
+        return weight_grad("gemm_dw_o", d, g1, D, s.O, D, g.w_o, g.b_o, sc, ss);
       }));
       const bool fuse_delta = d.dtype == kBF16 && D / d.H == 64;
       {
-        GemmDesc gd = desc(d, sc.g_act, true, D, (size_t)M * D * e, w.w_o, false, D, (size_t)D * D * e, M, D, D);
+        GemmDesc gd = desc(d, g1, true, D, (size_t)M * D * e, w.w_o, false, D, (size_t)D * D * e, M, D, D);
         EpiArgs ep; ep.out_act = sc.dO; ep.ldo = D;
         ep.o_in = s.O; ep.delta = sc.delta; ep.S = S; ep.H = d.H;
         ProfScope ps("gemm_dx_o", gemm_flops(M, D, D), gemm_bytes(d, M, D, D, (int)e), st);
@@ -378,25 +417,25 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         ProfScope ps("attn_bwd_delta", 0, (double)M * D * e * 2, st);
         SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, d.B, S, d.H, D / d.H, sc.delta, st));
       }
-      SR_TRY(join(kQkv));   // dqkv is still read by the previous block's dW_qkv
-      SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, d.B, S, d.H, D, st));
+      SR_TRY(join(kQkv + par));   // dqkv[par] may still be read by dW_qkv two blocks back
+      SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, dqkv, d.B, S, d.H, D, st));
       // QKV: dWqkv, dbqkv; du = dqkv Wqkv
-      SR_TRY(on_side(kQkv, [&](hipStream_t ss) {
-        return weight_grad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u1, D, g.w_qkv, g.b_qkv, sc, ss);
+      SR_TRY(on_side(kQkv + par, [&](hipStream_t ss) {
+        return weight_grad("gemm_dw_qkv", d, dqkv, 3 * D, s.u1, D, g.w_qkv, g.b_qkv, sc, ss);
       }));
       {
-        GemmDesc gd = desc(d, sc.dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,
+        GemmDesc gd = desc(d, dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,
                            M, D, 3 * D);
         EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
         ProfScope ps("gemm_dx_qkv", gemm_flops(M, D, 3 * D), gemm_bytes(d, M, D, 3 * D, 4), st);
         SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
       }
       // LN1 backward: g_res = g_res2 + LN1^T du (pre-LN: plus the activation copy for the next block)
-      if (!ada) SR_TRY(join(kO));   // g_act is still read by dW_o
+      if (!ada) SR_TRY(join(kFc2));   // g0 is still read by this block's dW_fc2
       {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2,
-                             d.B, S, D, sc.g_res, ada ? nullptr : sc.g_act, sc.lnpart, st));
+                             d.B, S, D, sc.g_res, ada ? nullptr : g0, sc.lnpart, st));
       }
       {
         ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
@@ -435,15 +474,16 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
       SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
     }
-    for (int k = 0; k < 4; ++k) SR_TRY(join(k));   // every gradient is complete when st is
+    for (int k = 0; k < kSlots; ++k) SR_TRY(join(k));   // every gradient is complete when st is
     return hipSuccess;
   };
   hipError_t err = run();
-  if (err != hipSuccess && side) {
+  if (err != hipSuccess && side && ev) {
     // leave no weight-gradient work unordered with respect to the caller's stream
-    for (int k = 0; k < 4; ++k)
-      if (pending[k]) (void)hipStreamWaitEvent(st, *done[k], 0);
+    for (int k = 0; k < kSlots; ++k)
+      if (pending[k]) (void)hipStreamWaitEvent(st, ev->done[k], 0);
   }
+  give_events(ev);
   delete[] sv;
   return err;
 }

@@ -22,7 +22,7 @@ struct BlockSaved {
 
 struct Scratch {
   float *g_res, *g_res2, *du, *delta, *wpart, *dbpart, *part, *lnpart, *dmod;
-  void *g_act, *dz, *dO, *dqkv;
+  void *g_act[2], *dz[2], *dO, *dqkv[2];
 };
 
 // Carve `base` (may be null: sizes only).  Returns the bytes used.
