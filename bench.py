@@ -176,10 +176,11 @@ def summarize_pmc(group: str, workload: str, fetch_csv: str, write_csv: str, com
         return statistics.mean(vals[keys[0]]), len(vals[keys[0]]), keys[0]
 
     def copy_entry(vals):
-        # the copy probe is the largest single dispatch among the copy kernels
+        # the copy probe is the largest dispatch of the runtime's buffer-copy kernel (torch's
+        # elementwise "copy" kernels convert types and read a different number of bytes)
         best = None
         for k, v in vals.items():
-            if "copy" in k.lower() or "Copy" in k:
+            if "copyBuffer" in k:
                 m = max(v)
                 if best is None or m > best[0]:
                     best = (m, k)
@@ -219,6 +220,49 @@ def summarize_pmc(group: str, workload: str, fetch_csv: str, write_csv: str, com
         "",
     ]
     return "\n".join(lines)
+
+
+def routing_sweep(D: int, sizes=(4050, 32768, 262144), reps: int = 5) -> list:
+    """HBM bandwidth of the gather and the residual-delta scatter (bf16, D columns, h0 read from x)
+    on one sample of L = 2K tokens, for K routed rows per call; a 512 MB write between calls
+    evicts the Infinity Cache, so the large sizes measure HBM.  Algorithmic bytes: gather
+    2KD*2 + 4K, scatter 3KD*2 + 4K."""
+    import torch
+    from paper_2607_02829_amd import abi
+    evict = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    out = []
+    for K in sizes:
+        L = 2 * K
+        cfg = abi.SrConfig(B=1, L=L, D=D, H=max(1, D // 64), F=4 * D, n_blocks=1, dtype=abi.SR_BF16,
+                           kind=abi.SR_BLOCK_PRELN, ln_eps=1e-6, idx_shared=0)
+        x = torch.randn((1, L, D), device="cuda").to(torch.bfloat16)
+        idx = torch.empty((1, K), dtype=torch.int32, device="cuda")
+        abi.sr_select_indices(cfg, K, abi.SR_SEL_RANDOM, 7, 0, None, None, idx)
+        h0 = torch.empty((1, K, D), dtype=torch.bfloat16, device="cuda")
+        h = torch.empty_like(h0)
+        times = {"gather": [], "scatter_delta": []}
+        for r in range(reps + 1):
+            for name in ("gather", "scatter_delta"):
+                evict.zero_()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                if name == "gather":
+                    abi.sr_gather(cfg, K, x, idx, h0)
+                else:   # h0 = NULL: the gathered rows are re-read from x (the backward's form)
+                    abi.sr_scatter_delta(cfg, K, x, h, None, idx)
+                e1.record()
+                torch.cuda.synchronize()
+                if r > 0:
+                    times[name].append(e0.elapsed_time(e1))
+        for name, nbytes in (("gather", 2 * K * D * 2 + 4 * K), ("scatter_delta", 3 * K * D * 2 + 4 * K)):
+            ms = sorted(times[name])[len(times[name]) // 2]
+            gbs = nbytes / (ms * 1e-3) / 1e9
+            out.append({"kernel": name, "rows": K, "bytes": nbytes, "us": round(ms * 1e3, 2),
+                        "GB/s": round(gbs, 1), "frac_of_8TB/s": round(gbs * 1e9 / PEAK_HBM_BYTES, 3)})
+        del x, idx, h0, h
+    del evict
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(w) -> dict:
@@ -267,6 +311,7 @@ def main():
     ap.add_argument("--workload", default="d025", help="tiny | b5625 | c1406 | d025 | edm")
     ap.add_argument("--dense-steps", type=int, default=3, help="timed steps of the dense keep=100%% mode (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-routing-sweep", action="store_true", help="skip the gather/scatter bandwidth sweep")
     ap.add_argument("--breakdown", action="store_true", help="print the per-kernel breakdown to stderr")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run one device-to-device copy of known size first (counter calibration)")
@@ -352,6 +397,18 @@ def main():
         del dn
         torch.cuda.empty_cache()
 
+    # routing kernels: in-step launch times (per-kernel breakdown) and a cache-evicting size sweep
+    routing = {"in_step": {}, "sweep": []}
+    for name in ("gather", "scatter_delta"):
+        if name in breakdown and breakdown[name]["launches"] > 0:
+            b = breakdown[name]
+            us = b["ms"] / b["launches"] * 1e3
+            gbs = b["bytes"] / b["launches"] / (us * 1e-6) / 1e9
+            routing["in_step"][name] = {"us": round(us, 2), "GB/s": round(gbs, 1),
+                                        "frac_of_8TB/s": round(gbs * 1e9 / PEAK_HBM_BYTES, 3)}
+    if w.dtype == "bf16" and not args.no_routing_sweep:
+        routing["sweep"] = routing_sweep(w.D)
+
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)
 
     routed_tok_s = w.B * w.K / (ms_step * 1e-3)
@@ -383,6 +440,7 @@ def main():
                      "frac": round(achieved / peak, 4), "traffic": traffic_for(dom, w.name),
                      "launches_timed": int(d["launches"]), "avg_launch_us": round(per_launch_ms * 1e3, 2)},
         "cpu_baseline": cpu,
+        "routing_bandwidth": routing,
         "outputs_finite": finite,
     }
     print(json.dumps(out), flush=True)

@@ -33,7 +33,8 @@
  *  - Support: D % 64 == 0, F % 64 == 0, D <= 2048, head dim D/H in {32, 64, 128}
  *    (bf16 with head dim 64 runs the MFMA attention kernels, every other case a
  *    generic fp32-accumulating kernel); 1 <= K <= L; B*L*D*elt < 2^31 bytes per
- *    tensor.  Anything else returns SR_EUNSUPPORTED.
+ *    token tensor, and for the block-stack calls also B*L*max(F, 3D)*4 < 2^31
+ *    (internal fp32 buffers).  Anything else returns SR_EUNSUPPORTED.
  */
 #ifndef SR_H
 #define SR_H

@@ -43,7 +43,9 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 size_t elt_of(int dtype) { return dtype == SR_BF16 ? 2 : 4; }
 
-sr_status check_cfg(const sr_config* c) {
+// Routing-only calls (selection, gather, scatter, index validation) touch [B, L, D] tensors, whose
+// byte offsets must fit 31 bits; the block stack also keeps [B*S, max(F, 3D)] fp32 buffers.
+sr_status check_cfg(const sr_config* c, bool routing_only = false) {
   SR_CHECK(c != nullptr, SR_EINVAL, "cfg is NULL");
   SR_CHECK(c->dtype == SR_F32 || c->dtype == SR_BF16, SR_EDTYPE, "unknown dtype %d", c->dtype);
   SR_CHECK(c->kind == SR_BLOCK_PRELN || c->kind == SR_BLOCK_ADALN, SR_EINVAL, "unknown block kind %d", c->kind);
@@ -57,8 +59,12 @@ sr_status check_cfg(const sr_config* c) {
   SR_CHECK(hd == 32 || hd == 64 || hd == 128, SR_EUNSUPPORTED, "head dim %d not in {32, 64, 128}", hd);
   SR_CHECK(c->ln_eps > 0.f, SR_EINVAL, "ln_eps must be > 0");
   SR_CHECK(c->idx_shared == 0 || c->idx_shared == 1, SR_EINVAL, "idx_shared must be 0 or 1");
-  const size_t big = (size_t)c->B * c->L * (size_t)std::max(c->F, 3 * c->D) * 4;
-  SR_CHECK(big < (1ull << 31), SR_EUNSUPPORTED, "tensors beyond 2 GiB are not supported");
+  const size_t tok = (size_t)c->B * c->L * c->D * (c->dtype == SR_BF16 ? 2 : 4);
+  SR_CHECK(tok < (1ull << 31), SR_EUNSUPPORTED, "token tensors beyond 2 GiB are not supported");
+  if (!routing_only) {
+    const size_t big = (size_t)c->B * c->L * (size_t)std::max(c->F, 3 * c->D) * 4;
+    SR_CHECK(big < (1ull << 31), SR_EUNSUPPORTED, "stack buffers beyond 2 GiB are not supported");
+  }
   return SR_OK;
 }
 
@@ -126,7 +132,7 @@ sr_status sr_workspace_bytes(const sr_config* cfg, int32_t S, size_t* saved_byte
 }
 
 sr_status sr_select_scratch_bytes(const sr_config* cfg, int32_t select_kind, size_t* scratch_bytes) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, true);
   if (s != SR_OK) return s;
   SR_CHECK(scratch_bytes != nullptr, SR_EINVAL, "scratch_bytes is NULL");
   SR_CHECK(select_kind == SR_SEL_RANDOM || select_kind == SR_SEL_TOPK_DIFFNORM, SR_EINVAL, "unknown selector %d",
@@ -138,7 +144,7 @@ sr_status sr_select_scratch_bytes(const sr_config* cfg, int32_t select_kind, siz
 sr_status sr_select_indices(const sr_config* cfg, int32_t K, int32_t select_kind, uint64_t seed, uint64_t step,
                             const void* x_t, const void* x_prev, int32_t* idx, void* scratch, size_t scratch_bytes,
                             void* stream) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, true);
   if (s != SR_OK) return s;
   SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
   SR_PTR(idx, "idx");
@@ -161,7 +167,7 @@ sr_status sr_select_indices(const sr_config* cfg, int32_t K, int32_t select_kind
 }
 
 sr_status sr_gather(const sr_config* cfg, int32_t K, const void* x, const int32_t* idx, void* h0, void* stream) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, true);
   if (s != SR_OK) return s;
   SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
   SR_PTR(x, "x");
@@ -175,7 +181,7 @@ sr_status sr_gather(const sr_config* cfg, int32_t K, const void* x, const int32_
 
 sr_status sr_scatter_delta(const sr_config* cfg, int32_t K, void* x, const void* h, const void* h0,
                            const int32_t* idx, void* stream) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, true);
   if (s != SR_OK) return s;
   SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
   SR_PTR(x, "x");
@@ -247,7 +253,7 @@ sr_status sr_dense_blocks_bwd(const sr_config* cfg, const sr_block_params* param
 }
 
 sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx, int32_t* ok_dev, void* stream) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, true);
   if (s != SR_OK) return s;
   SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
   SR_PTR(idx, "idx");
