@@ -124,17 +124,29 @@ SR_DEV i32x2 pack4(f32x4 v) {
   return w;
 }
 
-// Returns the EPI_DO partial sum of this chunk (0 otherwise).
+constexpr bool epi_has_bias(int epi) {
+  return epi == EPI_BIAS_ACT || epi == EPI_RESID || epi == EPI_GELU || epi == EPI_BIAS_F32;
+}
+
+// Bias of the four columns n..n+3 (zero for epilogues without one).
 template <int EPI>
-SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in) {
-  const size_t o = (size_t)m * e.ldo + n;
+SR_DEV f32x4 epi_bias(const EpiArgs& e, int n) {
   f32x4 b = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (EPI == EPI_BIAS_ACT || EPI == EPI_RESID || EPI == EPI_GELU || EPI == EPI_BIAS_F32) {
+  if constexpr (epi_has_bias(EPI)) {
     const i32x2 bw = *reinterpret_cast<const i32x2*>((const bf16_t*)e.bias + n);
-    const bf16_t* be = reinterpret_cast<const bf16_t*>(&bw);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) b[q] = bf2f(be[q]);
+    for (int q = 0; q < 2; ++q) {
+      b[2 * q] = __uint_as_float((uint32_t)bw[q] << 16);
+      b[2 * q + 1] = __uint_as_float((uint32_t)bw[q] & 0xFFFF0000u);
+    }
   }
+  return b;
+}
+
+// Returns the EPI_DO partial sum of this chunk (0 otherwise).  b: the columns' bias (epi_bias).
+template <int EPI>
+SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in, f32x4 b) {
+  const size_t o = (size_t)m * e.ldo + n;
   if constexpr (EPI == EPI_BIAS_ACT) {
     *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(v + b);
   } else if constexpr (EPI == EPI_RESID) {
@@ -465,42 +477,52 @@ __global__ __launch_bounds__(256, OCC) void gemm_mfma_kernel(const bf16_t* __res
     }
   }
 
-  // epilogue, 32 rows per pass (one i-block of one wave row): stage the fp32 result (register r
-  // of a 32 x 32 MFMA tile holds row 8 (r/4) + 4 h + r%4, column lane%32), then 4-column chunks
+  // epilogue in MI passes of 64 rows: pass p stages i-block p of both wave rows (every wave
+  // writes; register r of a 32 x 32 MFMA tile holds row 8 (r/4) + 4 h + r%4, column lane%32)
+  // as fp32 in LDS, then each thread finishes NB 4-column chunks.  The epilogue's global inputs
+  // (residual, GELU pre-activation, O) of every pass are loaded before the first pass and the
+  // bias once, so no pass waits on a global load it issued itself.
   if constexpr (EPI == EPI_DW)
     if (gridDim.x > (unsigned)(tiles_m * tiles_n)) ep.out_f32 = ep.part + (size_t)split * ep.split_stride;
-  constexpr int PR = 32;
+  constexpr int PR = 64;
   constexpr int EPI_LD = BN + 8;   // fp32 row stride: the two halves of a wave hit disjoint banks
   constexpr int CPRo = BN / 4;     // 4-column chunks per row
   constexpr int NB = PR * CPRo / 256;
+  static_assert(256 % CPRo == 0, "a thread's chunks share their columns");
   static_assert(PR * EPI_LD * 4 <= NST * SB, "epilogue staging exceeds the stages");
   float* stg = reinterpret_cast<float*>(smem);
+  // chunk q of pass p: staging row lr = c / CPRo (c = tid + 256 q), columns c4 .. c4 + 3
+  auto chunk_row = [&](int p, int q) {
+    const int lr = (threadIdx.x + 256 * q) / CPRo;
+    return m0 + (lr >> 5) * (BM / 2) + p * 32 + (lr & 31);
+  };
+  const int c4 = (threadIdx.x % CPRo) * 4;
+  const int n = n0 + c4;
+  const f32x4 bias = n < N ? epi_bias<EPI>(ep, n) : f32x4{0.f, 0.f, 0.f, 0.f};
+  EpiIn in[MI][NB];
 #pragma unroll
-  for (int p = 0; p < BM / PR; ++p) {
+  for (int p = 0; p < MI; ++p)
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      const int m = chunk_row(p, q);
+      if (m < M && n < N) epi_load<EPI>(ep, m, n, in[p][q]);
+    }
+#pragma unroll
+  for (int p = 0; p < MI; ++p) {
     if (p) __syncthreads();
-    if (wm == p / MI) {
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          stg[(8 * (r >> 2) + 4 * h + (r & 3)) * EPI_LD + wn * (BN / 2) + j * 32 + (lane & 31)] = acc[p % MI][j][r];
-    }
+      for (int r = 0; r < 16; ++r)
+        stg[(wm * 32 + 8 * (r >> 2) + 4 * h + (r & 3)) * EPI_LD + wn * (BN / 2) + j * 32 + (lane & 31)] = acc[p][j][r];
     __syncthreads();
-    EpiIn in[NB];
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
-      const int c = threadIdx.x + 256 * q;
-      const int m = m0 + p * PR + c / CPRo, n = n0 + (c % CPRo) * 4;
-      if (m < M && n < N) epi_load<EPI>(ep, m, n, in[q]);
-    }
-#pragma unroll
-    for (int q = 0; q < NB; ++q) {
-      const int c = threadIdx.x + 256 * q;
-      const int row = c / CPRo, c4 = (c % CPRo) * 4;
-      const int m = m0 + p * PR + row, n = n0 + c4;
+      const int lr = (threadIdx.x + 256 * q) / CPRo;
+      const int m = chunk_row(p, q);
       float part = 0.f;
       if (m < M && n < N)
-        part = epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stg + row * EPI_LD + c4), in[q]);
+        part = epi_store<EPI>(ep, m, n, *reinterpret_cast<const f32x4*>(stg + lr * EPI_LD + c4), in[p][q], bias);
       if constexpr (EPI == EPI_DO) {
         // the 16 lanes (tid % 16) of one head's 64 columns: butterfly within the group
 #pragma unroll
