@@ -227,7 +227,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
 
   f32x16 o[2];
   zero16(o[0]); zero16(o[1]);
-  float m_run = -INFINITY, l_run = 0.f;   // running max of the raw scores, partial sum (this half's keys)
+  // softmax denominators on the matrix cores: a 32-row A operand whose row 0 is all ones turns
+  // the P^T MFMA into the column sums of P^T, so lsum[0] of lane l32 (first half) is the sum of
+  // the bf16 probabilities of query l32 (the values the PV product uses); every other element
+  // stays zero
+  f32x16 lsum;
+  zero16(lsum);
+  bf16x8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = (__bf16)(l32 == 0 ? 1.0f : 0.0f);
+  float m_run = -INFINITY;   // running max of the raw scores
   // K row fragments of key unit U of stage SG
   auto read_k = [&](auto sg, auto uu, RawFrag<true> (&kr)[4]) {
     constexpr int SG = decltype(sg)::value, U = decltype(uu)::value;
@@ -239,28 +248,34 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) sc = mfma(kr[ks].settle(), qf[ks], sc);
   };
-  // online softmax of unit U, then O^T += V^T P^T (V^T fragments read first, so that their
-  // latency hides behind the arithmetic)
-  auto consume = [&](auto sg, auto uu, const f32x16& sc) {
+  // V^T fragments of unit U (read before the softmax arithmetic, so that their latency hides
+  // behind it)
+  auto read_vt = [&](auto sg, auto uu, RawFrag<false> (&vt)[2][2]) {
     constexpr int SG = decltype(sg)::value, U = decltype(uu)::value;
-    RawFrag<false> vt[2][2];
     static_for<2>([&](auto db) {
       static_for<2>([&](auto kk) {
         ta.template read<SG * SGB + TB, U * 32 + decltype(kk)::value * 16, decltype(db)::value>(vt[db.value][kk.value]);
       });
     });
-    float mx = sc[0];
+  };
+  // online softmax over the tile's 64 keys (one reference update for both units), then
+  // O^T += V^T P^T per unit
+  auto consume = [&](auto sg, const f32x16& sc0, const f32x16& sc1) {
+    RawFrag<false> vt0[2][2], vt1[2][2];
+    read_vt(sg, IC<0>{}, vt0);
+    read_vt(sg, IC<1>{}, vt1);
+    float mx = fmaxf(sc0[0], sc1[0]);
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sc[r]);
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(sc0[r], sc1[r]));
     mx = half_pair_max(mx);
     // lazy rescaling: the reference max m_run moves (and O, l are rescaled) only when a
     // row's max has grown by more than 8 in exp2 units; otherwise p = 2^((s - m_run) c) <= 256,
     // and since O and l share the reference the result is the same
-    const float grow = (fmaxf(m_run, mx) - m_run) * sl2;   // +inf on the first unit
+    const float grow = (fmaxf(m_run, mx) - m_run) * sl2;   // +inf on the first tile
     if (__ballot(grow > 8.0f)) {
       const float m_ref = grow > 8.0f ? mx : m_run;
       const float alpha = ex2((m_run - m_ref) * sl2);
-      l_run *= alpha;
+      lsum[0] *= alpha;
 #pragma unroll
       for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -268,25 +283,25 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
       m_run = m_ref;
     }
     const float nm = -m_run * sl2;
-    bf16x8 pb[2];
-    float pv[16];
+    bf16x8 pb0[2], pb1[2];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      pv[r] = ex2(fmaf(sc[r], sl2, nm));
-      pb[r >> 3][r & 7] = (__bf16)pv[r];
+      pb0[r >> 3][r & 7] = (__bf16)ex2(fmaf(sc0[r], sl2, nm));
+      pb1[r >> 3][r & 7] = (__bf16)ex2(fmaf(sc1[r], sl2, nm));
     }
-    // pairwise sum: shorter dependency chain than a running sum
 #pragma unroll
-    for (int w = 8; w >= 1; w >>= 1)
-#pragma unroll
-      for (int r = 0; r < w; ++r) pv[r] += pv[r + w];
-    const float psum = pv[0];
-    l_run += psum;
+    for (int kk = 0; kk < 2; ++kk) {
+      lsum = mfma(ones, pb0[kk], lsum);
+      lsum = mfma(ones, pb1[kk], lsum);
+    }
     lgkm_wait<0>();
 #pragma unroll
     for (int db = 0; db < 2; ++db)
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) o[db] = mfma(vt[db][kk].settle(), pb[kk], o[db]);
+      for (int kk = 0; kk < 2; ++kk) {
+        o[db] = mfma(vt0[db][kk].settle(), pb0[kk], o[db]);
+        o[db] = mfma(vt1[db][kk].settle(), pb1[kk], o[db]);
+      }
   };
 
   load(0, 0);
@@ -308,8 +323,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
       if (S - t * KT < 32) mask(sc0, t * KT);
       if (S - t * KT < 64) mask(sc1, t * KT + 32);
     }
-    consume(stg, IC<0>{}, sc0);
-    consume(stg, IC<1>{}, sc1);
+    consume(stg, sc0, sc1);
     wait_vm_lgkm0<kLoads>();   // tile t+1 resident (tile t+2's loads may still fly)
     lds_barrier();             // every wave done with tile t's stage
     load(t + 2, (s0 + 2) % NSTG);
@@ -325,7 +339,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
 
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();   // every wave is done with the stages before they hold the output
-  const float l_tot = half_pair_sum(l_run);
+  const float l_tot = half_pair_sum(lsum[0]);   // the second half's element is zero
   if (h32 == 0 && myq < S) lse[((size_t)b * H + hh) * S + myq] = m_run * sl2 + log2f(l_tot);
   stage_t(smem, o, 1.0f / l_tot, wid, lane);
   __syncthreads();
