@@ -290,7 +290,8 @@ __global__ __launch_bounds__(256) void attn_delta_kernel(const Ta* __restrict__ 
 // A block covers 64 columns with 16 row phases, combined through LDS.
 __global__ __launch_bounds__(1024) void reduce_cols_kernel(const float* __restrict__ part, int R, int G, int sum_groups,
                                                            int width, int half, float* __restrict__ out_lo,
-                                                           float* __restrict__ out_hi, int out_stride) {
+                                                           float* __restrict__ out_hi, int out_stride,
+                                                           int accumulate) {
   __shared__ float red[16][65];
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   const int c = blockIdx.x * 64 + tx;
@@ -316,12 +317,10 @@ __global__ __launch_bounds__(1024) void reduce_cols_kernel(const float* __restri
     if (ty < s) red[ty][tx] += red[ty + s][tx];
     __syncthreads();
   }
-  if (ty == 0 && c < width) {
-    if (c < half) {
-      if (out_lo) out_lo[(size_t)g * out_stride + c] = red[0][tx];
-    } else if (out_hi) {
-      out_hi[(size_t)g * out_stride + c - half] = red[0][tx];
-    }
+  if (ty == 0 && c < width) {   // accumulate: added to what the output holds
+    float* o = c < half ? (out_lo ? out_lo + (size_t)g * out_stride + c : nullptr)
+                        : (out_hi ? out_hi + (size_t)g * out_stride + c - half : nullptr);
+    if (o) *o = accumulate ? *o + red[0][tx] : red[0][tx];
   }
 }
 
@@ -409,10 +408,10 @@ hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, cons
 }
 
 hipError_t launch_reduce_cols(const float* part, int R, int G, int sum_groups, int width, int half, float* out_lo,
-                              float* out_hi, int out_stride, hipStream_t st) {
+                              float* out_hi, int out_stride, hipStream_t st, int accumulate) {
   dim3 g((width + 63) / 64, sum_groups ? 1 : G);
   hipLaunchKernelGGL(reduce_cols_kernel, g, dim3(1024), 0, st, part, R, G, sum_groups, width, half, out_lo, out_hi,
-                     out_stride);
+                     out_stride, accumulate);
   return hipGetLastError();
 }
 

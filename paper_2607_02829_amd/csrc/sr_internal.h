@@ -86,7 +86,16 @@ hipError_t launch_colsum(int xt, const void* X, int yt, const void* Y, const flo
 hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, const float* w, int wstride, int S, int D,
                           float* y32, hipStream_t st);
 hipError_t launch_reduce_cols(const float* part, int R, int G, int sum_groups, int width, int half, float* out_lo,
-                              float* out_hi, int out_stride, hipStream_t st);
+                              float* out_hi, int out_stride, hipStream_t st, int accumulate = 0);
+// Matrix-vector products of the adaLN conditioning (few rows B, bandwidth-bound in the weight):
+//  rows: y[b*ldy + j] = bias[j] + sum_d x[b*ldx + d] W[j*Dd + d]   (x, W, bias storage type)
+//  cols: y[b*ldy + n] (+)= sum_j x[b*ldx + j] W[j*N + n]           (x fp32, W storage type),
+//        through partial sums over row chunks (scratch of gemv_cols_scratch floats).
+hipError_t launch_gemv_rows(int dtype, const void* x, int ldx, const void* W, const void* bias, int B, int J, int Dd,
+                            float* y, int ldy, hipStream_t st);
+size_t gemv_cols_scratch(int B, int J, int N);
+hipError_t launch_gemv_cols(int dtype, const float* x, int ldx, const void* W, int B, int J, int N, float* y,
+                            int accumulate, float* part, hipStream_t st);
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st);
 hipError_t launch_attn_delta(int dtype, const void* dO, const void* O, int B, int S, int H, int hd, float* delta,
                              hipStream_t st);

@@ -121,6 +121,7 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   // stream, after the next write of the other one)
   for (int k = 0; k < 2; ++k) s.lnpart[k] = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
   s.dmod = c.take<float>((size_t)d.B * 6 * D * 4);
+  s.gvpart = d.kind == SR_BLOCK_ADALN ? c.take<float>(gemv_cols_scratch(d.B, 6 * d.D, d.D) * 4) : nullptr;
   // two of each buffer a weight-gradient GEMM reads on the side stream, so the main stream
   // rarely waits for it before writing the next one
   for (int k = 0; k < 2; ++k) s.g_act[k] = c.take<void>(M * D * e);
@@ -149,13 +150,9 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
     for (int i = 0; i < d.nb; ++i) {
       const BlockSaved& s = sv[i];
       const sr_block_params& w = p[i];
-      if (ada) {
-        GemmDesc g = desc(d, cond, true, D, (size_t)d.B * D * e, w.w_ada, true, D, (size_t)6 * D * D * e, d.B,
-                          6 * D, D);
-        g.use_mfma = false;
-        EpiArgs ep; ep.out_f32 = s.mod; ep.bias = w.b_ada; ep.ldo = 6 * D;
+      if (ada) {   // mod_b = c_b W_ada^T + b_ada
         ProfScope ps("mod", gemm_flops(d.B, 6 * D, D), gemm_bytes(d, d.B, 6 * D, D, 4), st);
-        SR_TRY(launch_gemm(g, EPI_BIAS_F32, ep, st));
+        SR_TRY(launch_gemv_rows(d.dtype, cond, D, w.w_ada, w.b_ada, d.B, 6 * D, D, s.mod, 6 * D, st));
       }
       {
         ProfScope ps("ln_fwd", 0, (double)M * D * (4 + e), st);
@@ -467,13 +464,9 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
           SR_TRY(launch_gemm(gd, EPI_F32, ep, st));
         }
         if (g.b_ada) SR_TRY(launch_reduce_cols(sc.dmod, d.B, 1, 1, 6 * D, 6 * D, g.b_ada, nullptr, 0, st));
-        if (dcond) {
-          GemmDesc gd = desc(d, sc.dmod, true, 6 * D, (size_t)d.B * 6 * D * 4, w.w_ada, false, D,
-                             (size_t)6 * D * D * e, d.B, D, 6 * D);
-          gd.use_mfma = false; gd.a_type = kF32;
-          EpiArgs ep; ep.out_f32 = dcond; ep.ldo = D;
-          SR_TRY(launch_gemm(gd, i == d.nb - 1 ? EPI_F32 : EPI_F32_ACC, ep, st));
-        }
+        if (dcond)   // dcond (+)= dmod W_ada, summed over the blocks in backward order
+          SR_TRY(launch_gemv_cols(d.dtype, sc.dmod, 6 * D, w.w_ada, d.B, 6 * D, D, dcond, i == d.nb - 1 ? 0 : 1,
+                                  sc.gvpart, st));
         // parameters the adaLN block does not use get zero gradients
         SR_TRY(zero_f32(g.ln1_w, D, st)); SR_TRY(zero_f32(g.ln1_b, D, st));
         SR_TRY(zero_f32(g.ln2_w, D, st)); SR_TRY(zero_f32(g.ln2_b, D, st));
