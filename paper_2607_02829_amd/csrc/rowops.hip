@@ -239,7 +239,20 @@ __global__ __launch_bounds__(256) void colsum_kernel(const TX* __restrict__ X, c
   if (c >= N) return;
   const int s0 = chunk * kColRows, s1 = min(S, s0 + kColRows);
   float acc = 0.f;
-  for (int s = s0; s < s1; ++s) {
+  // eight rows' loads in flight before their products are added, rows in ascending order
+  int s = s0;
+  for (; s + 8 <= s1; s += 8) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const size_t o = ((size_t)b * S + s + i) * N + c;
+      v[i] = to_f32<TX>(X[o]);
+      if (Y) v[i] *= to_f32<TY>(Y[o]);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += v[i];
+  }
+  for (; s < s1; ++s) {
     const size_t o = ((size_t)b * S + s) * N + c;
     float v = to_f32<TX>(X[o]);
     if (Y) v *= to_f32<TY>(Y[o]);
@@ -251,21 +264,53 @@ __global__ __launch_bounds__(256) void colsum_kernel(const TX* __restrict__ X, c
 
 // y = T(x) elementwise (storage -> fp32, fp32 -> storage, fp32 -> activation), with an
 // optional per-sample column weight (adaLN gates): y[b,s,c] = x * w[b*wstride + c].
-template <typename TI, typename TO>
-__global__ __launch_bounds__(256) void convert_kernel(const TI* __restrict__ x, TO* __restrict__ y, size_t n,
-                                                      const float* __restrict__ w, int wstride, int S, int D,
-                                                      float* __restrict__ y32) {
-  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  const size_t stride = (size_t)gridDim.x * 256;
-  for (; i < n; i += stride) {
-    float v = to_f32<TI>(x[i]);
-    if (w) {
-      const size_t row = i / D;
-      const int c = (int)(i - row * D);
-      v *= w[(row / S) * wstride + c];
+// Eight consecutive elements per thread (n and D multiples of 8, so the eight share a row).
+template <typename T>
+SR_DEV void load8(const T* p, float (&v)[8]) {
+  if constexpr (sizeof(T) == 4) {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { v[e] = a[e]; v[4 + e] = b[e]; }
+  } else {
+    const i32x4 w = *reinterpret_cast<const i32x4*>(p);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[2 * q] = __uint_as_float((uint32_t)w[q] << 16);
+      v[2 * q + 1] = __uint_as_float((uint32_t)w[q] & 0xFFFF0000u);
     }
-    y[i] = from_f32<TO>(v);
-    if (y32) y32[i] = v;
+  }
+}
+template <typename T>
+SR_DEV void store8(T* p, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 4) {
+    *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<f32x4*>(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  } else {
+    i32x4 w;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] = (int)f2bf2(v[2 * q], v[2 * q + 1]);
+    *reinterpret_cast<i32x4*>(p) = w;
+  }
+}
+
+template <typename TI, typename TO>
+__global__ __launch_bounds__(256) void convert_kernel(const TI* __restrict__ x, TO* __restrict__ y, uint32_t n8,
+                                                      const float* __restrict__ w, int wstride, uint32_t S,
+                                                      uint32_t D, float* __restrict__ y32) {
+  const uint32_t stride = gridDim.x * 256u;
+  for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < n8; i += stride) {
+    const size_t o = (size_t)i * 8;
+    float v[8];
+    load8<TI>(x + o, v);
+    if (w) {
+      const uint32_t row = (uint32_t)(o / D), c = (uint32_t)(o - (size_t)row * D);
+      float g[8];
+      load8<float>(w + (size_t)(row / S) * wstride + c, g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] *= g[e];
+    }
+    store8<TO>(y + o, v);
+    if (y32) store8<float>(y32 + o, v);
   }
 }
 
@@ -395,9 +440,12 @@ hipError_t launch_colsum(int xt, const void* X, int yt, const void* Y, const flo
 
 hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, const float* w, int wstride, int S,
                           int D, float* y32, hipStream_t st) {
-  dim3 g((unsigned)std::min<size_t>((n + 255) / 256, 65536));
-#define SR_CONV(TI, TO) \
-  hipLaunchKernelGGL((convert_kernel<TI, TO>), g, dim3(256), 0, st, (const TI*)x, (TO*)y, n, w, wstride, S, D, y32)
+  if (n % 8 != 0 || D % 8 != 0 || n / 8 > 0xFFFFFFFFull) return hipErrorInvalidValue;
+  const uint32_t n8 = (uint32_t)(n / 8);
+  dim3 g((unsigned)std::min<size_t>((n8 + 255) / 256, 65536));
+#define SR_CONV(TI, TO)                                                                                  \
+  hipLaunchKernelGGL((convert_kernel<TI, TO>), g, dim3(256), 0, st, (const TI*)x, (TO*)y, n8, w, wstride, \
+                     (uint32_t)S, (uint32_t)D, y32)
   if (ti == kBF16) {
     if (to == kBF16) SR_CONV(bf16_t, bf16_t); else SR_CONV(bf16_t, float);
   } else {
