@@ -54,6 +54,16 @@ def build(verbose: bool = False) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
+    # a kernel whose host-side launch stub was not emitted (the host pass drops it without an
+    # error when the kernel body does not compile for the host) leaves an undefined symbol of
+    # the library's own namespace: refuse such a library
+    nm = shutil.which("nm")
+    if nm:
+        r = subprocess.run([nm, "-D", "--undefined-only", tmp], capture_output=True, text=True)
+        own = [ln.split()[-1] for ln in r.stdout.splitlines() if "_ZN2sr" in ln]
+        if own:
+            os.remove(tmp)
+            raise RuntimeError("undefined symbols of libsr's own code:\n" + "\n".join(own[:10]))
     os.replace(tmp, OUT)
     if verbose:
         print(f"built {OUT}")

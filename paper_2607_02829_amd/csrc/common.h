@@ -37,6 +37,10 @@ template <typename T> SR_DEV T from_f32(float v);
 template <> SR_DEV float from_f32<float>(float v) { return v; }
 template <> SR_DEV bf16_t from_f32<bf16_t>(float v) { return f2bf(v); }
 
+// The wave's index in its workgroup as a wave-uniform (scalar) value, so that addresses derived
+// from it (LDS blocks, M0) stay in scalar registers.
+SR_DEV int wave_index() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
+
 // ---------------------------------------------------------------- wave reductions
 // Every lane ends with the same (bitwise) result: DPP exchanges within 16-lane rows
 // (pairs, quads, half-row mirror, row mirror), then v_permlane16_swap / v_permlane32_swap

@@ -215,30 +215,44 @@ SR_DEV int rswz(int k) {
 // One operand tile (R rows or r-columns, k0 .. k0+63) straight from global memory into LDS
 // (buffer_load ... lds, 16 bytes per lane, no VGPRs): each wave fills whole 1 KB blocks and
 // lane l lands at byte 16 l of its block, so it fetches the chunk the swizzle places there.
-// Offsets at or past the operand's extent read as zero.
+// Offsets at or past the operand's extent read as zero.  The lane's byte offsets for k0 = 0 are
+// computed once; a tile adds one wave-uniform byte offset (k0 * 2 for k-major operands,
+// k0 * ld * 2 for r-major ones), and the LDS block addresses are wave-uniform too, so a fill
+// costs one vector add per load.
 template <int R, bool KMAJ>
-SR_DEV void fill_tile(__amdgpu_buffer_rsrc_t rs, bf16_t* lds, int r0, int k0, int ld, bool valid) {
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  constexpr int BPW = R / 32;   // the tile is R/8 blocks, four waves
+struct TileFill {
+  static constexpr int BPW = R / 32;   // the tile is R/8 blocks of 1 KB, four waves
+  uint32_t off[BPW];
+  SR_DEV void init(int r0, int ld, int lane, int wid) {
 #pragma unroll
-  for (int i = 0; i < BPW; ++i) {
-    const int blk = wid * BPW + i;
-    uint32_t off;
-    if constexpr (KMAJ) {
-      const int row = blk * 8 + (lane >> 3);
-      const int c = (lane & 7) ^ kswz(row);
-      off = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(k0 + c * 8)) * 2u;
-    } else {
-      constexpr int CPR = R / 8, RPB = 64 / CPR;   // chunks per k-row, k-rows per block
-      const int k = blk * RPB + lane / CPR;
-      const int c = (lane % CPR) ^ rswz<R>(k);
-      off = ((uint32_t)(k0 + k) * (uint32_t)ld + (uint32_t)(r0 + c * 8)) * 2u;
+    for (int i = 0; i < BPW; ++i) {
+      const int blk = wid * BPW + i;
+      if constexpr (KMAJ) {
+        const int row = blk * 8 + (lane >> 3);
+        const int c = (lane & 7) ^ kswz(row);
+        off[i] = ((uint32_t)(r0 + row) * (uint32_t)ld + (uint32_t)(c * 8)) * 2u;
+      } else {
+        constexpr int CPR = R / 8, RPB = 64 / CPR;   // chunks per k-row, k-rows per block
+        const int k = blk * RPB + lane / CPR;
+        const int c = (lane % CPR) ^ rswz<R>(k);
+        off[i] = ((uint32_t)k * (uint32_t)ld + (uint32_t)(r0 + c * 8)) * 2u;
+      }
     }
-    // a fill past the last k-tile keeps the count of loads in flight uniform: it reads
-    // beyond every operand's extent (2 GiB at most), which returns zeros without a memory access
-    if (!valid) off = 0x80000000u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t*)(lds + blk * 512), 16, off, 0, 0, 0);
   }
+};
+
+// Issue one tile's fills.  delta: the wave-uniform byte offset of k0, or 0x80000000 for a fill
+// past the last k-tile, which keeps the count of loads in flight uniform: every offset then lies
+// at or beyond 2 GiB, past every operand's extent, and reads zeros without a memory access.
+// (It takes the offsets array: a function that takes the buffer resource together with the
+// TileFill structure, member or not, fails in the host compilation pass, which then drops the
+// kernels' launch stubs.)
+template <int BPW>
+SR_DEV void fill_issue(const uint32_t* off, __amdgpu_buffer_rsrc_t rs, bf16_t* lds, int wid, uint32_t delta) {
+#pragma unroll
+  for (int i = 0; i < BPW; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t*)(lds + (wid * BPW + i) * 512), 16, off[i] + delta, 0, 0,
+                                             0);
 }
 
 // Workgroups are handed to the eight XCDs round-robin by linear id.  Renumber them so that each
@@ -329,7 +343,7 @@ __global__ __launch_bounds__(256, OCC) void gemm_mfma_kernel(const bf16_t* __res
   static_assert(RPK < 16, "reads per k-step exceed the lgkmcnt range");
   __shared__ __attribute__((aligned(1024))) bf16_t smem[NST * STAGE];
 
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wid = wave_index();
   const int wm = wid >> 1, wn = wid & 1, h = lane >> 5;
   int tm, tn, split;
   tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn, split);
@@ -348,11 +362,16 @@ __global__ __launch_bounds__(256, OCC) void gemm_mfma_kernel(const bf16_t* __res
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  TileFill<BM, AK> fla;
+  TileFill<BN, BK> flb;
+  fla.init(m0, lda, lane, wid);
+  flb.init(n0, ldb, lane, wid);
   auto fill = [&](int t, int s) {
     bf16_t* st = smem + s * STAGE;
+    const uint32_t k0 = (uint32_t)(kbeg + t * GK);
     const bool valid = t < ntile;
-    fill_tile<BM, AK>(ra, st, m0, kbeg + t * GK, lda, valid);
-    fill_tile<BN, BK>(rb, st + BM * GK, n0, kbeg + t * GK, ldb, valid);
+    fill_issue<BM / 32>(fla.off, ra, st, wid, valid ? k0 * (AK ? 2u : 2u * (uint32_t)lda) : 0x80000000u);
+    fill_issue<BN / 32>(flb.off, rb, st + BM * GK, wid, valid ? k0 * (BK ? 2u : 2u * (uint32_t)ldb) : 0x80000000u);
   };
   const uint32_t sbase = lds_addr(smem);
   FA fad;
