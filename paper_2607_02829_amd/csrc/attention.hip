@@ -311,6 +311,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
   auto tile = [&](int t, auto stg) {
     constexpr int s0 = decltype(stg)::value;
     const bool rag = ragged && t + 1 == nt;
+    // tile t+2 into the stage of tile t-1, which every wave has left (the barrier that ended
+    // tile t-1); it then flies during tiles t and t+1
+    load(t + 2, (s0 + 2) % NSTG);
     // both units' score MFMAs first: unit 1's run while unit 0's softmax arithmetic does
     RawFrag<true> k0r[4], k1r[4];
     f32x16 sc0, sc1;
@@ -324,9 +327,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
       if (S - t * KT < 64) mask(sc1, t * KT + 32);
     }
     consume(stg, sc0, sc1);
-    wait_vm_lgkm0<kLoads>();   // tile t+1 resident (tile t+2's loads may still fly)
-    lds_barrier();             // every wave done with tile t's stage
-    load(t + 2, (s0 + 2) % NSTG);
+    wait_vm_lgkm0<kLoads>();   // tile t+1 resident: only tile t+2's loads may still fly
+    lds_barrier();             // ... for every wave, and every wave is done with tile t's stage
   };
   int t = 0;
   for (; t + NSTG <= nt; t += NSTG) {
@@ -558,6 +560,9 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
   auto tile = [&](int t, auto stg) {
     constexpr int s0 = decltype(stg)::value;
     const bool rag = ragged && t + 1 == nt;
+    // tile t+2 into the stage of tile t-1, which every wave has left (the barrier that ended
+    // tile t-1); it then flies during tiles t and t+1
+    load(t + 2, (s0 + 2) % NSTG);
     // both units' S^T / dP^T MFMAs first: unit 1's run while unit 0's arithmetic does
     RawFrag<true> k0r[4], v0r[4], k1r[4], v1r[4];
     f32x16 sv0, dp0, sv1, dp1;
@@ -576,9 +581,8 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
       grad(stg, IC<0>{}, sv0, dp0, t * KT, std::false_type{});
       grad(stg, IC<1>{}, sv1, dp1, t * KT + 32, std::false_type{});
     }
-    wait_vm_lgkm0<kLoads>();   // tile t+1 resident (tile t+2's loads may still fly)
-    lds_barrier();             // every wave done with tile t's stage
-    load(t + 2, (s0 + 2) % NSTG);
+    wait_vm_lgkm0<kLoads>();   // tile t+1 resident: only tile t+2's loads may still fly
+    lds_barrier();             // ... for every wave, and every wave is done with tile t's stage
   };
   int t = 0;
   for (; t + NSTG <= nt; t += NSTG) {
