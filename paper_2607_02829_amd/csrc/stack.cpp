@@ -117,7 +117,9 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   s.dbpart = c.take<float>(std::max<size_t>(dbp, 1) * 4);
   const size_t wmax = std::max<size_t>(std::max<size_t>(3 * D, F), 6 * D);
   s.part = c.take<float>((size_t)d.B * colsum_chunks(d.S) * wmax * 4);
-  s.lnpart = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
+  // LayerNorm parameter-gradient partials of LN2 and LN1 (pre-LN: their reductions run on the
+  // side stream, so each has its own buffer)
+  for (int k = 0; k < 2; ++k) s.lnpart[k] = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
   s.dmod = c.take<float>((size_t)d.B * 6 * D * 4);
   s.gvpart = d.kind == SR_BLOCK_ADALN ? c.take<float>(gemv_cols_scratch(d.B, 6 * d.D, d.D) * 4) : nullptr;
   // two of each buffer a weight-gradient GEMM reads on the side stream, so the main stream
@@ -331,6 +333,17 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
   enum { kFc2 = 0, kO = 1, kFc1 = 2, kQkv = 4 };
 
 
+  // pre-LN: the LayerNorm parameter gradients (column sums of the ln_bwd partials) are outputs
+  // only, so their reductions ride along with side-stream work that is forked anyway: LN2's with
+  // dW_o of the same block, LN1's with dW_fc2 of the next block (or at the end).  The joins that
+  // guard g1 and g0 also guard lnpart[0] and lnpart[1].
+  auto ln_reduce = [&](int k, float* dw, float* dbeta, hipStream_t ss) -> hipError_t {
+    if (!dw && !dbeta) return hipSuccess;
+    ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, ss);
+    return launch_reduce_cols(sc.lnpart[k], nln, d.B, 1, 2 * D, D, dw, dbeta, 0, ss);
+  };
+  const sr_block_grads* ln1_pending = nullptr;   // block whose LN1 reduction is still to run
+
   auto run = [&]() -> hipError_t {
     SR_TRY(side_stream(&side));
     SR_TRY(take_events(&ev));
@@ -356,9 +369,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(gate_grad(d, sc.g_res, s.m_out, sc.dmod, 5 * D, sc, st));
       }
       // FC2: dW2, db2; dz = (dm W2) * GELU'(z)
-      SR_TRY(on_side(kFc2, [&](hipStream_t ss) {
+      SR_TRY(on_side(kFc2, [&](hipStream_t ss) -> hipError_t {
+        if (ln1_pending) SR_TRY(ln_reduce(1, ln1_pending->ln1_w, ln1_pending->ln1_b, ss));
         return weight_grad("gemm_dw_fc2", d, g0, D, s.gz, F, g.w_fc2, g.b_fc2, sc, ss);
       }));
+      ln1_pending = nullptr;
       SR_TRY(join(kFc1 + par));   // dz[par] may still be read by dW_fc1 two blocks back
       {
         GemmDesc gd = desc(d, g0, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
@@ -381,14 +396,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
-                             d.B, S, D, sc.g_res2, ada ? nullptr : g1, sc.lnpart, st));
+                             d.B, S, D, sc.g_res2, ada ? nullptr : g1, sc.lnpart[0], st));
       }
-      {
+      if (ada) {   // dscale2 -> dmod[4D..5D), dshift2 -> dmod[3D..4D)
         ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
-        if (ada)   // dscale2 -> dmod[4D..5D), dshift2 -> dmod[3D..4D)
-          SR_TRY(launch_reduce_cols(sc.lnpart, nln, d.B, 0, 2 * D, D, sc.dmod + 4 * D, sc.dmod + 3 * D, 6 * D, st));
-        else if (g.ln2_w || g.ln2_b)
-          SR_TRY(launch_reduce_cols(sc.lnpart, nln, d.B, 1, 2 * D, D, g.ln2_w, g.ln2_b, 0, st));
+        SR_TRY(launch_reduce_cols(sc.lnpart[0], nln, d.B, 0, 2 * D, D, sc.dmod + 4 * D, sc.dmod + 3 * D, 6 * D, st));
       }
       if (ada) {
         // attention-branch gradient da = dh1 * gate1 and dgate1 = sum_s dh1 * a_out
@@ -399,7 +411,8 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       }
       // output projection: dWo, dbo; dO = da Wo (with the attention row statistic
       // delta = rowsum(dO * O) per head in the same epilogue when the head dim is 64)
-      SR_TRY(on_side(kO, [&](hipStream_t ss) {
+      SR_TRY(on_side(kO, [&](hipStream_t ss) -> hipError_t {
+        if (!ada) SR_TRY(ln_reduce(0, g.ln2_w, g.ln2_b, ss));
         return weight_grad("gemm_dw_o", d, g1, D, s.O, D, g.w_o, g.b_o, sc, ss);
       }));
       const bool fuse_delta = d.dtype == kBF16 && D / d.H == 64;
@@ -433,14 +446,13 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2,
-                             d.B, S, D, sc.g_res, ada ? nullptr : g0, sc.lnpart, st));
+                             d.B, S, D, sc.g_res, ada ? nullptr : g0, sc.lnpart[ada ? 0 : 1], st));
       }
-      {
+      if (ada) {   // dscale1 -> dmod[D..2D), dshift1 -> dmod[0..D)
         ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
-        if (ada)   // dscale1 -> dmod[D..2D), dshift1 -> dmod[0..D)
-          SR_TRY(launch_reduce_cols(sc.lnpart, nln, d.B, 0, 2 * D, D, sc.dmod + D, sc.dmod, 6 * D, st));
-        else if (g.ln1_w || g.ln1_b)
-          SR_TRY(launch_reduce_cols(sc.lnpart, nln, d.B, 1, 2 * D, D, g.ln1_w, g.ln1_b, 0, st));
+        SR_TRY(launch_reduce_cols(sc.lnpart[0], nln, d.B, 0, 2 * D, D, sc.dmod + D, sc.dmod, 6 * D, st));
+      } else {
+        ln1_pending = &g;
       }
       if (ada) {
         // dW_ada = dmod^T c ; db_ada = sum_b dmod ; dcond (+)= dmod W_ada
@@ -468,6 +480,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
       SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
     }
+    if (ln1_pending) SR_TRY(ln_reduce(1, ln1_pending->ln1_w, ln1_pending->ln1_b, st));
     for (int k = 0; k < kSlots; ++k) SR_TRY(join(k));   // every gradient is complete when st is
     return hipSuccess;
   };

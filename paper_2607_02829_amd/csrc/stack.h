@@ -21,7 +21,7 @@ struct BlockSaved {
 };
 
 struct Scratch {
-  float *g_res, *g_res2, *du, *delta, *wpart, *dbpart, *part, *lnpart, *dmod, *gvpart;
+  float *g_res, *g_res2, *du, *delta, *wpart, *dbpart, *part, *lnpart[2], *dmod, *gvpart;
   void *g_act[2], *dz[2], *dO, *dqkv[2];
 };
 
