@@ -2,11 +2,14 @@
 // deterministic top-k selector, plus the index-set validator.
 //
 // Random: per sample, the K tokens with the smallest counter-based SplitMix64 keys,
-// in ascending token order (see include/sr.h).  One workgroup per sample runs an
-// 8-pass radix select (8 bits per pass) for the K-th smallest key, recomputing the
-// keys on the fly (no key storage, so L is not bounded by LDS), then compacts the
-// tokens whose key is <= that threshold in index order with a block-wide scan.
-// Keys of one sample are distinct (mix is a bijection), so exactly K tokens pass.
+// in ascending token order (see include/sr.h).  One workgroup per sample computes
+// the keys once into LDS (up to kSelCache tokens; beyond that they are recomputed in
+// every pass) and runs a radix select, 8 bits per pass from the top, for the K-th
+// smallest key.  The descent stops at the first pass whose chosen digit bin is taken
+// whole (the K-th key is the largest in it): then exactly the keys whose top bits are
+// <= the chosen prefix are kept.  At L = 16200, K = 4050 that is two passes.  The
+// kept tokens are compacted in index order with a block-wide scan.  Keys of one
+// sample are distinct (mix is a bijection), so the last pass always ends the descent.
 //
 // Top-k: a wave per token evaluates the fp32 score in the fixed order of the
 // header (16-byte chunks round-robin over 64 lanes, xor butterfly), then one
@@ -48,12 +51,14 @@ SR_DEV int block_flag_scan(bool flag, int* wsum, int* total) {
 
 // One radix pass: among keys with (key & mask) == prefix, histogram the digit at
 // `shift`, find the digit holding the k-th smallest (1-based) and update prefix/k.
-// hist: 256 ints of LDS; sh: 2 words of LDS for the broadcast.
+// Returns true when k equals the count of the chosen digit's bin (every key matching
+// the new prefix is <= the k-th smallest).  hist: 256 ints of LDS; sh: 3 words of LDS
+// for the broadcast.
 template <typename KeyFn>
-SR_DEV void radix_pass(KeyFn key_of, int L, int shift, uint64_t& prefix, uint64_t& mask,
+SR_DEV bool radix_pass(KeyFn key_of, int L, int shift, uint64_t& prefix, uint64_t& mask,
                        int& k, int* hist, uint64_t* sh) {
   for (int t = threadIdx.x; t < 256; t += blockDim.x) hist[t] = 0;
-  if (threadIdx.x == 0) { sh[0] = 0; sh[1] = 1; }
+  if (threadIdx.x == 0) { sh[0] = 0; sh[1] = 1; sh[2] = 0; }
   __syncthreads();
   for (int i = threadIdx.x; i < L; i += blockDim.x) {
     uint64_t key = key_of(i);
@@ -82,36 +87,49 @@ SR_DEV void radix_pass(KeyFn key_of, int L, int shift, uint64_t& prefix, uint64_
     if (cnt > 0 && excl < k && k <= incl) {
       sh[0] = (uint64_t)threadIdx.x;
       sh[1] = (uint64_t)(k - excl);
+      sh[2] = (uint64_t)cnt;
     }
   }
   __syncthreads();
   uint64_t d = sh[0];
   k = (int)sh[1];
+  const bool whole = (uint64_t)k == sh[2];
   prefix |= d << shift;
   mask |= 255ull << shift;
   __syncthreads();
+  return whole;
 }
 
+constexpr int kSelCache = 19968;   // keys kept in LDS (156 KB) when L <= kSelCache
+
 __global__ __launch_bounds__(kSelThreads) void select_random_kernel(int L, int K, uint64_t seed,
-                                                                      uint64_t step, int32_t* idx) {
+                                                                     uint64_t step, int32_t* idx) {
+  __shared__ uint64_t kc[kSelCache];
   __shared__ int hist[256 + 4];
-  __shared__ uint64_t sh[2];
+  __shared__ uint64_t sh[3];
   __shared__ int wsum[kSelWaves];
   const int b = blockIdx.x;
   const uint64_t s_step = mix64(seed + (step + 1ull) * kGamma);
   const uint64_t s_b = mix64(s_step + ((uint64_t)b + 1ull) * kGamma);
   auto key_of = [&](int i) { return mix64(s_b + ((uint64_t)i + 1ull) * kGamma); };
+  const bool cached = L <= kSelCache;
+  if (cached) {
+    for (int i = threadIdx.x; i < L; i += blockDim.x) kc[i] = key_of(i);
+    __syncthreads();
+  }
+  auto key_at = [&](int i) { return cached ? kc[i] : key_of(i); };
 
   uint64_t prefix = 0, mask = 0;
   int k = K;
-  for (int shift = 56; shift >= 0; shift -= 8) radix_pass(key_of, L, shift, prefix, mask, k, hist, sh);
-  const uint64_t thr = prefix;   // the K-th smallest key
+  for (int shift = 56; shift >= 0; shift -= 8)
+    if (radix_pass(key_at, L, shift, prefix, mask, k, hist, sh)) break;
+  // exactly K keys have (key & mask) <= prefix: the chosen bin is taken whole
 
   int32_t* out = idx + (size_t)b * K;
   int base = 0;
   for (int i0 = 0; i0 < L; i0 += blockDim.x) {
     int i = i0 + threadIdx.x;
-    bool f = (i < L) && (key_of(i) <= thr);
+    bool f = (i < L) && ((key_at(i) & mask) <= prefix);
     int tot;
     int pos = block_flag_scan(f, wsum, &tot);
     if (f && base + pos < K) out[base + pos] = i;
@@ -154,7 +172,7 @@ __global__ __launch_bounds__(256) void topk_score_kernel(const T* __restrict__ x
 __global__ __launch_bounds__(kSelThreads) void select_topk_kernel(const float* __restrict__ score,
                                                                     int L, int K, int32_t* idx) {
   __shared__ int hist[256 + 4];
-  __shared__ uint64_t sh[2];
+  __shared__ uint64_t sh[3];
   __shared__ int wsum[kSelWaves];
   const int b = blockIdx.x;
   const float* sc = score + (size_t)b * L;

@@ -18,6 +18,7 @@ def _cfg(B, L, D=64, dtype="bf16", shared=0):
 @pytest.mark.parametrize("B,L,K", [
     (1, 128, 32), (8, 512, 128), (2, 8192, 2048), (1, 16200, 4050),   # the workloads' shapes
     (3, 5, 1), (2, 9, 9), (1, 1, 1), (1, 1025, 1000), (1, 20000, 3), (4, 3000, 2999),
+    (1, 19968, 4992), (2, 40000, 10000),   # keys held in LDS up to 19968 tokens, recomputed above
 ])
 def test_select_random_bitexact(B, L, K):
     import torch
