@@ -118,6 +118,24 @@ def time_steps(st: Step, steps: int, warmup: int, start: int = 0, profile_filter
     return (t1 - t0) * 1e3 / steps, ev0.elapsed_time(ev1) / steps, prof
 
 
+class TrunkStep:
+    """The whole trunk with a (2, n - 4, 2) dense-sparse-dense split (the deterministic
+    forecaster's (2, 8, 2) at 12 blocks): forward + backward of all n blocks per step."""
+
+    def __init__(self, w, seed: int = 42):
+        from paper_2607_02829_amd import device, inputs
+        from paper_2607_02829_amd.trunk import Trunk
+        self.split = (2, w.n_blocks - 4, 2)
+        params = inputs.params_to_storage(inputs.block_params(w), w.dtype)
+        self.trunk = Trunk(w, self.split, params, seed=seed)
+        self.x0 = device.to_device(inputs.to_storage(inputs.token_field(w, 0), w.dtype))
+        self.g3 = device.to_device(inputs.to_storage(inputs.upstream_grad(w), w.dtype))
+
+    def run(self, step: int):
+        self.trunk.forward(self.x0, step)
+        self.trunk.backward(self.g3)
+
+
 def kernel_breakdown(st: Step, step_index: int):
     """One profiled step with every launch group bracketed by events."""
     import torch
@@ -310,6 +328,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="d025", help="tiny | b5625 | c1406 | d025 | edm")
     ap.add_argument("--dense-steps", type=int, default=3, help="timed steps of the dense keep=100%% mode (0: skip)")
+    ap.add_argument("--trunk-steps", type=int, default=3,
+                    help="timed steps of the whole (2, n-4, 2) trunk, pre-LN workloads (0: skip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routing-sweep", action="store_true", help="skip the gather/scatter bandwidth sweep")
     ap.add_argument("--breakdown", action="store_true", help="print the per-kernel breakdown to stderr")
@@ -397,6 +417,22 @@ def main():
         del dn
         torch.cuda.empty_cache()
 
+    # ---------------------------------------------------------------- whole trunk (2, n-4, 2)
+    trunk = None
+    if args.trunk_steps > 0 and w.kind == "preln" and w.n_blocks >= 5 and w.backward:
+        tr = TrunkStep(w)
+        tr.run(0)
+        torch.cuda.synchronize()
+        tms, _, _ = time_steps(tr, args.trunk_steps, 1, start=1)
+        n1, n2, n3 = tr.split
+        trunk = {"split": list(tr.split), "ms_per_step": round(tms, 3),
+                 "speedup_vs_dense": round(dense["ms_per_step"] / tms, 3) if dense else None,
+                 "eq_speedup_estimate": round(w.n_blocks / (n1 + n2 * w.keep ** 2 + n3), 3),
+                 "outputs_finite": bool(torch.isfinite(tr.trunk.x3.float()).all().item()
+                                        and torch.isfinite(tr.trunk.g0.float()).all().item())}
+        del tr
+        torch.cuda.empty_cache()
+
     # routing kernels: in-step launch times (per-kernel breakdown) and a cache-evicting size sweep
     routing = {"in_step": {}, "sweep": []}
     for name in ("gather", "scatter_delta"):
@@ -434,6 +470,7 @@ def main():
         "stack_mfma_frac": round(blk_flops / (ms_step * 1e-3) / PEAK_BF16_FLOPS, 4),
         "dense": dense,
         "speedup_vs_dense": round(dense["ms_per_step"] / ms_step, 3) if dense else None,
+        "trunk": trunk,
         "peak_bytes": {"sparse": int(sparse_peak), "dense": dense["peak_bytes"] if dense else None,
                        "ratio": round(dense["peak_bytes"] / sparse_peak, 3) if dense else None},
         "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved_u, 2), "peak": peak_u, "unit": unit,

@@ -17,6 +17,13 @@ inputs.  Its output is rounded to the storage type once, at the end, before the
 scatter (the HIP path keeps an fp32 residual stream inside the stack and rounds
 at the same point).
 
+Trunk (Sec. 3.2 "Three-stage block partition", Eq. partition): n1 dense early
+blocks, the routed step on n2 middle blocks, n3 dense late blocks.  Each stage's
+output is rounded to the storage type once (the dense stages' outputs and the
+scatter's result are storage tensors on the HIP path too); the backward is the
+late stage's VJP, the routed step's VJP and the early stage's VJP, with the same
+roundings of the stage gradients.
+
 Pins: keep = 100% with I = 0..L-1 equals the dense stack (fp64, to rounding);
 unselected rows bit-identical; zero-initialised residual branches make x' == x
 bit for bit; per-sample independence.
@@ -85,3 +92,27 @@ def dense_forward(x, params, H, eps, kind="preln", cond=None):
     p64 = params_f64(params)
     c64 = None if cond is None else storage_to_f64(cond)
     return stack_fwd(storage_to_f64(x), p64, H, eps, kind, c64)
+
+
+def trunk_forward(x0, idx, params, split, H, eps):
+    """x0: (B, L, D) storage; params: n1 + n2 + n3 blocks (early, middle, late).
+    Returns (x3 fp64, caches of the three stages)."""
+    n1, n2, n3 = split
+    assert len(params) == n1 + n2 + n3
+    dtype = "bf16" if np.asarray(x0).dtype == np.uint16 else "f32"
+    x1, c_early = dense_forward(x0, params[:n1], H, eps)
+    x2, _, _, _, c_mid = routed_forward(f64_to_storage(x1, dtype), idx, params[n1:n1 + n2], H, eps)
+    x3, c_late = dense_forward(x2, params[n1 + n2:], H, eps)
+    return x3, (c_early, c_mid, c_late)
+
+
+def trunk_backward(g3, idx, params, split, caches):
+    """g3: (B, L, D) storage gradient of the trunk output.  Returns (g0 fp64, grads of
+    all n1 + n2 + n3 blocks in trunk order)."""
+    n1, n2, n3 = split
+    dtype = "bf16" if np.asarray(g3).dtype == np.uint16 else "f32"
+    c_early, c_mid, c_late = caches
+    g2, gr_late, _ = stack_bwd(storage_to_f64(g3), params_f64(params[n1 + n2:]), c_late)
+    g1, _, gr_mid, _ = routed_backward(f64_to_storage(g2, dtype), idx, params[n1:n1 + n2], c_mid)
+    g0, gr_early, _ = stack_bwd(storage_to_f64(g1), params_f64(params[:n1]), c_early)
+    return g0, gr_early + gr_mid + gr_late

@@ -1,0 +1,96 @@
+"""The whole block trunk with a dense-sparse-dense split (Sec. 3.2 "Three-stage block
+partition", Eq. partition; Alg. 1).
+
+A trunk of n1 + n2 + n3 pre-LN blocks runs its n1 early blocks densely on all L
+tokens, its n2 middle blocks on K routed tokens per sample (random selection,
+gather, blocks, residual-delta scatter into the early blocks' output), and its
+n3 late blocks densely again; the backward runs the three stages in reverse,
+with the routing VJP (gather of the gradient, the middle blocks' VJP, scatter of
+the gradient delta) between the two dense ones.  The split of the deterministic
+forecaster is (2, 8, 2) (Sec. 4.1, deterministic model; App. A.1); Eq. speedup
+(Sec. 3.2) estimates the trunk speedup over the dense trunk as N / (n1 + n2 r^2 + n3),
+counting attention cost only.
+
+Orchestration only: every step is a libsr entry point enqueued on the caller's
+current stream; the three stages have their own configs, parameters, gradients
+and saved activations and share one scratch buffer (their calls are ordered on
+the stream, and each backward joins its second stream before it returns).
+"""
+from __future__ import annotations
+
+from . import abi, device
+
+
+class Trunk:
+    """Device buffers and the launch sequence of one trunk forward + backward.
+
+    ``params_storage``: n1 + n2 + n3 per-block storage dicts (early, middle, late).
+    The dense stages read and write whole (B, L, D) sequences; the routed stage
+    scatters into the early stage's output in place, which is then the late
+    stage's input."""
+
+    def __init__(self, w, split, params_storage, K: int | None = None, seed: int = 42):
+        import torch
+        n1, n2, n3 = split
+        if min(n1, n2, n3) < 1:
+            raise ValueError(f"split {split}: every stage needs at least one block")
+        if len(params_storage) != n1 + n2 + n3:
+            raise ValueError(f"{len(params_storage)} blocks of parameters for split {split}")
+        if w.kind != "preln":
+            raise ValueError("the trunk is built for pre-LN blocks")
+        self.w, self.split, self.seed = w, tuple(split), seed
+        self.K = w.K if K is None else K
+        if not 1 <= self.K <= w.L:
+            raise ValueError(f"K={self.K} outside [1, L={w.L}]")
+        self.cfg = [device.config_for(w, n_blocks=n) for n in split]
+        bounds = (0, n1, n1 + n2, n1 + n2 + n3)
+        self.params = [device.DeviceParams(params_storage[bounds[i]:bounds[i + 1]], w.kind) for i in range(3)]
+        self.grads = [device.DeviceGrads(w, n, skip_unused=True) for n in split]
+        S = (w.L, self.K, w.L)
+        self.saved = []
+        scratch_bytes = 16
+        for c, s in zip(self.cfg, S):
+            sb, cb = abi.sr_workspace_bytes(c, s)
+            self.saved.append(torch.empty(max(sb, 16), dtype=torch.uint8, device="cuda"))
+            scratch_bytes = max(scratch_bytes, cb)
+        self.scratch = torch.empty(scratch_bytes, dtype=torch.uint8, device="cuda")
+        dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        B, L, D, K = w.B, w.L, w.D, self.K
+        self.x1 = torch.empty((B, L, D), dtype=dt, device="cuda")     # early output; routed stage writes into it
+        self.x3 = torch.empty_like(self.x1)                            # trunk output
+        self.g2 = torch.empty_like(self.x1)                            # late-stage input gradient, then dx of x1
+        self.g0 = torch.empty_like(self.x1)                            # trunk input gradient
+        self.idx = torch.empty((B, K), dtype=torch.int32, device="cuda")
+        self.h0 = torch.empty((B, K, D), dtype=dt, device="cuda")
+        self.h = torch.empty_like(self.h0)
+        self.gh = torch.empty_like(self.h0)
+        self.dh = torch.empty_like(self.h0)
+
+    def forward(self, x0, step: int):
+        """x0: (B, L, D) storage tensor (not modified).  Returns the trunk output x3."""
+        a, (ce, cm, cl), (pe, pm, pl) = abi, self.cfg, self.params
+        K = self.K
+        a.sr_dense_blocks_fwd(ce, pe.array, None, x0, self.x1, self.saved[0], self.scratch)
+        a.sr_select_indices(cm, K, a.SR_SEL_RANDOM, self.seed, step, None, None, self.idx)
+        a.sr_gather(cm, K, self.x1, self.idx, self.h0)
+        a.sr_sparse_blocks_fwd(cm, K, pm.array, None, self.h0, self.h, self.saved[1], self.scratch)
+        a.sr_scatter_delta(cm, K, self.x1, self.h, self.h0, self.idx)
+        a.sr_dense_blocks_fwd(cl, pl.array, None, self.x1, self.x3, self.saved[2], self.scratch)
+        return self.x3
+
+    def backward(self, g3):
+        """g3: (B, L, D) storage gradient of the trunk output (not modified).  Returns the
+        input gradient g0; the parameter gradients are in ``self.grads`` (early, middle, late)."""
+        a, (ce, cm, cl), (pe, pm, pl) = abi, self.cfg, self.params
+        ge, gm, gl = (g.array for g in self.grads)
+        K = self.K
+        a.sr_dense_blocks_bwd(cl, pl.array, None, self.saved[2], g3, self.g2, gl, None, self.scratch)
+        a.sr_gather(cm, K, self.g2, self.idx, self.gh)
+        a.sr_sparse_blocks_bwd(cm, K, pm.array, None, self.saved[1], self.gh, self.dh, gm, None, self.scratch)
+        a.sr_scatter_delta(cm, K, self.g2, self.dh, None, self.idx)
+        a.sr_dense_blocks_bwd(ce, pe.array, None, self.saved[0], self.g2, self.g0, ge, None, self.scratch)
+        return self.g0
+
+    def block_grads(self):
+        """The fp32 gradient tensors of all n1 + n2 + n3 blocks, in trunk order."""
+        return [g for stage in self.grads for g in stage.tensors]
