@@ -122,18 +122,46 @@ class TrunkStep:
     """The whole trunk with a (2, n - 4, 2) dense-sparse-dense split (the deterministic
     forecaster's (2, 8, 2) at 12 blocks): forward + backward of all n blocks per step."""
 
-    def __init__(self, w, seed: int = 42):
+    def __init__(self, w, seed: int = 42, split=None, K: int | None = None):
         from paper_2607_02829_amd import device, inputs
         from paper_2607_02829_amd.trunk import Trunk
-        self.split = (2, w.n_blocks - 4, 2)
-        params = inputs.params_to_storage(inputs.block_params(w), w.dtype)
-        self.trunk = Trunk(w, self.split, params, seed=seed)
+        self.split = (2, w.n_blocks - 4, 2) if split is None else tuple(split)
+        params = inputs.params_to_storage(inputs.block_params(w, sum(self.split)), w.dtype)
+        self.trunk = Trunk(w, self.split, params, K=K, seed=seed)
         self.x0 = device.to_device(inputs.to_storage(inputs.token_field(w, 0), w.dtype))
         self.g3 = device.to_device(inputs.to_storage(inputs.upstream_grad(w), w.dtype))
 
     def run(self, step: int):
         self.trunk.forward(self.x0, step)
         self.trunk.backward(self.g3)
+
+
+def trunk_sweep(w, dense_ms: float | None, steps: int = 3) -> dict:
+    """The trunk over the keep ratios of the paper's keep-ratio ablation at the (2, n-4, 2)
+    split, and over the block splits of its split ablation at r = 0.25 (Sec. 4.4, "Effect of
+    keep ratio" / "Effect of block split"): ms per fwd + bwd step and speedup over the dense
+    n-block step.  K = floor(r L) per sample; r = 1 routes every token through the middle."""
+    import math
+    import torch
+    out = {"keep": [], "split": []}
+    n = w.n_blocks
+    runs = [("keep", (2, n - 4, 2), r) for r in (0.10, 0.25, 0.50, 0.75, 1.0)]
+    runs += [("split", s, 0.25) for s in ((1, n - 2, 1), (3, n - 6, 3), (4, n - 8, 4)) if min(s) >= 1]
+    for kind, split, r in runs:
+        K = max(1, math.floor(r * w.L))
+        tr = TrunkStep(w, split=split, K=K)
+        tr.run(0)
+        torch.cuda.synchronize()
+        tms, _, _ = time_steps(tr, steps, 1, start=1)
+        n1, n2, n3 = split
+        rec = {"split": list(split), "keep": r, "K": K, "ms_per_step": round(tms, 3),
+               "speedup_vs_dense": round(dense_ms / tms, 3) if dense_ms else None,
+               "eq_speedup_estimate": round(n / (n1 + n2 * r * r + n3), 3)}
+        out[kind].append(rec)
+        log(f"trunk {kind}: split {split} r={r} K={K}: {tms:.2f} ms, speedup {rec['speedup_vs_dense']}")
+        del tr
+        torch.cuda.empty_cache()
+    return out
 
 
 def kernel_breakdown(st: Step, step_index: int):
@@ -330,6 +358,8 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=3, help="timed steps of the dense keep=100%% mode (0: skip)")
     ap.add_argument("--trunk-steps", type=int, default=3,
                     help="timed steps of the whole (2, n-4, 2) trunk, pre-LN workloads (0: skip)")
+    ap.add_argument("--trunk-sweep", action="store_true",
+                    help="also time the trunk over keep ratios 0.10-1.0 and block splits (pre-LN workloads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routing-sweep", action="store_true", help="skip the gather/scatter bandwidth sweep")
     ap.add_argument("--breakdown", action="store_true", help="print the per-kernel breakdown to stderr")
@@ -432,6 +462,8 @@ def main():
                                         and torch.isfinite(tr.trunk.g0.float()).all().item())}
         del tr
         torch.cuda.empty_cache()
+        if args.trunk_sweep:
+            trunk["sweep"] = trunk_sweep(w, dense["ms_per_step"] if dense else None)
 
     # routing kernels: in-step launch times (per-kernel breakdown) and a cache-evicting size sweep
     routing = {"in_step": {}, "sweep": []}
