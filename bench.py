@@ -122,12 +122,12 @@ class TrunkStep:
     """The whole trunk with a (2, n - 4, 2) dense-sparse-dense split (the deterministic
     forecaster's (2, 8, 2) at 12 blocks): forward + backward of all n blocks per step."""
 
-    def __init__(self, w, seed: int = 42, split=None, K: int | None = None):
+    def __init__(self, w, seed: int = 42, split=None, K: int | None = None, select: str = "random"):
         from paper_2607_02829_amd import device, inputs
         from paper_2607_02829_amd.trunk import Trunk
         self.split = (2, w.n_blocks - 4, 2) if split is None else tuple(split)
         params = inputs.params_to_storage(inputs.block_params(w, sum(self.split)), w.dtype)
-        self.trunk = Trunk(w, self.split, params, K=K, seed=seed)
+        self.trunk = Trunk(w, self.split, params, K=K, seed=seed, select=select)
         self.x0 = device.to_device(inputs.to_storage(inputs.token_field(w, 0), w.dtype))
         self.g3 = device.to_device(inputs.to_storage(inputs.upstream_grad(w), w.dtype))
 
@@ -455,13 +455,23 @@ def main():
         torch.cuda.synchronize()
         tms, _, _ = time_steps(tr, args.trunk_steps, 1, start=1)
         n1, n2, n3 = tr.split
-        trunk = {"split": list(tr.split), "ms_per_step": round(tms, 3),
-                 "speedup_vs_dense": round(dense["ms_per_step"] / tms, 3) if dense else None,
-                 "eq_speedup_estimate": round(w.n_blocks / (n1 + n2 * w.keep ** 2 + n3), 3),
-                 "outputs_finite": bool(torch.isfinite(tr.trunk.x3.float()).all().item()
-                                        and torch.isfinite(tr.trunk.g0.float()).all().item())}
+        finite_trunk = bool(torch.isfinite(tr.trunk.x3.float()).all().item()
+                            and torch.isfinite(tr.trunk.g0.float()).all().item())
         del tr
         torch.cuda.empty_cache()
+        # the attention-score selector (top-K by attention received in the last dense-early
+        # block) in place of random selection: its overhead per step
+        tra = TrunkStep(w, select="attn")
+        tra.run(0)
+        torch.cuda.synchronize()
+        ams, _, _ = time_steps(tra, args.trunk_steps, 1, start=1)
+        del tra
+        torch.cuda.empty_cache()
+        trunk = {"split": list((2, w.n_blocks - 4, 2)), "ms_per_step": round(tms, 3),
+                 "attn_selector_ms_per_step": round(ams, 3), "attn_selector_overhead_ms": round(ams - tms, 3),
+                 "speedup_vs_dense": round(dense["ms_per_step"] / tms, 3) if dense else None,
+                 "eq_speedup_estimate": round(w.n_blocks / (n1 + n2 * w.keep ** 2 + n3), 3),
+                 "outputs_finite": finite_trunk}
         if args.trunk_sweep:
             trunk["sweep"] = trunk_sweep(w, dense["ms_per_step"] if dense else None)
 

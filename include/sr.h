@@ -195,6 +195,30 @@ SR_API sr_status sr_dense_blocks_bwd(const sr_config* cfg, const sr_block_params
 SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx,
                               int32_t* ok_dev, void* stream);
 
+/* Attention received per token, for the attention-score selector (top-K by
+ * self-attention score from the last dense-early block: Sec. 4.4 "Random vs. learned
+ * token selection", Tab. selection).  For block `block` (0-based) of the forward that
+ * wrote `saved` on S tokens per sample (sr_sparse_blocks_fwd, or S = L for
+ * sr_dense_blocks_fwd):
+ *   colsum[b,h,j] = sum over i < S of P_h[i,j],  P_h = softmax_j(q_i . k_j / sqrt(hd)),
+ * the forward's probabilities (recomputed from its saved q, k and row log-sum-exp).
+ *   saved: that forward's buffer, at least sr_workspace_bytes(cfg, S) bytes, unchanged
+ *          since the forward (the call only reads it).
+ *   colsum: [B,H,S] fp32 out, overwritten.  Sums run in a fixed order (deterministic).
+ * Per head, the S column sums add up to S up to rounding (every row of P sums to 1). */
+SR_API sr_status sr_attention_colsums(const sr_config* cfg, int32_t S, const void* saved,
+                               size_t saved_bytes, int32_t block, float* colsum,
+                               void* stream);
+
+/* Top-K by given scores: per sample b, score_j = sum over p < parts of planes[b,p,j],
+ * added in fp32 in plane order starting from +0 (parts = H with sr_attention_colsums'
+ * output gives the attention received summed over heads); the K largest scores are
+ * kept, ties to the lower token index, idx ascending.
+ *   planes: [B,parts,L] fp32 (or [1,parts,L] with idx_shared), finite and >= 0.
+ *   idx: [B,K] int32 out (or [1,K] with idx_shared); 1 <= K <= L, parts >= 1. */
+SR_API sr_status sr_select_topk_scores(const sr_config* cfg, int32_t K, const float* planes,
+                                int32_t parts, int32_t* idx, void* stream);
+
 /* Launch timing for measurement (not needed by the method).  After
  * sr_profile_start, every library launch group whose name contains `name_filter`
  * ("" or NULL = all) is bracketed by HIP events on its own stream.  With no filter the
@@ -204,7 +228,8 @@ SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int3
  * sr_profile_stop waits for those events, stops recording and writes one line per
  * name: "<name> <launches> <total_ms> <algorithmic_flops> <algorithmic_bytes>\n"
  * into `out` (NUL-terminated, truncated to out_bytes); *needed receives the full
- * size.  Names: select_random, select_topk, gather, scatter_delta, ln_fwd, ln_bwd,
+ * size.  Names: select_random, select_topk, select_topk_scores, attn_colsum, gather,
+ * scatter_delta, ln_fwd, ln_bwd,
  * gemm_<op> (qkv, o, fc1, fc2, dx_fc2, dx_fc1, dx_o, dx_qkv, dw_<op>), attn_fwd,
  * attn_bwd_dkv, attn_bwd_dq, attn_bwd_delta, reduce, colsum, convert, mod. */
 SR_API sr_status sr_profile_start(const char* name_filter);

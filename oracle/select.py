@@ -47,6 +47,23 @@ Pins: the result lies within the fp32 summation error bound of the exact fp64
 sum; fp64-ranked brute force gives the same set when no near-tie exists; planted
 exact ties resolve to the lower index; K = L keeps all tokens; a hand-computed
 case where the butterfly order changes the fp32 result.
+
+Attention-score selection (Sec. 4.4 "Random vs. learned token selection";
+Tab. selection: top-K by self-attention score from the last dense-early block)
+------------------------------------------------------------------------------
+The paper names the selector but not the score.  Reading taken: the score of
+token j is the attention it receives, a_j = sum_h sum_i P_h[i, j], with P_h the
+softmax(q k^T / sqrt(hd)) of head h of that block's forward over all S tokens.
+``attention_colsums`` gives the per-head column sums colsum[b, h, j] in fp64.
+The ranking takes per-head planes in fp32 and adds them in head order from +0
+(the planes the HIP path computes are the input of its selection, so the order
+of that fp32 sum is part of the definition); then the K largest, ties to the
+lower index, ascending, as for the top-k selector above.
+
+Pins: every row of P sums to 1, so each head's column sums add up to S; zero
+queries give uniform rows, so every column sum is 1; a loop-written softmax on a
+tiny case; permuting the tokens permutes the column sums; planted ties in the
+planes resolve to the lower index; one plane reduces to the top-k ranking.
 """
 from __future__ import annotations
 
@@ -119,7 +136,38 @@ def topk_score(x_t: np.ndarray, x_prev: np.ndarray) -> np.ndarray:
 
 def select_topk(x_t: np.ndarray, x_prev: np.ndarray, K: int) -> np.ndarray:
     """(B, K) int32: the K largest scores, ties to the lower index, ascending."""
-    score = topk_score(x_t, x_prev)
+    return _largest_k(topk_score(x_t, x_prev), K)
+
+
+def attention_colsums(q: np.ndarray, k: np.ndarray) -> np.ndarray:
+    """q, k: (B, H, S, hd) fp64, a block's queries and keys.  Returns (B, H, S) fp64:
+    colsum[b, h, j] = sum_i softmax_j(q_i . k_j / sqrt(hd))."""
+    B, H, S, hd = q.shape
+    out = np.empty((B, H, S), dtype=np.float64)
+    for b in range(B):
+        for h in range(H):
+            s = q[b, h] @ k[b, h].T / np.sqrt(hd)
+            e = np.exp(s - s.max(axis=1, keepdims=True))
+            P = e / e.sum(axis=1, keepdims=True)
+            out[b, h] = P.sum(axis=0)
+    return out
+
+
+def planes_score(planes: np.ndarray) -> np.ndarray:
+    """planes: (B, parts, L) float32 -> (B, L) float32, summed in plane order from +0."""
+    planes = np.asarray(planes, dtype=np.float32)
+    s = np.zeros((planes.shape[0], planes.shape[2]), dtype=np.float32)
+    for p in range(planes.shape[1]):
+        s = (s + planes[:, p]).astype(np.float32)
+    return s
+
+
+def select_topk_planes(planes: np.ndarray, K: int) -> np.ndarray:
+    """(B, K) int32: the K largest plane-summed scores, ties to the lower index, ascending."""
+    return _largest_k(planes_score(planes), K)
+
+
+def _largest_k(score: np.ndarray, K: int) -> np.ndarray:
     B, L = score.shape
     if not 0 <= K <= L:
         raise ValueError("need 0 <= K <= L")

@@ -24,7 +24,7 @@ PARAM_FIELDS = ("ln1_w", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o", "ln2_w", "ln2_
 EXPORTS = ("sr_last_error", "sr_version", "sr_workspace_bytes", "sr_select_scratch_bytes",
            "sr_select_indices", "sr_gather", "sr_scatter_delta", "sr_sparse_blocks_fwd",
            "sr_sparse_blocks_bwd", "sr_dense_blocks_fwd", "sr_dense_blocks_bwd", "sr_validate_indices",
-           "sr_profile_start", "sr_profile_stop")
+           "sr_attention_colsums", "sr_select_topk_scores", "sr_profile_start", "sr_profile_stop")
 
 
 class SrLibraryMissing(RuntimeError):
@@ -78,6 +78,8 @@ def lib(path: str = LIB_PATH):
         "sr_dense_blocks_fwd": ([CP, P, P, P, P, P, SZ, P, SZ, P], I32),
         "sr_dense_blocks_bwd": ([CP, P, P, P, SZ, P, P, P, P, P, SZ, P], I32),
         "sr_validate_indices": ([CP, I32, P, P, P], I32),
+        "sr_attention_colsums": ([CP, I32, P, SZ, I32, P, P], I32),
+        "sr_select_topk_scores": ([CP, I32, P, I32, P, P], I32),
         "sr_profile_start": ([ctypes.c_char_p], I32),
         "sr_profile_stop": ([ctypes.c_char_p, SZ, ctypes.POINTER(SZ)], I32),
     }
@@ -179,6 +181,15 @@ def sr_dense_blocks_bwd(cfg, params, cond, saved, dx_out, dx_in, grads, dcond, s
 
 def sr_validate_indices(cfg, K, idx, ok_dev, stream=None):
     _check(lib().sr_validate_indices(ctypes.byref(cfg), K, _p(idx), _p(ok_dev), _stream(stream)))
+
+
+def sr_attention_colsums(cfg, S, saved, block, colsum, stream=None):
+    _check(lib().sr_attention_colsums(ctypes.byref(cfg), S, _p(saved), _nbytes(saved), block, _p(colsum),
+                                      _stream(stream)))
+
+
+def sr_select_topk_scores(cfg, K, planes, parts, idx, stream=None):
+    _check(lib().sr_select_topk_scores(ctypes.byref(cfg), K, _p(planes), parts, _p(idx), _stream(stream)))
 
 
 def sr_profile_start(name_filter: str = "") -> None:

@@ -4,6 +4,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "../../include/sr.h"
 #include "profile.h"
@@ -250,6 +251,42 @@ sr_status sr_dense_blocks_bwd(const sr_config* cfg, const sr_block_params* param
   if (s != SR_OK) return s;
   return sr_sparse_blocks_bwd(cfg, cfg->L, params, cond, saved, saved_bytes, dx_out, dx_in, grads, dcond, scratch,
                               scratch_bytes, stream);
+}
+
+sr_status sr_attention_colsums(const sr_config* cfg, int32_t S, const void* saved, size_t saved_bytes, int32_t block,
+                               float* colsum, void* stream) {
+  sr_status s = check_cfg(cfg);
+  if (s != SR_OK) return s;
+  SR_CHECK(S >= 1 && S <= cfg->L, SR_ESHAPE, "S=%d outside [1, L=%d]", S, cfg->L);
+  SR_CHECK(block >= 0 && block < cfg->n_blocks, SR_EINVAL, "block %d outside [0, n_blocks=%d)", block,
+           cfg->n_blocks);
+  if ((s = check_ws(cfg, S, saved, saved_bytes, nullptr, 0, false)) != SR_OK) return s;
+  SR_PTR(colsum, "colsum");
+  sr::Dims d = dims_of(cfg, S);
+  std::vector<sr::BlockSaved> bs((size_t)cfg->n_blocks);
+  sr::layout_saved(d, (char*)saved, bs.data());
+  const int hd = cfg->D / cfg->H;
+  hipStream_t st = (hipStream_t)stream;
+  sr::ProfScope ps("attn_colsum", 2.0 * cfg->B * cfg->H * (double)S * S * hd,
+                   (double)cfg->B * S * 2 * cfg->D * elt_of(cfg->dtype) + 8.0 * cfg->B * cfg->H * S, st);
+  return hip_status(sr::launch_attn_colsum(d.dtype, bs[block].qkv, bs[block].lse, colsum, cfg->B, S, cfg->H, cfg->D,
+                                           st),
+                    "attn_colsum");
+}
+
+sr_status sr_select_topk_scores(const sr_config* cfg, int32_t K, const float* planes, int32_t parts, int32_t* idx,
+                                void* stream) {
+  sr_status s = check_cfg(cfg, true);
+  if (s != SR_OK) return s;
+  SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
+  SR_CHECK(parts >= 1, SR_EINVAL, "parts=%d must be >= 1", parts);
+  const int rows = cfg->idx_shared ? 1 : cfg->B;
+  SR_CHECK((size_t)rows * parts * cfg->L * 4 < (1ull << 31), SR_EUNSUPPORTED, "score planes beyond 2 GiB");
+  SR_PTR(planes, "planes");
+  SR_PTR(idx, "idx");
+  hipStream_t st = (hipStream_t)stream;
+  sr::ProfScope ps("select_topk_scores", 0, (double)rows * parts * cfg->L * 4 + (double)rows * K * 4, st);
+  return hip_status(sr::launch_select_topk_planes(rows, cfg->L, K, parts, planes, idx, st), "select_topk_scores");
 }
 
 sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx, int32_t* ok_dev, void* stream) {

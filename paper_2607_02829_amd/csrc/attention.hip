@@ -713,6 +713,111 @@ __global__ __launch_bounds__(64) void attn_bwd_dkv_simple(const Ta* __restrict__
   }
 }
 
+// ------------------------------------------------------------------------- column sums
+// colsum[b,h,j] = sum over the S queries i of P[i,j], P = exp2(s * sl2 - lse) the forward's
+// probabilities: the attention token j receives in head h.  MFMA: the dK/dV kernel's score
+// half; a wave owns 32 keys (key per lane) and streams 64-query tiles; each lane sums its
+// 16 query rows per unit in tile, unit and row order, then the two half-waves (which hold
+// the other 16 rows of each unit) are added.  Deterministic.
+__global__ __launch_bounds__(256, 2) void attn_colsum_mfma(const bf16_t* __restrict__ qkv,
+                                                           const float* __restrict__ lse,
+                                                           float* __restrict__ colsum, int S, int H, int D,
+                                                           float sl2) {
+  __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * TE];   // stage: Q tile
+  __shared__ __attribute__((aligned(16))) float fsm[NSTG * KT];     // stage: lse of the tile's rows
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
+  const int b = blockIdx.z, hh = blockIdx.y;
+  const size_t ld = 3 * (size_t)D;
+  const bf16_t* kp = qkv + (size_t)b * S * ld + D + hh * HD;
+  const int mykey = blockIdx.x * QW + wid * 32 + l32;
+  const int nt = (S + KT - 1) / KT;
+  const bool ragged = S % KT != 0;
+
+  bf16x8 kf[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) kf[ks] = mykey < S ? ld8(kp + (size_t)mykey * ld + ks * 16 + 8 * h32) : zero8();
+
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
+  const __amdgpu_buffer_rsrc_t rl = make_rsrc(lse, (uint32_t)((size_t)gridDim.z * H * S * 4));
+  const uint32_t qbase = (uint32_t)(((size_t)b * S * ld + hh * HD) * 2);
+  const uint32_t lbase = (uint32_t)(((size_t)b * H + hh) * S * 4);
+  auto load = [&](int t, int s) {
+    tile_load(rq, qbase, (uint32_t)ld, t * KT, smem + s * TE);
+    const uint32_t lo = lbase + (uint32_t)(t * KT + lane) * 4u;
+    if (wid == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_ptr_t*)(fsm + s * KT), 4, lo, 0, 0, 0);
+  };
+  float csum = 0.f;
+  auto unit = [&](int s, int u, int q0, auto rag) {
+    const bf16_t* Qs = smem + s * TE;
+    f32x16 sv;
+    zero16(sv);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) sv = mfma(row_frag(Qs, u * 32, ks), kf[ks], sv);
+    const float* ls = fsm + s * KT + u * 32;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int ql = srow(r, h32);
+      float p = ex2(fmaf(sv[r], sl2, -ls[ql]));
+      if constexpr (decltype(rag)::value) {
+        if (q0 + ql >= S) p = 0.f;
+      }
+      csum += p;
+    }
+  };
+
+  load(0, 0);
+  if (nt > 1) load(1, 1);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  auto tile = [&](int t, auto stg) {
+    constexpr int s0 = decltype(stg)::value, s2 = (s0 + 2) % NSTG;
+    const bool rag = ragged && t + 1 == nt;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (rag) unit(s0, u, t * KT + u * 32, std::true_type{});
+      else unit(s0, u, t * KT + u * 32, std::false_type{});
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();   // tile t+1 resident; tile t's stage no longer read
+    if (t + 2 < nt) load(t + 2, s2);
+  };
+  int t = 0;
+  for (; t + NSTG <= nt; t += NSTG) {
+    tile(t, IC<0>{});
+    tile(t + 1, IC<1>{});
+    tile(t + 2, IC<2>{});
+  }
+  if (t < nt) tile(t, IC<0>{});
+  if (t + 1 < nt) tile(t + 1, IC<1>{});
+  __builtin_amdgcn_s_waitcnt(0);
+
+  csum += __shfl_xor(csum, 32, 64);
+  if (h32 == 0 && mykey < S) colsum[((size_t)b * H + hh) * S + mykey] = csum;
+}
+
+template <typename Ta, int HDT>
+__global__ __launch_bounds__(64) void attn_colsum_simple(const Ta* __restrict__ qkv, const float* __restrict__ lse,
+                                                         float* __restrict__ colsum, int S, int H, int D,
+                                                         float sl2) {
+  const int b = blockIdx.z, hh = blockIdx.y;
+  const int k = blockIdx.x * 64 + threadIdx.x;
+  if (k >= S) return;
+  const size_t ld = 3 * (size_t)D;
+  const Ta* base = qkv + (size_t)b * S * ld;
+  float kv[HDT];
+#pragma unroll
+  for (int d = 0; d < HDT; ++d) kv[d] = to_f32<Ta>(base[(size_t)k * ld + D + hh * HDT + d]);
+  float acc = 0.f;
+  for (int q = 0; q < S; ++q) {
+    const Ta* qr = base + (size_t)q * ld + hh * HDT;
+    float s = 0.f;
+#pragma unroll
+    for (int d = 0; d < HDT; ++d) s = fmaf(to_f32<Ta>(qr[d]), kv[d], s);
+    acc += exp2f(s * sl2 - lse[((size_t)b * H + hh) * S + q]);
+  }
+  colsum[((size_t)b * H + hh) * S + k] = acc;
+}
+
 // ------------------------------------------------------------------------------ launchers
 
 static inline float attn_sl2(int hd) { return 1.4426950408889634f / sqrtf((float)hd); }
@@ -779,6 +884,29 @@ hipError_t launch_attn_bwd(int dtype, const void* qkv, const void* dO, const flo
   if (dtype == kBF16)
     return bwd_simple((const bf16_t*)qkv, (const bf16_t*)dO, lse, delta, (bf16_t*)dqkv, B, S, H, D, hd, st);
   return bwd_simple((const float*)qkv, (const float*)dO, lse, delta, (float*)dqkv, B, S, H, D, hd, st);
+}
+
+template <typename Ta>
+static hipError_t colsum_simple(const Ta* qkv, const float* lse, float* colsum, int B, int S, int H, int D, int hd,
+                                hipStream_t st) {
+  dim3 g((S + 63) / 64, H, B);
+  const float sl2 = attn_sl2(hd);
+  if (hd == 32) hipLaunchKernelGGL((attn_colsum_simple<Ta, 32>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
+  else if (hd == 64) hipLaunchKernelGGL((attn_colsum_simple<Ta, 64>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
+  else hipLaunchKernelGGL((attn_colsum_simple<Ta, 128>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_colsum(int dtype, const void* qkv, const float* lse, float* colsum, int B, int S, int H, int D,
+                              hipStream_t st) {
+  const int hd = D / H;
+  if (attn_uses_mfma(dtype, hd)) {
+    dim3 g((S + QW - 1) / QW, H, B);
+    hipLaunchKernelGGL(attn_colsum_mfma, g, dim3(256), 0, st, (const bf16_t*)qkv, lse, colsum, S, H, D, attn_sl2(hd));
+    return hipGetLastError();
+  }
+  if (dtype == kBF16) return colsum_simple((const bf16_t*)qkv, lse, colsum, B, S, H, D, hd, st);
+  return colsum_simple((const float*)qkv, lse, colsum, B, S, H, D, hd, st);
 }
 
 }  // namespace sr

@@ -169,16 +169,31 @@ __global__ __launch_bounds__(256) void topk_score_kernel(const T* __restrict__ x
   if (lane == 0) score[row] = acc;
 }
 
+constexpr int kTopkCache = 32768;   // keys kept in LDS (128 KB) when L <= kTopkCache
+
+// The score of token i is the fp32 sum of `parts` planes of L scores each, added in plane
+// order from +0 (one plane: the score itself).
 __global__ __launch_bounds__(kSelThreads) void select_topk_kernel(const float* __restrict__ score,
-                                                                    int L, int K, int32_t* idx) {
+                                                                    int parts, int L, int K, int32_t* idx) {
+  __shared__ uint32_t kc[kTopkCache];
   __shared__ int hist[256 + 4];
   __shared__ uint64_t sh[3];
   __shared__ int wsum[kSelWaves];
   const int b = blockIdx.x;
-  const float* sc = score + (size_t)b * L;
+  const float* sc = score + (size_t)b * parts * L;
   // Scores are >= +0, so their bit patterns order like the values; the complement
   // turns "largest" into "smallest".
-  auto key_of = [&](int i) { return (uint64_t)(~__float_as_uint(sc[i])); };
+  auto key_from = [&](int i) {
+    float s = 0.0f;
+    for (int p = 0; p < parts; ++p) s = __fadd_rn(s, sc[(size_t)p * L + i]);
+    return ~__float_as_uint(s);
+  };
+  const bool cached = L <= kTopkCache;
+  if (cached) {
+    for (int i = threadIdx.x; i < L; i += blockDim.x) kc[i] = key_from(i);
+    __syncthreads();
+  }
+  auto key_of = [&](int i) { return (uint64_t)(cached ? kc[i] : key_from(i)); };
   uint64_t prefix = 0, mask = 0;
   int k = K;
   for (int shift = 24; shift >= 0; shift -= 8) radix_pass(key_of, L, shift, prefix, mask, k, hist, sh);
@@ -237,7 +252,13 @@ hipError_t launch_select_topk(int dtype, int rows, int L, int D, int K, const vo
                        ntok, D, score);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(select_topk_kernel, dim3(rows), dim3(kSelThreads), 0, st, score, L, K, idx);
+  hipLaunchKernelGGL(select_topk_kernel, dim3(rows), dim3(kSelThreads), 0, st, score, 1, L, K, idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_topk_planes(int rows, int L, int K, int parts, const float* planes, int32_t* idx,
+                                     hipStream_t st) {
+  hipLaunchKernelGGL(select_topk_kernel, dim3(rows), dim3(kSelThreads), 0, st, planes, parts, L, K, idx);
   return hipGetLastError();
 }
 

@@ -67,6 +67,8 @@ struct GemmDesc {
 hipError_t launch_select_random(int rows, int L, int K, uint64_t seed, uint64_t step, int32_t* idx, hipStream_t st);
 hipError_t launch_select_topk(int dtype, int rows, int L, int D, int K, const void* xt, const void* xp, float* score,
                               int32_t* idx, hipStream_t st);
+hipError_t launch_select_topk_planes(int rows, int L, int K, int parts, const float* planes, int32_t* idx,
+                                     hipStream_t st);
 hipError_t launch_validate(const int32_t* idx, int rows, int K, int L, int32_t* ok, hipStream_t st);
 
 hipError_t launch_gather(int elt, int B, int L, int K, int D, const void* x, const int32_t* idx, void* h0, int shared,
@@ -109,6 +111,8 @@ void weight_grad_scratch(int M, int N, int K, size_t* part_floats, size_t* dbpar
 bool attn_uses_mfma(int dtype, int hd);
 hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int B, int S, int H, int D,
                            hipStream_t st);
+hipError_t launch_attn_colsum(int dtype, const void* qkv, const float* lse, float* colsum, int B, int S, int H, int D,
+                              hipStream_t st);
 hipError_t launch_attn_bwd(int dtype, const void* qkv, const void* dO, const float* lse, const float* delta,
                            void* dqkv, int B, int S, int H, int D, hipStream_t st);
 

@@ -2,8 +2,9 @@
 partition", Eq. partition; Alg. 1).
 
 A trunk of n1 + n2 + n3 pre-LN blocks runs its n1 early blocks densely on all L
-tokens, its n2 middle blocks on K routed tokens per sample (random selection,
-gather, blocks, residual-delta scatter into the early blocks' output), and its
+tokens, its n2 middle blocks on K routed tokens per sample (random selection, or
+top-K by attention received in the last early block; gather, blocks,
+residual-delta scatter into the early blocks' output), and its
 n3 late blocks densely again; the backward runs the three stages in reverse,
 with the routing VJP (gather of the gradient, the middle blocks' VJP, scatter of
 the gradient delta) between the two dense ones.  The split of the deterministic
@@ -29,7 +30,10 @@ class Trunk:
     scatters into the early stage's output in place, which is then the late
     stage's input."""
 
-    def __init__(self, w, split, params_storage, K: int | None = None, seed: int = 42):
+    def __init__(self, w, split, params_storage, K: int | None = None, seed: int = 42, select: str = "random"):
+        """``select``: "random" (the method's selector) or "attn" (top-K by the attention each
+        token receives in the last dense-early block, summed over heads: the paper's
+        attention-score ablation)."""
         import torch
         n1, n2, n3 = split
         if min(n1, n2, n3) < 1:
@@ -38,7 +42,9 @@ class Trunk:
             raise ValueError(f"{len(params_storage)} blocks of parameters for split {split}")
         if w.kind != "preln":
             raise ValueError("the trunk is built for pre-LN blocks")
-        self.w, self.split, self.seed = w, tuple(split), seed
+        if select not in ("random", "attn"):
+            raise ValueError(f"unknown selector {select!r}")
+        self.w, self.split, self.seed, self.select = w, tuple(split), seed, select
         self.K = w.K if K is None else K
         if not 1 <= self.K <= w.L:
             raise ValueError(f"K={self.K} outside [1, L={w.L}]")
@@ -65,13 +71,18 @@ class Trunk:
         self.h = torch.empty_like(self.h0)
         self.gh = torch.empty_like(self.h0)
         self.dh = torch.empty_like(self.h0)
+        self.colsum = (torch.empty((B, w.H, L), dtype=torch.float32, device="cuda") if select == "attn" else None)
 
     def forward(self, x0, step: int):
         """x0: (B, L, D) storage tensor (not modified).  Returns the trunk output x3."""
         a, (ce, cm, cl), (pe, pm, pl) = abi, self.cfg, self.params
         K = self.K
         a.sr_dense_blocks_fwd(ce, pe.array, None, x0, self.x1, self.saved[0], self.scratch)
-        a.sr_select_indices(cm, K, a.SR_SEL_RANDOM, self.seed, step, None, None, self.idx)
+        if self.select == "attn":
+            a.sr_attention_colsums(ce, self.w.L, self.saved[0], self.split[0] - 1, self.colsum)
+            a.sr_select_topk_scores(cm, K, self.colsum, self.w.H, self.idx)
+        else:
+            a.sr_select_indices(cm, K, a.SR_SEL_RANDOM, self.seed, step, None, None, self.idx)
         a.sr_gather(cm, K, self.x1, self.idx, self.h0)
         a.sr_sparse_blocks_fwd(cm, K, pm.array, None, self.h0, self.h, self.saved[1], self.scratch)
         a.sr_scatter_delta(cm, K, self.x1, self.h, self.h0, self.idx)
