@@ -46,10 +46,10 @@ def log(*a):
 class Step:
     """Device buffers and the launch sequence of one routed (or dense) step."""
 
-    def __init__(self, w, dense: bool, seed: int = 42):
+    def __init__(self, w, dense: bool, seed: int = 42, fused: bool = True):
         import torch
         from paper_2607_02829_amd import abi, device, inputs
-        self.abi, self.w, self.dense = abi, w, dense
+        self.abi, self.w, self.dense, self.fused = abi, w, dense, fused
         self.cfg = device.config_for(w)
         self.K = w.L if dense else w.K
         self.S = self.K
@@ -88,6 +88,10 @@ class Step:
             return
         x_t = self.x if self.sel == a.SR_SEL_TOPK_DIFFNORM else None
         a.sr_select_indices(c, K, self.sel, self.seed, step, x_t, self.x_prev, self.idx, self.sel_scratch)
+        if self.fused:   # gather and scatter fused into the stack's first and last steps
+            a.sr_routed_blocks_fwd(c, K, self.idx, p, self.cond, self.x, self.saved)
+            a.sr_routed_blocks_bwd(c, K, self.idx, p, self.cond, self.saved, self.g, g, self.dcond, self.scratch)
+            return
         a.sr_gather(c, K, self.x, self.idx, self.h0)
         a.sr_sparse_blocks_fwd(c, S, p, self.cond, self.h0, self.h, self.saved, self.scratch)
         a.sr_scatter_delta(c, K, self.x, self.h, self.h0, self.idx)
@@ -363,6 +367,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routing-sweep", action="store_true", help="skip the gather/scatter bandwidth sweep")
     ap.add_argument("--breakdown", action="store_true", help="print the per-kernel breakdown to stderr")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time the routed step as separate gather / blocks / scatter calls (default: the fused "
+                         "sr_routed_blocks_fwd/bwd)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run one device-to-device copy of known size first (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("GROUP", "FETCH_CSV", "WRITE_CSV", "OUT_MD"),
@@ -401,7 +408,7 @@ def main():
     # ---------------------------------------------------------------- routed (sparse) mode
     torch.cuda.reset_peak_memory_stats()
     base_mem = torch.cuda.memory_allocated()
-    sp = Step(w, dense=False)
+    sp = Step(w, dense=False, fused=not args.unfused)
     sp.run(0)
     torch.cuda.synchronize()
     sparse_peak = torch.cuda.max_memory_allocated() - base_mem
@@ -507,6 +514,7 @@ def main():
                                f"D={w.D}, H={w.H}, F={w.F}, {w.n_blocks} {w.kind} blocks, {w.select} selection",
                    "B": w.B, "L": w.L, "K": w.K, "D": w.D, "H": w.H, "F": w.F, "n_blocks": w.n_blocks,
                    "parallelism": "none (1 GPU)"},
+        "routed_step_calls": "separate gather / blocks / scatter" if args.unfused else "fused (sr_routed_blocks_fwd/bwd)",
         "gpu_ms_per_step_events": round(ms_gpu, 4),
         "full_grid_tokens_per_s": round(w.B * w.L / (ms_step * 1e-3), 1),
         "stack_mfma_frac": round(blk_flops / (ms_step * 1e-3) / PEAK_BF16_FLOPS, 4),

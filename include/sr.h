@@ -190,6 +190,30 @@ SR_API sr_status sr_dense_blocks_bwd(const sr_config* cfg, const sr_block_params
                               const void* dx_out, void* dx_in, const sr_block_grads* grads,
                               float* dcond, void* scratch, size_t scratch_bytes, void* stream);
 
+/* The routed step's forward in one call (Alg. 1 stage 2): gather, the n_blocks blocks on
+ * the K routed tokens, residual-delta scatter, with the gather fused into the stack's input
+ * step and the scatter into the last block's output epilogue.  In place on x:
+ *   x[b,i,:] <- rnd( f32(x0[b,i,:]) + (f32(h[b,k,:]) - f32(x0[b,i,:])) ),  i = idx[b,k],
+ * h = the stack's output on h0 = x0[idx] rounded to the storage type; bit for bit the
+ * result of sr_gather + sr_sparse_blocks_fwd + sr_scatter_delta.  Rows not in idx keep x0.
+ *   idx: [B,K] (or [1,K] with idx_shared), duplicate-free rows inside [0,L).
+ *   saved: sr_workspace_bytes(cfg, K) bytes; it holds what sr_routed_blocks_bwd (or
+ *          sr_sparse_blocks_bwd with S = K) needs.  No scratch. */
+SR_API sr_status sr_routed_blocks_fwd(const sr_config* cfg, int32_t K, const int32_t* idx,
+                               const sr_block_params* params, const void* cond, void* x,
+                               void* saved, size_t saved_bytes, void* stream);
+
+/* Its backward in one call, in place on g (in: gradient of x', out: gradient of x0):
+ *   g <- g + Scatter(J^T g[I] - g[I], I)  (the gradient delta rounded once, as in
+ * sr_scatter_delta(g, dh_in, NULL, idx)); bit for bit the result of sr_gather(g) +
+ * sr_sparse_blocks_bwd + sr_scatter_delta.  grads, dcond, scratch as for
+ * sr_sparse_blocks_bwd with S = K. */
+SR_API sr_status sr_routed_blocks_bwd(const sr_config* cfg, int32_t K, const int32_t* idx,
+                               const sr_block_params* params, const void* cond,
+                               const void* saved, size_t saved_bytes, void* g,
+                               const sr_block_grads* grads, float* dcond, void* scratch,
+                               size_t scratch_bytes, void* stream);
+
 /* Debug check of an index set: *ok_dev (device int32) is set to 1 if every row of
  * idx is strictly increasing and inside [0,L), else 0. */
 SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx,
@@ -229,7 +253,7 @@ SR_API sr_status sr_select_topk_scores(const sr_config* cfg, int32_t K, const fl
  * name: "<name> <launches> <total_ms> <algorithmic_flops> <algorithmic_bytes>\n"
  * into `out` (NUL-terminated, truncated to out_bytes); *needed receives the full
  * size.  Names: select_random, select_topk, select_topk_scores, attn_colsum, gather,
- * scatter_delta, ln_fwd, ln_bwd,
+ * scatter_delta, gather_f32, scatter_f32, ln_fwd, ln_bwd,
  * gemm_<op> (qkv, o, fc1, fc2, dx_fc2, dx_fc1, dx_o, dx_qkv, dw_<op>), attn_fwd,
  * attn_bwd_dkv, attn_bwd_dq, attn_bwd_delta, reduce, colsum, convert, mod. */
 SR_API sr_status sr_profile_start(const char* name_filter);

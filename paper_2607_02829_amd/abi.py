@@ -24,7 +24,8 @@ PARAM_FIELDS = ("ln1_w", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o", "ln2_w", "ln2_
 EXPORTS = ("sr_last_error", "sr_version", "sr_workspace_bytes", "sr_select_scratch_bytes",
            "sr_select_indices", "sr_gather", "sr_scatter_delta", "sr_sparse_blocks_fwd",
            "sr_sparse_blocks_bwd", "sr_dense_blocks_fwd", "sr_dense_blocks_bwd", "sr_validate_indices",
-           "sr_attention_colsums", "sr_select_topk_scores", "sr_profile_start", "sr_profile_stop")
+           "sr_attention_colsums", "sr_select_topk_scores", "sr_routed_blocks_fwd", "sr_routed_blocks_bwd",
+           "sr_profile_start", "sr_profile_stop")
 
 
 class SrLibraryMissing(RuntimeError):
@@ -79,6 +80,8 @@ def lib(path: str = LIB_PATH):
         "sr_dense_blocks_bwd": ([CP, P, P, P, SZ, P, P, P, P, P, SZ, P], I32),
         "sr_validate_indices": ([CP, I32, P, P, P], I32),
         "sr_attention_colsums": ([CP, I32, P, SZ, I32, P, P], I32),
+        "sr_routed_blocks_fwd": ([CP, I32, P, P, P, P, P, SZ, P], I32),
+        "sr_routed_blocks_bwd": ([CP, I32, P, P, P, P, SZ, P, P, P, P, SZ, P], I32),
         "sr_select_topk_scores": ([CP, I32, P, I32, P, P], I32),
         "sr_profile_start": ([ctypes.c_char_p], I32),
         "sr_profile_stop": ([ctypes.c_char_p, SZ, ctypes.POINTER(SZ)], I32),
@@ -181,6 +184,16 @@ def sr_dense_blocks_bwd(cfg, params, cond, saved, dx_out, dx_in, grads, dcond, s
 
 def sr_validate_indices(cfg, K, idx, ok_dev, stream=None):
     _check(lib().sr_validate_indices(ctypes.byref(cfg), K, _p(idx), _p(ok_dev), _stream(stream)))
+
+
+def sr_routed_blocks_fwd(cfg, K, idx, params, cond, x, saved, stream=None):
+    _check(lib().sr_routed_blocks_fwd(ctypes.byref(cfg), K, _p(idx), params, _p(cond), _p(x), _p(saved),
+                                      _nbytes(saved), _stream(stream)))
+
+
+def sr_routed_blocks_bwd(cfg, K, idx, params, cond, saved, g, grads, dcond, scratch, stream=None):
+    _check(lib().sr_routed_blocks_bwd(ctypes.byref(cfg), K, _p(idx), params, _p(cond), _p(saved), _nbytes(saved),
+                                      _p(g), grads, _p(dcond), _p(scratch), _nbytes(scratch), _stream(stream)))
 
 
 def sr_attention_colsums(cfg, S, saved, block, colsum, stream=None):

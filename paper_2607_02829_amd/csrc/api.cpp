@@ -234,6 +234,46 @@ sr_status sr_sparse_blocks_bwd(const sr_config* cfg, int32_t S, const sr_block_p
                     "blocks_bwd");
 }
 
+sr_status sr_routed_blocks_fwd(const sr_config* cfg, int32_t K, const int32_t* idx, const sr_block_params* params,
+                               const void* cond, void* x, void* saved, size_t saved_bytes, void* stream) {
+  sr_status s = check_cfg(cfg);
+  if (s != SR_OK) return s;
+  SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
+  SR_CHECK(cfg->n_blocks >= 1, SR_EINVAL, "n_blocks must be >= 1");
+  if ((s = check_params(cfg, params, cond)) != SR_OK) return s;
+  SR_PTR(idx, "idx");
+  SR_PTR(x, "x");
+  if ((s = check_ws(cfg, K, saved, saved_bytes, nullptr, 0, false)) != SR_OK) return s;
+  sr::Dims d = dims_of(cfg, K);
+  sr::Route rt;
+  rt.idx = idx; rt.x = x; rt.shared = cfg->idx_shared;
+  return hip_status(sr::stack_fwd(d, params, cond, nullptr, nullptr, (char*)saved, (hipStream_t)stream, &rt),
+                    "routed_blocks_fwd");
+}
+
+sr_status sr_routed_blocks_bwd(const sr_config* cfg, int32_t K, const int32_t* idx, const sr_block_params* params,
+                               const void* cond, const void* saved, size_t saved_bytes, void* g,
+                               const sr_block_grads* grads, float* dcond, void* scratch, size_t scratch_bytes,
+                               void* stream) {
+  sr_status s = check_cfg(cfg);
+  if (s != SR_OK) return s;
+  SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
+  SR_CHECK(cfg->n_blocks >= 1, SR_EINVAL, "n_blocks must be >= 1");
+  if ((s = check_params(cfg, params, cond)) != SR_OK) return s;
+  SR_PTR(idx, "idx");
+  SR_PTR(g, "g");
+  SR_CHECK(grads != nullptr, SR_EINVAL, "grads is NULL");
+  if (dcond) SR_CHECK(aligned16(dcond), SR_EALIGN, "dcond is not 16-byte aligned");
+  if ((s = check_ws(cfg, K, saved, saved_bytes, scratch, scratch_bytes, true)) != SR_OK) return s;
+  sr::Dims d = dims_of(cfg, K);
+  sr::Route rt;
+  rt.idx = idx; rt.x = g; rt.shared = cfg->idx_shared;
+  return hip_status(sr::stack_bwd(d, params, cond, (const char*)saved, nullptr, nullptr, grads,
+                                  cfg->kind == SR_BLOCK_ADALN ? dcond : nullptr, (char*)scratch, (hipStream_t)stream,
+                                  &rt),
+                    "routed_blocks_bwd");
+}
+
 sr_status sr_dense_blocks_fwd(const sr_config* cfg, const sr_block_params* params, const void* cond,
                               const void* x_in, void* x_out, void* saved, size_t saved_bytes, void* scratch,
                               size_t scratch_bytes, void* stream) {

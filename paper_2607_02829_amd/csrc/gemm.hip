@@ -85,6 +85,13 @@ SR_DEV void epilogue(const EpiArgs& e, int m, int n, float v) {
     const float r = e.resid[o] + t;
     if (e.out_f32) e.out_f32[o] = r;
     if (e.out_st) ((T*)e.out_st)[o] = from_f32<T>(r);
+    if (e.sc_x) {
+      const int b = m / e.S, s = m - b * e.S;
+      const int i = e.sc_idx[(e.sc_shared ? 0 : b) * e.S + s];
+      T* xp = (T*)e.sc_x + ((size_t)b * e.sc_L + i) * e.ldo + n;
+      const float x0 = to_f32<T>(*xp);
+      *xp = from_f32<T>(__fadd_rn(x0, __fsub_rn(to_f32<T>(from_f32<T>(r)), x0)));
+    }
   } else if constexpr (EPI == EPI_GELU) {
     const float z = v + to_f32<T>(((const T*)e.bias)[n]);
     ((Ta*)e.out_act)[o] = from_f32<Ta>(z);
@@ -125,6 +132,14 @@ SR_DEV i32x2 pack4(f32x4 v) {
   w[1] = (int)f2bf2(v[2], v[3]);
   return w;
 }
+SR_DEV f32x4 unpack4(i32x2 w) {
+  f32x4 v;
+  v[0] = __uint_as_float((uint32_t)w[0] << 16);
+  v[1] = __uint_as_float((uint32_t)w[0] & 0xFFFF0000u);
+  v[2] = __uint_as_float((uint32_t)w[1] << 16);
+  v[3] = __uint_as_float((uint32_t)w[1] & 0xFFFF0000u);
+  return v;
+}
 
 constexpr bool epi_has_bias(int epi) {
   return epi == EPI_BIAS_ACT || epi == EPI_RESID || epi == EPI_GELU || epi == EPI_BIAS_F32;
@@ -160,6 +175,17 @@ SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in,
     const f32x4 r = in.resid + t;
     if (e.out_f32) *reinterpret_cast<f32x4*>(e.out_f32 + o) = r;
     if (e.out_st) *reinterpret_cast<i32x2*>((bf16_t*)e.out_st + o) = pack4(r);
+    if (e.sc_x) {
+      const int b = m / e.S, s = m - b * e.S;
+      const int i = e.sc_idx[(e.sc_shared ? 0 : b) * e.S + s];
+      bf16_t* xp = (bf16_t*)e.sc_x + ((size_t)b * e.sc_L + i) * e.ldo + n;
+      const f32x4 x0 = unpack4(*reinterpret_cast<const i32x2*>(xp));
+      const f32x4 h = unpack4(pack4(r));
+      f32x4 xn;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) xn[q] = __fadd_rn(x0[q], __fsub_rn(h[q], x0[q]));
+      *reinterpret_cast<i32x2*>(xp) = pack4(xn);
+    }
   } else if constexpr (EPI == EPI_GELU) {
     const f32x4 z = v + b;
     f32x4 gz;

@@ -58,6 +58,102 @@ __global__ __launch_bounds__(256) void scatter_delta_kernel(i32x4* __restrict__ 
   }
 }
 
+// Fused forms for the stack's boundaries (one wave per routed row, 16-byte chunks of x):
+// y32[b,k,:] = f32(x[b, idx[b,k], :]) (and ycopy[b,k,:] = x[b, idx[b,k], :] if given) -- the
+// gather fused with the conversion of the stack's input to its fp32 residual stream;
+template <typename T>
+__global__ __launch_bounds__(256) void gather_rows_f32_kernel(const i32x4* __restrict__ x,
+                                                              const int32_t* __restrict__ idx,
+                                                              float* __restrict__ y32, i32x4* __restrict__ ycopy,
+                                                              int B, int L, int K, int chunks, int shared) {
+  constexpr int V = 16 / sizeof(T);
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= B * K) return;
+  const int b = r / K, k = r - b * K;
+  const int i = idx[(shared ? 0 : b) * K + k];
+  const i32x4* xr = x + ((size_t)b * L + i) * chunks;
+  float* yr = y32 + (size_t)r * chunks * V;
+  for (int c = lane; c < chunks; c += 64) {
+    const i32x4 v = xr[c];
+    if (ycopy) ycopy[(size_t)r * chunks + c] = v;
+    const T* ev = reinterpret_cast<const T*>(&v);
+#pragma unroll
+    for (int q = 0; q < V; q += 4) {
+      f32x4 f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) f[e] = to_f32<T>(ev[q + e]);
+      *reinterpret_cast<f32x4*>(yr + (size_t)c * V + q) = f;
+    }
+  }
+}
+
+// x[b,i,:] = rnd(f32(x[b,i,:]) + (f32(rnd(h32[b,k,:])) - f32(x[b,i,:]))), i = idx[b,k]: the
+// residual-delta scatter with h0 re-read from x, fused with the rounding of the stack's fp32
+// output to the storage type (the same values as converting h32 and then scattering).
+template <typename T>
+__global__ __launch_bounds__(256) void scatter_f32_delta_kernel(i32x4* __restrict__ x, const float* __restrict__ h32,
+                                                                const int32_t* __restrict__ idx, int B, int L, int K,
+                                                                int chunks, int shared) {
+#pragma clang fp contract(off)
+  constexpr int V = 16 / sizeof(T);
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= B * K) return;
+  const int b = r / K, k = r - b * K;
+  const int i = idx[(shared ? 0 : b) * K + k];
+  i32x4* xr = x + ((size_t)b * L + i) * chunks;
+  const float* hr = h32 + (size_t)r * chunks * V;
+  for (int c = lane; c < chunks; c += 64) {
+    const i32x4 vx = xr[c];
+    float hv[V];
+#pragma unroll
+    for (int q = 0; q < V; q += 4) {
+      const f32x4 f = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(hr + (size_t)c * V + q));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) hv[q + e] = f[e];
+    }
+    const T* ex = reinterpret_cast<const T*>(&vx);
+    i32x4 out;
+    T* eo = reinterpret_cast<T*>(&out);
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      const float x0 = to_f32<T>(ex[e]);
+      const float d = __fsub_rn(to_f32<T>(from_f32<T>(hv[e])), x0);
+      eo[e] = from_f32<T>(__fadd_rn(x0, d));
+    }
+    xr[c] = out;
+  }
+}
+
+hipError_t launch_gather_rows_f32(int dtype, int B, int L, int K, int D, const void* x, const int32_t* idx,
+                                  float* y32, void* ycopy, int shared, hipStream_t st) {
+  const int elt = dtype == kBF16 ? 2 : 4;
+  const int chunks = D * elt / 16;
+  dim3 g((B * K + kRowsPerBlock - 1) / kRowsPerBlock);
+  if (dtype == kBF16)
+    hipLaunchKernelGGL(gather_rows_f32_kernel<bf16_t>, g, dim3(256), 0, st, (const i32x4*)x, idx, y32, (i32x4*)ycopy,
+                       B, L, K, chunks, shared);
+  else
+    hipLaunchKernelGGL(gather_rows_f32_kernel<float>, g, dim3(256), 0, st, (const i32x4*)x, idx, y32, (i32x4*)ycopy,
+                       B, L, K, chunks, shared);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_f32_delta(int dtype, int B, int L, int K, int D, void* x, const float* h32,
+                                    const int32_t* idx, int shared, hipStream_t st) {
+  const int elt = dtype == kBF16 ? 2 : 4;
+  const int chunks = D * elt / 16;
+  dim3 g((B * K + kRowsPerBlock - 1) / kRowsPerBlock);
+  if (dtype == kBF16)
+    hipLaunchKernelGGL(scatter_f32_delta_kernel<bf16_t>, g, dim3(256), 0, st, (i32x4*)x, h32, idx, B, L, K, chunks,
+                       shared);
+  else
+    hipLaunchKernelGGL(scatter_f32_delta_kernel<float>, g, dim3(256), 0, st, (i32x4*)x, h32, idx, B, L, K, chunks,
+                       shared);
+  return hipGetLastError();
+}
+
 hipError_t launch_gather(int elt, int B, int L, int K, int D, const void* x, const int32_t* idx, void* h0,
                          int shared, hipStream_t st) {
   const int chunks = D * elt / 16;

@@ -36,6 +36,12 @@ struct EpiArgs {
   const void* z_in = nullptr;   // pre-activation for GELU'
   long long ldo = 0;            // row stride of the outputs
   int S = 1;                    // rows per sample (gate indexing)
+  // EPI_RESID with sc_x: instead of out_st, the residual-delta scatter of the storage-rounded
+  // result into the full sequence, x[b, i, n] = rnd(x0 + (rnd(r) - x0)), x0 = x[b, i, n],
+  // i = sc_idx[(sc_shared ? 0 : b) * S + s] for row m = b * S + s (rows of x have ldo elements)
+  void* sc_x = nullptr;
+  const int32_t* sc_idx = nullptr;
+  int sc_L = 0, sc_shared = 0;
   long long split_stride = 0;   // element stride between split-K partial outputs
   // EPI_DW (weight gradient, reduction over tokens): out_f32 receives dW and db_out (optional)
   // the row sums of A (the bias gradient); with split-K each split writes its plane of part,
@@ -73,6 +79,10 @@ hipError_t launch_validate(const int32_t* idx, int rows, int K, int L, int32_t* 
 
 hipError_t launch_gather(int elt, int B, int L, int K, int D, const void* x, const int32_t* idx, void* h0, int shared,
                          hipStream_t st);
+hipError_t launch_gather_rows_f32(int dtype, int B, int L, int K, int D, const void* x, const int32_t* idx,
+                                  float* y32, void* ycopy, int shared, hipStream_t st);
+hipError_t launch_scatter_f32_delta(int dtype, int B, int L, int K, int D, void* x, const float* h32,
+                                    const int32_t* idx, int shared, hipStream_t st);
 hipError_t launch_scatter_delta(int dtype, int B, int L, int K, int D, void* x, const void* h, const void* h0,
                                 const int32_t* idx, int shared, hipStream_t st);
 

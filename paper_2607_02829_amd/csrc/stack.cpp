@@ -135,7 +135,7 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
 // ============================================================================ forward
 
 hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, const void* h_in, void* h_out,
-                     char* saved, hipStream_t st) {
+                     char* saved, hipStream_t st, const Route* rt) {
   BlockSaved* sv = new BlockSaved[d.nb];
   layout_saved(d, saved, sv);
   const int M = d.M, D = d.D, F = d.F, S = d.S;
@@ -143,7 +143,10 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
   const bool ada = d.kind == SR_BLOCK_ADALN;
   hipError_t err = hipSuccess;
   auto run = [&]() -> hipError_t {
-    {
+    if (rt) {
+      ProfScope ps("gather_f32", 0, (double)M * D * (e + 4) + 4.0 * M, st);
+      SR_TRY(launch_gather_rows_f32(d.dtype, d.B, d.L, S, D, rt->x, rt->idx, sv[0].hin, nullptr, rt->shared, st));
+    } else {
       ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
       SR_TRY(launch_convert(d.dtype, h_in, kF32, sv[0].hin, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
     }
@@ -190,7 +193,13 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
       {
         GemmDesc g = desc(d, s.gz, true, F, (size_t)M * F * e, w.w_fc2, true, F, (size_t)D * F * e, M, D, F);
         EpiArgs ep; ep.bias = w.b_fc2; ep.resid = s.h1; ep.ldo = D; ep.S = S;
-        if (i + 1 < d.nb) ep.out_f32 = sv[i + 1].hin; else ep.out_st = h_out;
+        if (i + 1 < d.nb) {
+          ep.out_f32 = sv[i + 1].hin;
+        } else if (rt) {   // x[I] = rnd(x0 + (rnd(h) - x0)) in the epilogue
+          ep.sc_x = rt->x; ep.sc_idx = rt->idx; ep.sc_L = d.L; ep.sc_shared = rt->shared;
+        } else {
+          ep.out_st = h_out;
+        }
         if (ada) { ep.gate = s.mod + 5 * D; ep.gate_stride = 6 * D; ep.a_save = s.m_out; }
         ProfScope ps("gemm_fc2", gemm_flops(M, D, F), gemm_bytes(d, M, D, F, 8), st);
         SR_TRY(launch_gemm(g, EPI_RESID, ep, st));
@@ -298,7 +307,7 @@ void give_events(BwdEvents* e) {
 
 hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, const char* saved,
                      const void* dh_out, void* dh_in, const sr_block_grads* gr, float* dcond, char* scratch,
-                     hipStream_t st) {
+                     hipStream_t st, const Route* rt) {
   BlockSaved* sv = new BlockSaved[d.nb];
   layout_saved(d, const_cast<char*>(saved), sv);
   Scratch sc;
@@ -348,7 +357,10 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
     SR_TRY(side_stream(&side));
     SR_TRY(take_events(&ev));
     // g_res = fp32(dh_out) and, for pre-LN, its activation copy
-    {
+    if (rt) {   // gather of the gradient fused with its conversion
+      ProfScope ps("gather_f32", 0, (double)M * D * (2 * e + 4) + 4.0 * M, st);
+      SR_TRY(launch_gather_rows_f32(d.dtype, d.B, d.L, S, D, rt->x, rt->idx, sc.g_res, sc.g_act[0], rt->shared, st));
+    } else {
       ProfScope ps("convert", 0, (double)M * D * (2 * e + 4), st);
       SR_TRY(launch_convert(d.dtype, dh_out, d.dtype, sc.g_act[0], (size_t)M * D, nullptr, 0, S, D, sc.g_res, st));
     }
@@ -476,7 +488,10 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(zero_f32(g.b_ada, (size_t)6 * D, st));
       }
     }
-    {
+    if (rt) {   // residual-delta scatter of the gradient fused with its rounding
+      ProfScope ps("scatter_f32", 0, (double)M * D * (2 * e + 4) + 4.0 * M, st);
+      SR_TRY(launch_scatter_f32_delta(d.dtype, d.B, d.L, S, D, rt->x, sc.g_res, rt->idx, rt->shared, st));
+    } else {
       ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
       SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
     }

@@ -1,0 +1,91 @@
+"""GPU tests of the fused routed step (Alg. 1 stage 2 in one call per direction):
+sr_routed_blocks_fwd / sr_routed_blocks_bwd against sr_gather + sr_sparse_blocks_fwd/bwd +
+sr_scatter_delta on the same inputs, bit for bit (x', the input gradient, every weight
+gradient, dcond), and the fused forward against the oracle's routed step."""
+import numpy as np
+import pytest
+
+from gpu_helpers import rel_err, tol_for
+from oracle import select as osel
+from oracle import stack as ostack
+from oracle.numerics import storage_to_f64
+from paper_2607_02829_amd import abi, device, inputs
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    "bf16": (inputs.small("rf_a", Hg=10, Wg=21), 2, 52, 0),
+    "bf16_shared_idx": (inputs.small("rf_b", Hg=10, Wg=21), 2, 61, 1),
+    "f32": (inputs.small("rf_c", Hg=9, Wg=11, D=128, H=2, F=512, dtype="f32"), 2, 25, 0),
+    "adaln_bf16": (inputs.small("rf_d", Hg=10, Wg=21, kind="adaln"), 2, 50, 0),
+    "d025_full": (inputs.WORKLOADS["d025"], 12, 4050, 0),
+}
+
+
+def _run(w, nb, K, shared, fused):
+    import torch
+    params = inputs.params_to_storage(inputs.block_params(w, nb, randomise_affine=True), w.dtype)
+    cond = inputs.to_storage(inputs.cond_vector(w), w.dtype) if w.kind == "adaln" else None
+    x = inputs.to_storage(inputs.token_field(w), w.dtype)
+    g = inputs.to_storage(inputs.upstream_grad(w), w.dtype)
+    cfg = device.config_for(w, n_blocks=nb, idx_shared=shared)
+    dp = device.DeviceParams(params, w.kind)
+    gr = device.DeviceGrads(w, nb)
+    c = device.to_device(cond) if cond is not None else None
+    dcond = torch.empty((w.B, w.D), dtype=torch.float32, device="cuda") if cond is not None else None
+    xd, gd = device.to_device(x), device.to_device(g)
+    rows = 1 if shared else w.B
+    idx = torch.empty((rows, K), dtype=torch.int32, device="cuda")
+    abi.sr_select_indices(cfg, K, abi.SR_SEL_RANDOM, 5, 3, None, None, idx)
+    saved, scratch = device.workspace(cfg, K)
+    if fused:
+        abi.sr_routed_blocks_fwd(cfg, K, idx, dp.array, c, xd, saved)
+        abi.sr_routed_blocks_bwd(cfg, K, idx, dp.array, c, saved, gd, gr.array, dcond, scratch)
+    else:
+        h0 = torch.empty((w.B, K, w.D), dtype=xd.dtype, device="cuda")
+        h, gh, dh = torch.empty_like(h0), torch.empty_like(h0), torch.empty_like(h0)
+        abi.sr_gather(cfg, K, xd, idx, h0)
+        abi.sr_sparse_blocks_fwd(cfg, K, dp.array, c, h0, h, saved, scratch)
+        abi.sr_scatter_delta(cfg, K, xd, h, h0, idx)
+        abi.sr_gather(cfg, K, gd, idx, gh)
+        abi.sr_sparse_blocks_bwd(cfg, K, dp.array, c, saved, gh, dh, gr.array, dcond, scratch)
+        abi.sr_scatter_delta(cfg, K, gd, dh, None, idx)
+    torch.cuda.synchronize()
+    out = {"x": device.to_host(xd), "g": device.to_host(gd), "idx": idx.cpu().numpy(),
+           "grads": [{k: v.cpu().numpy() for k, v in t.items()} for t in gr.tensors]}
+    if dcond is not None:
+        out["dcond"] = dcond.cpu().numpy()
+    return out, (x, params, cond)
+
+
+def _bits(a):
+    a = np.ascontiguousarray(a)
+    return a.view(np.uint8)
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_fused_equals_unfused_bitwise(case):
+    w, nb, K, shared = CASES[case]
+    print(f"[routed fused {case}] B={w.B} L={w.L} K={K} blocks={nb} {w.dtype} {w.kind} shared={shared}", flush=True)
+    f, _ = _run(w, nb, K, shared, fused=True)
+    u, _ = _run(w, nb, K, shared, fused=False)
+    assert np.array_equal(f["idx"], u["idx"])
+    assert np.array_equal(_bits(f["x"]), _bits(u["x"])), "x'"
+    assert np.array_equal(_bits(f["g"]), _bits(u["g"])), "dx0"
+    for i, (a, b) in enumerate(zip(f["grads"], u["grads"])):
+        for k in a:
+            assert np.array_equal(_bits(a[k]), _bits(b[k])), f"block {i} {k}"
+    if "dcond" in f:
+        assert np.array_equal(_bits(f["dcond"]), _bits(u["dcond"]))
+
+
+def test_fused_forward_against_oracle():
+    w, nb, K, shared = CASES["bf16"]
+    f, (x, params, _) = _run(w, nb, K, shared, fused=True)
+    idx = osel.select_random(w.B, w.L, K, 5, 3)
+    assert np.array_equal(f["idx"], idx)
+    want, *_ = ostack.routed_forward(x, idx, params, w.H, 1e-6)
+    for b in range(w.B):
+        mask = np.ones(w.L, bool); mask[idx[b]] = False
+        assert np.array_equal(f["x"][b, mask], x[b, mask])     # unselected rows untouched
+    assert rel_err(storage_to_f64(f["x"]), storage_to_f64(want)) <= tol_for(w.dtype)
