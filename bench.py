@@ -4,7 +4,9 @@
 One step is one pass of the whole hot path over one batch:
     select -> gather -> blocks fwd -> residual-delta scatter
            -> gather(g) -> blocks bwd -> scatter(g)
-(Alg. 1 stage 2 and its backward), on the 0.25 deg workload by default:
+(Alg. 1 stage 2 and its backward; by default through the fused calls, which gather into
+the stack's first step and scatter from its last; --unfused times the separate calls),
+on the 0.25 deg workload by default:
 B=1, 90 x 180 token grid (L=16200), keep 25% (K=4050), D=1024, 16 heads, MLP 4096,
 12 middle blocks, bf16 storage with fp32 accumulation, synthetic smooth token
 fields and N(0, 0.02) weights, all resident in HBM before timing starts.
@@ -484,7 +486,7 @@ def main():
 
     # routing kernels: in-step launch times (per-kernel breakdown) and a cache-evicting size sweep
     routing = {"in_step": {}, "sweep": []}
-    for name in ("gather", "scatter_delta"):
+    for name in ("gather", "scatter_delta", "gather_f32", "scatter_f32"):
         if name in breakdown and breakdown[name]["launches"] > 0:
             b = breakdown[name]
             us = b["ms"] / b["launches"] * 1e3
