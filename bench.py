@@ -170,6 +170,36 @@ def trunk_sweep(w, dense_ms: float | None, steps: int = 3) -> dict:
     return out
 
 
+def graph_timing(st: Step, steps: int, warmup: int) -> dict:
+    """Capture one routed step (selection + the fused forward and backward, whose second-stream
+    weight gradients are forked and joined inside the capture) in a HIP graph and time its
+    replays: the launch cost of ~40 kernels per block leaves the step.  Every replay redoes the
+    whole step on the current state, with the draw fixed at capture (a graph replays its launch
+    arguments)."""
+    import torch
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        st.run(10_000)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        st.run(10_001)
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.replay()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    finite = bool(torch.isfinite(st.x.float()).all().item() and torch.isfinite(st.g.float()).all().item())
+    del g
+    return {"ms_per_step": round(ms, 4), "routed_tokens_per_s": round(st.w.B * st.K / (ms * 1e-3), 1),
+            "outputs_finite": finite}
+
+
 def kernel_breakdown(st: Step, step_index: int):
     """One profiled step with every launch group bracketed by events."""
     import torch
@@ -369,6 +399,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routing-sweep", action="store_true", help="skip the gather/scatter bandwidth sweep")
     ap.add_argument("--breakdown", action="store_true", help="print the per-kernel breakdown to stderr")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the fused routed step captured once in a HIP graph and replayed (the draw is "
+                         "the one fixed at capture)")
     ap.add_argument("--unfused", action="store_true",
                     help="time the routed step as separate gather / blocks / scatter calls (default: the fused "
                          "sr_routed_blocks_fwd/bwd)")
@@ -424,6 +457,9 @@ def main():
     # timed region: K steps; HIP events bracket only the dominant kernel's launches
     ms_step, ms_gpu, prof = time_steps(sp, args.steps, args.warmup, start=2, profile_filter=dom)
     finite = bool(torch.isfinite(sp.x.float()).all().item() and torch.isfinite(sp.g.float()).all().item())
+    graph = None
+    if args.graph:
+        graph = graph_timing(sp, args.steps, args.warmup)
     del sp
     torch.cuda.empty_cache()
 
@@ -523,6 +559,7 @@ def main():
         "dense": dense,
         "speedup_vs_dense": round(dense["ms_per_step"] / ms_step, 3) if dense else None,
         "trunk": trunk,
+        "graph": graph,
         "peak_bytes": {"sparse": int(sparse_peak), "dense": dense["peak_bytes"] if dense else None,
                        "ratio": round(dense["peak_bytes"] / sparse_peak, 3) if dense else None},
         "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved_u, 2), "peak": peak_u, "unit": unit,

@@ -21,6 +21,10 @@
  *    stream per device (created on the first call, default priority, kept until the
  *    process ends) for its weight gradients, joined to `stream` through events: all of
  *    the call's work is complete when later work on `stream` starts.
+ *  - Calls can be captured into a HIP graph (after one eager call has created the second
+ *    stream and its events): they record no memset and no host synchronisation, and the
+ *    backward forks and joins its second stream through events on `stream`.  A replay
+ *    repeats the captured scalar arguments (seed, step, sizes).
  *  - Arguments are validated on the host before anything is enqueued; on error
  *    nothing is launched, a non-zero sr_status is returned and sr_last_error()
  *    (thread-local) describes it.  SR_EHIP reports a failed launch.
