@@ -5,8 +5,8 @@
 // 2D + h*hd); O and dO are [B*S, D]; dqkv mirrors qkv.  lse[b,h,s] is the base-2
 // log-sum-exp of the scaled scores, so P = exp2(s * log2(e)/sqrt(hd) - lse).
 //
-// MFMA kernels (hd = 64, bf16, v_mfma_f32_32x32x16_bf16).  A workgroup of four waves
-// owns 128 rows (32 per wave) of the resident dimension and streams the other one in
+// MFMA kernels (hd = 64, bf16, v_mfma_f32_32x32x16_bf16).  A workgroup of NW waves
+// owns 32 NW rows (32 per wave) of the resident dimension and streams the other one in
 // 64-row tiles of one head:
 //  * forward: a wave owns 32 queries and forms S^T = K Q^T per 32-key unit, so each
 //    lane holds one query's scores and the online-softmax state is per lane; the row
@@ -37,13 +37,16 @@ namespace sr {
 
 constexpr int HD = 64;
 constexpr int AP = HD + 8;   // padded row (bf16) of the output staging tile
-constexpr int QW = 128;      // rows (queries or keys) per workgroup, 32 per wave
+constexpr int QW = 128;      // keys per workgroup of the column-sum kernel (four waves, 32 each)
 constexpr int KT = 64;       // tile of the streamed dimension
 constexpr int TE = KT * HD;  // bf16 elements of one 64 x 64 tile (8 KB)
 constexpr int NSTG = 3;      // LDS stages
-// Waves per dK/dV workgroup: eight (256 keys) share each Q / dO tile, one workgroup per CU at
-// two waves per SIMD; measured 2-3 % faster than four at 4050 tokens.
+// Waves per workgroup of the MFMA kernels: eight (256 rows) share each streamed tile in LDS, at
+// one workgroup per CU and two waves per SIMD; against four, measured 2-4 % faster per kernel
+// at 4050 tokens (forward 94 -> 90, dK/dV 159 -> 155, dQ 112 -> 108 us).
 constexpr int kDkvWaves = 8;
+constexpr int kFwdWaves = 8;
+constexpr int kDqWaves = 8;
 
 
 SR_DEV bf16x8 zero8() {
@@ -199,14 +202,16 @@ SR_DEV void unstage(const bf16_t* stage, bf16_t* dst, size_t ld, int r0, int S) 
 
 // ------------------------------------------------------------------------------ forward
 
-__global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ O,
+// NW waves (32 queries each) per workgroup share the K / V tiles.
+template <int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ O,
                                                      float* __restrict__ lse, int S, int H, int D, float sl2) {
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
   const size_t ld = 3 * (size_t)D;
   const bf16_t* qp = qkv + (size_t)b * S * ld + hh * HD;
-  const int myq = blockIdx.x * QW + wid * 32 + l32;
+  const int myq = blockIdx.x * (32 * NW) + wid * 32 + l32;
   const int nt = (S + KT - 1) / KT;
   const bool ragged = S % KT != 0;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
@@ -221,10 +226,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) qf[ks] = myq < S ? ld8(qp + (size_t)myq * ld + ks * 16 + 8 * h32) : zero8();
 
-  constexpr int kLoads = 2 * kTileLoads;   // per thread per tile
+  constexpr int kLoads = 2 * (8 / NW);   // buffer loads per thread per tile (two tiles)
   auto load = [&](int t, int s) {
-    tile_load(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE, t < nt);
-    tile_load(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE, t < nt);
+    tile_load<NW>(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE, t < nt);
+    tile_load<NW>(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE, t < nt);
   };
   auto mask = [&](f32x16& sc, int k0) {   // keys past S do not exist
 #pragma unroll
@@ -352,7 +357,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_mfma(const bf16_t* __restrict
   if (h32 == 0 && myq < S) lse[((size_t)b * H + hh) * S + myq] = m_run * sl2 + log2f(l_tot);
   stage_t(smem, o, 1.0f / l_tot, wid, lane);
   __syncthreads();
-  unstage(smem, O + (size_t)b * S * D + hh * HD, D, blockIdx.x * QW, S);
+  unstage<NW>(smem, O + (size_t)b * S * D + hh * HD, D, blockIdx.x * (32 * NW), S);
 }
 
 // ------------------------------------------------------------------------------ backward dK, dV
@@ -484,7 +489,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
 
 // ------------------------------------------------------------------------------ backward dQ
 
-__global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ dO,
+// NW waves (32 queries each) per workgroup share the K / V tiles.
+template <int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ dO,
                                                         const float* __restrict__ lse, const float* __restrict__ delta,
                                                         bf16_t* __restrict__ dqkv, int S, int H, int D, float sl2,
                                                         float scale) {
@@ -494,7 +501,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
   const size_t ld = 3 * (size_t)D;
   const bf16_t* qp = qkv + (size_t)b * S * ld + hh * HD;
   const bf16_t* dop = dO + (size_t)b * S * D + hh * HD;
-  const int myq = blockIdx.x * QW + wid * 32 + l32;
+  const int myq = blockIdx.x * (32 * NW) + wid * 32 + l32;
   const int nt = (S + KT - 1) / KT;
   const bool ragged = S % KT != 0;
 
@@ -516,10 +523,10 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
   TrAddr ta;
   ra.init(lds_addr(smem), lane);
   ta.init(lds_addr(smem), lane);
-  constexpr int kLoads = 2 * kTileLoads;   // per thread per tile
+  constexpr int kLoads = 2 * (8 / NW);   // buffer loads per thread per tile (two tiles)
   auto load = [&](int t, int s) {
-    tile_load(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE, t < nt);
-    tile_load(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE, t < nt);
+    tile_load<NW>(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE, t < nt);
+    tile_load<NW>(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE, t < nt);
   };
   // K (tile 0) or V (tile 1) row fragments of key unit U of stage SG
   auto read_rows = [&](auto sg, auto uu, auto tl, RawFrag<true> (&fr)[4]) {
@@ -606,7 +613,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_mfma(const bf16_t* __restr
   __syncthreads();
   stage_t(smem, dq, scale, wid, lane);
   __syncthreads();
-  unstage(smem, dqkv + (size_t)b * S * ld + hh * HD, ld, blockIdx.x * QW, S);
+  unstage<NW>(smem, dqkv + (size_t)b * S * ld + hh * HD, ld, blockIdx.x * (32 * NW), S);
 }
 
 // ------------------------------------------------------------------------------ generic kernels
@@ -860,8 +867,9 @@ hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int 
                            hipStream_t st) {
   const int hd = D / H;
   if (attn_uses_mfma(dtype, hd)) {
-    dim3 g((S + QW - 1) / QW, H, B);
-    hipLaunchKernelGGL(attn_fwd_mfma, g, dim3(256), 0, st, (const bf16_t*)qkv, (bf16_t*)O, lse, S, H, D,
+    constexpr int kw = kFwdWaves;
+    dim3 g((S + 32 * kw - 1) / (32 * kw), H, B);
+    hipLaunchKernelGGL(attn_fwd_mfma<kw>, g, dim3(64 * kw), 0, st, (const bf16_t*)qkv, (bf16_t*)O, lse, S, H, D,
                        attn_sl2(hd));
     return hipGetLastError();
   }
@@ -873,7 +881,6 @@ hipError_t launch_attn_bwd(int dtype, const void* qkv, const void* dO, const flo
                            void* dqkv, int B, int S, int H, int D, hipStream_t st) {
   const int hd = D / H;
   if (attn_uses_mfma(dtype, hd)) {
-    dim3 g((S + QW - 1) / QW, H, B);
     const float sl2 = attn_sl2(hd), sc = 1.0f / sqrtf((float)hd);
     const double units = 2.0 * B * (double)S * S * D;   // one S x S x hd product over all heads
     {
@@ -886,8 +893,10 @@ hipError_t launch_attn_bwd(int dtype, const void* qkv, const void* dO, const flo
     }
     {
       ProfScope ps("attn_bwd_dq", units, (double)B * S * D * 2 * 5, st);
-      hipLaunchKernelGGL(attn_bwd_dq_mfma, g, dim3(256), 0, st, (const bf16_t*)qkv, (const bf16_t*)dO, lse, delta,
-                         (bf16_t*)dqkv, S, H, D, sl2, sc);
+      constexpr int kw = kDqWaves;
+      dim3 gq((S + 32 * kw - 1) / (32 * kw), H, B);
+      hipLaunchKernelGGL(attn_bwd_dq_mfma<kw>, gq, dim3(64 * kw), 0, st, (const bf16_t*)qkv, (const bf16_t*)dO, lse,
+                         delta, (bf16_t*)dqkv, S, H, D, sl2, sc);
     }
     return hipGetLastError();
   }
