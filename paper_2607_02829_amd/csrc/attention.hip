@@ -37,7 +37,6 @@ namespace sr {
 
 constexpr int HD = 64;
 constexpr int AP = HD + 8;   // padded row (bf16) of the output staging tile
-constexpr int QW = 128;      // keys per workgroup of the column-sum kernel (four waves, 32 each)
 constexpr int KT = 64;       // tile of the streamed dimension
 constexpr int TE = KT * HD;  // bf16 elements of one 64 x 64 tile (8 KB)
 constexpr int NSTG = 3;      // LDS stages
@@ -735,7 +734,8 @@ __global__ __launch_bounds__(64) void attn_bwd_dkv_simple(const Ta* __restrict__
 // half; a wave owns 32 keys (key per lane) and streams 64-query tiles; each lane sums its
 // 16 query rows per unit in tile, unit and row order, then the two half-waves (which hold
 // the other 16 rows of each unit) are added.  Deterministic.
-__global__ __launch_bounds__(256, 2) void attn_colsum_mfma(const bf16_t* __restrict__ qkv,
+template <int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_colsum_mfma(const bf16_t* __restrict__ qkv,
                                                            const float* __restrict__ lse,
                                                            float* __restrict__ colsum, int S, int H, int D,
                                                            float sl2) {
@@ -745,7 +745,7 @@ __global__ __launch_bounds__(256, 2) void attn_colsum_mfma(const bf16_t* __restr
   const int b = blockIdx.z, hh = blockIdx.y;
   const size_t ld = 3 * (size_t)D;
   const bf16_t* kp = qkv + (size_t)b * S * ld + D + hh * HD;
-  const int mykey = blockIdx.x * QW + wid * 32 + l32;
+  const int mykey = blockIdx.x * (32 * NW) + wid * 32 + l32;
   const int nt = (S + KT - 1) / KT;
   const bool ragged = S % KT != 0;
 
@@ -758,7 +758,7 @@ __global__ __launch_bounds__(256, 2) void attn_colsum_mfma(const bf16_t* __restr
   const uint32_t qbase = (uint32_t)(((size_t)b * S * ld + hh * HD) * 2);
   const uint32_t lbase = (uint32_t)(((size_t)b * H + hh) * S * 4);
   auto load = [&](int t, int s) {
-    tile_load(rq, qbase, (uint32_t)ld, t * KT, smem + s * TE);
+    tile_load<NW>(rq, qbase, (uint32_t)ld, t * KT, smem + s * TE);
     const uint32_t lo = lbase + (uint32_t)(t * KT + lane) * 4u;
     if (wid == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_ptr_t*)(fsm + s * KT), 4, lo, 0, 0, 0);
   };
@@ -921,8 +921,10 @@ hipError_t launch_attn_colsum(int dtype, const void* qkv, const float* lse, floa
                               hipStream_t st) {
   const int hd = D / H;
   if (attn_uses_mfma(dtype, hd)) {
-    dim3 g((S + QW - 1) / QW, H, B);
-    hipLaunchKernelGGL(attn_colsum_mfma, g, dim3(256), 0, st, (const bf16_t*)qkv, lse, colsum, S, H, D, attn_sl2(hd));
+    constexpr int kw = kDkvWaves;   // the dK/dV kernel's score half: the same shape
+    dim3 g((S + 32 * kw - 1) / (32 * kw), H, B);
+    hipLaunchKernelGGL(attn_colsum_mfma<kw>, g, dim3(64 * kw), 0, st, (const bf16_t*)qkv, lse, colsum, S, H, D,
+                       attn_sl2(hd));
     return hipGetLastError();
   }
   if (dtype == kBF16) return colsum_simple((const bf16_t*)qkv, lse, colsum, B, S, H, D, hd, st);
