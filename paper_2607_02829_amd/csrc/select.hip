@@ -185,7 +185,13 @@ __global__ __launch_bounds__(kSelThreads) void select_topk_kernel(const float* _
   // turns "largest" into "smallest".
   auto key_from = [&](int i) {
     float s = 0.0f;
-    for (int p = 0; p < parts; ++p) s = __fadd_rn(s, sc[(size_t)p * L + i]);
+    int p = 0;
+    for (; p + 4 <= parts; p += 4) {   // four planes' loads in flight, added in plane order
+      const float a0 = sc[(size_t)p * L + i], a1 = sc[(size_t)(p + 1) * L + i];
+      const float a2 = sc[(size_t)(p + 2) * L + i], a3 = sc[(size_t)(p + 3) * L + i];
+      s = __fadd_rn(__fadd_rn(__fadd_rn(__fadd_rn(s, a0), a1), a2), a3);
+    }
+    for (; p < parts; ++p) s = __fadd_rn(s, sc[(size_t)p * L + i]);
     return ~__float_as_uint(s);
   };
   const bool cached = L <= kTopkCache;
