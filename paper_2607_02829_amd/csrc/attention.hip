@@ -18,6 +18,8 @@
 //    dK^T += Q^T dS.
 //  * backward dQ: a wave owns 32 queries; per 32-key unit S^T, dP^T and dQ^T += K^T dS^T.
 // Two backward passes (instead of atomics) keep the result deterministic.
+//  * column sums of P (the attention each key receives, for the attention-score selector of
+//    Sec. 4.4): the dK/dV kernel's score half.
 //
 // Tiles go from global memory straight into LDS (buffer_load ... lds), three stages deep
 // (tile t+2 is in flight while tile t is consumed), row-major with an XOR swizzle of the
@@ -101,7 +103,6 @@ SR_DEV void tile_load(__amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t ld, int
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t*)(dst + blk * 512), 16, off, 0, 0, 0);
   }
 }
-constexpr int kTileLoads = 2;   // buffer loads per thread of one tile_load
 
 // Fragment of the 32 rows r0.. (MFMA row index = lane % 32), k-step ks of the 64 columns.
 SR_DEV bf16x8 row_frag(const bf16_t* tile, int r0, int ks) {
