@@ -97,3 +97,32 @@ def test_bad_call_arguments_rejected_before_launch():
     ada = _cfg(kind=abi.SR_BLOCK_ADALN)
     st = lib.sr_sparse_blocks_fwd(ctypes.byref(ada), 25, params, None, fake, fake + 4096, fake, 1 << 40, None, 0, None)
     assert st == abi.SR_EINVAL        # adaLN without cond
+
+
+def test_new_entry_points_reject_bad_arguments_before_launch():
+    _lib_or_skip()
+    import ctypes
+    cfg = _cfg()
+    fake = 1 << 40
+    lib = abi.lib()
+    # attention column sums: block outside [0, n_blocks), S > L, saved too small
+    assert lib.sr_attention_colsums(ctypes.byref(cfg), 25, fake, 1 << 40, 2, fake, None) == abi.SR_EINVAL
+    assert lib.sr_attention_colsums(ctypes.byref(cfg), 101, fake, 1 << 40, 0, fake, None) == abi.SR_ESHAPE
+    assert lib.sr_attention_colsums(ctypes.byref(cfg), 25, fake, 16, 0, fake, None) == abi.SR_EWORKSPACE
+    # top-K over score planes: parts < 1, K > L, NULL planes
+    assert lib.sr_select_topk_scores(ctypes.byref(cfg), 10, fake, 0, fake, None) == abi.SR_EINVAL
+    assert lib.sr_select_topk_scores(ctypes.byref(cfg), 101, fake, 4, fake, None) == abi.SR_ESHAPE
+    assert lib.sr_select_topk_scores(ctypes.byref(cfg), 10, None, 4, fake, None) == abi.SR_EINVAL
+    # fused routed step: K > L, NULL idx, saved too small, backward without scratch
+    params = (abi.SrBlockParams * 2)()
+    for i in range(2):
+        for n in abi.PARAM_FIELDS:
+            setattr(params[i], n, fake)
+    grads = (abi.SrBlockGrads * 2)()
+    assert lib.sr_routed_blocks_fwd(ctypes.byref(cfg), 101, fake, params, None, fake, fake, 1 << 40, None) == abi.SR_ESHAPE
+    assert lib.sr_routed_blocks_fwd(ctypes.byref(cfg), 25, None, params, None, fake, fake, 1 << 40, None) == abi.SR_EINVAL
+    assert lib.sr_routed_blocks_fwd(ctypes.byref(cfg), 25, fake, params, None, fake, fake, 16, None) == abi.SR_EWORKSPACE
+    st = lib.sr_routed_blocks_bwd(ctypes.byref(cfg), 25, fake, params, None, fake, 1 << 40, fake, grads, None, None, 0,
+                                  None)
+    assert st in (abi.SR_EINVAL, abi.SR_EWORKSPACE)
+    assert abi.sr_last_error()
