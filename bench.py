@@ -200,6 +200,44 @@ def graph_timing(st: Step, steps: int, warmup: int) -> dict:
             "outputs_finite": finite}
 
 
+def cross_attention_timing(reps: int = 5) -> dict:
+    """The asymmetric attention of the generative block's sparse stage at its shape (2 samples,
+    2048 routed queries against 8192 conditioning tokens, 16 heads, D = 1024, bf16), forward
+    and backward through sr_cross_attention_fwd / _bwd (generic kernels), HIP-event timed."""
+    import torch
+    from paper_2607_02829_amd import abi
+    B, Sq, Skv, D, H = 2, 2048, 8192, 1024, 16
+    cfg = abi.SrConfig(B=B, L=1, D=D, H=H, F=64, n_blocks=1, dtype=abi.SR_BF16, kind=abi.SR_BLOCK_PRELN,
+                       ln_eps=1e-6, idx_shared=0)
+    g = torch.Generator(device="cuda").manual_seed(5)
+    q = torch.randn((B, Sq, D), device="cuda", generator=g).to(torch.bfloat16)
+    kv = torch.randn((B, Skv, 2 * D), device="cuda", generator=g).to(torch.bfloat16)
+    dO = torch.randn((B, Sq, D), device="cuda", generator=g).to(torch.bfloat16)
+    O, dq, dkv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(kv)
+    lse = torch.empty((B, H, Sq), dtype=torch.float32, device="cuda")
+    delta = torch.empty_like(lse)
+    times = {"fwd": [], "bwd": []}
+    for r in range(reps + 1):
+        for name in ("fwd", "bwd"):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            if name == "fwd":
+                abi.sr_cross_attention_fwd(cfg, Sq, Skv, q, kv, O, lse)
+            else:
+                abi.sr_cross_attention_bwd(cfg, Sq, Skv, q, kv, O, dO, lse, dq, dkv, delta)
+            e1.record()
+            torch.cuda.synchronize()
+            if r > 0:
+                times[name].append(e0.elapsed_time(e1))
+    out = {"shape": {"B": B, "Sq": Sq, "Skv": Skv, "D": D, "H": H}, "kernels": "generic"}
+    for name, mult in (("fwd", 4.0), ("bwd", 8.0)):
+        ms = sorted(times[name])[len(times[name]) // 2]
+        flops = mult * B * Sq * Skv * D
+        out[name] = {"ms": round(ms, 3), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
+                     "frac_of_2.5PF": round(flops / (ms * 1e-3) / PEAK_BF16_FLOPS, 4)}
+    return out
+
+
 def kernel_breakdown(st: Step, step_index: int):
     """One profiled step with every launch group bracketed by events."""
     import torch
@@ -402,6 +440,8 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="also time the fused routed step captured once in a HIP graph and replayed (the draw is "
                          "the one fixed at capture)")
+    ap.add_argument("--cross-attention", action="store_true",
+                    help="also time the generative block's asymmetric attention (2048 queries x 8192 keys)")
     ap.add_argument("--unfused", action="store_true",
                     help="time the routed step as separate gather / blocks / scatter calls (default: the fused "
                          "sr_routed_blocks_fwd/bwd)")
@@ -532,6 +572,7 @@ def main():
     if w.dtype == "bf16" and not args.no_routing_sweep:
         routing["sweep"] = routing_sweep(w.D)
 
+    xattn = cross_attention_timing() if args.cross_attention else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)
 
     routed_tok_s = w.B * w.K / (ms_step * 1e-3)
@@ -560,6 +601,7 @@ def main():
         "speedup_vs_dense": round(dense["ms_per_step"] / ms_step, 3) if dense else None,
         "trunk": trunk,
         "graph": graph,
+        "cross_attention": xattn,
         "peak_bytes": {"sparse": int(sparse_peak), "dense": dense["peak_bytes"] if dense else None,
                        "ratio": round(dense["peak_bytes"] / sparse_peak, 3) if dense else None},
         "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved_u, 2), "peak": peak_u, "unit": unit,

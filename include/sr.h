@@ -218,6 +218,26 @@ SR_API sr_status sr_routed_blocks_bwd(const sr_config* cfg, int32_t K, const int
                                const sr_block_grads* grads, float* dcond, void* scratch,
                                size_t scratch_bytes, void* stream);
 
+/* Asymmetric attention of the generative block's sparse middle stage (Sec. 3.4,
+ * "Integration with Generative Forecasting"): queries from Sq tokens (the routed ones),
+ * keys and values from Skv tokens (the whole conditioning sequence); per sample and head
+ *   O = softmax(q k^T / sqrt(hd)) v   over the Skv keys,   cost O(Sq Skv D).
+ * cfg supplies B, D, H (head dim D/H in {32, 64, 128}) and the storage dtype; L and the block
+ * fields are not used.
+ *   q: [B,Sq,D]; kv: [B,Skv,2D] (k of head h at columns h*hd .., v at D + h*hd ..);
+ *   O: [B,Sq,D] out; lse: [B,H,Sq] fp32 out, the base-2 log-sum-exp of the scaled scores.
+ * Generic kernels (one thread per query or key, fp32 accumulation, deterministic). */
+SR_API sr_status sr_cross_attention_fwd(const sr_config* cfg, int32_t Sq, int32_t Skv, const void* q,
+                                 const void* kv, void* O, float* lse, void* stream);
+
+/* Its backward: dq [B,Sq,D] and dkv [B,Skv,2D] (dk, dv in kv's layout) out, from the
+ * forward's q, kv, O, lse and the output gradient dO [B,Sq,D]; delta: [B,H,Sq] fp32
+ * caller scratch (receives rowsum(dO * O) per head). */
+SR_API sr_status sr_cross_attention_bwd(const sr_config* cfg, int32_t Sq, int32_t Skv, const void* q,
+                                 const void* kv, const void* O, const void* dO,
+                                 const float* lse, void* dq, void* dkv, float* delta,
+                                 void* stream);
+
 /* Debug check of an index set: *ok_dev (device int32) is set to 1 if every row of
  * idx is strictly increasing and inside [0,L), else 0. */
 SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx,
@@ -256,7 +276,8 @@ SR_API sr_status sr_select_topk_scores(const sr_config* cfg, int32_t K, const fl
  * sr_profile_stop waits for those events, stops recording and writes one line per
  * name: "<name> <launches> <total_ms> <algorithmic_flops> <algorithmic_bytes>\n"
  * into `out` (NUL-terminated, truncated to out_bytes); *needed receives the full
- * size.  Names: select_random, select_topk, select_topk_scores, attn_colsum, gather,
+ * size.  Names: select_random, select_topk, select_topk_scores, attn_colsum, xattn_fwd,
+ * xattn_bwd, gather,
  * scatter_delta, gather_f32, scatter_f32, ln_fwd, ln_bwd,
  * gemm_<op> (qkv, o, fc1, fc2, dx_fc2, dx_fc1, dx_o, dx_qkv, dw_<op>), attn_fwd,
  * attn_bwd_dkv, attn_bwd_dq, attn_bwd_delta, reduce, colsum, convert, mod. */

@@ -25,6 +25,7 @@ EXPORTS = ("sr_last_error", "sr_version", "sr_workspace_bytes", "sr_select_scrat
            "sr_select_indices", "sr_gather", "sr_scatter_delta", "sr_sparse_blocks_fwd",
            "sr_sparse_blocks_bwd", "sr_dense_blocks_fwd", "sr_dense_blocks_bwd", "sr_validate_indices",
            "sr_attention_colsums", "sr_select_topk_scores", "sr_routed_blocks_fwd", "sr_routed_blocks_bwd",
+           "sr_cross_attention_fwd", "sr_cross_attention_bwd",
            "sr_profile_start", "sr_profile_stop")
 
 
@@ -81,6 +82,8 @@ def lib(path: str = LIB_PATH):
         "sr_validate_indices": ([CP, I32, P, P, P], I32),
         "sr_attention_colsums": ([CP, I32, P, SZ, I32, P, P], I32),
         "sr_routed_blocks_fwd": ([CP, I32, P, P, P, P, P, SZ, P], I32),
+        "sr_cross_attention_fwd": ([CP, I32, I32, P, P, P, P, P], I32),
+        "sr_cross_attention_bwd": ([CP, I32, I32, P, P, P, P, P, P, P, P, P], I32),
         "sr_routed_blocks_bwd": ([CP, I32, P, P, P, P, SZ, P, P, P, P, SZ, P], I32),
         "sr_select_topk_scores": ([CP, I32, P, I32, P, P], I32),
         "sr_profile_start": ([ctypes.c_char_p], I32),
@@ -194,6 +197,15 @@ def sr_routed_blocks_fwd(cfg, K, idx, params, cond, x, saved, stream=None):
 def sr_routed_blocks_bwd(cfg, K, idx, params, cond, saved, g, grads, dcond, scratch, stream=None):
     _check(lib().sr_routed_blocks_bwd(ctypes.byref(cfg), K, _p(idx), params, _p(cond), _p(saved), _nbytes(saved),
                                       _p(g), grads, _p(dcond), _p(scratch), _nbytes(scratch), _stream(stream)))
+
+
+def sr_cross_attention_fwd(cfg, Sq, Skv, q, kv, O, lse, stream=None):
+    _check(lib().sr_cross_attention_fwd(ctypes.byref(cfg), Sq, Skv, _p(q), _p(kv), _p(O), _p(lse), _stream(stream)))
+
+
+def sr_cross_attention_bwd(cfg, Sq, Skv, q, kv, O, dO, lse, dq, dkv, delta, stream=None):
+    _check(lib().sr_cross_attention_bwd(ctypes.byref(cfg), Sq, Skv, _p(q), _p(kv), _p(O), _p(dO), _p(lse), _p(dq),
+                                        _p(dkv), _p(delta), _stream(stream)))
 
 
 def sr_attention_colsums(cfg, S, saved, block, colsum, stream=None):

@@ -13,7 +13,8 @@ ROOT = os.path.dirname(HERE)
 OUT = os.path.join(HERE, "libsr.so")
 BUILD = os.path.join(ROOT, "_build")
 
-SOURCES = ["select.hip", "routing.hip", "rowops.hip", "gemv.hip", "gemm.hip", "attention.hip", "stack.cpp", "api.cpp", "profile.cpp"]
+SOURCES = ["select.hip", "routing.hip", "rowops.hip", "gemv.hip", "gemm.hip", "attention.hip", "cross_attention.hip",
+           "stack.cpp", "api.cpp", "profile.cpp"]
 # Files whose floating-point results are part of a bit-exact contract (top-k score,
 # scatter rounding): no multiply-add contraction anywhere in them.
 NO_CONTRACT = {"select.hip", "routing.hip"}

@@ -329,6 +329,56 @@ sr_status sr_select_topk_scores(const sr_config* cfg, int32_t K, const float* pl
   return hip_status(sr::launch_select_topk_planes(rows, cfg->L, K, parts, planes, idx, st), "select_topk_scores");
 }
 
+namespace {
+sr_status check_xattn(const sr_config* cfg, int32_t Sq, int32_t Skv) {
+  sr_status s = check_cfg(cfg, true);
+  if (s != SR_OK) return s;
+  SR_CHECK(Sq >= 1 && Skv >= 1, SR_ESHAPE, "Sq=%d and Skv=%d must be >= 1", Sq, Skv);
+  const size_t e = elt_of(cfg->dtype);
+  SR_CHECK((size_t)cfg->B * Skv * 2 * cfg->D * e < (1ull << 31) && (size_t)cfg->B * Sq * cfg->D * e < (1ull << 31),
+           SR_EUNSUPPORTED, "attention operands beyond 2 GiB are not supported");
+  return SR_OK;
+}
+}  // namespace
+
+sr_status sr_cross_attention_fwd(const sr_config* cfg, int32_t Sq, int32_t Skv, const void* q, const void* kv,
+                                 void* O, float* lse, void* stream) {
+  sr_status s = check_xattn(cfg, Sq, Skv);
+  if (s != SR_OK) return s;
+  SR_PTR(q, "q");
+  SR_PTR(kv, "kv");
+  SR_PTR(O, "O");
+  SR_PTR(lse, "lse");
+  hipStream_t st = (hipStream_t)stream;
+  const int dt = cfg->dtype == SR_BF16 ? sr::kBF16 : sr::kF32;
+  const size_t e = elt_of(cfg->dtype);
+  sr::ProfScope ps("xattn_fwd", 4.0 * cfg->B * (double)Sq * Skv * cfg->D,
+                   (double)cfg->B * (2.0 * Sq + 2.0 * Skv) * cfg->D * e, st);
+  return hip_status(sr::launch_xattn_fwd(dt, q, kv, O, lse, cfg->B, Sq, Skv, cfg->H, cfg->D, st), "xattn_fwd");
+}
+
+sr_status sr_cross_attention_bwd(const sr_config* cfg, int32_t Sq, int32_t Skv, const void* q, const void* kv,
+                                 const void* O, const void* dO, const float* lse, void* dq, void* dkv, float* delta,
+                                 void* stream) {
+  sr_status s = check_xattn(cfg, Sq, Skv);
+  if (s != SR_OK) return s;
+  SR_PTR(q, "q");
+  SR_PTR(kv, "kv");
+  SR_PTR(O, "O");
+  SR_PTR(dO, "dO");
+  SR_PTR(lse, "lse");
+  SR_PTR(dq, "dq");
+  SR_PTR(dkv, "dkv");
+  SR_PTR(delta, "delta");
+  hipStream_t st = (hipStream_t)stream;
+  const int dt = cfg->dtype == SR_BF16 ? sr::kBF16 : sr::kF32;
+  const size_t e = elt_of(cfg->dtype);
+  sr::ProfScope ps("xattn_bwd", 8.0 * cfg->B * (double)Sq * Skv * cfg->D,
+                   (double)cfg->B * (5.0 * Sq + 4.0 * Skv) * cfg->D * e, st);
+  return hip_status(sr::launch_xattn_bwd(dt, q, kv, O, dO, lse, delta, dq, dkv, cfg->B, Sq, Skv, cfg->H, cfg->D, st),
+                    "xattn_bwd");
+}
+
 sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx, int32_t* ok_dev, void* stream) {
   sr_status s = check_cfg(cfg, true);
   if (s != SR_OK) return s;

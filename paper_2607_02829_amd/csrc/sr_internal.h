@@ -123,6 +123,10 @@ hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int 
                            hipStream_t st);
 hipError_t launch_attn_colsum(int dtype, const void* qkv, const float* lse, float* colsum, int B, int S, int H, int D,
                               hipStream_t st);
+hipError_t launch_xattn_fwd(int dtype, const void* q, const void* kv, void* O, float* lse, int B, int Sq, int Skv,
+                            int H, int D, hipStream_t st);
+hipError_t launch_xattn_bwd(int dtype, const void* q, const void* kv, const void* O, const void* dO, const float* lse,
+                            float* delta, void* dq, void* dkv, int B, int Sq, int Skv, int H, int D, hipStream_t st);
 hipError_t launch_attn_bwd(int dtype, const void* qkv, const void* dO, const float* lse, const float* delta,
                            void* dqkv, int B, int S, int H, int D, hipStream_t st);
 

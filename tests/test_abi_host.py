@@ -126,3 +126,17 @@ def test_new_entry_points_reject_bad_arguments_before_launch():
                                   None)
     assert st in (abi.SR_EINVAL, abi.SR_EWORKSPACE)
     assert abi.sr_last_error()
+
+
+def test_cross_attention_rejects_bad_arguments_before_launch():
+    _lib_or_skip()
+    import ctypes
+    cfg = _cfg()
+    fake = 1 << 40
+    lib = abi.lib()
+    assert lib.sr_cross_attention_fwd(ctypes.byref(cfg), 0, 10, fake, fake, fake, fake, None) == abi.SR_ESHAPE
+    assert lib.sr_cross_attention_fwd(ctypes.byref(cfg), 10, 10, None, fake, fake, fake, None) == abi.SR_EINVAL
+    assert lib.sr_cross_attention_bwd(ctypes.byref(cfg), 10, 0, fake, fake, fake, fake, fake, fake, fake, fake,
+                                      None) == abi.SR_ESHAPE
+    assert lib.sr_cross_attention_bwd(ctypes.byref(cfg), 10, 10, fake, fake, fake, fake, fake, fake, fake, None,
+                                      None) == abi.SR_EINVAL
