@@ -203,7 +203,8 @@ def graph_timing(st: Step, steps: int, warmup: int) -> dict:
 def cross_attention_timing(reps: int = 5) -> dict:
     """The asymmetric attention of the generative block's sparse stage at its shape (2 samples,
     2048 routed queries against 8192 conditioning tokens, 16 heads, D = 1024, bf16), forward
-    and backward through sr_cross_attention_fwd / _bwd (generic kernels), HIP-event timed."""
+    and backward through sr_cross_attention_fwd / _bwd (the MFMA attention kernels), HIP-event
+    timed; algorithmic FLOPs 4 B Sq Skv D forward, 8 B Sq Skv D backward."""
     import torch
     from paper_2607_02829_amd import abi
     B, Sq, Skv, D, H = 2, 2048, 8192, 1024, 16
@@ -229,7 +230,7 @@ def cross_attention_timing(reps: int = 5) -> dict:
             torch.cuda.synchronize()
             if r > 0:
                 times[name].append(e0.elapsed_time(e1))
-    out = {"shape": {"B": B, "Sq": Sq, "Skv": Skv, "D": D, "H": H}, "kernels": "generic"}
+    out = {"shape": {"B": B, "Sq": Sq, "Skv": Skv, "D": D, "H": H}, "kernels": "mfma (bf16, head dim 64)"}
     for name, mult in (("fwd", 4.0), ("bwd", 8.0)):
         ms = sorted(times[name])[len(times[name]) // 2]
         flops = mult * B * Sq * Skv * D

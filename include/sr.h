@@ -226,7 +226,8 @@ SR_API sr_status sr_routed_blocks_bwd(const sr_config* cfg, int32_t K, const int
  * fields are not used.
  *   q: [B,Sq,D]; kv: [B,Skv,2D] (k of head h at columns h*hd .., v at D + h*hd ..);
  *   O: [B,Sq,D] out; lse: [B,H,Sq] fp32 out, the base-2 log-sum-exp of the scaled scores.
- * Generic kernels (one thread per query or key, fp32 accumulation, deterministic). */
+ * bf16 with head dim 64 runs the MFMA attention kernels (the self-attention kernels, given
+ * the two buffers and token counts); other cases generic kernels.  Deterministic. */
 SR_API sr_status sr_cross_attention_fwd(const sr_config* cfg, int32_t Sq, int32_t Skv, const void* q,
                                  const void* kv, void* O, float* lse, void* stream);
 

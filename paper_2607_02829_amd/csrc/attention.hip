@@ -203,19 +203,22 @@ SR_DEV void unstage(const bf16_t* stage, bf16_t* dst, size_t ld, int r0, int S) 
 // ------------------------------------------------------------------------------ forward
 
 // NW waves (32 queries each) per workgroup share the K / V tiles.
+// Queries: Sq rows of q (row stride ldq); keys: Skv rows of kv (row stride ldkv), values D
+// columns after the keys; kv_elems: elements addressable from kv (the buffer's extent).
 template <int NW>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ O,
-                                                     float* __restrict__ lse, int S, int H, int D, float sl2) {
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* __restrict__ q, int ldq,
+                                                     const bf16_t* __restrict__ kv, int ldkv, uint32_t kv_elems,
+                                                     bf16_t* __restrict__ O, float* __restrict__ lse, int Sq, int Skv,
+                                                     int H, int D, float sl2) {
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
-  const size_t ld = 3 * (size_t)D;
-  const bf16_t* qp = qkv + (size_t)b * S * ld + hh * HD;
+  const bf16_t* qp = q + (size_t)b * Sq * ldq + hh * HD;
   const int myq = blockIdx.x * (32 * NW) + wid * 32 + l32;
-  const int nt = (S + KT - 1) / KT;
-  const bool ragged = S % KT != 0;
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
-  const uint32_t kbase = (uint32_t)(((size_t)b * S * ld + D + hh * HD) * 2);
+  const int nt = (Skv + KT - 1) / KT;
+  const bool ragged = Skv % KT != 0;
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(kv, kv_elems * 2u);
+  const uint32_t kbase = (uint32_t)(((size_t)b * Skv * ldkv + hh * HD) * 2);
   const uint32_t vbase = kbase + (uint32_t)D * 2u;
   RowAddr ra;
   TrAddr ta;
@@ -224,17 +227,17 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
 
   bf16x8 qf[4];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) qf[ks] = myq < S ? ld8(qp + (size_t)myq * ld + ks * 16 + 8 * h32) : zero8();
+  for (int ks = 0; ks < 4; ++ks) qf[ks] = myq < Sq ? ld8(qp + (size_t)myq * ldq + ks * 16 + 8 * h32) : zero8();
 
   constexpr int kLoads = 2 * (8 / NW);   // buffer loads per thread per tile (two tiles)
   auto load = [&](int t, int s) {
-    tile_load<NW>(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE, t < nt);
-    tile_load<NW>(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE, t < nt);
+    tile_load<NW>(rq, kbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE, t < nt);
+    tile_load<NW>(rq, vbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE + TE, t < nt);
   };
-  auto mask = [&](f32x16& sc, int k0) {   // keys past S do not exist
+  auto mask = [&](f32x16& sc, int k0) {   // keys past Skv do not exist
 #pragma unroll
     for (int r = 0; r < 16; ++r)
-      if (k0 + srow(r, h32) >= S) sc[r] = -INFINITY;
+      if (k0 + srow(r, h32) >= Skv) sc[r] = -INFINITY;
   };
 
   f32x16 o[2];
@@ -335,8 +338,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
     scores(k0r, sc0);
     scores(k1r, sc1);
     if (rag) {
-      if (S - t * KT < 32) mask(sc0, t * KT);
-      if (S - t * KT < 64) mask(sc1, t * KT + 32);
+      if (Skv - t * KT < 32) mask(sc0, t * KT);
+      if (Skv - t * KT < 64) mask(sc1, t * KT + 32);
     }
     consume(stg, sc0, sc1);
     wait_vm_lgkm0<kLoads>();   // tile t+1 resident: only tile t+2's loads may still fly
@@ -354,50 +357,52 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();   // every wave is done with the stages before they hold the output
   const float l_tot = half_pair_sum(lsum[0]);   // the second half's element is zero
-  if (h32 == 0 && myq < S) lse[((size_t)b * H + hh) * S + myq] = m_run * sl2 + log2f(l_tot);
+  if (h32 == 0 && myq < Sq) lse[((size_t)b * H + hh) * Sq + myq] = m_run * sl2 + log2f(l_tot);
   stage_t(smem, o, 1.0f / l_tot, wid, lane);
   __syncthreads();
-  unstage<NW>(smem, O + (size_t)b * S * D + hh * HD, D, blockIdx.x * (32 * NW), S);
+  unstage<NW>(smem, O + (size_t)b * Sq * D + hh * HD, D, blockIdx.x * (32 * NW), Sq);
 }
 
 // ------------------------------------------------------------------------------ backward dK, dV
 
 // NW waves (32 keys each) per workgroup share the Q / dO tiles.
 template <int NW>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ dO,
+// Keys: Skv rows of kv (stride ldkv, values D columns on); queries: Sq rows of q (stride ldq,
+// q_elems addressable elements); dK to dk_out (stride ldo), dV D columns after it.
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_t* __restrict__ q, int ldq,
+                                                         uint32_t q_elems, const bf16_t* __restrict__ kv, int ldkv,
+                                                         const bf16_t* __restrict__ dO,
                                                          const float* __restrict__ lse, const float* __restrict__ delta,
-                                                         bf16_t* __restrict__ dqkv, int S, int H, int D, float sl2,
-                                                         float scale) {
+                                                         bf16_t* __restrict__ dk_out, int ldo, int Sq, int Skv, int H,
+                                                         int D, float sl2, float scale) {
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: Q tile, dO tile
   __shared__ __attribute__((aligned(16))) float fsm[NSTG * 2 * KT];     // stage: lse, delta of the tile's rows
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
-  const size_t ld = 3 * (size_t)D;
-  const bf16_t* base = qkv + (size_t)b * S * ld;
-  const bf16_t* kp = base + D + hh * HD;
-  const bf16_t* vp = base + 2 * D + hh * HD;
+  const bf16_t* kp = kv + (size_t)b * Skv * ldkv + hh * HD;
+  const bf16_t* vp = kp + D;
   const int mykey = blockIdx.x * (32 * NW) + wid * 32 + l32;
-  const int nt = (S + KT - 1) / KT;
-  const bool ragged = S % KT != 0;
+  const int nt = (Sq + KT - 1) / KT;
+  const bool ragged = Sq % KT != 0;
 
   bf16x8 kf[4], vf[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
-    kf[ks] = mykey < S ? ld8(kp + (size_t)mykey * ld + ks * 16 + 8 * h32) : zero8();
-    vf[ks] = mykey < S ? ld8(vp + (size_t)mykey * ld + ks * 16 + 8 * h32) : zero8();
+    kf[ks] = mykey < Skv ? ld8(kp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8();
+    vf[ks] = mykey < Skv ? ld8(vp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8();
   }
   f32x16 dv[2], dk[2];
   zero16(dv[0]); zero16(dv[1]); zero16(dk[0]); zero16(dk[1]);
 
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
-  const __amdgpu_buffer_rsrc_t rd = make_rsrc(dO, (uint32_t)((size_t)gridDim.z * S * D * 2));
-  const __amdgpu_buffer_rsrc_t rl = make_rsrc(lse, (uint32_t)((size_t)gridDim.z * H * S * 4));
-  const __amdgpu_buffer_rsrc_t rdl = make_rsrc(delta, (uint32_t)((size_t)gridDim.z * H * S * 4));
-  const uint32_t qbase = (uint32_t)(((size_t)b * S * ld + hh * HD) * 2);
-  const uint32_t dbase = (uint32_t)(((size_t)b * S * D + hh * HD) * 2);
-  const uint32_t lbase = (uint32_t)(((size_t)b * H + hh) * S * 4);
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q, q_elems * 2u);
+  const __amdgpu_buffer_rsrc_t rd = make_rsrc(dO, (uint32_t)((size_t)gridDim.z * Sq * D * 2));
+  const __amdgpu_buffer_rsrc_t rl = make_rsrc(lse, (uint32_t)((size_t)gridDim.z * H * Sq * 4));
+  const __amdgpu_buffer_rsrc_t rdl = make_rsrc(delta, (uint32_t)((size_t)gridDim.z * H * Sq * 4));
+  const uint32_t qbase = (uint32_t)(((size_t)b * Sq * ldq + hh * HD) * 2);
+  const uint32_t dbase = (uint32_t)(((size_t)b * Sq * D + hh * HD) * 2);
+  const uint32_t lbase = (uint32_t)(((size_t)b * H + hh) * Sq * 4);
   auto load = [&](int t, int s) {
-    tile_load<NW>(rq, qbase, (uint32_t)ld, t * KT, smem + s * 2 * TE);
+    tile_load<NW>(rq, qbase, (uint32_t)ldq, t * KT, smem + s * 2 * TE);
     tile_load<NW>(rd, dbase, (uint32_t)D, t * KT, smem + s * 2 * TE + TE);
     const uint32_t lo = lbase + (uint32_t)(t * KT + lane) * 4u;
     if (wid == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_ptr_t*)(fsm + s * 2 * KT), 4, lo, 0, 0, 0);
@@ -429,7 +434,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
       float p = ex2(fmaf(sv[r], sl2, -ls[ql]));
       float ds = p * (dpv[r] - dls[ql]);
       if constexpr (decltype(rag)::value) {
-        if (q0 + ql >= S) { p = 0.f; ds = 0.f; }
+        if (q0 + ql >= Sq) { p = 0.f; ds = 0.f; }
       }
       pb[r >> 3][r & 7] = (__bf16)p;
       sb[r >> 3][r & 7] = (__bf16)ds;
@@ -477,47 +482,50 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
 
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  bf16_t* out = dqkv + (size_t)b * S * ld;
+  bf16_t* out = dk_out + (size_t)b * Skv * ldo;
   stage_t(smem, dk, scale, wid, lane);
   __syncthreads();
-  unstage<NW>(smem, out + D + hh * HD, ld, blockIdx.x * (32 * NW), S);
+  unstage<NW>(smem, out + hh * HD, ldo, blockIdx.x * (32 * NW), Skv);
   __syncthreads();
   stage_t(smem, dv, 1.0f, wid, lane);
   __syncthreads();
-  unstage<NW>(smem, out + 2 * D + hh * HD, ld, blockIdx.x * (32 * NW), S);
+  unstage<NW>(smem, out + D + hh * HD, ldo, blockIdx.x * (32 * NW), Skv);
 }
 
 // ------------------------------------------------------------------------------ backward dQ
 
 // NW waves (32 queries each) per workgroup share the K / V tiles.
 template <int NW>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ dO,
+// Queries: Sq rows of q (stride ldq); keys: Skv rows of kv (stride ldkv, kv_elems addressable
+// elements, values D columns on); dQ to dq_out (stride ldo).
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t* __restrict__ q, int ldq,
+                                                        const bf16_t* __restrict__ kv, int ldkv, uint32_t kv_elems,
+                                                        const bf16_t* __restrict__ dO,
                                                         const float* __restrict__ lse, const float* __restrict__ delta,
-                                                        bf16_t* __restrict__ dqkv, int S, int H, int D, float sl2,
-                                                        float scale) {
+                                                        bf16_t* __restrict__ dq_out, int ldo, int Sq, int Skv, int H,
+                                                        int D, float sl2, float scale) {
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
-  const size_t ld = 3 * (size_t)D;
-  const bf16_t* qp = qkv + (size_t)b * S * ld + hh * HD;
-  const bf16_t* dop = dO + (size_t)b * S * D + hh * HD;
+  const bf16_t* qp = q + (size_t)b * Sq * ldq + hh * HD;
+  const bf16_t* dop = dO + (size_t)b * Sq * D + hh * HD;
   const int myq = blockIdx.x * (32 * NW) + wid * 32 + l32;
-  const int nt = (S + KT - 1) / KT;
-  const bool ragged = S % KT != 0;
+  const int nt = (Skv + KT - 1) / KT;
+  const bool ragged = Skv % KT != 0;
 
   bf16x8 qf[4], df[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
-    qf[ks] = myq < S ? ld8(qp + (size_t)myq * ld + ks * 16 + 8 * h32) : zero8();
-    df[ks] = myq < S ? ld8(dop + (size_t)myq * D + ks * 16 + 8 * h32) : zero8();
+    qf[ks] = myq < Sq ? ld8(qp + (size_t)myq * ldq + ks * 16 + 8 * h32) : zero8();
+    df[ks] = myq < Sq ? ld8(dop + (size_t)myq * D + ks * 16 + 8 * h32) : zero8();
   }
-  const float nlse = myq < S ? -lse[((size_t)b * H + hh) * S + myq] : -INFINITY;
-  const float dl_q = myq < S ? delta[((size_t)b * H + hh) * S + myq] : 0.f;
+  const float nlse = myq < Sq ? -lse[((size_t)b * H + hh) * Sq + myq] : -INFINITY;
+  const float dl_q = myq < Sq ? delta[((size_t)b * H + hh) * Sq + myq] : 0.f;
   f32x16 dq[2];
   zero16(dq[0]); zero16(dq[1]);
 
-  const __amdgpu_buffer_rsrc_t rq = make_rsrc(qkv, (uint32_t)((size_t)gridDim.z * S * ld * 2));
-  const uint32_t kbase = (uint32_t)(((size_t)b * S * ld + D + hh * HD) * 2);
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(kv, kv_elems * 2u);
+  const uint32_t kbase = (uint32_t)(((size_t)b * Skv * ldkv + hh * HD) * 2);
   const uint32_t vbase = kbase + (uint32_t)D * 2u;
   RowAddr ra;
   TrAddr ta;
@@ -525,8 +533,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t
   ta.init(lds_addr(smem), lane);
   constexpr int kLoads = 2 * (8 / NW);   // buffer loads per thread per tile (two tiles)
   auto load = [&](int t, int s) {
-    tile_load<NW>(rq, kbase, (uint32_t)ld, t * KT, smem + s * 2 * TE, t < nt);
-    tile_load<NW>(rq, vbase, (uint32_t)ld, t * KT, smem + s * 2 * TE + TE, t < nt);
+    tile_load<NW>(rq, kbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE, t < nt);
+    tile_load<NW>(rq, vbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE + TE, t < nt);
   };
   // K (tile 0) or V (tile 1) row fragments of key unit U of stage SG
   auto read_rows = [&](auto sg, auto uu, auto tl, RawFrag<true> (&fr)[4]) {
@@ -558,7 +566,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t
       const float p = ex2(fmaf(sv[r], sl2, nlse));
       float ds = p * (dpv[r] - dl_q);
       if constexpr (decltype(rag)::value) {
-        if (k0 + srow(r, h32) >= S) ds = 0.f;
+        if (k0 + srow(r, h32) >= Skv) ds = 0.f;
       }
       sb[r >> 3][r & 7] = (__bf16)ds;
     }
@@ -613,7 +621,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t
   __syncthreads();
   stage_t(smem, dq, scale, wid, lane);
   __syncthreads();
-  unstage<NW>(smem, dqkv + (size_t)b * S * ld + hh * HD, ld, blockIdx.x * (32 * NW), S);
+  unstage<NW>(smem, dq_out + (size_t)b * Sq * ldo + hh * HD, ldo, blockIdx.x * (32 * NW), Sq);
 }
 
 // ------------------------------------------------------------------------------ generic kernels
@@ -864,15 +872,52 @@ static hipError_t bwd_simple(const Ta* qkv, const Ta* dO, const float* lse, cons
   return hipGetLastError();
 }
 
+#define SR_TRY_HIP(x)                 \
+  do {                                \
+    hipError_t e_ = (x);              \
+    if (e_ != hipSuccess) return e_;  \
+  } while (0)
+
+// The MFMA kernels on Sq query rows and Skv key/value rows (self-attention: both S, q, k and v
+// in one token-major qkv buffer; asymmetric attention: separate buffers).
+hipError_t launch_attn_fwd_mfma(const bf16_t* q, int ldq, const bf16_t* kv, int ldkv, uint32_t kv_elems, bf16_t* O,
+                                float* lse, int B, int Sq, int Skv, int H, int D, hipStream_t st) {
+  constexpr int kw = kFwdWaves;
+  dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
+  hipLaunchKernelGGL(attn_fwd_mfma<kw>, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv, H, D,
+                     attn_sl2(D / H));
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_dkv_mfma(const bf16_t* q, int ldq, uint32_t q_elems, const bf16_t* kv, int ldkv,
+                                const bf16_t* dO, const float* lse, const float* delta, bf16_t* dk_out, int ldo, int B,
+                                int Sq, int Skv, int H, int D, hipStream_t st) {
+  constexpr int kw = kDkvWaves;
+  dim3 g((Skv + 32 * kw - 1) / (32 * kw), H, B);
+  const int hd = D / H;
+  hipLaunchKernelGGL(attn_bwd_dkv_mfma<kw>, g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta, dk_out,
+                     ldo, Sq, Skv, H, D, attn_sl2(hd), 1.0f / sqrtf((float)hd));
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_dq_mfma(const bf16_t* q, int ldq, const bf16_t* kv, int ldkv, uint32_t kv_elems,
+                               const bf16_t* dO, const float* lse, const float* delta, bf16_t* dq_out, int ldo, int B,
+                               int Sq, int Skv, int H, int D, hipStream_t st) {
+  constexpr int kw = kDqWaves;
+  dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
+  const int hd = D / H;
+  hipLaunchKernelGGL(attn_bwd_dq_mfma<kw>, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta, dq_out,
+                     ldo, Sq, Skv, H, D, attn_sl2(hd), 1.0f / sqrtf((float)hd));
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int B, int S, int H, int D,
                            hipStream_t st) {
   const int hd = D / H;
   if (attn_uses_mfma(dtype, hd)) {
-    constexpr int kw = kFwdWaves;
-    dim3 g((S + 32 * kw - 1) / (32 * kw), H, B);
-    hipLaunchKernelGGL(attn_fwd_mfma<kw>, g, dim3(64 * kw), 0, st, (const bf16_t*)qkv, (bf16_t*)O, lse, S, H, D,
-                       attn_sl2(hd));
-    return hipGetLastError();
+    const bf16_t* q = (const bf16_t*)qkv;
+    return launch_attn_fwd_mfma(q, 3 * D, q + D, 3 * D, (uint32_t)((size_t)B * S * 3 * D - D), (bf16_t*)O, lse, B,
+                                S, S, H, D, st);
   }
   if (dtype == kBF16) return fwd_simple((const bf16_t*)qkv, (bf16_t*)O, lse, B, S, H, D, hd, st);
   return fwd_simple((const float*)qkv, (float*)O, lse, B, S, H, D, hd, st);
@@ -884,22 +929,21 @@ hipError_t launch_attn_bwd(int dtype, const void* qkv, const void* dO, const flo
   if (attn_uses_mfma(dtype, hd)) {
     const float sl2 = attn_sl2(hd), sc = 1.0f / sqrtf((float)hd);
     const double units = 2.0 * B * (double)S * S * D;   // one S x S x hd product over all heads
+    const bf16_t* q = (const bf16_t*)qkv;
+    const uint32_t all = (uint32_t)((size_t)B * S * 3 * D);
     {
       // algorithmic: dP, dV, dK (the recomputed scores are not counted)
       ProfScope ps("attn_bwd_dkv", 3 * units, (double)B * S * D * 2 * 6, st);
-      constexpr int kw = kDkvWaves;
-      dim3 gk((S + 32 * kw - 1) / (32 * kw), H, B);
-      hipLaunchKernelGGL(attn_bwd_dkv_mfma<kw>, gk, dim3(64 * kw), 0, st, (const bf16_t*)qkv, (const bf16_t*)dO, lse,
-                         delta, (bf16_t*)dqkv, S, H, D, sl2, sc);
+      SR_TRY_HIP(launch_attn_dkv_mfma(q, 3 * D, all, q + D, 3 * D, (const bf16_t*)dO, lse, delta, (bf16_t*)dqkv + D,
+                                      3 * D, B, S, S, H, D, st));
     }
     {
       ProfScope ps("attn_bwd_dq", units, (double)B * S * D * 2 * 5, st);
-      constexpr int kw = kDqWaves;
-      dim3 gq((S + 32 * kw - 1) / (32 * kw), H, B);
-      hipLaunchKernelGGL(attn_bwd_dq_mfma<kw>, gq, dim3(64 * kw), 0, st, (const bf16_t*)qkv, (const bf16_t*)dO, lse,
-                         delta, (bf16_t*)dqkv, S, H, D, sl2, sc);
+      SR_TRY_HIP(launch_attn_dq_mfma(q, 3 * D, q + D, 3 * D, all - D, (const bf16_t*)dO, lse, delta, (bf16_t*)dqkv,
+                                     3 * D, B, S, S, H, D, st));
     }
-    return hipGetLastError();
+    (void)sl2; (void)sc;
+    return hipSuccess;
   }
   ProfScope ps("attn_bwd_generic", 8.0 * B * (double)S * S * D, 0, st);
   if (dtype == kBF16)

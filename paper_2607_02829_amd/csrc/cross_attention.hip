@@ -7,9 +7,10 @@
 // at column h*hd, v at D + h*hd); lse, delta [B, H, Sq], lse the base-2 log-sum-exp of the scaled
 // scores (P = exp2(s * log2(e)/sqrt(hd) - lse)), delta = rowsum(dO * O) per head.
 //
-// Generic kernels (any storage type, hd in {32, 64, 128}): one thread per query (forward with
-// online softmax, dQ) or per key (dK and dV, summing over the queries in order), fp32
-// accumulation, deterministic.  The MFMA attention kernels still take one token count.
+// bf16 with hd = 64 runs the MFMA attention kernels (attention.hip), which take the query and
+// key/value buffers and their token counts separately.  Generic kernels (any storage type, hd in
+// {32, 64, 128}) for the rest: one thread per query (forward with online softmax, dQ) or per
+// key (dK and dV, summing over the queries in order), fp32 accumulation, deterministic.
 #include "common.h"
 #include "sr_internal.h"
 
@@ -160,6 +161,9 @@ static hipError_t xbwd(const Ta* q, const Ta* kv, const Ta* dO, const float* lse
 
 hipError_t launch_xattn_fwd(int dtype, const void* q, const void* kv, void* O, float* lse, int B, int Sq, int Skv,
                             int H, int D, hipStream_t st) {
+  if (attn_uses_mfma(dtype, D / H))
+    return launch_attn_fwd_mfma((const bf16_t*)q, D, (const bf16_t*)kv, 2 * D, (uint32_t)((size_t)B * Skv * 2 * D),
+                                (bf16_t*)O, lse, B, Sq, Skv, H, D, st);
   if (dtype == kBF16) return xfwd((const bf16_t*)q, (const bf16_t*)kv, (bf16_t*)O, lse, B, Sq, Skv, H, D, st);
   return xfwd((const float*)q, (const float*)kv, (float*)O, lse, B, Sq, Skv, H, D, st);
 }
@@ -168,6 +172,14 @@ hipError_t launch_xattn_bwd(int dtype, const void* q, const void* kv, const void
                             float* delta, void* dq, void* dkv, int B, int Sq, int Skv, int H, int D, hipStream_t st) {
   hipError_t e = launch_attn_delta(dtype, dO, O, B, Sq, H, D / H, delta, st);
   if (e != hipSuccess) return e;
+  if (attn_uses_mfma(dtype, D / H)) {
+    const bf16_t *qb = (const bf16_t*)q, *kvb = (const bf16_t*)kv, *dOb = (const bf16_t*)dO;
+    e = launch_attn_dkv_mfma(qb, D, (uint32_t)((size_t)B * Sq * D), kvb, 2 * D, dOb, lse, delta, (bf16_t*)dkv, 2 * D, B,
+                             Sq, Skv, H, D, st);
+    if (e != hipSuccess) return e;
+    return launch_attn_dq_mfma(qb, D, kvb, 2 * D, (uint32_t)((size_t)B * Skv * 2 * D), dOb, lse, delta, (bf16_t*)dq, D,
+                               B, Sq, Skv, H, D, st);
+  }
   if (dtype == kBF16)
     return xbwd((const bf16_t*)q, (const bf16_t*)kv, (const bf16_t*)dO, lse, delta, (bf16_t*)dq, (bf16_t*)dkv, B, Sq,
                 Skv, H, D, st);

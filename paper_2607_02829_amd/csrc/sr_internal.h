@@ -123,6 +123,15 @@ hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int 
                            hipStream_t st);
 hipError_t launch_attn_colsum(int dtype, const void* qkv, const float* lse, float* colsum, int B, int S, int H, int D,
                               hipStream_t st);
+// bf16 operands as their 16-bit patterns
+hipError_t launch_attn_fwd_mfma(const uint16_t* q, int ldq, const uint16_t* kv, int ldkv, uint32_t kv_elems, uint16_t* O,
+                                float* lse, int B, int Sq, int Skv, int H, int D, hipStream_t st);
+hipError_t launch_attn_dkv_mfma(const uint16_t* q, int ldq, uint32_t q_elems, const uint16_t* kv, int ldkv,
+                                const uint16_t* dO, const float* lse, const float* delta, uint16_t* dk_out, int ldo, int B,
+                                int Sq, int Skv, int H, int D, hipStream_t st);
+hipError_t launch_attn_dq_mfma(const uint16_t* q, int ldq, const uint16_t* kv, int ldkv, uint32_t kv_elems,
+                               const uint16_t* dO, const float* lse, const float* delta, uint16_t* dq_out, int ldo, int B,
+                               int Sq, int Skv, int H, int D, hipStream_t st);
 hipError_t launch_xattn_fwd(int dtype, const void* q, const void* kv, void* O, float* lse, int B, int Sq, int Skv,
                             int H, int D, hipStream_t st);
 hipError_t launch_xattn_bwd(int dtype, const void* q, const void* kv, const void* O, const void* dO, const float* lse,
