@@ -19,3 +19,5 @@ def test_trunk_rejects_bad_arguments():
         Trunk(w, (1, 1, 1), params, K=w.L + 1)             # K beyond L
     with pytest.raises(ValueError):
         Trunk(w.with_(kind="adaln"), (1, 1, 1), params)    # pre-LN blocks only
+    with pytest.raises(ValueError):
+        Trunk(w, (1, 1, 1), params, select="gradient")     # random or attention-score selection
