@@ -19,6 +19,7 @@ CASES = {
     "f32": (inputs.small("rf_c", Hg=9, Wg=11, D=128, H=2, F=512, dtype="f32"), 2, 25, 0),
     "adaln_bf16": (inputs.small("rf_d", Hg=10, Wg=21, kind="adaln"), 2, 50, 0),
     "d025_full": (inputs.WORKLOADS["d025"], 12, 4050, 0),
+    "b5625_full": (inputs.WORKLOADS["b5625"], 8, 128, 0),           # eight samples at full width
     "all_tokens": (inputs.small("rf_e", Hg=6, Wg=11), 2, 66, 0),   # K = L
     "one_token": (inputs.small("rf_f", Hg=6, Wg=11), 2, 1, 0),     # K = 1
 }
