@@ -178,3 +178,28 @@ def test_sampled_rows_match_full():
     full, _ = blk.block_fwd(h, p, H, EPS)
     part, _ = blk.block_fwd(h, p, H, EPS, rows=rows)
     np.testing.assert_allclose(part, full[:, rows], rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("Sq,Skv", [(5, 13), (13, 5), (1, 9), (7, 1)])
+def test_attention_with_two_token_counts_matches_torch(Sq, Skv):
+    # the oracle's attention with different query and key counts (the generative block's
+    # asymmetric attention) against torch fp64 autograd of softmax(q k^T / sqrt(hd)) v
+    rng = np.random.default_rng([Sq, Skv])
+    B, H, hd = 2, 3, 8
+    q = rng.standard_normal((B, H, Sq, hd))
+    k = rng.standard_normal((B, H, Skv, hd))
+    v = rng.standard_normal((B, H, Skv, hd))
+    dO = rng.standard_normal((B, H, Sq, hd))
+    out = blk.attention_fwd(q, k, v)
+    dq, dk, dv = blk.attention_bwd(q, k, v, dO)
+    tq, tk, tv = (torch.tensor(a, requires_grad=True) for a in (q, k, v))
+    tout = torch.softmax(tq @ tk.transpose(-1, -2) / math.sqrt(hd), dim=-1) @ tv
+    tout.backward(torch.tensor(dO))
+    np.testing.assert_allclose(out, tout.detach().numpy(), rtol=1e-12, atol=1e-12)
+    for a, t in ((dq, tq), (dk, tk), (dv, tv)):
+        np.testing.assert_allclose(a, t.grad.numpy(), rtol=1e-10, atol=1e-10)
+    # brute force on one (sample, head, query)
+    s = [sum(q[1, 2, Sq - 1, d] * k[1, 2, j, d] for d in range(hd)) / math.sqrt(hd) for j in range(Skv)]
+    e = [math.exp(x - max(s)) for x in s]
+    want = [sum(e[j] * v[1, 2, j, d] for j in range(Skv)) / sum(e) for d in range(hd)]
+    np.testing.assert_allclose(out[1, 2, Sq - 1], want, rtol=1e-12, atol=1e-12)
