@@ -59,3 +59,27 @@ def test_trunk_fwd_bwd(case):
     bad = {k: v for k, v in errs.items() if not v <= tol_for(w.dtype)}
     assert not bad, bad
 
+
+
+def test_trunk_bitwise_repeatable():
+    # two forward + backward passes of the (2, 8, 2) trunk on the same inputs give identical
+    # bits: the three stages share one scratch buffer and each backward's second stream is
+    # joined before the next stage runs
+    import torch
+    w, split, K = CASES["b5625_282"]
+    params = inputs.params_to_storage(inputs.block_params(w, sum(split), randomise_affine=True), w.dtype)
+    x0 = device.to_device(inputs.to_storage(inputs.token_field(w), w.dtype))
+    g3 = device.to_device(inputs.to_storage(inputs.upstream_grad(w), w.dtype))
+    tr = Trunk(w, split, params, K=K, seed=4)
+    runs = []
+    for _ in range(2):
+        x3 = tr.forward(x0, 1).clone()
+        g0 = tr.backward(g3).clone()
+        torch.cuda.synchronize()
+        runs.append((x3, g0, [{k: v.clone() for k, v in g.items()} for g in tr.block_grads()]))
+    (a3, a0, ag), (b3, b0, bg) = runs
+    assert torch.equal(a3.view(torch.int16), b3.view(torch.int16))
+    assert torch.equal(a0.view(torch.int16), b0.view(torch.int16))
+    for x, y in zip(ag, bg):
+        for k in x:
+            assert torch.equal(x[k].view(torch.int32), y[k].view(torch.int32)), k
