@@ -142,3 +142,22 @@ def test_trunk_with_attention_selector():
     ref_g0, _ = ostack.trunk_backward(g3, idx, params, split, caches)
     assert rel_err(storage_to_f64(x3), ref_x3) <= tol_for(w.dtype)
     assert rel_err(storage_to_f64(g0), ref_g0) <= tol_for(w.dtype)
+
+
+def test_colsums_repeatable_and_shared_index_selection():
+    import torch
+    # the column sums are computed in a fixed order: two calls give identical bits
+    w, S = inputs.small("cs_rep", Hg=20, Wg=20), 400
+    h, params, _, _ = host_inputs(w, 2, randomise_affine=True, S=S)
+    a = _gpu_colsums(w, S, h, params, (1,))[0]
+    b = _gpu_colsums(w, S, h, params, (1,))[0]
+    assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+    # idx_shared = 1: one index set, drawn from the first plane set, for all samples
+    rng = np.random.default_rng(17)
+    B, parts, L, K = 3, 4, 500, 123
+    planes = rng.random((1, parts, L)).astype(np.float32)
+    cfg = abi.SrConfig(B=B, L=L, D=64, H=1, F=64, n_blocks=1, dtype=abi.SR_F32, kind=abi.SR_BLOCK_PRELN,
+                       ln_eps=1e-6, idx_shared=1)
+    idx = torch.full((1, K), -1, dtype=torch.int32, device="cuda")
+    abi.sr_select_topk_scores(cfg, K, torch.from_numpy(planes).cuda(), parts, idx)
+    assert np.array_equal(idx.cpu().numpy(), osel.select_topk_planes(planes, K))
