@@ -222,8 +222,8 @@ SR_API sr_status sr_routed_blocks_bwd(const sr_config* cfg, int32_t K, const int
  * "Integration with Generative Forecasting"): queries from Sq tokens (the routed ones),
  * keys and values from Skv tokens (the whole conditioning sequence); per sample and head
  *   O = softmax(q k^T / sqrt(hd)) v   over the Skv keys,   cost O(Sq Skv D).
- * cfg supplies B, D, H (head dim D/H in {32, 64, 128}) and the storage dtype; L and the block
- * fields are not used.
+ * Only cfg's B, D, H and dtype are read and validated (D % 64 == 0, head dim D/H in
+ * {32, 64, 128}); L, F, n_blocks, kind, ln_eps and idx_shared are ignored.
  *   q: [B,Sq,D]; kv: [B,Skv,2D] (k of head h at columns h*hd .., v at D + h*hd ..);
  *   O: [B,Sq,D] out; lse: [B,H,Sq] fp32 out, the base-2 log-sum-exp of the scaled scores.
  * bf16 with head dim 64 runs the MFMA attention kernels (the self-attention kernels, given
@@ -244,9 +244,9 @@ SR_API sr_status sr_cross_attention_bwd(const sr_config* cfg, int32_t Sq, int32_
 SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx,
                               int32_t* ok_dev, void* stream);
 
-/* Attention received per token, for the attention-score selector (top-K by
- * self-attention score from the last dense-early block: Sec. 4.4 "Random vs. learned
- * token selection", Tab. selection).  For block `block` (0-based) of the forward that
+/* Attention received per token, for the attention-score selector (keep the K tokens that the
+ * final block of the dense early stage attends to most: Sec. 4.4 "Random vs. learned token
+ * selection", Tab. selection).  For block `block` (0-based) of the forward that
  * wrote `saved` on S tokens per sample (sr_sparse_blocks_fwd, or S = L for
  * sr_dense_blocks_fwd):
  *   colsum[b,h,j] = sum over i < S of P_h[i,j],  P_h = softmax_j(q_i . k_j / sqrt(hd)),

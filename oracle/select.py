@@ -49,8 +49,8 @@ exact ties resolve to the lower index; K = L keeps all tokens; a hand-computed
 case where the butterfly order changes the fp32 result.
 
 Attention-score selection (Sec. 4.4 "Random vs. learned token selection";
-Tab. selection: top-K by self-attention score from the last dense-early block)
-------------------------------------------------------------------------------
+Tab. selection: keep the tokens the final dense-early block attends to most)
+----------------------------------------------------------------------------
 The paper names the selector but not the score.  Reading taken: the score of
 token j is the attention it receives, a_j = sum_h sum_i P_h[i, j], with P_h the
 softmax(q k^T / sqrt(hd)) of head h of that block's forward over all S tokens.

@@ -89,11 +89,17 @@ sr_status check_params(const sr_config* c, const sr_block_params* p, const void*
       SR_CHECK(q != nullptr, SR_EINVAL, "block %d: a weight or bias pointer is NULL", i);
       SR_CHECK(aligned16(q), SR_EALIGN, "block %d: a weight or bias pointer is not 16-byte aligned", i);
     }
+    // the row kernels read gamma / beta and the modulation weights with 8- and 16-byte loads
     if (c->kind == SR_BLOCK_PRELN) {
       const void* ln[] = {w.ln1_w, w.ln1_b, w.ln2_w, w.ln2_b};
-      for (const void* q : ln) SR_CHECK(q != nullptr, SR_EINVAL, "block %d: a LayerNorm parameter is NULL", i);
+      for (const void* q : ln) {
+        SR_CHECK(q != nullptr, SR_EINVAL, "block %d: a LayerNorm parameter is NULL", i);
+        SR_CHECK(aligned16(q), SR_EALIGN, "block %d: a LayerNorm parameter is not 16-byte aligned", i);
+      }
     } else {
       SR_CHECK(w.w_ada && w.b_ada, SR_EINVAL, "block %d: adaLN needs w_ada and b_ada", i);
+      SR_CHECK(aligned16(w.w_ada) && aligned16(w.b_ada), SR_EALIGN,
+               "block %d: w_ada or b_ada is not 16-byte aligned", i);
     }
   }
   if (c->kind == SR_BLOCK_ADALN) SR_PTR(cond, "cond");
@@ -330,9 +336,17 @@ sr_status sr_select_topk_scores(const sr_config* cfg, int32_t K, const float* pl
 }
 
 namespace {
-sr_status check_xattn(const sr_config* cfg, int32_t Sq, int32_t Skv) {
-  sr_status s = check_cfg(cfg, true);
-  if (s != SR_OK) return s;
+// The asymmetric attention reads only B, D, H and the storage type of cfg.
+sr_status check_xattn(const sr_config* c, int32_t Sq, int32_t Skv) {
+  SR_CHECK(c != nullptr, SR_EINVAL, "cfg is NULL");
+  SR_CHECK(c->dtype == SR_F32 || c->dtype == SR_BF16, SR_EDTYPE, "unknown dtype %d", c->dtype);
+  SR_CHECK(c->B >= 1 && c->D >= 1 && c->H >= 1, SR_EINVAL, "sizes must be positive (B=%d D=%d H=%d)", c->B, c->D,
+           c->H);
+  SR_CHECK(c->D % c->H == 0, SR_ESHAPE, "D=%d is not a multiple of H=%d", c->D, c->H);
+  SR_CHECK(c->D % 64 == 0, SR_EUNSUPPORTED, "D=%d must be a multiple of 64", c->D);
+  const int hd = c->D / c->H;
+  SR_CHECK(hd == 32 || hd == 64 || hd == 128, SR_EUNSUPPORTED, "head dim %d not in {32, 64, 128}", hd);
+  const sr_config* cfg = c;
   SR_CHECK(Sq >= 1 && Skv >= 1, SR_ESHAPE, "Sq=%d and Skv=%d must be >= 1", Sq, Skv);
   const size_t e = elt_of(cfg->dtype);
   SR_CHECK((size_t)cfg->B * Skv * 2 * cfg->D * e < (1ull << 31) && (size_t)cfg->B * Sq * cfg->D * e < (1ull << 31),

@@ -140,3 +140,39 @@ def test_cross_attention_rejects_bad_arguments_before_launch():
                                       None) == abi.SR_ESHAPE
     assert lib.sr_cross_attention_bwd(ctypes.byref(cfg), 10, 10, fake, fake, fake, fake, fake, fake, fake, None,
                                       None) == abi.SR_EINVAL
+
+
+def test_layernorm_and_modulation_pointers_alignment_checked():
+    # the row kernels read gamma / beta and W_ada / b_ada with vector loads: a misaligned
+    # pointer is rejected before any launch
+    _lib_or_skip()
+    import ctypes
+    fake = 1 << 40
+    lib = abi.lib()
+    for kind, field in ((abi.SR_BLOCK_PRELN, "ln1_w"), (abi.SR_BLOCK_PRELN, "ln2_b"),
+                        (abi.SR_BLOCK_ADALN, "w_ada"), (abi.SR_BLOCK_ADALN, "b_ada")):
+        cfg = _cfg(kind=kind)
+        params = (abi.SrBlockParams * 2)()
+        for i in range(2):
+            for n in abi.PARAM_FIELDS:
+                setattr(params[i], n, fake)
+        setattr(params[1], field, fake + 2)
+        st = lib.sr_sparse_blocks_fwd(ctypes.byref(cfg), 25, params, fake, fake, fake + 4096, fake, 1 << 40, None,
+                                      0, None)
+        assert st == abi.SR_EALIGN, (kind, field)
+        assert field.split("_")[0] in abi.sr_last_error() or "aligned" in abi.sr_last_error()
+
+
+def test_cross_attention_ignores_block_fields():
+    # only B, D, H and dtype of cfg are read: block fields that would be invalid for the block
+    # calls do not make the asymmetric attention fail
+    _lib_or_skip()
+    import ctypes
+    fake = 1 << 40
+    lib = abi.lib()
+    cfg = _cfg(L=0, F=0, n_blocks=-1, kind=9, ln_eps=0.0, idx_shared=5)
+    # the first failure is the one of the call's own arguments (Sq = 0), not of the ignored fields
+    assert lib.sr_cross_attention_fwd(ctypes.byref(cfg), 0, 10, fake, fake, fake, fake, None) == abi.SR_ESHAPE
+    assert lib.sr_cross_attention_fwd(ctypes.byref(cfg), 10, 10, None, fake, fake, fake, None) == abi.SR_EINVAL
+    assert lib.sr_cross_attention_fwd(ctypes.byref(_cfg(D=96, H=3)), 10, 10, fake, fake, fake, fake,
+                                      None) == abi.SR_EUNSUPPORTED
