@@ -146,6 +146,20 @@ SR_API sr_status sr_select_indices(const sr_config* cfg, int32_t K, int32_t sele
                             const void* x_prev, int32_t* idx, void* scratch,
                             size_t scratch_bytes, void* stream);
 
+/* sr_select_indices without a scratch argument and without allocating, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results and errors as sr_select_indices; the
+ * SR_SEL_TOPK_DIFFNORM scores go to a device array that the library holds on each GPU it runs
+ * on until the process ends (SR_SELECT_NOALLOC_MAX_TOKENS fp32 values, 4 MiB per GPU), looked
+ * up once per GPU on the first call there.  B*L (L with idx_shared) above that limit returns
+ * SR_EUNSUPPORTED before anything is enqueued.  Every call on one GPU shares its array: calls
+ * that overlap on one GPU (different streams, threads) race and must be ordered by the caller.
+ * SR_SEL_RANDOM uses no scratch and runs as in sr_select_indices. */
+#define SR_SELECT_NOALLOC_MAX_TOKENS (1 << 20)
+SR_API sr_status sr_select_indices_noalloc(const sr_config* cfg, int32_t K, int32_t select_kind,
+                                    uint64_t seed, uint64_t step, const void* x_t,
+                                    const void* x_prev, int32_t* idx, void* stream);
+
 /* Gather (Sec. 3.2, h0 = Gather(x, I)): h0[b,k,:] = x[b, idx[b,k], :], a bit copy.
  *   x: [B,L,D] storage dtype; idx: [B,K] (or [1,K]); h0: [B,K,D] out.
  *   idx entries must lie in [0,L) (sr_select_indices guarantees it). */

@@ -22,7 +22,7 @@ PARAM_FIELDS = ("ln1_w", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o", "ln2_w", "ln2_
                 "w_fc1", "b_fc1", "w_fc2", "b_fc2", "w_ada", "b_ada")
 
 EXPORTS = ("sr_last_error", "sr_version", "sr_workspace_bytes", "sr_select_scratch_bytes",
-           "sr_select_indices", "sr_gather", "sr_scatter_delta", "sr_sparse_blocks_fwd",
+           "sr_select_indices", "sr_select_indices_noalloc", "sr_gather", "sr_scatter_delta", "sr_sparse_blocks_fwd",
            "sr_sparse_blocks_bwd", "sr_dense_blocks_fwd", "sr_dense_blocks_bwd", "sr_validate_indices",
            "sr_attention_colsums", "sr_select_topk_scores", "sr_routed_blocks_fwd", "sr_routed_blocks_bwd",
            "sr_cross_attention_fwd", "sr_cross_attention_bwd",
@@ -73,6 +73,7 @@ def lib(path: str = LIB_PATH):
         "sr_workspace_bytes": ([CP, I32, ctypes.POINTER(SZ), ctypes.POINTER(SZ)], I32),
         "sr_select_scratch_bytes": ([CP, I32, ctypes.POINTER(SZ)], I32),
         "sr_select_indices": ([CP, I32, I32, U64, U64, P, P, P, P, SZ, P], I32),
+        "sr_select_indices_noalloc": ([CP, I32, I32, U64, U64, P, P, P, P], I32),
         "sr_gather": ([CP, I32, P, P, P, P], I32),
         "sr_scatter_delta": ([CP, I32, P, P, P, P, P], I32),
         "sr_sparse_blocks_fwd": ([CP, I32, P, P, P, P, P, SZ, P, SZ, P], I32),
@@ -152,6 +153,14 @@ def sr_select_scratch_bytes(cfg: SrConfig, select_kind: int) -> int:
 def sr_select_indices(cfg, K, select_kind, seed, step, x_t, x_prev, idx, scratch=None, stream=None):
     _check(lib().sr_select_indices(ctypes.byref(cfg), K, select_kind, seed, step, _p(x_t), _p(x_prev),
                                    _p(idx), _p(scratch), _nbytes(scratch), _stream(stream)))
+
+
+def sr_select_indices_noalloc(cfg, K, select_kind, seed, step, x_t, x_prev, idx, stream=None):
+    _check(lib().sr_select_indices_noalloc(ctypes.byref(cfg), K, select_kind, seed, step, _p(x_t), _p(x_prev),
+                                           _p(idx), _stream(stream)))
+
+
+SR_SELECT_NOALLOC_MAX_TOKENS = 1 << 20
 
 
 def sr_gather(cfg, K, x, idx, h0, stream=None):

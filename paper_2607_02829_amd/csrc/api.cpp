@@ -10,6 +10,9 @@
 #include "profile.h"
 #include "stack.h"
 
+static_assert(SR_SELECT_NOALLOC_MAX_TOKENS == sr::kSelStaticScores,
+              "the header's limit is the size of the library's score array");
+
 namespace {
 
 thread_local std::string g_err;
@@ -170,6 +173,33 @@ sr_status sr_select_indices(const sr_config* cfg, int32_t K, int32_t select_kind
   const int dt = cfg->dtype == SR_BF16 ? sr::kBF16 : sr::kF32;
   sr::ProfScope ps("select_topk", 0, (double)rows * cfg->L * cfg->D * 2 * elt_of(cfg->dtype), st);
   return hip_status(sr::launch_select_topk(dt, rows, cfg->L, cfg->D, K, x_t, x_prev, (float*)scratch, idx, st),
+                    "select_topk");
+}
+
+sr_status sr_select_indices_noalloc(const sr_config* cfg, int32_t K, int32_t select_kind, uint64_t seed,
+                                    uint64_t step, const void* x_t, const void* x_prev, int32_t* idx,
+                                    void* stream) {
+  sr_status s = check_cfg(cfg, true);
+  if (s != SR_OK) return s;
+  SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
+  SR_PTR(idx, "idx");
+  const int rows = cfg->idx_shared ? 1 : cfg->B;
+  hipStream_t st = (hipStream_t)stream;
+  if (select_kind == SR_SEL_RANDOM) {   // needs no scratch: the same launch as sr_select_indices
+    sr::ProfScope ps("select_random", 0, (double)rows * K * 4, st);
+    return hip_status(sr::launch_select_random(rows, cfg->L, K, seed, step, idx, st), "select_random");
+  }
+  SR_CHECK(select_kind == SR_SEL_TOPK_DIFFNORM, SR_EINVAL, "unknown selector %d", select_kind);
+  SR_PTR(x_t, "x_t");
+  SR_PTR(x_prev, "x_prev");
+  SR_CHECK((size_t)rows * cfg->L <= (size_t)SR_SELECT_NOALLOC_MAX_TOKENS, SR_EUNSUPPORTED,
+           "top-k selection without allocation scores at most %d tokens per call (B*L = %zu)",
+           SR_SELECT_NOALLOC_MAX_TOKENS, (size_t)rows * cfg->L);
+  float* score = nullptr;
+  if ((s = hip_status(sr::select_static_scratch(&score), "select_static_scratch")) != SR_OK) return s;
+  const int dt = cfg->dtype == SR_BF16 ? sr::kBF16 : sr::kF32;
+  sr::ProfScope ps("select_topk", 0, (double)rows * cfg->L * cfg->D * 2 * elt_of(cfg->dtype), st);
+  return hip_status(sr::launch_select_topk(dt, rows, cfg->L, cfg->D, K, x_t, x_prev, score, idx, st),
                     "select_topk");
 }
 

@@ -14,6 +14,8 @@
 // Top-k: a wave per token evaluates the fp32 score in the fixed order of the
 // header (16-byte chunks round-robin over 64 lanes, xor butterfly), then one
 // workgroup per sample radix-selects the K largest (ties to the lower index).
+#include <mutex>
+
 #include "common.h"
 #include "sr_internal.h"
 
@@ -244,6 +246,32 @@ hipError_t launch_select_random(int rows, int L, int K, uint64_t seed, uint64_t 
                                 hipStream_t st) {
   hipLaunchKernelGGL(select_random_kernel, dim3(rows), dim3(kSelThreads), 0, st, L, K, seed, step, idx);
   return hipGetLastError();
+}
+
+// Score scratch of the allocation-free top-k selection (sr_select_indices_noalloc): one array
+// per GPU, held until the process ends, shared by every call on that GPU (calls that overlap on
+// one GPU race).  In host code the array's name stands for a host-side shadow, not the device
+// memory: kernels receive the device address that select_static_scratch() looked up.
+static __device__ __align__(256) float scratch[kSelStaticScores];
+
+hipError_t select_static_scratch(float** out) {
+  constexpr int kMaxDev = 64;
+  static std::mutex mu;
+  static float* dev_ptr[kMaxDev] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDev) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!dev_ptr[dev]) {   // once per device, with that device current
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    dev_ptr[dev] = static_cast<float*>(p);
+  }
+  *out = dev_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_select_topk(int dtype, int rows, int L, int D, int K, const void* xt, const void* xp,

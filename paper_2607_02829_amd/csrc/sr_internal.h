@@ -73,6 +73,10 @@ struct GemmDesc {
 hipError_t launch_select_random(int rows, int L, int K, uint64_t seed, uint64_t step, int32_t* idx, hipStream_t st);
 hipError_t launch_select_topk(int dtype, int rows, int L, int D, int K, const void* xt, const void* xp, float* score,
                               int32_t* idx, hipStream_t st);
+// Allocation-free top-k selection: fp32 scores of at most kSelStaticScores tokens (rows * L) in a
+// file-scope device array of select.hip; *out receives its address on the current device.
+constexpr int kSelStaticScores = 1 << 20;
+hipError_t select_static_scratch(float** out);
 hipError_t launch_select_topk_planes(int rows, int L, int K, int parts, const float* planes, int32_t* idx,
                                      hipStream_t st);
 hipError_t launch_validate(const int32_t* idx, int rows, int K, int L, int32_t* ok, hipStream_t st);
