@@ -1,11 +1,12 @@
 """GPU parity at the workloads' full sizes, in the launch configuration bench.py times:
 the complete 0.25 deg routed stack (12 blocks, K = 4050) forward and backward against the
 fp64 oracle, one block at the 1.40625 deg and diffusion (adaLN) shapes, the dense
-S = 16200 block on sampled query rows, and a whole routed step at the 0.25 deg shape."""
+S = 16200 block forward on sampled query rows and forward + backward in full (the keep = 100 %
+mode that the speedup is measured against), and a whole routed step at the 0.25 deg shape."""
 import numpy as np
 import pytest
 
-from gpu_helpers import compare, gpu_blocks, host_inputs, oracle_blocks, rel_err, tol_for
+from gpu_helpers import check_pairs, compare, gpu_blocks, host_inputs, oracle_blocks, pairs, rel_err, tol_for
 from oracle import block as oblk
 from oracle import routing as orouting
 from oracle import select as osel
@@ -86,3 +87,16 @@ def test_d025_routed_step():  # noqa: C901
     # the scatter applied to the GPU's own h is bit-exact against the oracle's scatter of it
     want_x = orouting.scatter_delta(x, device.to_host(h), orouting.gather(x, want_idx), want_idx)
     assert np.array_equal(got_x, want_x)
+
+
+@pytest.mark.timeout(900)
+def test_d025_dense_block_fwd_bwd():
+    # keep = 100 % (Sec. 3.4, r = 1): one block forward and backward on all L = 16200 tokens, every
+    # output and gradient against the fp64 oracle (its attention loops over heads: ~8 GB per head)
+    w = inputs.WORKLOADS["d025"]
+    h, params, cond, dh = host_inputs(w, 1, randomise_affine=True, S=w.L)
+    print(f"[d025 dense] S={w.L}: GPU", flush=True)
+    gpu = gpu_blocks(w, w.L, h, params, cond, dh, dense=True)
+    print("[d025 dense] oracle (fp64, a few minutes)", flush=True)
+    ref = oracle_blocks(w, h, params, cond, dh)
+    check_pairs(pairs(gpu, ref, w.kind), w.dtype, "[d025 dense]")

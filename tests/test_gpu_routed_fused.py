@@ -1,11 +1,12 @@
 """GPU tests of the fused routed step (Alg. 1 stage 2 in one call per direction):
 sr_routed_blocks_fwd / sr_routed_blocks_bwd against sr_gather + sr_sparse_blocks_fwd/bwd +
 sr_scatter_delta on the same inputs, bit for bit (x', the input gradient, every weight
-gradient, dcond), and the fused forward against the oracle's routed step."""
+gradient, dcond), and the fused forward and backward against the oracle's routed step and its
+vector-Jacobian product (the backward of Eq. scatter: dx0 = g + Scatter(J^T g[I] - g[I], I))."""
 import numpy as np
 import pytest
 
-from gpu_helpers import rel_err, tol_for
+from gpu_helpers import check_pairs, rel_err, tol_for
 from oracle import select as osel
 from oracle import stack as ostack
 from oracle.numerics import storage_to_f64
@@ -92,3 +93,32 @@ def test_fused_forward_against_oracle():
         mask = np.ones(w.L, bool); mask[idx[b]] = False
         assert np.array_equal(f["x"][b, mask], x[b, mask])     # unselected rows untouched
     assert rel_err(storage_to_f64(f["x"]), storage_to_f64(want)) <= tol_for(w.dtype)
+
+
+@pytest.mark.parametrize("case", ["bf16", "adaln_bf16", "b5625_full"])
+def test_fused_backward_against_oracle(case):
+    w, nb, K, shared = CASES[case]
+    print(f"[routed fused bwd vs oracle {case}] B={w.B} L={w.L} K={K} blocks={nb} {w.kind}", flush=True)
+    f, (x, params, cond) = _run(w, nb, K, shared, fused=True)
+    idx = osel.select_random(w.B, w.L, K, 5, 3)
+    assert np.array_equal(f["idx"], idx)
+    g = inputs.to_storage(inputs.upstream_grad(w), w.dtype)
+    print(f"[routed fused bwd vs oracle {case}] oracle", flush=True)
+    x_ref, _, _, _, caches = ostack.routed_forward(x, idx, params, w.H, 1e-6, w.kind, cond)
+    dx0, _, grads, dcond = ostack.routed_backward(g, idx, params, caches)
+    # rows never routed: dx0 = g bit for bit (the identity path of Eq. scatter)
+    for b in range(w.B):
+        mask = np.ones(w.L, bool); mask[idx[b]] = False
+        assert np.array_equal(f["g"][b, mask], g[b, mask])
+    items = [("x'", storage_to_f64(f["x"]), storage_to_f64(x_ref)),
+             ("dx0", storage_to_f64(f["g"]), storage_to_f64(dx0))]
+    for i, (gg, rg) in enumerate(zip(f["grads"], grads)):
+        for name, v in gg.items():
+            unused = (w.kind == "preln" and name in ("w_ada", "b_ada")) or (w.kind == "adaln" and name.startswith("ln"))
+            if unused:
+                assert not np.any(v), f"block {i} {name}: unused parameter gradient is not zero"
+                continue
+            items.append((f"b{i}.{name}", v, rg[name]))
+    if dcond is not None:
+        items.append(("dcond", f["dcond"], dcond))
+    check_pairs(items, w.dtype, f"[routed fused bwd vs oracle {case}]")
