@@ -35,8 +35,8 @@
  *    F MLP width, n_blocks middle blocks; S = K (routed) or L (dense) tokens per
  *    sample inside the stack.
  *  - Support: D % 64 == 0, F % 64 == 0, D <= 2048, head dim D/H in {32, 64, 128}
- *    (bf16 with head dim 64 runs the MFMA attention kernels, every other case a
- *    generic fp32-accumulating kernel); 1 <= K <= L; B*L*D*elt < 2^31 bytes per
+ *    (bf16 with head dim 64 or 128 runs the MFMA attention kernels, fp32 storage and
+ *    head dim 32 a generic fp32-accumulating kernel); 1 <= K <= L; B*L*D*elt < 2^31 bytes per
  *    token tensor, and for the block-stack calls also B*L*max(F, 3D)*4 < 2^31
  *    (internal fp32 buffers).  Anything else returns SR_EUNSUPPORTED.
  */
@@ -240,8 +240,8 @@ SR_API sr_status sr_routed_blocks_bwd(const sr_config* cfg, int32_t K, const int
  * {32, 64, 128}); L, F, n_blocks, kind, ln_eps and idx_shared are ignored.
  *   q: [B,Sq,D]; kv: [B,Skv,2D] (k of head h at columns h*hd .., v at D + h*hd ..);
  *   O: [B,Sq,D] out; lse: [B,H,Sq] fp32 out, the base-2 log-sum-exp of the scaled scores.
- * bf16 with head dim 64 runs the MFMA attention kernels (the self-attention kernels, given
- * the two buffers and token counts); other cases generic kernels.  Deterministic. */
+ * bf16 with head dim 64 or 128 runs the MFMA attention kernels (the self-attention kernels,
+ * given the two buffers and token counts); other cases generic kernels.  Deterministic. */
 SR_API sr_status sr_cross_attention_fwd(const sr_config* cfg, int32_t Sq, int32_t Skv, const void* q,
                                  const void* kv, void* O, float* lse, void* stream);
 

@@ -5,8 +5,8 @@
 // 2D + h*hd); O and dO are [B*S, D]; dqkv mirrors qkv.  lse[b,h,s] is the base-2
 // log-sum-exp of the scaled scores, so P = exp2(s * log2(e)/sqrt(hd) - lse).
 //
-// MFMA kernels (hd = 64, bf16, v_mfma_f32_32x32x16_bf16).  A workgroup of NW waves
-// owns 32 NW rows (32 per wave) of the resident dimension and streams the other one in
+// MFMA kernels (head dim 64 or 128, bf16, v_mfma_f32_32x32x16_bf16).  A workgroup of NW
+// waves owns 32 NW rows (32 per wave) of the resident dimension and streams the other one in
 // 64-row tiles of one head:
 //  * forward: a wave owns 32 queries and forms S^T = K Q^T per 32-key unit, so each
 //    lane holds one query's scores and the online-softmax state is per lane; the row
@@ -27,8 +27,8 @@
 // dO^T, K^T) are read with ds_read_b64_tr_b16, which hands each lane four consecutive rows
 // of one column, so no transposed copy is ever written.
 //
-// Generic kernels (any storage type, hd in {32, 64, 128}): one thread per row,
-// online softmax over keys, fp32 throughout.
+// Generic kernels (fp32 storage, or bf16 at head dim 32): one thread per row, online softmax
+// over keys, fp32 throughout.
 #include <type_traits>
 
 #include "common.h"
@@ -37,17 +37,29 @@
 
 namespace sr {
 
-constexpr int HD = 64;
-constexpr int AP = HD + 8;   // padded row (bf16) of the output staging tile
 constexpr int KT = 64;       // tile of the streamed dimension
-constexpr int TE = KT * HD;  // bf16 elements of one 64 x 64 tile (8 KB)
 constexpr int NSTG = 3;      // LDS stages
-// Waves per workgroup of the MFMA kernels: eight (256 rows) share each streamed tile in LDS, at
-// one workgroup per CU and two waves per SIMD; against four, measured 2-4 % faster per kernel
-// at 4050 tokens (forward 94 -> 90, dK/dV 159 -> 155, dQ 112 -> 108 us).
-constexpr int kDkvWaves = 8;
-constexpr int kFwdWaves = 8;
-constexpr int kDqWaves = 8;
+// Waves per workgroup of the MFMA kernels at head dim 64: eight (256 rows) share each streamed
+// tile in LDS, at one workgroup per CU and two waves per SIMD; against four, measured 2-4 %
+// faster per kernel at 4050 tokens (forward 94 -> 90, dK/dV 159 -> 155, dQ 112 -> 108 us).  At
+// head dim 128 the accumulators of a 32-row unit take twice the registers, so four waves (128
+// rows) per workgroup, one per SIMD with the whole register file.
+template <int HD>
+constexpr int attn_waves() { return HD == 64 ? 8 : 4; }
+
+// Geometry of a 64-row tile of one head (head dim HD, bf16).
+template <int HD>
+struct Geo {
+  static_assert(HD == 64 || HD == 128, "MFMA attention head dims");
+  static constexpr int AP = HD + 8;     // padded row (bf16) of the output staging tile
+  static constexpr int TE = KT * HD;    // bf16 elements of one 64-row tile
+  static constexpr int TB = TE * 2;     // bytes of one tile
+  static constexpr int SGB = 2 * TB;    // bytes of one stage (two tiles)
+  static constexpr int KS = HD / 16;    // MFMA k-steps over the head dimension
+  static constexpr int DB = HD / 32;    // 32-column blocks of the head dimension
+  static constexpr int CPR = HD / 8;    // 16-byte chunks per row
+  static constexpr int BLK = HD / 8;    // 1 KB blocks of a tile
+};
 
 
 SR_DEV bf16x8 zero8() {
@@ -70,32 +82,45 @@ SR_DEV void zero16(f32x16& a) {
   for (int r = 0; r < 16; ++r) a[r] = 0.f;
 }
 
-// LDS tile: 64 rows of 64 bf16 (eight 16-byte chunks); chunk c of row r sits at chunk
-// position c ^ swz(r).  Among any 16 consecutive rows the even ones use eight different
-// positions and so do the odd ones (conflict-free 16-byte fragment reads); rows r and r+2
-// of each group of four differ in bit 2 of the position, so the four rows x 64 bytes that
-// half a wave's transposed read touches fall in different banks (measured conflict-free
-// for both read kinds, where plain XOR swizzles within 64-byte groups cost one extra pass
-// per transposed read); rows 16 apart share a swizzle, so fragment addresses of different
-// 16-row groups differ by constants (instruction offsets rather than address registers).
-SR_DEV int swz(int row) { return (((row >> 1) & 1) << 2) | ((row >> 2) & 3); }
-SR_DEV int toff(int row, int chunk) { return row * HD + ((chunk ^ swz(row)) << 3); }
+// LDS tile: 64 rows of HD bf16 (HD / 8 16-byte chunks each); chunk c of row r sits at chunk
+// position c ^ swz(r).  The LDS serves 256 bytes (64 banks) per pass.
+//  * HD = 64 (128-byte rows): among any 16 consecutive rows the even ones use eight different
+//    positions and so do the odd ones (conflict-free 16-byte fragment reads); rows r and r+2 of
+//    each group of four differ in bit 2 of the position, so the four rows x 64 bytes that half
+//    a wave's transposed read touches fall in different banks (measured conflict-free for both
+//    read kinds, where plain XOR swizzles within 64-byte groups cost one extra pass per
+//    transposed read).
+//  * HD = 128 (256-byte rows, each one whole pass of the banks): 16 consecutive rows take 16
+//    different positions (16-byte fragment reads of 16 lanes cover every bank once), and bits
+//    2-3 of the position follow the row mod 4, so the four rows x 64 bytes of a half-wave's
+//    transposed read land in four different 64-byte quarters.
+// Rows 16 apart share a swizzle, so fragment addresses of different 16-row groups differ by
+// constants (instruction offsets rather than address registers).
+template <int HD>
+SR_DEV int swz(int row) {
+  if constexpr (HD == 64) return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
+  else return ((row & 3) << 2) | ((row >> 2) & 3);
+}
+template <int HD>
+SR_DEV int toff(int row, int chunk) { return row * HD + ((chunk ^ swz<HD>(row)) << 3); }
 
 // Rows r0..r0+63 of one head (columns base.. of a row-major tensor with row length ld)
-// into the LDS tile dst: eight 1 KB blocks of eight rows, two per wave; lane l lands at
+// into the LDS tile dst: HD / 8 blocks of 1 KB (64 / (HD / 8) rows each); lane l lands at
 // byte 16 l of its block, so it fetches the chunk that the swizzle places there.  Rows past
 // the sample's S tokens are read without a guard: they belong to the next sample (finite
 // values the callers mask) or lie past the tensor, where the buffer load returns zero.
-// NW waves share the eight blocks (8 / NW each).
-template <int NW = 4>
+// NW waves share the blocks.
+template <int HD, int NW>
 SR_DEV void tile_load(__amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t ld, int r0, bf16_t* dst, bool valid = true) {
+  using G = Geo<HD>;
+  static_assert(G::BLK % NW == 0, "tile blocks per wave");
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  constexpr int PER = 8 / NW;
+  constexpr int PER = G::BLK / NW, RPB = 64 / G::CPR;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int blk = wid * PER + i;
-    const int row = blk * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ swz(row);
+    const int row = blk * RPB + lane / G::CPR;
+    const int c = (lane % G::CPR) ^ swz<HD>(row);
     uint32_t off = base + ((uint32_t)(r0 + row) * ld + (uint32_t)c * 8u) * 2u;
     // a load past the last tile keeps the number of loads in flight uniform: it reads beyond
     // every tensor's extent (2 GiB at most), which returns zeros without a memory access
@@ -104,10 +129,11 @@ SR_DEV void tile_load(__amdgpu_buffer_rsrc_t rs, uint32_t base, uint32_t ld, int
   }
 }
 
-// Fragment of the 32 rows r0.. (MFMA row index = lane % 32), k-step ks of the 64 columns.
+// Fragment of the 32 rows r0.. (MFMA row index = lane % 32), k-step ks of the HD columns.
+template <int HD>
 SR_DEV bf16x8 row_frag(const bf16_t* tile, int r0, int ks) {
   const int lane = threadIdx.x & 63;
-  return ld8(tile + toff(r0 + (lane & 31), 2 * ks + (lane >> 5)));
+  return ld8(tile + toff<HD>(r0 + (lane & 31), 2 * ks + (lane >> 5)));
 }
 
 // Transposed fragment: MFMA row index = tile column c0 + lane % 32, k = tile rows, in the
@@ -115,13 +141,14 @@ SR_DEV bf16x8 row_frag(const bf16_t* tile, int r0, int ks) {
 // 4..7 rows k0 + 8 + 4h .. (h = lane / 32).  ds_read_b64_tr_b16 gives lane i of each
 // 16-lane group column i of the four rows addressed by the group (lane s: row s / 4,
 // columns 4 (s % 4) .. + 3).
+template <int HD>
 SR_DEV bf16x8 tr_frag(const bf16_t* tile, int k0, int c0) {
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4, s = lane & 15;
   const int col = c0 + 16 * (g & 1) + 4 * (s & 3);
   const int r1 = k0 + 4 * (g >> 1) + (s >> 2), r2 = r1 + 8;
-  const v4s lo = ds_tr(tile + r1 * HD + (((col >> 3) ^ swz(r1)) << 3) + (col & 7));
-  const v4s hi = ds_tr(tile + r2 * HD + (((col >> 3) ^ swz(r2)) << 3) + (col & 7));
+  const v4s lo = ds_tr(tile + r1 * HD + (((col >> 3) ^ swz<HD>(r1)) << 3) + (col & 7));
+  const v4s hi = ds_tr(tile + r2 * HD + (((col >> 3) ^ swz<HD>(r2)) << 3) + (col & 7));
   i32x4 w;
   w[0] = __builtin_bit_cast(i32x2, lo)[0];
   w[1] = __builtin_bit_cast(i32x2, lo)[1];
@@ -131,21 +158,21 @@ SR_DEV bf16x8 tr_frag(const bf16_t* tile, int k0, int c0) {
 }
 
 // Explicit fragment reads (see lds_read16) from one LDS array of NSTG stages, each holding two
-// 64 x 64 tiles (tile p of stage s at byte offset (2 s + p) TB): per-lane base addresses are
+// 64 x HD tiles (tile p of stage s at byte offset (2 s + p) TB): per-lane base addresses are
 // fixed, and the stage, tile, row-group and k-step offsets are instruction immediates.  The
 // compiler then neither waits for fills in flight into other stages nor keeps per-stage
 // address registers; the kernels wait (lgkm_wait) before using what they read.
-constexpr int TB = TE * 2;    // bytes of one tile
-constexpr int SGB = 2 * TB;   // bytes of one stage
 
 // Row fragment: MFMA row index = tile row R0 + lane % 32 (R0 a multiple of 16, which keeps
-// the swizzle), k-step KSV of the 64 columns.
+// the swizzle), k-step KSV of the HD columns.
+template <int HD>
 struct RowAddr {
-  uint32_t a[4];
+  uint32_t a[HD / 16];
   SR_DEV void init(uint32_t base, int lane) {
     const int l32 = lane & 31, h = lane >> 5;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) a[ks] = base + (uint32_t)(l32 * HD + (((2 * ks + h) ^ swz(l32)) << 3)) * 2u;
+    for (int ks = 0; ks < HD / 16; ++ks)
+      a[ks] = base + (uint32_t)(l32 * HD + (((2 * ks + h) ^ swz<HD>(l32)) << 3)) * 2u;
   }
   template <int OFF, int R0, int KSV>
   SR_DEV void read(RawFrag<true>& f) const {
@@ -153,50 +180,54 @@ struct RowAddr {
   }
 };
 
-// Transposed fragment (as tr_frag): MFMA row index = tile column 32 DB + lane % 32, k = tile
+// Transposed fragment (as tr_frag): MFMA row index = tile column 32 DBV + lane % 32, k = tile
 // rows K0 + 4 h .. + 3 (first read) and K0 + 8 + 4 h .. + 3 (second read), K0 a multiple of 16.
+template <int HD>
 struct TrAddr {
-  uint32_t a[2][2];
+  uint32_t a[HD / 32][2];
   SR_DEV void init(uint32_t base, int lane) {
     const int g = lane >> 4, s = lane & 15;
 #pragma unroll
-    for (int db = 0; db < 2; ++db) {
+    for (int db = 0; db < HD / 32; ++db) {
       const int col = 32 * db + 16 * (g & 1) + 4 * (s & 3);
       const int r1 = 4 * (g >> 1) + (s >> 2), r2 = r1 + 8;
-      a[db][0] = base + (uint32_t)(r1 * HD + (((col >> 3) ^ swz(r1)) << 3) + (col & 7)) * 2u;
-      a[db][1] = base + (uint32_t)(r2 * HD + (((col >> 3) ^ swz(r2)) << 3) + (col & 7)) * 2u;
+      a[db][0] = base + (uint32_t)(r1 * HD + (((col >> 3) ^ swz<HD>(r1)) << 3) + (col & 7)) * 2u;
+      a[db][1] = base + (uint32_t)(r2 * HD + (((col >> 3) ^ swz<HD>(r2)) << 3) + (col & 7)) * 2u;
     }
   }
-  template <int OFF, int K0, int DB>
+  template <int OFF, int K0, int DBV>
   SR_DEV void read(RawFrag<false>& f) const {
-    f.lo = rdtr<OFF + K0 * HD * 2>(a[DB][0]);
-    f.hi = rdtr<OFF + K0 * HD * 2>(a[DB][1]);
+    f.lo = rdtr<OFF + K0 * HD * 2>(a[DBV][0]);
+    f.hi = rdtr<OFF + K0 * HD * 2>(a[DBV][1]);
   }
 };
 
 // Row index (within a 32-row unit) of score register r of this lane.
 SR_DEV int srow(int r, int h32) { return 8 * (r >> 2) + 4 * h32 + (r & 3); }
 
-// Write a wave's 32 x 64 result (held transposed: acc[db][r] = X[d][row]) to LDS
+// Write a wave's 32 x HD result (held transposed: acc[db][r] = X[d][row]) to LDS
 // stage[row_local][d], scaled.
-SR_DEV void stage_t(bf16_t* stage, const f32x16 acc[2], float mul, int wid, int lane) {
+template <int HD>
+SR_DEV void stage_t(bf16_t* stage, const f32x16 acc[HD / 32], float mul, int wid, int lane) {
   const int l32 = lane & 31, h32 = lane >> 5;
 #pragma unroll
-  for (int db = 0; db < 2; ++db)
+  for (int db = 0; db < HD / 32; ++db)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) stage[(wid * 32 + l32) * AP + db * 32 + srow(r, h32)] = f2bf(acc[db][r] * mul);
+    for (int r = 0; r < 16; ++r)
+      stage[(wid * 32 + l32) * Geo<HD>::AP + db * 32 + srow(r, h32)] = f2bf(acc[db][r] * mul);
 }
 
-// Copy the (32 NW) x 64 staged tile to rows r0.. of dst (column block of one head); NW waves.
-template <int NW = 4>
+// Copy the (32 NW) x HD staged tile to rows r0.. of dst (column block of one head); NW waves.
+template <int HD, int NW>
 SR_DEV void unstage(const bf16_t* stage, bf16_t* dst, size_t ld, int r0, int S) {
+  constexpr int CPR = Geo<HD>::CPR;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < CPR / 2; ++i) {
     const int c = threadIdx.x + 64 * NW * i;
-    const int row = c >> 3, kc = c & 7;
+    const int row = c / CPR, kc = c % CPR;
     if (r0 + row < S)
       *reinterpret_cast<i32x4*>(dst + (size_t)(r0 + row) * ld + kc * 8) =
-          *reinterpret_cast<const i32x4*>(stage + row * AP + kc * 8);
+          *reinterpret_cast<const i32x4*>(stage + row * Geo<HD>::AP + kc * 8);
   }
 }
 
@@ -205,11 +236,13 @@ SR_DEV void unstage(const bf16_t* stage, bf16_t* dst, size_t ld, int r0, int S) 
 // NW waves (32 queries each) per workgroup share the K / V tiles.
 // Queries: Sq rows of q (row stride ldq); keys: Skv rows of kv (row stride ldkv), values D
 // columns after the keys; kv_elems: elements addressable from kv (the buffer's extent).
-template <int NW>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* __restrict__ q, int ldq,
+template <int HD, int NW>
+__global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_fwd_mfma(const bf16_t* __restrict__ q, int ldq,
                                                      const bf16_t* __restrict__ kv, int ldkv, uint32_t kv_elems,
                                                      bf16_t* __restrict__ O, float* __restrict__ lse, int Sq, int Skv,
                                                      int H, int D, float sl2) {
+  using G = Geo<HD>;
+  constexpr int TE = G::TE, TB = G::TB, SGB = G::SGB, KS = G::KS, DB = G::DB;
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
@@ -220,19 +253,19 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(kv, kv_elems * 2u);
   const uint32_t kbase = (uint32_t)(((size_t)b * Skv * ldkv + hh * HD) * 2);
   const uint32_t vbase = kbase + (uint32_t)D * 2u;
-  RowAddr ra;
-  TrAddr ta;
+  RowAddr<HD> ra;
+  TrAddr<HD> ta;
   ra.init(lds_addr(smem), lane);
   ta.init(lds_addr(smem), lane);
 
-  bf16x8 qf[4];
+  bf16x8 qf[KS];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) qf[ks] = myq < Sq ? ld8(qp + (size_t)myq * ldq + ks * 16 + 8 * h32) : zero8();
+  for (int ks = 0; ks < KS; ++ks) qf[ks] = myq < Sq ? ld8(qp + (size_t)myq * ldq + ks * 16 + 8 * h32) : zero8();
 
-  constexpr int kLoads = 2 * (8 / NW);   // buffer loads per thread per tile (two tiles)
+  constexpr int kLoads = 2 * (G::BLK / NW);   // buffer loads per thread per tile (two tiles)
   auto load = [&](int t, int s) {
-    tile_load<NW>(rq, kbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE, t < nt);
-    tile_load<NW>(rq, vbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE + TE, t < nt);
+    tile_load<HD, NW>(rq, kbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE, t < nt);
+    tile_load<HD, NW>(rq, vbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE + TE, t < nt);
   };
   auto mask = [&](f32x16& sc, int k0) {   // keys past Skv do not exist
 #pragma unroll
@@ -240,8 +273,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
       if (k0 + srow(r, h32) >= Skv) sc[r] = -INFINITY;
   };
 
-  f32x16 o[2];
-  zero16(o[0]); zero16(o[1]);
+  f32x16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) zero16(o[db]);
   // softmax denominators on the matrix cores: a 32-row A operand whose row 0 is all ones turns
   // the P^T MFMA into the column sums of P^T, so lsum[0] of lane l32 (first half) is the sum of
   // the bf16 probabilities of query l32 (the values the PV product uses); every other element
@@ -253,21 +287,21 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
   for (int i = 0; i < 8; ++i) ones[i] = (__bf16)(l32 == 0 ? 1.0f : 0.0f);
   float m_run = -INFINITY;   // running max of the raw scores
   // K row fragments of key unit U of stage SG
-  auto read_k = [&](auto sg, auto uu, RawFrag<true> (&kr)[4]) {
+  auto read_k = [&](auto sg, auto uu, RawFrag<true> (&kr)[KS]) {
     constexpr int SG = decltype(sg)::value, U = decltype(uu)::value;
-    static_for<4>([&](auto ks) { ra.template read<SG * SGB, U * 32, decltype(ks)::value>(kr[ks.value]); });
+    static_for<KS>([&](auto ks) { ra.template read<SG * SGB, U * 32, decltype(ks)::value>(kr[ks.value]); });
   };
   // S^T = K Q^T of a unit: register r holds key srow(r), query l32
-  auto scores = [&](RawFrag<true> (&kr)[4], f32x16& sc) {
+  auto scores = [&](RawFrag<true> (&kr)[KS], f32x16& sc) {
     zero16(sc);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) sc = mfma(kr[ks].settle(), qf[ks], sc);
+    for (int ks = 0; ks < KS; ++ks) sc = mfma(kr[ks].settle(), qf[ks], sc);
   };
   // V^T fragments of unit U (read before the softmax arithmetic, so that their latency hides
   // behind it)
-  auto read_vt = [&](auto sg, auto uu, RawFrag<false> (&vt)[2][2]) {
+  auto read_vt = [&](auto sg, auto uu, RawFrag<false> (&vt)[DB][2]) {
     constexpr int SG = decltype(sg)::value, U = decltype(uu)::value;
-    static_for<2>([&](auto db) {
+    static_for<DB>([&](auto db) {
       static_for<2>([&](auto kk) {
         ta.template read<SG * SGB + TB, U * 32 + decltype(kk)::value * 16, decltype(db)::value>(vt[db.value][kk.value]);
       });
@@ -276,7 +310,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
   // online softmax over the tile's 64 keys (one reference update for both units), then
   // O^T += V^T P^T per unit
   auto consume = [&](auto sg, const f32x16& sc0, const f32x16& sc1) {
-    RawFrag<false> vt0[2][2], vt1[2][2];
+    RawFrag<false> vt0[DB][2], vt1[DB][2];
     read_vt(sg, IC<0>{}, vt0);
     read_vt(sg, IC<1>{}, vt1);
     float mx = fmaxf(sc0[0], sc1[0]);
@@ -292,7 +326,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
       const float alpha = ex2((m_run - m_ref) * sl2);
       lsum[0] *= alpha;
 #pragma unroll
-      for (int db = 0; db < 2; ++db)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
       m_run = m_ref;
@@ -311,7 +345,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
     }
     lgkm_wait<0>();
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         o[db] = mfma(vt0[db][kk].settle(), pb0[kk], o[db]);
@@ -330,7 +364,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
     // tile t-1); it then flies during tiles t and t+1
     load(t + 2, (s0 + 2) % NSTG);
     // both units' score MFMAs first: unit 1's run while unit 0's softmax arithmetic does
-    RawFrag<true> k0r[4], k1r[4];
+    RawFrag<true> k0r[KS], k1r[KS];
     f32x16 sc0, sc1;
     read_k(stg, IC<0>{}, k0r);
     read_k(stg, IC<1>{}, k1r);
@@ -358,23 +392,25 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_fwd_mfma(const bf16_t* _
   __syncthreads();   // every wave is done with the stages before they hold the output
   const float l_tot = half_pair_sum(lsum[0]);   // the second half's element is zero
   if (h32 == 0 && myq < Sq) lse[((size_t)b * H + hh) * Sq + myq] = m_run * sl2 + log2f(l_tot);
-  stage_t(smem, o, 1.0f / l_tot, wid, lane);
+  stage_t<HD>(smem, o, 1.0f / l_tot, wid, lane);
   __syncthreads();
-  unstage<NW>(smem, O + (size_t)b * Sq * D + hh * HD, D, blockIdx.x * (32 * NW), Sq);
+  unstage<HD, NW>(smem, O + (size_t)b * Sq * D + hh * HD, D, blockIdx.x * (32 * NW), Sq);
 }
 
 // ------------------------------------------------------------------------------ backward dK, dV
 
 // NW waves (32 keys each) per workgroup share the Q / dO tiles.
-template <int NW>
+template <int HD, int NW>
 // Keys: Skv rows of kv (stride ldkv, values D columns on); queries: Sq rows of q (stride ldq,
 // q_elems addressable elements); dK to dk_out (stride ldo), dV D columns after it.
-__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_t* __restrict__ q, int ldq,
+__global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dkv_mfma(const bf16_t* __restrict__ q, int ldq,
                                                          uint32_t q_elems, const bf16_t* __restrict__ kv, int ldkv,
                                                          const bf16_t* __restrict__ dO,
                                                          const float* __restrict__ lse, const float* __restrict__ delta,
                                                          bf16_t* __restrict__ dk_out, int ldo, int Sq, int Skv, int H,
                                                          int D, float sl2, float scale) {
+  using G = Geo<HD>;
+  constexpr int TE = G::TE, KS = G::KS, DB = G::DB;
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: Q tile, dO tile
   __shared__ __attribute__((aligned(16))) float fsm[NSTG * 2 * KT];     // stage: lse, delta of the tile's rows
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
@@ -385,14 +421,15 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
   const int nt = (Sq + KT - 1) / KT;
   const bool ragged = Sq % KT != 0;
 
-  bf16x8 kf[4], vf[4];
+  bf16x8 kf[KS], vf[KS];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
+  for (int ks = 0; ks < KS; ++ks) {
     kf[ks] = mykey < Skv ? ld8(kp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8();
     vf[ks] = mykey < Skv ? ld8(vp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8();
   }
-  f32x16 dv[2], dk[2];
-  zero16(dv[0]); zero16(dv[1]); zero16(dk[0]); zero16(dk[1]);
+  f32x16 dv[DB], dk[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) { zero16(dv[db]); zero16(dk[db]); }
 
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(q, q_elems * 2u);
   const __amdgpu_buffer_rsrc_t rd = make_rsrc(dO, (uint32_t)((size_t)gridDim.z * Sq * D * 2));
@@ -402,8 +439,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
   const uint32_t dbase = (uint32_t)(((size_t)b * Sq * D + hh * HD) * 2);
   const uint32_t lbase = (uint32_t)(((size_t)b * H + hh) * Sq * 4);
   auto load = [&](int t, int s) {
-    tile_load<NW>(rq, qbase, (uint32_t)ldq, t * KT, smem + s * 2 * TE);
-    tile_load<NW>(rd, dbase, (uint32_t)D, t * KT, smem + s * 2 * TE + TE);
+    tile_load<HD, NW>(rq, qbase, (uint32_t)ldq, t * KT, smem + s * 2 * TE);
+    tile_load<HD, NW>(rd, dbase, (uint32_t)D, t * KT, smem + s * 2 * TE + TE);
     const uint32_t lo = lbase + (uint32_t)(t * KT + lane) * 4u;
     if (wid == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_ptr_t*)(fsm + s * 2 * KT), 4, lo, 0, 0, 0);
     if (wid == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(rdl, (lds_ptr_t*)(fsm + s * 2 * KT + KT), 4, lo, 0, 0, 0);
@@ -413,13 +450,13 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
     const bf16_t* Qs = smem + s * 2 * TE;
     zero16(sv);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) sv = mfma(row_frag(Qs, u * 32, ks), kf[ks], sv);
+    for (int ks = 0; ks < KS; ++ks) sv = mfma(row_frag<HD>(Qs, u * 32, ks), kf[ks], sv);
   };
   auto dp_of = [&](int s, int u, f32x16& dpv) {
     const bf16_t* dOs = smem + s * 2 * TE + TE;
     zero16(dpv);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) dpv = mfma(row_frag(dOs, u * 32, ks), vf[ks], dpv);
+    for (int ks = 0; ks < KS; ++ks) dpv = mfma(row_frag<HD>(dOs, u * 32, ks), vf[ks], dpv);
   };
   // P, dS of the unit (queries past S contribute nothing), then dV^T += dO^T P, dK^T += Q^T dS
   auto grad = [&](int s, int u, const f32x16& sv, int q0, auto rag) {
@@ -445,11 +482,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
     const bf16_t* Qs = smem + s * 2 * TE;
     const bf16_t* dOs = Qs + TE;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        dv[db] = mfma(tr_frag(dOs, u * 32 + kk * 16, db * 32), pb[kk], dv[db]);
-        dk[db] = mfma(tr_frag(Qs, u * 32 + kk * 16, db * 32), sb[kk], dk[db]);
+        dv[db] = mfma(tr_frag<HD>(dOs, u * 32 + kk * 16, db * 32), pb[kk], dv[db]);
+        dk[db] = mfma(tr_frag<HD>(Qs, u * 32 + kk * 16, db * 32), sb[kk], dk[db]);
       }
   };
 
@@ -460,7 +497,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
   auto tile = [&](int t, auto stg) {
     constexpr int s0 = decltype(stg)::value, s2 = (s0 + 2) % NSTG;
     const bool rag = ragged && t + 1 == nt;
-#pragma unroll
+    // head dim 128: one query unit at a time (unrolled, the two units' live ranges spill)
+#pragma unroll (HD == 64 ? 2 : 1)
     for (int u = 0; u < 2; ++u) {
       f32x16 sv;
       s_of(s0, u, sv);
@@ -483,27 +521,29 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dkv_mfma(const bf16_
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   bf16_t* out = dk_out + (size_t)b * Skv * ldo;
-  stage_t(smem, dk, scale, wid, lane);
+  stage_t<HD>(smem, dk, scale, wid, lane);
   __syncthreads();
-  unstage<NW>(smem, out + hh * HD, ldo, blockIdx.x * (32 * NW), Skv);
+  unstage<HD, NW>(smem, out + hh * HD, ldo, blockIdx.x * (32 * NW), Skv);
   __syncthreads();
-  stage_t(smem, dv, 1.0f, wid, lane);
+  stage_t<HD>(smem, dv, 1.0f, wid, lane);
   __syncthreads();
-  unstage<NW>(smem, out + D + hh * HD, ldo, blockIdx.x * (32 * NW), Skv);
+  unstage<HD, NW>(smem, out + D + hh * HD, ldo, blockIdx.x * (32 * NW), Skv);
 }
 
 // ------------------------------------------------------------------------------ backward dQ
 
 // NW waves (32 queries each) per workgroup share the K / V tiles.
-template <int NW>
+template <int HD, int NW>
 // Queries: Sq rows of q (stride ldq); keys: Skv rows of kv (stride ldkv, kv_elems addressable
 // elements, values D columns on); dQ to dq_out (stride ldo).
-__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t* __restrict__ q, int ldq,
+__global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dq_mfma(const bf16_t* __restrict__ q, int ldq,
                                                         const bf16_t* __restrict__ kv, int ldkv, uint32_t kv_elems,
                                                         const bf16_t* __restrict__ dO,
                                                         const float* __restrict__ lse, const float* __restrict__ delta,
                                                         bf16_t* __restrict__ dq_out, int ldo, int Sq, int Skv, int H,
                                                         int D, float sl2, float scale) {
+  using G = Geo<HD>;
+  constexpr int TE = G::TE, TB = G::TB, SGB = G::SGB, KS = G::KS, DB = G::DB;
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
   const int b = blockIdx.z, hh = blockIdx.y;
@@ -513,39 +553,40 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t
   const int nt = (Skv + KT - 1) / KT;
   const bool ragged = Skv % KT != 0;
 
-  bf16x8 qf[4], df[4];
+  bf16x8 qf[KS], df[KS];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
+  for (int ks = 0; ks < KS; ++ks) {
     qf[ks] = myq < Sq ? ld8(qp + (size_t)myq * ldq + ks * 16 + 8 * h32) : zero8();
     df[ks] = myq < Sq ? ld8(dop + (size_t)myq * D + ks * 16 + 8 * h32) : zero8();
   }
   const float nlse = myq < Sq ? -lse[((size_t)b * H + hh) * Sq + myq] : -INFINITY;
   const float dl_q = myq < Sq ? delta[((size_t)b * H + hh) * Sq + myq] : 0.f;
-  f32x16 dq[2];
-  zero16(dq[0]); zero16(dq[1]);
+  f32x16 dq[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) zero16(dq[db]);
 
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(kv, kv_elems * 2u);
   const uint32_t kbase = (uint32_t)(((size_t)b * Skv * ldkv + hh * HD) * 2);
   const uint32_t vbase = kbase + (uint32_t)D * 2u;
-  RowAddr ra;
-  TrAddr ta;
+  RowAddr<HD> ra;
+  TrAddr<HD> ta;
   ra.init(lds_addr(smem), lane);
   ta.init(lds_addr(smem), lane);
-  constexpr int kLoads = 2 * (8 / NW);   // buffer loads per thread per tile (two tiles)
+  constexpr int kLoads = 2 * (G::BLK / NW);   // buffer loads per thread per tile (two tiles)
   auto load = [&](int t, int s) {
-    tile_load<NW>(rq, kbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE, t < nt);
-    tile_load<NW>(rq, vbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE + TE, t < nt);
+    tile_load<HD, NW>(rq, kbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE, t < nt);
+    tile_load<HD, NW>(rq, vbase, (uint32_t)ldkv, t * KT, smem + s * 2 * TE + TE, t < nt);
   };
   // K (tile 0) or V (tile 1) row fragments of key unit U of stage SG
-  auto read_rows = [&](auto sg, auto uu, auto tl, RawFrag<true> (&fr)[4]) {
+  auto read_rows = [&](auto sg, auto uu, auto tl, RawFrag<true> (&fr)[KS]) {
     constexpr int SG = decltype(sg)::value, U = decltype(uu)::value, TL = decltype(tl)::value;
-    static_for<4>([&](auto ks) { ra.template read<SG * SGB + TL * TB, U * 32, decltype(ks)::value>(fr[ks.value]); });
+    static_for<KS>([&](auto ks) { ra.template read<SG * SGB + TL * TB, U * 32, decltype(ks)::value>(fr[ks.value]); });
   };
   // S^T = K Q^T and dP^T = V dO^T of a key unit: register r holds key srow(r), query l32
-  auto sd = [&](RawFrag<true> (&kr)[4], RawFrag<true> (&vr)[4], f32x16& sv, f32x16& dpv) {
+  auto sd = [&](RawFrag<true> (&kr)[KS], RawFrag<true> (&vr)[KS], f32x16& sv, f32x16& dpv) {
     zero16(sv); zero16(dpv);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int ks = 0; ks < KS; ++ks) {
       sv = mfma(kr[ks].settle(), qf[ks], sv);
       dpv = mfma(vr[ks].settle(), df[ks], dpv);
     }
@@ -554,8 +595,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t
   // first, so that their latency hides behind the arithmetic)
   auto grad = [&](auto sg, auto uu, const f32x16& sv, const f32x16& dpv, int k0, auto rag) {
     constexpr int SG = decltype(sg)::value, U = decltype(uu)::value;
-    RawFrag<false> fk[2][2];
-    static_for<2>([&](auto db) {
+    RawFrag<false> fk[DB][2];
+    static_for<DB>([&](auto db) {
       static_for<2>([&](auto kk) {
         ta.template read<SG * SGB, U * 32 + decltype(kk)::value * 16, decltype(db)::value>(fk[db.value][kk.value]);
       });
@@ -572,7 +613,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t
     }
     lgkm_wait<0>();
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) dq[db] = mfma(fk[db][kk].settle(), sb[kk], dq[db]);
   };
@@ -588,7 +629,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t
     // tile t-1); it then flies during tiles t and t+1
     load(t + 2, (s0 + 2) % NSTG);
     // both units' S^T / dP^T MFMAs first: unit 1's run while unit 0's arithmetic does
-    RawFrag<true> k0r[4], v0r[4], k1r[4], v1r[4];
+    RawFrag<true> k0r[KS], v0r[KS], k1r[KS], v1r[KS];
     f32x16 sv0, dp0, sv1, dp1;
     read_rows(stg, IC<0>{}, IC<0>{}, k0r);
     read_rows(stg, IC<0>{}, IC<1>{}, v0r);
@@ -619,9 +660,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bwd_dq_mfma(const bf16_t
 
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  stage_t(smem, dq, scale, wid, lane);
+  stage_t<HD>(smem, dq, scale, wid, lane);
   __syncthreads();
-  unstage<NW>(smem, dq_out + (size_t)b * Sq * ldo + hh * HD, ldo, blockIdx.x * (32 * NW), Sq);
+  unstage<HD, NW>(smem, dq_out + (size_t)b * Sq * ldo + hh * HD, ldo, blockIdx.x * (32 * NW), Sq);
 }
 
 // ------------------------------------------------------------------------------ generic kernels
@@ -748,6 +789,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_colsum_mfma(const bf16_t
                                                            const float* __restrict__ lse,
                                                            float* __restrict__ colsum, int S, int H, int D,
                                                            float sl2) {
+  constexpr int HD = 64;   // the deterministic model's head dim (the selector's block)
+  constexpr int TE = Geo<HD>::TE;
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * TE];   // stage: Q tile
   __shared__ __attribute__((aligned(16))) float fsm[NSTG * KT];     // stage: lse of the tile's rows
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
@@ -767,7 +810,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_colsum_mfma(const bf16_t
   const uint32_t qbase = (uint32_t)(((size_t)b * S * ld + hh * HD) * 2);
   const uint32_t lbase = (uint32_t)(((size_t)b * H + hh) * S * 4);
   auto load = [&](int t, int s) {
-    tile_load<NW>(rq, qbase, (uint32_t)ld, t * KT, smem + s * TE);
+    tile_load<HD, NW>(rq, qbase, (uint32_t)ld, t * KT, smem + s * TE);
     const uint32_t lo = lbase + (uint32_t)(t * KT + lane) * 4u;
     if (wid == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_ptr_t*)(fsm + s * KT), 4, lo, 0, 0, 0);
   };
@@ -777,7 +820,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_colsum_mfma(const bf16_t
     f32x16 sv;
     zero16(sv);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) sv = mfma(row_frag(Qs, u * 32, ks), kf[ks], sv);
+    for (int ks = 0; ks < 4; ++ks) sv = mfma(row_frag<HD>(Qs, u * 32, ks), kf[ks], sv);
     const float* ls = fsm + s * KT + u * 32;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -847,7 +890,7 @@ __global__ __launch_bounds__(64) void attn_colsum_simple(const Ta* __restrict__ 
 
 static inline float attn_sl2(int hd) { return 1.4426950408889634f / sqrtf((float)hd); }
 
-bool attn_uses_mfma(int dtype, int hd) { return dtype == kBF16 && hd == HD; }
+bool attn_uses_mfma(int dtype, int hd) { return dtype == kBF16 && (hd == 64 || hd == 128); }
 
 template <typename Ta>
 static hipError_t fwd_simple(const Ta* qkv, Ta* O, float* lse, int B, int S, int H, int D, int hd, hipStream_t st) {
@@ -880,35 +923,58 @@ static hipError_t bwd_simple(const Ta* qkv, const Ta* dO, const float* lse, cons
 
 // The MFMA kernels on Sq query rows and Skv key/value rows (self-attention: both S, q, k and v
 // in one token-major qkv buffer; asymmetric attention: separate buffers).
+template <int HD>
+static hipError_t fwd_mfma_hd(const bf16_t* q, int ldq, const bf16_t* kv, int ldkv, uint32_t kv_elems, bf16_t* O,
+                              float* lse, int B, int Sq, int Skv, int H, int D, hipStream_t st) {
+  constexpr int kw = attn_waves<HD>();
+  dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
+  hipLaunchKernelGGL((attn_fwd_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv,
+                     H, D, attn_sl2(HD));
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_fwd_mfma(const bf16_t* q, int ldq, const bf16_t* kv, int ldkv, uint32_t kv_elems, bf16_t* O,
                                 float* lse, int B, int Sq, int Skv, int H, int D, hipStream_t st) {
-  constexpr int kw = kFwdWaves;
-  dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
-  hipLaunchKernelGGL(attn_fwd_mfma<kw>, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv, H, D,
-                     attn_sl2(D / H));
+  if (D / H == 128) return fwd_mfma_hd<128>(q, ldq, kv, ldkv, kv_elems, O, lse, B, Sq, Skv, H, D, st);
+  return fwd_mfma_hd<64>(q, ldq, kv, ldkv, kv_elems, O, lse, B, Sq, Skv, H, D, st);
+}
+
+template <int HD>
+static hipError_t dkv_mfma_hd(const bf16_t* q, int ldq, uint32_t q_elems, const bf16_t* kv, int ldkv,
+                              const bf16_t* dO, const float* lse, const float* delta, bf16_t* dk_out, int ldo, int B,
+                              int Sq, int Skv, int H, int D, hipStream_t st) {
+  constexpr int kw = attn_waves<HD>();
+  dim3 g((Skv + 32 * kw - 1) / (32 * kw), H, B);
+  hipLaunchKernelGGL((attn_bwd_dkv_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta,
+                     dk_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   return hipGetLastError();
 }
 
 hipError_t launch_attn_dkv_mfma(const bf16_t* q, int ldq, uint32_t q_elems, const bf16_t* kv, int ldkv,
                                 const bf16_t* dO, const float* lse, const float* delta, bf16_t* dk_out, int ldo, int B,
                                 int Sq, int Skv, int H, int D, hipStream_t st) {
-  constexpr int kw = kDkvWaves;
-  dim3 g((Skv + 32 * kw - 1) / (32 * kw), H, B);
-  const int hd = D / H;
-  hipLaunchKernelGGL(attn_bwd_dkv_mfma<kw>, g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta, dk_out,
-                     ldo, Sq, Skv, H, D, attn_sl2(hd), 1.0f / sqrtf((float)hd));
+  if (D / H == 128)
+    return dkv_mfma_hd<128>(q, ldq, q_elems, kv, ldkv, dO, lse, delta, dk_out, ldo, B, Sq, Skv, H, D, st);
+  return dkv_mfma_hd<64>(q, ldq, q_elems, kv, ldkv, dO, lse, delta, dk_out, ldo, B, Sq, Skv, H, D, st);
+}
+
+template <int HD>
+static hipError_t dq_mfma_hd(const bf16_t* q, int ldq, const bf16_t* kv, int ldkv, uint32_t kv_elems,
+                             const bf16_t* dO, const float* lse, const float* delta, bf16_t* dq_out, int ldo, int B,
+                             int Sq, int Skv, int H, int D, hipStream_t st) {
+  constexpr int kw = attn_waves<HD>();
+  dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
+  hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta,
+                     dq_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   return hipGetLastError();
 }
 
 hipError_t launch_attn_dq_mfma(const bf16_t* q, int ldq, const bf16_t* kv, int ldkv, uint32_t kv_elems,
                                const bf16_t* dO, const float* lse, const float* delta, bf16_t* dq_out, int ldo, int B,
                                int Sq, int Skv, int H, int D, hipStream_t st) {
-  constexpr int kw = kDqWaves;
-  dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
-  const int hd = D / H;
-  hipLaunchKernelGGL(attn_bwd_dq_mfma<kw>, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta, dq_out,
-                     ldo, Sq, Skv, H, D, attn_sl2(hd), 1.0f / sqrtf((float)hd));
-  return hipGetLastError();
+  if (D / H == 128)
+    return dq_mfma_hd<128>(q, ldq, kv, ldkv, kv_elems, dO, lse, delta, dq_out, ldo, B, Sq, Skv, H, D, st);
+  return dq_mfma_hd<64>(q, ldq, kv, ldkv, kv_elems, dO, lse, delta, dq_out, ldo, B, Sq, Skv, H, D, st);
 }
 
 hipError_t launch_attn_fwd(int dtype, const void* qkv, void* O, float* lse, int B, int S, int H, int D,
@@ -965,8 +1031,8 @@ static hipError_t colsum_simple(const Ta* qkv, const float* lse, float* colsum, 
 hipError_t launch_attn_colsum(int dtype, const void* qkv, const float* lse, float* colsum, int B, int S, int H, int D,
                               hipStream_t st) {
   const int hd = D / H;
-  if (attn_uses_mfma(dtype, hd)) {
-    constexpr int kw = kDkvWaves;   // the dK/dV kernel's score half: the same shape
+  if (dtype == kBF16 && hd == 64) {   // MFMA column sums at head dim 64; other head dims generic
+    constexpr int kw = attn_waves<64>();   // the dK/dV kernel's score half: the same shape
     dim3 g((S + 32 * kw - 1) / (32 * kw), H, B);
     hipLaunchKernelGGL(attn_colsum_mfma<kw>, g, dim3(64 * kw), 0, st, (const bf16_t*)qkv, lse, colsum, S, H, D,
                        attn_sl2(hd));

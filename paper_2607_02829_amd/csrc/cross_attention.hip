@@ -7,9 +7,9 @@
 // at column h*hd, v at D + h*hd); lse, delta [B, H, Sq], lse the base-2 log-sum-exp of the scaled
 // scores (P = exp2(s * log2(e)/sqrt(hd) - lse)), delta = rowsum(dO * O) per head.
 //
-// bf16 with hd = 64 runs the MFMA attention kernels (attention.hip), which take the query and
-// key/value buffers and their token counts separately.  Generic kernels (any storage type, hd in
-// {32, 64, 128}) for the rest: one thread per query (forward with online softmax, dQ) or per
+// bf16 with hd = 64 or 128 runs the MFMA attention kernels (attention.hip), which take the query
+// and key/value buffers and their token counts separately.  Generic kernels (fp32 storage, or
+// bf16 at hd = 32) for the rest: one thread per query (forward with online softmax, dQ) or per
 // key (dK and dV, summing over the queries in order), fp32 accumulation, deterministic.
 #include "common.h"
 #include "sr_internal.h"

@@ -35,8 +35,12 @@ def test_preln_bf16_hd32_generic_attention():
     _check(inputs.small(name="hd32", H=8), 70, 1)
 
 
-def test_preln_bf16_hd128_generic_attention():
+def test_preln_bf16_hd128_mfma_attention():
+    # head dim 128 (the generative model's 8 heads x 128) on the MFMA attention kernels: one ragged
+    # tile, then several 128-query workgroups and 64-key tiles with a ragged tail, and adaLN
     _check(inputs.small(name="hd128", H=2), 45, 1)
+    _check(inputs.small(name="hd128_b", H=2, Hg=20, Wg=20), 333, 2)
+    _check(inputs.small(name="hd128_ada", H=2, kind="adaln"), 150, 1)
 
 
 def test_preln_f32_small_fwd_bwd():

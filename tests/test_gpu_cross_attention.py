@@ -44,6 +44,9 @@ def _gpu(B, Sq, Skv, D, H, dtype, q, kv, dO):
     (2, 20, 1, 256, 2, "bf16"), (2, 33, 77, 256, 4, "f32"), (1, 64, 200, 256, 8, "bf16"),
     # the MFMA path across its 256-row workgroups and 64-row tiles, ragged on both sides
     (3, 257, 511, 256, 4, "bf16"), (2, 256, 64, 256, 4, "bf16"), (1, 1, 1, 256, 4, "bf16"),
+    # head dim 128 (MFMA, 128-row workgroups): ragged on both sides, Sq < Skv and Sq > Skv, one token
+    (2, 129, 257, 256, 2, "bf16"), (1, 300, 65, 512, 4, "bf16"), (2, 1, 130, 256, 2, "bf16"),
+    (2, 70, 1, 256, 2, "bf16"), (2, 33, 77, 256, 2, "f32"),
 ])
 def test_cross_attention_matches_oracle(B, Sq, Skv, D, H, dtype):
     print(f"[xattn] B={B} Sq={Sq} Skv={Skv} D={D} H={H} {dtype}", flush=True)
@@ -86,6 +89,35 @@ def test_cross_attention_at_the_generative_shape():
              ("dk", storage_to_f64(dkv)[..., :D], oblk.merge_heads(dk_ref)),
              ("dv", storage_to_f64(dkv)[..., D:], oblk.merge_heads(dv_ref))]
     check_pairs(items, "bf16", "[xattn edm]")
+
+
+def test_cross_attention_at_the_generative_shape_hd128():
+    # the generative model's heads (8 x 128, App. A.1 EDM table) at 2 x 2048 queries x 8192 keys
+    B, Sq, Skv, D, H = 2, 2048, 8192, 1024, 8
+    print(f"[xattn edm hd128] B={B} Sq={Sq} Skv={Skv} D={D} H={H}", flush=True)
+    q, kv, dO = _data(B, Sq, Skv, D, "bf16", 2)
+    O, lse, dq, dkv = _gpu(B, Sq, Skv, D, H, "bf16", q, kv, dO)
+    q64, kv64, dO64 = storage_to_f64(q), storage_to_f64(kv), storage_to_f64(dO)
+    qh = oblk.split_heads(q64, H)
+    kh = oblk.split_heads(kv64[..., :D], H)
+    vh = oblk.split_heads(kv64[..., D:], H)
+    print("[xattn edm hd128] oracle", flush=True)
+    O_ref = oblk.merge_heads(oblk.attention_fwd(qh, kh, vh))
+    dq_ref, dk_ref, dv_ref = oblk.attention_bwd(qh, kh, vh, oblk.split_heads(dO64, H))
+    items = [("O", storage_to_f64(O), O_ref), ("dq", storage_to_f64(dq), oblk.merge_heads(dq_ref)),
+             ("dk", storage_to_f64(dkv)[..., :D], oblk.merge_heads(dk_ref)),
+             ("dv", storage_to_f64(dkv)[..., D:], oblk.merge_heads(dv_ref))]
+    check_pairs(items, "bf16", "[xattn edm hd128]")
+
+
+@pytest.mark.parametrize("H", [4, 2])
+def test_cross_attention_bitwise_repeatable_hd(H):
+    B, Sq, Skv, D = 2, 300, 700, 256
+    q, kv, dO = _data(B, Sq, Skv, D, "bf16", 4)
+    a = _gpu(B, Sq, Skv, D, H, "bf16", q, kv, dO)
+    b = _gpu(B, Sq, Skv, D, H, "bf16", q, kv, dO)
+    for x, y in zip(a, b):
+        assert np.array_equal(np.ascontiguousarray(x).view(np.uint8), np.ascontiguousarray(y).view(np.uint8))
 
 
 def test_cross_attention_bitwise_repeatable():
