@@ -253,6 +253,56 @@ SR_API sr_status sr_cross_attention_bwd(const sr_config* cfg, int32_t Sq, int32_
                                  const float* lse, void* dq, void* dkv, float* delta,
                                  void* stream);
 
+/* The generative model's block (Sec. 3.4 "Integration with Generative Forecasting", Alg. 2
+ * stage 2; App. A.1 EDM table: FiLM -> self-attention -> sigma-gated cross-attention -> MLP),
+ * on S tokens per sample (the K routed ones in the sparse stage, S = L for the dense block)
+ * with cross-attention to all L conditioning tokens (the asymmetric design):
+ *   (shift, scale) = e W_film^T + b_film;   g = sigmoid(e W_g^T + b_g)       (per sample)
+ *   u  = LN0(h) (1 + scale) + shift            LN0: LayerNorm without affine parameters
+ *   h1 = h + SelfAttn(u)                       w_qkv [3D,D], b_qkv, w_o [D,D], b_o (over S tokens)
+ *   h2 = h1 + g * (CrossAttn(LNc(h1), Z_c) W_oc^T + b_oc)
+ *        queries LNc(h1) W_q^T + b_q (S tokens), [keys values] = Z_c W_kv^T + b_kv (L tokens,
+ *        rows of w_kv [2D,D] ordered k, v, head-major within each)
+ *   h' = h2 + GELU(LN2(h2) W_fc1^T + b_fc1) W_fc2^T + b_fc2
+ * e: the noise embedding [B,D]; Z_c: the conditioning tokens [B,L,D]; both storage dtype and
+ * shared by every block.  nn.Linear layout [out, in], storage dtype. */
+typedef struct {
+  const void *w_film, *b_film, *w_qkv, *b_qkv, *w_o, *b_o;
+  const void *lnc_w, *lnc_b, *w_q, *b_q, *w_kv, *b_kv, *w_oc, *b_oc, *w_g, *b_g;
+  const void *ln2_w, *ln2_b, *w_fc1, *b_fc1, *w_fc2, *b_fc2;
+} sr_edm_block_params;
+
+/* Its gradients, fp32, shaped like the parameters, OVERWRITTEN; a NULL member skips one. */
+typedef struct {
+  float *w_film, *b_film, *w_qkv, *b_qkv, *w_o, *b_o;
+  float *lnc_w, *lnc_b, *w_q, *b_q, *w_kv, *b_kv, *w_oc, *b_oc, *w_g, *b_g;
+  float *ln2_w, *ln2_b, *w_fc1, *b_fc1, *w_fc2, *b_fc2;
+} sr_edm_block_grads;
+
+/* Bytes of `saved` and `scratch` for the generative blocks at S query tokens per sample and
+ * cfg->L conditioning tokens (cfg->kind and cfg->idx_shared are not used). */
+SR_API sr_status sr_edm_workspace_bytes(const sr_config* cfg, int32_t S, size_t* saved_bytes,
+                                 size_t* scratch_bytes);
+
+/* cfg->n_blocks generative blocks on h_in [B,S,D] -> h_out [B,S,D] (may not alias), given the
+ * noise embedding e [B,D] and the conditioning tokens zc [B,L,D] (L = cfg->L), storage dtype.
+ * The residual stream is fp32 inside; h_out is rounded once.  saved: activations for
+ * sr_edm_blocks_bwd (sr_edm_workspace_bytes), which must outlive it.  The sparse stage of
+ * Alg. 2 is sr_gather -> this call with S = K -> sr_scatter_delta. */
+SR_API sr_status sr_edm_blocks_fwd(const sr_config* cfg, int32_t S, const sr_edm_block_params* params,
+                            const void* e, const void* zc, const void* h_in, void* h_out, void* saved,
+                            size_t saved_bytes, void* stream);
+
+/* Its vector-Jacobian product: dh_in [B,S,D] storage out (may alias dh_out); grads (host array
+ * of n_blocks, fp32, overwritten); dzc [B,L,D] fp32 out, the gradient of the conditioning
+ * tokens summed over the blocks, and de [B,D] fp32 out, that of the noise embedding summed over
+ * the blocks (either may be NULL). */
+SR_API sr_status sr_edm_blocks_bwd(const sr_config* cfg, int32_t S, const sr_edm_block_params* params,
+                            const void* e, const void* zc, const void* saved, size_t saved_bytes,
+                            const void* dh_out, void* dh_in, const sr_edm_block_grads* grads,
+                            float* dzc, float* de, void* scratch, size_t scratch_bytes,
+                            void* stream);
+
 /* Debug check of an index set: *ok_dev (device int32) is set to 1 if every row of
  * idx is strictly increasing and inside [0,L), else 0. */
 SR_API sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx,

@@ -26,6 +26,7 @@ EXPORTS = ("sr_last_error", "sr_version", "sr_workspace_bytes", "sr_select_scrat
            "sr_sparse_blocks_bwd", "sr_dense_blocks_fwd", "sr_dense_blocks_bwd", "sr_validate_indices",
            "sr_attention_colsums", "sr_select_topk_scores", "sr_routed_blocks_fwd", "sr_routed_blocks_bwd",
            "sr_cross_attention_fwd", "sr_cross_attention_bwd",
+           "sr_edm_workspace_bytes", "sr_edm_blocks_fwd", "sr_edm_blocks_bwd",
            "sr_profile_start", "sr_profile_stop")
 
 
@@ -52,6 +53,19 @@ class SrBlockParams(ctypes.Structure):
 
 class SrBlockGrads(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in PARAM_FIELDS]
+
+
+EDM_PARAM_FIELDS = ("w_film", "b_film", "w_qkv", "b_qkv", "w_o", "b_o",
+                    "lnc_w", "lnc_b", "w_q", "b_q", "w_kv", "b_kv", "w_oc", "b_oc", "w_g", "b_g",
+                    "ln2_w", "ln2_b", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
+
+
+class SrEdmBlockParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in EDM_PARAM_FIELDS]
+
+
+class SrEdmBlockGrads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in EDM_PARAM_FIELDS]
 
 
 _lib = None
@@ -87,6 +101,9 @@ def lib(path: str = LIB_PATH):
         "sr_cross_attention_bwd": ([CP, I32, I32, P, P, P, P, P, P, P, P, P], I32),
         "sr_routed_blocks_bwd": ([CP, I32, P, P, P, P, SZ, P, P, P, P, SZ, P], I32),
         "sr_select_topk_scores": ([CP, I32, P, I32, P, P], I32),
+        "sr_edm_workspace_bytes": ([CP, I32, ctypes.POINTER(SZ), ctypes.POINTER(SZ)], I32),
+        "sr_edm_blocks_fwd": ([CP, I32, P, P, P, P, P, P, SZ, P], I32),
+        "sr_edm_blocks_bwd": ([CP, I32, P, P, P, P, SZ, P, P, P, P, P, P, SZ, P], I32),
         "sr_profile_start": ([ctypes.c_char_p], I32),
         "sr_profile_stop": ([ctypes.c_char_p, SZ, ctypes.POINTER(SZ)], I32),
     }
@@ -215,6 +232,23 @@ def sr_cross_attention_fwd(cfg, Sq, Skv, q, kv, O, lse, stream=None):
 def sr_cross_attention_bwd(cfg, Sq, Skv, q, kv, O, dO, lse, dq, dkv, delta, stream=None):
     _check(lib().sr_cross_attention_bwd(ctypes.byref(cfg), Sq, Skv, _p(q), _p(kv), _p(O), _p(dO), _p(lse), _p(dq),
                                         _p(dkv), _p(delta), _stream(stream)))
+
+
+def sr_edm_workspace_bytes(cfg: SrConfig, S: int) -> tuple[int, int]:
+    a, b = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().sr_edm_workspace_bytes(ctypes.byref(cfg), S, ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
+
+
+def sr_edm_blocks_fwd(cfg, S, params, e, zc, h_in, h_out, saved, stream=None):
+    _check(lib().sr_edm_blocks_fwd(ctypes.byref(cfg), S, params, _p(e), _p(zc), _p(h_in), _p(h_out), _p(saved),
+                                   _nbytes(saved), _stream(stream)))
+
+
+def sr_edm_blocks_bwd(cfg, S, params, e, zc, saved, dh_out, dh_in, grads, dzc, de, scratch, stream=None):
+    _check(lib().sr_edm_blocks_bwd(ctypes.byref(cfg), S, params, _p(e), _p(zc), _p(saved), _nbytes(saved),
+                                   _p(dh_out), _p(dh_in), grads, _p(dzc), _p(de), _p(scratch), _nbytes(scratch),
+                                   _stream(stream)))
 
 
 def sr_attention_colsums(cfg, S, saved, block, colsum, stream=None):

@@ -14,7 +14,7 @@ OUT = os.path.join(HERE, "libsr.so")
 BUILD = os.path.join(ROOT, "_build")
 
 SOURCES = ["select.hip", "routing.hip", "rowops.hip", "gemv.hip", "gemm.hip", "attention.hip", "cross_attention.hip",
-           "stack.cpp", "api.cpp", "profile.cpp"]
+           "edm.hip", "stack.cpp", "api.cpp", "profile.cpp"]
 # Files whose floating-point results are part of a bit-exact contract (top-k score,
 # scatter rounding): no multiply-add contraction anywhere in them.
 NO_CONTRACT = {"select.hip", "routing.hip"}

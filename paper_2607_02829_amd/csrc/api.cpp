@@ -1,5 +1,6 @@
 // C ABI of libsr (declared and documented in include/sr.h): argument validation
 // on the host, then launches on the caller's stream.  Nothing is allocated here.
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -7,6 +8,7 @@
 #include <vector>
 
 #include "../../include/sr.h"
+#include "edm.h"
 #include "profile.h"
 #include "stack.h"
 
@@ -421,6 +423,105 @@ sr_status sr_cross_attention_bwd(const sr_config* cfg, int32_t Sq, int32_t Skv, 
                    (double)cfg->B * (5.0 * Sq + 4.0 * Skv) * cfg->D * e, st);
   return hip_status(sr::launch_xattn_bwd(dt, q, kv, O, dO, lse, delta, dq, dkv, cfg->B, Sq, Skv, cfg->H, cfg->D, st),
                     "xattn_bwd");
+}
+
+namespace {
+// The generative blocks read B, L (conditioning tokens), D, H, F, n_blocks, dtype and ln_eps.
+sr_status check_edm(const sr_config* c, int32_t S) {
+  SR_CHECK(c != nullptr, SR_EINVAL, "cfg is NULL");
+  SR_CHECK(c->dtype == SR_F32 || c->dtype == SR_BF16, SR_EDTYPE, "unknown dtype %d", c->dtype);
+  SR_CHECK(c->B >= 1 && c->L >= 1 && c->D >= 1 && c->H >= 1 && c->F >= 1 && c->n_blocks >= 1, SR_EINVAL,
+           "sizes must be positive (B=%d L=%d D=%d H=%d F=%d n_blocks=%d)", c->B, c->L, c->D, c->H, c->F,
+           c->n_blocks);
+  SR_CHECK(S >= 1, SR_ESHAPE, "S=%d must be >= 1", S);
+  SR_CHECK(c->D % c->H == 0, SR_ESHAPE, "D=%d is not a multiple of H=%d", c->D, c->H);
+  SR_CHECK(c->D % 64 == 0 && c->F % 64 == 0, SR_EUNSUPPORTED, "D=%d and F=%d must be multiples of 64", c->D, c->F);
+  SR_CHECK(c->D <= 2048, SR_EUNSUPPORTED, "D=%d > 2048", c->D);
+  const int hd = c->D / c->H;
+  SR_CHECK(hd == 32 || hd == 64 || hd == 128, SR_EUNSUPPORTED, "head dim %d not in {32, 64, 128}", hd);
+  SR_CHECK(c->ln_eps > 0.f, SR_EINVAL, "ln_eps must be > 0");
+  const size_t rows = (size_t)c->B * std::max<int32_t>(S, c->L);
+  SR_CHECK(rows * (size_t)std::max(c->F, 3 * c->D) * 4 < (1ull << 31), SR_EUNSUPPORTED,
+           "stack buffers beyond 2 GiB are not supported");
+  return SR_OK;
+}
+
+sr::EdmDims edm_dims(const sr_config* c, int S) {
+  sr::EdmDims d;
+  d.B = c->B; d.L = c->L; d.D = c->D; d.H = c->H; d.F = c->F; d.nb = c->n_blocks; d.S = S;
+  d.M = c->B * S; d.Mc = c->B * c->L;
+  d.dtype = c->dtype == SR_BF16 ? sr::kBF16 : sr::kF32;
+  d.eps = c->ln_eps;
+  d.elt = elt_of(c->dtype);
+  return d;
+}
+
+sr_status check_edm_params(const sr_config* c, const sr_edm_block_params* p) {
+  SR_CHECK(p != nullptr, SR_EINVAL, "params is NULL");
+  for (int i = 0; i < c->n_blocks; ++i) {
+    const sr_edm_block_params& w = p[i];
+    const void* all[] = {w.w_film, w.b_film, w.w_qkv, w.b_qkv, w.w_o, w.b_o, w.lnc_w, w.lnc_b, w.w_q, w.b_q, w.w_kv,
+                         w.b_kv, w.w_oc, w.b_oc, w.w_g, w.b_g, w.ln2_w, w.ln2_b, w.w_fc1, w.b_fc1, w.w_fc2, w.b_fc2};
+    for (const void* q : all) {
+      SR_CHECK(q != nullptr, SR_EINVAL, "generative block %d: a parameter pointer is NULL", i);
+      SR_CHECK(aligned16(q), SR_EALIGN, "generative block %d: a parameter pointer is not 16-byte aligned", i);
+    }
+  }
+  return SR_OK;
+}
+}  // namespace
+
+sr_status sr_edm_workspace_bytes(const sr_config* cfg, int32_t S, size_t* saved_bytes, size_t* scratch_bytes) {
+  sr_status s = check_edm(cfg, S);
+  if (s != SR_OK) return s;
+  sr::EdmDims d = edm_dims(cfg, S);
+  if (saved_bytes) *saved_bytes = sr::edm_layout_saved(d, nullptr, nullptr);
+  if (scratch_bytes) *scratch_bytes = sr::edm_layout_scratch(d, nullptr, nullptr);
+  return SR_OK;
+}
+
+sr_status sr_edm_blocks_fwd(const sr_config* cfg, int32_t S, const sr_edm_block_params* params, const void* e,
+                            const void* zc, const void* h_in, void* h_out, void* saved, size_t saved_bytes,
+                            void* stream) {
+  sr_status s = check_edm(cfg, S);
+  if (s != SR_OK) return s;
+  if ((s = check_edm_params(cfg, params)) != SR_OK) return s;
+  SR_PTR(e, "e");
+  SR_PTR(zc, "zc");
+  SR_PTR(h_in, "h_in");
+  SR_PTR(h_out, "h_out");
+  SR_CHECK(h_in != h_out, SR_EINVAL, "h_out may not alias h_in");
+  size_t sb = 0;
+  sr_edm_workspace_bytes(cfg, S, &sb, nullptr);
+  SR_PTR(saved, "saved");
+  SR_CHECK(saved_bytes >= sb, SR_EWORKSPACE, "saved buffer has %zu bytes, needs %zu", saved_bytes, sb);
+  return hip_status(sr::edm_fwd(edm_dims(cfg, S), params, e, zc, h_in, h_out, (char*)saved, (hipStream_t)stream),
+                    "edm_blocks_fwd");
+}
+
+sr_status sr_edm_blocks_bwd(const sr_config* cfg, int32_t S, const sr_edm_block_params* params, const void* e,
+                            const void* zc, const void* saved, size_t saved_bytes, const void* dh_out, void* dh_in,
+                            const sr_edm_block_grads* grads, float* dzc, float* de, void* scratch,
+                            size_t scratch_bytes, void* stream) {
+  sr_status s = check_edm(cfg, S);
+  if (s != SR_OK) return s;
+  if ((s = check_edm_params(cfg, params)) != SR_OK) return s;
+  SR_PTR(e, "e");
+  SR_PTR(zc, "zc");
+  SR_PTR(dh_out, "dh_out");
+  SR_PTR(dh_in, "dh_in");
+  SR_CHECK(grads != nullptr, SR_EINVAL, "grads is NULL");
+  if (dzc) SR_CHECK(aligned16(dzc), SR_EALIGN, "dzc is not 16-byte aligned");
+  if (de) SR_CHECK(aligned16(de), SR_EALIGN, "de is not 16-byte aligned");
+  size_t sb = 0, cb = 0;
+  sr_edm_workspace_bytes(cfg, S, &sb, &cb);
+  SR_PTR(saved, "saved");
+  SR_CHECK(saved_bytes >= sb, SR_EWORKSPACE, "saved buffer has %zu bytes, needs %zu", saved_bytes, sb);
+  SR_PTR(scratch, "scratch");
+  SR_CHECK(scratch_bytes >= cb, SR_EWORKSPACE, "scratch buffer has %zu bytes, needs %zu", scratch_bytes, cb);
+  return hip_status(sr::edm_bwd(edm_dims(cfg, S), params, e, zc, (const char*)saved, dh_out, dh_in, grads, dzc, de,
+                                (char*)scratch, (hipStream_t)stream),
+                    "edm_blocks_bwd");
 }
 
 sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx, int32_t* ok_dev, void* stream) {

@@ -80,3 +80,43 @@ def workspace(cfg: abi.SrConfig, S: int, device="cuda"):
     sb, cb = abi.sr_workspace_bytes(cfg, S)
     return (torch.empty(max(sb, 16), dtype=torch.uint8, device=device),
             torch.empty(max(cb, 16), dtype=torch.uint8, device=device))
+
+
+class DeviceEdmParams:
+    """Generative-block parameters on the GPU plus the host array of sr_edm_block_params."""
+
+    def __init__(self, params_storage: list[dict[str, np.ndarray]], device="cuda"):
+        self.tensors = [{k: to_device(v, device) for k, v in p.items()} for p in params_storage]
+        self.array = (abi.SrEdmBlockParams * len(self.tensors))()
+        for i, p in enumerate(self.tensors):
+            for name in abi.EDM_PARAM_FIELDS:
+                setattr(self.array[i], name, p[name].data_ptr())
+
+
+class DeviceEdmGrads:
+    """fp32 gradient buffers of n generative blocks plus the host array of sr_edm_block_grads."""
+
+    def __init__(self, D: int, F: int, n_blocks: int, device="cuda"):
+        import torch
+        shapes = edm_param_shapes(D, F)
+        self.tensors = [{k: torch.full(s, float("nan"), dtype=torch.float32, device=device)
+                         for k, s in shapes.items()} for _ in range(n_blocks)]
+        self.array = (abi.SrEdmBlockGrads * n_blocks)()
+        for i, g in enumerate(self.tensors):
+            for name in abi.EDM_PARAM_FIELDS:
+                setattr(self.array[i], name, g[name].data_ptr())
+
+
+def edm_param_shapes(D: int, F: int) -> dict[str, tuple[int, ...]]:
+    return {"w_film": (2 * D, D), "b_film": (2 * D,), "w_qkv": (3 * D, D), "b_qkv": (3 * D,), "w_o": (D, D),
+            "b_o": (D,), "lnc_w": (D,), "lnc_b": (D,), "w_q": (D, D), "b_q": (D,), "w_kv": (2 * D, D),
+            "b_kv": (2 * D,), "w_oc": (D, D), "b_oc": (D,), "w_g": (D, D), "b_g": (D,), "ln2_w": (D,),
+            "ln2_b": (D,), "w_fc1": (F, D), "b_fc1": (F,), "w_fc2": (D, F), "b_fc2": (D,)}
+
+
+def edm_workspace(cfg: abi.SrConfig, S: int, device="cuda"):
+    """(saved, scratch) uint8 GPU tensors sized by sr_edm_workspace_bytes."""
+    import torch
+    sb, cb = abi.sr_edm_workspace_bytes(cfg, S)
+    return (torch.empty(max(sb, 16), dtype=torch.uint8, device=device),
+            torch.empty(max(cb, 16), dtype=torch.uint8, device=device))

@@ -15,6 +15,8 @@ b5625  8       16 x 32  (5.625 deg, p=2)  512    128   1024 16  4096  8   bf16  
 c1406  2       64 x 128 (1.40625 deg, p=2) 8192  2048  1024 16  4096  8   bf16    random
 d025   1       90 x 180 (0.25 deg, p=8)   16200  4050  1024 16  4096  12  bf16    random
 edm    2       64 x 128                   8192   2048  1024 16  4096  8   bf16    top-k (adaLN)
+gen    2       64 x 128                   8192   2048  1024 8   4096  4   bf16    random (generative
+                                                                                block, Z_c of L tokens)
 =====  ======  =========================  =====  ====  ==  ===  ====  ==  ======  ==========
 
 Token fields stand in for ERA5 (not available): a smooth Gaussian random field
@@ -49,7 +51,7 @@ class Workload:
     n_blocks: int
     keep: float
     dtype: str       # "f32" | "bf16"  (storage type; accumulation is always fp32)
-    kind: str        # "preln" | "adaln"
+    kind: str        # "preln" | "adaln" | "edm" (the generative model's block)
     select: str      # "random" | "topk"
     ell: float       # correlation length of the token field, in tokens
     backward: bool
@@ -78,6 +80,10 @@ WORKLOADS = {
     "c1406": Workload("c1406", 2, 64, 128, 1024, 16, 4096, 8, 0.25, "bf16", "preln", "random", 4.0, True, 2),
     "d025": Workload("d025", 1, 90, 180, 1024, 16, 4096, 12, 0.25, "bf16", "preln", "random", 6.0, True, 3),
     "edm": Workload("edm", 2, 64, 128, 1024, 16, 4096, 8, 0.25, "bf16", "adaln", "topk", 4.0, True, 4),
+    # the generative model's sparse middle stage (App. A.1 EDM table: D = 1024, 8 heads of 128,
+    # split (2, 4, 2)) on the 1.40625 deg token grid: 4 blocks on K = 2048 routed tokens with
+    # cross-attention to all 8192 conditioning tokens
+    "gen": Workload("gen", 2, 64, 128, 1024, 8, 4096, 4, 0.25, "bf16", "edm", "random", 4.0, True, 5),
 }
 
 
@@ -185,6 +191,54 @@ def block_params(w: Workload, n_blocks: int | None = None, randomise_affine: boo
             p[name] = np.asarray(v, dtype=np.float32)
         out.append(p)
     return out
+
+
+EDM_PARAM_NAMES = (
+    "w_film", "b_film", "w_qkv", "b_qkv", "w_o", "b_o",
+    "lnc_w", "lnc_b", "w_q", "b_q", "w_kv", "b_kv", "w_oc", "b_oc", "w_g", "b_g",
+    "ln2_w", "ln2_b", "w_fc1", "b_fc1", "w_fc2", "b_fc2",
+)
+
+
+def edm_block_params(w: Workload, n_blocks: int | None = None, randomise_affine: bool = False,
+                     std: float = 0.02) -> list[dict[str, np.ndarray]]:
+    """Parameters of the generative model's blocks ([out, in] layout, fp32): linear weights
+    N(0, std), biases 0, LayerNorm gamma = 1 and beta = 0 unless ``randomise_affine`` (then
+    biases and beta N(0, 0.05), gamma 1 + N(0, 0.1), so every gradient path carries signal)."""
+    D, F = w.D, w.F
+    nb = w.n_blocks if n_blocks is None else n_blocks
+    shapes = {"w_film": (2 * D, D), "b_film": (2 * D,), "w_qkv": (3 * D, D), "b_qkv": (3 * D,),
+              "w_o": (D, D), "b_o": (D,), "lnc_w": (D,), "lnc_b": (D,), "w_q": (D, D), "b_q": (D,),
+              "w_kv": (2 * D, D), "b_kv": (2 * D,), "w_oc": (D, D), "b_oc": (D,), "w_g": (D, D), "b_g": (D,),
+              "ln2_w": (D,), "ln2_b": (D,), "w_fc1": (F, D), "b_fc1": (F,), "w_fc2": (D, F), "b_fc2": (D,)}
+    out = []
+    for i in range(nb):
+        rng = np.random.default_rng([5000 + w.seed, i])
+        p = {}
+        for name in EDM_PARAM_NAMES:
+            shp = shapes[name]
+            if name.startswith("w_"):
+                v = rng.normal(0.0, std, size=shp)
+            elif name in ("lnc_w", "ln2_w"):
+                v = 1.0 + (rng.normal(0.0, 0.1, size=shp) if randomise_affine else np.zeros(shp))
+            else:
+                v = rng.normal(0.0, 0.05, size=shp) if randomise_affine else np.zeros(shp)
+            p[name] = np.asarray(v, dtype=np.float32)
+        out.append(p)
+    return out
+
+
+def noise_embedding(w: Workload) -> np.ndarray:
+    """Stand-in for the noise embedding e_sigma, one global vector per sample: N(0,1) of shape
+    (B, D) (the embedding MLP of ln(sigma) is not on the path)."""
+    rng = np.random.default_rng([6000 + w.seed])
+    return rng.standard_normal((w.B, w.D), dtype=np.float32)
+
+
+def conditioning_tokens(w: Workload) -> np.ndarray:
+    """Conditioning sequence Z_c (B, L, D): an independent smooth field on the same token grid
+    (the history frames' tokens)."""
+    return token_field(w, 2)
 
 
 def params_to_storage(params: list[dict[str, np.ndarray]], dtype: str) -> list[dict[str, np.ndarray]]:

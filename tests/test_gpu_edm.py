@@ -1,0 +1,178 @@
+"""GPU parity of the generative model's blocks with the asymmetric attention of the sparse
+middle stage (Sec. 3.4 "Integration with Generative Forecasting", Alg. 2 stage 2; App. A.1 EDM
+table): sr_edm_blocks_fwd / _bwd through the C ABI against the fp64 oracle (oracle/edm_block.py)
+on the same seeded inputs -- outputs, input gradients, the gradients of the conditioning tokens
+Z_c and of the noise embedding e (summed over blocks) and every parameter gradient -- at S > L,
+S < L, S = 1, head dims 64 and 128, fp32 and bf16, the full 2 x 2048 x 8192 generative shape, and
+the routed stage (select, gather, blocks, residual-delta scatter and its backward)."""
+import numpy as np
+import pytest
+
+from gpu_helpers import check_pairs
+from oracle import edm_block as oeb
+from oracle import routing as orouting
+from oracle import select as osel
+from oracle.numerics import f64_to_storage, storage_to_f64
+from paper_2607_02829_amd import abi, device, inputs
+
+pytestmark = pytest.mark.gpu
+EPS = 1e-6
+
+
+def _cfg(w, L, nb):
+    return abi.SrConfig(B=w.B, L=L, D=w.D, H=w.H, F=w.F, n_blocks=nb,
+                        dtype=abi.SR_BF16 if w.dtype == "bf16" else abi.SR_F32, kind=abi.SR_BLOCK_PRELN,
+                        ln_eps=EPS, idx_shared=0)
+
+
+def _host(w, S, nb):
+    """Seeded storage inputs: S query tokens, the workload's L conditioning tokens, e, params, dh."""
+    wq = w.with_(Hg=1, Wg=S, seed=w.seed + 100)
+    h = inputs.to_storage(inputs.token_field(wq, 0), w.dtype)
+    zc = inputs.to_storage(inputs.conditioning_tokens(w), w.dtype)
+    e = inputs.to_storage(inputs.noise_embedding(w), w.dtype)
+    params = inputs.params_to_storage(inputs.edm_block_params(w, nb, randomise_affine=True), w.dtype)
+    dh = inputs.to_storage(inputs.upstream_grad(w, rows=S), w.dtype)
+    return h, zc, e, params, dh
+
+
+def _gpu(w, S, nb, h, zc, e, params, dh):
+    import torch
+    cfg = _cfg(w, w.L, nb)
+    dp = device.DeviceEdmParams(params)
+    gr = device.DeviceEdmGrads(w.D, w.F, nb)
+    hd, zd, ed, dhd = (device.to_device(a) for a in (h, zc, e, dh))
+    h_out = torch.empty_like(hd)
+    saved, scratch = device.edm_workspace(cfg, S)
+    abi.sr_edm_blocks_fwd(cfg, S, dp.array, ed, zd, hd, h_out, saved)
+    dh_in = torch.empty_like(dhd)
+    dzc = torch.full((w.B, w.L, w.D), float("nan"), dtype=torch.float32, device="cuda")
+    de = torch.full((w.B, w.D), float("nan"), dtype=torch.float32, device="cuda")
+    abi.sr_edm_blocks_bwd(cfg, S, dp.array, ed, zd, saved, dhd, dh_in, gr.array, dzc, de, scratch)
+    torch.cuda.synchronize()
+    return {"h_out": device.to_host(h_out), "dh_in": device.to_host(dh_in), "dzc": dzc.cpu().numpy(),
+            "de": de.cpu().numpy(), "grads": [{k: v.cpu().numpy() for k, v in g.items()} for g in gr.tensors]}
+
+
+def _oracle(w, h, zc, e, params, dh):
+    """The stack of oracle blocks in fp64; Z_c and e are shared, their gradients summed."""
+    p64 = [{k: storage_to_f64(v) for k, v in p.items()} for p in params]
+    z64, e64 = storage_to_f64(zc), storage_to_f64(e)
+    x = storage_to_f64(h)
+    caches = []
+    for p in p64:
+        x, c = oeb.edm_block_fwd(x, z64, e64, p, w.H, EPS)
+        caches.append(c)
+    g = storage_to_f64(dh)
+    dzc, de, grads = 0.0, 0.0, [None] * len(p64)
+    for i in reversed(range(len(p64))):
+        g, grads[i], dz, dee = oeb.edm_block_bwd(g, p64[i], caches[i])
+        dzc, de = dzc + dz, de + dee
+    return {"h_out": x, "dh_in": g, "dzc": dzc, "de": de, "grads": grads}
+
+
+def _items(gpu, ref):
+    items = [("h_out", storage_to_f64(gpu["h_out"]), ref["h_out"]),
+             ("dh_in", storage_to_f64(gpu["dh_in"]), ref["dh_in"]),
+             ("dzc", gpu["dzc"], ref["dzc"]), ("de", gpu["de"], ref["de"])]
+    for i, (gg, rg) in enumerate(zip(gpu["grads"], ref["grads"])):
+        for name in abi.EDM_PARAM_FIELDS:
+            items.append((f"b{i}.{name}", gg[name], rg[name]))
+    return items
+
+
+CASES = {
+    # name: (workload with L conditioning tokens, S query tokens, blocks)
+    "bf16_hd64_S<L": (inputs.small("edm_a", Hg=10, Wg=13, H=4, kind="edm"), 50, 2),
+    "bf16_hd64_S>L": (inputs.small("edm_b", Hg=1, Wg=37, H=4, kind="edm"), 130, 2),
+    "bf16_hd128_S<L": (inputs.small("edm_c", Hg=12, Wg=25, H=2, kind="edm"), 77, 2),
+    "bf16_hd128_S=1": (inputs.small("edm_d", Hg=5, Wg=13, H=2, kind="edm"), 1, 1),
+    "bf16_hd128_L=1": (inputs.small("edm_e", Hg=1, Wg=1, H=2, kind="edm"), 70, 1),
+    "f32_hd64": (inputs.small("edm_f", Hg=7, Wg=10, D=128, H=2, F=256, dtype="f32", kind="edm"), 33, 2),
+    "f32_hd128_S>L": (inputs.small("edm_g", Hg=3, Wg=3, D=256, H=2, F=512, dtype="f32", kind="edm"), 20, 1),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_edm_blocks_match_oracle(case):
+    w, S, nb = CASES[case]
+    print(f"[edm {case}] B={w.B} S={S} L={w.L} D={w.D} H={w.H} F={w.F} blocks={nb} {w.dtype}", flush=True)
+    h, zc, e, params, dh = _host(w, S, nb)
+    gpu = _gpu(w, S, nb, h, zc, e, params, dh)
+    ref = _oracle(w, h, zc, e, params, dh)
+    check_pairs(_items(gpu, ref), w.dtype, f"[edm {case}]")
+
+
+def test_edm_block_at_the_generative_shape():
+    # one block of the generative model (D = 1024, 8 heads of 128, F = 4096) on K = 2048 routed
+    # tokens per sample against all L = 8192 conditioning tokens, B = 2
+    w = inputs.WORKLOADS["gen"]
+    S = w.K
+    print(f"[edm gen] B={w.B} S={S} L={w.L} D={w.D} H={w.H}: GPU", flush=True)
+    h, zc, e, params, dh = _host(w, S, 1)
+    gpu = _gpu(w, S, 1, h, zc, e, params, dh)
+    print("[edm gen] oracle", flush=True)
+    ref = _oracle(w, h, zc, e, params, dh)
+    check_pairs(_items(gpu, ref), w.dtype, "[edm gen]")
+
+
+def test_edm_routed_stage():
+    # Alg. 2 stage 2: K = floor(rL) random tokens of Z_x are gathered, run through the blocks
+    # (cross-attention to all of Z_c), and their residual delta is scattered back; the backward
+    # is the same routing around the blocks' vector-Jacobian product
+    import torch
+    w = inputs.small("edm_route", Hg=12, Wg=20, H=2, kind="edm")
+    nb, K = 2, w.K
+    x = inputs.to_storage(inputs.token_field(w, 0), w.dtype)
+    zc = inputs.to_storage(inputs.conditioning_tokens(w), w.dtype)
+    e = inputs.to_storage(inputs.noise_embedding(w), w.dtype)
+    params = inputs.params_to_storage(inputs.edm_block_params(w, nb, randomise_affine=True), w.dtype)
+    g = inputs.to_storage(inputs.upstream_grad(w), w.dtype)
+    cfg = _cfg(w, w.L, nb)
+    xd, zd, ed, gd = (device.to_device(a) for a in (x, zc, e, g))
+    dp = device.DeviceEdmParams(params)
+    gr = device.DeviceEdmGrads(w.D, w.F, nb)
+    idx = torch.empty((w.B, K), dtype=torch.int32, device="cuda")
+    abi.sr_select_indices(cfg, K, abi.SR_SEL_RANDOM, 9, 2, None, None, idx)
+    h0 = torch.empty((w.B, K, w.D), dtype=xd.dtype, device="cuda")
+    h, gh, dh = torch.empty_like(h0), torch.empty_like(h0), torch.empty_like(h0)
+    saved, scratch = device.edm_workspace(cfg, K)
+    abi.sr_gather(cfg, K, xd, idx, h0)
+    abi.sr_edm_blocks_fwd(cfg, K, dp.array, ed, zd, h0, h, saved)
+    abi.sr_scatter_delta(cfg, K, xd, h, h0, idx)
+    dzc = torch.empty((w.B, w.L, w.D), dtype=torch.float32, device="cuda")
+    de = torch.empty((w.B, w.D), dtype=torch.float32, device="cuda")
+    abi.sr_gather(cfg, K, gd, idx, gh)
+    abi.sr_edm_blocks_bwd(cfg, K, dp.array, ed, zd, saved, gh, dh, gr.array, dzc, de, scratch)
+    abi.sr_scatter_delta(cfg, K, gd, dh, None, idx)
+    torch.cuda.synchronize()
+    want_idx = osel.select_random(w.B, w.L, K, 9, 2)
+    assert np.array_equal(idx.cpu().numpy(), want_idx)
+    # oracle: gather, the blocks in fp64, one rounding, residual-delta scatter; backward likewise
+    oh0 = orouting.gather(x, want_idx)
+    ref = _oracle(w, oh0, zc, e, params, orouting.gather(g, want_idx))
+    x_ref = orouting.scatter_delta(x, f64_to_storage(ref["h_out"], w.dtype), oh0, want_idx)
+    dx0_ref = orouting.scatter_delta(g, f64_to_storage(ref["dh_in"], w.dtype), orouting.gather(g, want_idx), want_idx)
+    got_x, got_g = device.to_host(xd), device.to_host(gd)
+    for b in range(w.B):   # tokens never routed keep x0 (and g) bit for bit
+        mask = np.ones(w.L, bool); mask[want_idx[b]] = False
+        assert np.array_equal(got_x[b, mask], x[b, mask]) and np.array_equal(got_g[b, mask], g[b, mask])
+    items = [("x'", storage_to_f64(got_x), storage_to_f64(x_ref)), ("dx0", storage_to_f64(got_g),
+                                                                    storage_to_f64(dx0_ref)),
+             ("dzc", dzc.cpu().numpy(), ref["dzc"]), ("de", de.cpu().numpy(), ref["de"])]
+    for i, gg in enumerate(gr.tensors):
+        for name in abi.EDM_PARAM_FIELDS:
+            items.append((f"b{i}.{name}", gg[name].cpu().numpy(), ref["grads"][i][name]))
+    check_pairs(items, w.dtype, "[edm routed]")
+
+
+def test_edm_blocks_bitwise_repeatable():
+    w, S, nb = CASES["bf16_hd128_S<L"]
+    h, zc, e, params, dh = _host(w, S, nb)
+    a = _gpu(w, S, nb, h, zc, e, params, dh)
+    b = _gpu(w, S, nb, h, zc, e, params, dh)
+    for k in ("h_out", "dh_in", "dzc", "de"):
+        assert np.array_equal(np.ascontiguousarray(a[k]).view(np.uint8), np.ascontiguousarray(b[k]).view(np.uint8)), k
+    for ga, gb in zip(a["grads"], b["grads"]):
+        for k in ga:
+            assert np.array_equal(ga[k].view(np.uint8), gb[k].view(np.uint8)), k
