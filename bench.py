@@ -142,6 +142,132 @@ class TrunkStep:
         self.trunk.backward(self.g3)
 
 
+def block_flops(w, S: int, n_blocks: int | None = None) -> float:
+    """Algorithmic FLOPs of the pre-LN / adaLN blocks' forward + backward on S tokens per sample
+    (3 x the forward's M (24 D^2 + 4 S D) at F = 4D; no attention recompute counted)."""
+    nb = w.n_blocks if n_blocks is None else n_blocks
+    M = w.B * S
+    return 3.0 * nb * (2 * M * (3 * w.D * w.D + w.D * w.D + 2 * w.D * w.F) + 4.0 * w.B * S * S * w.D)
+
+
+def workload_summary(name: str, steps: int = 5, dense_steps: int = 2) -> dict:
+    """Routed and dense step of another workload (fused routed calls as in the main line):
+    ms per step, routed tokens/s, speedup over dense, and the stack's MFMA fraction."""
+    import torch
+    from paper_2607_02829_amd import inputs
+    w = inputs.WORKLOADS[name]
+    sp = Step(w, dense=False)
+    sp.run(0)
+    torch.cuda.synchronize()
+    ms, _, _ = time_steps(sp, steps, 2, start=1)
+    del sp
+    torch.cuda.empty_cache()
+    dn = Step(w, dense=True)
+    dn.run(0)
+    torch.cuda.synchronize()
+    dms, _, _ = time_steps(dn, dense_steps, 1, start=1)
+    del dn
+    torch.cuda.empty_cache()
+    rec = {"config": f"B={w.B}, {w.Hg}x{w.Wg} tokens (L={w.L}), K={w.K}, D={w.D}, H={w.H}, F={w.F}, "
+                     f"{w.n_blocks} {w.kind} blocks, {w.select} selection, {w.dtype}",
+           "ms_per_step": round(ms, 3), "routed_tokens_per_s": round(w.B * w.K / (ms * 1e-3), 1),
+           "dense_ms_per_step": round(dms, 3), "speedup_vs_dense": round(dms / ms, 3),
+           "stack_mfma_frac": round(block_flops(w, w.K) / (ms * 1e-3) / PEAK_BF16_FLOPS, 4),
+           "dense_stack_mfma_frac": round(block_flops(w, w.L) / (dms * 1e-3) / PEAK_BF16_FLOPS, 4)}
+    log(f"workload {name}: {ms:.2f} ms routed, {dms:.2f} ms dense, speedup {rec['speedup_vs_dense']}")
+    return rec
+
+
+class GenStep:
+    """The generative model's sparse middle stage (Alg. 2 stage 2): select K tokens of Z_x, gather,
+    the blocks (FiLM, self-attention on the K tokens, sigma-gated cross-attention to all L
+    conditioning tokens, MLP), residual-delta scatter, and the backward through the same routing;
+    or (dense) the same blocks on all L tokens of Z_x."""
+
+    def __init__(self, w, dense: bool, seed: int = 42):
+        import torch
+        from paper_2607_02829_amd import abi, device, inputs
+        self.abi, self.w, self.dense, self.seed = abi, w, dense, seed
+        self.cfg = abi.SrConfig(B=w.B, L=w.L, D=w.D, H=w.H, F=w.F, n_blocks=w.n_blocks, dtype=abi.SR_BF16,
+                                kind=abi.SR_BLOCK_PRELN, ln_eps=1e-6, idx_shared=0)
+        self.K = w.L if dense else w.K
+        st = lambda a: device.to_device(inputs.to_storage(a, w.dtype))
+        self.x, self.zc, self.e = st(inputs.token_field(w, 0)), st(inputs.conditioning_tokens(w)), \
+            st(inputs.noise_embedding(w))
+        self.g = st(inputs.upstream_grad(w))
+        self.params = device.DeviceEdmParams(inputs.params_to_storage(inputs.edm_block_params(w), w.dtype))
+        self.grads = device.DeviceEdmGrads(w.D, w.F, w.n_blocks)
+        self.dzc = torch.empty((w.B, w.L, w.D), dtype=torch.float32, device="cuda")
+        self.de = torch.empty((w.B, w.D), dtype=torch.float32, device="cuda")
+        self.saved, self.scratch = device.edm_workspace(self.cfg, self.K)
+        if dense:
+            self.x_out, self.dx = torch.empty_like(self.x), torch.empty_like(self.x)
+        else:
+            self.idx = torch.empty((w.B, self.K), dtype=torch.int32, device="cuda")
+            self.h0 = torch.empty((w.B, self.K, w.D), dtype=self.x.dtype, device="cuda")
+            self.h, self.gh, self.dh = torch.empty_like(self.h0), torch.empty_like(self.h0), torch.empty_like(self.h0)
+
+    def run(self, step: int):
+        a, c, K, p, g = self.abi, self.cfg, self.K, self.params.array, self.grads.array
+        if self.dense:
+            a.sr_edm_blocks_fwd(c, K, p, self.e, self.zc, self.x, self.x_out, self.saved)
+            a.sr_edm_blocks_bwd(c, K, p, self.e, self.zc, self.saved, self.g, self.dx, g, self.dzc, self.de,
+                                self.scratch)
+            return
+        a.sr_select_indices(c, K, a.SR_SEL_RANDOM, self.seed, step, None, None, self.idx)
+        a.sr_gather(c, K, self.x, self.idx, self.h0)
+        a.sr_edm_blocks_fwd(c, K, p, self.e, self.zc, self.h0, self.h, self.saved)
+        a.sr_scatter_delta(c, K, self.x, self.h, self.h0, self.idx)
+        a.sr_gather(c, K, self.g, self.idx, self.gh)
+        a.sr_edm_blocks_bwd(c, K, p, self.e, self.zc, self.saved, self.gh, self.dh, g, self.dzc, self.de,
+                            self.scratch)
+        a.sr_scatter_delta(c, K, self.g, self.dh, None, self.idx)
+
+
+def edm_flops(w, S: int) -> float:
+    """Algorithmic FLOPs of the generative blocks' forward + backward on S query tokens with L
+    conditioning tokens: the S-row GEMMs (QKV, O, Q, O_c, FC1, FC2), the K/V projection of the L
+    conditioning rows, self-attention over S and cross-attention S x L; 3 x the forward."""
+    D, F = w.D, w.F
+    M, Mc = w.B * S, w.B * w.L
+    fwd = 2.0 * M * (3 * D * D + 3 * D * D + 2 * D * F) + 2.0 * Mc * 2 * D * D \
+        + 4.0 * w.B * S * S * D + 4.0 * w.B * S * w.L * D
+    return 3.0 * w.n_blocks * fwd
+
+
+def generative_stage(steps: int = 5, dense_steps: int = 3) -> dict:
+    """The generative model's sparse middle stage against its dense blocks at the 1.40625 deg token
+    grid (B = 2, L = 8192, K = 2048, D = 1024, 8 heads of 128, F = 4096, the 4 middle blocks of the
+    (2, 4, 2) split): ms per fwd + bwd step, speedup, MFMA fraction, peak memory."""
+    import torch
+    from paper_2607_02829_amd import inputs
+    w = inputs.WORKLOADS["gen"]
+    out = {"config": f"B={w.B}, {w.Hg}x{w.Wg} tokens (L={w.L}), K={w.K}, D={w.D}, {w.H} heads of {w.hd}, F={w.F}, "
+                     f"{w.n_blocks} generative blocks (FiLM, self-attention, sigma-gated cross-attention to all "
+                     f"L conditioning tokens, MLP), random selection, bf16"}
+    for dense in (False, True):
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        st = GenStep(w, dense)
+        st.run(0)
+        torch.cuda.synchronize()
+        peak = torch.cuda.max_memory_allocated() - base
+        ms, _, _ = time_steps(st, dense_steps if dense else steps, 1, start=1)
+        finite = bool(torch.isfinite((st.dx if dense else st.g).float()).all().item())
+        del st
+        torch.cuda.empty_cache()
+        S = w.L if dense else w.K
+        out["dense" if dense else "sparse"] = {
+            "ms_per_step": round(ms, 3), "peak_bytes": int(peak),
+            "mfma_frac": round(edm_flops(w, S) / (ms * 1e-3) / PEAK_BF16_FLOPS, 4), "outputs_finite": finite}
+    out["routed_tokens_per_s"] = round(w.B * w.K / (out["sparse"]["ms_per_step"] * 1e-3), 1)
+    out["speedup_vs_dense"] = round(out["dense"]["ms_per_step"] / out["sparse"]["ms_per_step"], 3)
+    out["peak_ratio"] = round(out["dense"]["peak_bytes"] / out["sparse"]["peak_bytes"], 3)
+    log(f"generative stage: {out['sparse']['ms_per_step']} ms sparse, {out['dense']['ms_per_step']} ms dense, "
+        f"speedup {out['speedup_vs_dense']}")
+    return out
+
+
 def trunk_sweep(w, dense_ms: float | None, steps: int = 3) -> dict:
     """The trunk over the keep ratios of the paper's keep-ratio ablation at the (2, n-4, 2)
     split, and over the block splits of its split ablation at r = 0.25 (Sec. 4.4, "Effect of
@@ -433,8 +559,12 @@ def main():
     ap.add_argument("--dense-steps", type=int, default=3, help="timed steps of the dense keep=100%% mode (0: skip)")
     ap.add_argument("--trunk-steps", type=int, default=3,
                     help="timed steps of the whole (2, n-4, 2) trunk, pre-LN workloads (0: skip)")
-    ap.add_argument("--trunk-sweep", action="store_true",
-                    help="also time the trunk over keep ratios 0.10-1.0 and block splits (pre-LN workloads)")
+    ap.add_argument("--no-trunk-sweep", action="store_true",
+                    help="skip the trunk over keep ratios 0.10-1.0 and block splits (pre-LN workloads)")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the routed and dense steps of the other grids (5.625, 1.40625 deg, diffusion)")
+    ap.add_argument("--no-generative", action="store_true",
+                    help="skip the generative model's sparse middle stage against its dense blocks")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routing-sweep", action="store_true", help="skip the gather/scatter bandwidth sweep")
     ap.add_argument("--breakdown", action="store_true", help="print the per-kernel breakdown to stderr")
@@ -516,8 +646,7 @@ def main():
         achieved_u, peak_u = achieved / 1e9, peak / 1e9
 
     # whole-stack MFMA fraction: algorithmic block FLOPs per step over step time
-    M = w.B * w.K
-    blk_flops = 3 * w.n_blocks * (2 * M * (3 * w.D * w.D + w.D * w.D + 2 * w.D * w.F) + 4 * w.B * w.K * w.K * w.D)
+    blk_flops = block_flops(w, w.K)
 
     # ---------------------------------------------------------------- dense keep=100% mode
     dense = None
@@ -558,7 +687,7 @@ def main():
                  "speedup_vs_dense": round(dense["ms_per_step"] / tms, 3) if dense else None,
                  "eq_speedup_estimate": round(w.n_blocks / (n1 + n2 * w.keep ** 2 + n3), 3),
                  "outputs_finite": finite_trunk}
-        if args.trunk_sweep:
+        if not args.no_trunk_sweep:
             trunk["sweep"] = trunk_sweep(w, dense["ms_per_step"] if dense else None)
 
     # routing kernels: in-step launch times (per-kernel breakdown) and a cache-evicting size sweep
@@ -573,6 +702,10 @@ def main():
     if w.dtype == "bf16" and not args.no_routing_sweep:
         routing["sweep"] = routing_sweep(w.D)
 
+    workloads = None
+    if not args.no_workloads:
+        workloads = {n: workload_summary(n) for n in ("b5625", "c1406", "edm") if n != w.name}
+    generative = None if args.no_generative else generative_stage()
     xattn = cross_attention_timing() if args.cross_attention else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(w)
 
@@ -601,6 +734,8 @@ def main():
         "dense": dense,
         "speedup_vs_dense": round(dense["ms_per_step"] / ms_step, 3) if dense else None,
         "trunk": trunk,
+        "workloads": workloads,
+        "generative": generative,
         "graph": graph,
         "cross_attention": xattn,
         "peak_bytes": {"sparse": int(sparse_peak), "dense": dense["peak_bytes"] if dense else None,
