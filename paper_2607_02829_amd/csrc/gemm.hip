@@ -23,7 +23,7 @@
 //   EPI_BIAS_ACT  out_act = Ta(v + bias)                           (QKV)
 //   EPI_RESID     t = v + bias; [adaLN: a_save = Ta(t); t *= gate_b]
 //                 out_f32 = resid + t; [out_st = T(out_f32)]       (O-proj, FC2)
-//   EPI_GELU      z = v + bias; out_act = Ta(z); out_act2 = Ta(GELU(z))   (FC1)
+//   EPI_GELU      z = Ta(v + bias); out_act = z; out_act2 = Ta(GELU(z))    (FC1)
 //   EPI_DGELU     out_act = Ta(v * GELU'(z_in))                     (FC2 dX)
 //   EPI_ACT       out_act = Ta(v)                                   (O-proj dX)
 //   EPI_F32       out_f32[split] = v                                (dX for LN, dW partials)
@@ -93,9 +93,9 @@ SR_DEV void epilogue(const EpiArgs& e, int m, int n, float v) {
       *xp = from_f32<T>(__fadd_rn(x0, __fsub_rn(to_f32<T>(from_f32<T>(r)), x0)));
     }
   } else if constexpr (EPI == EPI_GELU) {
-    const float z = v + to_f32<T>(((const T*)e.bias)[n]);
-    ((Ta*)e.out_act)[o] = from_f32<Ta>(z);
-    ((Ta*)e.out_act2)[o] = from_f32<Ta>(gelu_f(z));
+    const Ta z = from_f32<Ta>(v + to_f32<T>(((const T*)e.bias)[n]));
+    ((Ta*)e.out_act)[o] = z;
+    ((Ta*)e.out_act2)[o] = from_f32<Ta>(gelu_f(to_f32<Ta>(z)));   // of the stored z (recomputed bit for bit)
   } else if constexpr (EPI == EPI_DGELU) {
     const float z = to_f32<Ta>(((const Ta*)e.z_in)[o]);
     ((Ta*)e.out_act)[o] = from_f32<Ta>(v * gelu_grad_f(z));
@@ -187,11 +187,13 @@ SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in,
       *reinterpret_cast<i32x2*>(xp) = pack4(xn);
     }
   } else if constexpr (EPI == EPI_GELU) {
-    const f32x4 z = v + b;
+    // GELU of the stored (rounded) pre-activation, so the backward recomputes it bit for bit
+    const i32x2 zb = pack4(v + b);
+    const f32x4 z = unpack4(zb);
     f32x4 gz;
 #pragma unroll
     for (int q = 0; q < 4; ++q) gz[q] = gelu_f(z[q]);
-    *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(z);
+    *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = zb;
     *reinterpret_cast<i32x2*>((bf16_t*)e.out_act2 + o) = pack4(gz);
   } else if constexpr (EPI == EPI_DGELU) {
     const bf16_t* ze = reinterpret_cast<const bf16_t*>(&in.z);
@@ -784,6 +786,45 @@ hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_
     case EPI_DO: return g.use_mfma ? run_mfma<EPI_DO, bf16_t, bf16_t>(g, ep, st) : hipErrorInvalidValue;
   }
   return hipErrorInvalidValue;
+}
+
+// gz = Ta(GELU(z)) from the stored FC1 pre-activation: the FC1 epilogue's values, recomputed for
+// the FC2 weight gradient instead of being kept from the forward.  Eight elements per thread.
+template <typename Ta>
+__global__ __launch_bounds__(256) void gelu_kernel(const Ta* __restrict__ z, Ta* __restrict__ gz, size_t n8) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (size_t)gridDim.x * 256) {
+    if constexpr (sizeof(Ta) == 2) {
+      const i32x4 w = reinterpret_cast<const i32x4*>(z)[i];
+      i32x4 out;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        i32x2 zb;
+        zb[0] = w[2 * h];
+        zb[1] = w[2 * h + 1];
+        const f32x4 zf = unpack4(zb);
+        f32x4 g;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) g[q] = gelu_f(zf[q]);
+        const i32x2 gb = pack4(g);
+        out[2 * h] = gb[0];
+        out[2 * h + 1] = gb[1];
+      }
+      reinterpret_cast<i32x4*>(gz)[i] = out;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) gz[8 * i + q] = gelu_f(z[8 * i + q]);
+    }
+  }
+}
+
+hipError_t launch_gelu(int dtype, const void* z, void* gz, size_t n, hipStream_t st) {
+  const size_t n8 = n / 8;   // n is a multiple of 64 (F % 64 == 0)
+  const dim3 g((unsigned)std::min<size_t>((n8 + 255) / 256, 4096));
+  if (dtype == kBF16)
+    hipLaunchKernelGGL(gelu_kernel<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)z, (bf16_t*)gz, n8);
+  else
+    hipLaunchKernelGGL(gelu_kernel<float>, g, dim3(256), 0, st, (const float*)z, (float*)gz, n8);
+  return hipGetLastError();
 }
 
 void weight_grad_scratch(int M, int N, int K, size_t* part_floats, size_t* dbpart_floats) {

@@ -56,12 +56,20 @@ template <int V> SR_DEV void stv(bf16_t* p, const float* v) {
 // x: fp32 [M, D]; mod (adaLN): fp32 [B, 6D] with shift at mod_off, scale at mod_off + D.
 // One row per wave.  NJC > 0: every lane holds exactly NJC groups of V columns (D = 64 V NJC,
 // all loads unconditional and issued together); NJC = 0: any D <= 64 V kMaxPerLane.
-template <typename T, typename Ta, int V, int NJC>
+// GATHER: the input row is token i = gidx[(gshared ? 0 : b) * S + s] of sample b of the token
+// sequence gsrc [B, gL, D] (storage type), for row m = b * S + s; its fp32 values are also
+// written to xcopy[m] (the residual stream the block keeps): the gather of the routed rows and
+// the first LayerNorm in one pass, with the values and arithmetic of the separate steps.
+// APPLY: mean and rstd are read from mean_out / rstd_out (the forward's statistics) instead of
+// computed, and nothing else is written but y: the LayerNorm output recomputed bit for bit.
+template <typename T, typename Ta, int V, int NJC, bool GATHER = false, bool APPLY = false>
 __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x, const T* __restrict__ gamma,
                                                      const T* __restrict__ beta, const float* __restrict__ mod,
                                                      int mod_off, int M, int S, int D, float eps,
                                                      Ta* __restrict__ y, float* __restrict__ mean_out,
-                                                     float* __restrict__ rstd_out) {
+                                                     float* __restrict__ rstd_out, const T* __restrict__ gsrc = nullptr,
+                                                     const int32_t* __restrict__ gidx = nullptr, int gL = 0,
+                                                     int gshared = 0, float* __restrict__ xcopy = nullptr) {
   constexpr int NJ = NJC > 0 ? NJC : kMaxPerLane / V;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -69,13 +77,19 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
   const int n = NJC > 0 ? NJC : D / (64 * V);
   const float* xr = x + (size_t)row * D;
   const int b = row / S;
+  const T* gr = nullptr;
+  if constexpr (GATHER) {
+    const int i = gidx[(size_t)(gshared ? 0 : b) * S + (row - b * S)];
+    gr = gsrc + ((size_t)b * gL + i) * D;
+  }
   const float* shift = mod ? mod + (size_t)b * 6 * D + mod_off : nullptr;
   float v[NJ][V], w[NJ][V], bb[NJ][V];
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
     if (j < n) {
       const int c = col_of<V>(lane, j);
-      ldv<V>(xr + c, v[j]);
+      if constexpr (GATHER) ldv<V>(gr + c, v[j]);
+      else ldv<V>(xr + c, v[j]);
       if (mod) {
         ldv<V>(shift + D + c, w[j]);
         ldv<V>(shift + c, bb[j]);
@@ -84,20 +98,31 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
         ldv<V>(beta + c, bb[j]);
       }
     }
-  float s = 0.f;
+  if constexpr (GATHER) {
 #pragma unroll
-  for (int j = 0; j < NJ; ++j)
-    if (j < n)
+    for (int j = 0; j < NJ; ++j)
+      if (j < n) stv<V>(xcopy + (size_t)row * D + col_of<V>(lane, j), v[j]);
+  }
+  float mean, rstd;
+  if constexpr (APPLY) {
+    mean = mean_out[row];
+    rstd = rstd_out[row];
+  } else {
+    float s = 0.f;
 #pragma unroll
-      for (int e = 0; e < V; ++e) s += v[j][e];
-  const float mean = wave_sum(s) / (float)D;
-  float q = 0.f;
+    for (int j = 0; j < NJ; ++j)
+      if (j < n)
 #pragma unroll
-  for (int j = 0; j < NJ; ++j)
-    if (j < n)
+        for (int e = 0; e < V; ++e) s += v[j][e];
+    mean = wave_sum(s) / (float)D;
+    float q = 0.f;
 #pragma unroll
-      for (int e = 0; e < V; ++e) { const float d = v[j][e] - mean; q += d * d; }
-  const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+    for (int j = 0; j < NJ; ++j)
+      if (j < n)
+#pragma unroll
+        for (int e = 0; e < V; ++e) { const float d = v[j][e] - mean; q += d * d; }
+    rstd = 1.0f / sqrtf(wave_sum(q) / (float)D + eps);
+  }
   Ta* yr = y + (size_t)row * D;
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
@@ -107,7 +132,9 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
       for (int e = 0; e < V; ++e) o[e] = (v[j][e] - mean) * rstd * (mod ? w[j][e] + 1.0f : w[j][e]) + bb[j][e];
       stv<V>(yr + col_of<V>(lane, j), o);
     }
-  if (lane == 0) { mean_out[row] = mean; rstd_out[row] = rstd; }
+  if constexpr (!APPLY) {
+    if (lane == 0) { mean_out[row] = mean; rstd_out[row] = rstd; }
+  }
 }
 
 // Backward.  du: fp32 [M, D] gradient of the LayerNorm output (after modulation);
@@ -395,6 +422,48 @@ hipError_t launch_ln_fwd(int dtype, const float* x, const void* gamma, const voi
   if (dtype == kBF16) { SR_LNF_T(bf16_t); } else { SR_LNF_T(float); }
 #undef SR_LNF_T
 #undef SR_LNF
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_fwd_gather(int dtype, const void* xsrc, const int32_t* idx, int L, int shared, float* xcopy,
+                                const void* gamma, const void* beta, const float* mod, int mod_off, int M, int S,
+                                int D, float eps, void* y, float* mean, float* rstd, hipStream_t st) {
+#define SR_LNG(T, V, NJC)                                                                                         \
+  hipLaunchKernelGGL((ln_fwd_kernel<T, T, V, NJC, true>), grid1d(M, 4), dim3(256), 0, st, (const float*)nullptr, \
+                     (const T*)gamma, (const T*)beta, mod, mod_off, M, S, D, eps, (T*)y, mean, rstd,              \
+                     (const T*)xsrc, idx, L, shared, xcopy)
+#define SR_LNG_T(T)                                      \
+  switch (D % 256 == 0 ? D / 256 : 0) {                  \
+    case 1: SR_LNG(T, 4, 1); break;                      \
+    case 2: SR_LNG(T, 4, 2); break;                      \
+    case 4: SR_LNG(T, 4, 4); break;                      \
+    case 8: SR_LNG(T, 4, 8); break;                      \
+    default: if (D % 256 == 0) SR_LNG(T, 4, 0); else SR_LNG(T, 1, 0); \
+  }
+  if (dtype == kBF16) { SR_LNG_T(bf16_t); } else { SR_LNG_T(float); }
+#undef SR_LNG_T
+#undef SR_LNG
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_apply(int dtype, const float* x, const void* gamma, const void* beta, const float* mod,
+                           int mod_off, int M, int S, int D, const float* mean, const float* rstd, void* y,
+                           hipStream_t st) {
+#define SR_LNA(T, V, NJC)                                                                                       \
+  hipLaunchKernelGGL((ln_fwd_kernel<T, T, V, NJC, false, true>), grid1d(M, 4), dim3(256), 0, st, x,            \
+                     (const T*)gamma, (const T*)beta, mod, mod_off, M, S, D, 0.0f, (T*)y, const_cast<float*>(mean), \
+                     const_cast<float*>(rstd), (const T*)nullptr, (const int32_t*)nullptr, 0, 0, (float*)nullptr)
+#define SR_LNA_T(T)                                      \
+  switch (D % 256 == 0 ? D / 256 : 0) {                  \
+    case 1: SR_LNA(T, 4, 1); break;                      \
+    case 2: SR_LNA(T, 4, 2); break;                      \
+    case 4: SR_LNA(T, 4, 4); break;                      \
+    case 8: SR_LNA(T, 4, 8); break;                      \
+    default: if (D % 256 == 0) SR_LNA(T, 4, 0); else SR_LNA(T, 1, 0); \
+  }
+  if (dtype == kBF16) { SR_LNA_T(bf16_t); } else { SR_LNA_T(float); }
+#undef SR_LNA_T
+#undef SR_LNA
   return hipGetLastError();
 }
 

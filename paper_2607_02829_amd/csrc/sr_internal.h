@@ -92,6 +92,18 @@ hipError_t launch_scatter_delta(int dtype, int B, int L, int K, int D, void* x, 
 
 hipError_t launch_ln_fwd(int dtype, const float* x, const void* gamma, const void* beta, const float* mod, int mod_off,
                          int M, int S, int D, float eps, void* y, float* mean, float* rstd, hipStream_t st);
+// ln_fwd on the routed rows x[b, idx[b, s]] of the token sequence xsrc [B, L, D] (storage type),
+// also writing their fp32 values to xcopy [B*S, D].
+hipError_t launch_ln_fwd_gather(int dtype, const void* xsrc, const int32_t* idx, int L, int shared, float* xcopy,
+                                const void* gamma, const void* beta, const float* mod, int mod_off, int M, int S,
+                                int D, float eps, void* y, float* mean, float* rstd, hipStream_t st);
+// The LayerNorm output from the forward's saved statistics, bit for bit the ln_fwd result.
+hipError_t launch_ln_apply(int dtype, const float* x, const void* gamma, const void* beta, const float* mod,
+                           int mod_off, int M, int S, int D, const float* mean, const float* rstd, void* y,
+                           hipStream_t st);
+// gz = GELU(z) of the stored FC1 pre-activation (n elements, a multiple of 8), bit for bit the
+// FC1 epilogue's second output.
+hipError_t launch_gelu(int dtype, const void* z, void* gz, size_t n, hipStream_t st);
 int ln_bwd_chunks(int S);
 hipError_t launch_ln_bwd(int dtype, const float* du, const float* x, const float* mean, const float* rstd,
                          const void* gamma, const float* mod, int mod_off, const float* dres, int B, int S, int D,

@@ -3,7 +3,8 @@
 //
 // Forward, per block (pre-LN; adaLN replaces the LN affine by the per-sample
 // modulation and gates the two residual branches):
-//   u1 = LN1(h)                      rowops  ln_fwd
+//   u1 = LN1(h)                      rowops  ln_fwd (routed calls: the first block's reads the
+//                                                    rows x[idx] itself, ln_fwd_gather)
 //   qkv = u1 W_qkv^T + b_qkv         gemm    EPI_BIAS_ACT
 //   O, lse = attention(qkv)          attention fwd
 //   h1 = h + O W_o^T + b_o           gemm    EPI_RESID
@@ -68,6 +69,10 @@ GemmDesc desc(const Dims& d, const void* A, bool ak, long long lda, size_t abyte
 
 }  // namespace
 
+// Per block: what the backward reads.  The LayerNorm outputs u1, u2 and GELU(z) are forward
+// temporaries shared by all blocks (the backward recomputes them from the fp32 residual stream
+// and the saved statistics, and from z, bit for bit), 12 of the 36.9 KB per token and block at
+// D = 1024.
 size_t layout_saved(const Dims& d, char* base, BlockSaved* out) {
   Carver c(base);
   const size_t M = d.M, D = d.D, F = d.F, e = d.elt;
@@ -76,16 +81,13 @@ size_t layout_saved(const Dims& d, char* base, BlockSaved* out) {
     s.hin = c.take<float>(M * D * 4);
     s.mean1 = c.take<float>(M * 4);
     s.rstd1 = c.take<float>(M * 4);
-    s.u1 = c.take<void>(M * D * e);
     s.qkv = c.take<void>(M * 3 * D * e);
     s.O = c.take<void>(M * D * e);
     s.lse = c.take<float>((size_t)d.B * d.H * d.S * 4);
     s.h1 = c.take<float>(M * D * 4);
     s.mean2 = c.take<float>(M * 4);
     s.rstd2 = c.take<float>(M * 4);
-    s.u2 = c.take<void>(M * D * e);
     s.z = c.take<void>(M * F * e);
-    s.gz = c.take<void>(M * F * e);
     if (d.kind == SR_BLOCK_ADALN) {
       s.mod = c.take<float>((size_t)d.B * 6 * D * 4);
       s.a_out = c.take<void>(M * D * e);
@@ -93,6 +95,10 @@ size_t layout_saved(const Dims& d, char* base, BlockSaved* out) {
     }
     if (out) out[i] = s;
   }
+  void* u_tmp = c.take<void>(M * D * e);
+  void* gz_tmp = c.take<void>(M * F * e);
+  if (out)
+    for (int i = 0; i < d.nb; ++i) { out[i].u1 = out[i].u2 = u_tmp; out[i].gz = gz_tmp; }
   return c.off;
 }
 
@@ -128,6 +134,9 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   for (int k = 0; k < 2; ++k) s.dz[k] = c.take<void>(M * F * e);
   s.dO = c.take<void>(M * D * e);
   for (int k = 0; k < 2; ++k) s.dqkv[k] = c.take<void>(M * 3 * D * e);
+  // recomputed operands of the weight-gradient GEMMs (written and read on the second stream)
+  s.u_rc = c.take<void>(M * D * e);
+  s.gz_rc = c.take<void>(M * F * e);
   if (out) *out = s;
   return c.off;
 }
@@ -143,10 +152,7 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
   const bool ada = d.kind == SR_BLOCK_ADALN;
   hipError_t err = hipSuccess;
   auto run = [&]() -> hipError_t {
-    if (rt) {
-      ProfScope ps("gather_f32", 0, (double)M * D * (e + 4) + 4.0 * M, st);
-      SR_TRY(launch_gather_rows_f32(d.dtype, d.B, d.L, S, D, rt->x, rt->idx, sv[0].hin, nullptr, rt->shared, st));
-    } else {
+    if (!rt) {   // the fp32 residual stream from h_in (routed calls gather it in the first LayerNorm)
       ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
       SR_TRY(launch_convert(d.dtype, h_in, kF32, sv[0].hin, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
     }
@@ -157,7 +163,11 @@ hipError_t stack_fwd(const Dims& d, const sr_block_params* p, const void* cond, 
         ProfScope ps("mod", gemm_flops(d.B, 6 * D, D), gemm_bytes(d, d.B, 6 * D, D, 4), st);
         SR_TRY(launch_gemv_rows(d.dtype, cond, D, w.w_ada, w.b_ada, d.B, 6 * D, D, s.mod, 6 * D, st));
       }
-      {
+      if (rt && i == 0) {   // x[idx] rows -> fp32 residual copy and LN1, one pass
+        ProfScope ps("ln_fwd_gather", 0, (double)M * D * (2 * e + 4) + 4.0 * M, st);
+        SR_TRY(launch_ln_fwd_gather(d.dtype, rt->x, rt->idx, d.L, rt->shared, s.hin, w.ln1_w, w.ln1_b,
+                                    ada ? s.mod : nullptr, 0, M, S, D, d.eps, s.u1, s.mean1, s.rstd1, st));
+      } else {
         ProfScope ps("ln_fwd", 0, (double)M * D * (4 + e), st);
         SR_TRY(launch_ln_fwd(d.dtype, s.hin, w.ln1_w, w.ln1_b, ada ? s.mod : nullptr, 0, M, S, D, d.eps, s.u1,
                              s.mean1, s.rstd1, st));
@@ -383,7 +393,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       // FC2: dW2, db2; dz = (dm W2) * GELU'(z)
       SR_TRY(on_side(kFc2, [&](hipStream_t ss) -> hipError_t {
         if (ln1_pending) SR_TRY(ln_reduce(1, ln1_pending->ln1_w, ln1_pending->ln1_b, ss));
-        return weight_grad("gemm_dw_fc2", d, g0, D, s.gz, F, g.w_fc2, g.b_fc2, sc, ss);
+        if (g.w_fc2 || g.b_fc2) {   // GELU(z) recomputed from the stored pre-activation
+          ProfScope ps("recompute", 0, (double)M * F * e * 2, ss);
+          SR_TRY(launch_gelu(d.dtype, s.z, sc.gz_rc, (size_t)M * F, ss));
+        }
+        return weight_grad("gemm_dw_fc2", d, g0, D, sc.gz_rc, F, g.w_fc2, g.b_fc2, sc, ss);
       }));
       ln1_pending = nullptr;
       SR_TRY(join(kFc1 + par));   // dz[par] may still be read by dW_fc1 two blocks back
@@ -394,8 +408,13 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(launch_gemm(gd, EPI_DGELU, ep, st));
       }
       // FC1: dW1, db1; du = dz W1
-      SR_TRY(on_side(kFc1 + par, [&](hipStream_t ss) {
-        return weight_grad("gemm_dw_fc1", d, dz, F, s.u2, D, g.w_fc1, g.b_fc1, sc, ss);
+      SR_TRY(on_side(kFc1 + par, [&](hipStream_t ss) -> hipError_t {
+        if (g.w_fc1 || g.b_fc1) {   // u2 = LN2(h1) recomputed from the saved statistics
+          ProfScope ps("recompute", 0, (double)M * D * (4 + e), ss);
+          SR_TRY(launch_ln_apply(d.dtype, s.h1, w.ln2_w, w.ln2_b, ada ? s.mod : nullptr, 3 * D, M, S, D, s.mean2,
+                                 s.rstd2, sc.u_rc, ss));
+        }
+        return weight_grad("gemm_dw_fc1", d, dz, F, sc.u_rc, D, g.w_fc1, g.b_fc1, sc, ss);
       }));
       {
         GemmDesc gd = desc(d, dz, true, F, (size_t)M * F * e, w.w_fc1, false, D, (size_t)F * D * e, M, D, F);
@@ -443,8 +462,13 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       SR_TRY(join(kQkv + par));   // dqkv[par] may still be read by dW_qkv two blocks back
       SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, dqkv, d.B, S, d.H, D, st));
       // QKV: dWqkv, dbqkv; du = dqkv Wqkv
-      SR_TRY(on_side(kQkv + par, [&](hipStream_t ss) {
-        return weight_grad("gemm_dw_qkv", d, dqkv, 3 * D, s.u1, D, g.w_qkv, g.b_qkv, sc, ss);
+      SR_TRY(on_side(kQkv + par, [&](hipStream_t ss) -> hipError_t {
+        if (g.w_qkv || g.b_qkv) {   // u1 = LN1(h) recomputed from the saved statistics
+          ProfScope ps("recompute", 0, (double)M * D * (4 + e), ss);
+          SR_TRY(launch_ln_apply(d.dtype, s.hin, w.ln1_w, w.ln1_b, ada ? s.mod : nullptr, 0, M, S, D, s.mean1,
+                                 s.rstd1, sc.u_rc, ss));
+        }
+        return weight_grad("gemm_dw_qkv", d, dqkv, 3 * D, sc.u_rc, D, g.w_qkv, g.b_qkv, sc, ss);
       }));
       {
         GemmDesc gd = desc(d, dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,

@@ -22,7 +22,7 @@ struct BlockSaved {
 
 struct Scratch {
   float *g_res, *g_res2, *du, *delta, *wpart, *dbpart, *part, *lnpart[2], *dmod, *gvpart;
-  void *g_act[2], *dz[2], *dO, *dqkv[2];
+  void *g_act[2], *dz[2], *dO, *dqkv[2], *u_rc, *gz_rc;
 };
 
 // Routing fused into the stack's boundaries: the input rows are gathered from x by idx
