@@ -31,6 +31,16 @@
  *  - Storage dtype (sr_config.dtype): SR_F32 or SR_BF16.  Activations, weights,
  *    biases, LayerNorm parameters and the conditioning vector are stored in it;
  *    all accumulation is fp32; weight gradients and dcond are always fp32.
+ *  - Non-finite values: a NaN or Inf in a sample's inputs (tokens, conditioning) or in the
+ *    parameters gives non-finite values in that sample's outputs and gradients (attention mixes
+ *    every token of a sample, so all of its routed rows may be affected; which elements is not
+ *    specified) and in the parameter gradients; other samples' results are unchanged and rows
+ *    the scatter does not touch keep their values.  Nothing is clamped or checked on the GPU.
+ *  - Debugging: with SR_DEBUG=1 in the environment (read at every call), sr_gather,
+ *    sr_scatter_delta and sr_routed_blocks_fwd/bwd copy idx to the host, synchronising
+ *    `stream`, and return SR_EINVAL before any launch if a row is not strictly increasing
+ *    inside [0, L).  Off by default (no host synchronisation on the hot path); not for use
+ *    under graph capture.
  *  - Shapes: B samples, L tokens per sample, D channels, H heads (D % H == 0),
  *    F MLP width, n_blocks middle blocks; S = K (routed) or L (dense) tokens per
  *    sample inside the stack.

@@ -2,6 +2,7 @@
 // on the host, then launches on the caller's stream.  Nothing is allocated here.
 #include <algorithm>
 #include <cstdarg>
+#include <cstdlib>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -71,6 +72,27 @@ sr_status check_cfg(const sr_config* c, bool routing_only = false) {
     const size_t big = (size_t)c->B * c->L * (size_t)std::max(c->F, 3 * c->D) * 4;
     SR_CHECK(big < (1ull << 31), SR_EUNSUPPORTED, "stack buffers beyond 2 GiB are not supported");
   }
+  return SR_OK;
+}
+
+// SR_DEBUG=1 in the environment (read at every call): calls that take an index set copy it to
+// the host (synchronising the stream) and reject one that is not strictly increasing inside
+// [0, L) before launching anything.
+sr_status debug_check_indices(const sr_config* cfg, int32_t K, const int32_t* idx, hipStream_t st) {
+  const char* v = getenv("SR_DEBUG");
+  if (!(v && v[0] == '1')) return SR_OK;
+  const int rows = cfg->idx_shared ? 1 : cfg->B;
+  std::vector<int32_t> h((size_t)rows * K);
+  hipError_t e = hipMemcpyAsync(h.data(), idx, h.size() * sizeof(int32_t), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_status(e, "SR_DEBUG index check");
+  for (int r = 0; r < rows; ++r)
+    for (int k = 0; k < K; ++k) {
+      const int32_t x = h[(size_t)r * K + k];
+      const bool ok = x >= 0 && x < cfg->L && (k == 0 || x > h[(size_t)r * K + k - 1]);
+      SR_CHECK(ok, SR_EINVAL, "SR_DEBUG: idx[%d][%d] = %d breaks a strictly increasing index set inside [0, L=%d)",
+               r, k, x, cfg->L);
+    }
   return SR_OK;
 }
 
@@ -212,6 +234,7 @@ sr_status sr_gather(const sr_config* cfg, int32_t K, const void* x, const int32_
   SR_PTR(x, "x");
   SR_PTR(idx, "idx");
   SR_PTR(h0, "h0");
+  if ((s = debug_check_indices(cfg, K, idx, (hipStream_t)stream)) != SR_OK) return s;
   sr::ProfScope ps("gather", 0, 2.0 * cfg->B * K * cfg->D * elt_of(cfg->dtype) + 4.0 * cfg->B * K, (hipStream_t)stream);
   return hip_status(sr::launch_gather((int)elt_of(cfg->dtype), cfg->B, cfg->L, K, cfg->D, x, idx, h0,
                                       cfg->idx_shared, (hipStream_t)stream),
@@ -227,6 +250,7 @@ sr_status sr_scatter_delta(const sr_config* cfg, int32_t K, void* x, const void*
   SR_PTR(h, "h");
   SR_PTR(idx, "idx");
   if (h0) SR_CHECK(aligned16(h0), SR_EALIGN, "h0 is not 16-byte aligned");
+  if ((s = debug_check_indices(cfg, K, idx, (hipStream_t)stream)) != SR_OK) return s;
   const int dt = cfg->dtype == SR_BF16 ? sr::kBF16 : sr::kF32;
   sr::ProfScope ps("scatter_delta", 0, (h0 ? 4.0 : 3.0) * cfg->B * K * cfg->D * elt_of(cfg->dtype) + 4.0 * cfg->B * K,
                    (hipStream_t)stream);
@@ -282,6 +306,7 @@ sr_status sr_routed_blocks_fwd(const sr_config* cfg, int32_t K, const int32_t* i
   SR_PTR(idx, "idx");
   SR_PTR(x, "x");
   if ((s = check_ws(cfg, K, saved, saved_bytes, nullptr, 0, false)) != SR_OK) return s;
+  if ((s = debug_check_indices(cfg, K, idx, (hipStream_t)stream)) != SR_OK) return s;
   sr::Dims d = dims_of(cfg, K);
   sr::Route rt;
   rt.idx = idx; rt.x = x; rt.shared = cfg->idx_shared;
@@ -303,6 +328,7 @@ sr_status sr_routed_blocks_bwd(const sr_config* cfg, int32_t K, const int32_t* i
   SR_CHECK(grads != nullptr, SR_EINVAL, "grads is NULL");
   if (dcond) SR_CHECK(aligned16(dcond), SR_EALIGN, "dcond is not 16-byte aligned");
   if ((s = check_ws(cfg, K, saved, saved_bytes, scratch, scratch_bytes, true)) != SR_OK) return s;
+  if ((s = debug_check_indices(cfg, K, idx, (hipStream_t)stream)) != SR_OK) return s;
   sr::Dims d = dims_of(cfg, K);
   sr::Route rt;
   rt.idx = idx; rt.x = g; rt.shared = cfg->idx_shared;

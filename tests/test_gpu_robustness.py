@@ -1,0 +1,81 @@
+"""Failure handling on the GPU: the SR_DEBUG index validation rejects bad index sets before any
+launch, and a NaN in one sample's tokens stays in that sample (the other samples' results are
+bit-identical to a clean run; rows the scatter does not touch keep their values)."""
+import numpy as np
+import pytest
+
+from paper_2607_02829_amd import abi, device, inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def test_sr_debug_rejects_bad_index_sets(monkeypatch):
+    import torch
+    w = inputs.small("dbg", B=2, Hg=4, Wg=10)
+    cfg = device.config_for(w)
+    x = device.to_device(inputs.to_storage(inputs.token_field(w), w.dtype))
+    h0 = torch.empty((w.B, 5, w.D), dtype=x.dtype, device="cuda")
+    mk = lambda rows: torch.tensor(rows, dtype=torch.int32, device="cuda")
+    good = mk([[0, 3, 7, 8, 39], [1, 2, 3, 4, 5]])
+    monkeypatch.setenv("SR_DEBUG", "1")
+    abi.sr_gather(cfg, 5, x, good, h0)
+    torch.cuda.synchronize()
+    # in range but not strictly increasing: harmless to the kernels, so this proves the check is on
+    with pytest.raises(abi.SrError) as ei:
+        abi.sr_gather(cfg, 5, x, mk([[0, 3, 3, 8, 39], [1, 2, 3, 4, 5]]), h0)
+    assert ei.value.status == abi.SR_EINVAL and "SR_DEBUG" in abi.sr_last_error()
+    # out of range (L = 40): rejected before any launch by every call that takes idx
+    oob = mk([[0, 3, 7, 8, 40], [1, 2, 3, 4, 5]])
+    with pytest.raises(abi.SrError):
+        abi.sr_gather(cfg, 5, x, oob, h0)
+    with pytest.raises(abi.SrError):
+        abi.sr_scatter_delta(cfg, 5, x, h0, None, oob)
+    params = device.DeviceParams(inputs.params_to_storage(inputs.block_params(w), w.dtype), w.kind)
+    saved, scratch = device.workspace(cfg, 5)
+    with pytest.raises(abi.SrError):
+        abi.sr_routed_blocks_fwd(cfg, 5, oob, params.array, None, x, saved)
+    grads = device.DeviceGrads(w, w.n_blocks)
+    with pytest.raises(abi.SrError):
+        abi.sr_routed_blocks_bwd(cfg, 5, mk([[-1, 3, 7, 8, 9], [1, 2, 3, 4, 5]]), params.array, None, saved, x,
+                                 grads.array, None, scratch)
+    monkeypatch.delenv("SR_DEBUG")
+    torch.cuda.synchronize()
+
+
+def _routed(w, x, g, params, K):
+    import torch
+    cfg = device.config_for(w)
+    dp = device.DeviceParams(params, w.kind)
+    gr = device.DeviceGrads(w, w.n_blocks)
+    xd, gd = device.to_device(x), device.to_device(g)
+    idx = torch.empty((w.B, K), dtype=torch.int32, device="cuda")
+    abi.sr_select_indices(cfg, K, abi.SR_SEL_RANDOM, 3, 1, None, None, idx)
+    saved, scratch = device.workspace(cfg, K)
+    abi.sr_routed_blocks_fwd(cfg, K, idx, dp.array, None, xd, saved)
+    abi.sr_routed_blocks_bwd(cfg, K, idx, dp.array, None, saved, gd, gr.array, None, scratch)
+    torch.cuda.synchronize()
+    return device.to_host(xd), device.to_host(gd), idx.cpu().numpy(), gr.tensors[0]["w_qkv"].cpu().numpy()
+
+
+def test_nan_in_one_sample_stays_in_that_sample():
+    w = inputs.small("nan", B=2, Hg=10, Wg=20)
+    K = w.K
+    x = inputs.to_storage(inputs.token_field(w), w.dtype)
+    g = inputs.to_storage(inputs.upstream_grad(w), w.dtype)
+    params = inputs.params_to_storage(inputs.block_params(w), w.dtype)
+    x_clean, g_clean, idx, _ = _routed(w, x, g, params, K)
+    bad = x.copy()
+    bad[0, idx[0, 3], 5] = 0x7FC0            # a bf16 NaN in one routed token of sample 0
+    x_bad, g_bad, idx2, dw = _routed(w, bad, g, params, K)
+    assert np.array_equal(idx, idx2)
+    bits = lambda a: np.ascontiguousarray(a).view(np.uint8)
+    # sample 1 is untouched by sample 0's NaN, forward and backward, bit for bit
+    assert np.array_equal(bits(x_bad[1]), bits(x_clean[1]))
+    assert np.array_equal(bits(g_bad[1]), bits(g_clean[1]))
+    # sample 0: its routed rows become non-finite, its other rows keep x0 / g exactly
+    to32 = lambda a: (a.astype(np.uint32) << 16).view(np.float32)
+    assert not np.isfinite(to32(x_bad[0, idx[0]])).all()
+    mask = np.ones(w.L, bool); mask[idx[0]] = False
+    assert np.array_equal(bits(x_bad[0, mask]), bits(bad[0, mask]))
+    assert np.array_equal(bits(g_bad[0, mask]), bits(g[0, mask]))
+    assert not np.isfinite(dw).all()          # parameter gradients sum over both samples
