@@ -328,12 +328,17 @@ def graph_timing(st: Step, steps: int, warmup: int) -> dict:
 
 def cross_attention_timing(reps: int = 5) -> dict:
     """The asymmetric attention of the generative block's sparse stage at its shape (2 samples,
-    2048 routed queries against 8192 conditioning tokens, 16 heads, D = 1024, bf16), forward
-    and backward through sr_cross_attention_fwd / _bwd (the MFMA attention kernels), HIP-event
-    timed; algorithmic FLOPs 4 B Sq Skv D forward, 8 B Sq Skv D backward."""
+    2048 routed queries against 8192 conditioning tokens, D = 1024, bf16) with 16 heads of 64 and
+    with the generative model's 8 heads of 128."""
+    return {f"heads_{H}x{1024 // H}": cross_attention_one(H, reps) for H in (16, 8)}
+
+
+def cross_attention_one(H: int, reps: int = 5) -> dict:
+    """Forward and backward through sr_cross_attention_fwd / _bwd (the MFMA attention kernels),
+    HIP-event timed; algorithmic FLOPs 4 B Sq Skv D forward, 8 B Sq Skv D backward."""
     import torch
     from paper_2607_02829_amd import abi
-    B, Sq, Skv, D, H = 2, 2048, 8192, 1024, 16
+    B, Sq, Skv, D = 2, 2048, 8192, 1024
     cfg = abi.SrConfig(B=B, L=1, D=D, H=H, F=64, n_blocks=1, dtype=abi.SR_BF16, kind=abi.SR_BLOCK_PRELN,
                        ln_eps=1e-6, idx_shared=0)
     g = torch.Generator(device="cuda").manual_seed(5)
@@ -356,7 +361,7 @@ def cross_attention_timing(reps: int = 5) -> dict:
             torch.cuda.synchronize()
             if r > 0:
                 times[name].append(e0.elapsed_time(e1))
-    out = {"shape": {"B": B, "Sq": Sq, "Skv": Skv, "D": D, "H": H}, "kernels": "mfma (bf16, head dim 64)"}
+    out = {"shape": {"B": B, "Sq": Sq, "Skv": Skv, "D": D, "H": H}, "kernels": f"mfma (bf16, head dim {D // H})"}
     for name, mult in (("fwd", 4.0), ("bwd", 8.0)):
         ms = sorted(times[name])[len(times[name]) // 2]
         flops = mult * B * Sq * Skv * D
@@ -466,6 +471,75 @@ def summarize_pmc(group: str, workload: str, fetch_csv: str, write_csv: str, com
         f"- source_sha256: `{source_hash(group)}`",
         "",
     ]
+    return "\n".join(lines)
+
+
+# routing kernels: symbol -> (label, algorithmic bytes of one dispatch on `rows` rows of D columns)
+ROUTING_KERNELS = {
+    "gather_kernel": ("gather (h0 = x[idx], bf16)", lambda rows, D: 2 * rows * D * 2 + 4 * rows),
+    "scatter_delta_kernel": ("residual-delta scatter, h0 re-read from x (bf16)", lambda rows, D: 3 * rows * D * 2 + 4 * rows),
+    "gather_rows_f32_kernel": ("gradient gather into fp32 + bf16 copies (backward)", lambda rows, D: rows * D * 8 + 4 * rows),
+    "scatter_f32_delta_kernel": ("rounding + residual-delta scatter of the fp32 gradient (backward)",
+                                 lambda rows, D: rows * D * 8 + 4 * rows),
+    "ln_fwd_kernel": ("first LayerNorm with the gather (forward): x[idx] -> fp32 copy + LN1",
+                      lambda rows, D: rows * D * 8 + 12 * rows),
+}
+ROUTING_ROWS_PER_BLOCK = 4   # one wave per row, four waves per 256-thread workgroup
+
+
+def summarize_routing_pmc(fetch_csv: str, write_csv: str, command: str, D: int = 1024) -> str:
+    """HBM traffic of the routing kernels per dispatch size from two rocprofv3 --pmc runs
+    (FETCH_SIZE, WRITE_SIZE), scaled by the copy probe, against their algorithmic bytes."""
+    import csv
+    import statistics
+
+    def per_dispatch(path, counter):
+        out = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            out.setdefault((r["Kernel_Name"], int(r["Grid_Size"])), []).append(float(r["Counter_Value"]))
+        return out
+
+    fetch, write = per_dispatch(fetch_csv, "FETCH_SIZE"), per_dispatch(write_csv, "WRITE_SIZE")
+    copy = [(max(v), k) for k, v in fetch.items() if "copyBuffer" in k[0]]
+    copyw = [(max(v), k) for k, v in write.items() if "copyBuffer" in k[0]]
+    if not copy or not copyw:
+        raise SystemExit("no copy-probe dispatch in the counter files")
+    f_scale = COPY_PROBE_BYTES / (max(copy)[0] * 1024.0)
+    w_scale = COPY_PROBE_BYTES / (max(copyw)[0] * 1024.0)
+    lines = [
+        "# HBM traffic of the routing kernels (gather, residual-delta scatter and their fused forms)",
+        "",
+        "rocprofv3 counter passes (one counter per run), KiB per dispatch averaged over the dispatches",
+        f"of one kernel and grid size, scaled by the same counters on a {COPY_PROBE_BYTES}-byte device copy",
+        f"(FETCH_SIZE x {f_scale:.4f}, WRITE_SIZE x {w_scale:.4f}); rows = one wave per row (grid threads / 64);",
+        "algorithmic bytes as in `bench.py` (one read of each input, one write of each output).",
+        "",
+        "Commands (repository root on the GPU box, `cd /tmp && export TMPDIR=/tmp` first):",
+        "",
+        "```",
+        command,
+        "```",
+        "",
+        "| kernel | rows | dispatches | fetch MB | write MB | HBM MB | algorithmic MB | HBM / algorithmic |",
+        "|---|---:|---:|---:|---:|---:|---:|---:|",
+    ]
+    for (name, grid), fv in sorted(fetch.items(), key=lambda kv: (kv[0][0], kv[0][1])):
+        sym = next((k for k in ROUTING_KERNELS if k in name.split("(")[0]), None)
+        if sym is None or (name, grid) not in write:
+            continue
+        if sym == "ln_fwd_kernel":   # only the gathering form (fifth template argument)
+            targs = name.split("(")[0].split("<", 1)[-1].rstrip(">").split(", ")
+            if len(targs) < 5 or targs[4] != "true":
+                continue
+        rows = grid // 64
+        f = statistics.mean(fv) * 1024.0 * f_scale
+        w = statistics.mean(write[(name, grid)]) * 1024.0 * w_scale
+        alg = ROUTING_KERNELS[sym][1](rows, D)
+        lines.append(f"| `{sym}` ({ROUTING_KERNELS[sym][0]}) | {rows} | {len(fv)} | {f / 1e6:.2f} | {w / 1e6:.2f} | "
+                     f"{(f + w) / 1e6:.2f} | {alg / 1e6:.2f} | {(f + w) / alg:.3f} |")
+    lines.append("")
     return "\n".join(lines)
 
 
@@ -581,11 +655,23 @@ def main():
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("GROUP", "FETCH_CSV", "WRITE_CSV", "OUT_MD"),
                     help="write the HBM-traffic summary of GROUP from two rocprofv3 --pmc CSVs and exit")
     ap.add_argument("--pmc-command", default="", help="command text recorded in the summary")
+    ap.add_argument("--summarize-routing-pmc", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "OUT_MD"),
+                    help="write the routing kernels' HBM-traffic summary from two rocprofv3 --pmc CSVs and exit")
+    ap.add_argument("--generative-only", action="store_true",
+                    help="time only the generative stage against its dense blocks (one JSON line)")
     args = ap.parse_args()
 
     if args.summarize_pmc:
         group, fcsv, wcsv, out_md = args.summarize_pmc
         text = summarize_pmc(group, args.workload, fcsv, wcsv, args.pmc_command)
+        with open(out_md, "w") as f:
+            f.write(text)
+        print(text)
+        return
+
+    if args.summarize_routing_pmc:
+        fcsv, wcsv, out_md = args.summarize_routing_pmc
+        text = summarize_routing_pmc(fcsv, wcsv, args.pmc_command)
         with open(out_md, "w") as f:
             f.write(text)
         print(text)
@@ -602,6 +688,9 @@ def main():
     abi.lib()
     torch.cuda.set_device(0)
     w = inputs.WORKLOADS[args.workload]
+    if args.generative_only:
+        print(json.dumps({"generative": generative_stage(args.steps, max(1, args.steps // 2))}), flush=True)
+        return
     if args.copy_probe:
         src = torch.empty(COPY_PROBE_BYTES, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)

@@ -341,19 +341,33 @@ __global__ __launch_bounds__(256) void convert_kernel(const TI* __restrict__ x, 
   }
 }
 
-// delta[b,h,s] = sum_d dO[b,s,h*hd+d] * O[b,s,h*hd+d]
+// delta[b,h,s] = sum_d dO[b,s,h*hd+d] * O[b,s,h*hd+d].  One wave per token row: lane l takes
+// columns 8l .. 8l+7 of each 512-column pass (16-byte loads of bf16), so a head's hd columns lie
+// on hd/8 consecutive lanes, which add their partial sums with an xor butterfly (fixed order);
+// the group's first lane stores.
 template <typename Ta>
 __global__ __launch_bounds__(256) void attn_delta_kernel(const Ta* __restrict__ dO, const Ta* __restrict__ O,
                                                          int B, int S, int H, int hd, float* __restrict__ delta) {
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  if (t >= B * S * H) return;
-  const int h = t % H;
-  const int row = t / H;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= B * S) return;
+  const int D = H * hd, G = hd / 8;   // lanes per head in a pass (4, 8 or 16)
   const int b = row / S, s = row - b * S;
-  const size_t o = (size_t)row * H * hd + (size_t)h * hd;
-  float acc = 0.f;
-  for (int d = 0; d < hd; ++d) acc += to_f32<Ta>(dO[o + d]) * to_f32<Ta>(O[o + d]);
-  delta[((size_t)b * H + h) * S + s] = acc;
+  const Ta* dr = dO + (size_t)row * D;
+  const Ta* orow = O + (size_t)row * D;
+  for (int c0 = 0; c0 < D; c0 += 512) {
+    const int c = c0 + 8 * lane;
+    float acc = 0.f;
+    if (c < D) {
+      float a[8], o[8];
+      load8<Ta>(dr + c, a);
+      load8<Ta>(orow + c, o);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc += a[e] * o[e];
+    }
+    for (int off = G / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (c < D && (lane & (G - 1)) == 0) delta[((size_t)b * H + c / hd) * S + s] = acc;
+  }
 }
 
 // Column sums of row partials, in a fixed order (deterministic):
@@ -540,12 +554,12 @@ hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st) {
 
 hipError_t launch_attn_delta(int dtype, const void* dO, const void* O, int B, int S, int H, int hd, float* delta,
                              hipStream_t st) {
-  const size_t n = (size_t)B * S * H;
+  const size_t rows = (size_t)B * S;
   if (dtype == kBF16)
-    hipLaunchKernelGGL(attn_delta_kernel<bf16_t>, grid1d(n, 256), dim3(256), 0, st, (const bf16_t*)dO,
+    hipLaunchKernelGGL(attn_delta_kernel<bf16_t>, grid1d(rows, 4), dim3(256), 0, st, (const bf16_t*)dO,
                        (const bf16_t*)O, B, S, H, hd, delta);
   else
-    hipLaunchKernelGGL(attn_delta_kernel<float>, grid1d(n, 256), dim3(256), 0, st, (const float*)dO,
+    hipLaunchKernelGGL(attn_delta_kernel<float>, grid1d(rows, 4), dim3(256), 0, st, (const float*)dO,
                        (const float*)O, B, S, H, hd, delta);
   return hipGetLastError();
 }
