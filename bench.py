@@ -581,7 +581,26 @@ def routing_sweep(D: int, sizes=(4050, 32768, 262144), reps: int = 5) -> list:
             out.append({"kernel": name, "rows": K, "bytes": nbytes, "us": round(ms * 1e3, 2),
                         "GB/s": round(gbs, 1), "frac_of_8TB/s": round(gbs * 1e9 / PEAK_HBM_BYTES, 3)})
         del x, idx, h0, h
-    del evict
+    # reference: a plain device-to-device copy of the largest gather's size (reads and writes
+    # the same bytes contiguously), timed the same way
+    n = 2 * sizes[-1] * D * 2
+    src = torch.empty(n // 2, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    times = []
+    for r in range(reps + 1):
+        evict.zero_()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        if r > 0:
+            times.append(e0.elapsed_time(e1))
+    ms = sorted(times)[len(times) // 2]
+    gbs = n / (ms * 1e-3) / 1e9
+    out.append({"kernel": "device copy (reference)", "rows": sizes[-1], "bytes": n, "us": round(ms * 1e3, 2),
+                "GB/s": round(gbs, 1), "frac_of_8TB/s": round(gbs * 1e9 / PEAK_HBM_BYTES, 3)})
+    del src, dst, evict
     torch.cuda.empty_cache()
     return out
 
