@@ -21,6 +21,9 @@ NO_CONTRACT = {"select.hip", "routing.hip"}
 # Files whose arithmetic never meets a NaN (softmax of finite scores, -inf masks): max/min
 # without NaN canonicalisation.
 NO_NANS = {"attention.hip"}
+# Files whose kernels read LDS fragments with inline assembly: their gfx950 assembly is kept
+# and checked (isa_scan) for registers touched while such a read is in flight.
+ASYNC_READS = {"attention.hip", "gemm.hip"}
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -38,6 +41,8 @@ def _compile(src: str) -> str:
         cmd.insert(1, "-ffp-contract=off")
     if src in NO_NANS:
         cmd.insert(1, "-fno-honor-nans")
+    if src in ASYNC_READS:
+        cmd.insert(1, "-save-temps=obj")
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -46,10 +51,29 @@ def _compile(src: str) -> str:
     return obj
 
 
+def device_asm_path(src: str) -> str:
+    """Where the build keeps the gfx950 assembly of an ASYNC_READS source."""
+    return os.path.join(BUILD, os.path.splitext(src)[0] + "-hip-amdgcn-amd-amdhsa-gfx950.s")
+
+
+def check_async_reads() -> dict:
+    """Kernels of the ASYNC_READS sources that touch a register while an LDS read into it is in
+    flight (empty when sound)."""
+    from .isa_scan import kernel_hazards
+    bad = {}
+    for src in sorted(ASYNC_READS):
+        with open(device_asm_path(src)) as f:
+            bad.update({k: v for k, v in kernel_hazards(f.read()).items() if v})
+    return bad
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
+    bad = check_async_reads()
+    if bad:
+        raise RuntimeError(f"registers touched while their LDS reads are in flight: {bad}")
     tmp = OUT + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)

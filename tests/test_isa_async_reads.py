@@ -1,0 +1,46 @@
+"""The explicit (inline-assembly) LDS fragment reads of the MFMA kernels are only sound if the
+compiler never touches their destination registers before the wait that retires them.  The build
+keeps the gfx950 assembly of the sources that use them and refuses a library that breaks this;
+here the scan itself is pinned on hand-written sequences, and the kept assembly is rescanned."""
+import os
+
+import pytest
+
+from paper_2607_02829_amd import build
+from paper_2607_02829_amd.isa_scan import kernel_hazards
+
+
+def test_scan_flags_a_copy_of_an_in_flight_destination():
+    asm = """_Zk:
+\tds_read_b128 a[0:3], v1 offset:0
+\tv_accvgpr_read_b32 v4, a2
+\ts_waitcnt lgkmcnt(0)
+\tv_accvgpr_read_b32 v5, a3
+.Lfunc_end0:
+_Zok:
+\tds_read_b128 v[0:3], v9 offset:0
+\tds_read_b128 v[4:7], v9 offset:64
+\ts_waitcnt lgkmcnt(1)
+\tv_add_u32 v10, v0, v1
+\ts_waitcnt lgkmcnt(0)
+\tv_add_u32 v11, v4, v5
+.Lfunc_end1:
+_Zw:
+\tds_read_b64_tr_b16 v[2:3], v9 offset:0
+\tv_mov_b32 v3, 0
+\ts_waitcnt lgkmcnt(0)
+.Lfunc_end2:
+"""
+    # a copy before the wait, a read retired by lgkmcnt(1) (in order), a write into a pending register
+    assert kernel_hazards(asm) == {"_Zk": 1, "_Zok": 0, "_Zw": 1}
+
+
+@pytest.mark.parametrize("src", sorted(build.ASYNC_READS))
+def test_built_kernels_keep_in_flight_registers_untouched(src):
+    path = build.device_asm_path(src)
+    if not os.path.exists(path):
+        pytest.skip("library not built here")
+    with open(path) as f:
+        hz = kernel_hazards(f.read())
+    assert hz, "no kernels in the kept assembly"
+    assert not {k: v for k, v in hz.items() if v}
