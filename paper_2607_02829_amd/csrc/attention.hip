@@ -231,6 +231,21 @@ SR_DEV void unstage(const bf16_t* stage, bf16_t* dst, size_t ld, int r0, int S) 
   }
 }
 
+// Workgroups go to the eight XCDs in dispatch order round-robin (linear id mod 8), and each XCD
+// has its own L2.  The MFMA kernels remap their ids so that the workgroups of one (sample, head)
+// pair -- which all stream the same tiles -- run on one XCD: dispatch slot s of XCD x takes the
+// (x N / 8 + s)-th (block, head, sample) triple in block-fastest order.  Identity when the
+// grid's size N is not a multiple of 8.
+struct TileId {
+  int blk, h, b;
+};
+SR_DEV TileId xcd_tile_id() {
+  const int nb = gridDim.x, nh = gridDim.y, n = nb * nh * gridDim.z;
+  int l = blockIdx.x + nb * (blockIdx.y + nh * blockIdx.z);
+  if ((n & 7) == 0) l = (l & 7) * (n >> 3) + (l >> 3);
+  return {l % nb, (l / nb) % nh, l / (nb * nh)};
+}
+
 // ------------------------------------------------------------------------------ forward
 
 // NW waves (32 queries each) per workgroup share the K / V tiles.
@@ -245,9 +260,10 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_fwd_mfma(
   constexpr int TE = G::TE, TB = G::TB, SGB = G::SGB, KS = G::KS, DB = G::DB;
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
-  const int b = blockIdx.z, hh = blockIdx.y;
+  const TileId id = xcd_tile_id();
+  const int b = id.b, hh = id.h;
   const bf16_t* qp = q + (size_t)b * Sq * ldq + hh * HD;
-  const int myq = blockIdx.x * (32 * NW) + wid * 32 + l32;
+  const int myq = id.blk * (32 * NW) + wid * 32 + l32;
   const int nt = (Skv + KT - 1) / KT;
   const bool ragged = Skv % KT != 0;
   const __amdgpu_buffer_rsrc_t rq = make_rsrc(kv, kv_elems * 2u);
@@ -394,7 +410,7 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_fwd_mfma(
   if (h32 == 0 && myq < Sq) lse[((size_t)b * H + hh) * Sq + myq] = m_run * sl2 + log2f(l_tot);
   stage_t<HD>(smem, o, 1.0f / l_tot, wid, lane);
   __syncthreads();
-  unstage<HD, NW>(smem, O + (size_t)b * Sq * D + hh * HD, D, blockIdx.x * (32 * NW), Sq);
+  unstage<HD, NW>(smem, O + (size_t)b * Sq * D + hh * HD, D, id.blk * (32 * NW), Sq);
 }
 
 // ------------------------------------------------------------------------------ backward dK, dV
@@ -414,10 +430,11 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dkv_m
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: Q tile, dO tile
   __shared__ __attribute__((aligned(16))) float fsm[NSTG * 2 * KT];     // stage: lse, delta of the tile's rows
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
-  const int b = blockIdx.z, hh = blockIdx.y;
+  const TileId id = xcd_tile_id();
+  const int b = id.b, hh = id.h;
   const bf16_t* kp = kv + (size_t)b * Skv * ldkv + hh * HD;
   const bf16_t* vp = kp + D;
-  const int mykey = blockIdx.x * (32 * NW) + wid * 32 + l32;
+  const int mykey = id.blk * (32 * NW) + wid * 32 + l32;
   const int nt = (Sq + KT - 1) / KT;
   const bool ragged = Sq % KT != 0;
 
@@ -523,11 +540,11 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dkv_m
   bf16_t* out = dk_out + (size_t)b * Skv * ldo;
   stage_t<HD>(smem, dk, scale, wid, lane);
   __syncthreads();
-  unstage<HD, NW>(smem, out + hh * HD, ldo, blockIdx.x * (32 * NW), Skv);
+  unstage<HD, NW>(smem, out + hh * HD, ldo, id.blk * (32 * NW), Skv);
   __syncthreads();
   stage_t<HD>(smem, dv, 1.0f, wid, lane);
   __syncthreads();
-  unstage<HD, NW>(smem, out + D + hh * HD, ldo, blockIdx.x * (32 * NW), Skv);
+  unstage<HD, NW>(smem, out + D + hh * HD, ldo, id.blk * (32 * NW), Skv);
 }
 
 // ------------------------------------------------------------------------------ backward dQ
@@ -546,10 +563,11 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dq_mf
   constexpr int TE = G::TE, TB = G::TB, SGB = G::SGB, KS = G::KS, DB = G::DB;
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * 2 * TE];   // stage: K tile, V tile
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
-  const int b = blockIdx.z, hh = blockIdx.y;
+  const TileId id = xcd_tile_id();
+  const int b = id.b, hh = id.h;
   const bf16_t* qp = q + (size_t)b * Sq * ldq + hh * HD;
   const bf16_t* dop = dO + (size_t)b * Sq * D + hh * HD;
-  const int myq = blockIdx.x * (32 * NW) + wid * 32 + l32;
+  const int myq = id.blk * (32 * NW) + wid * 32 + l32;
   const int nt = (Skv + KT - 1) / KT;
   const bool ragged = Skv % KT != 0;
 
@@ -662,7 +680,7 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dq_mf
   __syncthreads();
   stage_t<HD>(smem, dq, scale, wid, lane);
   __syncthreads();
-  unstage<HD, NW>(smem, dq_out + (size_t)b * Sq * ldo + hh * HD, ldo, blockIdx.x * (32 * NW), Sq);
+  unstage<HD, NW>(smem, dq_out + (size_t)b * Sq * ldo + hh * HD, ldo, id.blk * (32 * NW), Sq);
 }
 
 // ------------------------------------------------------------------------------ generic kernels
@@ -794,10 +812,11 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_colsum_mfma(const bf16_t
   __shared__ __attribute__((aligned(16))) bf16_t smem[NSTG * TE];   // stage: Q tile
   __shared__ __attribute__((aligned(16))) float fsm[NSTG * KT];     // stage: lse of the tile's rows
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, l32 = lane & 31, h32 = lane >> 5;
-  const int b = blockIdx.z, hh = blockIdx.y;
+  const TileId id = xcd_tile_id();
+  const int b = id.b, hh = id.h;
   const size_t ld = 3 * (size_t)D;
   const bf16_t* kp = qkv + (size_t)b * S * ld + D + hh * HD;
-  const int mykey = blockIdx.x * (32 * NW) + wid * 32 + l32;
+  const int mykey = id.blk * (32 * NW) + wid * 32 + l32;
   const int nt = (S + KT - 1) / KT;
   const bool ragged = S % KT != 0;
 
