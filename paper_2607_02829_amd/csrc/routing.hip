@@ -8,19 +8,48 @@ namespace sr {
 
 constexpr int kRowsPerBlock = 4;   // one wave per row, 4 waves per workgroup
 
-// h0[b,k,:] = x[b, idx[b,k], :]
+// h0[b,k,:] = x[b, idx[b,k], :]: two rows per wave, each pass issuing all of its loads (two
+// 16-byte chunks per lane and row) before its stores.  Non-temporal accesses: a gathered row is
+// read once and the copy is not re-read by this kernel, and keeping both out of the caches'
+// replacement measured 0.59 -> 0.77 of 8 TB/s at 262144 rows of 2 KB.
+constexpr int kGatherRows = 2;   // rows per wave
+
 __global__ __launch_bounds__(256) void gather_kernel(const i32x4* __restrict__ x,
                                                      const int32_t* __restrict__ idx,
                                                      i32x4* __restrict__ h0, int B, int L, int K,
                                                      int chunks, int shared) {
   const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
-  if (r >= B * K) return;
-  const int b = r / K, k = r - b * K;
-  const int i = idx[(shared ? 0 : b) * K + k];
-  const i32x4* src = x + ((size_t)b * L + i) * chunks;
-  i32x4* dst = h0 + (size_t)r * chunks;
-  for (int c = lane; c < chunks; c += 64) dst[c] = src[c];
+  const int r0 = (blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6)) * kGatherRows;
+  if (r0 >= B * K) return;
+  const i32x4* src[kGatherRows];
+  i32x4* dst[kGatherRows];
+  bool ok[kGatherRows];
+#pragma unroll
+  for (int q = 0; q < kGatherRows; ++q) {
+    const int r = r0 + q;
+    ok[q] = r < B * K;
+    const int b = ok[q] ? r / K : 0, k = ok[q] ? r - b * K : 0;
+    const int i = ok[q] ? idx[(shared ? 0 : b) * K + k] : 0;
+    src[q] = x + ((size_t)b * L + i) * chunks;
+    dst[q] = h0 + (size_t)r * chunks;
+  }
+  for (int c0 = 0; c0 < chunks; c0 += 128) {
+    i32x4 v[kGatherRows][2];
+#pragma unroll
+    for (int q = 0; q < kGatherRows; ++q)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int c = c0 + 64 * u + lane;
+        if (ok[q] && c < chunks) v[q][u] = __builtin_nontemporal_load(src[q] + c);
+      }
+#pragma unroll
+    for (int q = 0; q < kGatherRows; ++q)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int c = c0 + 64 * u + lane;
+        if (ok[q] && c < chunks) __builtin_nontemporal_store(v[q][u], dst[q] + c);
+      }
+  }
 }
 
 // x[b,i,:] = rnd(f32(x[b,i,:]) + (f32(h[b,k,:]) - f32(h0[b,k,:]))), i = idx[b,k]
@@ -157,7 +186,8 @@ hipError_t launch_scatter_f32_delta(int dtype, int B, int L, int K, int D, void*
 hipError_t launch_gather(int elt, int B, int L, int K, int D, const void* x, const int32_t* idx, void* h0,
                          int shared, hipStream_t st) {
   const int chunks = D * elt / 16;
-  dim3 g((B * K + kRowsPerBlock - 1) / kRowsPerBlock);
+  constexpr int rows = kRowsPerBlock * kGatherRows;
+  dim3 g((B * K + rows - 1) / rows);
   hipLaunchKernelGGL(gather_kernel, g, dim3(256), 0, st, (const i32x4*)x, idx, (i32x4*)h0, B, L, K, chunks,
                      shared);
   return hipGetLastError();
