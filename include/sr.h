@@ -47,8 +47,9 @@
  *  - Support: D % 64 == 0, F % 64 == 0, D <= 2048, head dim D/H in {32, 64, 128}
  *    (bf16 with head dim 64 or 128 runs the MFMA attention kernels, fp32 storage and
  *    head dim 32 a generic fp32-accumulating kernel); 1 <= K <= L; B*L*D*elt < 2^31 bytes per
- *    token tensor, and for the block-stack calls also B*L*max(F, 3D)*4 < 2^31
- *    (internal fp32 buffers).  Anything else returns SR_EUNSUPPORTED.
+ *    token tensor, and for the block-stack calls also B*S*max(F, 3D)*4 < 2^31 with S the
+ *    call's rows per sample (the S or K routed tokens; L for the dense calls), which size the
+ *    internal fp32 buffers.  Anything else returns SR_EUNSUPPORTED.
  */
 #ifndef SR_H
 #define SR_H

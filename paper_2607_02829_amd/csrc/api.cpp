@@ -52,7 +52,9 @@ size_t elt_of(int dtype) { return dtype == SR_BF16 ? 2 : 4; }
 
 // Routing-only calls (selection, gather, scatter, index validation) touch [B, L, D] tensors, whose
 // byte offsets must fit 31 bits; the block stack also keeps [B*S, max(F, 3D)] fp32 buffers.
-sr_status check_cfg(const sr_config* c, bool routing_only = false) {
+// rows: the stack's rows per sample in the call (S or K routed tokens; L when not given), which
+// sizes its activation buffers.
+sr_status check_cfg(const sr_config* c, bool routing_only = false, int64_t rows = 0) {
   SR_CHECK(c != nullptr, SR_EINVAL, "cfg is NULL");
   SR_CHECK(c->dtype == SR_F32 || c->dtype == SR_BF16, SR_EDTYPE, "unknown dtype %d", c->dtype);
   SR_CHECK(c->kind == SR_BLOCK_PRELN || c->kind == SR_BLOCK_ADALN, SR_EINVAL, "unknown block kind %d", c->kind);
@@ -69,8 +71,11 @@ sr_status check_cfg(const sr_config* c, bool routing_only = false) {
   const size_t tok = (size_t)c->B * c->L * c->D * (c->dtype == SR_BF16 ? 2 : 4);
   SR_CHECK(tok < (1ull << 31), SR_EUNSUPPORTED, "token tensors beyond 2 GiB are not supported");
   if (!routing_only) {
-    const size_t big = (size_t)c->B * c->L * (size_t)std::max(c->F, 3 * c->D) * 4;
-    SR_CHECK(big < (1ull << 31), SR_EUNSUPPORTED, "stack buffers beyond 2 GiB are not supported");
+    const int64_t r = rows > 0 && rows <= c->L ? rows : c->L;
+    const size_t big = (size_t)c->B * (size_t)r * (size_t)std::max(c->F, 3 * c->D) * 4;
+    SR_CHECK(big < (1ull << 31), SR_EUNSUPPORTED,
+             "stack buffers beyond 2 GiB are not supported (B=%d x %lld rows x max(F, 3D) x 4 bytes)", c->B,
+             (long long)r);
   }
   return SR_OK;
 }
@@ -156,7 +161,7 @@ const char* sr_last_error(void) { return g_err.c_str(); }
 const char* sr_version(void) { return "libsr 0.1 (gfx950)"; }
 
 sr_status sr_workspace_bytes(const sr_config* cfg, int32_t S, size_t* saved_bytes, size_t* scratch_bytes) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, false, S);
   if (s != SR_OK) return s;
   SR_CHECK(S >= 1, SR_EINVAL, "S=%d must be >= 1", S);
   sr::Dims d = dims_of(cfg, S);
@@ -263,7 +268,7 @@ sr_status sr_sparse_blocks_fwd(const sr_config* cfg, int32_t S, const sr_block_p
                                const void* h_in, void* h_out, void* saved, size_t saved_bytes, void* scratch,
                                size_t scratch_bytes, void* stream) {
   (void)scratch; (void)scratch_bytes;
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, false, S);
   if (s != SR_OK) return s;
   SR_CHECK(S >= 1 && S <= cfg->L, SR_ESHAPE, "S=%d outside [1, L=%d]", S, cfg->L);
   SR_CHECK(cfg->n_blocks >= 1, SR_EINVAL, "n_blocks must be >= 1");
@@ -280,7 +285,7 @@ sr_status sr_sparse_blocks_bwd(const sr_config* cfg, int32_t S, const sr_block_p
                                const void* saved, size_t saved_bytes, const void* dh_out, void* dh_in,
                                const sr_block_grads* grads, float* dcond, void* scratch, size_t scratch_bytes,
                                void* stream) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, false, S);
   if (s != SR_OK) return s;
   SR_CHECK(S >= 1 && S <= cfg->L, SR_ESHAPE, "S=%d outside [1, L=%d]", S, cfg->L);
   SR_CHECK(cfg->n_blocks >= 1, SR_EINVAL, "n_blocks must be >= 1");
@@ -298,7 +303,7 @@ sr_status sr_sparse_blocks_bwd(const sr_config* cfg, int32_t S, const sr_block_p
 
 sr_status sr_routed_blocks_fwd(const sr_config* cfg, int32_t K, const int32_t* idx, const sr_block_params* params,
                                const void* cond, void* x, void* saved, size_t saved_bytes, void* stream) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, false, K);
   if (s != SR_OK) return s;
   SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
   SR_CHECK(cfg->n_blocks >= 1, SR_EINVAL, "n_blocks must be >= 1");
@@ -318,7 +323,7 @@ sr_status sr_routed_blocks_bwd(const sr_config* cfg, int32_t K, const int32_t* i
                                const void* cond, const void* saved, size_t saved_bytes, void* g,
                                const sr_block_grads* grads, float* dcond, void* scratch, size_t scratch_bytes,
                                void* stream) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, false, K);
   if (s != SR_OK) return s;
   SR_CHECK(K >= 1 && K <= cfg->L, SR_ESHAPE, "K=%d outside [1, L=%d]", K, cfg->L);
   SR_CHECK(cfg->n_blocks >= 1, SR_EINVAL, "n_blocks must be >= 1");
@@ -359,7 +364,7 @@ sr_status sr_dense_blocks_bwd(const sr_config* cfg, const sr_block_params* param
 
 sr_status sr_attention_colsums(const sr_config* cfg, int32_t S, const void* saved, size_t saved_bytes, int32_t block,
                                float* colsum, void* stream) {
-  sr_status s = check_cfg(cfg);
+  sr_status s = check_cfg(cfg, false, S);
   if (s != SR_OK) return s;
   SR_CHECK(S >= 1 && S <= cfg->L, SR_ESHAPE, "S=%d outside [1, L=%d]", S, cfg->L);
   SR_CHECK(block >= 0 && block < cfg->n_blocks, SR_EINVAL, "block %d outside [0, n_blocks=%d)", block,

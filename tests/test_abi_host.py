@@ -52,6 +52,18 @@ def test_workspace_sizes_scale_with_tokens():
     assert s2 - 2 * (s3 - s2) >= 2 * 100 * (256 + 1024) * 2   # plus the shared temporaries
 
 
+def test_stack_buffer_limit_counts_the_calls_rows():
+    # 0.25 deg shape at B = 16: the routed stack's K = 4050 rows per sample stay below the 2 GiB
+    # of its fp32 buffers (16 x 4050 x 4096 x 4 bytes), the dense one's L = 16200 rows do not
+    _lib_or_skip()
+    cfg = _cfg(B=16, L=16200, D=1024, H=16, F=4096, n_blocks=12)
+    saved, scratch = abi.sr_workspace_bytes(cfg, 4050)
+    assert saved > 0 and scratch > 0
+    with pytest.raises(abi.SrError) as ei:
+        abi.sr_workspace_bytes(cfg, 16200)
+    assert ei.value.status == abi.SR_EUNSUPPORTED and "2 GiB" in abi.sr_last_error()
+
+
 @pytest.mark.parametrize("kw,status", [
     (dict(D=250), abi.SR_ESHAPE),          # D % H != 0  (250 % 4)
     (dict(D=192, H=4, F=768), abi.SR_EUNSUPPORTED),   # head dim 48
