@@ -602,6 +602,49 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
   }
 }
 
+// Several reductions in one launch (the weight gradients of one block): job j takes blocks
+// [first[j], first[j + 1]) and does exactly what reduce_splits_kernel does for it.
+struct ReduceJobs {
+  ReduceJob job[kMaxReduceJobs];
+  int first[kMaxReduceJobs + 1];
+};
+__global__ __launch_bounds__(256) void reduce_jobs_kernel(ReduceJobs rj) {
+  int j = 0;
+  while (j + 1 < kMaxReduceJobs && (int)blockIdx.x >= rj.first[j + 1]) ++j;
+  const ReduceJob& b = rj.job[j];
+  const size_t n4 = b.splits > 1 ? b.n / 4 : 0;
+  const size_t i = (size_t)(blockIdx.x - rj.first[j]) * 256 + threadIdx.x;
+  if (i < n4) {
+    const f32x4* p = reinterpret_cast<const f32x4*>(b.part);
+    f32x4 s = p[i];
+    for (int z = 1; z < b.splits; ++z) s += p[(size_t)z * n4 + i];
+    reinterpret_cast<f32x4*>(b.out)[i] = s;
+  } else if (b.dbout && i - n4 < (size_t)b.nb) {
+    const size_t c = i - n4;
+    float s = b.dbpart[c];
+    for (int z = 1; z < b.dbparts; ++z) s += b.dbpart[(size_t)z * b.nb + c];
+    b.dbout[c] = s;
+  }
+}
+
+hipError_t launch_reduce_jobs(const ReduceJob* jobs, int njobs, hipStream_t st) {
+  ReduceJobs rj{};
+  int blocks = 0, k = 0;
+  for (int j = 0; j < njobs && k < kMaxReduceJobs; ++j) {
+    const ReduceJob& b = jobs[j];
+    const size_t total = (b.splits > 1 ? b.n / 4 : 0) + (b.dbout ? b.nb : 0);
+    if (total == 0) continue;
+    rj.job[k] = b;
+    rj.first[k] = blocks;
+    blocks += (int)((total + 255) / 256);
+    ++k;
+  }
+  if (blocks == 0) return hipSuccess;
+  for (int j = k; j <= kMaxReduceJobs; ++j) rj.first[j] = blocks;
+  hipLaunchKernelGGL(reduce_jobs_kernel, dim3((unsigned)blocks), dim3(256), 0, st, rj);
+  return hipGetLastError();
+}
+
 static hipError_t launch_reduce(const float* part, int splits, size_t n, float* out, const float* dbpart, int dbparts,
                                 int nb, float* dbout, hipStream_t st) {
   const size_t n4 = splits > 1 ? n / 4 : 0;
@@ -833,7 +876,9 @@ void weight_grad_scratch(int M, int N, int K, size_t* part_floats, size_t* dbpar
   *dbpart_floats = (size_t)p.splits * p.tiles_n * M;
 }
 
-hipError_t launch_weight_grad(const GemmDesc& g, float* dw, float* db, float* part, float* dbpart, hipStream_t st) {
+hipError_t launch_weight_grad(const GemmDesc& g, float* dw, float* db, float* part, float* dbpart, hipStream_t st,
+                              ReduceJob* defer) {
+  if (defer) *defer = ReduceJob{};
   EpiArgs ep;
   ep.ldo = g.N;
   if (!g.use_mfma) {
@@ -850,8 +895,13 @@ hipError_t launch_weight_grad(const GemmDesc& g, float* dw, float* db, float* pa
   ep.dbpart = dbpart;
   hipError_t e = run_shape<EPI_DW, bf16_t, bf16_t>(p.shape, g, ep, p.splits, p.kps, st);
   if (e != hipSuccess) return e;
-  if (p.splits > 1 || (db && nparts > 1))
+  if (p.splits > 1 || (db && nparts > 1)) {
+    if (defer) {
+      *defer = ReduceJob{part, p.splits, (size_t)g.M * g.N, dw, dbpart, nparts, g.M, nparts > 1 ? db : nullptr};
+      return hipSuccess;
+    }
     return launch_reduce(part, p.splits, (size_t)g.M * g.N, dw, dbpart, nparts, g.M, nparts > 1 ? db : nullptr, st);
+  }
   return hipSuccess;
 }
 

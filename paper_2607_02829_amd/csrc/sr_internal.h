@@ -131,7 +131,25 @@ hipError_t launch_attn_delta(int dtype, const void* dO, const void* O, int B, in
 hipError_t launch_gemm(const GemmDesc& g, int epi, const EpiArgs& ep, hipStream_t st);
 // Weight gradient dW[M x N] = sum_k A(m, k) B(n, k) over tokens k (both operands token-major)
 // and db[m] = sum_k A(m, k) (optional).  part / dbpart: scratch of the sizes below.
-hipError_t launch_weight_grad(const GemmDesc& g, float* dw, float* db, float* part, float* dbpart, hipStream_t st);
+// A weight gradient's reduction of its split-K planes (part: splits planes of n) into out and of
+// its bias-gradient partial rows (dbparts rows of nb) into dbout, in part order.
+struct ReduceJob {
+  const float* part = nullptr;
+  int splits = 1;
+  size_t n = 0;
+  float* out = nullptr;
+  const float* dbpart = nullptr;
+  int dbparts = 1;
+  int nb = 0;
+  float* dbout = nullptr;
+};
+constexpr int kMaxReduceJobs = 4;
+// With defer, the reduction the weight gradient needs (if any) is described there instead of
+// launched; launch_reduce_jobs then runs up to kMaxReduceJobs of them in one launch, with the
+// arithmetic and order of the single ones.
+hipError_t launch_weight_grad(const GemmDesc& g, float* dw, float* db, float* part, float* dbpart, hipStream_t st,
+                              ReduceJob* defer = nullptr);
+hipError_t launch_reduce_jobs(const ReduceJob* jobs, int njobs, hipStream_t st);
 void weight_grad_scratch(int M, int N, int K, size_t* part_floats, size_t* dbpart_floats);
 
 bool attn_uses_mfma(int dtype, int hd);

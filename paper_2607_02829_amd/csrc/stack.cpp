@@ -102,6 +102,10 @@ size_t layout_saved(const Dims& d, char* base, BlockSaved* out) {
   return c.off;
 }
 
+// weight-gradient kinds: rows and columns of dW as {0: 3D, 1: D, 2: F} and {1: D, 2: F}
+enum { kWgQkv = 0, kWgO = 1, kWgFc1 = 2, kWgFc2 = 3 };
+static const int kWeightGradShapes[4][2] = {{0, 1}, {1, 1}, {2, 1}, {1, 2}};
+
 size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   Carver c(base);
   const size_t M = d.M, D = d.D, F = d.F, e = d.elt;
@@ -110,17 +114,14 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   s.g_res2 = c.take<float>(M * D * 4);
   s.du = c.take<float>(M * D * 4);
   s.delta = c.take<float>((size_t)d.B * d.H * d.S * 4);
-  size_t wp = 0, dbp = 0, wmax_out = 0;
-  const int shapes[4][2] = {{3 * d.D, d.D}, {d.D, d.D}, {d.F, d.D}, {d.D, d.F}};
-  for (auto& sh : shapes) {
+  for (int k = 0; k < 4; ++k) {
+    const int* sh = kWeightGradShapes[k];
+    const int rows = sh[0] == 0 ? 3 * d.D : sh[0] == 1 ? d.D : d.F, cols = sh[1] == 1 ? d.D : d.F;
     size_t pf = 0, df = 0;
-    if (d.dtype == kBF16) weight_grad_scratch(sh[0], sh[1], d.M, &pf, &df);
-    wp = std::max(wp, pf);
-    dbp = std::max(dbp, df);
-    wmax_out = std::max(wmax_out, (size_t)sh[0] * sh[1]);
+    if (d.dtype == kBF16) weight_grad_scratch(rows, cols, d.M, &pf, &df);
+    s.wpart[k] = c.take<float>((pf + (size_t)rows * cols) * 4);   // split partials, then an unwanted dW
+    s.dbpart[k] = c.take<float>(std::max<size_t>(df, 1) * 4);
   }
-  s.wpart = c.take<float>((wp + wmax_out) * 4);   // split partials, then room for an unwanted dW
-  s.dbpart = c.take<float>(std::max<size_t>(dbp, 1) * 4);
   const size_t wmax = std::max<size_t>(std::max<size_t>(3 * D, F), 6 * D);
   s.part = c.take<float>((size_t)d.B * colsum_chunks(d.S) * wmax * 4);
   // LayerNorm parameter-gradient partials of LN2 and LN1 (pre-LN: their reductions run on the
@@ -228,16 +229,19 @@ namespace {
 
 // dW[N x K] = sum_m dY[m, n] X[m, k] and db[n] = sum_m dY[m, n], both operands token-major
 // ([M, N] and [M, K]); the GEMM layer picks the tile shape and any split over tokens.
+// The reduction it needs (split planes, bias partial rows) is left in *job, for one launch per
+// block (launch_reduce_jobs).
 hipError_t weight_grad(const char* name, const Dims& d, const void* dY, int N, const void* X, int K, float* out,
-                       float* db, const Scratch& sc, hipStream_t st) {
+                       float* db, const Scratch& sc, int kind, ReduceJob* job, hipStream_t st) {
+  *job = ReduceJob{};
   if (!out && !db) return hipSuccess;
   const size_t e = d.elt;
   GemmDesc g = desc(d, dY, false, N, (size_t)d.M * N * e, X, false, K, (size_t)d.M * K * e, N, K, d.M);
   size_t pf = 0, df = 0;
   if (g.use_mfma) weight_grad_scratch(N, K, d.M, &pf, &df);
-  float* dw = out ? out : sc.wpart + pf;   // the kernel always produces dW; park an unwanted one in scratch
+  float* dw = out ? out : sc.wpart[kind] + pf;   // the kernel always produces dW; park an unwanted one
   ProfScope ps(name, gemm_flops(N, K, d.M), gemm_bytes(d, N, K, d.M, 4), st);
-  return launch_weight_grad(g, dw, db, sc.wpart, sc.dbpart, st);
+  return launch_weight_grad(g, dw, db, sc.wpart[kind], sc.dbpart[kind], st, job);
 }
 
 // dmod[b, off + c] = sum_s X[b,s,c] * Y[b,s,c]  (adaLN gate gradients)
@@ -383,6 +387,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       const int par = i & 1;
       void* const dz = sc.dz[par];
       void* const dqkv = sc.dqkv[par];
+      ReduceJob jobs[4];   // this block's weight-gradient reductions, launched after dW_qkv
       if (ada) {
         // MLP-branch gradient dm = dh' * gate2 (activation copy) and dgate2 = sum_s dh' * m_out
         SR_TRY(join(kFc2));   // g0 may still be read by the previous block's dW_fc2
@@ -397,7 +402,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
           ProfScope ps("recompute", 0, (double)M * F * e * 2, ss);
           SR_TRY(launch_gelu(d.dtype, s.z, sc.gz_rc, (size_t)M * F, ss));
         }
-        return weight_grad("gemm_dw_fc2", d, g0, D, sc.gz_rc, F, g.w_fc2, g.b_fc2, sc, ss);
+        return weight_grad("gemm_dw_fc2", d, g0, D, sc.gz_rc, F, g.w_fc2, g.b_fc2, sc, kWgFc2, &jobs[kWgFc2], ss);
       }));
       ln1_pending = nullptr;
       SR_TRY(join(kFc1 + par));   // dz[par] may still be read by dW_fc1 two blocks back
@@ -414,7 +419,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
           SR_TRY(launch_ln_apply(d.dtype, s.h1, w.ln2_w, w.ln2_b, ada ? s.mod : nullptr, 3 * D, M, S, D, s.mean2,
                                  s.rstd2, sc.u_rc, ss));
         }
-        return weight_grad("gemm_dw_fc1", d, dz, F, sc.u_rc, D, g.w_fc1, g.b_fc1, sc, ss);
+        return weight_grad("gemm_dw_fc1", d, dz, F, sc.u_rc, D, g.w_fc1, g.b_fc1, sc, kWgFc1, &jobs[kWgFc1], ss);
       }));
       {
         GemmDesc gd = desc(d, dz, true, F, (size_t)M * F * e, w.w_fc1, false, D, (size_t)F * D * e, M, D, F);
@@ -444,7 +449,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       // delta = rowsum(dO * O) per head in the same epilogue when the head dim is 64)
       SR_TRY(on_side(kO, [&](hipStream_t ss) -> hipError_t {
         if (!ada) SR_TRY(ln_reduce(0, g.ln2_w, g.ln2_b, ss));
-        return weight_grad("gemm_dw_o", d, g1, D, s.O, D, g.w_o, g.b_o, sc, ss);
+        return weight_grad("gemm_dw_o", d, g1, D, s.O, D, g.w_o, g.b_o, sc, kWgO, &jobs[kWgO], ss);
       }));
       const bool fuse_delta = d.dtype == kBF16 && D / d.H == 64;
       {
@@ -468,7 +473,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
           SR_TRY(launch_ln_apply(d.dtype, s.hin, w.ln1_w, w.ln1_b, ada ? s.mod : nullptr, 0, M, S, D, s.mean1,
                                  s.rstd1, sc.u_rc, ss));
         }
-        return weight_grad("gemm_dw_qkv", d, dqkv, 3 * D, sc.u_rc, D, g.w_qkv, g.b_qkv, sc, ss);
+        SR_TRY(weight_grad("gemm_dw_qkv", d, dqkv, 3 * D, sc.u_rc, D, g.w_qkv, g.b_qkv, sc, kWgQkv, &jobs[kWgQkv],
+                           ss));
+        // the block's four weight-gradient reductions in one launch, in the order of the single ones
+        ProfScope ps("reduce_dw", 0, 0, ss);
+        return launch_reduce_jobs(jobs, 4, ss);
       }));
       {
         GemmDesc gd = desc(d, dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,

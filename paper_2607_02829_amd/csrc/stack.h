@@ -21,7 +21,11 @@ struct BlockSaved {
 };
 
 struct Scratch {
-  float *g_res, *g_res2, *du, *delta, *wpart, *dbpart, *part, *lnpart[2], *dmod, *gvpart;
+  // weight-gradient partials per kind (QKV, output projection, FC1, FC2): split planes, then room
+  // for an unwanted dW; bias-gradient partial rows.  One set per kind, so that a block's four
+  // reductions can run as one launch after its last weight gradient.
+  float *wpart[4], *dbpart[4];
+  float *g_res, *g_res2, *du, *delta, *part, *lnpart[2], *dmod, *gvpart;
   void *g_act[2], *dz[2], *dO, *dqkv[2], *u_rc, *gz_rc;
 };
 
