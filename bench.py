@@ -475,6 +475,7 @@ def summarize_pmc(group: str, workload: str, fetch_csv: str, write_csv: str, com
 
 
 # routing kernels: symbol -> (label, algorithmic bytes of one dispatch on `rows` rows of D columns)
+# kernel symbol: (what it does, algorithmic bytes for `rows` routed rows of D columns)
 ROUTING_KERNELS = {
     "gather_kernel": ("gather (h0 = x[idx], bf16)", lambda rows, D: 2 * rows * D * 2 + 4 * rows),
     "scatter_delta_kernel": ("residual-delta scatter, h0 re-read from x (bf16)", lambda rows, D: 3 * rows * D * 2 + 4 * rows),
@@ -485,6 +486,7 @@ ROUTING_KERNELS = {
                       lambda rows, D: rows * D * 8 + 12 * rows),
 }
 ROUTING_ROWS_PER_BLOCK = 4   # one wave per row, four waves per 256-thread workgroup
+ROUTING_ROWS_PER_WAVE = {"gather_kernel": 2}   # the others take one row per wave
 
 
 def summarize_routing_pmc(fetch_csv: str, write_csv: str, command: str, D: int = 1024) -> str:
@@ -513,7 +515,8 @@ def summarize_routing_pmc(fetch_csv: str, write_csv: str, command: str, D: int =
         "",
         "rocprofv3 counter passes (one counter per run), KiB per dispatch averaged over the dispatches",
         f"of one kernel and grid size, scaled by the same counters on a {COPY_PROBE_BYTES}-byte device copy",
-        f"(FETCH_SIZE x {f_scale:.4f}, WRITE_SIZE x {w_scale:.4f}); rows = one wave per row (grid threads / 64);",
+        f"(FETCH_SIZE x {f_scale:.4f}, WRITE_SIZE x {w_scale:.4f}); rows = grid threads / 64 x rows per wave",
+        "(two for the gather, one for the others; the grid's last workgroup may be partly idle);",
         "algorithmic bytes as in `bench.py` (one read of each input, one write of each output).",
         "",
         "Commands (repository root on the GPU box, `cd /tmp && export TMPDIR=/tmp` first):",
@@ -533,7 +536,7 @@ def summarize_routing_pmc(fetch_csv: str, write_csv: str, command: str, D: int =
             targs = name.split("(")[0].split("<", 1)[-1].rstrip(">").split(", ")
             if len(targs) < 5 or targs[4] != "true":
                 continue
-        rows = grid // 64
+        rows = grid // 64 * ROUTING_ROWS_PER_WAVE.get(sym, 1)
         f = statistics.mean(fv) * 1024.0 * f_scale
         w = statistics.mean(write[(name, grid)]) * 1024.0 * w_scale
         alg = ROUTING_KERNELS[sym][1](rows, D)
