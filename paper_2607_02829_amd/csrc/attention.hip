@@ -70,6 +70,13 @@ SR_DEV bf16x8 zero8() {
 }
 
 SR_DEV bf16x8 ld8(const bf16_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
+// sign flip of eight bf16 values (exact)
+SR_DEV bf16x8 neg8(bf16x8 v) {
+  i32x4 w = __builtin_bit_cast(i32x4, v);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w[i] ^= (int)0x80008000u;
+  return __builtin_bit_cast(bf16x8, w);
+}
 
 SR_DEV f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) { return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0); }
 
@@ -438,11 +445,13 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dkv_m
   const int nt = (Sq + KT - 1) / KT;
   const bool ragged = Sq % KT != 0;
 
+  // K and -V fragments of the wave's keys (V negated: dP - Delta is then accumulated as
+  // Delta + dO (-V)^T, starting from Delta, which saves a subtraction per score)
   bf16x8 kf[KS], vf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     kf[ks] = mykey < Skv ? ld8(kp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8();
-    vf[ks] = mykey < Skv ? ld8(vp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8();
+    vf[ks] = neg8(mykey < Skv ? ld8(vp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8());
   }
   f32x16 dv[DB], dk[DB];
 #pragma unroll
@@ -469,9 +478,16 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dkv_m
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) sv = mfma(row_frag<HD>(Qs, u * 32, ks), kf[ks], sv);
   };
+  // Delta - dP (= -(dP - Delta)): the accumulator starts from the Delta of the register's query
+  // (rows 8 g + 4 h32 .. + 3 for registers 4 g .. 4 g + 3) and adds dO (-V)^T
   auto dp_of = [&](int s, int u, f32x16& dpv) {
     const bf16_t* dOs = smem + s * 2 * TE + TE;
-    zero16(dpv);
+    const float* dls = fsm + s * 2 * KT + KT + u * 32 + 4 * h32;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 d4 = *reinterpret_cast<const float4*>(dls + 8 * g);
+      dpv[4 * g] = d4.x; dpv[4 * g + 1] = d4.y; dpv[4 * g + 2] = d4.z; dpv[4 * g + 3] = d4.w;
+    }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) dpv = mfma(row_frag<HD>(dOs, u * 32, ks), vf[ks], dpv);
   };
@@ -480,13 +496,12 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dkv_m
     f32x16 dpv;
     dp_of(s, u, dpv);
     const float* ls = fsm + s * 2 * KT + u * 32;
-    const float* dls = ls + KT;
     bf16x8 pb[2], sb[2];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int ql = srow(r, h32);
       float p = ex2(fmaf(sv[r], sl2, -ls[ql]));
-      float ds = p * (dpv[r] - dls[ql]);
+      float ds = -p * dpv[r];
       if constexpr (decltype(rag)::value) {
         if (q0 + ql >= Sq) { p = 0.f; ds = 0.f; }
       }
@@ -571,14 +586,19 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dq_mf
   const int nt = (Skv + KT - 1) / KT;
   const bool ragged = Skv % KT != 0;
 
+  // Q and -dO fragments of the wave's queries (dO negated: dP - Delta is then accumulated as
+  // Delta + V (-dO)^T from a constant start, which saves a subtraction per score)
   bf16x8 qf[KS], df[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     qf[ks] = myq < Sq ? ld8(qp + (size_t)myq * ldq + ks * 16 + 8 * h32) : zero8();
-    df[ks] = myq < Sq ? ld8(dop + (size_t)myq * D + ks * 16 + 8 * h32) : zero8();
+    df[ks] = neg8(myq < Sq ? ld8(dop + (size_t)myq * D + ks * 16 + 8 * h32) : zero8());
   }
   const float nlse = myq < Sq ? -lse[((size_t)b * H + hh) * Sq + myq] : -INFINITY;
   const float dl_q = myq < Sq ? delta[((size_t)b * H + hh) * Sq + myq] : 0.f;
+  f32x16 dl16;   // the dP^T accumulator's start: Delta of the lane's query in every register
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dl16[r] = dl_q;
   f32x16 dq[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) zero16(dq[db]);
@@ -602,7 +622,8 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dq_mf
   };
   // S^T = K Q^T and dP^T = V dO^T of a key unit: register r holds key srow(r), query l32
   auto sd = [&](RawFrag<true> (&kr)[KS], RawFrag<true> (&vr)[KS], f32x16& sv, f32x16& dpv) {
-    zero16(sv); zero16(dpv);
+    zero16(sv);
+    dpv = dl16;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       sv = mfma(kr[ks].settle(), qf[ks], sv);
@@ -623,7 +644,7 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dq_mf
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const float p = ex2(fmaf(sv[r], sl2, nlse));
-      float ds = p * (dpv[r] - dl_q);
+      float ds = -p * dpv[r];
       if constexpr (decltype(rag)::value) {
         if (k0 + srow(r, h32) >= Skv) ds = 0.f;
       }
