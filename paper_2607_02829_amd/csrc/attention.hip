@@ -562,6 +562,388 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dkv_m
   unstage<HD, NW>(smem, out + D + hh * HD, ldo, id.blk * (32 * NW), Skv);
 }
 
+// ------------------------------------------------------ backward dK, dV at head dim 128: one wave per SIMD
+// Four waves of 32 keys (128 keys per workgroup), one per SIMD with the whole register file, the
+// work of consecutive 32-query units overlapped inside each wave:
+//   unit j:  X_j = [S_j = Q_j K^T, dP_j = dO_j V^T]   (16 MFMAs, VGPR results)
+//            V_j = [P_j = exp2(S_j sl2 - lse), dS_j = P_j (dP_j - Delta)]   (vector work)
+//            Y_j = [dV^T += dO_j^T P_j, dK^T += Q_j^T dS_j]   (16 MFMAs into AGPR accumulators)
+// Step j issues X_{j+1} under V_j, then Y_j.  At head dim 128 a unit has 32 MFMAs (1 024 cycles)
+// for about 80 vector instructions, so one wave can issue both; the compiler-scheduled kernel
+// keeps its accumulators and operands in AGPRs at this register count and moves the scores back
+// and forth through accumulator copies.
+// Every MFMA and fragment read is inline assembly with explicit register classes: K, V (B operands
+// of X), the Q / dO row fragments (A operands of X) and the accumulators in AGPRs, which gfx950
+// MFMAs read and LDS reads write directly (240 AGPRs: K, V 64, accumulators 128, row fragments 48 in a
+// ring of twelve slots);
+// scores, dP, lse, Delta, P, dS and the transposed fragments (two 8-byte reads form one operand)
+// in VGPRs.  The compiler cannot see into the assembly, so the hazards it would cover are covered
+// explicitly: s_nop before the vector unit reads MFMA results, before MFMAs read vector results,
+// and before the accumulators are read out.
+// Each step is 32 regions of one MFMA (and one or two score registers of vector work, split in two
+// parts one region apart so that no instruction waits on another of its own region).  Fragment
+// reads are issued after the MFMA that last read the register they overwrite (row fragments run
+// through a ring of twelve slots: X MFMAs 12..15 reuse the slots of X MFMAs 0..3 of the same unit;
+// lse / Delta and the transposed fragments are single-buffered), in a rolling window of at most 15
+// in flight; a read is retired about seven regions after it is issued.
+// LDS: the Q tiles of the four stages in the first 64 KB, the dO tiles in the next 64 KB (every
+// fragment offset fits the instruction's 16-bit offset field), filled two tiles ahead.
+namespace dkvh {
+constexpr int NST = 4;            // LDS stages
+constexpr int NW = 4;             // waves
+constexpr int HD = 128;
+constexpr int KS = HD / 16;       // MFMA k-steps over the head dimension
+constexpr int DB = HD / 32;       // 32-column blocks of the head dimension
+constexpr int TE = KT * HD;       // bf16 elements of a 64-row tile
+constexpr int TBB = TE * 2;       // bytes of a tile (16 KB)
+constexpr int DOFF = NST * TBB;   // byte offset of the dO tiles (64 KB)
+constexpr int LPT = 2 * (TE / 512 / NW) + 1;   // buffer loads per wave per tile (Q, dO, lse / Delta / padding)
+
+template <int OFF>
+SR_DEV i32x4 rd16a(uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  i32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=a"(v) : "v"(a), "i"(OFF));
+  return v;
+}
+template <int OFF>
+SR_DEV i32x4 rd16v(uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  i32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(OFF));
+  return v;
+}
+template <int OFF>
+SR_DEV i32x2 rdtrv(uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  i32x2 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(a), "i"(OFF));
+  return v;
+}
+// c (VGPR) = a * b (+ c), operands in AGPRs (X)
+SR_DEV void mma_v0(f32x16& c, const i32x4& a, const i32x4& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=v"(c) : "a"(a), "a"(b));
+}
+SR_DEV void mma_v(f32x16& c, const i32x4& a, const i32x4& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(c) : "a"(a), "a"(b));
+}
+// c (AGPR) += a * b, operands in VGPRs (Y)
+SR_DEV void mma_a(f32x16& c, const i32x4& a, const i32x4& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+template <typename V>
+SR_DEV void pin_a(V& v) {
+  asm volatile("" : "+a"(v));
+}
+SR_DEV i32x4 join(const i32x2& lo, const i32x2& hi) {
+  i32x4 w;
+  w[0] = lo[0]; w[1] = lo[1]; w[2] = hi[0]; w[3] = hi[1];
+  return w;
+}
+// Region schedule of a step (32 regions): the MFMA of region R is X MFMA R (R < 12), Y MFMA R - 12
+// of query half 0 (12 <= R < 20), X MFMA R - 8 (20 <= R < 24) or Y MFMA R - 24 of half 1.  X MFMA m:
+// k-step m / 2 of S (even m) or of dP (odd m); Y MFMA n: dV^T of column block n / 2 (even
+// n) or dK^T (odd n).
+constexpr int kind_of(int R) { return R < 12 ? 0 : R < 20 ? 1 : R < 24 ? 0 : 2; }   // 0 X, 1 Y half 0, 2 Y half 1
+constexpr int idx_of(int R) { return R < 12 ? R : R < 20 ? R - 12 : R < 24 ? R - 8 : R - 24; }
+// region of part a of score register r (part b one region later): registers 0..7 complete before
+// region 12, 8..15 before region 20
+constexpr int va_region(int r) { return r < 8 ? (r * 3) / 2 : 11 + (r - 8); }
+}  // namespace dkvh
+
+__global__ __launch_bounds__(256, 1) void attn_bwd_dkv_h128(const bf16_t* __restrict__ q, int ldq, uint32_t q_elems,
+                                                            const bf16_t* __restrict__ kv, int ldkv,
+                                                            const bf16_t* __restrict__ dO,
+                                                            const float* __restrict__ lse,
+                                                            const float* __restrict__ delta,
+                                                            bf16_t* __restrict__ dk_out, int ldo, int Sq, int Skv,
+                                                            int H, int D, float sl2, float scale) {
+  using namespace dkvh;
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * NST * TE];   // Q tiles, then dO tiles
+  __shared__ __attribute__((aligned(16))) float fsm[NST * 2 * KT];       // stage: lse, Delta of the tile's rows
+  __shared__ __attribute__((aligned(16))) float fdummy[64];              // target of the padding loads
+  const int lane = threadIdx.x & 63, l32 = lane & 31, h32 = lane >> 5;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const TileId id = xcd_tile_id();
+  const int b = id.b, hh = id.h;
+  const bf16_t* kp = kv + (size_t)b * Skv * ldkv + hh * HD;
+  const bf16_t* vp = kp + D;
+  const int mykey = id.blk * (32 * NW) + wid * 32 + l32;
+  const int nt = (Sq + KT - 1) / KT;
+  const int nu = 2 * nt;   // 32-query units
+  const bool ragged = Sq % KT != 0;
+
+  // K and V fragments of the wave's keys, in AGPRs
+  i32x4 kf[KS], vf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    kf[ks] = __builtin_bit_cast(i32x4, mykey < Skv ? ld8(kp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8());
+    vf[ks] = __builtin_bit_cast(i32x4, mykey < Skv ? ld8(vp + (size_t)mykey * ldkv + ks * 16 + 8 * h32) : zero8());
+  }
+  f32x16 dv[DB], dk[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) { zero16(dv[db]); zero16(dk[db]); }
+  static_for<KS>([&](auto k) { pin_a(kf[k.value]); pin_a(vf[k.value]); });
+  static_for<DB>([&](auto d) { pin_a(dv[d.value]); pin_a(dk[d.value]); });
+  asm volatile("s_nop 7" ::: "memory");   // AGPR writes before the first MFMA reads
+
+  const __amdgpu_buffer_rsrc_t rq = make_rsrc(q, q_elems * 2u);
+  const __amdgpu_buffer_rsrc_t rd = make_rsrc(dO, (uint32_t)((size_t)gridDim.z * Sq * D * 2));
+  const __amdgpu_buffer_rsrc_t rl = make_rsrc(lse, (uint32_t)((size_t)gridDim.z * H * Sq * 4));
+  const __amdgpu_buffer_rsrc_t rdl = make_rsrc(delta, (uint32_t)((size_t)gridDim.z * H * Sq * 4));
+  const uint32_t qbase = (uint32_t)(((size_t)b * Sq * ldq + hh * HD) * 2);
+  const uint32_t dbase = (uint32_t)(((size_t)b * Sq * D + hh * HD) * 2);
+  const uint32_t lbase = (uint32_t)(((size_t)b * H + hh) * Sq * 4);
+  // tile t into stage s: Q and dO (four 16-byte loads each per wave), lse (wave 0), Delta (wave 1)
+  // or a padding load (waves 2, 3: offset past every extent, reads zero, touches no memory), so
+  // that every wave has LPT loads per tile in flight
+  auto fill = [&](int t, int s) __attribute__((always_inline)) {
+    const bool valid = t < nt;
+    tile_load<HD, NW>(rq, qbase, (uint32_t)ldq, t * KT, smem + s * TE, valid);
+    tile_load<HD, NW>(rd, dbase, (uint32_t)D, t * KT, smem + NST * TE + s * TE, valid);
+    const uint32_t lo = valid ? lbase + (uint32_t)(t * KT + lane) * 4u : 0x80000000u;
+    if (wid == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_ptr_t*)(fsm + s * 2 * KT), 4, lo, 0, 0, 0);
+    else if (wid == 1) __builtin_amdgcn_raw_ptr_buffer_load_lds(rdl, (lds_ptr_t*)(fsm + s * 2 * KT + KT), 4, lo, 0, 0, 0);
+    else __builtin_amdgcn_raw_ptr_buffer_load_lds(rl, (lds_ptr_t*)fdummy, 4, 0x80000000u, 0, 0, 0);
+  };
+
+  // per-lane LDS addresses (stage 0, unit 0 of the Q tiles; the dO tiles DOFF bytes on);
+  // stages, units and query halves are instruction offsets
+  const uint32_t sbase = lds_addr(smem);
+  uint32_t ra[KS], rad[KS];   // row fragments: rows lane % 32 of a unit, k-step ks
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    ra[ks] = sbase + (uint32_t)(l32 * HD + (((2 * ks + h32) ^ swz<HD>(l32)) << 3)) * 2u;
+    rad[ks] = ra[ks] + DOFF;
+  }
+  uint32_t ta[DB][2], tad[DB][2];   // transposed fragments: column block db, first / second read
+  {
+    const int g = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int col = 32 * db + 16 * (g & 1) + 4 * (s & 3);
+      const int r1 = 4 * (g >> 1) + (s >> 2), r2 = r1 + 8;
+      ta[db][0] = sbase + (uint32_t)(r1 * HD + (((col >> 3) ^ swz<HD>(r1)) << 3) + (col & 7)) * 2u;
+      ta[db][1] = sbase + (uint32_t)(r2 * HD + (((col >> 3) ^ swz<HD>(r2)) << 3) + (col & 7)) * 2u;
+      tad[db][0] = ta[db][0] + DOFF;
+      tad[db][1] = ta[db][1] + DOFF;
+    }
+  }
+  const uint32_t la = lds_addr(fsm) + 16u * h32;   // lse / Delta: rows 4 h32 .. + 3 of each group of 8
+
+  // row fragments of X (AGPR): X MFMA m (k-step m / 2 of Q for even m, of dO for odd m) reads slot
+  // m % 12
+  i32x4 rf[12];
+  // transposed fragments of Y (VGPR): a ring of eight pairs, pair n = the A operand of Y MFMA n of
+  // either query half (half 1 of a unit is read after half 0's MFMA n, half 0 of the next unit
+  // after half 1's)
+  i32x2 tf[2 * 2 * DB];
+  i32x4 ld[8];                 // lse (groups 0..3), Delta (groups 0..3) of V (VGPR)
+  f32x16 sc[2], dpv[2];        // S and dP of a unit, by parity (VGPR)
+  bf16x8 pb[2], sb[2];         // P and dS in bf16, query halves (VGPR)
+  float pt[16], dt[16];        // part a results of V
+
+  // ---- fragment reads of unit u (U = u % 8: stage (U / 2) % 4, half U % 2)
+  // row fragment of X MFMA M (k-step M / 2 of Q for even M, of dO for odd M) into slot M % 12
+  auto read_row = [&](auto ui, auto mi) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, M = decltype(mi)::value, K = M / 2;
+    constexpr int OFF = ((U / 2) % NST) * TBB + (U % 2) * 32 * HD * 2;
+    if constexpr (M % 2 == 0) rf[M % 12] = rd16a<OFF>(ra[K]);
+    else rf[M % 12] = rd16a<OFF>(rad[K]);
+  };
+  // lse (G = 0..3) or Delta (G = 4..7) group G % 4 of unit u
+  auto read_stat = [&](auto ui, auto gi) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, G = decltype(gi)::value;
+    constexpr int OFF = ((U / 2) % NST) * 2 * KT * 4 + (U % 2) * 32 * 4 + (G >= 4 ? KT * 4 : 0) + (G % 4) * 32;
+    ld[G] = rd16v<OFF>(la);
+  };
+  // transposed fragment pair of Y MFMA N of query half KK into tf[2N], tf[2N+1]: dO^T of column
+  // block N / 2 (even N) or Q^T of column block N / 2 (odd N)
+  auto read_tr = [&](auto ui, auto kki, auto ni) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, KK = decltype(kki)::value, N = decltype(ni)::value;
+    constexpr int C = N / 2;
+    constexpr int OFF = ((U / 2) % NST) * TBB + ((U % 2) * 32 + KK * 16) * HD * 2;
+    if constexpr (N % 2 == 0) {
+      tf[2 * N] = rdtrv<OFF>(tad[C][0]);
+      tf[2 * N + 1] = rdtrv<OFF>(tad[C][1]);
+    } else {
+      tf[2 * N] = rdtrv<OFF>(ta[C][0]);
+      tf[2 * N + 1] = rdtrv<OFF>(ta[C][1]);
+    }
+  };
+  // X MFMA M of the unit whose row fragments are in rf, into sc / dpv [P]
+  auto xmma = [&](auto pi, auto mi) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value, M = decltype(mi)::value, K = M / 2;
+    f32x16& acc = M % 2 ? dpv[P] : sc[P];
+    const i32x4& fr = rf[M % 12];
+    const i32x4& kvf = M % 2 ? vf[K] : kf[K];
+    if constexpr (K == 0) mma_v0(acc, fr, kvf);
+    else mma_v(acc, fr, kvf);
+  };
+  // Y MFMA N of query half KK
+  auto ymma = [&](auto kki, auto ni) __attribute__((always_inline)) {
+    constexpr int KK = decltype(kki)::value, N = decltype(ni)::value, C = N / 2;
+    if constexpr (N % 2 == 0)
+      mma_a(dv[C], join(tf[2 * N], tf[2 * N + 1]), __builtin_bit_cast(i32x4, pb[KK]));
+    else
+      mma_a(dk[C], join(tf[2 * N], tf[2 * N + 1]), __builtin_bit_cast(i32x4, sb[KK]));
+  };
+  // vector work of score register r of the unit in sc / dpv [P] (lse, Delta from ld)
+  auto vpart_a = [&](auto pi, auto ri) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value, r = decltype(ri)::value;
+    pt[r] = ex2(fmaf(sc[P][r], sl2, -__int_as_float(ld[r >> 2][r & 3])));
+    dt[r] = dpv[P][r] - __int_as_float(ld[4 + (r >> 2)][r & 3]);
+  };
+  auto vpart_b = [&](auto ri) __attribute__((always_inline)) {
+    constexpr int r = decltype(ri)::value;
+    pb[r >> 3][r & 7] = (__bf16)pt[r];
+    sb[r >> 3][r & 7] = (__bf16)(pt[r] * dt[r]);
+  };
+  const int rem = Sq - (nt - 1) * KT;   // valid rows of the last tile
+  auto mask_rows = [&](int u) __attribute__((always_inline)) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (u * 32 + 8 * g + 4 * h32 + i >= rem) ld[g][i] = 0x7f800000;   // lse = +inf: P = 0, dS = 0
+  };
+
+  // reads issued in region R of step j, each after the MFMA that last read the registers it
+  // overwrites: rows of X MFMAs 12..15 of unit j+1 (regions 1..4, slots of MFMAs 0..3), of MFMAs
+  // 4..11 of unit j+2 (regions 5..12) and of MFMAs 0..3 of unit j+2 (regions 21..24, after X
+  // MFMAs 12..15 of unit j+1); transposed pairs of unit j, half 1 (regions 13..20, after half 0's
+  // MFMAs) and of unit j+1, half 0 (regions 25..31 and after the last, after half 1's); lse /
+  // Delta of unit j+1 (regions 21..24, after the last vector read of unit j's)
+  auto reads_of = [&](auto ri, auto ui) __attribute__((always_inline)) {
+    constexpr int R = decltype(ri)::value, U = decltype(ui)::value;
+    constexpr int UR = (U + 2) % 8, UN = (U + 1) % 8;
+    constexpr int mrow = (R >= 1 && R <= 4) ? R + 11 : (R >= 5 && R <= 12) ? R - 1 : (R >= 21 && R <= 24) ? R - 21 : -1;
+    constexpr int urow = (R >= 1 && R <= 4) ? UN : UR;
+    constexpr int nrow = mrow >= 0 ? 1 : 0;
+    constexpr int ntr1 = (R >= 13 && R <= 20) ? R - 13 : -1;   // unit j, half 1
+    constexpr int ntr0 = (R >= 25 && R <= 31) ? R - 25 : -1;   // unit j+1, half 0
+    constexpr int ntr = (ntr0 >= 0 || ntr1 >= 0) ? 2 : 0;
+    // lse / Delta of unit j+1 (the last part-a read of ld is in region va_region(15) = 18): regions 21..24
+    constexpr int nst = (R >= 21 && R <= 24) ? 2 : 0;
+    constexpr int n = nrow + ntr + nst;
+    if constexpr (n > 0) {
+      lgkm_wait<15 - n>();
+      if constexpr (mrow >= 0) read_row(IC<urow>{}, IC<mrow>{});
+      if constexpr (ntr1 >= 0) read_tr(IC<U>{}, IC<1>{}, IC<ntr1>{});
+      if constexpr (ntr0 >= 0) read_tr(IC<UN>{}, IC<0>{}, IC<ntr0>{});
+      if constexpr (nst > 0) {
+        read_stat(IC<UN>{}, IC<2 * (R - 21)>{});
+        read_stat(IC<UN>{}, IC<2 * (R - 21) + 1>{});
+      }
+    }
+  };
+
+  auto step = [&](auto ui, int j) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, P = U % 2, Q = 1 - P;
+    if constexpr (P == 0) {
+      // tile boundary: tile j/2 + 1 resident (only tile j/2 + 2's loads still in flight), then
+      // refill the stage of tile j/2 - 1, whose reads all retired during the previous step
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPT) : "memory");
+      lds_barrier();
+      fill(j / 2 + 3, (U / 2 + 3) % NST);
+    }
+    lgkm_wait<14>();   // lse / Delta of unit j, rows 0..11 of unit j+1 retired (sixteen reads followed them)
+    static_for<8>([&](auto g) { pin(ld[g.value]); });
+    if (ragged && j >= nu - 2) mask_rows(P);   // units of the last tile
+    asm volatile("s_nop 11" : "+v"(sc[P]), "+v"(dpv[P]));   // X_j's results readable by the vector unit
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<32>([&](auto ri) {
+      constexpr int R = ri.value, KD = kind_of(R), I = idx_of(R);
+      if constexpr (R == 12) asm volatile("s_nop 4" : "+v"(pb[0]), "+v"(sb[0]));
+      if constexpr (R == 24) asm volatile("s_nop 4" : "+v"(pb[1]), "+v"(sb[1]));
+      if constexpr (KD == 0) xmma(IC<Q>{}, IC<I>{});
+      else ymma(IC<KD - 1>{}, IC<I>{});
+      static_for<16>([&](auto r) {
+        if constexpr (va_region(r.value) == R) vpart_a(IC<P>{}, r);
+        if constexpr (va_region(r.value) + 1 == R) vpart_b(r);
+      });
+      reads_of(ri, ui);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    lgkm_wait<13>();
+    read_tr(IC<(U + 1) % 8>{}, IC<0>{}, IC<7>{});
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // prologue: tiles 0..2 in flight; tile 0 resident; X_0; the reads of step 0
+  fill(0, 0);
+  fill(1, 1);
+  fill(2, 2);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPT) : "memory");
+  lds_barrier();
+  static_for<12>([&](auto m) {
+    if constexpr (m.value == 8) lgkm_wait<7>();
+    read_row(IC<0>{}, m);
+  });
+  lgkm_wait<0>();
+  static_for<12>([&](auto m) { xmma(IC<0>{}, m); });
+  static_for<4>([&](auto m) { read_row(IC<0>{}, IC<12 + m.value>{}); });   // slots of MFMAs 0..3
+  lgkm_wait<0>();
+  static_for<4>([&](auto m) { xmma(IC<0>{}, IC<12 + m.value>{}); });
+  static_for<12>([&](auto m) {   // rows 0..11 of unit 1, after X_0 read the slots
+    if constexpr (m.value % 6 == 0) lgkm_wait<7>();
+    read_row(IC<1>{}, m);
+  });
+  lgkm_wait<7>();
+  static_for<8>([&](auto g) { read_stat(IC<0>{}, g); });
+  static_for<8>([&](auto n) {
+    if constexpr (n.value % 4 == 0) lgkm_wait<7>();
+    read_tr(IC<0>{}, IC<0>{}, n);
+  });
+  __builtin_amdgcn_sched_barrier(0);
+
+  int j = 0;
+  for (; j + 8 <= nu; j += 8) {
+    step(IC<0>{}, j);
+    step(IC<1>{}, j + 1);
+    step(IC<2>{}, j + 2);
+    step(IC<3>{}, j + 3);
+    step(IC<4>{}, j + 4);
+    step(IC<5>{}, j + 5);
+    step(IC<6>{}, j + 6);
+    step(IC<7>{}, j + 7);
+  }
+  if (j < nu) {   // nu - j is 2, 4 or 6
+    step(IC<0>{}, j);
+    step(IC<1>{}, j + 1);
+    if (j + 2 < nu) {
+      step(IC<2>{}, j + 2);
+      step(IC<3>{}, j + 3);
+      if (j + 4 < nu) {
+        step(IC<4>{}, j + 4);
+        step(IC<5>{}, j + 5);
+      }
+    }
+  }
+
+  // The last steps read ahead for units past the end: retire those reads with their destination
+  // registers still held (pinned behind the wait), or the compiler would hand the registers of
+  // reads still in flight to other values.
+  lgkm_wait<0>();
+  static_for<8>([&](auto g) { pin(ld[g.value]); });
+  static_for<12>([&](auto e) { pin_a(rf[e.value]); });
+  static_for<4 * DB>([&](auto f) { pin(tf[f.value]); });
+  // accumulators readable by the vector unit; every load retired
+  static_for<DB>([&](auto d) { pin_a(dv[d.value]); pin_a(dk[d.value]); });
+  asm volatile("s_nop 15\n\ts_nop 15" ::: "memory");
+  static_for<DB>([&](auto d) { pin_a(dv[d.value]); pin_a(dk[d.value]); });
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  bf16_t* out = dk_out + (size_t)b * Skv * ldo;
+  stage_t<HD>(smem, dk, scale, wid, lane);
+  __syncthreads();
+  unstage<HD, NW>(smem, out + hh * HD, ldo, id.blk * (32 * NW), Skv);
+  __syncthreads();
+  stage_t<HD>(smem, dv, 1.0f, wid, lane);
+  __syncthreads();
+  unstage<HD, NW>(smem, out + D + hh * HD, ldo, id.blk * (32 * NW), Skv);
+}
+
 // ------------------------------------------------------------------------------ backward dQ
 
 // NW waves (32 queries each) per workgroup share the K / V tiles.
@@ -985,6 +1367,13 @@ static hipError_t dkv_mfma_hd(const bf16_t* q, int ldq, uint32_t q_elems, const 
                               int Sq, int Skv, int H, int D, hipStream_t st) {
   constexpr int kw = attn_waves<HD>();
   dim3 g((Skv + 32 * kw - 1) / (32 * kw), H, B);
+#ifndef SR_DKV128_PLAIN
+  if constexpr (HD == 128) {
+    hipLaunchKernelGGL(attn_bwd_dkv_h128, g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta, dk_out,
+                       ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
+    return hipGetLastError();
+  }
+#endif
   hipLaunchKernelGGL((attn_bwd_dkv_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta,
                      dk_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   return hipGetLastError();
