@@ -1086,6 +1086,270 @@ __global__ __launch_bounds__(64 * NW, HD == 64 ? 8 / NW : 1) void attn_bwd_dq_mf
   unstage<HD, NW>(smem, dq_out + (size_t)b * Sq * ldo + hh * HD, ldo, id.blk * (32 * NW), Sq);
 }
 
+// ------------------------------------------------------------ backward dQ at head dim 128: one wave per SIMD
+// The register-explicit form of the dK/dV kernel above, for dQ: four waves of 32 queries, one per
+// SIMD, streaming 64-key tiles (two 32-key units each):
+//   unit j:  X_j = [S^T_j = K_j Q^T, Delta - dP^T_j = Delta + V_j (-dO)^T]   (16 MFMAs, VGPR results)
+//            V_j = [P = exp2(S^T sl2 - lse), dS^T = -P (Delta - dP^T)]   (lse, Delta: the lane's query)
+//            Y_j = [dQ^T += K_j^T dS^T_j]   (8 MFMAs into AGPR accumulators)
+// Q and -dO of the wave's queries (B operands of X), the accumulators and the K / V row fragments
+// (A operands of X, a ring of twelve slots) in AGPRs; scores, dP, P, dS and the transposed K
+// fragments (a ring of eight pairs) in VGPRs.  24 one-MFMA regions per step, vector work split in
+// two parts one region apart, fragment reads in a rolling window of at most 15 in flight, each
+// issued after the MFMA that last read the registers it overwrites.  LDS: the K tiles of the four
+// stages in the first 64 KB, the V tiles in the next 64 KB, filled two tiles ahead.
+namespace dqh {
+constexpr int NST = 4;
+constexpr int NW = 4;
+constexpr int HD = 128;
+constexpr int KS = HD / 16;
+constexpr int DB = HD / 32;
+constexpr int TE = KT * HD;
+constexpr int TBB = TE * 2;
+constexpr int VOFF = NST * TBB;                // byte offset of the V tiles (64 KB)
+constexpr int LPT = 2 * (TE / 512 / NW);       // buffer loads per wave per tile (K, V)
+// region R of a step: X MFMA R (R < 12), Y MFMA R - 12 (12 <= R < 16, query half... key half 0),
+// X MFMA R - 4 (16 <= R < 20), Y MFMA R - 16 (20 <= R < 24, key half 1).  X MFMA m: k-step m / 2 of
+// S^T (even m) or of Delta - dP^T (odd m); Y MFMA n: key half n / 4, column block n % 4.
+constexpr int kind_of(int R) { return R < 12 ? 0 : R < 16 ? 1 : R < 20 ? 0 : 1; }
+constexpr int idx_of(int R) { return R < 12 ? R : R < 16 ? R - 12 : R < 20 ? R - 4 : R - 16; }
+constexpr int va_region(int r) { return r < 8 ? (r * 3) / 2 : 11 + (r - 8); }
+}  // namespace dqh
+
+__global__ __launch_bounds__(256, 1) void attn_bwd_dq_h128(const bf16_t* __restrict__ q, int ldq,
+                                                           const bf16_t* __restrict__ kv, int ldkv,
+                                                           uint32_t kv_elems, const bf16_t* __restrict__ dO,
+                                                           const float* __restrict__ lse,
+                                                           const float* __restrict__ delta,
+                                                           bf16_t* __restrict__ dq_out, int ldo, int Sq, int Skv,
+                                                           int H, int D, float sl2, float scale) {
+  using namespace dqh;
+  using dkvh::rd16a;
+  using dkvh::rdtrv;
+  using dkvh::mma_v0;
+  using dkvh::mma_v;
+  using dkvh::mma_a;
+  using dkvh::pin_a;
+  using dkvh::join;
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * NST * TE];   // K tiles, then V tiles
+  const int lane = threadIdx.x & 63, l32 = lane & 31, h32 = lane >> 5;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const TileId id = xcd_tile_id();
+  const int b = id.b, hh = id.h;
+  const bf16_t* qp = q + (size_t)b * Sq * ldq + hh * HD;
+  const bf16_t* dop = dO + (size_t)b * Sq * D + hh * HD;
+  const int myq = id.blk * (32 * NW) + wid * 32 + l32;
+  const int nt = (Skv + KT - 1) / KT;
+  const int nu = 2 * nt;
+  const bool ragged = Skv % KT != 0;
+
+  // Q and -dO fragments of the wave's queries (AGPR); dO negated so that the dP^T chain
+  // accumulates Delta - dP^T from a start tuple holding the query's Delta
+  i32x4 qf[KS], df[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    qf[ks] = __builtin_bit_cast(i32x4, myq < Sq ? ld8(qp + (size_t)myq * ldq + ks * 16 + 8 * h32) : zero8());
+    df[ks] = __builtin_bit_cast(i32x4, neg8(myq < Sq ? ld8(dop + (size_t)myq * D + ks * 16 + 8 * h32) : zero8()));
+  }
+  const float nlse = myq < Sq ? -lse[((size_t)b * H + hh) * Sq + myq] : -INFINITY;
+  const float dl_q = myq < Sq ? delta[((size_t)b * H + hh) * Sq + myq] : 0.f;
+  f32x16 dl16;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dl16[r] = dl_q;
+  f32x16 dq[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) zero16(dq[db]);
+  static_for<KS>([&](auto k) { pin_a(qf[k.value]); pin_a(df[k.value]); });
+  static_for<DB>([&](auto d) { pin_a(dq[d.value]); });
+  asm volatile("s_nop 7" ::: "memory");   // AGPR writes before the first MFMA reads
+
+  const __amdgpu_buffer_rsrc_t rkv = make_rsrc(kv, kv_elems * 2u);
+  const uint32_t kbase = (uint32_t)(((size_t)b * Skv * ldkv + hh * HD) * 2);
+  const uint32_t vbase = kbase + (uint32_t)D * 2u;
+  auto fill = [&](int t, int s) __attribute__((always_inline)) {
+    const bool valid = t < nt;
+    tile_load<HD, NW>(rkv, kbase, (uint32_t)ldkv, t * KT, smem + s * TE, valid);
+    tile_load<HD, NW>(rkv, vbase, (uint32_t)ldkv, t * KT, smem + NST * TE + s * TE, valid);
+  };
+
+  const uint32_t sbase = lds_addr(smem);
+  uint32_t ra[KS], rav[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    ra[ks] = sbase + (uint32_t)(l32 * HD + (((2 * ks + h32) ^ swz<HD>(l32)) << 3)) * 2u;
+    rav[ks] = ra[ks] + VOFF;
+  }
+  uint32_t ta[DB][2];
+  {
+    const int g = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int col = 32 * db + 16 * (g & 1) + 4 * (s & 3);
+      const int r1 = 4 * (g >> 1) + (s >> 2), r2 = r1 + 8;
+      ta[db][0] = sbase + (uint32_t)(r1 * HD + (((col >> 3) ^ swz<HD>(r1)) << 3) + (col & 7)) * 2u;
+      ta[db][1] = sbase + (uint32_t)(r2 * HD + (((col >> 3) ^ swz<HD>(r2)) << 3) + (col & 7)) * 2u;
+    }
+  }
+
+  i32x4 rf[12];                // K / V row fragments of X, slot m % 12 (AGPR)
+  i32x2 tf[2 * 2 * DB];        // K^T fragments of Y MFMA n: tf[2n], tf[2n+1] (VGPR)
+  f32x16 sc[2], dpv[2];        // S^T and Delta - dP^T of a unit, by parity (VGPR)
+  bf16x8 sb[2];                // dS^T in bf16, key halves (VGPR)
+  float pt[16], dt[16];
+
+  // row fragment of X MFMA M of unit u (K k-step M / 2 for even M, V for odd M) into slot M % 12
+  auto read_row = [&](auto ui, auto mi) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, M = decltype(mi)::value, K = M / 2;
+    constexpr int OFF = ((U / 2) % NST) * TBB + (U % 2) * 32 * HD * 2;
+    if constexpr (M % 2 == 0) rf[M % 12] = rd16a<OFF>(ra[K]);
+    else rf[M % 12] = rd16a<OFF>(rav[K]);
+  };
+  // K^T fragment pair of Y MFMA N (key half N / 4, column block N % 4) of unit u
+  auto read_tr = [&](auto ui, auto ni) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, N = decltype(ni)::value, KK = N / 4, C = N % 4;
+    constexpr int OFF = ((U / 2) % NST) * TBB + ((U % 2) * 32 + KK * 16) * HD * 2;
+    tf[2 * N] = rdtrv<OFF>(ta[C][0]);
+    tf[2 * N + 1] = rdtrv<OFF>(ta[C][1]);
+  };
+  auto xmma = [&](auto pi, auto mi) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value, M = decltype(mi)::value, K = M / 2;
+    if constexpr (M % 2 == 0) {
+      if constexpr (K == 0) mma_v0(sc[P], rf[0], qf[0]);
+      else mma_v(sc[P], rf[M % 12], qf[K]);
+    } else {
+      if constexpr (K == 0) asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=v"(dpv[P]) : "a"(rf[1]), "a"(df[0]), "v"(dl16));
+      else mma_v(dpv[P], rf[M % 12], df[K]);
+    }
+  };
+  auto ymma = [&](auto ni) __attribute__((always_inline)) {
+    constexpr int N = decltype(ni)::value, KK = N / 4, C = N % 4;
+    mma_a(dq[C], join(tf[2 * N], tf[2 * N + 1]), __builtin_bit_cast(i32x4, sb[KK]));
+  };
+  auto vpart_a = [&](auto pi, auto ri) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value, r = decltype(ri)::value;
+    pt[r] = ex2(fmaf(sc[P][r], sl2, nlse));
+    dt[r] = dpv[P][r];
+  };
+  auto vpart_b = [&](auto ri) __attribute__((always_inline)) {
+    constexpr int r = decltype(ri)::value;
+    sb[r >> 3][r & 7] = (__bf16)(-pt[r] * dt[r]);
+  };
+  const int rem = Skv - (nt - 1) * KT;   // valid keys of the last tile
+  // keys past Skv (units of the last, ragged tile): S^T = -inf, so P = 0 and dS = 0
+  auto mask_keys = [&](auto pi, int u) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (u * 32 + srow(r, h32) >= rem) sc[P][r] = -INFINITY;
+  };
+  // reads issued in region R of step j: rows of X MFMAs 12..15 of unit j+1 (regions 1..4, slots of
+  // MFMAs 0..3), of MFMAs 4..11 of unit j+2 (regions 5..12), of MFMAs 0..3 of unit j+2 (regions
+  // 17..20, after X MFMAs 12..15 of unit j+1); the K^T pair of Y MFMA n of unit j+1 after Y MFMA n
+  // of unit j (regions 13..16 for n = 0..3, 21..23 and after the last for n = 4..7)
+  auto reads_of = [&](auto ri, auto ui) __attribute__((always_inline)) {
+    constexpr int R = decltype(ri)::value, U = decltype(ui)::value;
+    constexpr int UR = (U + 2) % 8, UN = (U + 1) % 8;
+    constexpr int mrow = (R >= 1 && R <= 4) ? R + 11 : (R >= 5 && R <= 12) ? R - 1 : (R >= 17 && R <= 20) ? R - 17 : -1;
+    constexpr int urow = (R >= 1 && R <= 4) ? UN : UR;
+    constexpr int ntr = (R >= 13 && R <= 16) ? R - 13 : (R >= 21 && R <= 23) ? R - 17 : -1;
+    constexpr int n = (mrow >= 0 ? 1 : 0) + (ntr >= 0 ? 2 : 0);
+    if constexpr (n > 0) {
+      lgkm_wait<15 - n>();
+      if constexpr (mrow >= 0) read_row(IC<urow>{}, IC<mrow>{});
+      if constexpr (ntr >= 0) read_tr(IC<UN>{}, IC<ntr>{});
+    }
+  };
+
+  auto step = [&](auto ui, int j) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, P = U % 2, Q = 1 - P;
+    if constexpr (P == 0) {
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LPT) : "memory");
+      lds_barrier();
+      fill(j / 2 + 3, (U / 2 + 3) % NST);
+    }
+    lgkm_wait<13>();   // rows 0..11 of unit j+1 retired
+    asm volatile("s_nop 11" : "+v"(sc[P]), "+v"(dpv[P]));   // X_j's results readable by the vector unit
+    if (ragged && j >= nu - 2) mask_keys(IC<P>{}, P);
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<24>([&](auto ri) {
+      constexpr int R = ri.value, KD = kind_of(R), I = idx_of(R);
+      if constexpr (R == 12) asm volatile("s_nop 4" : "+v"(sb[0]));
+      if constexpr (R == 20) asm volatile("s_nop 4" : "+v"(sb[1]));
+      if constexpr (KD == 0) xmma(IC<Q>{}, IC<I>{});
+      else ymma(IC<I>{});
+      static_for<16>([&](auto r) {
+        if constexpr (va_region(r.value) == R) vpart_a(IC<P>{}, r);
+        if constexpr (va_region(r.value) + 1 == R) vpart_b(r);
+      });
+      reads_of(ri, ui);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    lgkm_wait<13>();
+    read_tr(IC<(U + 1) % 8>{}, IC<7>{});
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  fill(0, 0);
+  fill(1, 1);
+  fill(2, 2);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * LPT) : "memory");
+  lds_barrier();
+  static_for<12>([&](auto m) {
+    if constexpr (m.value == 8) lgkm_wait<7>();
+    read_row(IC<0>{}, m);
+  });
+  lgkm_wait<0>();
+  static_for<12>([&](auto m) { xmma(IC<0>{}, m); });
+  static_for<4>([&](auto m) { read_row(IC<0>{}, IC<12 + m.value>{}); });
+  lgkm_wait<0>();
+  static_for<4>([&](auto m) { xmma(IC<0>{}, IC<12 + m.value>{}); });
+  static_for<12>([&](auto m) {
+    if constexpr (m.value % 6 == 0) lgkm_wait<7>();
+    read_row(IC<1>{}, m);
+  });
+  static_for<8>([&](auto n) {
+    if constexpr (n.value % 4 == 0) lgkm_wait<7>();
+    read_tr(IC<0>{}, n);
+  });
+  __builtin_amdgcn_sched_barrier(0);
+
+  int j = 0;
+  for (; j + 8 <= nu; j += 8) {
+    step(IC<0>{}, j);
+    step(IC<1>{}, j + 1);
+    step(IC<2>{}, j + 2);
+    step(IC<3>{}, j + 3);
+    step(IC<4>{}, j + 4);
+    step(IC<5>{}, j + 5);
+    step(IC<6>{}, j + 6);
+    step(IC<7>{}, j + 7);
+  }
+  if (j < nu) {
+    step(IC<0>{}, j);
+    step(IC<1>{}, j + 1);
+    if (j + 2 < nu) {
+      step(IC<2>{}, j + 2);
+      step(IC<3>{}, j + 3);
+      if (j + 4 < nu) {
+        step(IC<4>{}, j + 4);
+        step(IC<5>{}, j + 5);
+      }
+    }
+  }
+
+  lgkm_wait<0>();
+  static_for<12>([&](auto e) { pin_a(rf[e.value]); });
+  static_for<4 * DB>([&](auto f) { pin(tf[f.value]); });
+  static_for<DB>([&](auto d) { pin_a(dq[d.value]); });
+  asm volatile("s_nop 15\n\ts_nop 15" ::: "memory");
+  static_for<DB>([&](auto d) { pin_a(dq[d.value]); });
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  stage_t<HD>(smem, dq, scale, wid, lane);
+  __syncthreads();
+  unstage<HD, NW>(smem, dq_out + (size_t)b * Sq * ldo + hh * HD, ldo, id.blk * (32 * NW), Sq);
+}
+
 // ------------------------------------------------------------------------------ generic kernels
 
 template <typename Ta, int HDT>
@@ -1393,6 +1657,13 @@ static hipError_t dq_mfma_hd(const bf16_t* q, int ldq, const bf16_t* kv, int ldk
                              int Sq, int Skv, int H, int D, hipStream_t st) {
   constexpr int kw = attn_waves<HD>();
   dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
+#ifndef SR_DQ128_PLAIN
+  if constexpr (HD == 128) {
+    hipLaunchKernelGGL(attn_bwd_dq_h128, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta, dq_out,
+                       ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
+    return hipGetLastError();
+  }
+#endif
   hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta,
                      dq_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   return hipGetLastError();
