@@ -1350,6 +1350,300 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_h128(const bf16_t* __restr
   unstage<HD, NW>(smem, dq_out + (size_t)b * Sq * ldo + hh * HD, ldo, id.blk * (32 * NW), Sq);
 }
 
+// ------------------------------------------------------------ forward at head dim 128: one wave per SIMD
+// The register-explicit form of the attention forward: four waves of 32 queries, one per SIMD,
+// streaming 64-key tiles, one tile per step:
+//   X_t = [S^T_t = K_t Q^T]   (16 MFMAs: two 32-key units x 8 k-steps, VGPR results)
+//   V_t = [row max, lazy rescale, P^T = exp2(S^T sl2 - m) in bf16]   (vector work)
+//   Y_t = [l += colsums(P^T) (4 MFMAs with a ones operand), O^T += V_t^T P^T (16 MFMAs)]
+// Step t issues X_{t+1} under V_t, then Y_t.  Q of the wave's queries (B operand of X), the O^T
+// and row-sum accumulators, the ones operand and the K row fragments (A operands of X, a ring of
+// twelve slots) in AGPRs; scores, P and the V^T fragments (a ring of eight pairs) in VGPRs.  36
+// one-MFMA regions per step, fragment reads in a rolling window of at most 15 in flight, each
+// issued after the MFMA that last read the registers it overwrites.  A step reads fragments of
+// tiles t+1 and t+2, so the tile barrier waits for every fill (tile t+2's, issued a step
+// earlier).  LDS: K tiles of the four stages in the first 64 KB, V tiles in the next 64 KB.
+namespace fwh {
+constexpr int NST = 4;
+constexpr int NW = 4;
+constexpr int HD = 128;
+constexpr int KS = HD / 16;
+constexpr int DB = HD / 32;
+constexpr int TE = KT * HD;
+constexpr int TBB = TE * 2;
+constexpr int VOFF = NST * TBB;
+// region R: X MFMA R (R < 16: unit R % 2, k-step R / 2); Y MFMA R - 16 of unit 0 (16 <= R < 26)
+// or R - 26 of unit 1: Y MFMA i < 2 is the row-sum MFMA of query half... key half i, i >= 2 the
+// O^T MFMA of column block (i - 2) / 2, key half (i - 2) % 2.
+// part a (exp) of score register r of unit u in region 5 + 8 u + r / 2, part b one region later
+}  // namespace fwh
+
+__global__ __launch_bounds__(256, 1) void attn_fwd_h128(const bf16_t* __restrict__ q, int ldq,
+                                                        const bf16_t* __restrict__ kv, int ldkv, uint32_t kv_elems,
+                                                        bf16_t* __restrict__ O, float* __restrict__ lse, int Sq,
+                                                        int Skv, int H, int D, float sl2) {
+  using namespace fwh;
+  using dkvh::rd16a;
+  using dkvh::rdtrv;
+  using dkvh::mma_v0;
+  using dkvh::mma_v;
+  using dkvh::mma_a;
+  using dkvh::pin_a;
+  using dkvh::join;
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * NST * TE];   // K tiles, then V tiles
+  const int lane = threadIdx.x & 63, l32 = lane & 31, h32 = lane >> 5;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const TileId id = xcd_tile_id();
+  const int b = id.b, hh = id.h;
+  const bf16_t* qp = q + (size_t)b * Sq * ldq + hh * HD;
+  const int myq = id.blk * (32 * NW) + wid * 32 + l32;
+  const int nt = (Skv + KT - 1) / KT;
+  const bool ragged = Skv % KT != 0;
+
+  i32x4 qf[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+    qf[ks] = __builtin_bit_cast(i32x4, myq < Sq ? ld8(qp + (size_t)myq * ldq + ks * 16 + 8 * h32) : zero8());
+  f32x16 o[DB], lsum;
+#pragma unroll
+  for (int db = 0; db < DB; ++db) zero16(o[db]);
+  zero16(lsum);
+  // softmax denominators on the matrix cores: an A operand whose row 0 is all ones turns the P^T
+  // MFMA into the column sums of P^T, so lsum[0] of lane l32 (first half) sums the bf16
+  // probabilities of query l32 (the values the PV product uses); every other element stays zero
+  bf16x8 ones8;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones8[i] = (__bf16)(l32 == 0 ? 1.0f : 0.0f);
+  i32x4 ones = __builtin_bit_cast(i32x4, ones8);
+  static_for<KS>([&](auto k) { pin_a(qf[k.value]); });
+  static_for<DB>([&](auto d) { pin_a(o[d.value]); });
+  pin_a(lsum);
+  pin_a(ones);
+  asm volatile("s_nop 7" ::: "memory");
+  float m_run = -INFINITY;   // running reference max of the raw scores
+
+  const __amdgpu_buffer_rsrc_t rkv = make_rsrc(kv, kv_elems * 2u);
+  const uint32_t kbase = (uint32_t)(((size_t)b * Skv * ldkv + hh * HD) * 2);
+  const uint32_t vbase = kbase + (uint32_t)D * 2u;
+  auto fill = [&](int t, int s) __attribute__((always_inline)) {
+    const bool valid = t < nt;
+    tile_load<HD, NW>(rkv, kbase, (uint32_t)ldkv, t * KT, smem + s * TE, valid);
+    tile_load<HD, NW>(rkv, vbase, (uint32_t)ldkv, t * KT, smem + NST * TE + s * TE, valid);
+  };
+  const uint32_t sbase = lds_addr(smem);
+  uint32_t ra[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) ra[ks] = sbase + (uint32_t)(l32 * HD + (((2 * ks + h32) ^ swz<HD>(l32)) << 3)) * 2u;
+  uint32_t tav[DB][2];
+  {
+    const int g = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int col = 32 * db + 16 * (g & 1) + 4 * (s & 3);
+      const int r1 = 4 * (g >> 1) + (s >> 2), r2 = r1 + 8;
+      tav[db][0] = sbase + VOFF + (uint32_t)(r1 * HD + (((col >> 3) ^ swz<HD>(r1)) << 3) + (col & 7)) * 2u;
+      tav[db][1] = sbase + VOFF + (uint32_t)(r2 * HD + (((col >> 3) ^ swz<HD>(r2)) << 3) + (col & 7)) * 2u;
+    }
+  }
+
+  i32x4 rf[12];             // K row fragments of X, slot m % 12 (AGPR)
+  i32x2 tf[16];             // V^T fragments of O^T MFMA n (n = 0..7 of a unit): tf[2n], tf[2n+1] (VGPR)
+  f32x16 sc[2][2];          // S^T of the two units of a tile, by parity (VGPR)
+  bf16x8 pb[2][2];          // P^T in bf16: unit, key half (VGPR)
+  float pt[2][16];
+
+  // K row fragment of X MFMA M of tile t (T = t % 4): unit M % 2, k-step M / 2, slot M % 12
+  auto read_row = [&](auto ti, auto mi) __attribute__((always_inline)) {
+    constexpr int T = decltype(ti)::value, M = decltype(mi)::value;
+    constexpr int OFF = (T % NST) * TBB + (M % 2) * 32 * HD * 2;
+    rf[M % 12] = rd16a<OFF>(ra[M / 2]);
+  };
+  // V^T pair of O^T MFMA N (column block N / 2, key half N % 2) of unit U of tile t
+  auto read_tr = [&](auto ti, auto ui, auto ni) __attribute__((always_inline)) {
+    constexpr int T = decltype(ti)::value, U = decltype(ui)::value, N = decltype(ni)::value;
+    constexpr int C = N / 2, KK = N % 2;
+    constexpr int OFF = (T % NST) * TBB + (U * 32 + KK * 16) * HD * 2;
+    tf[2 * N] = rdtrv<OFF>(tav[C][0]);
+    tf[2 * N + 1] = rdtrv<OFF>(tav[C][1]);
+  };
+  auto xmma = [&](auto pi, auto mi) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value, M = decltype(mi)::value, U = M % 2, K = M / 2;
+    if constexpr (K == 0) mma_v0(sc[P][U], rf[M % 12], qf[0]);
+    else mma_v(sc[P][U], rf[M % 12], qf[K]);
+  };
+  // Y MFMA I of unit U: I < 2 row sums of key half I, else O^T of column block (I-2)/2, key half (I-2)%2
+  auto ymma = [&](auto ui, auto ii) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, I = decltype(ii)::value;
+    if constexpr (I < 2) {
+      asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(lsum) : "a"(ones), "v"(__builtin_bit_cast(i32x4, pb[U][I])));
+    } else {
+      constexpr int N = I - 2, C = N / 2, KK = N % 2;
+      mma_a(o[C], join(tf[2 * N], tf[2 * N + 1]), __builtin_bit_cast(i32x4, pb[U][KK]));
+    }
+  };
+  const int rem = Skv - (nt - 1) * KT;
+  auto mask_keys = [&](auto pi) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        if (u * 32 + srow(r, h32) >= rem) sc[P][u][r] = -INFINITY;
+  };
+  float nm = 0.f;
+  // row max of the tile over registers R0 .. R0+7 of both units (regions 0..3), the reference update
+  // (region 4)
+  float mx = -INFINITY;
+  auto vmax = [&](auto pi, auto qi) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value, Qp = decltype(qi)::value;
+    static_for<8>([&](auto i) {
+      constexpr int r = (Qp % 2) * 8 + i.value, u = Qp / 2;
+      mx = fmaxf(mx, sc[P][u][r]);
+    });
+  };
+  auto vref = [&]() __attribute__((always_inline)) {
+    mx = half_pair_max(mx);
+    // lazy rescaling: the reference max m_run moves (and O, l are rescaled) only when a row's
+    // max has grown by more than 8 in exp2 units; otherwise p = 2^((s - m_run) c) <= 256
+    const float grow = (fmaxf(m_run, mx) - m_run) * sl2;   // +inf on the first tile
+    if (__ballot(grow > 8.0f)) {
+      const float m_ref = grow > 8.0f ? mx : m_run;
+      const float alpha = ex2((m_run - m_ref) * sl2);
+      asm volatile("s_nop 15\n\ts_nop 3" ::: "memory");   // the accumulators' last MFMA writes landed
+      static_for<DB>([&](auto d) { pin_a(o[d.value]); });
+      pin_a(lsum);
+      lsum[0] *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      static_for<DB>([&](auto d) { pin_a(o[d.value]); });
+      pin_a(lsum);
+      asm volatile("s_nop 4" ::: "memory");   // accumulator writes before the next MFMAs read them
+      m_run = m_ref;
+    }
+    nm = -m_run * sl2;
+    mx = -INFINITY;
+  };
+  auto vpart_a = [&](auto pi, auto ui, auto ri) __attribute__((always_inline)) {
+    constexpr int P = decltype(pi)::value, U = decltype(ui)::value, r = decltype(ri)::value;
+    pt[U][r] = ex2(fmaf(sc[P][U][r], sl2, nm));
+  };
+  auto vpart_b = [&](auto ui, auto ri) __attribute__((always_inline)) {
+    constexpr int U = decltype(ui)::value, r = decltype(ri)::value;
+    pb[U][r >> 3][r & 7] = (__bf16)pt[U][r];
+  };
+  // reads issued in region R of step t: K rows of X MFMAs 12..15 of tile t+1 (regions 1..4, slots
+  // of MFMAs 0..3), of MFMAs 4..11 of tile t+2 (regions 5..12), of MFMAs 0..3 of tile t+2 (regions
+  // 13..16, after X MFMAs 12..15); V^T pairs of unit 1 of tile t after unit 0's O^T MFMA n (regions
+  // 19..26) and of unit 0 of tile t+1 after unit 1's (regions 29..35 and after the last)
+  auto reads_of = [&](auto ri, auto ti) __attribute__((always_inline)) {
+    constexpr int R = decltype(ri)::value, T = decltype(ti)::value;
+    constexpr int mrow = (R >= 1 && R <= 4) ? R + 11 : (R >= 5 && R <= 12) ? R - 1 : (R >= 13 && R <= 16) ? R - 13 : -1;
+    constexpr int trow = (R >= 1 && R <= 4) ? (T + 1) % 4 : (T + 2) % 4;
+    constexpr int ntr1 = (R >= 19 && R <= 26) ? R - 19 : -1;   // unit 1 of tile t
+    constexpr int ntr0 = (R >= 29 && R <= 35) ? R - 29 : -1;   // unit 0 of tile t+1
+    constexpr int n = (mrow >= 0 ? 1 : 0) + (ntr1 >= 0 || ntr0 >= 0 ? 2 : 0);
+    if constexpr (n > 0) {
+      lgkm_wait<15 - n>();
+      if constexpr (mrow >= 0) read_row(IC<trow>{}, IC<mrow>{});
+      if constexpr (ntr1 >= 0) read_tr(IC<T>{}, IC<1>{}, IC<ntr1>{});
+      if constexpr (ntr0 >= 0) read_tr(IC<(T + 1) % 4>{}, IC<0>{}, IC<ntr0>{});
+    }
+  };
+
+  auto step = [&](auto ti, int t) __attribute__((always_inline)) {
+    constexpr int T = decltype(ti)::value, P = T % 2, Q = 1 - P;
+    // tile barrier: tiles t+1, t+2 resident (tile t+2's fill was the last issued), then refill
+    // the stage of tile t-1, whose reads all retired during the previous step
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
+    fill(t + 3, (T + 3) % NST);
+    lgkm_wait<13>();
+    asm volatile("s_nop 11" : "+v"(sc[P][0]), "+v"(sc[P][1]));   // X_t's results readable by the vector unit
+    if (ragged && t == nt - 1) mask_keys(IC<P>{});
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<36>([&](auto ri) {
+      constexpr int R = ri.value;
+      if constexpr (R == 16) asm volatile("s_nop 4" : "+v"(pb[0][0]), "+v"(pb[0][1]));
+      if constexpr (R == 26) asm volatile("s_nop 4" : "+v"(pb[1][0]), "+v"(pb[1][1]));
+      if constexpr (R < 16) xmma(IC<Q>{}, IC<R>{});
+      else if constexpr (R < 26) ymma(IC<0>{}, IC<R - 16>{});
+      else ymma(IC<1>{}, IC<R - 26>{});
+      if constexpr (R < 4) vmax(IC<P>{}, IC<R>{});
+      if constexpr (R == 4) vref();
+      static_for<16>([&](auto r) {
+        constexpr int ra0 = 5 + r.value / 2, ra1 = 13 + r.value / 2;
+        if constexpr (ra0 == R) vpart_a(IC<P>{}, IC<0>{}, r);
+        if constexpr (ra0 + 1 == R) vpart_b(IC<0>{}, r);
+        if constexpr (ra1 == R) vpart_a(IC<P>{}, IC<1>{}, r);
+        if constexpr (ra1 + 1 == R) vpart_b(IC<1>{}, r);
+      });
+      reads_of(ri, ti);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    lgkm_wait<13>();
+    read_tr(IC<(T + 1) % 4>{}, IC<0>{}, IC<7>{});
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // prologue: tiles 0..2 resident; X_0; the reads of step 0 (rows 0..11 of tile 1, V^T of tile 0 unit 0)
+  fill(0, 0);
+  fill(1, 1);
+  fill(2, 2);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  lds_barrier();
+  static_for<12>([&](auto m) {
+    if constexpr (m.value == 8) lgkm_wait<7>();
+    read_row(IC<0>{}, m);
+  });
+  lgkm_wait<0>();
+  static_for<12>([&](auto m) { xmma(IC<0>{}, m); });
+  static_for<4>([&](auto m) { read_row(IC<0>{}, IC<12 + m.value>{}); });
+  lgkm_wait<0>();
+  static_for<4>([&](auto m) { xmma(IC<0>{}, IC<12 + m.value>{}); });
+  static_for<12>([&](auto m) {
+    if constexpr (m.value % 6 == 0) lgkm_wait<7>();
+    read_row(IC<1>{}, m);
+  });
+  static_for<8>([&](auto n) {
+    if constexpr (n.value % 4 == 0) lgkm_wait<7>();
+    read_tr(IC<0>{}, IC<0>{}, n);
+  });
+  __builtin_amdgcn_sched_barrier(0);
+
+  int t = 0;
+  for (; t + 4 <= nt; t += 4) {
+    step(IC<0>{}, t);
+    step(IC<1>{}, t + 1);
+    step(IC<2>{}, t + 2);
+    step(IC<3>{}, t + 3);
+  }
+  if (t < nt) {
+    step(IC<0>{}, t);
+    if (t + 1 < nt) {
+      step(IC<1>{}, t + 1);
+      if (t + 2 < nt) step(IC<2>{}, t + 2);
+    }
+  }
+
+  lgkm_wait<0>();
+  static_for<12>([&](auto e) { pin_a(rf[e.value]); });
+  static_for<16>([&](auto f) { pin(tf[f.value]); });
+  static_for<DB>([&](auto d) { pin_a(o[d.value]); });
+  pin_a(lsum);
+  asm volatile("s_nop 15\n\ts_nop 15" ::: "memory");
+  static_for<DB>([&](auto d) { pin_a(o[d.value]); });
+  pin_a(lsum);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();   // every wave is done with the stages before they hold the output
+  const float l_tot = half_pair_sum(lsum[0]);   // the second half's element is zero
+  if (h32 == 0 && myq < Sq) lse[((size_t)b * H + hh) * Sq + myq] = m_run * sl2 + log2f(l_tot);
+  stage_t<HD>(smem, o, 1.0f / l_tot, wid, lane);
+  __syncthreads();
+  unstage<HD, NW>(smem, O + (size_t)b * Sq * D + hh * HD, D, id.blk * (32 * NW), Sq);
+}
+
 // ------------------------------------------------------------------------------ generic kernels
 
 template <typename Ta, int HDT>
@@ -1614,6 +1908,13 @@ static hipError_t fwd_mfma_hd(const bf16_t* q, int ldq, const bf16_t* kv, int ld
                               float* lse, int B, int Sq, int Skv, int H, int D, hipStream_t st) {
   constexpr int kw = attn_waves<HD>();
   dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
+#ifndef SR_FWD128_PLAIN
+  if constexpr (HD == 128) {
+    hipLaunchKernelGGL(attn_fwd_h128, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv, H, D,
+                       attn_sl2(HD));
+    return hipGetLastError();
+  }
+#endif
   hipLaunchKernelGGL((attn_fwd_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv,
                      H, D, attn_sl2(HD));
   return hipGetLastError();
