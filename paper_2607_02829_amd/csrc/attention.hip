@@ -43,7 +43,9 @@ constexpr int NSTG = 3;      // LDS stages
 // tile in LDS, at one workgroup per CU and two waves per SIMD; against four, measured 2-4 %
 // faster per kernel at 4050 tokens (forward 94 -> 90, dK/dV 159 -> 155, dQ 112 -> 108 us).  At
 // head dim 128 the accumulators of a 32-row unit take twice the registers, so four waves (128
-// rows) per workgroup, one per SIMD with the whole register file.
+// rows) per workgroup, one per SIMD with the whole register file: the register-explicit kernels
+// attn_fwd_h128, attn_bwd_dkv_h128 and attn_bwd_dq_h128 (the templates below are instantiated at
+// head dim 64).
 template <int HD>
 constexpr int attn_waves() { return HD == 64 ? 8 : 4; }
 
@@ -1908,15 +1910,12 @@ static hipError_t fwd_mfma_hd(const bf16_t* q, int ldq, const bf16_t* kv, int ld
                               float* lse, int B, int Sq, int Skv, int H, int D, hipStream_t st) {
   constexpr int kw = attn_waves<HD>();
   dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
-#ifndef SR_FWD128_PLAIN
-  if constexpr (HD == 128) {
+  if constexpr (HD == 128)
     hipLaunchKernelGGL(attn_fwd_h128, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv, H, D,
                        attn_sl2(HD));
-    return hipGetLastError();
-  }
-#endif
-  hipLaunchKernelGGL((attn_fwd_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv,
-                     H, D, attn_sl2(HD));
+  else
+    hipLaunchKernelGGL((attn_fwd_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv,
+                       H, D, attn_sl2(HD));
   return hipGetLastError();
 }
 
@@ -1932,15 +1931,12 @@ static hipError_t dkv_mfma_hd(const bf16_t* q, int ldq, uint32_t q_elems, const 
                               int Sq, int Skv, int H, int D, hipStream_t st) {
   constexpr int kw = attn_waves<HD>();
   dim3 g((Skv + 32 * kw - 1) / (32 * kw), H, B);
-#ifndef SR_DKV128_PLAIN
-  if constexpr (HD == 128) {
+  if constexpr (HD == 128)
     hipLaunchKernelGGL(attn_bwd_dkv_h128, g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta, dk_out,
                        ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
-    return hipGetLastError();
-  }
-#endif
-  hipLaunchKernelGGL((attn_bwd_dkv_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta,
-                     dk_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
+  else
+    hipLaunchKernelGGL((attn_bwd_dkv_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse,
+                       delta, dk_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   return hipGetLastError();
 }
 
@@ -1958,15 +1954,12 @@ static hipError_t dq_mfma_hd(const bf16_t* q, int ldq, const bf16_t* kv, int ldk
                              int Sq, int Skv, int H, int D, hipStream_t st) {
   constexpr int kw = attn_waves<HD>();
   dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
-#ifndef SR_DQ128_PLAIN
-  if constexpr (HD == 128) {
+  if constexpr (HD == 128)
     hipLaunchKernelGGL(attn_bwd_dq_h128, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta, dq_out,
                        ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
-    return hipGetLastError();
-  }
-#endif
-  hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta,
-                     dq_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
+  else
+    hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse,
+                       delta, dq_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   return hipGetLastError();
 }
 
