@@ -1269,7 +1269,9 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_h128(const bf16_t* __restr
       lds_barrier();
       fill(j / 2 + 3, (U / 2 + 3) % NST);
     }
-    lgkm_wait<13>();   // rows 0..11 of unit j+1 retired
+    // rows of X MFMAs 0..3 of unit j+1 retired: they were read in regions 17..20 of the previous
+    // step, and eight reads followed them
+    lgkm_wait<8>();
     asm volatile("s_nop 11" : "+v"(sc[P]), "+v"(dpv[P]));   // X_j's results readable by the vector unit
     if (ragged && j >= nu - 2) mask_keys(IC<P>{}, P);
     __builtin_amdgcn_sched_barrier(0);
@@ -1569,6 +1571,11 @@ __global__ __launch_bounds__(256, 1) void attn_fwd_h128(const bf16_t* __restrict
       constexpr int R = ri.value;
       if constexpr (R == 16) asm volatile("s_nop 4" : "+v"(pb[0][0]), "+v"(pb[0][1]));
       if constexpr (R == 26) asm volatile("s_nop 4" : "+v"(pb[1][0]), "+v"(pb[1][1]));
+      // consumers whose reads are fewer than fifteen reads back: X MFMAs 12..15 (slots refilled in
+      // regions 1..4, ten reads before) and the O^T MFMAs of unit 1 (pairs read in regions 19..26,
+      // twelve or more reads before)
+      if constexpr (R >= 12 && R <= 15) lgkm_wait<10>();
+      if constexpr (R >= 28) lgkm_wait<12>();
       if constexpr (R < 16) xmma(IC<Q>{}, IC<R>{});
       else if constexpr (R < 26) ymma(IC<0>{}, IC<R - 16>{});
       else ymma(IC<1>{}, IC<R - 26>{});

@@ -35,6 +35,53 @@ _Zw:
     assert kernel_hazards(asm) == {"_Zk": 1, "_Zok": 0, "_Zw": 1}
 
 
+def test_scan_keeps_reads_a_wait_does_not_cover():
+    # lgkmcnt(14) with only two reads in flight retires neither: the MFMA reads a register of the
+    # first (a list slice that went negative once dropped it)
+    asm = """_Zfew:
+\tds_read_b128 a[0:3], v1 offset:0
+\tds_read_b128 a[4:7], v1 offset:64
+\ts_waitcnt lgkmcnt(14)
+\tv_mfma_f32_32x32x16_bf16 v[0:15], a[0:3], a[8:11], 0
+.Lfunc_end0:
+_Zsix:
+\tds_read_b128 a[0:3], v1 offset:0
+\tds_read_b128 a[4:7], v1 offset:64
+\tds_read_b128 a[8:11], v1 offset:128
+\ts_waitcnt lgkmcnt(2)
+\tv_mfma_f32_32x32x16_bf16 v[0:15], a[0:3], a[12:15], 0
+\tv_mfma_f32_32x32x16_bf16 v[16:31], a[4:7], a[12:15], 0
+.Lfunc_end1:
+"""
+    # the second kernel: lgkmcnt(2) retires the first read only, the second MFMA touches the second
+    assert kernel_hazards(asm) == {"_Zfew": 1, "_Zsix": 1}
+
+
+def test_scan_follows_branches_over_waits():
+    # the wait sits on the fall-through path only; the branch to .LBB0_2 skips it, so the use
+    # after the join still sees the read in flight.  On the second kernel both paths wait.
+    asm = """_Zbr:
+\tds_read_b128 v[0:3], v9 offset:0
+\ts_cbranch_vccz .LBB0_2
+\ts_waitcnt lgkmcnt(0)
+\tv_mov_b32 v20, 0
+.LBB0_2:
+\tv_add_u32 v10, v0, v1
+\ts_endpgm
+.Lfunc_end0:
+_Zboth:
+\tds_read_b128 v[0:3], v9 offset:0
+\ts_waitcnt lgkmcnt(0)
+\ts_cbranch_vccz .LBB1_2
+\tv_mov_b32 v20, 0
+.LBB1_2:
+\tv_add_u32 v10, v0, v1
+\ts_endpgm
+.Lfunc_end1:
+"""
+    assert kernel_hazards(asm) == {"_Zbr": 1, "_Zboth": 0}
+
+
 @pytest.mark.parametrize("src", sorted(build.ASYNC_READS))
 def test_built_kernels_keep_in_flight_registers_untouched(src):
     path = build.device_asm_path(src)
