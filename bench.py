@@ -128,12 +128,13 @@ class TrunkStep:
     """The whole trunk with a (2, n - 4, 2) dense-sparse-dense split (the deterministic
     forecaster's (2, 8, 2) at 12 blocks): forward + backward of all n blocks per step."""
 
-    def __init__(self, w, seed: int = 42, split=None, K: int | None = None, select: str = "random"):
+    def __init__(self, w, seed: int = 42, split=None, K: int | None = None, select: str = "random",
+                 checkpoint: bool = False):
         from paper_2607_02829_amd import device, inputs
         from paper_2607_02829_amd.trunk import Trunk
         self.split = (2, w.n_blocks - 4, 2) if split is None else tuple(split)
         params = inputs.params_to_storage(inputs.block_params(w, sum(self.split)), w.dtype)
-        self.trunk = Trunk(w, self.split, params, K=K, seed=seed, select=select)
+        self.trunk = Trunk(w, self.split, params, K=K, seed=seed, select=select, checkpoint=checkpoint)
         self.x0 = device.to_device(inputs.to_storage(inputs.token_field(w, 0), w.dtype))
         self.g3 = device.to_device(inputs.to_storage(inputs.upstream_grad(w), w.dtype))
 
@@ -776,9 +777,12 @@ def main():
     # ---------------------------------------------------------------- whole trunk (2, n-4, 2)
     trunk = None
     if args.trunk_steps > 0 and w.kind == "preln" and w.n_blocks >= 5 and w.backward:
+        torch.cuda.reset_peak_memory_stats()
+        base_mem = torch.cuda.memory_allocated()
         tr = TrunkStep(w)
         tr.run(0)
         torch.cuda.synchronize()
+        trunk_peak = torch.cuda.max_memory_allocated() - base_mem
         tms, _, _ = time_steps(tr, args.trunk_steps, 1, start=1)
         n1, n2, n3 = tr.split
         finite_trunk = bool(torch.isfinite(tr.trunk.x3.float()).all().item()
@@ -793,7 +797,20 @@ def main():
         ams, _, _ = time_steps(tra, args.trunk_steps, 1, start=1)
         del tra
         torch.cuda.empty_cache()
-        trunk = {"split": list((2, w.n_blocks - 4, 2)), "ms_per_step": round(tms, 3),
+        # activation checkpointing: one stage's saved activations at a time, each stage's
+        # forward run again before its backward
+        torch.cuda.reset_peak_memory_stats()
+        base_mem = torch.cuda.memory_allocated()
+        trc = TrunkStep(w, checkpoint=True)
+        trc.run(0)
+        torch.cuda.synchronize()
+        ckpt_peak = torch.cuda.max_memory_allocated() - base_mem
+        cms, _, _ = time_steps(trc, args.trunk_steps, 1, start=1)
+        del trc
+        torch.cuda.empty_cache()
+        trunk = {"split": list((2, w.n_blocks - 4, 2)), "ms_per_step": round(tms, 3), "peak_bytes": int(trunk_peak),
+                 "checkpoint": {"ms_per_step": round(cms, 3), "peak_bytes": int(ckpt_peak),
+                                "peak_ratio": round(trunk_peak / ckpt_peak, 3)},
                  "attn_selector_ms_per_step": round(ams, 3), "attn_selector_overhead_ms": round(ams - tms, 3),
                  "speedup_vs_dense": round(dense["ms_per_step"] / tms, 3) if dense else None,
                  "eq_speedup_estimate": round(w.n_blocks / (n1 + n2 * w.keep ** 2 + n3), 3),

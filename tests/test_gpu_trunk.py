@@ -83,3 +83,40 @@ def test_trunk_bitwise_repeatable():
     for x, y in zip(ag, bg):
         for k in x:
             assert torch.equal(x[k].view(torch.int32), y[k].view(torch.int32)), k
+
+
+@pytest.mark.parametrize("case,select", [("small_bf16_121", "random"), ("small_f32_212", "random"),
+                                         ("b5625_282", "random"), ("b5625_282", "attn")])
+def test_trunk_checkpoint_is_bitwise_the_plain_trunk(case, select):
+    # activation checkpointing re-runs each stage's forward before its backward from the kept
+    # stage input into one shared saved-activation buffer: the deterministic kernels must give
+    # the same bits for the output, the input gradient and every parameter gradient, and the
+    # forward's output must survive the recompute
+    import torch
+    w, split, K = CASES[case]
+    print(f"[trunk ckpt {case} {select}] B={w.B} L={w.L} K={K} split={split} {w.dtype}", flush=True)
+    params = inputs.params_to_storage(inputs.block_params(w, sum(split), randomise_affine=True), w.dtype)
+    x0 = device.to_device(inputs.to_storage(inputs.token_field(w), w.dtype))
+    g3 = device.to_device(inputs.to_storage(inputs.upstream_grad(w), w.dtype))
+    x0_host = device.to_host(x0)
+    out = []
+    for ck in (False, True):
+        tr = Trunk(w, split, params, K=K, seed=5, select=select, checkpoint=ck)
+        x3 = tr.forward(x0, 2).clone()
+        g0 = tr.backward(g3).clone()
+        torch.cuda.synchronize()
+        assert torch.equal(tr.x3, x3), "the forward's output changed during the backward"
+        out.append((tr.idx.clone(), x3, g0, [{k: v.clone() for k, v in g.items()} for g in tr.block_grads()],
+                    tr.saved[0].numel() if ck else sum(s.numel() for s in tr.saved)))
+        del tr
+    (ia, a3, a0, ag, sa), (ib, b3, b0, bg, sb) = out
+    assert np.array_equal(device.to_host(x0), x0_host)
+    assert torch.equal(ia, ib)
+    bits = torch.int16 if w.dtype == "bf16" else torch.int32
+    assert torch.equal(a3.view(bits), b3.view(bits))
+    assert torch.equal(a0.view(bits), b0.view(bits))
+    for x, y in zip(ag, bg):
+        for k in x:
+            assert torch.equal(x[k].view(torch.int32), y[k].view(torch.int32)), k
+    assert sb < sa, (sb, sa)   # one stage's saved activations instead of all three
+    print(f"[trunk ckpt {case} {select}] saved bytes {sa} -> {sb}", flush=True)

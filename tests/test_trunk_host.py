@@ -21,3 +21,5 @@ def test_trunk_rejects_bad_arguments():
         Trunk(w.with_(kind="adaln"), (1, 1, 1), params)    # pre-LN blocks only
     with pytest.raises(ValueError):
         Trunk(w, (1, 1, 1), params, select="gradient")     # random or attention-score selection
+    with pytest.raises(ValueError):
+        Trunk(w, (1, 1, 1), params, checkpoint="yes")      # checkpointing is on or off
