@@ -82,6 +82,35 @@ _Zboth:
     assert kernel_hazards(asm) == {"_Zbr": 1, "_Zboth": 0}
 
 
+def test_scan_carries_reads_around_loops():
+    # a read issued at the bottom of a loop body is still in flight at the top of the next
+    # iteration: the use there is flagged unless a wait sits on the back edge
+    asm = """_Zloop:
+\ts_mov_b32 s0, 4
+.LBB0_1:
+\tv_add_u32 v10, v0, v1
+\tds_read_b128 v[0:3], v9 offset:0
+\ts_add_i32 s0, s0, -1
+\ts_cmp_lg_u32 s0, 0
+\ts_cbranch_scc1 .LBB0_1
+\ts_waitcnt lgkmcnt(0)
+\ts_endpgm
+.Lfunc_end0:
+_Zloopok:
+\ts_mov_b32 s0, 4
+.LBB1_1:
+\tv_add_u32 v10, v0, v1
+\tds_read_b128 v[0:3], v9 offset:0
+\ts_add_i32 s0, s0, -1
+\ts_cmp_lg_u32 s0, 0
+\ts_waitcnt lgkmcnt(0)
+\ts_cbranch_scc1 .LBB1_1
+\ts_endpgm
+.Lfunc_end1:
+"""
+    assert kernel_hazards(asm) == {"_Zloop": 1, "_Zloopok": 0}
+
+
 @pytest.mark.parametrize("src", sorted(build.ASYNC_READS))
 def test_built_kernels_keep_in_flight_registers_untouched(src):
     path = build.device_asm_path(src)
