@@ -455,7 +455,7 @@ def summarize_pmc(group: str, workload: str, fetch_csv: str, write_csv: str, com
         f"{n_k} dispatches of the kernel; scaled by the same counters read on a device-to-device",
         f"copy of {COPY_PROBE_BYTES} bytes (`{copy_name.split('(')[0]}`).",
         "",
-        "Commands (repository root on the GPU box, `cd /tmp && export TMPDIR=/tmp` first):",
+        "Commands (repository root on the MI355X machine, `cd /tmp && export TMPDIR=/tmp` first):",
         "",
         "```",
         command,
@@ -520,7 +520,7 @@ def summarize_routing_pmc(fetch_csv: str, write_csv: str, command: str, D: int =
         "(two for the gather, one for the others; the grid's last workgroup may be partly idle);",
         "algorithmic bytes as in `bench.py` (one read of each input, one write of each output).",
         "",
-        "Commands (repository root on the GPU box, `cd /tmp && export TMPDIR=/tmp` first):",
+        "Commands (repository root on the MI355X machine, `cd /tmp && export TMPDIR=/tmp` first):",
         "",
         "```",
         command,
@@ -701,8 +701,8 @@ def main():
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the routed stack is built and timed on a single MI355X; "
-              "multi-GPU runs are not part of this build.", file=sys.stderr)
+        print("bench.py measures one GPU: the routed stack runs and is timed on a single MI355X; "
+              "sharding it over several GPUs is not implemented.", file=sys.stderr)
         sys.exit(2)
 
     import torch

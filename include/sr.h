@@ -72,7 +72,7 @@ typedef enum {
   SR_EDTYPE = 3,        /* unknown storage dtype                              */
   SR_EALIGN = 4,        /* a tensor pointer is not 16-byte aligned            */
   SR_EWORKSPACE = 5,    /* saved / scratch buffer smaller than required       */
-  SR_EUNSUPPORTED = 6,  /* valid but not supported by this build              */
+  SR_EUNSUPPORTED = 6,  /* valid but not supported by this library            */
   SR_EHIP = 7           /* a HIP launch failed; sr_last_error() has the text  */
 } sr_status;
 

@@ -52,7 +52,7 @@ def _compile(src: str) -> str:
 
 
 def device_asm_path(src: str) -> str:
-    """Where the build keeps the gfx950 assembly of an ASYNC_READS source."""
+    """Where build() keeps the gfx950 assembly of an ASYNC_READS source."""
     return os.path.join(BUILD, os.path.splitext(src)[0] + "-hip-amdgcn-amd-amdhsa-gfx950.s")
 
 

@@ -5,7 +5,7 @@ the method itself.  Both the HIP path and the CPU oracle receive exactly the
 arrays produced here.
 
 Workloads (token grids follow Sec. 4.1 "Dataset" and the architecture tables in
-App. A.1; the middle-stack sizes are the ones this build is measured on):
+App. A.1; the middle-stack sizes are the ones the benchmark measures):
 
 =====  ======  =========================  =====  ====  ==  ===  ====  ==  ======  ==========
 name   B       grid (tokens)              L      K     D   H    F     n2  dtype   selection

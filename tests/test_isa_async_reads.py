@@ -1,5 +1,5 @@
 """The explicit (inline-assembly) LDS fragment reads of the MFMA kernels are only sound if the
-compiler never touches their destination registers before the wait that retires them.  The build
+compiler never touches their destination registers before the wait that retires them.  build.py
 keeps the gfx950 assembly of the sources that use them and refuses a library that breaks this;
 here the scan itself is pinned on hand-written sequences, and the kept assembly is rescanned."""
 import os
