@@ -1885,9 +1885,9 @@ template <typename Ta>
 static hipError_t fwd_simple(const Ta* qkv, Ta* O, float* lse, int B, int S, int H, int D, int hd, hipStream_t st) {
   dim3 g((S + 63) / 64, H, B);
   const float sl2 = attn_sl2(hd);
-  if (hd == 32) hipLaunchKernelGGL((attn_fwd_simple<Ta, 32>), g, dim3(64), 0, st, qkv, O, lse, S, H, D, sl2);
-  else if (hd == 64) hipLaunchKernelGGL((attn_fwd_simple<Ta, 64>), g, dim3(64), 0, st, qkv, O, lse, S, H, D, sl2);
-  else hipLaunchKernelGGL((attn_fwd_simple<Ta, 128>), g, dim3(64), 0, st, qkv, O, lse, S, H, D, sl2);
+  if (hd == 32) SR_LAUNCH((attn_fwd_simple<Ta, 32>), g, dim3(64), 0, st, qkv, O, lse, S, H, D, sl2);
+  else if (hd == 64) SR_LAUNCH((attn_fwd_simple<Ta, 64>), g, dim3(64), 0, st, qkv, O, lse, S, H, D, sl2);
+  else SR_LAUNCH((attn_fwd_simple<Ta, 128>), g, dim3(64), 0, st, qkv, O, lse, S, H, D, sl2);
   return hipGetLastError();
 }
 
@@ -1897,8 +1897,8 @@ static hipError_t bwd_simple(const Ta* qkv, const Ta* dO, const float* lse, cons
   dim3 g((S + 63) / 64, H, B);
   const float sl2 = attn_sl2(hd), sc = 1.0f / sqrtf((float)hd);
 #define SR_ABS(HDV)                                                                                              \
-  hipLaunchKernelGGL((attn_bwd_dq_simple<Ta, HDV>), g, dim3(64), 0, st, qkv, dO, lse, delta, dqkv, S, H, D, sl2, sc); \
-  hipLaunchKernelGGL((attn_bwd_dkv_simple<Ta, HDV>), g, dim3(64), 0, st, qkv, dO, lse, delta, dqkv, S, H, D, sl2, sc)
+  SR_LAUNCH((attn_bwd_dq_simple<Ta, HDV>), g, dim3(64), 0, st, qkv, dO, lse, delta, dqkv, S, H, D, sl2, sc); \
+  SR_LAUNCH((attn_bwd_dkv_simple<Ta, HDV>), g, dim3(64), 0, st, qkv, dO, lse, delta, dqkv, S, H, D, sl2, sc)
   if (hd == 32) { SR_ABS(32); } else if (hd == 64) { SR_ABS(64); } else { SR_ABS(128); }
 #undef SR_ABS
   return hipGetLastError();
@@ -1918,10 +1918,10 @@ static hipError_t fwd_mfma_hd(const bf16_t* q, int ldq, const bf16_t* kv, int ld
   constexpr int kw = attn_waves<HD>();
   dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
   if constexpr (HD == 128)
-    hipLaunchKernelGGL(attn_fwd_h128, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv, H, D,
+    SR_LAUNCH(attn_fwd_h128, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv, H, D,
                        attn_sl2(HD));
   else
-    hipLaunchKernelGGL((attn_fwd_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv,
+    SR_LAUNCH((attn_fwd_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, O, lse, Sq, Skv,
                        H, D, attn_sl2(HD));
   return hipGetLastError();
 }
@@ -1939,10 +1939,10 @@ static hipError_t dkv_mfma_hd(const bf16_t* q, int ldq, uint32_t q_elems, const 
   constexpr int kw = attn_waves<HD>();
   dim3 g((Skv + 32 * kw - 1) / (32 * kw), H, B);
   if constexpr (HD == 128)
-    hipLaunchKernelGGL(attn_bwd_dkv_h128, g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta, dk_out,
+    SR_LAUNCH(attn_bwd_dkv_h128, g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse, delta, dk_out,
                        ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   else
-    hipLaunchKernelGGL((attn_bwd_dkv_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse,
+    SR_LAUNCH((attn_bwd_dkv_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, q_elems, kv, ldkv, dO, lse,
                        delta, dk_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   return hipGetLastError();
 }
@@ -1962,10 +1962,10 @@ static hipError_t dq_mfma_hd(const bf16_t* q, int ldq, const bf16_t* kv, int ldk
   constexpr int kw = attn_waves<HD>();
   dim3 g((Sq + 32 * kw - 1) / (32 * kw), H, B);
   if constexpr (HD == 128)
-    hipLaunchKernelGGL(attn_bwd_dq_h128, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta, dq_out,
+    SR_LAUNCH(attn_bwd_dq_h128, g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse, delta, dq_out,
                        ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   else
-    hipLaunchKernelGGL((attn_bwd_dq_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse,
+    SR_LAUNCH((attn_bwd_dq_mfma<HD, kw>), g, dim3(64 * kw), 0, st, q, ldq, kv, ldkv, kv_elems, dO, lse,
                        delta, dq_out, ldo, Sq, Skv, H, D, attn_sl2(HD), 1.0f / sqrtf((float)HD));
   return hipGetLastError();
 }
@@ -2023,9 +2023,9 @@ static hipError_t colsum_simple(const Ta* qkv, const float* lse, float* colsum, 
                                 hipStream_t st) {
   dim3 g((S + 63) / 64, H, B);
   const float sl2 = attn_sl2(hd);
-  if (hd == 32) hipLaunchKernelGGL((attn_colsum_simple<Ta, 32>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
-  else if (hd == 64) hipLaunchKernelGGL((attn_colsum_simple<Ta, 64>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
-  else hipLaunchKernelGGL((attn_colsum_simple<Ta, 128>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
+  if (hd == 32) SR_LAUNCH((attn_colsum_simple<Ta, 32>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
+  else if (hd == 64) SR_LAUNCH((attn_colsum_simple<Ta, 64>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
+  else SR_LAUNCH((attn_colsum_simple<Ta, 128>), g, dim3(64), 0, st, qkv, lse, colsum, S, H, D, sl2);
   return hipGetLastError();
 }
 
@@ -2035,7 +2035,7 @@ hipError_t launch_attn_colsum(int dtype, const void* qkv, const float* lse, floa
   if (dtype == kBF16 && hd == 64) {   // MFMA column sums at head dim 64; other head dims generic
     constexpr int kw = attn_waves<64>();   // the dK/dV kernel's score half: the same shape
     dim3 g((S + 32 * kw - 1) / (32 * kw), H, B);
-    hipLaunchKernelGGL(attn_colsum_mfma<kw>, g, dim3(64 * kw), 0, st, (const bf16_t*)qkv, lse, colsum, S, H, D,
+    SR_LAUNCH(attn_colsum_mfma<kw>, g, dim3(64 * kw), 0, st, (const bf16_t*)qkv, lse, colsum, S, H, D,
                        attn_sl2(hd));
     return hipGetLastError();
   }

@@ -1,7 +1,41 @@
 // Device-side helpers shared by the gfx950 kernels of libsr.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+namespace sr {
+// Completion events bound to kernels at launch.  Every kernel of the library is launched through
+// SR_LAUNCH.  While the calling thread's hook holds a stop event, each launch carries it (and the
+// start event, on the first launch only) with hipExtLaunchKernelGGL, so the events mark that
+// kernel's own start and end.  A separate event record between two kernels of one stream is a
+// marker packet that leaves the stream idle for several microseconds; a bound event costs about
+// a third of that.  Used for the timing of profiled launch groups and for the forks of the
+// backward's second stream (the side stream then waits on the event of the last kernel it needs).
+struct LaunchHook {
+  hipEvent_t start = nullptr;          // bound to the next launch only
+  hipEvent_t stop = nullptr;           // bound to every launch while set
+  hipStream_t last_stream = nullptr;   // stream and stop event of the most recent launch
+  hipEvent_t last_stop = nullptr;
+  unsigned long long launches = 0;     // launches through SR_LAUNCH on this thread
+};
+LaunchHook& launch_hook();   // per thread
+
+template <typename F, typename... A>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t st, A... args) {
+  LaunchHook& h = launch_hook();
+  if (h.stop) {
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, h.start, h.stop, 0, args...);
+    h.start = nullptr;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, shmem, st, args...);
+  }
+  h.last_stream = st;
+  h.last_stop = h.stop;
+  ++h.launches;
+}
+}  // namespace sr
+#define SR_LAUNCH(kernel, ...) ::sr::launch_kernel((kernel), __VA_ARGS__)
 
 typedef uint16_t bf16_t;   // bfloat16 bit pattern in memory
 

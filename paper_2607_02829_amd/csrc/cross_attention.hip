@@ -137,9 +137,9 @@ static hipError_t xfwd(const Ta* q, const Ta* kv, Ta* O, float* lse, int B, int 
   const int hd = D / H;
   dim3 g((Sq + 63) / 64, H, B);
   const float sl2 = xattn_sl2(hd);
-  if (hd == 32) hipLaunchKernelGGL((xattn_fwd_kernel<Ta, 32>), g, dim3(64), 0, st, q, kv, O, lse, Sq, Skv, H, D, sl2);
-  else if (hd == 64) hipLaunchKernelGGL((xattn_fwd_kernel<Ta, 64>), g, dim3(64), 0, st, q, kv, O, lse, Sq, Skv, H, D, sl2);
-  else hipLaunchKernelGGL((xattn_fwd_kernel<Ta, 128>), g, dim3(64), 0, st, q, kv, O, lse, Sq, Skv, H, D, sl2);
+  if (hd == 32) SR_LAUNCH((xattn_fwd_kernel<Ta, 32>), g, dim3(64), 0, st, q, kv, O, lse, Sq, Skv, H, D, sl2);
+  else if (hd == 64) SR_LAUNCH((xattn_fwd_kernel<Ta, 64>), g, dim3(64), 0, st, q, kv, O, lse, Sq, Skv, H, D, sl2);
+  else SR_LAUNCH((xattn_fwd_kernel<Ta, 128>), g, dim3(64), 0, st, q, kv, O, lse, Sq, Skv, H, D, sl2);
   return hipGetLastError();
 }
 
@@ -150,9 +150,9 @@ static hipError_t xbwd(const Ta* q, const Ta* kv, const Ta* dO, const float* lse
   dim3 gq((Sq + 63) / 64, H, B), gk((Skv + 63) / 64, H, B);
   const float sl2 = xattn_sl2(hd), sc = 1.0f / sqrtf((float)hd);
 #define SR_XB(HDV)                                                                                                 \
-  hipLaunchKernelGGL((xattn_bwd_dq_kernel<Ta, HDV>), gq, dim3(64), 0, st, q, kv, dO, lse, delta, dq, Sq, Skv, H, D, \
+  SR_LAUNCH((xattn_bwd_dq_kernel<Ta, HDV>), gq, dim3(64), 0, st, q, kv, dO, lse, delta, dq, Sq, Skv, H, D, \
                      sl2, sc);                                                                                     \
-  hipLaunchKernelGGL((xattn_bwd_dkv_kernel<Ta, HDV>), gk, dim3(64), 0, st, q, kv, dO, lse, delta, dkv, Sq, Skv, H, \
+  SR_LAUNCH((xattn_bwd_dkv_kernel<Ta, HDV>), gk, dim3(64), 0, st, q, kv, dO, lse, delta, dkv, Sq, Skv, H, \
                      D, sl2, sc)
   if (hd == 32) { SR_XB(32); } else if (hd == 64) { SR_XB(64); } else { SR_XB(128); }
 #undef SR_XB

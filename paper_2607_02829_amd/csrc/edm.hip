@@ -74,16 +74,16 @@ __global__ __launch_bounds__(256) void sum_samples_kernel(const float* __restric
 }
 
 hipError_t launch_sigmoid(float* x, int B, int D, int ld, hipStream_t st) {
-  hipLaunchKernelGGL(sigmoid_kernel, dim3((B * D + 255) / 256), dim3(256), 0, st, x, B, D, ld);
+  SR_LAUNCH(sigmoid_kernel, dim3((B * D + 255) / 256), dim3(256), 0, st, x, B, D, ld);
   return hipGetLastError();
 }
 hipError_t launch_sigmoid_grad(float* d, const float* gate, int B, int D, int ld, hipStream_t st) {
-  hipLaunchKernelGGL(sigmoid_grad_kernel, dim3((B * D + 255) / 256), dim3(256), 0, st, d, gate, B, D, ld);
+  SR_LAUNCH(sigmoid_grad_kernel, dim3((B * D + 255) / 256), dim3(256), 0, st, d, gate, B, D, ld);
   return hipGetLastError();
 }
 hipError_t launch_sum_samples(const float* x, int B, int n, int ld, float* out, hipStream_t st) {
   if (!out) return hipSuccess;
-  hipLaunchKernelGGL(sum_samples_kernel, dim3((n + 255) / 256), dim3(256), 0, st, x, B, n, ld, out);
+  SR_LAUNCH(sum_samples_kernel, dim3((n + 255) / 256), dim3(256), 0, st, x, B, n, ld, out);
   return hipGetLastError();
 }
 

@@ -641,7 +641,7 @@ hipError_t launch_reduce_jobs(const ReduceJob* jobs, int njobs, hipStream_t st) 
   }
   if (blocks == 0) return hipSuccess;
   for (int j = k; j <= kMaxReduceJobs; ++j) rj.first[j] = blocks;
-  hipLaunchKernelGGL(reduce_jobs_kernel, dim3((unsigned)blocks), dim3(256), 0, st, rj);
+  SR_LAUNCH(reduce_jobs_kernel, dim3((unsigned)blocks), dim3(256), 0, st, rj);
   return hipGetLastError();
 }
 
@@ -650,7 +650,7 @@ static hipError_t launch_reduce(const float* part, int splits, size_t n, float* 
   const size_t n4 = splits > 1 ? n / 4 : 0;
   const size_t total = n4 + (dbout ? nb : 0);
   if (total == 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, part, splits, n4,
+  SR_LAUNCH(reduce_splits_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, part, splits, n4,
                      out, dbpart, dbparts, nb, dbout);
   return hipGetLastError();
 }
@@ -715,7 +715,7 @@ static hipError_t run_mfma_tile(const GemmDesc& g, const EpiArgs& ep, int splits
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
   const dim3 grid((unsigned)(tiles_m * tiles_n * splits));
 #define SR_GEMM_L(AK, BK)                                                                                        \
-  hipLaunchKernelGGL((gemm_mfma_kernel<BM, BN, NST, OCC, AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st,            \
+  SR_LAUNCH((gemm_mfma_kernel<BM, BN, NST, OCC, AK, BK, EPI, T, Ta>), grid, dim3(256), 0, st,            \
                      (const bf16_t*)g.A, (const bf16_t*)g.B, g.M, g.N, g.K, (int)g.lda, (int)g.ldb,               \
                      (uint32_t)g.a_bytes, (uint32_t)g.b_bytes, kps, tiles_m, tiles_n, ep)
   if (g.a_kmajor && g.b_kmajor) SR_GEMM_L(true, true);
@@ -797,7 +797,7 @@ static hipError_t run_simple(const GemmDesc& g, const EpiArgs& ep, hipStream_t s
   dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, 1);
   const long long a_sm = g.a_kmajor ? g.lda : 1, a_sk = g.a_kmajor ? 1 : g.lda;
   const long long b_sn = g.b_kmajor ? g.ldb : 1, b_sk = g.b_kmajor ? 1 : g.ldb;
-  hipLaunchKernelGGL((gemm_simple_kernel<TA, TB, EPI, T, Ta>), grid, dim3(256), 0, st, (const TA*)g.A,
+  SR_LAUNCH((gemm_simple_kernel<TA, TB, EPI, T, Ta>), grid, dim3(256), 0, st, (const TA*)g.A,
                      (const TB*)g.B, g.M, g.N, g.K, a_sm, a_sk, b_sn, b_sk, ep);
   return hipGetLastError();
 }
@@ -864,9 +864,9 @@ hipError_t launch_gelu(int dtype, const void* z, void* gz, size_t n, hipStream_t
   const size_t n8 = n / 8;   // n is a multiple of 64 (F % 64 == 0)
   const dim3 g((unsigned)std::min<size_t>((n8 + 255) / 256, 4096));
   if (dtype == kBF16)
-    hipLaunchKernelGGL(gelu_kernel<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)z, (bf16_t*)gz, n8);
+    SR_LAUNCH(gelu_kernel<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)z, (bf16_t*)gz, n8);
   else
-    hipLaunchKernelGGL(gelu_kernel<float>, g, dim3(256), 0, st, (const float*)z, (float*)gz, n8);
+    SR_LAUNCH(gelu_kernel<float>, g, dim3(256), 0, st, (const float*)z, (float*)gz, n8);
   return hipGetLastError();
 }
 

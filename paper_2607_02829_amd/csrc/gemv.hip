@@ -112,10 +112,10 @@ hipError_t launch_gemv_rows(int dtype, const void* x, int ldx, const void* W, co
   if (Dd % V != 0) return hipErrorInvalidValue;
   const dim3 g((J + 3) / 4);
   if (dtype == kBF16)
-    hipLaunchKernelGGL(gemv_rows_kernel<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, ldx, (const bf16_t*)W,
+    SR_LAUNCH(gemv_rows_kernel<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, ldx, (const bf16_t*)W,
                        (const bf16_t*)bias, B, J, Dd, y, ldy);
   else
-    hipLaunchKernelGGL(gemv_rows_kernel<float>, g, dim3(256), 0, st, (const float*)x, ldx, (const float*)W,
+    SR_LAUNCH(gemv_rows_kernel<float>, g, dim3(256), 0, st, (const float*)x, ldx, (const float*)W,
                        (const float*)bias, B, J, Dd, y, ldy);
   return hipGetLastError();
 }
@@ -131,9 +131,9 @@ hipError_t launch_gemv_cols(int dtype, const float* x, int ldx, const void* W, i
   const int R = (J + kGemvRows - 1) / kGemvRows;
   const dim3 g((N / V + 63) / 64, R);
   if (dtype == kBF16)
-    hipLaunchKernelGGL(gemv_cols_kernel<bf16_t>, g, dim3(64), 0, st, x, ldx, (const bf16_t*)W, B, J, N, part);
+    SR_LAUNCH(gemv_cols_kernel<bf16_t>, g, dim3(64), 0, st, x, ldx, (const bf16_t*)W, B, J, N, part);
   else
-    hipLaunchKernelGGL(gemv_cols_kernel<float>, g, dim3(64), 0, st, x, ldx, (const float*)W, B, J, N, part);
+    SR_LAUNCH(gemv_cols_kernel<float>, g, dim3(64), 0, st, x, ldx, (const float*)W, B, J, N, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // y[b][n] (+)= sum_r part[r][b][n]: the B*N outputs as one row of width B*N (y contiguous)

@@ -1,6 +1,8 @@
 // Event-based launch timing (see profile.h) and its C entry points.
 #include "profile.h"
 
+#include "common.h"
+
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -38,6 +40,11 @@ hipEvent_t take_event() {
 
 }  // namespace
 
+LaunchHook& launch_hook() {
+  static thread_local LaunchHook h;
+  return h;
+}
+
 bool profiling() { return g_on; }
 bool profiling_all() {
   std::lock_guard<std::mutex> lk(g_mu);
@@ -50,15 +57,30 @@ ProfScope::ProfScope(const char* name, double flops, double bytes, hipStream_t s
   if (!g_filter.empty() && std::strstr(name, g_filter.c_str()) == nullptr) return;
   Rec r{name, take_event(), take_event(), flops, bytes};
   if (!r.a || !r.b) return;
-  hipEventRecord(r.a, st);
+  LaunchHook& h = launch_hook();
+  if (h.start) {   // an enclosing scope that has launched nothing yet starts here
+    hipEventRecord(h.start, st);
+    h.start = nullptr;
+  }
+  outer_start_ = h.start;
+  outer_stop_ = h.stop;
+  launches0_ = h.launches;
+  h.start = r.a;
+  h.stop = r.b;
   g_recs.push_back(r);
   slot_ = (int)g_recs.size() - 1;
 }
 
 ProfScope::~ProfScope() {
   if (slot_ < 0) return;
+  LaunchHook& h = launch_hook();
   std::lock_guard<std::mutex> lk(g_mu);
-  if (slot_ < (int)g_recs.size()) hipEventRecord(g_recs[slot_].b, st_);
+  if (h.launches == launches0_ && slot_ < (int)g_recs.size()) {   // nothing launched: an empty interval
+    hipEventRecord(g_recs[slot_].a, st_);
+    hipEventRecord(g_recs[slot_].b, st_);
+  }
+  h.start = outer_start_;
+  h.stop = outer_stop_;
 }
 
 }  // namespace sr

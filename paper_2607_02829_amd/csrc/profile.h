@@ -1,6 +1,8 @@
 // Optional per-launch timing with HIP events (off unless sr_profile_start is called).
-// A scope records an event before and after the launches it wraps, on the stream they
-// are launched on; sr_profile_stop sums elapsed times per name.
+// A scope binds a start event to the first kernel it launches and a stop event to the last
+// (the launch hook of common.h), so its interval is that of its kernels' own execution;
+// a scope that launches nothing records both events where it ends.  sr_profile_stop sums
+// elapsed times per name.
 #pragma once
 #include <hip/hip_runtime.h>
 
@@ -21,6 +23,8 @@ class ProfScope {
  private:
   int slot_ = -1;
   hipStream_t st_;
+  hipEvent_t outer_start_ = nullptr, outer_stop_ = nullptr;   // the enclosing binding, restored at the end
+  unsigned long long launches0_ = 0;
 };
 
 }  // namespace sr

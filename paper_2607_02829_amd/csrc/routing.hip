@@ -161,10 +161,10 @@ hipError_t launch_gather_rows_f32(int dtype, int B, int L, int K, int D, const v
   const int chunks = D * elt / 16;
   dim3 g((B * K + kRowsPerBlock - 1) / kRowsPerBlock);
   if (dtype == kBF16)
-    hipLaunchKernelGGL(gather_rows_f32_kernel<bf16_t>, g, dim3(256), 0, st, (const i32x4*)x, idx, y32, (i32x4*)ycopy,
+    SR_LAUNCH(gather_rows_f32_kernel<bf16_t>, g, dim3(256), 0, st, (const i32x4*)x, idx, y32, (i32x4*)ycopy,
                        B, L, K, chunks, shared);
   else
-    hipLaunchKernelGGL(gather_rows_f32_kernel<float>, g, dim3(256), 0, st, (const i32x4*)x, idx, y32, (i32x4*)ycopy,
+    SR_LAUNCH(gather_rows_f32_kernel<float>, g, dim3(256), 0, st, (const i32x4*)x, idx, y32, (i32x4*)ycopy,
                        B, L, K, chunks, shared);
   return hipGetLastError();
 }
@@ -175,10 +175,10 @@ hipError_t launch_scatter_f32_delta(int dtype, int B, int L, int K, int D, void*
   const int chunks = D * elt / 16;
   dim3 g((B * K + kRowsPerBlock - 1) / kRowsPerBlock);
   if (dtype == kBF16)
-    hipLaunchKernelGGL(scatter_f32_delta_kernel<bf16_t>, g, dim3(256), 0, st, (i32x4*)x, h32, idx, B, L, K, chunks,
+    SR_LAUNCH(scatter_f32_delta_kernel<bf16_t>, g, dim3(256), 0, st, (i32x4*)x, h32, idx, B, L, K, chunks,
                        shared);
   else
-    hipLaunchKernelGGL(scatter_f32_delta_kernel<float>, g, dim3(256), 0, st, (i32x4*)x, h32, idx, B, L, K, chunks,
+    SR_LAUNCH(scatter_f32_delta_kernel<float>, g, dim3(256), 0, st, (i32x4*)x, h32, idx, B, L, K, chunks,
                        shared);
   return hipGetLastError();
 }
@@ -188,7 +188,7 @@ hipError_t launch_gather(int elt, int B, int L, int K, int D, const void* x, con
   const int chunks = D * elt / 16;
   constexpr int rows = kRowsPerBlock * kGatherRows;
   dim3 g((B * K + rows - 1) / rows);
-  hipLaunchKernelGGL(gather_kernel, g, dim3(256), 0, st, (const i32x4*)x, idx, (i32x4*)h0, B, L, K, chunks,
+  SR_LAUNCH(gather_kernel, g, dim3(256), 0, st, (const i32x4*)x, idx, (i32x4*)h0, B, L, K, chunks,
                      shared);
   return hipGetLastError();
 }
@@ -199,10 +199,10 @@ hipError_t launch_scatter_delta(int dtype, int B, int L, int K, int D, void* x, 
   const int chunks = D * elt / 16;
   dim3 g((B * K + kRowsPerBlock - 1) / kRowsPerBlock);
   if (dtype == kBF16)
-    hipLaunchKernelGGL(scatter_delta_kernel<bf16_t>, g, dim3(256), 0, st, (i32x4*)x, (const i32x4*)h,
+    SR_LAUNCH(scatter_delta_kernel<bf16_t>, g, dim3(256), 0, st, (i32x4*)x, (const i32x4*)h,
                        (const i32x4*)h0, idx, B, L, K, chunks, shared);
   else
-    hipLaunchKernelGGL(scatter_delta_kernel<float>, g, dim3(256), 0, st, (i32x4*)x, (const i32x4*)h,
+    SR_LAUNCH(scatter_delta_kernel<float>, g, dim3(256), 0, st, (i32x4*)x, (const i32x4*)h,
                        (const i32x4*)h0, idx, B, L, K, chunks, shared);
   return hipGetLastError();
 }

@@ -67,9 +67,9 @@ __global__ __launch_bounds__(256) void ln_fwd_kernel(const float* __restrict__ x
                                                      const T* __restrict__ beta, const float* __restrict__ mod,
                                                      int mod_off, int M, int S, int D, float eps,
                                                      Ta* __restrict__ y, float* __restrict__ mean_out,
-                                                     float* __restrict__ rstd_out, const T* __restrict__ gsrc = nullptr,
-                                                     const int32_t* __restrict__ gidx = nullptr, int gL = 0,
-                                                     int gshared = 0, float* __restrict__ xcopy = nullptr) {
+                                                     float* __restrict__ rstd_out, const T* __restrict__ gsrc,
+                                                     const int32_t* __restrict__ gidx, int gL,
+                                                     int gshared, float* __restrict__ xcopy) {
   constexpr int NJ = NJC > 0 ? NJC : kMaxPerLane / V;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -423,8 +423,9 @@ hipError_t launch_ln_fwd(int dtype, const float* x, const void* gamma, const voi
                          int mod_off, int M, int S, int D, float eps, void* y, float* mean, float* rstd,
                          hipStream_t st) {
 #define SR_LNF(T, V, NJC)                                                                                    \
-  hipLaunchKernelGGL((ln_fwd_kernel<T, T, V, NJC>), grid1d(M, 4), dim3(256), 0, st, x, (const T*)gamma,      \
-                     (const T*)beta, mod, mod_off, M, S, D, eps, (T*)y, mean, rstd)
+  SR_LAUNCH((ln_fwd_kernel<T, T, V, NJC>), grid1d(M, 4), dim3(256), 0, st, x, (const T*)gamma,      \
+                     (const T*)beta, mod, mod_off, M, S, D, eps, (T*)y, mean, rstd, (const T*)nullptr, \
+                     (const int32_t*)nullptr, 0, 0, (float*)nullptr)
 #define SR_LNF_T(T)                                      \
   switch (D % 256 == 0 ? D / 256 : 0) {                  \
     case 1: SR_LNF(T, 4, 1); break;                      \
@@ -443,7 +444,7 @@ hipError_t launch_ln_fwd_gather(int dtype, const void* xsrc, const int32_t* idx,
                                 const void* gamma, const void* beta, const float* mod, int mod_off, int M, int S,
                                 int D, float eps, void* y, float* mean, float* rstd, hipStream_t st) {
 #define SR_LNG(T, V, NJC)                                                                                         \
-  hipLaunchKernelGGL((ln_fwd_kernel<T, T, V, NJC, true>), grid1d(M, 4), dim3(256), 0, st, (const float*)nullptr, \
+  SR_LAUNCH((ln_fwd_kernel<T, T, V, NJC, true>), grid1d(M, 4), dim3(256), 0, st, (const float*)nullptr, \
                      (const T*)gamma, (const T*)beta, mod, mod_off, M, S, D, eps, (T*)y, mean, rstd,              \
                      (const T*)xsrc, idx, L, shared, xcopy)
 #define SR_LNG_T(T)                                      \
@@ -464,7 +465,7 @@ hipError_t launch_ln_apply(int dtype, const float* x, const void* gamma, const v
                            int mod_off, int M, int S, int D, const float* mean, const float* rstd, void* y,
                            hipStream_t st) {
 #define SR_LNA(T, V, NJC)                                                                                       \
-  hipLaunchKernelGGL((ln_fwd_kernel<T, T, V, NJC, false, true>), grid1d(M, 4), dim3(256), 0, st, x,            \
+  SR_LAUNCH((ln_fwd_kernel<T, T, V, NJC, false, true>), grid1d(M, 4), dim3(256), 0, st, x,            \
                      (const T*)gamma, (const T*)beta, mod, mod_off, M, S, D, 0.0f, (T*)y, const_cast<float*>(mean), \
                      const_cast<float*>(rstd), (const T*)nullptr, (const int32_t*)nullptr, 0, 0, (float*)nullptr)
 #define SR_LNA_T(T)                                      \
@@ -488,7 +489,7 @@ hipError_t launch_ln_bwd(int dtype, const float* du, const float* x, const float
                          float* dx, void* dx_act, float* part, hipStream_t st) {
   dim3 g(ln_bwd_chunks(S), B);
 #define SR_LNB(T, V, NJC)                                                                                  \
-  hipLaunchKernelGGL((ln_bwd_kernel<T, T, V, NJC>), g, dim3(256), 0, st, du, x, mean, rstd, (const T*)gamma, \
+  SR_LAUNCH((ln_bwd_kernel<T, T, V, NJC>), g, dim3(256), 0, st, du, x, mean, rstd, (const T*)gamma, \
                      mod, mod_off, dres, S, D, dx, (T*)dx_act, part)
 #define SR_LNB_T(T)                                      \
   switch (D % 256 == 0 ? D / 256 : 0) {                  \
@@ -511,7 +512,7 @@ hipError_t launch_colsum(int xt, const void* X, int yt, const void* Y, const flo
                          int N, float* part, hipStream_t st) {
   dim3 g((N + 255) / 256, colsum_chunks(S), B);
 #define SR_COLSUM(TX, TY) \
-  hipLaunchKernelGGL((colsum_kernel<TX, TY>), g, dim3(256), 0, st, (const TX*)X, (const TY*)Y, w, wstride, S, N, part)
+  SR_LAUNCH((colsum_kernel<TX, TY>), g, dim3(256), 0, st, (const TX*)X, (const TY*)Y, w, wstride, S, N, part)
   if (xt == kBF16) {
     if (yt == kBF16) SR_COLSUM(bf16_t, bf16_t); else SR_COLSUM(bf16_t, float);
   } else {
@@ -527,7 +528,7 @@ hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, cons
   const uint32_t n8 = (uint32_t)(n / 8);
   dim3 g((unsigned)std::min<size_t>((n8 + 255) / 256, 65536));
 #define SR_CONV(TI, TO)                                                                                  \
-  hipLaunchKernelGGL((convert_kernel<TI, TO>), g, dim3(256), 0, st, (const TI*)x, (TO*)y, n8, w, wstride, \
+  SR_LAUNCH((convert_kernel<TI, TO>), g, dim3(256), 0, st, (const TI*)x, (TO*)y, n8, w, wstride, \
                      (uint32_t)S, (uint32_t)D, y32)
   if (ti == kBF16) {
     if (to == kBF16) SR_CONV(bf16_t, bf16_t); else SR_CONV(bf16_t, float);
@@ -541,14 +542,14 @@ hipError_t launch_convert(int ti, const void* x, int to, void* y, size_t n, cons
 hipError_t launch_reduce_cols(const float* part, int R, int G, int sum_groups, int width, int half, float* out_lo,
                               float* out_hi, int out_stride, hipStream_t st, int accumulate) {
   dim3 g((width + 63) / 64, sum_groups ? 1 : G);
-  hipLaunchKernelGGL(reduce_cols_kernel, g, dim3(1024), 0, st, part, R, G, sum_groups, width, half, out_lo, out_hi,
+  SR_LAUNCH(reduce_cols_kernel, g, dim3(1024), 0, st, part, R, G, sum_groups, width, half, out_lo, out_hi,
                      out_stride, accumulate);
   return hipGetLastError();
 }
 
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st) {
   dim3 g((unsigned)std::min<size_t>((n + 255) / 256, 65536));
-  hipLaunchKernelGGL(fill_kernel, g, dim3(256), 0, st, p, n, v);
+  SR_LAUNCH(fill_kernel, g, dim3(256), 0, st, p, n, v);
   return hipGetLastError();
 }
 
@@ -556,10 +557,10 @@ hipError_t launch_attn_delta(int dtype, const void* dO, const void* O, int B, in
                              hipStream_t st) {
   const size_t rows = (size_t)B * S;
   if (dtype == kBF16)
-    hipLaunchKernelGGL(attn_delta_kernel<bf16_t>, grid1d(rows, 4), dim3(256), 0, st, (const bf16_t*)dO,
+    SR_LAUNCH(attn_delta_kernel<bf16_t>, grid1d(rows, 4), dim3(256), 0, st, (const bf16_t*)dO,
                        (const bf16_t*)O, B, S, H, hd, delta);
   else
-    hipLaunchKernelGGL(attn_delta_kernel<float>, grid1d(rows, 4), dim3(256), 0, st, (const float*)dO,
+    SR_LAUNCH(attn_delta_kernel<float>, grid1d(rows, 4), dim3(256), 0, st, (const float*)dO,
                        (const float*)O, B, S, H, hd, delta);
   return hipGetLastError();
 }

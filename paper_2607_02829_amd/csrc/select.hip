@@ -244,7 +244,7 @@ __global__ __launch_bounds__(1024) void validate_kernel(const int32_t* idx, int 
 
 hipError_t launch_select_random(int rows, int L, int K, uint64_t seed, uint64_t step, int32_t* idx,
                                 hipStream_t st) {
-  hipLaunchKernelGGL(select_random_kernel, dim3(rows), dim3(kSelThreads), 0, st, L, K, seed, step, idx);
+  SR_LAUNCH(select_random_kernel, dim3(rows), dim3(kSelThreads), 0, st, L, K, seed, step, idx);
   return hipGetLastError();
 }
 
@@ -279,25 +279,25 @@ hipError_t launch_select_topk(int dtype, int rows, int L, int D, int K, const vo
   const int ntok = rows * L;
   dim3 g((ntok + 3) / 4);
   if (dtype == kBF16)
-    hipLaunchKernelGGL(topk_score_kernel<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)xt, (const bf16_t*)xp,
+    SR_LAUNCH(topk_score_kernel<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)xt, (const bf16_t*)xp,
                        ntok, D, score);
   else
-    hipLaunchKernelGGL(topk_score_kernel<float>, g, dim3(256), 0, st, (const float*)xt, (const float*)xp,
+    SR_LAUNCH(topk_score_kernel<float>, g, dim3(256), 0, st, (const float*)xt, (const float*)xp,
                        ntok, D, score);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(select_topk_kernel, dim3(rows), dim3(kSelThreads), 0, st, score, 1, L, K, idx);
+  SR_LAUNCH(select_topk_kernel, dim3(rows), dim3(kSelThreads), 0, st, score, 1, L, K, idx);
   return hipGetLastError();
 }
 
 hipError_t launch_select_topk_planes(int rows, int L, int K, int parts, const float* planes, int32_t* idx,
                                      hipStream_t st) {
-  hipLaunchKernelGGL(select_topk_kernel, dim3(rows), dim3(kSelThreads), 0, st, planes, parts, L, K, idx);
+  SR_LAUNCH(select_topk_kernel, dim3(rows), dim3(kSelThreads), 0, st, planes, parts, L, K, idx);
   return hipGetLastError();
 }
 
 hipError_t launch_validate(const int32_t* idx, int rows, int K, int L, int32_t* ok, hipStream_t st) {
-  hipLaunchKernelGGL(validate_kernel, dim3(1), dim3(1024), 0, st, idx, rows, K, L, ok);
+  SR_LAUNCH(validate_kernel, dim3(1), dim3(1024), 0, st, idx, rows, K, L, ok);
   return hipGetLastError();
 }
 

@@ -24,6 +24,7 @@
 #include <mutex>
 #include <vector>
 
+#include "common.h"
 #include "profile.h"
 
 namespace sr {
@@ -334,12 +335,38 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
   hipStream_t side = nullptr;
   BwdEvents* ev = nullptr;
   bool pending[kSlots] = {};   // recorded and not yet waited on
-  // side stream: wait for everything issued on st so far, run the weight gradient, signal slot
   const bool serial = profiling_all();
+  // Fork points: the main-stream kernels right before a fork carry the fork event themselves
+  // (bound at launch, see LaunchHook), and the fork waits on the event the last of them carries,
+  // provided no kernel was launched in between; otherwise it records the event on st.  Not while
+  // st is being captured into a graph (event records there become graph nodes).
+  hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+  const bool bind = !serial && hipStreamIsCapturing(st, &capture) == hipSuccess &&
+                    capture == hipStreamCaptureStatusNone;
+  hipEvent_t fork_ev = nullptr;         // event carried by the last kernel of the last fork point
+  unsigned long long fork_at = 0;       // launch count right after it
+  auto fork_point = [&](auto&& launch) -> hipError_t {
+    if (!bind) return launch();
+    LaunchHook& h = launch_hook();
+    const hipEvent_t outer = h.stop;
+    const unsigned long long n0 = h.launches;
+    h.stop = ev->fork;
+    const hipError_t r = launch();
+    h.stop = outer;
+    fork_ev = r == hipSuccess && h.launches > n0 && h.last_stream == st ? h.last_stop : nullptr;
+    fork_at = h.launches;
+    return r;
+  };
+  // side stream: wait for everything issued on st so far, run the weight gradient, signal slot
   auto on_side = [&](int slot, auto&& launch) -> hipError_t {
     if (serial) return launch(st);
-    SR_TRY(hipEventRecord(ev->fork, st));
-    SR_TRY(hipStreamWaitEvent(side, ev->fork, 0));
+    if (fork_ev && launch_hook().launches == fork_at) {
+      SR_TRY(hipStreamWaitEvent(side, fork_ev, 0));
+    } else {
+      SR_TRY(hipEventRecord(ev->fork, st));
+      SR_TRY(hipStreamWaitEvent(side, ev->fork, 0));
+    }
+    fork_ev = nullptr;
     SR_TRY(launch(side));
     SR_TRY(hipEventRecord(ev->done[slot], side));
     pending[slot] = true;
@@ -409,8 +436,10 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       {
         GemmDesc gd = desc(d, g0, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
         EpiArgs ep; ep.z_in = s.z; ep.out_act = dz; ep.ldo = F;
-        ProfScope ps("gemm_dx_fc2", gemm_flops(M, F, D), gemm_bytes(d, M, F, D, 2 * (int)e), st);
-        SR_TRY(launch_gemm(gd, EPI_DGELU, ep, st));
+        SR_TRY(fork_point([&]() -> hipError_t {
+          ProfScope ps("gemm_dx_fc2", gemm_flops(M, F, D), gemm_bytes(d, M, F, D, 2 * (int)e), st);
+          return launch_gemm(gd, EPI_DGELU, ep, st);
+        }));
       }
       // FC1: dW1, db1; du = dz W1
       SR_TRY(on_side(kFc1 + par, [&](hipStream_t ss) -> hipError_t {
@@ -429,11 +458,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       }
       // LN2 backward: g_res2 = g_res + LN2^T du (pre-LN also writes the activation copy)
       if (!ada) SR_TRY(join(kO));   // g1 may still be read by the previous block's dW_o
-      {
+      SR_TRY(fork_point([&]() -> hipError_t {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
-        SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
-                             d.B, S, D, sc.g_res2, ada ? nullptr : g1, sc.lnpart[0], st));
-      }
+        return launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
+                             d.B, S, D, sc.g_res2, ada ? nullptr : g1, sc.lnpart[0], st);
+      }));
       if (ada) {   // dscale2 -> dmod[4D..5D), dshift2 -> dmod[3D..4D)
         ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
         SR_TRY(launch_reduce_cols(sc.lnpart[0], nln, d.B, 0, 2 * D, D, sc.dmod + 4 * D, sc.dmod + 3 * D, 6 * D, st));
@@ -465,7 +494,9 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, d.B, S, d.H, D / d.H, sc.delta, st));
       }
       SR_TRY(join(kQkv + par));   // dqkv[par] may still be read by dW_qkv two blocks back
-      SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, dqkv, d.B, S, d.H, D, st));
+      SR_TRY(fork_point([&]() -> hipError_t {
+        return launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, dqkv, d.B, S, d.H, D, st);
+      }));
       // QKV: dWqkv, dbqkv; du = dqkv Wqkv
       SR_TRY(on_side(kQkv + par, [&](hipStream_t ss) -> hipError_t {
         if (g.w_qkv || g.b_qkv) {   // u1 = LN1(h) recomputed from the saved statistics
@@ -488,11 +519,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       }
       // LN1 backward: g_res = g_res2 + LN1^T du (pre-LN: plus the activation copy for the next block)
       if (!ada) SR_TRY(join(kFc2));   // g0 is still read by this block's dW_fc2
-      {
+      SR_TRY(fork_point([&]() -> hipError_t {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
-        SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2,
-                             d.B, S, D, sc.g_res, ada ? nullptr : g0, sc.lnpart[ada ? 0 : 1], st));
-      }
+        return launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2,
+                             d.B, S, D, sc.g_res, ada ? nullptr : g0, sc.lnpart[ada ? 0 : 1], st);
+      }));
       if (ada) {   // dscale1 -> dmod[D..2D), dshift1 -> dmod[0..D)
         ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
         SR_TRY(launch_reduce_cols(sc.lnpart[0], nln, d.B, 0, 2 * D, D, sc.dmod + D, sc.dmod, 6 * D, st));
