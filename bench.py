@@ -756,6 +756,13 @@ def main():
     else:
         achieved, peak, unit, bound = per_launch_bytes / (per_launch_ms * 1e-3), PEAK_HBM_BYTES, "GB/s", "hbm"
         achieved_u, peak_u = achieved / 1e9, peak / 1e9
+    # the sustained matrix-core rate of this machine (its clock under MFMA load), a second
+    # denominator beside the datasheet peak
+    sustained = None
+    if bound == "mfma":
+        sink = torch.empty(4, dtype=torch.float32, device="cuda")
+        sustained = abi.sr_probe_mfma_rate(sink)
+        torch.cuda.synchronize()
 
     # whole-stack MFMA fraction: algorithmic block FLOPs per step over step time
     blk_flops = block_flops(w, w.K)
@@ -870,7 +877,9 @@ def main():
                        "ratio": round(dense["peak_bytes"] / sparse_peak, 3) if dense else None},
         "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved_u, 2), "peak": peak_u, "unit": unit,
                      "frac": round(achieved / peak, 4), "traffic": traffic_for(dom, w.name),
-                     "launches_timed": int(d["launches"]), "avg_launch_us": round(per_launch_ms * 1e3, 2)},
+                     "launches_timed": int(d["launches"]), "avg_launch_us": round(per_launch_ms * 1e3, 2),
+                     "peak_sustained": round(sustained, 1) if sustained else None,
+                     "frac_sustained": round(achieved_u / sustained, 4) if sustained else None},
         "cpu_baseline": cpu,
         "routing_bandwidth": routing,
         "outputs_finite": finite,

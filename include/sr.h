@@ -360,6 +360,17 @@ SR_API sr_status sr_select_topk_scores(const sr_config* cfg, int32_t K, const fl
 SR_API sr_status sr_profile_start(const char* name_filter);
 SR_API sr_status sr_profile_stop(char* out, size_t out_bytes, size_t* needed);
 
+/* Sustained bf16 matrix-core rate of the current device, for the denominator of a
+ * measured roofline (not needed by the method).  Runs two launches of a register-only
+ * kernel (one workgroup of eight waves per compute unit, independent 32x32x16 bf16 MFMAs,
+ * no memory traffic in its loop; the first launch only lets the clock settle) on
+ * `stream`, times the second with HIP events and waits for it.
+ *   sink: device pointer to at least 4 writable bytes (the kernel stores one float there).
+ *   tflops: host pointer; receives the achieved dense bf16 TFLOP/s (the datasheet peak is
+ *   2500 at 2.4 GHz; the sustained rate reflects the clock under matrix load).
+ * Errors: SR_EINVAL for a NULL argument, SR_EHIP if a launch or event call fails. */
+SR_API sr_status sr_probe_mfma_rate(float* sink, double* tflops, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -27,7 +27,7 @@ EXPORTS = ("sr_last_error", "sr_version", "sr_workspace_bytes", "sr_select_scrat
            "sr_attention_colsums", "sr_select_topk_scores", "sr_routed_blocks_fwd", "sr_routed_blocks_bwd",
            "sr_cross_attention_fwd", "sr_cross_attention_bwd",
            "sr_edm_workspace_bytes", "sr_edm_blocks_fwd", "sr_edm_blocks_bwd",
-           "sr_profile_start", "sr_profile_stop")
+           "sr_profile_start", "sr_profile_stop", "sr_probe_mfma_rate")
 
 
 class SrLibraryMissing(RuntimeError):
@@ -106,6 +106,7 @@ def lib(path: str = LIB_PATH):
         "sr_edm_blocks_bwd": ([CP, I32, P, P, P, P, SZ, P, P, P, P, P, P, SZ, P], I32),
         "sr_profile_start": ([ctypes.c_char_p], I32),
         "sr_profile_stop": ([ctypes.c_char_p, SZ, ctypes.POINTER(SZ)], I32),
+        "sr_probe_mfma_rate": ([P, ctypes.POINTER(ctypes.c_double), P], I32),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -270,6 +271,13 @@ def sr_profile_stop() -> dict[str, dict[str, float]]:
     need = ctypes.c_size_t()
     _check(lib().sr_profile_stop(buf, len(buf), ctypes.byref(need)))
     return _parse_profile(buf.value.decode())
+
+
+def sr_probe_mfma_rate(sink, stream=None) -> float:
+    """Sustained dense bf16 MFMA TFLOP/s of the current device (sink: >= 4 bytes of device memory)."""
+    out = ctypes.c_double()
+    _check(lib().sr_probe_mfma_rate(_p(sink), ctypes.byref(out), _stream(stream)))
+    return out.value
 
 
 def _parse_profile(text: str) -> dict[str, dict[str, float]]:

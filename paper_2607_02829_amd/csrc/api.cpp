@@ -555,6 +555,11 @@ sr_status sr_edm_blocks_bwd(const sr_config* cfg, int32_t S, const sr_edm_block_
                     "edm_blocks_bwd");
 }
 
+sr_status sr_probe_mfma_rate(float* sink, double* tflops, void* stream) {
+  SR_CHECK(sink != nullptr && tflops != nullptr, SR_EINVAL, "sink and tflops must not be NULL");
+  return hip_status(sr::probe_mfma_rate(sink, tflops, (hipStream_t)stream), "probe_mfma_rate");
+}
+
 sr_status sr_validate_indices(const sr_config* cfg, int32_t K, const int32_t* idx, int32_t* ok_dev, void* stream) {
   sr_status s = check_cfg(cfg, true);
   if (s != SR_OK) return s;

@@ -83,6 +83,56 @@ ProfScope::~ProfScope() {
   h.stop = outer_stop_;
 }
 
+// Sustained bf16 matrix-core rate: eight waves per CU (two per SIMD), each issuing independent
+// v_mfma_f32_32x32x16_bf16 into eight accumulators, no memory traffic in the loop.  One
+// workgroup per CU, so the launch is a single round.
+constexpr int kProbeIters = 4096, kProbeAcc = 8;
+
+__global__ __launch_bounds__(512) void mfma_probe_kernel(float* sink, int iters) {
+  f32x16 acc[kProbeAcc];
+  for (int i = 0; i < kProbeAcc; ++i)
+    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+  i32x4 a = {(int)threadIdx.x, 0x3f803f80, 0x3f003f00, (int)blockIdx.x};
+  i32x4 b = {0x3c003c00, (int)threadIdx.x, 0x3e003e00, 0x3d003d00};
+  asm volatile("" : "+v"(a), "+v"(b));   // opaque operands: nothing folds
+  for (int it = 0; it < iters; ++it)
+#pragma unroll
+    for (int i = 0; i < kProbeAcc; ++i)
+      acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                       acc[i], 0, 0, 0);
+  float s = 0.f;
+  for (int i = 0; i < kProbeAcc; ++i)
+    for (int r = 0; r < 16; ++r) s += acc[i][r];
+  if (threadIdx.x == 0) sink[0] = s;   // keeps the work; every workgroup writes the same word
+}
+
+hipError_t probe_mfma_rate(float* sink, double* tflops, hipStream_t st) {
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  hipEvent_t a = nullptr, b = nullptr;
+  if ((e = hipEventCreate(&a)) != hipSuccess) return e;
+  if ((e = hipEventCreate(&b)) != hipSuccess) {
+    hipEventDestroy(a);
+    return e;
+  }
+  SR_LAUNCH(mfma_probe_kernel, dim3(cus), dim3(512), 0, st, sink, kProbeIters);   // warm-up (clock ramp)
+  e = hipEventRecord(a, st);
+  if (e == hipSuccess) SR_LAUNCH(mfma_probe_kernel, dim3(cus), dim3(512), 0, st, sink, kProbeIters);
+  if (e == hipSuccess) e = hipGetLastError();
+  if (e == hipSuccess) e = hipEventRecord(b, st);
+  if (e == hipSuccess) e = hipEventSynchronize(b);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+  hipEventDestroy(a);
+  hipEventDestroy(b);
+  if (e != hipSuccess) return e;
+  const double flops = (double)cus * 8 * kProbeIters * kProbeAcc * (2.0 * 32 * 32 * 16);
+  *tflops = ms > 0.f ? flops / (ms * 1e-3) / 1e12 : 0.0;
+  return hipSuccess;
+}
+
 }  // namespace sr
 
 extern "C" {

@@ -80,6 +80,8 @@ hipError_t select_static_scratch(float** out);
 hipError_t launch_select_topk_planes(int rows, int L, int K, int parts, const float* planes, int32_t* idx,
                                      hipStream_t st);
 hipError_t launch_validate(const int32_t* idx, int rows, int K, int L, int32_t* ok, hipStream_t st);
+// Sustained bf16 MFMA rate of the current device (TFLOP/s), timed on st (synchronises on it).
+hipError_t probe_mfma_rate(float* sink, double* tflops, hipStream_t st);
 
 hipError_t launch_gather(int elt, int B, int L, int K, int D, const void* x, const int32_t* idx, void* h0, int shared,
                          hipStream_t st);

@@ -192,3 +192,9 @@ def test_cross_attention_ignores_block_fields():
     assert lib.sr_cross_attention_fwd(ctypes.byref(cfg), 10, 10, None, fake, fake, fake, None) == abi.SR_EINVAL
     assert lib.sr_cross_attention_fwd(ctypes.byref(_cfg(D=96, H=3)), 10, 10, fake, fake, fake, fake,
                                       None) == abi.SR_EUNSUPPORTED
+
+
+def test_mfma_probe_rejects_null_arguments():
+    L = _lib_or_skip()
+    assert L.sr_probe_mfma_rate(None, None, None) == abi.SR_EINVAL
+    assert "NULL" in abi.lib().sr_last_error().decode()
