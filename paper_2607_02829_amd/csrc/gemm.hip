@@ -41,34 +41,58 @@ namespace sr {
 // GELU(z) = z Phi(z) and GELU'(z) = Phi(z) + z phi(z) with the standard normal CDF Phi and
 // density phi (exact GELU, not the tanh form).  Phi comes from erfc in the Chebyshev-fitted form
 // of Press et al. (Numerical Recipes, Sec. 6.2): with x = |z|/sqrt(2) and t = 1/(1 + x/2),
-// erfc(x) = t exp(-x^2 + q(t)); here q is a degree-9 least-squares fit of log2(erfc(x) e^{x^2} / t)
-// on t in (0, 1] (coefficients of our own fit).  Evaluated in fp32 the relative error of erfc is
+// erfc(x) = t exp(-x^2 + q(t)); here q is a least-squares polynomial fit of
+// log2(erfc(x) e^{x^2} / t) on t in (0, 1] (coefficients of our own fits), of degree 9 for fp32
+// activations and 5 for bf16 ones.  Evaluated in fp32 the relative error of erfc is, at degree 9,
 // below 2e-7 for x <= 4 and grows to 1.4e-5 near x = 8, where the rounding of the exponent
-// argument (about -92) dominates; bf16 outputs round at 2e-3.  Branch-free, one reciprocal and
-// one exp2; the tails have relative, not absolute, accuracy.
+// argument (about -92) dominates; at degree 5 it stays below 4.8e-5 for x <= 8.  bf16 outputs
+// round at 2e-3, forty times coarser, and the fp32 mode's gradients need the degree-9 fit.
+// Branch-free, one reciprocal and one exp2; the tails have relative, not absolute, accuracy.
+template <int DEG>
 SR_DEV float half_erfc_of(float z, float zz) {   // 0.5 erfc(|z|/sqrt(2)), zz = z*z
+  static_assert(DEG == 5 || DEG == 9, "fit degree");
   const float t = __builtin_amdgcn_rcpf(fmaf(fabsf(z), 0.35355339059327376f, 1.0f));
-  float q = 0.24651731550693512f;
-  q = fmaf(q, t, -1.1861149072647095f);
-  q = fmaf(q, t, 2.147474527359009f);
-  q = fmaf(q, t, -1.6377531290054321f);
-  q = fmaf(q, t, 0.40232160687446594f);
-  q = fmaf(q, t, -0.2687568664550781f);
-  q = fmaf(q, t, 0.13963006436824799f);
-  q = fmaf(q, t, 0.5397006273269653f);
-  q = fmaf(q, t, 1.4427292346954346f);
-  q = fmaf(q, t, -2.8257482051849365f);   // constant term minus 1: the factor 1/2
+  float q;
+  if constexpr (DEG == 9) {
+    q = 0.24651731550693512f;
+    q = fmaf(q, t, -1.1861149072647095f);
+    q = fmaf(q, t, 2.147474527359009f);
+    q = fmaf(q, t, -1.6377531290054321f);
+    q = fmaf(q, t, 0.40232160687446594f);
+    q = fmaf(q, t, -0.2687568664550781f);
+    q = fmaf(q, t, 0.13963006436824799f);
+    q = fmaf(q, t, 0.5397006273269653f);
+    q = fmaf(q, t, 1.4427292346954346f);
+    q = fmaf(q, t, -2.8257482051849365f);   // constant term minus 1: the factor 1/2
+  } else {
+    q = 0.278960645198822f;
+    q = fmaf(q, t, -0.8764582872390747f);
+    q = fmaf(q, t, 0.52732914686203f);
+    q = fmaf(q, t, 0.44432464241981506f);
+    q = fmaf(q, t, 1.451727271080017f);
+    q = fmaf(q, t, -2.82594895362854f);     // constant term minus 1: the factor 1/2
+  }
   return t * __builtin_amdgcn_exp2f(fmaf(zz, -0.72134752044448170f, q));
 }
+// fit degree for an activation storage type
+template <typename Ta>
+constexpr int gelu_deg() {
+  return sizeof(Ta) == 2 ? 5 : 9;
+}
+template <int DEG>
 SR_DEV float norm_cdf(float z, float zz) {
-  const float h = half_erfc_of(z, zz);
+  const float h = half_erfc_of<DEG>(z, zz);
   return z >= 0.f ? 1.0f - h : h;
 }
-SR_DEV float gelu_f(float z) { return z * norm_cdf(z, z * z); }
+template <int DEG>
+SR_DEV float gelu_f(float z) {
+  return z * norm_cdf<DEG>(z, z * z);
+}
+template <int DEG>
 SR_DEV float gelu_grad_f(float z) {
   const float zz = z * z;
   // phi(z) = 2^(-z^2 log2(e)/2 - log2(sqrt(2 pi)))
-  return norm_cdf(z, zz) + z * __builtin_amdgcn_exp2f(fmaf(zz, -0.72134752044448170f, -1.3257480647361593f));
+  return norm_cdf<DEG>(z, zz) + z * __builtin_amdgcn_exp2f(fmaf(zz, -0.72134752044448170f, -1.3257480647361593f));
 }
 
 template <int EPI, typename T, typename Ta>
@@ -95,10 +119,10 @@ SR_DEV void epilogue(const EpiArgs& e, int m, int n, float v) {
   } else if constexpr (EPI == EPI_GELU) {
     const Ta z = from_f32<Ta>(v + to_f32<T>(((const T*)e.bias)[n]));
     ((Ta*)e.out_act)[o] = z;
-    ((Ta*)e.out_act2)[o] = from_f32<Ta>(gelu_f(to_f32<Ta>(z)));   // of the stored z (recomputed bit for bit)
+    ((Ta*)e.out_act2)[o] = from_f32<Ta>(gelu_f<gelu_deg<Ta>()>(to_f32<Ta>(z)));   // of the stored z (recomputed bit for bit)
   } else if constexpr (EPI == EPI_DGELU) {
     const float z = to_f32<Ta>(((const Ta*)e.z_in)[o]);
-    ((Ta*)e.out_act)[o] = from_f32<Ta>(v * gelu_grad_f(z));
+    ((Ta*)e.out_act)[o] = from_f32<Ta>(v * gelu_grad_f<gelu_deg<Ta>()>(z));
   } else if constexpr (EPI == EPI_ACT) {
     ((Ta*)e.out_act)[o] = from_f32<Ta>(v);
   } else if constexpr (EPI == EPI_F32) {
@@ -192,14 +216,14 @@ SR_DEV float epi_store(const EpiArgs& e, int m, int n, f32x4 v, const EpiIn& in,
     const f32x4 z = unpack4(zb);
     f32x4 gz;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) gz[q] = gelu_f(z[q]);
+    for (int q = 0; q < 4; ++q) gz[q] = gelu_f<gelu_deg<bf16_t>()>(z[q]);
     *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = zb;
     *reinterpret_cast<i32x2*>((bf16_t*)e.out_act2 + o) = pack4(gz);
   } else if constexpr (EPI == EPI_DGELU) {
     const bf16_t* ze = reinterpret_cast<const bf16_t*>(&in.z);
     f32x4 d;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) d[q] = v[q] * gelu_grad_f(bf2f(ze[q]));
+    for (int q = 0; q < 4; ++q) d[q] = v[q] * gelu_grad_f<gelu_deg<bf16_t>()>(bf2f(ze[q]));
     *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(d);
   } else if constexpr (EPI == EPI_ACT) {
     *reinterpret_cast<i32x2*>((bf16_t*)e.out_act + o) = pack4(v);
@@ -847,7 +871,7 @@ __global__ __launch_bounds__(256) void gelu_kernel(const Ta* __restrict__ z, Ta*
         const f32x4 zf = unpack4(zb);
         f32x4 g;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) g[q] = gelu_f(zf[q]);
+        for (int q = 0; q < 4; ++q) g[q] = gelu_f<gelu_deg<Ta>()>(zf[q]);
         const i32x2 gb = pack4(g);
         out[2 * h] = gb[0];
         out[2 * h + 1] = gb[1];
@@ -855,7 +879,7 @@ __global__ __launch_bounds__(256) void gelu_kernel(const Ta* __restrict__ z, Ta*
       reinterpret_cast<i32x4*>(gz)[i] = out;
     } else {
 #pragma unroll
-      for (int q = 0; q < 8; ++q) gz[8 * i + q] = gelu_f(z[8 * i + q]);
+      for (int q = 0; q < 8; ++q) gz[8 * i + q] = gelu_f<gelu_deg<Ta>()>(z[8 * i + q]);
     }
   }
 }
