@@ -345,7 +345,8 @@ SR_API sr_status sr_select_topk_scores(const sr_config* cfg, int32_t K, const fl
 
 /* Launch timing for measurement (not needed by the method).  After
  * sr_profile_start, every library launch group whose name contains `name_filter`
- * ("" or NULL = all) is bracketed by HIP events on its own stream.  With no filter the
+ * ("" or NULL = all) is timed with HIP events bound to its first and last kernel at launch
+ * (hipExtLaunchKernelGGL), so a group's time is its kernels' own execution.  With no filter the
  * backward issues its weight-gradient GEMMs on the caller's stream (they normally run on
  * a second stream of the library, overlapping the rest), so each group is timed alone;
  * with a filter the overlap stays and the named groups are timed as they run.
