@@ -309,6 +309,35 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
     ProfScope ps("reduce", 0, (double)B * nln * 2 * D * 4, st);
     return launch_reduce_cols(sc.lnpart, nln, B, 1, 2 * D, D, dw, dbeta, 0, st);
   };
+  // The weight-gradient GEMMs run on the library's second stream, forked from st after their
+  // inputs are written; st waits for one (join) before it overwrites a buffer that GEMM reads:
+  // g_act (dW_fc2, then dW_o) within the block, dz, dc, dqc, dkvc and dqkv in the next block.
+  // The GEMMs share the split-K partial buffers, which the second stream's order serialises.
+  // While every launch group is being profiled they run on st, so each group's time is its own.
+  enum { kFc2 = 0, kFc1 = 1, kOc = 2, kQ = 3, kKv = 4, kO = 5, kQkv = 6 };
+  const bool serial = profiling_all();
+  hipStream_t side = nullptr;
+  BwdEvents* ev = nullptr;
+  bool pending[kSlots] = {};
+  auto on_side = [&](int slot, auto&& launch) -> hipError_t {
+    if (serial) return launch(st);
+    SR_TRY(hipEventRecord(ev->fork, st));
+    SR_TRY(hipStreamWaitEvent(side, ev->fork, 0));
+    SR_TRY(launch(side));
+    SR_TRY(hipEventRecord(ev->done[slot], side));
+    pending[slot] = true;
+    return hipSuccess;
+  };
+  auto join = [&](int slot) -> hipError_t {
+    if (pending[slot]) SR_TRY(hipStreamWaitEvent(st, ev->done[slot], 0));
+    pending[slot] = false;
+    return hipSuccess;
+  };
+  auto run = [&]() -> hipError_t {
+  if (!serial) {
+    SR_TRY(side_stream(&side));
+    SR_TRY(take_events(&ev));
+  }
   {   // g_res = fp32(dh_out) and its storage copy
     ProfScope ps("convert", 0, (double)M * D * (2 * d.elt + 4), st);
     SR_TRY(launch_convert(d.dtype, dh_out, d.dtype, sc.g_act, (size_t)M * D, nullptr, 0, S, D, sc.g_res, st));
@@ -319,12 +348,17 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
     const sr_edm_block_grads& g = gr[i];
     const bool first = i == d.nb - 1;   // the first block of the backward writes the shared sums
     // ---------------------------------------------------------------- MLP
-    SR_TRY(wgrad("gemm_dw_fc2", d, sc.g_act, D, s.gz, F, M, g.w_fc2, g.b_fc2, sc, st));
+    SR_TRY(on_side(kFc2, [&](hipStream_t ss) {
+      return wgrad("gemm_dw_fc2", d, sc.g_act, D, s.gz, F, M, g.w_fc2, g.b_fc2, sc, ss);
+    }));
+    SR_TRY(join(kFc1));   // dz may still be read by the previous block's dW_fc1
     {
       EpiArgs ep; ep.z_in = s.z; ep.out_act = sc.dz; ep.ldo = F;
       SR_TRY(linear_dx("gemm_dx_fc2", d, sc.g_act, M, D, w.w_fc2, F, EPI_DGELU, ep, st));
     }
-    SR_TRY(wgrad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, M, g.w_fc1, g.b_fc1, sc, st));
+    SR_TRY(on_side(kFc1, [&](hipStream_t ss) {
+      return wgrad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, M, g.w_fc1, g.b_fc1, sc, ss);
+    }));
     {
       EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
       SR_TRY(linear_dx("gemm_dx_fc1", d, sc.dz, M, F, w.w_fc1, D, EPI_F32, ep, st));
@@ -336,6 +370,7 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
     }
     SR_TRY(reduce_ln(g.ln2_w, g.ln2_b));
     // ---------------------------------------------------------------- gated cross-attention
+    SR_TRY(join(kOc));   // dc may still be read by the previous block's dW_oc
     {   // dc = dh2 g (storage copy); dlogit = sum_s dh2 c_out, then times g (1 - g)
       ProfScope ps("convert", 0, (double)M * D * (d.elt + 4), st);
       SR_TRY(launch_convert(kF32, sc.g_res2, d.dtype, sc.dc, (size_t)M * D, s.mod + 2 * D, 6 * D, S, D, nullptr, st));
@@ -346,18 +381,26 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
       SR_TRY(launch_reduce_cols(sc.part, colsum_chunks(S), B, 0, D, D, sc.dmod + 2 * D, nullptr, 6 * D, st));
       SR_TRY(launch_sigmoid_grad(sc.dmod + 2 * D, s.mod + 2 * D, B, D, 6 * D, st));
     }
-    SR_TRY(wgrad("gemm_dw_oc", d, sc.dc, D, s.Oc, D, M, g.w_oc, g.b_oc, sc, st));
+    SR_TRY(on_side(kOc, [&](hipStream_t ss) {
+      return wgrad("gemm_dw_oc", d, sc.dc, D, s.Oc, D, M, g.w_oc, g.b_oc, sc, ss);
+    }));
     {
       EpiArgs ep; ep.out_act = sc.dO; ep.ldo = D;
       SR_TRY(linear_dx("gemm_dx_oc", d, sc.dc, M, D, w.w_oc, D, EPI_ACT, ep, st));
     }
+    SR_TRY(join(kQ));    // dqc and dkvc may still be read by the previous block's dW_q, dW_kv
+    SR_TRY(join(kKv));
     {
       ProfScope ps("xattn_bwd", 8.0 * B * (double)S * d.L * D, (double)B * (5.0 * S + 4.0 * d.L) * D * d.elt, st);
       SR_TRY(launch_xattn_bwd(d.dtype, s.qc, s.kvc, s.Oc, sc.dO, s.lsec, sc.delta, sc.dqc, sc.dkvc, B, S, d.L, d.H, D,
                               st));
     }
-    SR_TRY(wgrad("gemm_dw_q", d, sc.dqc, D, s.uc, D, M, g.w_q, g.b_q, sc, st));
-    SR_TRY(wgrad("gemm_dw_kv", d, sc.dkvc, 2 * D, zc, D, Mc, g.w_kv, g.b_kv, sc, st));
+    SR_TRY(on_side(kQ, [&](hipStream_t ss) {
+      return wgrad("gemm_dw_q", d, sc.dqc, D, s.uc, D, M, g.w_q, g.b_q, sc, ss);
+    }));
+    SR_TRY(on_side(kKv, [&](hipStream_t ss) {
+      return wgrad("gemm_dw_kv", d, sc.dkvc, 2 * D, zc, D, Mc, g.w_kv, g.b_kv, sc, ss);
+    }));
     if (dzc) {   // dZ_c (+)= dkvc W_kv, summed over the blocks in backward order
       EpiArgs ep; ep.out_f32 = dzc; ep.ldo = D;
       SR_TRY(linear_dx("gemm_dzc", d, sc.dkvc, Mc, 2 * D, w.w_kv, D, first ? EPI_F32 : EPI_F32_ACC, ep, st));
@@ -366,6 +409,7 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
       EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
       SR_TRY(linear_dx("gemm_dx_q", d, sc.dqc, M, D, w.w_q, D, EPI_F32, ep, st));
     }
+    SR_TRY(join(kFc2));   // g_act is still read by this block's dW_fc2
     {   // dh1 = dh2 + LNc^T duc, with its storage copy for the output projection
       ProfScope ps("ln_bwd", 0, (double)M * D * (16 + d.elt), st);
       SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.h1, s.meanc, s.rstdc, w.lnc_w, nullptr, 0, sc.g_res2, B, S, D, sc.g_res,
@@ -373,7 +417,9 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
     }
     SR_TRY(reduce_ln(g.lnc_w, g.lnc_b));
     // ---------------------------------------------------------------- FiLM-modulated self-attention
-    SR_TRY(wgrad("gemm_dw_o", d, sc.g_act, D, s.O, D, M, g.w_o, g.b_o, sc, st));
+    SR_TRY(on_side(kO, [&](hipStream_t ss) {
+      return wgrad("gemm_dw_o", d, sc.g_act, D, s.O, D, M, g.w_o, g.b_o, sc, ss);
+    }));
     const bool fuse_delta = d.dtype == kBF16 && D / d.H == 64;
     {
       EpiArgs ep; ep.out_act = sc.dO; ep.ldo = D; ep.o_in = s.O; ep.delta = sc.delta; ep.S = S; ep.H = d.H;
@@ -383,12 +429,16 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
       ProfScope ps("attn_bwd_delta", 0, (double)M * D * d.elt * 2, st);
       SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, B, S, d.H, D / d.H, sc.delta, st));
     }
+    SR_TRY(join(kQkv));   // dqkv may still be read by the previous block's dW_qkv
     SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, B, S, d.H, D, st));
-    SR_TRY(wgrad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u, D, M, g.w_qkv, g.b_qkv, sc, st));
+    SR_TRY(on_side(kQkv, [&](hipStream_t ss) {
+      return wgrad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u, D, M, g.w_qkv, g.b_qkv, sc, ss);
+    }));
     {
       EpiArgs ep; ep.out_f32 = sc.du; ep.ldo = D;
       SR_TRY(linear_dx("gemm_dx_qkv", d, sc.dqkv, M, 3 * D, w.w_qkv, D, EPI_F32, ep, st));
     }
+    SR_TRY(join(kO));   // g_act is still read by this block's dW_o
     {   // dh = dh1 + LN0^T (du (1 + scale)); its partial column sums give dshift, dscale
       ProfScope ps("ln_bwd", 0, (double)M * D * (16 + d.elt), st);
       SR_TRY(launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean0, s.rstd0, nullptr, s.mod, 0, sc.g_res, B, S, D, sc.g_res2,
@@ -424,7 +474,17 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
     ProfScope ps("convert", 0, (double)M * D * (d.elt + 4), st);
     SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
   }
+  for (int k = 0; k < kSlots; ++k) SR_TRY(join(k));   // every gradient is complete when st is
   return hipSuccess;
+  };
+  hipError_t err = run();
+  if (err != hipSuccess && side && ev) {
+    // leave no weight-gradient work unordered with respect to the caller's stream
+    for (int k = 0; k < kSlots; ++k)
+      if (pending[k]) (void)hipStreamWaitEvent(st, ev->done[k], 0);
+  }
+  give_events(ev);
+  return err;
 }
 
 }  // namespace sr

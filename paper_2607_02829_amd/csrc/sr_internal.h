@@ -80,6 +80,21 @@ hipError_t select_static_scratch(float** out);
 hipError_t launch_select_topk_planes(int rows, int L, int K, int parts, const float* planes, int32_t* idx,
                                      hipStream_t st);
 hipError_t launch_validate(const int32_t* idx, int rows, int K, int L, int32_t* ok, hipStream_t st);
+
+// The backward's second stream (one per device, default priority, kept for the life of the
+// process) for the weight-gradient work, and pooled event sets of one backward call: fork
+// (caller stream -> second stream) and, per slot, the completion of the last weight-gradient
+// work that read a buffer the caller's stream will overwrite (second stream -> caller).
+hipError_t side_stream(hipStream_t* out);
+constexpr int kSlots = 8;
+struct BwdEvents {
+  hipEvent_t fork = nullptr;
+  hipEvent_t done[kSlots] = {};
+  int dev = -1;
+  hipError_t create();
+};
+hipError_t take_events(BwdEvents** out);
+void give_events(BwdEvents* e);
 // Sustained bf16 MFMA rate of the current device (TFLOP/s), timed on st (synchronises on it).
 hipError_t probe_mfma_rate(float* sink, double* tflops, hipStream_t st);
 

@@ -257,6 +257,8 @@ hipError_t zero_f32(float* p, size_t n, hipStream_t st) {
   return p ? launch_fill_f32(p, n, 0.0f, st) : hipSuccess;
 }
 
+}  // namespace
+
 // One extra stream per device for the weight-gradient work (default priority; created on
 // first use and kept for the life of the process).
 constexpr int kMaxDevices = 64;
@@ -277,19 +279,15 @@ hipError_t side_stream(hipStream_t* out) {
 // caller).  An event is re-recorded only after the waits on its previous record have been
 // enqueued.  Sets are created once and kept in a per-device pool (creating events per call
 // costs tens of microseconds of host time).
-constexpr int kSlots = 6;   // dW_fc2 (g_act[0]), dW_o (g_act[1]), dW_fc1 (dz[0..1]), dW_qkv (dqkv[0..1])
-struct BwdEvents {
-  hipEvent_t fork = nullptr;
-  hipEvent_t done[kSlots] = {};
-  int dev = -1;
-  hipError_t create() {
-    SR_TRY(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
-    for (hipEvent_t& e : done) SR_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    return hipSuccess;
-  }
-};
+hipError_t BwdEvents::create() {
+  SR_TRY(hipEventCreateWithFlags(&fork, hipEventDisableTiming));
+  for (hipEvent_t& e : done) SR_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  return hipSuccess;
+}
+namespace {
 std::mutex g_ev_mu;
 std::vector<BwdEvents*> g_ev_pool;
+}  // namespace
 hipError_t take_events(BwdEvents** out) {
   int dev = 0;
   SR_TRY(hipGetDevice(&dev));
@@ -317,8 +315,6 @@ void give_events(BwdEvents* e) {
   std::lock_guard<std::mutex> lock(g_ev_mu);
   g_ev_pool.push_back(e);
 }
-
-}  // namespace
 
 hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, const char* saved,
                      const void* dh_out, void* dh_in, const sr_block_grads* gr, float* dcond, char* scratch,
