@@ -319,12 +319,42 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
   hipStream_t side = nullptr;
   BwdEvents* ev = nullptr;
   bool pending[kSlots] = {};
+  // Fork points: the kernels right before a fork carry the fork event themselves (bound at
+  // launch, see LaunchHook), and the fork waits on the event the last of them carries; a fork
+  // that follows another with no kernel launched in between needs no wait at all (the second
+  // stream is already ordered after that point).  Not while st is being captured into a graph.
+  hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+  const bool bind = !serial && hipStreamIsCapturing(st, &capture) == hipSuccess &&
+                    capture == hipStreamCaptureStatusNone;
+  hipEvent_t fork_ev = nullptr;
+  unsigned long long fork_at = 0, forked_at = ~0ull;
+  auto fork_point = [&](auto&& launch) -> hipError_t {
+    if (!bind) return launch();
+    LaunchHook& h = launch_hook();
+    const hipEvent_t outer = h.stop;
+    const unsigned long long n0 = h.launches;
+    h.stop = outer ? outer : ev->fork;   // an enclosing binding (a timed group) serves the fork too
+    const hipError_t r = launch();
+    h.stop = outer;
+    fork_ev = r == hipSuccess && h.launches > n0 && h.last_stream == st ? h.last_stop : nullptr;
+    fork_at = h.launches;
+    return r;
+  };
   auto on_side = [&](int slot, auto&& launch) -> hipError_t {
     if (serial) return launch(st);
-    SR_TRY(hipEventRecord(ev->fork, st));
-    SR_TRY(hipStreamWaitEvent(side, ev->fork, 0));
+    const unsigned long long now = launch_hook().launches;
+    if (bind && now == forked_at) {
+      // nothing launched since the previous fork: the second stream already waits for it
+    } else if (fork_ev && now == fork_at) {
+      SR_TRY(hipStreamWaitEvent(side, fork_ev, 0));
+    } else {
+      SR_TRY(hipEventRecord(ev->fork, st));
+      SR_TRY(hipStreamWaitEvent(side, ev->fork, 0));
+    }
+    fork_ev = nullptr;
     SR_TRY(launch(side));
     SR_TRY(hipEventRecord(ev->done[slot], side));
+    forked_at = launch_hook().launches;   // counts the second stream's launches too
     pending[slot] = true;
     return hipSuccess;
   };
@@ -354,7 +384,7 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
     SR_TRY(join(kFc1));   // dz may still be read by the previous block's dW_fc1
     {
       EpiArgs ep; ep.z_in = s.z; ep.out_act = sc.dz; ep.ldo = F;
-      SR_TRY(linear_dx("gemm_dx_fc2", d, sc.g_act, M, D, w.w_fc2, F, EPI_DGELU, ep, st));
+      SR_TRY(fork_point([&] { return linear_dx("gemm_dx_fc2", d, sc.g_act, M, D, w.w_fc2, F, EPI_DGELU, ep, st); }));
     }
     SR_TRY(on_side(kFc1, [&](hipStream_t ss) {
       return wgrad("gemm_dw_fc1", d, sc.dz, F, s.u2, D, M, g.w_fc1, g.b_fc1, sc, ss);
@@ -375,12 +405,12 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
       ProfScope ps("convert", 0, (double)M * D * (d.elt + 4), st);
       SR_TRY(launch_convert(kF32, sc.g_res2, d.dtype, sc.dc, (size_t)M * D, s.mod + 2 * D, 6 * D, S, D, nullptr, st));
     }
-    {
+    SR_TRY(fork_point([&]() -> hipError_t {
       ProfScope ps("colsum", 0, (double)M * D * (4 + d.elt), st);
       SR_TRY(launch_colsum(kF32, sc.g_res2, d.dtype, s.c_out, nullptr, 0, B, S, D, sc.part, st));
       SR_TRY(launch_reduce_cols(sc.part, colsum_chunks(S), B, 0, D, D, sc.dmod + 2 * D, nullptr, 6 * D, st));
-      SR_TRY(launch_sigmoid_grad(sc.dmod + 2 * D, s.mod + 2 * D, B, D, 6 * D, st));
-    }
+      return launch_sigmoid_grad(sc.dmod + 2 * D, s.mod + 2 * D, B, D, 6 * D, st);
+    }));
     SR_TRY(on_side(kOc, [&](hipStream_t ss) {
       return wgrad("gemm_dw_oc", d, sc.dc, D, s.Oc, D, M, g.w_oc, g.b_oc, sc, ss);
     }));
@@ -392,8 +422,10 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
     SR_TRY(join(kKv));
     {
       ProfScope ps("xattn_bwd", 8.0 * B * (double)S * d.L * D, (double)B * (5.0 * S + 4.0 * d.L) * D * d.elt, st);
-      SR_TRY(launch_xattn_bwd(d.dtype, s.qc, s.kvc, s.Oc, sc.dO, s.lsec, sc.delta, sc.dqc, sc.dkvc, B, S, d.L, d.H, D,
-                              st));
+      SR_TRY(fork_point([&] {
+        return launch_xattn_bwd(d.dtype, s.qc, s.kvc, s.Oc, sc.dO, s.lsec, sc.delta, sc.dqc, sc.dkvc, B, S, d.L, d.H,
+                                D, st);
+      }));
     }
     SR_TRY(on_side(kQ, [&](hipStream_t ss) {
       return wgrad("gemm_dw_q", d, sc.dqc, D, s.uc, D, M, g.w_q, g.b_q, sc, ss);
@@ -430,7 +462,7 @@ hipError_t edm_bwd(const EdmDims& d, const sr_edm_block_params* p, const void* e
       SR_TRY(launch_attn_delta(d.dtype, sc.dO, s.O, B, S, d.H, D / d.H, sc.delta, st));
     }
     SR_TRY(join(kQkv));   // dqkv may still be read by the previous block's dW_qkv
-    SR_TRY(launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, B, S, d.H, D, st));
+    SR_TRY(fork_point([&] { return launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, sc.dqkv, B, S, d.H, D, st); }));
     SR_TRY(on_side(kQkv, [&](hipStream_t ss) {
       return wgrad("gemm_dw_qkv", d, sc.dqkv, 3 * D, s.u, D, M, g.w_qkv, g.b_qkv, sc, ss);
     }));

@@ -346,7 +346,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
     LaunchHook& h = launch_hook();
     const hipEvent_t outer = h.stop;
     const unsigned long long n0 = h.launches;
-    h.stop = ev->fork;
+    h.stop = outer ? outer : ev->fork;   // an enclosing binding (a timed group) serves the fork too
     const hipError_t r = launch();
     h.stop = outer;
     fork_ev = r == hipSuccess && h.launches > n0 && h.last_stream == st ? h.last_stop : nullptr;
