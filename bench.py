@@ -276,6 +276,7 @@ def trunk_sweep(w, dense_ms: float | None, steps: int = 3) -> dict:
     n-block step.  K = floor(r L) per sample; r = 1 routes every token through the middle."""
     import math
     import torch
+    from paper_2607_02829_amd.trunk import eq_speedup_estimate
     out = {"keep": [], "split": []}
     n = w.n_blocks
     runs = [("keep", (2, n - 4, 2), r) for r in (0.10, 0.25, 0.50, 0.75, 1.0)]
@@ -289,7 +290,7 @@ def trunk_sweep(w, dense_ms: float | None, steps: int = 3) -> dict:
         n1, n2, n3 = split
         rec = {"split": list(split), "keep": r, "K": K, "ms_per_step": round(tms, 3),
                "speedup_vs_dense": round(dense_ms / tms, 3) if dense_ms else None,
-               "eq_speedup_estimate": round(n / (n1 + n2 * r * r + n3), 3)}
+               "eq_speedup_estimate": round(eq_speedup_estimate(split, r), 3)}
         out[kind].append(rec)
         log(f"trunk {kind}: split {split} r={r} K={K}: {tms:.2f} ms, speedup {rec['speedup_vs_dense']}")
         del tr
@@ -784,6 +785,7 @@ def main():
     # ---------------------------------------------------------------- whole trunk (2, n-4, 2)
     trunk = None
     if args.trunk_steps > 0 and w.kind == "preln" and w.n_blocks >= 5 and w.backward:
+        from paper_2607_02829_amd.trunk import eq_speedup_estimate
         torch.cuda.reset_peak_memory_stats()
         base_mem = torch.cuda.memory_allocated()
         tr = TrunkStep(w)
@@ -820,7 +822,7 @@ def main():
                                 "peak_ratio": round(trunk_peak / ckpt_peak, 3)},
                  "attn_selector_ms_per_step": round(ams, 3), "attn_selector_overhead_ms": round(ams - tms, 3),
                  "speedup_vs_dense": round(dense["ms_per_step"] / tms, 3) if dense else None,
-                 "eq_speedup_estimate": round(w.n_blocks / (n1 + n2 * w.keep ** 2 + n3), 3),
+                 "eq_speedup_estimate": round(eq_speedup_estimate((n1, n2, n3), w.keep), 3),
                  "outputs_finite": finite_trunk}
         if not args.no_trunk_sweep:
             trunk["sweep"] = trunk_sweep(w, dense["ms_per_step"] if dense else None)

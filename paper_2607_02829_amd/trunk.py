@@ -30,6 +30,18 @@ from __future__ import annotations
 from . import abi, device
 
 
+def eq_speedup_estimate(split, keep: float) -> float:
+    """Attention-cost estimate of the trunk's speedup over the same blocks on all tokens
+    (Sec. 3.2, Eq. (speedup)): N / (n1 + n2 r^2 + n3) with N = n1 + n2 + n3; only the middle
+    blocks' attention is counted as shrinking, by r^2."""
+    n1, n2, n3 = (int(v) for v in split)
+    if min(n1, n2, n3) < 0 or n1 + n2 + n3 < 1:
+        raise ValueError(f"split {split} needs non-negative block counts and at least one block")
+    if not 0.0 < keep <= 1.0:
+        raise ValueError(f"keep ratio {keep} not in (0, 1]")
+    return (n1 + n2 + n3) / (n1 + n2 * keep * keep + n3)
+
+
 class Trunk:
     """Device buffers and the launch sequence of one trunk forward + backward.
 
