@@ -610,12 +610,12 @@ def routing_sweep(D: int, sizes=(4050, 32768, 262144), reps: int = 5) -> list:
     return out
 
 
-def cpu_baseline(w) -> dict:
-    """Time the oracle on a bounded sample: one block forward+backward on the K routed
-    tokens of one sample plus the routing (selection, gather, scatter) of one step;
-    the step time is estimated as n_blocks x block + routing."""
+def cpu_baseline(w, n_sample: int = 3) -> dict:
+    """Time the oracle on a bounded sample: n_sample blocks forward+backward on the K routed
+    tokens of one sample (about 10 s of CPU work at the 0.25 deg shape) plus the routing
+    (selection, gather, scatter) of one step; the step time is estimated as
+    n_blocks / n_sample x the sampled blocks + routing."""
     import numpy as np
-    from oracle import block as oblk
     from oracle import routing as orouting
     from oracle import select as osel
     from oracle import stack as ostack
@@ -628,24 +628,25 @@ def cpu_baseline(w) -> dict:
     except Exception:  # noqa: BLE001
         cores = os.cpu_count() or 1
     K = w.K
+    n_sample = max(1, min(n_sample, w.n_blocks))
     x = inputs.to_storage(inputs.token_field(w), w.dtype)[:1]
-    p = ostack.params_f64(inputs.params_to_storage(inputs.block_params(w, 1), w.dtype))[0]
+    p = ostack.params_f64(inputs.params_to_storage(inputs.block_params(w, n_sample), w.dtype))
     t0 = time.perf_counter()
     idx = osel.select_random(1, w.L, K, 42, 0)
     h0 = orouting.gather(x, idx)
     t1 = time.perf_counter()
-    out, cache = oblk.block_fwd(storage_to_f64(h0), p, w.H, 1e-6, w.kind)
-    t2 = time.perf_counter()
-    oblk.block_bwd(np.ones_like(out), p, cache)
+    out, caches = ostack.stack_fwd(storage_to_f64(h0), p, w.H, 1e-6, w.kind)
+    ostack.stack_bwd(np.ones_like(out), p, caches)
     t3 = time.perf_counter()
     orouting.scatter_delta(x, h0, h0, idx)
     t4 = time.perf_counter()
     routing_s = (t1 - t0) + (t4 - t3)
-    step_s = w.B * (w.n_blocks * (t3 - t1) + 2 * routing_s)
+    blocks_s = t3 - t1
+    step_s = w.B * (w.n_blocks / n_sample * blocks_s + 2 * routing_s)
     return {"value": w.B * K / step_s, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": (f"fp64 oracle: 1 block fwd+bwd on {K} routed tokens of 1 sample ({t3 - t1:.1f} s) plus "
-                       f"select/gather/scatter ({routing_s:.2f} s); step = B x (n_blocks x block + 2 x routing) "
-                       f"= {step_s:.1f} s (extrapolated)")}
+            "sample": (f"fp64 oracle: {n_sample} blocks fwd+bwd on {K} routed tokens of 1 sample ({blocks_s:.1f} s) "
+                       f"plus select/gather/scatter ({routing_s:.2f} s); step = B x (n_blocks / {n_sample} x "
+                       f"sampled blocks + 2 x routing) = {step_s:.1f} s (extrapolated)")}
 
 
 def main():
