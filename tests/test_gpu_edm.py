@@ -176,3 +176,27 @@ def test_edm_blocks_bitwise_repeatable():
     for ga, gb in zip(a["grads"], b["grads"]):
         for k in ga:
             assert np.array_equal(ga[k].view(np.uint8), gb[k].view(np.uint8)), k
+
+
+@pytest.mark.parametrize("case", ["bf16_hd64_S<L", "bf16_hd128_S<L", "f32_hd64"])
+def test_edm_two_stream_backward_is_bitwise_the_serial_order(case):
+    # timing every launch group (empty filter) runs the weight-gradient GEMMs on the caller's
+    # stream, in the serial order; the default backward forks them to the second stream and
+    # joins before each shared buffer is overwritten: results must not differ by a bit
+    w, S, nb = CASES[case]
+    print(f"[edm two-stream vs serial {case}]", flush=True)
+    h, zc, e, params, dh = _host(w, S, nb)
+    plain = _gpu(w, S, nb, h, zc, e, params, dh)
+    abi.sr_profile_start("")
+    try:
+        serial = _gpu(w, S, nb, h, zc, e, params, dh)
+    finally:
+        prof = abi.sr_profile_stop()
+    assert prof, "no launch group was timed"
+    for k in ("h_out", "dh_in", "dzc", "de"):
+        assert np.array_equal(np.ascontiguousarray(plain[k]).view(np.uint8),
+                              np.ascontiguousarray(serial[k]).view(np.uint8)), k
+    for ga, gb in zip(plain["grads"], serial["grads"]):
+        for k in ga:
+            assert np.array_equal(np.ascontiguousarray(ga[k]).view(np.uint8),
+                                  np.ascontiguousarray(gb[k]).view(np.uint8)), k
