@@ -626,18 +626,50 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
   }
 }
 
-// Several reductions in one launch (the weight gradients of one block): job j takes blocks
-// [first[j], first[j + 1]) and does exactly what reduce_splits_kernel does for it.
+// Several reductions in one launch (the reductions of one block's backward): job j takes blocks
+// [first[j], first[j + 1]).  A split-K / bias job does exactly what reduce_splits_kernel does for
+// it (one f32x4 or one bias column per thread); a column-sum job covers 64 columns per block
+// with 16 row phases, exactly as reduce_cols_kernel (summed over all rows, no accumulation).
 struct ReduceJobs {
   ReduceJob job[kMaxReduceJobs];
   int first[kMaxReduceJobs + 1];
 };
-__global__ __launch_bounds__(256) void reduce_jobs_kernel(ReduceJobs rj) {
+constexpr int kReduceJobThreads = 1024;
+__global__ __launch_bounds__(kReduceJobThreads) void reduce_jobs_kernel(ReduceJobs rj) {
+  __shared__ float red[16][65];
   int j = 0;
   while (j + 1 < kMaxReduceJobs && (int)blockIdx.x >= rj.first[j + 1]) ++j;
   const ReduceJob& b = rj.job[j];
+  const int blk = (int)blockIdx.x - rj.first[j];
+  if (b.rows > 0) {   // uniform over the block (one job per block)
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const int c = blk * 64 + tx;
+    float acc = 0.f;
+    if (c < b.width) {
+      int rr = ty;
+      for (; rr + 7 * 16 < b.rows; rr += 8 * 16) {
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = b.part[(size_t)(rr + i * 16) * b.width + c];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc += v[i];
+      }
+      for (; rr < b.rows; rr += 16) acc += b.part[(size_t)rr * b.width + c];
+    }
+    red[ty][tx] = acc;
+    __syncthreads();
+    for (int s = 8; s >= 1; s >>= 1) {
+      if (ty < s) red[ty][tx] += red[ty + s][tx];
+      __syncthreads();
+    }
+    if (ty == 0 && c < b.width) {
+      float* o = c < b.half ? (b.out ? b.out + c : nullptr) : (b.dbout ? b.dbout + (c - b.half) : nullptr);
+      if (o) *o = red[0][tx];
+    }
+    return;
+  }
   const size_t n4 = b.splits > 1 ? b.n / 4 : 0;
-  const size_t i = (size_t)(blockIdx.x - rj.first[j]) * 256 + threadIdx.x;
+  const size_t i = (size_t)blk * kReduceJobThreads + threadIdx.x;
   if (i < n4) {
     const f32x4* p = reinterpret_cast<const f32x4*>(b.part);
     f32x4 s = p[i];
@@ -654,18 +686,25 @@ __global__ __launch_bounds__(256) void reduce_jobs_kernel(ReduceJobs rj) {
 hipError_t launch_reduce_jobs(const ReduceJob* jobs, int njobs, hipStream_t st) {
   ReduceJobs rj{};
   int blocks = 0, k = 0;
-  for (int j = 0; j < njobs && k < kMaxReduceJobs; ++j) {
+  for (int j = 0; j < njobs; ++j) {
     const ReduceJob& b = jobs[j];
-    const size_t total = (b.splits > 1 ? b.n / 4 : 0) + (b.dbout ? b.nb : 0);
-    if (total == 0) continue;
+    int nblk;
+    if (b.rows > 0) {
+      nblk = (b.out || b.dbout) && b.width > 0 ? (b.width + 63) / 64 : 0;
+    } else {
+      const size_t total = (b.splits > 1 ? b.n / 4 : 0) + (b.dbout ? b.nb : 0);
+      nblk = (int)((total + kReduceJobThreads - 1) / kReduceJobThreads);
+    }
+    if (nblk == 0) continue;
+    if (k == kMaxReduceJobs) return hipErrorInvalidValue;   // more jobs than one launch holds
     rj.job[k] = b;
     rj.first[k] = blocks;
-    blocks += (int)((total + 255) / 256);
+    blocks += nblk;
     ++k;
   }
   if (blocks == 0) return hipSuccess;
   for (int j = k; j <= kMaxReduceJobs; ++j) rj.first[j] = blocks;
-  SR_LAUNCH(reduce_jobs_kernel, dim3((unsigned)blocks), dim3(256), 0, st, rj);
+  SR_LAUNCH(reduce_jobs_kernel, dim3((unsigned)blocks), dim3(kReduceJobThreads), 0, st, rj);
   return hipGetLastError();
 }
 

@@ -159,8 +159,14 @@ struct ReduceJob {
   int dbparts = 1;
   int nb = 0;
   float* dbout = nullptr;
+  // column-sum mode (rows > 0; the LayerNorm parameter gradients): part holds rows x width
+  // partials (row stride width), summed per column in the order of reduce_cols_kernel; columns
+  // below half go to out, the others to dbout (either may be NULL)
+  int rows = 0;
+  int width = 0;
+  int half = 0;
 };
-constexpr int kMaxReduceJobs = 4;
+constexpr int kMaxReduceJobs = 6;
 // With defer, the reduction the weight gradient needs (if any) is described there instead of
 // launched; launch_reduce_jobs then runs up to kMaxReduceJobs of them in one launch, with the
 // arithmetic and order of the single ones.

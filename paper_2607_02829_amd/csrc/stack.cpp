@@ -125,9 +125,10 @@ size_t layout_scratch(const Dims& d, char* base, Scratch* out) {
   }
   const size_t wmax = std::max<size_t>(std::max<size_t>(3 * D, F), 6 * D);
   s.part = c.take<float>((size_t)d.B * colsum_chunks(d.S) * wmax * 4);
-  // LayerNorm parameter-gradient partials of LN2 and LN1 (pre-LN: their reductions run on the
-  // side stream, so each has its own buffer)
-  for (int k = 0; k < 2; ++k) s.lnpart[k] = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
+  // LayerNorm parameter-gradient partials of LN2 and LN1, two of each by block parity (pre-LN:
+  // their reductions run on the side stream, one or two blocks after the partials are written)
+  for (int k = 0; k < 2; ++k)
+    for (int q = 0; q < 2; ++q) s.lnpart[k][q] = c.take<float>((size_t)d.B * ln_bwd_chunks(d.S) * 2 * D * 4);
   s.dmod = c.take<float>((size_t)d.B * 6 * D * 4);
   s.gvpart = d.kind == SR_BLOCK_ADALN ? c.take<float>(gemv_cols_scratch(d.B, 6 * d.D, d.D) * 4) : nullptr;
   // two of each buffer a weight-gradient GEMM reads on the side stream, so the main stream
@@ -380,15 +381,19 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
 
 
   // pre-LN: the LayerNorm parameter gradients (column sums of the ln_bwd partials) are outputs
-  // only, so their reductions ride along with side-stream work that is forked anyway: LN2's with
-  // dW_o of the same block, LN1's with dW_fc2 of the next block (or at the end).  The joins that
-  // guard g1 and g0 also guard lnpart[0] and lnpart[1].
-  auto ln_reduce = [&](int k, float* dw, float* dbeta, hipStream_t ss) -> hipError_t {
-    if (!dw && !dbeta) return hipSuccess;
-    ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, ss);
-    return launch_reduce_cols(sc.lnpart[k], nln, d.B, 1, 2 * D, D, dw, dbeta, 0, ss);
+  // only, so their reductions join the block's weight-gradient reductions in the one launch on
+  // the side stream after dW_qkv: LN2's of the same block, LN1's of the block before it in
+  // backward order (its LN1 backward runs after that launch is forked); the last LN1's at the
+  // end.  The partials alternate between two buffers by block parity: the next write of a
+  // buffer (two blocks later) follows the join that guards g1 (LN2) or g0 (LN1) of that block,
+  // which waits for side-stream work queued after the launch that read it.
+  auto ln_job = [&](const float* part, float* dw, float* dbeta) {
+    ReduceJob j;
+    j.part = part; j.rows = d.B * nln; j.width = 2 * D; j.half = D; j.out = dw; j.dbout = dbeta;
+    return j;
   };
   const sr_block_grads* ln1_pending = nullptr;   // block whose LN1 reduction is still to run
+  const float* ln1_pending_part = nullptr;
 
   auto run = [&]() -> hipError_t {
     SR_TRY(side_stream(&side));
@@ -410,7 +415,7 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       const int par = i & 1;
       void* const dz = sc.dz[par];
       void* const dqkv = sc.dqkv[par];
-      ReduceJob jobs[4];   // this block's weight-gradient reductions, launched after dW_qkv
+      ReduceJob jobs[6];   // this block's reductions (weights, LN2, the previous LN1), after dW_qkv
       if (ada) {
         // MLP-branch gradient dm = dh' * gate2 (activation copy) and dgate2 = sum_s dh' * m_out
         SR_TRY(join(kFc2));   // g0 may still be read by the previous block's dW_fc2
@@ -420,14 +425,12 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       }
       // FC2: dW2, db2; dz = (dm W2) * GELU'(z)
       SR_TRY(on_side(kFc2, [&](hipStream_t ss) -> hipError_t {
-        if (ln1_pending) SR_TRY(ln_reduce(1, ln1_pending->ln1_w, ln1_pending->ln1_b, ss));
         if (g.w_fc2 || g.b_fc2) {   // GELU(z) recomputed from the stored pre-activation
           ProfScope ps("recompute", 0, (double)M * F * e * 2, ss);
           SR_TRY(launch_gelu(d.dtype, s.z, sc.gz_rc, (size_t)M * F, ss));
         }
         return weight_grad("gemm_dw_fc2", d, g0, D, sc.gz_rc, F, g.w_fc2, g.b_fc2, sc, kWgFc2, &jobs[kWgFc2], ss);
       }));
-      ln1_pending = nullptr;
       SR_TRY(join(kFc1 + par));   // dz[par] may still be read by dW_fc1 two blocks back
       {
         GemmDesc gd = desc(d, g0, true, D, (size_t)M * D * e, w.w_fc2, false, F, (size_t)D * F * e, M, F, D);
@@ -457,11 +460,12 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       SR_TRY(fork_point([&]() -> hipError_t {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         return launch_ln_bwd(d.dtype, sc.du, s.h1, s.mean2, s.rstd2, w.ln2_w, ada ? s.mod : nullptr, 3 * D, sc.g_res,
-                             d.B, S, D, sc.g_res2, ada ? nullptr : g1, sc.lnpart[0], st);
+                             d.B, S, D, sc.g_res2, ada ? nullptr : g1, sc.lnpart[0][ada ? 0 : par], st);
       }));
       if (ada) {   // dscale2 -> dmod[4D..5D), dshift2 -> dmod[3D..4D)
         ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
-        SR_TRY(launch_reduce_cols(sc.lnpart[0], nln, d.B, 0, 2 * D, D, sc.dmod + 4 * D, sc.dmod + 3 * D, 6 * D, st));
+        SR_TRY(launch_reduce_cols(sc.lnpart[0][0], nln, d.B, 0, 2 * D, D, sc.dmod + 4 * D, sc.dmod + 3 * D, 6 * D,
+                                  st));
       }
       if (ada) {
         // attention-branch gradient da = dh1 * gate1 and dgate1 = sum_s dh1 * a_out
@@ -473,7 +477,6 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       // output projection: dWo, dbo; dO = da Wo (with the attention row statistic
       // delta = rowsum(dO * O) per head in the same epilogue when the head dim is 64)
       SR_TRY(on_side(kO, [&](hipStream_t ss) -> hipError_t {
-        if (!ada) SR_TRY(ln_reduce(0, g.ln2_w, g.ln2_b, ss));
         return weight_grad("gemm_dw_o", d, g1, D, s.O, D, g.w_o, g.b_o, sc, kWgO, &jobs[kWgO], ss);
       }));
       const bool fuse_delta = d.dtype == kBF16 && D / d.H == 64;
@@ -493,6 +496,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       SR_TRY(fork_point([&]() -> hipError_t {
         return launch_attn_bwd(d.dtype, s.qkv, sc.dO, s.lse, sc.delta, dqkv, d.B, S, d.H, D, st);
       }));
+      if (!ada) {   // LN2 of this block and LN1 of the block before it join the reduction launch
+        if (g.ln2_w || g.ln2_b) jobs[4] = ln_job(sc.lnpart[0][par], g.ln2_w, g.ln2_b);
+        if (ln1_pending && (ln1_pending->ln1_w || ln1_pending->ln1_b))
+          jobs[5] = ln_job(ln1_pending_part, ln1_pending->ln1_w, ln1_pending->ln1_b);
+      }
       // QKV: dWqkv, dbqkv; du = dqkv Wqkv
       SR_TRY(on_side(kQkv + par, [&](hipStream_t ss) -> hipError_t {
         if (g.w_qkv || g.b_qkv) {   // u1 = LN1(h) recomputed from the saved statistics
@@ -502,10 +510,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
         }
         SR_TRY(weight_grad("gemm_dw_qkv", d, dqkv, 3 * D, sc.u_rc, D, g.w_qkv, g.b_qkv, sc, kWgQkv, &jobs[kWgQkv],
                            ss));
-        // the block's four weight-gradient reductions in one launch, in the order of the single ones
+        // the block's reductions in one launch, each in the order of its single kernel
         ProfScope ps("reduce_dw", 0, 0, ss);
-        return launch_reduce_jobs(jobs, 4, ss);
+        return launch_reduce_jobs(jobs, 6, ss);
       }));
+      ln1_pending = nullptr;
       {
         GemmDesc gd = desc(d, dqkv, true, 3 * D, (size_t)M * 3 * D * e, w.w_qkv, false, D, (size_t)3 * D * D * e,
                            M, D, 3 * D);
@@ -518,13 +527,14 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       SR_TRY(fork_point([&]() -> hipError_t {
         ProfScope ps("ln_bwd", 0, (double)M * D * (16 + e), st);
         return launch_ln_bwd(d.dtype, sc.du, s.hin, s.mean1, s.rstd1, w.ln1_w, ada ? s.mod : nullptr, 0, sc.g_res2,
-                             d.B, S, D, sc.g_res, ada ? nullptr : g0, sc.lnpart[ada ? 0 : 1], st);
+                             d.B, S, D, sc.g_res, ada ? nullptr : g0, sc.lnpart[ada ? 0 : 1][ada ? 0 : par], st);
       }));
       if (ada) {   // dscale1 -> dmod[D..2D), dshift1 -> dmod[0..D)
         ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
-        SR_TRY(launch_reduce_cols(sc.lnpart[0], nln, d.B, 0, 2 * D, D, sc.dmod + D, sc.dmod, 6 * D, st));
+        SR_TRY(launch_reduce_cols(sc.lnpart[0][0], nln, d.B, 0, 2 * D, D, sc.dmod + D, sc.dmod, 6 * D, st));
       } else {
         ln1_pending = &g;
+        ln1_pending_part = sc.lnpart[1][par];
       }
       if (ada) {
         // dW_ada = dmod^T c ; db_ada = sum_b dmod ; dcond (+)= dmod W_ada
@@ -555,7 +565,11 @@ hipError_t stack_bwd(const Dims& d, const sr_block_params* p, const void* cond, 
       ProfScope ps("convert", 0, (double)M * D * (e + 4), st);
       SR_TRY(launch_convert(kF32, sc.g_res, d.dtype, dh_in, (size_t)M * D, nullptr, 0, S, D, nullptr, st));
     }
-    if (ln1_pending) SR_TRY(ln_reduce(1, ln1_pending->ln1_w, ln1_pending->ln1_b, st));
+    if (ln1_pending && (ln1_pending->ln1_w || ln1_pending->ln1_b)) {
+      ProfScope ps("reduce", 0, (double)d.B * nln * 2 * D * 4, st);
+      SR_TRY(launch_reduce_cols(ln1_pending_part, nln, d.B, 1, 2 * D, D, ln1_pending->ln1_w, ln1_pending->ln1_b, 0,
+                                st));
+    }
     for (int k = 0; k < kSlots; ++k) SR_TRY(join(k));   // every gradient is complete when st is
     return hipSuccess;
   };

@@ -25,7 +25,7 @@ struct Scratch {
   // for an unwanted dW; bias-gradient partial rows.  One set per kind, so that a block's four
   // reductions can run as one launch after its last weight gradient.
   float *wpart[4], *dbpart[4];
-  float *g_res, *g_res2, *du, *delta, *part, *lnpart[2], *dmod, *gvpart;
+  float *g_res, *g_res2, *du, *delta, *part, *lnpart[2][2], *dmod, *gvpart;
   void *g_act[2], *dz[2], *dO, *dqkv[2], *u_rc, *gz_rc;
 };
 
